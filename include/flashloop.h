@@ -1,0 +1,206 @@
+/*
+ * flashloop.h -- C ABI of the FlashLoop per-loop attention step for MI355X (gfx950).
+ *
+ * The step updates one layer of a looped Transformer block at sparse loop r >= 2 (the method of
+ * "FlashLoop: Fast and Memory-Efficient Looped Transformers via Lazy Updates"):
+ *   1. fl_select_tokens       pick the rows whose state moved most since loop r-1
+ *                             (Section 4.1; Appendix D.1, Eq. 5);
+ *   2. fl_kv_residual_quant   store K/V of those rows as group-wise low-bit residuals against the
+ *                             previous reconstruction (Section 4.3, Eq. 4; Appendix D.3, Eq. 8);
+ *   3. fl_kv_residual_dequant rebuild X_hat^(r) rows from the residual (Eq. 8);
+ *   4. fl_loop_sparse_attn    update the attention output of those rows from the previous loop's output
+ *                             with a mass-corrected correction over predicted key columns
+ *                             (Sections 3.2, 4.2, Eq. 3; Appendix D.2, Eq. 7).
+ * plus two set-up helpers for a dense source loop (Appendix D.2, Eq. 6 with all causal keys):
+ *   fl_column_scores, fl_select_columns.
+ *
+ * Conventions shared by every call
+ *   - Every data pointer is a DEVICE pointer (HIP device memory).  The caller allocates and owns all
+ *     memory and keeps it alive until the enqueued work has completed.  The library never allocates,
+ *     frees or synchronizes, and keeps no pointer after the call returns.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).  All work is enqueued
+ *     asynchronously on it; nothing is read back to the host.
+ *   - bf16 and fp16 values are passed as their raw 16-bit patterns (uint16_t).
+ *   - Layouts are dense and row-major as written: [B, N, H, d] means element (b, i, h, e) lives at
+ *     ((b * N + i) * H + h) * d + e.  Index lists are int32 and strictly ascending.
+ *   - Return value: FL_OK, or an FL_E_* status.  Arguments are validated on the host before anything
+ *     is enqueued; on a non-OK return nothing was launched and no output was written.  FL_E_HIP means
+ *     a launch was rejected by the runtime; faults inside kernels surface at the caller's next
+ *     synchronization.  fl_last_error() returns a thread-local message for the last non-OK return.
+ *   - Results are deterministic: the same inputs give bitwise-identical outputs (no float atomics).
+ *   - Supported sizes: head dim d in {64, 128}; B, N, H >= 1; N < 2^31 / (H * d).
+ */
+#ifndef FLASHLOOP_H
+#define FLASHLOOP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FL_ABI_VERSION 1
+
+enum fl_status {
+  FL_OK = 0,
+  FL_E_NULL = 1,        /* a required pointer is NULL */
+  FL_E_SHAPE = 2,       /* inconsistent or unsupported sizes */
+  FL_E_RANGE = 3,       /* a count is out of its range (e.g. k > n_cand) */
+  FL_E_UNSUPPORTED = 4, /* unsupported bit width, axis, mode or flag */
+  FL_E_WORKSPACE = 5,   /* workspace missing or too small */
+  FL_E_HIP = 6,         /* the HIP runtime rejected a launch */
+  FL_E_INTERNAL = 7
+};
+
+const char* fl_status_str(int status);
+const char* fl_last_error(void);
+int fl_abi_version(void);
+
+/* ------------------------------------------------------------------------------------------------
+ * (1) Token selection -- Section 4.1; Appendix D.1, Eq. 5.
+ *
+ * For every candidate row i of batch b the score is
+ *     s_i = ||delta_i||_2 / (||cur_i||_2 + eps)        (normalize != 0)
+ *     s_i = ||delta_i||_2                              (normalize == 0)
+ * over the concatenation of the (k_cur, k_prev) and (v_cur, v_prev) rows, with
+ * delta = fp32(cur) - fp32(prev) (fp32, round to nearest even) and both squared norms accumulated in
+ * fp64; the selection key is fp32(s_i) (round to nearest even).  The active set is the k candidates
+ * with the largest keys, ties broken by the lower row index, emitted in ascending row order.
+ *
+ *   k_cur, k_prev, v_cur, v_prev : bf16 [B, N, D] (D = H * d; rows of all heads).  v_cur and v_prev may
+ *                                  both be NULL to score one pair only.  Row starts 16-byte aligned.
+ *   cand     : int32 [B, n_cand] ascending candidate rows (the previous active set), or NULL for all N
+ *              rows (then n_cand must equal N).
+ *   k        : 0 <= k <= n_cand, else FL_E_RANGE.  n_cand <= 65536.
+ *   out_key  : fp32 [B, n_cand] selection keys, in candidate order (required).
+ *   out_idx  : int32 [B, k] the active rows, ascending (required when k > 0).
+ *   out_slot : int32 [B, N] position of each row in out_idx, -1 for rows not selected (NULL = skip).
+ *   D must be a multiple of 8.
+ * ---------------------------------------------------------------------------------------------- */
+int fl_select_tokens(const uint16_t* k_cur, const uint16_t* k_prev,
+                     const uint16_t* v_cur, const uint16_t* v_prev,
+                     int B, int N, int D,
+                     const int32_t* cand, int n_cand, int k, int normalize, double eps,
+                     float* out_key, int32_t* out_idx, int32_t* out_slot, void* stream);
+
+/* ------------------------------------------------------------------------------------------------
+ * (2a) Residual quantization -- Section 4.3, Eq. 4; Appendix D.3, Eq. 8; Appendix E (asymmetric
+ * group-wise quantization with scale and offset from the group min/max; keys per channel, values per
+ * token).
+ *
+ * For packed row p < k with token i = idx[b, p]:  delta = fp32(x_cur[b,i]) - fp32(x_ref[b,i]).
+ *   axis FL_AXIS_TOKEN   (keys):   a group is G consecutive packed rows x one (head, channel); the last
+ *                                  group may be partial.  scale/zero: fp16 [B, ceil(k/G), H, d].
+ *   axis FL_AXIS_CHANNEL (values): a group is one (row, head) x G consecutive channels (G | d).
+ *                                  scale/zero: fp16 [B, k, H, d/G].
+ * Per group: z = largest fp16 <= min, s = smallest fp16 >= (max - z) / (2^bits - 1) (fp64), and codes
+ * q = clamp(rint(fp32(delta - z) / fp32(s)), 0, 2^bits - 1) (IEEE fp32 division, ties to even;
+ * q = 0 when s == 0).  Signed zeros in z and s are stored as +0.
+ * Codes: uint8 [B, k, H, d * bits / 8], packed LSB-first along channels (channel e at byte
+ * e*bits/8, bit (e mod 8/bits)*bits); bits = 8 is one byte per code; bits = 16 stores the raw bf16
+ * state (no quantization; scale/zero untouched and may be NULL).
+ *
+ *   x_cur    : bf16 [B, N, H, d] the loop-r state X^(r).
+ *   x_ref    : bf16 [B, N, H, d] the previous reconstruction X_hat^(r-1), or NULL for zeros (the base).
+ *   idx      : int32 [B, k] ascending active rows, or NULL for all rows (then k must equal N).
+ *   bits     : 2, 4, 8 or 16.  group: 8 <= G <= 128, a multiple of 8 (and G | d on the CHANNEL axis).
+ *   out_rows : optional bf16 [B, k, H, d]: also write the reconstructed rows
+ *              bf16(fp32(x_ref[b,i]) + fp32(z + q*s)) (what fl_kv_residual_dequant COMPACT returns).
+ *              May alias x_ref only when idx is NULL (in-place base reconstruction).
+ * ---------------------------------------------------------------------------------------------- */
+enum fl_axis { FL_AXIS_TOKEN = 0, FL_AXIS_CHANNEL = 1 };
+
+int fl_kv_residual_quant(const uint16_t* x_cur, const uint16_t* x_ref, const int32_t* idx, int k,
+                         int B, int N, int H, int d, int bits, int group, int axis,
+                         uint8_t* codes, uint16_t* scale, uint16_t* zero, uint16_t* out_rows,
+                         void* stream);
+
+/* ------------------------------------------------------------------------------------------------
+ * (2b) Residual dequantization and reconstruction -- Eq. 4 and Appendix D.3, Eq. 8:
+ *     X_hat^(r)[i] = bf16(fp32(X_hat^(r-1)[i]) + fp32(z + q * s))   for i = idx[b, p], p < k;
+ * other rows keep X_hat^(r-1).  q * s is exact in fp32, so the sum is rounded once.
+ *   mode FL_DQ_COMPACT : read x_hat rows, write out_rows bf16 [B, k, H, d]; x_hat is not modified.
+ *   mode FL_DQ_COMMIT  : update rows idx of x_hat in place (out_rows must be NULL).
+ * codes/scale/zero/bits/group/axis as produced by fl_kv_residual_quant.  idx NULL = all rows (k = N).
+ * ---------------------------------------------------------------------------------------------- */
+enum fl_dq_mode { FL_DQ_COMPACT = 0, FL_DQ_COMMIT = 1 };
+
+int fl_kv_residual_dequant(const uint8_t* codes, const uint16_t* scale, const uint16_t* zero,
+                           const int32_t* idx, int k, int B, int N, int H, int d,
+                           int bits, int group, int axis, int mode,
+                           uint16_t* x_hat, uint16_t* out_rows, void* stream);
+
+/* ------------------------------------------------------------------------------------------------
+ * (3) Mass-corrected sparse attention update -- Sections 3.2 and 4.2, Eq. 3; Appendix D.2, Eq. 7.
+ *
+ * For every updated row i = rows[b, p] (p < k) and head h, over the column set
+ *     S_i = ({cols[b, h, :]} U {j : i - window < j <= i}) restricted to j <= i   (a set)
+ * with sigma = sm_scale:
+ *   subtract (loop r-1):  pp_j = exp(sigma q_prev_i . k_cache_j - lse_ref_i),  m_i = sum pp_j,
+ *                         sub = sum pp_j v_cache_j
+ *   add      (loop r):    L = logsumexp_j (sigma q_cur_i . knew_j),  pc_j = m_i exp(sigma q_cur_i.knew_j - L),
+ *                         add = sum pc_j vnew_j
+ *   o_i <- o_i - sub + add,   lse_ref_i <- L - log(m_i)
+ * where knew_j/vnew_j is row slot[b, j] of k_new/v_new when slot[b, j] >= 0 (a row updated this loop)
+ * and the cache row otherwise.  Rows with an empty S_i or m_i == 0 are left unchanged; rows not in
+ * `rows` are never touched.  lse_ref carries the cached column mass: exp(logit - lse_ref) reproduces
+ * the cached probabilities of the previous loop.
+ *
+ * flags FL_ATTN_DENSE (the dense source loop): rows is NULL (every row, k = N), cols/slot/q_prev/
+ *   k_new/v_new are unused, window is ignored (S_i = [0, i]); writes o_i = softmax(sigma q_i K^T) V
+ *   over j <= i and lse_ref_i = its log-normaliser (inputs o/lse_ref are overwritten, not read).
+ *
+ *   q_cur, q_prev     : bf16 [B, N, H, d]  (queries of loop r and r-1)
+ *   k_cache, v_cache  : bf16 [B, N, H, d]  X_hat^(r-1)
+ *   k_new, v_new      : bf16 [B, k, H, d]  X_hat^(r) of the rows, in `rows` order
+ *   slot              : int32 [B, N]       position in rows, or -1
+ *   rows              : int32 [B, k]       ascending updated rows
+ *   cols              : int32 [B, H, c_list] ascending column list (0 <= c_list <= N)
+ *   window            : band width w >= 0
+ *   lse_ref           : fp32 [B, N, H]     in/out
+ *   o                 : fp32 [B, N, H, d]  in/out
+ *   ws, ws_bytes      : workspace of at least fl_loop_sparse_attn_ws(...) bytes (may be NULL if 0).
+ * Attention products use bf16 MFMA with fp32 accumulation for q.k and fp16 MFMA for p.v (values are
+ * converted bf16 -> fp16, exact for |v| in [2^-14, 65504]); softmax and the update are fp32.
+ * ---------------------------------------------------------------------------------------------- */
+enum fl_attn_flags { FL_ATTN_DENSE = 1 };
+
+size_t fl_loop_sparse_attn_ws(int B, int N, int H, int d, int k, int c_list, int window, int flags);
+
+int fl_loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev,
+                        const uint16_t* k_cache, const uint16_t* v_cache,
+                        const uint16_t* k_new, const uint16_t* v_new,
+                        const int32_t* slot, const int32_t* rows, int k,
+                        const int32_t* cols, int c_list, int window,
+                        int B, int N, int H, int d, float sm_scale, int flags,
+                        float* lse_ref, float* o, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------------------------------
+ * (4) Column statistic of a dense source loop -- Appendix D.2, Eq. 6 with all causal keys and cached
+ * mass 1, summed over all rows of a prefill:
+ *     col_key[b, h, j] = fp32( sum_{i >= j} exp(l_ij - lse_i) ),  l_ij = sigma * sum_e q_ie k_je,
+ *     lse_i = log sum_{j <= i} exp(l_ij),   sigma = 1 / sqrt(d),
+ * all in fp64 (products of bf16 values are exact in fp64).
+ *   q, k_cache : bf16 [B, N, H, d];  col_key : fp32 [B, H, N].
+ *   ws         : at least fl_column_scores_ws(B, N, H) bytes (the fp64 row log-normalisers).
+ * ---------------------------------------------------------------------------------------------- */
+size_t fl_column_scores_ws(int B, int N, int H);
+
+int fl_column_scores(const uint16_t* q, const uint16_t* k_cache, int B, int N, int H, int d,
+                     float* col_key, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------------------------------
+ * (5) Column list -- Appendix D.2, Eq. 6: S = {0 .. n_sink-1} U TopK_t(col_key over j >= n_sink),
+ * ties broken by the lower column index, emitted ascending.
+ *   col_key : fp32 [B, H, N];  cols : int32 [B, H, ns + t] with ns = min(n_sink, N);
+ *   0 <= t <= N - ns, else FL_E_RANGE;  N - ns <= 65536.
+ * ---------------------------------------------------------------------------------------------- */
+int fl_select_columns(const float* col_key, int B, int H, int N, int n_sink, int t,
+                      int32_t* cols, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FLASHLOOP_H */

@@ -1,0 +1,415 @@
+// Cross-loop K/V residual codec: Section 4.3, Eq. 4; Appendix D.3, Eq. 8; quantizer of Appendix E.
+//
+// All kernels stream rows with 16-byte loads: one thread owns 8 consecutive channels of a row, so codes
+// of those channels form one 2/4/8-byte word (LSB-first packing) and metadata loads are 2 or 16 bytes.
+//   quant_token   (keys, per-channel groups of G packed rows): a 256-thread workgroup owns one group of
+//                 rows x 256 channels; 8 row slices reduce min/max through LDS, then the same threads
+//                 encode their rows from registers (no second pass over HBM).
+//   quant_channel (values, per-token groups of G channels): the G/8 threads of a group reduce min/max
+//                 with lane shuffles.
+//   dequant       rebuilds bf16(x_hat + z + q*s) rows, compact or in place.
+// Both quantizers optionally write the reconstructed rows (fusing the compact dequantization).
+#include "fl_common.h"
+
+namespace fl {
+
+struct Row8 {
+  float v[8];
+};
+
+__device__ __forceinline__ Row8 load_bf16x8(const uint16_t* p) {
+  uint4 w = *reinterpret_cast<const uint4*>(p);
+  const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+  Row8 r;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    r.v[2 * t] = __uint_as_float(ws[t] << 16);
+    r.v[2 * t + 1] = __uint_as_float(ws[t] & 0xFFFF0000u);
+  }
+  return r;
+}
+
+__device__ __forceinline__ void store_bf16x8(uint16_t* p, const Row8& r) {
+  uint32_t ws[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+    ws[t] = f32_to_bf16_rne(r.v[2 * t]) | (f32_to_bf16_rne(r.v[2 * t + 1]) << 16);
+  *reinterpret_cast<uint4*>(p) = make_uint4(ws[0], ws[1], ws[2], ws[3]);
+}
+
+// Encode one value: q = clamp(rint(fp32(delta - z) / s), 0, qmax), 0 when s == 0.
+__device__ __forceinline__ uint32_t encode1(float delta, float z, float s, int qmax) {
+  if (s == 0.0f) return 0u;
+  float t = (delta - z) / s;                 // IEEE division (correctly rounded build)
+  t = __builtin_rintf(t);
+  t = fminf(fmaxf(t, 0.0f), (float)qmax);
+  return (uint32_t)t;
+}
+
+template <int BITS>
+__device__ __forceinline__ void store_codes8(uint8_t* dst, const uint32_t q[8]) {
+  if constexpr (BITS == 8) {
+    uint32_t lo = q[0] | (q[1] << 8) | (q[2] << 16) | (q[3] << 24);
+    uint32_t hi = q[4] | (q[5] << 8) | (q[6] << 16) | (q[7] << 24);
+    *reinterpret_cast<uint2*>(dst) = make_uint2(lo, hi);
+  } else {
+    uint32_t w = 0;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) w |= q[t] << (t * BITS);
+    if constexpr (BITS == 4) *reinterpret_cast<uint32_t*>(dst) = w;
+    else *reinterpret_cast<uint16_t*>(dst) = (uint16_t)w;
+  }
+}
+
+template <int BITS>
+__device__ __forceinline__ void load_codes8(const uint8_t* src, uint32_t q[8]) {
+  constexpr uint32_t mask = (1u << BITS) - 1u;
+  if constexpr (BITS == 8) {
+    uint2 w = *reinterpret_cast<const uint2*>(src);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      q[t] = (w.x >> (8 * t)) & mask;
+      q[t + 4] = (w.y >> (8 * t)) & mask;
+    }
+  } else {
+    uint32_t w = (BITS == 4) ? *reinterpret_cast<const uint32_t*>(src)
+                             : (uint32_t)*reinterpret_cast<const uint16_t*>(src);
+#pragma unroll
+    for (int t = 0; t < 8; ++t) q[t] = (w >> (t * BITS)) & mask;
+  }
+}
+
+// Group metadata from fp32 min/max: z = fp16 down(min), s = fp16 up((max - z) / qmax), both fp64.
+__device__ __forceinline__ void group_meta(float mn, float mx, int qmax, double& z, double& s) {
+  z = f16_down_value((double)mn);
+  s = f16_up_value(((double)mx - z) / (double)qmax);
+}
+
+// ---- keys: per-channel groups along packed rows ----------------------------------------------------
+constexpr int kTokSlices = 8;
+constexpr int kTokChunks = 32;      // 32 threads x 8 channels = 256 channels per workgroup
+
+template <int BITS, int RPS>
+__global__ __launch_bounds__(kTokSlices * kTokChunks) void quant_token_kernel(
+    const uint16_t* __restrict__ x_cur, const uint16_t* __restrict__ x_ref,
+    const int32_t* __restrict__ idx, int k, int N, int HD, int G, uint8_t* __restrict__ codes,
+    uint16_t* __restrict__ scale, uint16_t* __restrict__ zero, uint16_t* __restrict__ out_rows) {
+  __shared__ float s_mn[kTokSlices][kTokChunks * 8];
+  __shared__ float s_mx[kTokSlices][kTokChunks * 8];
+  __shared__ float s_z[kTokChunks * 8];
+  __shared__ float s_s[kTokChunks * 8];
+  constexpr int qmax = (1 << BITS) - 1;
+  const int slice = threadIdx.x / kTokChunks, chunk = threadIdx.x % kTokChunks;
+  const int g = blockIdx.y, b = blockIdx.z;
+  const int c0 = blockIdx.x * (kTokChunks * 8) + chunk * 8;
+  const bool ch_ok = c0 < HD;
+  const int ng = (k + G - 1) / G;
+
+  float dl[RPS][8];
+  uint4 ref_raw[RPS];
+  float mn[8], mx[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t) { mn[t] = INFINITY; mx[t] = -INFINITY; }
+#pragma unroll
+  for (int j = 0; j < RPS; ++j) {
+    const int p = g * G + slice * RPS + j;
+    ref_raw[j] = make_uint4(0, 0, 0, 0);
+    if (ch_ok && p < k) {
+      const int64_t i = idx ? (int64_t)idx[(int64_t)b * k + p] : (int64_t)p;
+      const int64_t off = ((int64_t)b * N + i) * HD + c0;
+      Row8 c = load_bf16x8(x_cur + off);
+      Row8 r{};
+      if (x_ref) {
+        ref_raw[j] = *reinterpret_cast<const uint4*>(x_ref + off);
+        r = load_bf16x8(x_ref + off);
+      }
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        dl[j][t] = c.v[t] - r.v[t];
+        mn[t] = fminf(mn[t], dl[j][t]);
+        mx[t] = fmaxf(mx[t], dl[j][t]);
+      }
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < 8; ++t) {
+    s_mn[slice][chunk * 8 + t] = mn[t];
+    s_mx[slice][chunk * 8 + t] = mx[t];
+  }
+  __syncthreads();
+  {
+    const int ch = threadIdx.x;   // 256 threads, one channel each
+    const int c = blockIdx.x * (kTokChunks * 8) + ch;
+    float a = INFINITY, bb = -INFINITY;
+#pragma unroll
+    for (int sl = 0; sl < kTokSlices; ++sl) {
+      a = fminf(a, s_mn[sl][ch]);
+      bb = fmaxf(bb, s_mx[sl][ch]);
+    }
+    double z = 0.0, s = 0.0;
+    if (c < HD) {
+      group_meta(a, bb, qmax, z, s);
+      const int64_t m = ((int64_t)b * ng + g) * HD + c;
+      zero[m] = (uint16_t)f16_bits_of_exact(z);
+      scale[m] = (uint16_t)f16_bits_of_exact(s);
+    }
+    s_z[ch] = (float)z;
+    s_s[ch] = (float)s;
+  }
+  __syncthreads();
+  if (!ch_ok) return;
+  float z8[8], s8[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t) {
+    z8[t] = s_z[chunk * 8 + t];
+    s8[t] = s_s[chunk * 8 + t];
+  }
+  const int row_bytes = HD * BITS / 8;
+#pragma unroll
+  for (int j = 0; j < RPS; ++j) {
+    const int p = g * G + slice * RPS + j;
+    if (p >= k) break;
+    uint32_t q[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) q[t] = encode1(dl[j][t], z8[t], s8[t], qmax);
+    store_codes8<BITS>(codes + ((int64_t)b * k + p) * row_bytes + c0 * BITS / 8, q);
+    if (out_rows) {
+      const uint32_t rw[4] = {ref_raw[j].x, ref_raw[j].y, ref_raw[j].z, ref_raw[j].w};
+      Row8 o;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        float ref = (t & 1) ? __uint_as_float(rw[t >> 1] & 0xFFFF0000u) : __uint_as_float(rw[t >> 1] << 16);
+        float dq = z8[t] + (float)q[t] * s8[t];     // q * s exact in fp32: one rounding
+        o.v[t] = ref + dq;
+      }
+      store_bf16x8(out_rows + ((int64_t)b * k + p) * HD + c0, o);
+    }
+  }
+}
+
+// ---- values: per-token groups of G channels ----------------------------------------------------------
+template <int BITS>
+__global__ __launch_bounds__(256) void quant_channel_kernel(
+    const uint16_t* __restrict__ x_cur, const uint16_t* __restrict__ x_ref,
+    const int32_t* __restrict__ idx, int k, int N, int HD, int G, uint8_t* __restrict__ codes,
+    uint16_t* __restrict__ scale, uint16_t* __restrict__ zero, uint16_t* __restrict__ out_rows) {
+  constexpr int qmax = (1 << BITS) - 1;
+  const int chunks = HD / 8;
+  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t total = (int64_t)gridDim.y * k * chunks;   // gridDim.y == B
+  const int b = blockIdx.y;
+  const int64_t local = tid;                               // within batch b
+  const bool ok = local < (int64_t)k * chunks;
+  const int p = ok ? (int)(local / chunks) : 0;
+  const int chunk = ok ? (int)(local % chunks) : 0;
+  (void)total;
+  const int c0 = chunk * 8;
+  float dl[8];
+  uint4 ref_raw = make_uint4(0, 0, 0, 0);
+  float mn = INFINITY, mx = -INFINITY;
+  if (ok) {
+    const int64_t i = idx ? (int64_t)idx[(int64_t)b * k + p] : (int64_t)p;
+    const int64_t off = ((int64_t)b * N + i) * HD + c0;
+    Row8 c = load_bf16x8(x_cur + off);
+    Row8 r{};
+    if (x_ref) {
+      ref_raw = *reinterpret_cast<const uint4*>(x_ref + off);
+      r = load_bf16x8(x_ref + off);
+    }
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      dl[t] = c.v[t] - r.v[t];
+      mn = fminf(mn, dl[t]);
+      mx = fmaxf(mx, dl[t]);
+    }
+  }
+  // reduce across the G/8 consecutive lanes of the group (groups never straddle a wave)
+  for (int off = 1; off < G / 8; off <<= 1) {
+    mn = fminf(mn, __shfl_xor(mn, off, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+  }
+  if (!ok) return;
+  double z, s;
+  group_meta(mn, mx, qmax, z, s);
+  if ((chunk % (G / 8)) == 0) {
+    const int64_t m = ((int64_t)b * k + p) * (HD / G) + c0 / G;
+    zero[m] = (uint16_t)f16_bits_of_exact(z);
+    scale[m] = (uint16_t)f16_bits_of_exact(s);
+  }
+  const float z32 = (float)z, s32 = (float)s;
+  uint32_t q[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t) q[t] = encode1(dl[t], z32, s32, qmax);
+  store_codes8<BITS>(codes + ((int64_t)b * k + p) * (HD * BITS / 8) + c0 * BITS / 8, q);
+  if (out_rows) {
+    const uint32_t rw[4] = {ref_raw.x, ref_raw.y, ref_raw.z, ref_raw.w};
+    Row8 o;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      float ref = (t & 1) ? __uint_as_float(rw[t >> 1] & 0xFFFF0000u) : __uint_as_float(rw[t >> 1] << 16);
+      o.v[t] = ref + (z32 + (float)q[t] * s32);
+    }
+    store_bf16x8(out_rows + ((int64_t)b * k + p) * HD + c0, o);
+  }
+}
+
+// ---- bits = 16: the payload is the raw state ---------------------------------------------------------
+__global__ __launch_bounds__(256) void passthrough_kernel(const uint16_t* __restrict__ x_cur,
+                                                          const int32_t* __restrict__ idx, int k,
+                                                          int N, int HD, uint8_t* __restrict__ codes,
+                                                          uint16_t* __restrict__ out_rows) {
+  const int chunks = HD / 8;
+  const int64_t local = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int b = blockIdx.y;
+  if (local >= (int64_t)k * chunks) return;
+  const int p = (int)(local / chunks), c0 = (int)(local % chunks) * 8;
+  const int64_t i = idx ? (int64_t)idx[(int64_t)b * k + p] : (int64_t)p;
+  uint4 w = *reinterpret_cast<const uint4*>(x_cur + ((int64_t)b * N + i) * HD + c0);
+  *reinterpret_cast<uint4*>(codes + (((int64_t)b * k + p) * HD + c0) * 2) = w;
+  if (out_rows) *reinterpret_cast<uint4*>(out_rows + ((int64_t)b * k + p) * HD + c0) = w;
+}
+
+// ---- dequantization / reconstruction ------------------------------------------------------------------
+template <int BITS, int AXIS>
+__global__ __launch_bounds__(256) void dequant_kernel(
+    const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scale,
+    const uint16_t* __restrict__ zero, const int32_t* __restrict__ idx, int k, int N, int HD, int G,
+    uint16_t* x_hat, uint16_t* out_rows) {
+  const int chunks = HD / 8;
+  const int64_t local = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int b = blockIdx.y;
+  if (local >= (int64_t)k * chunks) return;
+  const int p = (int)(local / chunks), c0 = (int)(local % chunks) * 8;
+  const int64_t i = idx ? (int64_t)idx[(int64_t)b * k + p] : (int64_t)p;
+  const int64_t xoff = ((int64_t)b * N + i) * HD + c0;
+  uint16_t* dst = out_rows ? out_rows + ((int64_t)b * k + p) * HD + c0 : x_hat + xoff;
+  if constexpr (BITS == 16) {
+    *reinterpret_cast<uint4*>(dst) =
+        *reinterpret_cast<const uint4*>(codes + (((int64_t)b * k + p) * HD + c0) * 2);
+  } else {
+    uint32_t q[8];
+    load_codes8<BITS>(codes + ((int64_t)b * k + p) * (HD * BITS / 8) + c0 * BITS / 8, q);
+    float z8[8], s8[8];
+    if constexpr (AXIS == FL_AXIS_TOKEN) {
+      const int ng = (k + G - 1) / G;
+      const int64_t m = ((int64_t)b * ng + p / G) * HD + c0;
+      uint4 zw = *reinterpret_cast<const uint4*>(zero + m);
+      uint4 sw = *reinterpret_cast<const uint4*>(scale + m);
+      const uint32_t za[4] = {zw.x, zw.y, zw.z, zw.w}, sa[4] = {sw.x, sw.y, sw.z, sw.w};
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        z8[t] = f16_bits_to_f32((t & 1) ? (za[t >> 1] >> 16) : (za[t >> 1] & 0xFFFFu));
+        s8[t] = f16_bits_to_f32((t & 1) ? (sa[t >> 1] >> 16) : (sa[t >> 1] & 0xFFFFu));
+      }
+    } else {
+      const int64_t m = ((int64_t)b * k + p) * (HD / G) + c0 / G;
+      const float z = f16_bits_to_f32(zero[m]), s = f16_bits_to_f32(scale[m]);
+#pragma unroll
+      for (int t = 0; t < 8; ++t) { z8[t] = z; s8[t] = s; }
+    }
+    Row8 x = load_bf16x8(x_hat + xoff);
+    Row8 o;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) o.v[t] = x.v[t] + (z8[t] + (float)q[t] * s8[t]);
+    store_bf16x8(dst, o);
+  }
+}
+
+static int check_codec_args(const char* fn, const void* codes, const void* a, int k, int B, int N,
+                            int H, int d, int bits, int group, int axis, bool need_meta,
+                            const void* scale, const void* zero, const void* idx) {
+  FL_REQUIRE(codes && a, FL_E_NULL, "%s: codes and the state pointer are required", fn);
+  FL_REQUIRE(B >= 1 && N >= 1 && H >= 1, FL_E_SHAPE, "%s: need B, N, H >= 1", fn);
+  FL_REQUIRE(d == 64 || d == 128, FL_E_SHAPE, "%s: head dim %d not in {64, 128}", fn, d);
+  FL_REQUIRE((int64_t)N * H * d < ((int64_t)1 << 31), FL_E_SHAPE, "%s: N * H * d too large", fn);
+  FL_REQUIRE(idx != nullptr || k == N, FL_E_SHAPE, "%s: without idx, k must equal N", fn);
+  FL_REQUIRE(k >= 0 && k <= N, FL_E_RANGE, "%s: k=%d outside [0, N]", fn, k);
+  FL_REQUIRE(bits == 2 || bits == 4 || bits == 8 || bits == 16, FL_E_UNSUPPORTED,
+             "%s: bits=%d not in {2, 4, 8, 16}", fn, bits);
+  FL_REQUIRE(axis == FL_AXIS_TOKEN || axis == FL_AXIS_CHANNEL, FL_E_UNSUPPORTED, "%s: bad axis %d", fn, axis);
+  if (bits != 16) {
+    FL_REQUIRE(group >= 8 && group <= 128 && group % 8 == 0 && (group & (group - 1)) == 0,
+               FL_E_UNSUPPORTED, "%s: group=%d must be a power of two in [8, 128]", fn, group);
+    FL_REQUIRE(axis == FL_AXIS_TOKEN || d % group == 0, FL_E_SHAPE,
+               "%s: CHANNEL axis needs group | d (group=%d, d=%d)", fn, group, d);
+    if (need_meta) FL_REQUIRE(scale && zero, FL_E_NULL, "%s: scale and zero are required", fn);
+  }
+  return FL_OK;
+}
+
+}  // namespace fl
+
+using namespace fl;
+
+extern "C" int fl_kv_residual_quant(const uint16_t* x_cur, const uint16_t* x_ref, const int32_t* idx,
+                                    int k, int B, int N, int H, int d, int bits, int group, int axis,
+                                    uint8_t* codes, uint16_t* scale, uint16_t* zero,
+                                    uint16_t* out_rows, void* stream) {
+  FL_API_BEGIN
+  int rc = check_codec_args("fl_kv_residual_quant", codes, x_cur, k, B, N, H, d, bits, group, axis,
+                            true, scale, zero, idx);
+  if (rc != FL_OK) return rc;
+  FL_REQUIRE(!(out_rows && out_rows == x_ref && idx), FL_E_SHAPE,
+             "fl_kv_residual_quant: out_rows may alias x_ref only when idx is NULL");
+  if (k == 0) return FL_OK;
+  hipStream_t st = as_stream(stream);
+  const int HD = H * d;
+  if (bits == 16) {
+    dim3 grid((unsigned)(((int64_t)k * (HD / 8) + 255) / 256), B);
+    passthrough_kernel<<<grid, 256, 0, st>>>(x_cur, idx, k, N, HD, codes, out_rows);
+    return check_launch("passthrough_kernel");
+  }
+  if (axis == FL_AXIS_TOKEN) {
+    dim3 grid((HD + 255) / 256, (k + group - 1) / group, B);
+#define FL_QT(BB, RR)                                                                          \
+  quant_token_kernel<BB, RR><<<grid, 256, 0, st>>>(x_cur, x_ref, idx, k, N, HD, group, codes, \
+                                                   scale, zero, out_rows)
+#define FL_QT_BITS(BB)                                   \
+  switch (group / 8) {                                   \
+    case 1: FL_QT(BB, 1); break;                         \
+    case 2: FL_QT(BB, 2); break;                         \
+    case 4: FL_QT(BB, 4); break;                         \
+    case 8: FL_QT(BB, 8); break;                         \
+    default: FL_QT(BB, 16); break;                       \
+  }
+    if (bits == 2) { FL_QT_BITS(2) } else if (bits == 4) { FL_QT_BITS(4) } else { FL_QT_BITS(8) }
+#undef FL_QT_BITS
+#undef FL_QT
+    return check_launch("quant_token_kernel");
+  }
+  dim3 grid((unsigned)(((int64_t)k * (HD / 8) + 255) / 256), B);
+  if (bits == 2) quant_channel_kernel<2><<<grid, 256, 0, st>>>(x_cur, x_ref, idx, k, N, HD, group, codes, scale, zero, out_rows);
+  else if (bits == 4) quant_channel_kernel<4><<<grid, 256, 0, st>>>(x_cur, x_ref, idx, k, N, HD, group, codes, scale, zero, out_rows);
+  else quant_channel_kernel<8><<<grid, 256, 0, st>>>(x_cur, x_ref, idx, k, N, HD, group, codes, scale, zero, out_rows);
+  return check_launch("quant_channel_kernel");
+  FL_API_END
+}
+
+extern "C" int fl_kv_residual_dequant(const uint8_t* codes, const uint16_t* scale, const uint16_t* zero,
+                                      const int32_t* idx, int k, int B, int N, int H, int d, int bits,
+                                      int group, int axis, int mode, uint16_t* x_hat,
+                                      uint16_t* out_rows, void* stream) {
+  FL_API_BEGIN
+  int rc = check_codec_args("fl_kv_residual_dequant", codes, x_hat, k, B, N, H, d, bits, group, axis,
+                            true, scale, zero, idx);
+  if (rc != FL_OK) return rc;
+  FL_REQUIRE(mode == FL_DQ_COMPACT || mode == FL_DQ_COMMIT, FL_E_UNSUPPORTED,
+             "fl_kv_residual_dequant: bad mode %d", mode);
+  FL_REQUIRE(mode == FL_DQ_COMMIT ? out_rows == nullptr : out_rows != nullptr, FL_E_NULL,
+             "fl_kv_residual_dequant: COMPACT needs out_rows, COMMIT needs out_rows == NULL");
+  if (k == 0) return FL_OK;
+  const int HD = H * d;
+  dim3 grid((unsigned)(((int64_t)k * (HD / 8) + 255) / 256), B);
+  hipStream_t st = as_stream(stream);
+#define FL_DQ(BB, AA) \
+  dequant_kernel<BB, AA><<<grid, 256, 0, st>>>(codes, scale, zero, idx, k, N, HD, group, x_hat, out_rows)
+  if (bits == 16) FL_DQ(16, 0);
+  else if (axis == FL_AXIS_TOKEN) {
+    if (bits == 2) FL_DQ(2, FL_AXIS_TOKEN); else if (bits == 4) FL_DQ(4, FL_AXIS_TOKEN); else FL_DQ(8, FL_AXIS_TOKEN);
+  } else {
+    if (bits == 2) FL_DQ(2, FL_AXIS_CHANNEL); else if (bits == 4) FL_DQ(4, FL_AXIS_CHANNEL); else FL_DQ(8, FL_AXIS_CHANNEL);
+  }
+#undef FL_DQ
+  return check_launch("dequant_kernel");
+  FL_API_END
+}

@@ -1,0 +1,253 @@
+// Token selection (Section 4.1; Appendix D.1, Eq. 5) and column-list selection (Appendix D.2, Eq. 6).
+//
+// score_rows: one wave per candidate row streams the four bf16 rows (K and V, current and previous)
+//   with 16-byte loads, forms fp32 differences, accumulates squared norms in fp64, reduces across the
+//   wave and writes the fp32 key.  HBM-bound: 4 * D * 2 bytes per candidate.
+// topk_select: one 1024-thread workgroup per segment.  Keys are mapped to order-preserving uint32 and
+//   held in registers (M per thread); the k-th largest key is found bit by bit from the MSB with block
+//   counts (32 passes, no atomics), then the selected positions are compacted in candidate order with
+//   two block scans, which emits rows ascending and breaks ties by the lower index.
+#include "fl_common.h"
+
+namespace fl {
+
+constexpr int kScoreWaves = 4;
+
+__device__ __forceinline__ void accum_pair(uint4 c, uint4 p, double& num, double& den) {
+  const uint32_t cw[4] = {c.x, c.y, c.z, c.w};
+  const uint32_t pw[4] = {p.x, p.y, p.z, p.w};
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    float c0 = __uint_as_float(cw[t] << 16), c1 = __uint_as_float(cw[t] & 0xFFFF0000u);
+    float p0 = __uint_as_float(pw[t] << 16), p1 = __uint_as_float(pw[t] & 0xFFFF0000u);
+    double d0 = (double)(c0 - p0), d1 = (double)(c1 - p1);   // fp32 difference, then exact widen
+    num += d0 * d0;
+    num += d1 * d1;
+    den += (double)c0 * (double)c0;
+    den += (double)c1 * (double)c1;
+  }
+}
+
+__global__ __launch_bounds__(64 * kScoreWaves) void score_rows_kernel(
+    const uint16_t* __restrict__ k_cur, const uint16_t* __restrict__ k_prev,
+    const uint16_t* __restrict__ v_cur, const uint16_t* __restrict__ v_prev, int N, int D,
+    const int32_t* __restrict__ cand, int n_cand, int normalize, double eps,
+    float* __restrict__ out_key) {
+  const int lane = threadIdx.x & 63;
+  const int p = blockIdx.x * kScoreWaves + (threadIdx.x >> 6);
+  const int b = blockIdx.y;
+  if (p >= n_cand) return;
+  const int64_t row = cand ? (int64_t)cand[(int64_t)b * n_cand + p] : (int64_t)p;
+  const int64_t base = ((int64_t)b * N + row) * D;
+  double num = 0.0, den = 0.0;
+#pragma unroll 4
+  for (int e = lane * 8; e < D; e += 512) {
+    uint4 kc = *reinterpret_cast<const uint4*>(k_cur + base + e);
+    uint4 kp = *reinterpret_cast<const uint4*>(k_prev + base + e);
+    uint4 vc = make_uint4(0, 0, 0, 0), vp = make_uint4(0, 0, 0, 0);
+    if (v_cur) {
+      vc = *reinterpret_cast<const uint4*>(v_cur + base + e);
+      vp = *reinterpret_cast<const uint4*>(v_prev + base + e);
+    }
+    accum_pair(kc, kp, num, den);
+    accum_pair(vc, vp, num, den);
+  }
+  num = wave_sum_f64(num);
+  den = wave_sum_f64(den);
+  if (lane == 0) {
+    double s = normalize ? sqrt(num) / (sqrt(den) + eps) : sqrt(num);
+    out_key[(int64_t)b * n_cand + p] = (float)s;
+  }
+}
+
+// ---- block-wide helpers for a 1024-thread workgroup (16 waves) -----------------------------------
+constexpr int kTopkThreads = 1024;
+constexpr int kTopkWaves = kTopkThreads / 64;
+
+__device__ __forceinline__ int block_sum(int v, int* red /* [2][16] */, int parity) {
+  v = wave_sum_i32(v);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) red[parity * kTopkWaves + w] = v;
+  __syncthreads();
+  int total = 0;
+#pragma unroll
+  for (int i = 0; i < kTopkWaves; ++i) total += red[parity * kTopkWaves + i];
+  return total;   // callers alternate parity, so the next write never races this read
+}
+
+// Exclusive prefix sum over threads in thread order; returns the prefix and sets *total.
+__device__ __forceinline__ int block_exclusive_scan(int v, int* scratch /* [16] */, int* total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int incl = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    int t = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += t;
+  }
+  __syncthreads();                                   // previous users of scratch are done
+  if (lane == 63) scratch[w] = incl;
+  __syncthreads();
+  int before = 0, all = 0;
+#pragma unroll
+  for (int i = 0; i < kTopkWaves; ++i) {
+    int s = scratch[i];
+    before += (i < w) ? s : 0;
+    all += s;
+  }
+  *total = all;
+  return before + incl - v;
+}
+
+__device__ __forceinline__ uint32_t orderable(float f) {
+  uint32_t u = __float_as_uint(f + 0.0f);   // -0 and +0 are the same key
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Segment s selects the top k of n keys.  Position p has id cand[p] (cand != NULL) or id_base + p.
+// Selected ids are written ascending at out[s * out_stride + n_prefix + pos]; ids 0..n_prefix-1 are
+// written first (column sinks).  Optional slot map: slot[s * slot_n + id] = pos (or -1).
+template <int M>
+__global__ __launch_bounds__(kTopkThreads) void topk_select_kernel(
+    const float* __restrict__ keys, int64_t key_stride, int n, int k,
+    const int32_t* __restrict__ cand, int64_t cand_stride, int id_base,
+    int32_t* __restrict__ out, int64_t out_stride, int n_prefix,
+    int32_t* __restrict__ slot, int slot_n) {
+  __shared__ int red[2 * kTopkWaves];
+  __shared__ int scan_scratch[kTopkWaves];
+  const int s = blockIdx.x;
+  const int t = threadIdx.x;
+  const float* kp = keys + (int64_t)s * key_stride;
+  const int32_t* cp = cand ? cand + (int64_t)s * cand_stride : nullptr;
+  int32_t* op = out + (int64_t)s * out_stride;
+
+  if (slot) {
+    int32_t* sp = slot + (int64_t)s * slot_n;
+    for (int i = t; i < slot_n; i += kTopkThreads) sp[i] = -1;
+  }
+  for (int i = t; i < n_prefix; i += kTopkThreads) op[i] = i;
+
+  uint32_t u[M];
+#pragma unroll
+  for (int j = 0; j < M; ++j) {
+    int p = t * M + j;
+    u[j] = (p < n) ? orderable(kp[p]) : 0u;
+  }
+
+  // k-th largest key, one bit at a time from the MSB
+  uint32_t prefix = 0, mask = 0;
+  int krem = k;
+  if (k > 0) {
+    for (int bit = 31; bit >= 0; --bit) {
+      const uint32_t want = prefix | (1u << bit), m2 = mask | (1u << bit);
+      int cnt = 0;
+#pragma unroll
+      for (int j = 0; j < M; ++j) cnt += ((t * M + j) < n && (u[j] & m2) == want) ? 1 : 0;
+      cnt = block_sum(cnt, red, bit & 1);
+      if (cnt >= krem) prefix = want; else krem -= cnt;
+      mask = m2;
+    }
+  }
+  // krem = how many keys equal to the threshold are taken, lowest positions first
+  int n_eq = 0;
+#pragma unroll
+  for (int j = 0; j < M; ++j) n_eq += (k > 0 && (t * M + j) < n && u[j] == prefix) ? 1 : 0;
+  int total;
+  int eq_rank = block_exclusive_scan(n_eq, scan_scratch, &total);
+  int n_sel = 0;
+  bool sel[M];
+#pragma unroll
+  for (int j = 0; j < M; ++j) {
+    const bool valid = k > 0 && (t * M + j) < n;
+    const bool eq = valid && u[j] == prefix;
+    sel[j] = valid && (u[j] > prefix || (eq && eq_rank < krem));
+    eq_rank += eq ? 1 : 0;
+    n_sel += sel[j] ? 1 : 0;
+  }
+  int pos = block_exclusive_scan(n_sel, scan_scratch, &total);
+  if (slot) {
+    __threadfence();
+    __syncthreads();   // the -1 fill above is complete before positions are written
+  }
+#pragma unroll
+  for (int j = 0; j < M; ++j) {
+    if (sel[j] && pos < k) {      // exactly k positions are selected; the bound is a safety net
+      const int p = t * M + j;
+      const int id = cp ? cp[p] : id_base + p;
+      op[n_prefix + pos] = id;
+      if (slot) slot[(int64_t)s * slot_n + id] = pos;
+      ++pos;
+    }
+  }
+}
+
+static int launch_topk(int segments, const float* keys, int64_t key_stride, int n, int k,
+                       const int32_t* cand, int64_t cand_stride, int id_base, int32_t* out,
+                       int64_t out_stride, int n_prefix, int32_t* slot, int slot_n,
+                       hipStream_t st) {
+  const int per = (n + kTopkThreads - 1) / kTopkThreads;
+  dim3 grid(segments), block(kTopkThreads);
+#define FL_TOPK(MM)                                                                          \
+  topk_select_kernel<MM><<<grid, block, 0, st>>>(keys, key_stride, n, k, cand, cand_stride, \
+                                                 id_base, out, out_stride, n_prefix, slot,  \
+                                                 slot_n)
+  if (per <= 1) FL_TOPK(1);
+  else if (per <= 2) FL_TOPK(2);
+  else if (per <= 4) FL_TOPK(4);
+  else if (per <= 8) FL_TOPK(8);
+  else if (per <= 16) FL_TOPK(16);
+  else if (per <= 32) FL_TOPK(32);
+  else if (per <= 64) FL_TOPK(64);
+  else return set_error(FL_E_SHAPE, "top-k over %d keys exceeds the 65536 supported", n);
+#undef FL_TOPK
+  return check_launch("topk_select_kernel");
+}
+
+}  // namespace fl
+
+using namespace fl;
+
+extern "C" int fl_select_tokens(const uint16_t* k_cur, const uint16_t* k_prev,
+                                const uint16_t* v_cur, const uint16_t* v_prev, int B, int N, int D,
+                                const int32_t* cand, int n_cand, int k, int normalize, double eps,
+                                float* out_key, int32_t* out_idx, int32_t* out_slot, void* stream) {
+  FL_API_BEGIN
+  FL_REQUIRE(k_cur && k_prev && out_key, FL_E_NULL, "fl_select_tokens: k_cur, k_prev and out_key are required");
+  FL_REQUIRE((v_cur == nullptr) == (v_prev == nullptr), FL_E_NULL,
+             "fl_select_tokens: v_cur and v_prev must both be set or both be NULL");
+  FL_REQUIRE(B >= 1 && N >= 1 && D >= 8 && D % 8 == 0, FL_E_SHAPE,
+             "fl_select_tokens: need B, N >= 1 and D a positive multiple of 8 (B=%d N=%d D=%d)", B, N, D);
+  FL_REQUIRE((int64_t)N * D < (int64_t)1 << 40, FL_E_SHAPE, "fl_select_tokens: N * D too large");
+  FL_REQUIRE(cand != nullptr || n_cand == N, FL_E_SHAPE,
+             "fl_select_tokens: without a candidate list n_cand must equal N");
+  FL_REQUIRE(n_cand >= 0 && n_cand <= N, FL_E_RANGE, "fl_select_tokens: n_cand=%d outside [0, N]", n_cand);
+  FL_REQUIRE(n_cand <= 65536, FL_E_SHAPE, "fl_select_tokens: n_cand=%d exceeds 65536", n_cand);
+  FL_REQUIRE(k >= 0 && k <= n_cand, FL_E_RANGE, "fl_select_tokens: k=%d outside [0, n_cand=%d]", k, n_cand);
+  FL_REQUIRE(k == 0 || out_idx, FL_E_NULL, "fl_select_tokens: out_idx is required when k > 0");
+  FL_REQUIRE(eps >= 0.0, FL_E_RANGE, "fl_select_tokens: eps must be >= 0");
+  hipStream_t st = as_stream(stream);
+  if (n_cand > 0) {
+    dim3 grid((n_cand + kScoreWaves - 1) / kScoreWaves, B), block(64 * kScoreWaves);
+    score_rows_kernel<<<grid, block, 0, st>>>(k_cur, k_prev, v_cur, v_prev, N, D, cand, n_cand,
+                                              normalize, eps, out_key);
+    int rc = check_launch("score_rows_kernel");
+    if (rc != FL_OK) return rc;
+  }
+  if (k == 0 && !out_slot) return FL_OK;
+  return launch_topk(B, out_key, n_cand, n_cand, k, cand, n_cand, 0, out_idx, k, 0, out_slot, N, st);
+  FL_API_END
+}
+
+extern "C" int fl_select_columns(const float* col_key, int B, int H, int N, int n_sink, int t,
+                                 int32_t* cols, void* stream) {
+  FL_API_BEGIN
+  FL_REQUIRE(col_key && cols, FL_E_NULL, "fl_select_columns: col_key and cols are required");
+  FL_REQUIRE(B >= 1 && H >= 1 && N >= 1, FL_E_SHAPE, "fl_select_columns: need B, H, N >= 1");
+  FL_REQUIRE(n_sink >= 0, FL_E_RANGE, "fl_select_columns: n_sink must be >= 0");
+  const int ns = n_sink < N ? n_sink : N;
+  FL_REQUIRE(t >= 0 && t <= N - ns, FL_E_RANGE, "fl_select_columns: t=%d outside [0, N - n_sink]", t);
+  FL_REQUIRE(N - ns <= 65536, FL_E_SHAPE, "fl_select_columns: N - n_sink exceeds 65536");
+  if (ns + t == 0) return FL_OK;
+  return launch_topk(B * H, col_key + ns, N, N - ns, t, nullptr, 0, ns, cols, ns + t, ns, nullptr, 0,
+                     as_stream(stream));
+  FL_API_END
+}

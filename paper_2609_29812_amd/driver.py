@@ -1,0 +1,58 @@
+"""Per-layer sequencing of the FlashLoop step on one GPU (device tensors only; all math is in the library).
+
+setup()       dense source loop 1: base codec of K (per-channel groups) and V (per-token groups) with the
+              reconstruction written straight into the caches, dense causal attention over the
+              reconstructed base, fp64 column statistic and the column list (Appendix D.2, Eq. 6).
+sparse_step() one sparse loop r >= 2: select the active rows among the previous loop's (Eq. 5), quantize
+              their K/V residuals against the caches and reconstruct the new rows (Eq. 8), apply the
+              mass-corrected update to their outputs (Eq. 7), then commit the new rows into the caches.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import torch
+
+from . import flashloop as fl
+
+
+@dataclass
+class LayerState:
+    k_hat: torch.Tensor            # bf16 [B, N, H, d]  X_hat of the last finished loop
+    v_hat: torch.Tensor
+    o: torch.Tensor                # fp32 [B, N, H, d]
+    lse: torch.Tensor              # fp32 [B, N, H]
+    cols: torch.Tensor             # int32 [B, H, c_list]
+    cand: torch.Tensor | None = None   # int32 [B, k] active rows of the last loop (None after loop 1)
+    window: int = 0
+    group: int = 64
+    base: dict = field(default_factory=dict)
+
+
+def setup(q1, k1, v1, base_bits, group, n_sink, t, window):
+    B, N, H, d = k1.shape
+    k_hat = torch.empty_like(k1)
+    v_hat = torch.empty_like(v1)
+    ck, sk, zk, _ = fl.kv_residual_quant(k1, None, None, base_bits, group, fl.AXIS_TOKEN, rows=k_hat)
+    cv, sv, zv, _ = fl.kv_residual_quant(v1, None, None, base_bits, group, fl.AXIS_CHANNEL, rows=v_hat)
+    o, lse = fl.dense_attn(q1, k_hat, v_hat)
+    col_key = fl.column_scores(q1, k_hat)
+    cols = fl.select_columns(col_key, n_sink, t)
+    st = LayerState(k_hat, v_hat, o, lse, cols, None, window, group)
+    st.base = dict(codes_k=ck, scale_k=sk, zero_k=zk, codes_v=cv, scale_v=sv, zero_v=zv, col_key=col_key)
+    return st
+
+
+def sparse_step(st: LayerState, qr, qp, kr, kp, vr, vp, k_r, bits, keep=False):
+    """Advance the layer by one sparse loop.  Returns the loop's outputs when keep=True."""
+    idx, slot, key = fl.select_tokens(kr, kp, vr, vp, k_r, cand=st.cand)
+    ck, sk, zk, k_new = fl.kv_residual_quant(kr, st.k_hat, idx, bits, st.group, fl.AXIS_TOKEN)
+    cv, sv, zv, v_new = fl.kv_residual_quant(vr, st.v_hat, idx, bits, st.group, fl.AXIS_CHANNEL)
+    fl.loop_sparse_attn(qr, qp, st.k_hat, st.v_hat, k_new, v_new, slot, idx, st.cols, st.window, st.lse, st.o)
+    fl.kv_residual_dequant(ck, sk, zk, idx, bits, st.group, fl.AXIS_TOKEN, st.k_hat, mode=fl.DQ_COMMIT)
+    fl.kv_residual_dequant(cv, sv, zv, idx, bits, st.group, fl.AXIS_CHANNEL, st.v_hat, mode=fl.DQ_COMMIT)
+    st.cand = idx
+    if keep:
+        return dict(idx=idx, slot=slot, key=key, codes_k=ck, scale_k=sk, zero_k=zk, codes_v=cv,
+                    scale_v=sv, zero_v=zv, k_new=k_new, v_new=v_new)
+    return None

@@ -1,0 +1,243 @@
+"""Thin ctypes binding of libflashloop.so (argument marshalling only).
+
+Every function takes torch tensors that live on the ROCm device, checks dtype/shape/contiguity,
+allocates outputs with torch, and passes raw device pointers plus the current HIP stream to the C ABI
+declared in include/flashloop.h.  All arithmetic happens in the library's HIP kernels; if the library
+is missing this module raises instead of falling back to anything else.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libflashloop.so")
+
+AXIS_TOKEN = 0
+AXIS_CHANNEL = 1
+DQ_COMPACT = 0
+DQ_COMMIT = 1
+ATTN_DENSE = 1
+
+_c_p = ctypes.c_void_p
+_c_i = ctypes.c_int
+_c_d = ctypes.c_double
+_c_f = ctypes.c_float
+_c_sz = ctypes.c_size_t
+
+_SIGNATURES = {
+    "fl_status_str": (ctypes.c_char_p, [_c_i]),
+    "fl_last_error": (ctypes.c_char_p, []),
+    "fl_abi_version": (_c_i, []),
+    "fl_select_tokens": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_i, _c_i, _c_i, _c_p, _c_i, _c_i, _c_i, _c_d,
+                                _c_p, _c_p, _c_p, _c_p]),
+    "fl_kv_residual_quant": (_c_i, [_c_p, _c_p, _c_p, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i,
+                                    _c_p, _c_p, _c_p, _c_p, _c_p]),
+    "fl_kv_residual_dequant": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i,
+                                      _c_i, _c_i, _c_p, _c_p, _c_p]),
+    "fl_loop_sparse_attn_ws": (_c_sz, [_c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i]),
+    "fl_loop_sparse_attn": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_i, _c_p, _c_i, _c_i,
+                                   _c_i, _c_i, _c_i, _c_i, _c_f, _c_i, _c_p, _c_p, _c_p, _c_sz, _c_p]),
+    "fl_column_scores_ws": (_c_sz, [_c_i, _c_i, _c_i]),
+    "fl_column_scores": (_c_i, [_c_p, _c_p, _c_i, _c_i, _c_i, _c_i, _c_p, _c_p, _c_sz, _c_p]),
+    "fl_select_columns": (_c_i, [_c_p, _c_i, _c_i, _c_i, _c_i, _c_i, _c_p, _c_p]),
+}
+
+EXPORTS = tuple(_SIGNATURES)
+
+_lib = None
+
+
+class FlashLoopError(RuntimeError):
+    pass
+
+
+def load(path: str = LIB_PATH):
+    """Load the HIP library (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise FlashLoopError(f"{path} is missing: build it with `python -m paper_2609_29812_amd.build`")
+    lib = ctypes.CDLL(path)
+    for name, (res, args) in _SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(rc: int, fn: str):
+    if rc != 0:
+        lib = load()
+        raise FlashLoopError(f"{fn}: {lib.fl_status_str(rc).decode()}: {lib.fl_last_error().decode()}")
+
+
+def _p(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _dev(t, dtype, name, shape=None):
+    if t is None:
+        return
+    if not t.is_cuda:
+        raise FlashLoopError(f"{name} must be a device tensor")
+    if t.dtype != dtype:
+        raise FlashLoopError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise FlashLoopError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise FlashLoopError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+# ---- (1) token selection ----------------------------------------------------------------------------
+def select_tokens(k_cur, k_prev, v_cur, v_prev, k, cand=None, normalize=True, eps=1e-6, slot=True,
+                  out_key=None, out_idx=None, out_slot=None):
+    """Active rows of the loop: returns (idx int32 [B, k], slot int32 [B, N] or None, key fp32 [B, n])."""
+    B, N = k_cur.shape[:2]
+    D = k_cur.numel() // (B * N)
+    for name, t in (("k_cur", k_cur), ("k_prev", k_prev), ("v_cur", v_cur), ("v_prev", v_prev)):
+        _dev(t, torch.bfloat16, name, None if t is None else k_cur.shape)
+    n_cand = N if cand is None else cand.shape[1]
+    _dev(cand, torch.int32, "cand", None if cand is None else (B, n_cand))
+    dev = k_cur.device
+    out_key = torch.empty(B, n_cand, dtype=torch.float32, device=dev) if out_key is None else out_key
+    out_idx = torch.empty(B, k, dtype=torch.int32, device=dev) if out_idx is None else out_idx
+    if slot and out_slot is None:
+        out_slot = torch.empty(B, N, dtype=torch.int32, device=dev)
+    rc = load().fl_select_tokens(_p(k_cur), _p(k_prev), _p(v_cur), _p(v_prev), B, N, D, _p(cand), n_cand,
+                                 k, 1 if normalize else 0, eps, _p(out_key), _p(out_idx),
+                                 _p(out_slot) if slot else None, _stream())
+    _check(rc, "fl_select_tokens")
+    return out_idx, (out_slot if slot else None), out_key
+
+
+# ---- (2) residual codec -----------------------------------------------------------------------------
+def meta_shape(B, k, H, d, group, axis):
+    return (B, -(-k // group), H, d) if axis == AXIS_TOKEN else (B, k, H, d // group)
+
+
+def kv_residual_quant(x_cur, x_ref, idx, bits, group, axis, rows=True, out=None):
+    """Quantize the residual of rows idx (None = all rows).  Returns (codes, scale, zero, rows)."""
+    B, N, H, d = x_cur.shape
+    _dev(x_cur, torch.bfloat16, "x_cur")
+    _dev(x_ref, torch.bfloat16, "x_ref", x_cur.shape)
+    k = N if idx is None else idx.shape[1]
+    _dev(idx, torch.int32, "idx", None if idx is None else (B, k))
+    dev = x_cur.device
+    o = out or {}
+    codes = o.get("codes")
+    if codes is None:
+        codes = torch.empty(B, k, H, d * bits // 8, dtype=torch.uint8, device=dev)
+    scale = zero = None
+    if bits != 16:
+        shp = meta_shape(B, k, H, d, group, axis)
+        scale = o.get("scale") if o.get("scale") is not None else torch.empty(shp, dtype=torch.float16, device=dev)
+        zero = o.get("zero") if o.get("zero") is not None else torch.empty(shp, dtype=torch.float16, device=dev)
+    out_rows = None
+    if rows is True:
+        out_rows = torch.empty(B, k, H, d, dtype=torch.bfloat16, device=dev)
+    elif rows is not None and rows is not False:
+        out_rows = rows
+    rc = load().fl_kv_residual_quant(_p(x_cur), _p(x_ref), _p(idx), k, B, N, H, d, bits, group, axis,
+                                     _p(codes), _p(scale), _p(zero), _p(out_rows), _stream())
+    _check(rc, "fl_kv_residual_quant")
+    return codes, scale, zero, out_rows
+
+
+def kv_residual_dequant(codes, scale, zero, idx, bits, group, axis, x_hat, mode=DQ_COMPACT):
+    """COMPACT: returns the reconstructed rows [B, k, H, d]; COMMIT: updates x_hat in place."""
+    B, N, H, d = x_hat.shape
+    _dev(x_hat, torch.bfloat16, "x_hat")
+    k = N if idx is None else idx.shape[1]
+    _dev(idx, torch.int32, "idx", None if idx is None else (B, k))
+    _dev(codes, torch.uint8, "codes", (B, k, H, d * bits // 8))
+    if bits != 16:
+        shp = meta_shape(B, k, H, d, group, axis)
+        _dev(scale, torch.float16, "scale", shp)
+        _dev(zero, torch.float16, "zero", shp)
+    out_rows = None
+    if mode == DQ_COMPACT:
+        out_rows = torch.empty(B, k, H, d, dtype=torch.bfloat16, device=x_hat.device)
+    rc = load().fl_kv_residual_dequant(_p(codes), _p(scale), _p(zero), _p(idx), k, B, N, H, d, bits, group,
+                                       axis, mode, _p(x_hat), _p(out_rows), _stream())
+    _check(rc, "fl_kv_residual_dequant")
+    return out_rows if mode == DQ_COMPACT else x_hat
+
+
+# ---- (3) attention ----------------------------------------------------------------------------------
+def loop_sparse_attn(q_cur, q_prev, k_cache, v_cache, k_new, v_new, slot, rows, cols, window, lse_ref, o,
+                     sm_scale=None, ws=None):
+    """Mass-corrected update of rows `rows` (in place on lse_ref and o)."""
+    B, N, H, d = q_cur.shape
+    k = rows.shape[1]
+    for name, t in (("q_cur", q_cur), ("q_prev", q_prev), ("k_cache", k_cache), ("v_cache", v_cache)):
+        _dev(t, torch.bfloat16, name, q_cur.shape)
+    _dev(k_new, torch.bfloat16, "k_new", (B, k, H, d))
+    _dev(v_new, torch.bfloat16, "v_new", (B, k, H, d))
+    _dev(slot, torch.int32, "slot", (B, N))
+    _dev(rows, torch.int32, "rows", (B, k))
+    c_list = 0 if cols is None else cols.shape[2]
+    _dev(cols, torch.int32, "cols", None if cols is None else (B, H, c_list))
+    _dev(lse_ref, torch.float32, "lse_ref", (B, N, H))
+    _dev(o, torch.float32, "o", (B, N, H, d))
+    sm_scale = 1.0 / math.sqrt(d) if sm_scale is None else sm_scale
+    lib = load()
+    need = lib.fl_loop_sparse_attn_ws(B, N, H, d, k, c_list, window, 0)
+    if need and (ws is None or ws.numel() < need):
+        ws = torch.empty(need, dtype=torch.uint8, device=q_cur.device)
+    rc = lib.fl_loop_sparse_attn(_p(q_cur), _p(q_prev), _p(k_cache), _p(v_cache), _p(k_new), _p(v_new),
+                                 _p(slot), _p(rows), k, _p(cols), c_list, window, B, N, H, d, sm_scale, 0,
+                                 _p(lse_ref), _p(o), _p(ws) if need else None, need, _stream())
+    _check(rc, "fl_loop_sparse_attn")
+    return o, lse_ref
+
+
+def dense_attn(q, k_cache, v_cache, o=None, lse=None, sm_scale=None):
+    """Dense causal loop: returns (o fp32 [B, N, H, d], lse fp32 [B, N, H])."""
+    B, N, H, d = q.shape
+    for name, t in (("q", q), ("k_cache", k_cache), ("v_cache", v_cache)):
+        _dev(t, torch.bfloat16, name, q.shape)
+    o = torch.empty(B, N, H, d, dtype=torch.float32, device=q.device) if o is None else o
+    lse = torch.empty(B, N, H, dtype=torch.float32, device=q.device) if lse is None else lse
+    sm_scale = 1.0 / math.sqrt(d) if sm_scale is None else sm_scale
+    lib = load()
+    need = lib.fl_loop_sparse_attn_ws(B, N, H, d, N, 0, 0, ATTN_DENSE)
+    ws = torch.empty(need, dtype=torch.uint8, device=q.device) if need else None
+    rc = lib.fl_loop_sparse_attn(_p(q), None, _p(k_cache), _p(v_cache), None, None, None, None, N, None, 0, 0,
+                                 B, N, H, d, sm_scale, ATTN_DENSE, _p(lse), _p(o), _p(ws), need, _stream())
+    _check(rc, "fl_loop_sparse_attn(dense)")
+    return o, lse
+
+
+def column_scores(q, k_cache):
+    """fp32 column keys [B, H, N] of a dense source loop (fp64 inside)."""
+    B, N, H, d = q.shape
+    _dev(q, torch.bfloat16, "q")
+    _dev(k_cache, torch.bfloat16, "k_cache", q.shape)
+    lib = load()
+    need = lib.fl_column_scores_ws(B, N, H)
+    ws = torch.empty(need, dtype=torch.uint8, device=q.device)
+    col_key = torch.empty(B, H, N, dtype=torch.float32, device=q.device)
+    rc = lib.fl_column_scores(_p(q), _p(k_cache), B, N, H, d, _p(col_key), _p(ws), need, _stream())
+    _check(rc, "fl_column_scores")
+    return col_key
+
+
+def select_columns(col_key, n_sink, t):
+    """Column list [B, H, min(n_sink, N) + t], ascending."""
+    B, H, N = col_key.shape
+    _dev(col_key, torch.float32, "col_key")
+    ns = min(n_sink, N)
+    cols = torch.empty(B, H, ns + t, dtype=torch.int32, device=col_key.device)
+    rc = load().fl_select_columns(_p(col_key), B, H, N, n_sink, t, _p(cols), _stream())
+    _check(rc, "fl_select_columns")
+    return cols

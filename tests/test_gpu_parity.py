@@ -1,0 +1,276 @@
+"""GPU parity of every call of the C ABI against the CPU oracle, at sizes the oracle finishes in seconds.
+
+Bit-exact: token keys' top-k indices and slots (keys themselves within one fp32 ulp), residual codes,
+fp16 scale/zero bit patterns, reconstructed bf16 rows and caches, column lists.  Tolerance (max-abs
+1e-2, relative Frobenius 2e-3 vs fp64): attention outputs and log-normalisers.
+Shapes span several tiles with ragged tails (row tiles of 32, column tiles of 32, groups of 32/64).
+"""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import (assert_close, assert_keys_close, down, down_bits16, f16_bits, say, up, up_bf16)
+from oracle import attention as att
+from oracle import chain, codec, select
+from oracle.numerics import bf16_to_f64, f32_to_bf16
+from workloads import get, make_layer
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def F():
+    from paper_2609_29812_amd import flashloop
+    flashloop.load()
+    return flashloop
+
+
+def _bf16(rng, shape, scale=1.0):
+    return f32_to_bf16((rng.standard_normal(shape) * scale).astype(np.float32))
+
+
+# ---------------------------------------------------------------------------------------------------
+SELECT_CASES = [("C1", {}), ("C2", dict(seq=3000, heads=4)),
+                ("C5", dict(seq=2500, heads=2, batch=3, col_budget=200))]
+
+
+@pytest.mark.parametrize("name,over", SELECT_CASES)
+def test_select_tokens_over_loops(F, name, over):
+    w = get(name).replace(**over)
+    st = make_layer(w)
+    say(f"select {w.name} B={w.batch} N={w.seq} H={w.heads}")
+    cand = None
+    for r in range(2, w.loops + 1):
+        pairs = [(st.k[r - 1], st.k[r - 2]), (st.v[r - 1], st.v[r - 2])]
+        want_key = select.token_keys(pairs, cand)
+        want_idx, want_slot = select.nested_topk(want_key, cand, w.k(r), w.seq)
+        idx, slot, key = F.select_tokens(up_bf16(st.k[r - 1]), up_bf16(st.k[r - 2]), up_bf16(st.v[r - 1]),
+                                         up_bf16(st.v[r - 2]), w.k(r),
+                                         cand=None if cand is None else up(cand))
+        torch.cuda.synchronize()
+        assert_keys_close(down(key), want_key, f"loop {r} keys")
+        assert np.array_equal(down(idx), want_idx), f"loop {r}: active rows differ"
+        assert np.array_equal(down(slot), want_slot), f"loop {r}: slot map differs"
+        cand = want_idx
+
+
+def test_select_tokens_ties_edges_and_one_pair(F):
+    rng = np.random.default_rng(21)
+    B, N, H, d = 2, 700, 2, 64
+    cur, prev = _bf16(rng, (B, N, H, d)), _bf16(rng, (B, N, H, d))
+    for dup in (5, 40, 41, 300, 699):            # exact ties with row 3 / row 200
+        src = 3 if dup < 200 else 200
+        cur[:, dup], prev[:, dup] = cur[:, src], prev[:, src]
+    dc, dp = up_bf16(cur), up_bf16(prev)
+    for k in (0, 1, 2, 37, 350, 699, 700):
+        want_key = select.token_keys([(cur, prev)])
+        want_idx, want_slot = select.nested_topk(want_key, None, k, N)
+        idx, slot, key = F.select_tokens(dc, dp, None, None, k)
+        torch.cuda.synchronize()
+        assert np.array_equal(down(idx), want_idx), k
+        assert np.array_equal(down(slot), want_slot), k
+    # unnormalized scores
+    want_key = select.token_keys([(cur, prev)], normalize=False)
+    _, _, key = F.select_tokens(dc, dp, None, None, 10, normalize=False)
+    assert_keys_close(down(key), want_key, "unnormalized keys")
+
+
+# ---------------------------------------------------------------------------------------------------
+@pytest.mark.parametrize("bits", [2, 4, 8, 16])
+@pytest.mark.parametrize("axis", [codec.AXIS_TOKEN, codec.AXIS_CHANNEL])
+@pytest.mark.parametrize("d,G", [(64, 32), (128, 64)])
+def test_codec_matches_oracle(F, bits, axis, d, G):
+    rng = np.random.default_rng(bits * 100 + axis * 10 + d)
+    B, N, H, k = 2, 300, 3, 150                    # 150 = 2*64 + 22: a partial last TOKEN group
+    ref = _bf16(rng, (B, N, H, d))
+    cur = f32_to_bf16(bf16_to_f64(ref).astype(np.float32) + (rng.standard_normal((B, N, H, d)) * 0.05)
+                      .astype(np.float32))
+    idx = np.stack([np.sort(rng.choice(N, k, replace=False)) for _ in range(B)]).astype(np.int32)
+    enc = codec.quantize(cur, ref, idx, bits, G, axis)
+    x_hat, new_rows = codec.reconstruct(ref, cur, idx, enc, bits, G, axis)
+    d_ref = up_bf16(ref)
+    codes, scale, zero, rows = F.kv_residual_quant(up_bf16(cur), d_ref, up(idx), bits, G, axis)
+    torch.cuda.synchronize()
+    assert np.array_equal(down(codes), enc["codes"]), "codes differ"
+    if bits != 16:
+        assert np.array_equal(down(scale).view(np.uint16), f16_bits(enc["scale"])), "scale differs"
+        assert np.array_equal(down(zero).view(np.uint16), f16_bits(enc["zero"])), "zero differs"
+    assert np.array_equal(down_bits16(rows), new_rows), "reconstructed rows differ"
+    compact = F.kv_residual_dequant(codes, scale, zero, up(idx), bits, G, axis, d_ref, mode=F.DQ_COMPACT)
+    torch.cuda.synchronize()
+    assert np.array_equal(down_bits16(compact), new_rows), "COMPACT dequant differs"
+    F.kv_residual_dequant(codes, scale, zero, up(idx), bits, G, axis, d_ref, mode=F.DQ_COMMIT)
+    torch.cuda.synchronize()
+    assert np.array_equal(down_bits16(d_ref), x_hat), "COMMIT dequant differs"
+
+
+@pytest.mark.parametrize("axis", [codec.AXIS_TOKEN, codec.AXIS_CHANNEL])
+def test_base_codec_all_rows(F, axis):
+    rng = np.random.default_rng(5 + axis)
+    B, N, H, d, G = 1, 333, 2, 128, 64
+    x = _bf16(rng, (B, N, H, d))
+    enc = codec.quantize(x, None, None, 4, G, axis)
+    x_hat, _ = codec.reconstruct(None, x, None, enc, 4, G, axis)
+    out = torch.empty(B, N, H, d, dtype=torch.bfloat16, device="cuda")
+    codes, scale, zero, _ = F.kv_residual_quant(up_bf16(x), None, None, 4, G, axis, rows=out)
+    torch.cuda.synchronize()
+    assert np.array_equal(down(codes), enc["codes"])
+    assert np.array_equal(down(scale).view(np.uint16), f16_bits(enc["scale"]))
+    assert np.array_equal(down(zero).view(np.uint16), f16_bits(enc["zero"]))
+    assert np.array_equal(down_bits16(out), x_hat)
+
+
+# ---------------------------------------------------------------------------------------------------
+@pytest.mark.parametrize("d", [64, 128])
+def test_dense_loop_and_column_selection(F, d):
+    rng = np.random.default_rng(d)
+    B, N, H = 2, 333, 2
+    q, k, v = (_bf16(rng, (B, N, H, d)) for _ in range(3))
+    o, lse = F.dense_attn(up_bf16(q), up_bf16(k), up_bf16(v))
+    col_key = F.column_scores(up_bf16(q), up_bf16(k))
+    cols = F.select_columns(col_key, 4, 60)
+    torch.cuda.synchronize()
+    go, gl, gk, gc = down(o), down(lse), down(col_key), down(cols)
+    sc = 1 / np.sqrt(d)
+    want_o = np.empty((B, N, H, d))
+    want_l = np.empty((B, N, H))
+    for b in range(B):
+        for h in range(H):
+            oo, ll, cs = att.dense_loop(bf16_to_f64(q[b, :, h]), bf16_to_f64(k[b, :, h]),
+                                        bf16_to_f64(v[b, :, h]), sc)
+            want_o[b, :, h], want_l[b, :, h] = oo, ll
+            assert_keys_close(gk[b, h], cs.astype(np.float32), f"column keys b={b} h={h}")
+            assert np.array_equal(gc[b, h], att.select_columns(cs.astype(np.float32), 4, 60))
+    assert_close(go, want_o, f"dense o d={d}")
+    assert_close(gl, want_l, f"dense lse d={d}")
+
+
+# ---------------------------------------------------------------------------------------------------
+CHAIN_CASES = [
+    ("C1", {}),
+    ("C2", dict(seq=1024, heads=3, col_budget=128)),
+    ("C4", dict(seq=2000, heads=2, window=128, col_budget=4 + 128 + 300)),
+    ("C5", dict(seq=1200, heads=2, batch=2, col_budget=200)),
+    ("C3", dict(seq=1500, heads=2, col_budget=160)),
+]
+
+
+def _dict_to_array(dct, B, H):
+    return np.stack([np.stack([dct[b, h] for h in range(H)], axis=1) for b in range(B)])
+
+
+@pytest.mark.parametrize("name,over", CHAIN_CASES)
+def test_chain_matches_oracle(F, name, over):
+    """GPU state end to end (setup, then every sparse loop) against the oracle's chain."""
+    from paper_2609_29812_amd import driver
+    w = get(name).replace(**over)
+    st = make_layer(w)
+    say(f"chain {w.name} B={w.batch} N={w.seq} H={w.heads} d={w.head_dim} R={w.loops} w={w.window}")
+    rec = chain.run_layer(st)
+    B, H = w.batch, w.heads
+    dev = {n: [up_bf16(a) for a in getattr(st, n)] for n in "qkv"}
+    gs = driver.setup(dev["q"][0], dev["k"][0], dev["v"][0], w.base_bits, w.group, w.n_sink, w.top_cols,
+                      w.window)
+    torch.cuda.synchronize()
+    assert np.array_equal(down_bits16(gs.k_hat), rec.k_hat1), "base K reconstruction differs"
+    assert np.array_equal(down_bits16(gs.v_hat), rec.v_hat1), "base V reconstruction differs"
+    assert np.array_equal(down(gs.base["codes_k"]), rec.enc_k1["codes"])
+    assert np.array_equal(down(gs.base["codes_v"]), rec.enc_v1["codes"])
+    gk = down(gs.base["col_key"])
+    for b in range(B):
+        for h in range(H):
+            assert_keys_close(gk[b, h], rec.colkey[b, h], f"column keys b={b} h={h}")
+    want_cols = np.stack([np.stack([rec.cols[b, h] for h in range(H)]) for b in range(B)])
+    assert np.array_equal(down(gs.cols), want_cols), "column lists differ"
+    assert_close(down(gs.o), _dict_to_array(rec.o1, B, H), "loop 1 o")
+    assert_close(down(gs.lse), _dict_to_array(rec.lse1, B, H), "loop 1 lse")
+    for lr in rec.loops:
+        r = lr.r
+        out = driver.sparse_step(gs, dev["q"][r - 1], dev["q"][r - 2], dev["k"][r - 1], dev["k"][r - 2],
+                                 dev["v"][r - 1], dev["v"][r - 2], w.k(r), w.bits_at(r), keep=True)
+        torch.cuda.synchronize()
+        say(f" loop {r}: k={w.k(r)} bits={w.bits_at(r)}")
+        assert_keys_close(down(out["key"]), lr.keys, f"loop {r} keys")
+        assert np.array_equal(down(out["idx"]), lr.idx), f"loop {r} active rows"
+        assert np.array_equal(down(out["slot"]), lr.slot), f"loop {r} slot"
+        assert np.array_equal(down(out["codes_k"]), lr.enc_k["codes"]), f"loop {r} K codes"
+        assert np.array_equal(down(out["codes_v"]), lr.enc_v["codes"]), f"loop {r} V codes"
+        if w.bits_at(r) != 16:
+            assert np.array_equal(down(out["scale_k"]).view(np.uint16), f16_bits(lr.enc_k["scale"]))
+            assert np.array_equal(down(out["zero_k"]).view(np.uint16), f16_bits(lr.enc_k["zero"]))
+            assert np.array_equal(down(out["scale_v"]).view(np.uint16), f16_bits(lr.enc_v["scale"]))
+            assert np.array_equal(down(out["zero_v"]).view(np.uint16), f16_bits(lr.enc_v["zero"]))
+        assert np.array_equal(down_bits16(out["k_new"]), lr.k_new), f"loop {r} new K rows"
+        assert np.array_equal(down_bits16(out["v_new"]), lr.v_new), f"loop {r} new V rows"
+        assert_close(down(gs.o), _dict_to_array(lr.o, B, H), f"loop {r} o (chained)")
+        assert_close(down(gs.lse), _dict_to_array(lr.lse, B, H), f"loop {r} lse (chained)")
+    assert np.array_equal(down_bits16(gs.k_hat), rec.k_hat), "final K cache differs"
+    assert np.array_equal(down_bits16(gs.v_hat), rec.v_hat), "final V cache differs"
+
+
+@pytest.mark.parametrize("name,over", [("C4", dict(seq=1100, heads=2, window=100, col_budget=4 + 100 + 150)),
+                                       ("C2", dict(seq=900, heads=2, head_dim=64, col_budget=100))])
+def test_sparse_attn_stepwise_from_oracle_state(F, name, over):
+    """One call of fl_loop_sparse_attn fed exactly the oracle's loop r-1 state."""
+    w = get(name).replace(**over)
+    st = make_layer(w)
+    rec = chain.run_layer(st)
+    B, H = w.batch, w.heads
+    o_prev, l_prev = _dict_to_array(rec.o1, B, H), _dict_to_array(rec.lse1, B, H)
+    k_hat, v_hat = rec.k_hat1, rec.v_hat1
+    cols = up(np.stack([np.stack([rec.cols[b, h] for h in range(H)]) for b in range(B)]))
+    for lr in rec.loops:
+        r = lr.r
+        o = up(o_prev.astype(np.float32))
+        lse = up(l_prev.astype(np.float32))
+        F.loop_sparse_attn(up_bf16(st.q[r - 1]), up_bf16(st.q[r - 2]), up_bf16(k_hat), up_bf16(v_hat),
+                           up_bf16(lr.k_new), up_bf16(lr.v_new), up(lr.slot), up(lr.idx), cols, w.window,
+                           lse, o)
+        torch.cuda.synchronize()
+        want_o, want_l = _dict_to_array(lr.o, B, H), _dict_to_array(lr.lse, B, H)
+        rows = lr.idx[0]
+        assert_close(down(o)[:, rows], want_o[:, rows], f"loop {r} o (step-wise, active rows)")
+        assert_close(down(lse)[:, rows], want_l[:, rows], f"loop {r} lse (step-wise, active rows)")
+        others = np.setdiff1d(np.arange(w.seq), rows)
+        assert np.array_equal(down(o)[:, others], o_prev.astype(np.float32)[:, others])
+        o_prev, l_prev = want_o, want_l
+        k_hat = codec.reconstruct(k_hat, st.k[r - 1], lr.idx, lr.enc_k, w.bits_at(r), w.group, codec.AXIS_TOKEN)[0]
+        v_hat = codec.reconstruct(v_hat, st.v[r - 1], lr.idx, lr.enc_v, w.bits_at(r), w.group, codec.AXIS_CHANNEL)[0]
+
+
+def test_all_rows_all_columns_no_quantization_is_dense_attention(F):
+    """The special case that reduces the chain to exact dense attention of each loop, on the GPU."""
+    from paper_2609_29812_amd import driver
+    w = get("C2").replace(seq=500, heads=2, head_dim=128, topk_frac=(1.0, 1.0, 1.0), bits=(16, 16, 16),
+                          col_budget=500, n_sink=500)
+    st = make_layer(w)
+    dev = {n: [up_bf16(a) for a in getattr(st, n)] for n in "qkv"}
+    gs = driver.setup(dev["q"][0], dev["k"][0], dev["v"][0], 16, w.group, w.seq, 0, 0)
+    for r in range(2, w.loops + 1):
+        driver.sparse_step(gs, dev["q"][r - 1], dev["q"][r - 2], dev["k"][r - 1], dev["k"][r - 2],
+                           dev["v"][r - 1], dev["v"][r - 2], w.seq, 16)
+        o, lse = F.dense_attn(dev["q"][r - 1], dev["k"][r - 1], dev["v"][r - 1])
+        torch.cuda.synchronize()
+        assert_close(down(gs.o), down(o), f"loop {r}: corrected vs dense (GPU)")
+        for h in range(w.heads):
+            want, _, _ = att.dense_loop(*(bf16_to_f64(getattr(st, n)[r - 1][0, :, h]) for n in "qkv"),
+                                        w.sm_scale, want_colscore=False)
+            assert_close(down(gs.o)[0, :, h], want, f"loop {r} h={h}: corrected vs oracle dense")
+
+
+def test_results_are_deterministic(F):
+    from paper_2609_29812_amd import driver
+    w = get("C4").replace(seq=1500, heads=2, window=64, col_budget=4 + 64 + 200)
+    st = make_layer(w)
+    outs = []
+    for _ in range(2):
+        dev = {n: [up_bf16(a) for a in getattr(st, n)] for n in "qkv"}
+        gs = driver.setup(dev["q"][0], dev["k"][0], dev["v"][0], w.base_bits, w.group, w.n_sink,
+                          w.top_cols, w.window)
+        for r in range(2, w.loops + 1):
+            driver.sparse_step(gs, dev["q"][r - 1], dev["q"][r - 2], dev["k"][r - 1], dev["k"][r - 2],
+                               dev["v"][r - 1], dev["v"][r - 2], w.k(r), w.bits_at(r))
+        torch.cuda.synchronize()
+        outs.append([down(gs.o), down(gs.lse), down_bits16(gs.k_hat), down(gs.cols), down(gs.base["col_key"])])
+    for a, b in zip(*outs):
+        assert np.array_equal(a.view(np.uint8), b.view(np.uint8))

@@ -44,6 +44,9 @@ def test_directed_fp16_rounding_matches_exhaustive_table():
     for x, dn, u in zip(xs.tolist(), down.tolist(), up.tolist()):
         assert dn == _table_down(x), x
         assert u == _table_up(x), x
+    # zeros are stored as +0 whatever their sign (a stated reading)
+    for z in (f16_down(np.array([0.0, -0.0])), f16_up(np.array([0.0, -0.0]))):
+        assert z.view(np.uint16).tolist() == [0, 0]
     # saturation outside the fp16 range (a stated reading)
     assert float(f16_down(np.array([-1e6]))[0]) == -65504.0
     assert float(f16_up(np.array([1e6]))[0]) == 65504.0
