@@ -1,0 +1,378 @@
+"""Benchmark of the FlashLoop per-loop step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload C4] [--no-cpu-baseline]
+    python bench.py --copy-calib        # plain copy kernel of known size (HBM counter calibration)
+
+One step = every sparse loop r = 2..R of one layer over one batch of synthetic input, each loop being
+the whole hot path: token scoring + top-k, K and V residual quantization (with the reconstructed new
+rows), the mass-corrected sparse attention update, and the in-place dequantization that commits the new
+rows into the K/V caches.  The dense loop-1 set-up (base codec, dense attention, fp64 column statistic,
+column lists) runs once before timing.  Inputs are resident in HBM before the timed region; every step
+re-runs loops 2..R on the state the previous step left (the work of each call depends only on the
+fixed budgets, not on the values).
+
+Prints ONE JSON line with the metric (updated rows per second per layer-loop), the roofline of the
+dominant kernel measured with HIP events on the launch stream, and the CPU oracle timed on a bounded
+sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "updated-token attn rows/s per layer-loop + achieved HBM GB/s & MFMA % at 32K"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+MFMA_BF16_TFLOPS = 2500.0      # dense bf16/fp16 MFMA
+PROFILE_DIR = os.path.join(ROOT, "profiles")
+ATTN_SRC = os.path.join(ROOT, "paper_2609_29812_amd", "csrc", "fl_attn.hip")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+# ---- algorithmic work of each call (what the method itself must move / compute) ----------------------
+def attn_work(idx, cols, slot, N, H, d, window, B):
+    """Exact algorithmic bytes and flops of one sparse attention launch.
+
+    flops = 8 d * sum over (b, h, i in A) |S_i|  (two passes, each q.k and p.v);
+    bytes = Q rows of loops r and r-1, o and lse in/out of the updated rows, every distinct column of
+            K/V touched by some S_i (cache rows, plus the new rows of updated columns), the column list
+            and the slot entries of the touched columns.
+    """
+    flops = 0.0
+    nbytes = 0.0
+    for b in range(B):
+        rows = idx[b].astype(np.int64)
+        k = rows.size
+        upd = slot[b] >= 0
+        for h in range(H):
+            g = np.sort(cols[b, h].astype(np.int64))
+            n_list = np.searchsorted(g, rows - window, side="right")         # list columns j <= i - w
+            n_band = np.minimum(window, rows + 1) if window > 0 else 0
+            flops += 8.0 * d * float(np.sum(n_list + n_band))
+            used = np.zeros(N, dtype=bool)
+            if rows.size:
+                used[g[g <= rows.max() - window]] = True
+                if window > 0:
+                    diff = np.zeros(N + 1, dtype=np.int64)
+                    np.add.at(diff, np.maximum(rows - window + 1, 0), 1)
+                    np.add.at(diff, rows + 1, -1)
+                    used |= np.cumsum(diff[:N]) > 0
+            n_used = int(used.sum())
+            n_new = int((used & upd).sum())
+            nbytes += (n_used + n_new) * d * 2 * 2          # K and V rows, bf16
+            nbytes += n_used * 4 + g.size * 4               # slot lookups and the column list
+        nbytes += k * H * d * 2 * 2                         # q_cur, q_prev rows
+        nbytes += k * H * d * 4 * 2 + k * H * 4 * 2         # o and lse in/out
+        nbytes += k * 4
+    return nbytes, flops
+
+
+def codec_bytes(k, H, d, bits, group, axis_token, B):
+    """quantize: read cur + ref rows, write codes + metadata + reconstructed rows."""
+    rows = B * k * H * d
+    meta = B * (math.ceil(k / group) * H * d if axis_token else k * H * (d // group)) * 2 * 2
+    return rows * 2 * 2 + rows * bits / 8 + meta + rows * 2 + B * k * 4
+
+
+def commit_bytes(k, H, d, bits, group, axis_token, B):
+    """dequantize in place: read codes + metadata + cache rows, write cache rows."""
+    rows = B * k * H * d
+    meta = B * (math.ceil(k / group) * H * d if axis_token else k * H * (d // group)) * 2 * 2
+    return rows * bits / 8 + meta + rows * 2 * 2 + B * k * 4
+
+
+def select_bytes(n_cand, N, D, k, B):
+    return B * (n_cand * D * 2 * 4 + n_cand * 4 * 2 + k * 4 + N * 4 + n_cand * 4)
+
+
+# ---- the timed step ------------------------------------------------------------------------------------
+class Step:
+    def __init__(self, w, dev, gs, fl, torch):
+        self.w, self.dev, self.gs, self.fl, self.torch = w, dev, gs, fl, torch
+
+    def run(self, events=None):
+        """One step (loops 2..R).  events: optional dict name -> list of (start, end) event pairs."""
+        w, dev, gs, fl = self.w, self.dev, self.gs, self.fl
+        torch = self.torch
+        gs.cand = None
+        trace = []
+
+        def timed(name, fn):
+            if events is None:
+                return fn()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            out = fn()
+            e1.record()
+            events.setdefault(name, []).append((e0, e1))
+            return out
+
+        for r in range(2, w.loops + 1):
+            qr, qp = dev["q"][r - 1], dev["q"][r - 2]
+            kr, kp = dev["k"][r - 1], dev["k"][r - 2]
+            vr, vp = dev["v"][r - 1], dev["v"][r - 2]
+            bits, kk = w.bits_at(r), w.k(r)
+            idx, slot, _ = timed(f"select r{r}", lambda: fl.select_tokens(kr, kp, vr, vp, kk, cand=gs.cand))
+            ck, sk, zk, k_new = timed(f"quant_k r{r}", lambda: fl.kv_residual_quant(
+                kr, gs.k_hat, idx, bits, gs.group, fl.AXIS_TOKEN))
+            cv, sv, zv, v_new = timed(f"quant_v r{r}", lambda: fl.kv_residual_quant(
+                vr, gs.v_hat, idx, bits, gs.group, fl.AXIS_CHANNEL))
+            timed(f"attn r{r}", lambda: fl.loop_sparse_attn(qr, qp, gs.k_hat, gs.v_hat, k_new, v_new, slot, idx,
+                                                             gs.cols, gs.window, gs.lse, gs.o))
+            timed(f"commit_k r{r}", lambda: fl.kv_residual_dequant(ck, sk, zk, idx, bits, gs.group, fl.AXIS_TOKEN,
+                                                                    gs.k_hat, mode=fl.DQ_COMMIT))
+            timed(f"commit_v r{r}", lambda: fl.kv_residual_dequant(cv, sv, zv, idx, bits, gs.group,
+                                                                    fl.AXIS_CHANNEL, gs.v_hat, mode=fl.DQ_COMMIT))
+            trace.append((r, idx, slot))
+            gs.cand = idx
+        return trace
+
+
+def source_sha(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def load_traffic(kernel, workload):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if taken on the current source."""
+    path = os.path.join(PROFILE_DIR, f"{kernel}_{workload}_pmc.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("source_sha") != source_sha(ATTN_SRC):
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+# ---- CPU oracle leg ------------------------------------------------------------------------------------
+def cpu_baseline(w, st, threads_note):
+    """The oracle's per-loop step (select + codec for every head, the update for every active row of
+    head 0, scaled by the head count) on the host cores; the dense loop-1 set-up for head 0 is untimed."""
+    from oracle import attention as att
+    from oracle import chain as och
+    from oracle import codec, select
+    from oracle.numerics import bf16_to_f64
+
+    t0 = time.time()
+    rec = och.loop1(st, heads=[0])
+    log(f"[cpu] oracle loop-1 setup (head 0, untimed) {time.time() - t0:.1f}s")
+    o = {key: v.copy() for key, v in rec.o1.items()}
+    lse = {key: v.copy() for key, v in rec.lse1.items()}
+    k_hat, v_hat = rec.k_hat1, rec.v_hat1
+    cand = None
+    t_est = 0.0
+    t_cpu = 0.0
+    rows_total = 0
+    for r in range(2, w.loops + 1):
+        ta = time.perf_counter()
+        keys = select.token_keys([(st.k[r - 1], st.k[r - 2]), (st.v[r - 1], st.v[r - 2])], cand)
+        idx, slot = select.nested_topk(keys, cand, w.k(r), w.seq)
+        bits = w.bits_at(r)
+        ek = codec.quantize(st.k[r - 1], k_hat, idx, bits, w.group, codec.AXIS_TOKEN)
+        k_new_hat, _ = codec.reconstruct(k_hat, st.k[r - 1], idx, ek, bits, w.group, codec.AXIS_TOKEN)
+        ev = codec.quantize(st.v[r - 1], v_hat, idx, bits, w.group, codec.AXIS_CHANNEL)
+        v_new_hat, _ = codec.reconstruct(v_hat, st.v[r - 1], idx, ev, bits, w.group, codec.AXIS_CHANNEL)
+        tb = time.perf_counter()
+        for b in range(w.batch):
+            kp, vp = bf16_to_f64(k_hat[b, :, 0]), bf16_to_f64(v_hat[b, :, 0])
+            kc, vc = bf16_to_f64(k_new_hat[b, :, 0]), bf16_to_f64(v_new_hat[b, :, 0])
+            qc, qp = bf16_to_f64(st.q[r - 1][b, :, 0]), bf16_to_f64(st.q[r - 2][b, :, 0])
+            for i in idx[b]:
+                S = att.row_columns(rec.cols[b, 0], int(i), w.window)
+                o[b, 0][i], lse[b, 0][i], _ = att.correct_row(S, qc[i], qp[i], kp, vp, kc, vc, lse[b, 0][i],
+                                                              o[b, 0][i], w.sm_scale)
+        tc = time.perf_counter()
+        t_est += (tb - ta) + (tc - tb) * w.heads
+        t_cpu += tc - ta
+        rows_total += w.batch * w.k(r)
+        k_hat, v_hat, cand = k_new_hat, v_new_hat, idx
+    return {
+        "value": rows_total / t_est,
+        "unit": "rows/s",
+        "cores": threads_note,
+        "kind": "oracle",
+        "sample": (f"{w.name} loops 2-{w.loops}: token scoring, top-k and the K/V residual codec for all "
+                   f"{w.heads} heads, the mass-corrected update for every active row of head 0 only "
+                   f"(its time x{w.heads}); {t_cpu:.1f}s of CPU work, estimated full step {t_est:.1f}s"),
+    }
+
+
+def blas_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        n = [i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"]
+        return max(n) if n else 1
+    except Exception:
+        return 1
+
+
+# ---- copy calibration ----------------------------------------------------------------------------------
+def copy_calib():
+    import torch
+    nbytes = 1 << 30
+    src = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": nbytes, "copy_bytes_written": nbytes, "dispatches": 5}), flush=True)
+
+
+# ---- main ----------------------------------------------------------------------------------------------
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="C4")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calib", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for {args.gpus}); "
+              "the step would shard by head with one small all-gather of row-score partials.", flush=True)
+        sys.exit(2)
+    import torch
+    torch.cuda.set_device(0)
+    if args.copy_calib:
+        copy_calib()
+        return
+
+    from paper_2609_29812_amd import driver
+    from paper_2609_29812_amd import flashloop as fl
+    from workloads import get, make_layer
+
+    fl.load()
+    w = get(args.workload)
+    t0 = time.time()
+    st = make_layer(w)
+    log(f"[bench] generated {w.name} in {time.time() - t0:.1f}s")
+
+    def up(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda().view(torch.bfloat16)
+
+    dev = {n: [up(a) for a in getattr(st, n)] for n in "qkv"}
+    t0 = time.time()
+    gs = driver.setup(dev["q"][0], dev["k"][0], dev["v"][0], w.base_bits, w.group, w.n_sink, w.top_cols,
+                      w.window)
+    torch.cuda.synchronize()
+    log(f"[bench] loop-1 setup on GPU {time.time() - t0:.2f}s")
+    step = Step(w, dev, gs, fl, torch)
+
+    for _ in range(args.warmup):
+        step.run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_wall = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        step.run()
+    e1.record()
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    ms_step = e0.elapsed_time(e1) / args.steps
+    rows_per_step = sum(w.batch * w.k(r) for r in range(2, w.loops + 1))
+    log(f"[bench] {args.steps} steps: {ms_step:.4f} ms/step (wall {t_wall / args.steps * 1e3:.4f} ms)")
+
+    # per-call durations with events on the launch stream (a separate pass, same work)
+    events = {}
+    reps = max(3, min(args.steps, 10))
+    trace = None
+    for _ in range(reps):
+        trace = step.run(events)
+    torch.cuda.synchronize()
+    dur_us = {name: float(np.mean([a.elapsed_time(b) for a, b in pairs])) * 1e3 for name, pairs in events.items()}
+
+    cols = gs.cols.cpu().numpy()
+    B, N, H, d = w.batch, w.seq, w.heads, w.head_dim
+    kernels = {}
+    attn_bytes = attn_flops = attn_us = 0.0
+    total_bytes = 0.0
+    n_cand = N
+    for r, idx_t, slot_t in trace:
+        idx, slot = idx_t.cpu().numpy(), slot_t.cpu().numpy()
+        kr, bits = w.k(r), w.bits_at(r)
+        by, fl_ = attn_work(idx, cols, slot, N, H, d, w.window, B)
+        work = {
+            f"select r{r}": (select_bytes(n_cand, N, H * d, kr, B), 0.0),
+            f"quant_k r{r}": (codec_bytes(kr, H, d, bits, w.group, True, B), 0.0),
+            f"quant_v r{r}": (codec_bytes(kr, H, d, bits, w.group, False, B), 0.0),
+            f"attn r{r}": (by, fl_),
+            f"commit_k r{r}": (commit_bytes(kr, H, d, bits, w.group, True, B), 0.0),
+            f"commit_v r{r}": (commit_bytes(kr, H, d, bits, w.group, False, B), 0.0),
+        }
+        for name, (nb, nf) in work.items():
+            us = dur_us[name]
+            kernels[name] = {"us": round(us, 2), "GB/s": round(nb / us / 1e3, 1),
+                             "TFLOP/s": round(nf / us / 1e6, 2) if nf else None,
+                             "alg_MB": round(nb / 1e6, 2), "alg_GF": round(nf / 1e9, 3) if nf else None}
+            total_bytes += nb
+        attn_bytes += by
+        attn_flops += fl_
+        attn_us += dur_us[f"attn r{r}"]
+        n_cand = kr
+    for name, kv in kernels.items():
+        log(f"  {name:12s} {kv['us']:9.2f} us  {kv['GB/s']:8.1f} GB/s  alg {kv['alg_MB']:8.2f} MB"
+            + (f"  {kv['TFLOP/s']:7.2f} TFLOP/s" if kv["TFLOP/s"] else ""))
+    n_loops = w.loops - 1
+    t_hbm = attn_bytes / (HBM_PEAK_GBS * 1e9)
+    t_mfma = attn_flops / (MFMA_BF16_TFLOPS * 1e12)
+    bound = "hbm" if t_hbm >= t_mfma else "mfma"
+    if bound == "hbm":
+        achieved = attn_bytes / n_loops / (attn_us / n_loops * 1e-6) / 1e9
+        peak, unit = HBM_PEAK_GBS, "GB/s"
+    else:
+        achieved = attn_flops / n_loops / (attn_us / n_loops * 1e-6) / 1e12
+        peak, unit = MFMA_BF16_TFLOPS, "TFLOP/s"
+    traffic = load_traffic("loop_attn", w.name)
+    roofline = {"kernel": "loop_attn_kernel", "bound": bound, "achieved": round(achieved, 2), "peak": peak,
+                "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic,
+                "alg_bytes_per_launch": round(attn_bytes / n_loops), "alg_flops_per_launch": round(attn_flops / n_loops),
+                "avg_launch_us": round(attn_us / n_loops, 2),
+                "mfma_frac": round(attn_flops / (attn_us * 1e-6) / 1e12 / MFMA_BF16_TFLOPS, 4),
+                "hbm_frac": round(attn_bytes / (attn_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+
+    result = {
+        "metric": METRIC,
+        "value": round(rows_per_step / (ms_step * 1e-3), 1),
+        "unit": "rows/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "batch": B, "seq": N, "heads": H, "head_dim": d, "loops": w.loops,
+                   "sparse_loops": f"2-{w.loops}", "rows_per_step": rows_per_step,
+                   "k_per_loop": [w.k(r) for r in range(2, w.loops + 1)], "column_budget": w.col_budget,
+                   "window": w.window, "residual_bits": list(w.bits), "group": w.group},
+        "step_hbm_GBps": round(total_bytes / (ms_step * 1e-3) / 1e9, 1),
+        "attn_rows_per_s": round(rows_per_step / (attn_us * 1e-6), 1),
+        "roofline": roofline,
+        "kernels": kernels,
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(w, st, blas_threads())
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()
