@@ -1,26 +1,39 @@
 // Mass-corrected sparse attention update (Sections 3.2 and 4.2, Eq. 3; Appendix D.2, Eq. 7) and the
 // dense source loop (Eq. 2, causal).
 //
-// A wave owns 32 updated rows of one (batch, head).  Columns are visited in tiles of 32:
-//   list phase : entries of the per-(batch, head) column list with j + window <= i (columns inside the
-//                row's band are left to the band phase, so a column in both is counted once);
-//   band phase : the contiguous range covering every row's band (i - window, i], masked per row;
-//                the dense loop is the band phase with an unbounded window.
-// Per tile the gathered K rows are staged in LDS row-major (bf16) and the V rows transposed (fp16), for
-// the loop r-1 state (cache) and the loop r state (new rows via the slot map, cache otherwise).
-// Scores are computed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16 so that each lane holds
-// 16 columns of a single row; the probabilities then feed O^T += V^T P^T (v_mfma_f32_32x32x16_f16)
-// straight from registers, and every accumulator of a lane belongs to that lane's row.
+// Column sets.  For updated row i the columns are S_i = (list U band(i)) restricted to j <= i; a column
+// in both is counted once by giving list columns the condition j + window <= i and band columns
+// i - window < j <= i.  The subtract pass needs the loop r-1 state of every column of S_i; the add pass
+// needs the loop r state, which differs from the cache only for columns updated in this loop (those in
+// the active set).  So every tile is staged from ONE state:
+//   phase A  list columns, cache state      subtract: all; add: columns not updated this loop
+//   phase B  band columns, cache state      subtract: all; add: columns not updated this loop
+//   phase C  updated list columns, new rows add only (compacted per (batch, head) by a prep kernel)
+//   phase D  updated band columns, new rows add only (a contiguous range of the active rows)
+// The dense loop is phase B alone with an unbounded band.
+//
+// Work decomposition.  A workgroup of 4 waves takes consecutive updated rows of one (batch, head): 64
+// rows in the sparse update, where waves 0-1 run the subtract pass and waves 2-3 the add pass for the
+// same two groups of 32 rows, and 128 rows in the dense loop, where every wave runs the softmax pass.
+// The row tiles of one (batch, head) map to one XCD so its list columns stay in that XCD's L2.
+//
+// Data movement.  Column tiles of 32 are gathered straight from HBM into a ring of 4 LDS slots with
+// buffer_load ... lds (no registers), three tiles ahead of the one being computed; out-of-range offsets
+// return zeros, which masks padding without branches.  K rows are stored with their 16-byte chunks
+// XOR-swizzled by the row and read as the A operand of S^T = K Q^T (v_mfma_f32_32x32x16_bf16), so each
+// lane holds 16 columns of one row.  V rows are converted in place to fp16 (exact for |v| in
+// [2^-14, 65504]) by the wave whose DMA wrote them, and read transposed with ds_read_b64_tr_b16 as the A
+// operand of O^T += V^T P^T (v_mfma_f32_32x32x16_f16, P in fp16).
 //   subtract pass : pp = exp(a - lse_ref), no running max needed (lse_ref bounds the logits);
 //   add pass      : online softmax with a running max shared by the two half-waves of a row.
 #include "fl_common.h"
 
+#include <climits>
+
 namespace fl {
 
-constexpr int kBM = 32;      // rows per wave
-constexpr int kBN = 32;      // columns per tile
-constexpr int kKPad = 8;     // bf16 elements of padding per LDS K row
-constexpr int kVPad = 4;     // fp16 elements of padding per LDS V^T row
+constexpr int kBN = 32;            // columns per tile
+constexpr int kRing = 4;           // LDS ring slots
 
 struct AttnArgs {
   const uint16_t* q_cur;
@@ -32,263 +45,458 @@ struct AttnArgs {
   const int32_t* slot;
   const int32_t* rows;
   const int32_t* cols;
+  const int2* desc;          // [B, H, c_list] (column, slot) of the list (prep kernel)
+  const int2* upd;           // [B, H, c_list] compacted updated list columns (prep kernel)
+  const int32_t* n_upd;      // [B, H]
   float* lse_ref;
   float* o;
-  int k, c_list, window, N, H;
-  float scale_log2;   // sm_scale * log2(e)
-  int dense;
+  int k, c_list, window, B, N, H;
+  float scale_log2;          // sm_scale * log2(e)
 };
 
-template <int D>
-struct AttnSmem {
-  uint16_t k[2][kBN][D + kKPad];     // [0] loop r-1 (cache), [1] loop r
-  _Float16 vt[2][D][kBN + kVPad];
-  int cid[kBN];
-  int nslot[kBN];
-};
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+constexpr uint32_t kOOB = 0x80000000u;   // beyond every descriptor's range (ranges stay <= 2^31)
+#define FL_LDS(p) ((__attribute__((address_space(3))) void*)(p))
+#define FL_LDS4(p) ((__attribute__((address_space(3))) i16x4*)(p))
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+
+// s_waitcnt vmcnt(n) with every other counter left alone (gfx9 encoding).
+#define FL_WAIT_VM(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (7 << 4) | (15 << 8) | ((((n) >> 4) & 3) << 14))
+// LDS traffic done, then a workgroup barrier without a memory fence (LDS-DMA waits are explicit).
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+}
 
 __device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
-  _Float16 ha = (_Float16)a, hb = (_Float16)b;
-  return (uint32_t)__builtin_bit_cast(uint16_t, ha) | ((uint32_t)__builtin_bit_cast(uint16_t, hb) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){a, b}, f16x2));
 }
 
-// bf16 pair (packed in a uint32) -> fp16 pair, exact for normal-range values.
-__device__ __forceinline__ uint32_t bf16x2_to_f16x2(uint32_t w) {
-  return pack_f16x2(__uint_as_float(w << 16), __uint_as_float(w & 0xFFFF0000u));
+// max / sum of a lane and lane ^ 32 (the two half-waves hold disjoint columns of the same row)
+__device__ __forceinline__ float xor32_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float xor32_add(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// Stage one tile of gathered K (row-major) and V (transposed, fp16) for both states into LDS.
+// One ring slot: the LDS-DMA target of one tile.  Column ids and flags live in separate arrays (never
+// a DMA target), so the compiler's LDS-DMA tracking does not order them behind pending tile loads.
 template <int D>
-__device__ __forceinline__ void stage_tile(const AttnArgs& a, AttnSmem<D>& sm, int b, int h,
-                                           bool need_old) {
-  const int lane = threadIdx.x;
-  constexpr int CH = D / 8;                   // 16-byte chunks per row
-  const int64_t HD = (int64_t)a.H * D;
-  // K: 32 columns x CH chunks
-#pragma unroll
-  for (int q = lane; q < kBN * CH; q += 64) {
-    const int c = q / CH, ch = q % CH;
-    const int cid = sm.cid[c], ns = sm.nslot[c];
-    uint4 old = make_uint4(0, 0, 0, 0), nw;
-    if (cid >= 0)
-      old = *reinterpret_cast<const uint4*>(a.k_cache + ((int64_t)b * a.N + cid) * HD + (int64_t)h * D + ch * 8);
-    nw = old;
-    if (ns >= 0)
-      nw = *reinterpret_cast<const uint4*>(a.k_new + ((int64_t)b * a.k + ns) * HD + (int64_t)h * D + ch * 8);
-    if (need_old) *reinterpret_cast<uint4*>(&sm.k[0][c][ch * 8]) = old;
-    *reinterpret_cast<uint4*>(&sm.k[1][c][ch * 8]) = nw;
-  }
-  // V: groups of 4 columns x CH chunks, written transposed (dims x columns)
-#pragma unroll
-  for (int q = lane; q < (kBN / 4) * CH; q += 64) {
-    const int cg = q / CH, ch = q % CH;
-    uint4 vo[4], vn[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int c = cg * 4 + u;
-      const int cid = sm.cid[c], ns = sm.nslot[c];
-      vo[u] = make_uint4(0, 0, 0, 0);
-      if (cid >= 0)
-        vo[u] = *reinterpret_cast<const uint4*>(a.v_cache + ((int64_t)b * a.N + cid) * HD + (int64_t)h * D + ch * 8);
-      vn[u] = vo[u];
-      if (ns >= 0)
-        vn[u] = *reinterpret_cast<const uint4*>(a.v_new + ((int64_t)b * a.k + ns) * HD + (int64_t)h * D + ch * 8);
-    }
-#pragma unroll
-    for (int which = 0; which < 2; ++which) {
-      if (which == 0 && !need_old) continue;
-      const uint4* src = which ? vn : vo;
-      // element e of chunk: word e/2, half e&1
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        uint32_t hv[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const uint32_t wsel = (e >> 1) == 0 ? src[u].x : (e >> 1) == 1 ? src[u].y : (e >> 1) == 2 ? src[u].z : src[u].w;
-          const uint32_t bits = (e & 1) ? (wsel >> 16) : (wsel & 0xFFFFu);
-          hv[u] = bits;
-        }
-        const uint32_t lo = pack_f16x2(bf16_to_f32(hv[0]), bf16_to_f32(hv[1]));
-        const uint32_t hi = pack_f16x2(bf16_to_f32(hv[2]), bf16_to_f32(hv[3]));
-        *reinterpret_cast<uint2*>(&sm.vt[which][ch * 8 + e][cg * 4]) = make_uint2(lo, hi);
-      }
-    }
-  }
-}
+struct Slot {
+  uint16_t k[kBN * D];     // row c at c*D; its 16-byte chunk ch sits at chunk position ch ^ (c & 7)
+  uint16_t v[kBN * D];     // same layout; converted in place from bf16 to fp16 before use
+};
 
-template <int D>
-__global__ __launch_bounds__(64) void loop_attn_kernel(AttnArgs a) {
-  __shared__ AttnSmem<D> sm;
-  constexpr int KS = D / 16;    // k-steps of the QK^T contraction
-  constexpr int DB = D / 32;    // 32-dim blocks of the output
-  const int lane = threadIdx.x;
-  const int hw = lane >> 5;     // half-wave
-  const int r32 = lane & 31;    // this lane's row within the tile
-  const int p0 = blockIdx.x * kBM;
-  const int h = blockIdx.y, b = blockIdx.z;
-  const int64_t HD = (int64_t)a.H * D;
+__device__ __forceinline__ int swz(int c, int ch) { return ch ^ (c & 7); }
 
-  const int p = p0 + r32;
+template <int D, bool DENSE>
+__global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
+  constexpr int GROUPS = DENSE ? 4 : 2;
+  constexpr int BM = 32 * GROUPS;
+  constexpr int KS = D / 16;              // k-steps of QK^T
+  constexpr int DB = D / 32;              // 32-dim output blocks
+  constexpr int CH = D / 8;               // 16-byte chunks per row
+  constexpr int COLS_PER_INST = 64 / CH;  // rows covered by one 1 KB LDS-DMA instruction
+  constexpr int INST_PER_TILE = kBN / COLS_PER_INST;
+  constexpr int INST_PER_WAVE = INST_PER_TILE / 4;   // per tensor (K and V each)
+  __shared__ Slot<D> s0, s1, s2, s3;
+  __shared__ int tcid[8][kBN];            // column ids of tile v in entry v % 8 (-1 = padding)
+  __shared__ int trow[8][kBN];            // the row each column is loaded from (cache or new rows)
+  __shared__ int tupd[8][kBN];            // 1 when that column was updated this loop (phases A/B)
+  __shared__ int tany[8];                 // some column of tile v was updated (phases A/B)
+  __shared__ float xm[2][64];
+  __shared__ int s_meta[2];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int hw = lane >> 5;
+  const int r32 = lane & 31;
+  const int group = wave % GROUPS;
+  const bool add_pass = DENSE || wave >= 2;
+
+  // work item -> (batch*head, row tile); the row tiles of one (batch, head) stay on one XCD
+  const int n_rt = (a.k + BM - 1) / BM;
+  const int n_bh = a.B * a.H;
+  int bh, rt;
+  if ((n_bh & 7) == 0) {
+    const int g = blockIdx.x & 7, s = blockIdx.x >> 3;
+    bh = g + 8 * (s / n_rt);
+    rt = n_rt - 1 - (s % n_rt);
+  } else {
+    bh = blockIdx.x / n_rt;
+    rt = n_rt - 1 - (blockIdx.x % n_rt);
+  }
+  const int b = bh / a.H, h = bh % a.H;
+  const int64_t HD = (int64_t)a.H * D;
+  const int32_t* rowp = DENSE ? nullptr : a.rows + (int64_t)b * a.k;
+  auto row_of = [&](int p) { return DENSE ? p : rowp[p]; };
+
+  const int p0 = rt * BM;
+  const int last_p = min(p0 + BM, a.k) - 1;
+  const int min_row = row_of(p0), max_row = row_of(last_p);
+  const int gp0 = p0 + 32 * group;
+  const bool group_has_rows = gp0 < a.k;
+  const int gmin = group_has_rows ? row_of(gp0) : 0;
+  const int gmax = group_has_rows ? row_of(min(gp0 + 32, a.k) - 1) : -1;
+  const int p = gp0 + r32;
   const bool row_ok = p < a.k;
-  const int row_i = row_ok ? (a.rows ? a.rows[(int64_t)b * a.k + p] : p) : -1;
-  const int last_p = min(p0 + kBM, a.k) - 1;
-  const int min_row = a.rows ? a.rows[(int64_t)b * a.k + p0] : p0;
-  const int max_row = a.rows ? a.rows[(int64_t)b * a.k + last_p] : last_p;
+  const int row_i = row_ok ? row_of(p) : -1;
 
-  // Q fragments (B operand of S^T = K Q^T): row r32, dims 16*ks + 8*hw .. +7
-  bf16x8 qc[KS], qp[KS];
+  // query fragments (B operand of S^T = K Q^T): row r32, dims 16*ks + 8*hw .. +7
+  bf16x8 qf[KS];
   {
+    const uint16_t* qsrc = add_pass ? a.q_cur : a.q_prev;
     const int64_t qoff = ((int64_t)b * a.N + (row_ok ? row_i : 0)) * HD + (int64_t)h * D + hw * 8;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      uint4 w = row_ok ? *reinterpret_cast<const uint4*>(a.q_cur + qoff + ks * 16) : make_uint4(0, 0, 0, 0);
-      qc[ks] = __builtin_bit_cast(bf16x8, w);
-      uint4 wp = make_uint4(0, 0, 0, 0);
-      if (!a.dense && row_ok) wp = *reinterpret_cast<const uint4*>(a.q_prev + qoff + ks * 16);
-      qp[ks] = __builtin_bit_cast(bf16x8, wp);
+      uint4 w = row_ok ? *reinterpret_cast<const uint4*>(qsrc + qoff + ks * 16) : make_uint4(0, 0, 0, 0);
+      qf[ks] = __builtin_bit_cast(bf16x8, w);
     }
   }
   float lse2 = 0.0f;
-  if (!a.dense && row_ok) lse2 = a.lse_ref[((int64_t)b * a.N + row_i) * a.H + h] * 1.4426950408889634f;
+  if (!DENSE && !add_pass && row_ok) lse2 = a.lse_ref[((int64_t)b * a.N + row_i) * a.H + h] * 1.4426950408889634f;
 
-  f32x16 acc_add[DB], acc_sub[DB];
-#pragma unroll
-  for (int db = 0; db < DB; ++db) {
-    acc_add[db] = f32x16{};
-    acc_sub[db] = f32x16{};
+  // ---- phase extents (uniform) ----------------------------------------------------------------------
+  const int2* descp = DENSE ? nullptr : a.desc + ((int64_t)b * a.H + h) * a.c_list;
+  const int2* updp = DENSE ? nullptr : a.upd + ((int64_t)b * a.H + h) * a.c_list;
+  if (tid < 2) {
+    int n = 0;
+    if (!DENSE && a.c_list > 0) {
+      // tid 0: list entries with j + window <= max_row; tid 1: the same among the updated entries
+      const int2* lp = tid == 0 ? descp : updp;
+      const int len = tid == 0 ? a.c_list : a.n_upd[(int64_t)b * a.H + h];
+      const int lim = max_row - a.window;
+      int lo = 0, hi = len;
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (lp[mid].x <= lim) lo = mid + 1; else hi = mid;
+      }
+      n = lo;
+    }
+    s_meta[tid] = n;
   }
-  float run_max = -INFINITY, lsum = 0.0f, msub = 0.0f;
-
-  // phase extents
-  const int32_t* colp = a.cols ? a.cols + ((int64_t)b * a.H + h) * a.c_list : nullptr;
-  int n_list = 0;
-  if (!a.dense && colp && a.c_list > 0) {
-    const int lim = max_row - a.window;    // list columns need j + window <= i
-    int lo = 0, hi = a.c_list;             // first index with cols[idx] > lim
+  // band extent of the workgroup's rows
+  const int bandLo = DENSE ? 0 : (a.window > 0 ? max(0, min_row - a.window + 1) : 0);
+  const int bandHi = DENSE ? max_row : (a.window > 0 ? max_row : -1);
+  // phase D: the active rows inside [bandLo, bandHi] are a contiguous range of the sorted row list,
+  // ending with this tile's last row
+  int pa = 0, pb = 0;
+  if (!DENSE && a.window > 0) {
+    int lo = 0, hi = a.k;
     while (lo < hi) {
-      int mid = (lo + hi) >> 1;
-      if (colp[mid] <= lim) lo = mid + 1; else hi = mid;
+      const int mid = (lo + hi) >> 1;
+      if (rowp[mid] < bandLo) lo = mid + 1; else hi = mid;
     }
-    n_list = lo;
+    pa = lo;
+    pb = last_p + 1;
   }
-  int band_lo = 0, band_hi = -1;
-  if (a.dense) {
-    band_lo = 0;
-    band_hi = max_row;
-  } else if (a.window > 0) {
-    band_lo = max(0, min_row - a.window + 1);
-    band_hi = max_row;
-  }
-  const int n_list_tiles = (n_list + kBN - 1) / kBN;
-  const int n_band_tiles = band_hi >= band_lo ? (band_hi - band_lo + 1 + kBN - 1) / kBN : 0;
-  const bool need_old = !a.dense;
+  __syncthreads();
+  const int nA = s_meta[0];
+  const int nC = s_meta[1];
+  const int tA = (nA + kBN - 1) / kBN;
+  const int tB = bandHi >= bandLo ? (bandHi - bandLo + kBN) / kBN : 0;
+  const int tC = (nC + kBN - 1) / kBN;
+  const int tD = (pb - pa + kBN - 1) / kBN;
+  const int n_old = tA + tB;             // tiles staged from the cache state
+  const int n_tiles = n_old + tC + tD;
 
-  for (int tile = 0; tile < n_list_tiles + n_band_tiles; ++tile) {
-    const bool in_list = tile < n_list_tiles;
+  // ---- tile descriptors ----------------------------------------------------------------------------
+  // For tile v every lane c < 32 loads two words per step (always two VMEM ops, out-of-range offsets for
+  // words a phase does not need) six tiles ahead; two steps later they are finalized into the LDS ring
+  // tcid/trow/tupd[v % 8], and three steps after that the tile's LDS-DMA reads its row offsets there.
+  const int c32 = lane & 31;
+  const rsrc_t descR = make_rsrc(DENSE ? (const void*)a.k_cache : (const void*)descp, DENSE ? 0u : (uint32_t)a.c_list * 8u);
+  const rsrc_t updR = make_rsrc(DENSE ? (const void*)a.k_cache : (const void*)updp, DENSE ? 0u : (uint32_t)a.c_list * 8u);
+  const rsrc_t slotR = make_rsrc(DENSE ? (const void*)a.k_cache : (const void*)(a.slot + (int64_t)b * a.N),
+                                 DENSE ? 0u : (uint32_t)a.N * 4u);
+  const rsrc_t rowsR = make_rsrc(DENSE ? (const void*)a.k_cache : (const void*)rowp, DENSE ? 0u : (uint32_t)a.k * 4u);
+  // phase of tile v: 0 = A, 1 = B, 2 = C, 3 = D, 4 = past the end; idx = position within the phase
+  auto tile_phase = [=](int v, int c, int& idx, bool& valid) {
+    int phase;
+    if (v < tA) { phase = 0; idx = v * kBN + c; valid = idx < nA; }
+    else if (v < n_old) { phase = 1; idx = bandLo + (v - tA) * kBN + c; valid = idx <= bandHi; }
+    else if (v < n_old + tC) { phase = 2; idx = (v - n_old) * kBN + c; valid = idx < nC; }
+    else if (v < n_tiles) { phase = 3; idx = pa + (v - n_old - tC) * kBN + c; valid = idx < pb; }
+    else { phase = 4; idx = 0; valid = false; }
+    return phase;
+  };
+  auto load_desc = [=](int v, int& w0, int& w1) {
+    int idx;
+    bool valid;
+    const int phase = tile_phase(v, c32, idx, valid);   // uniform: the branches below are scalar
+    const uint32_t i8 = valid ? (uint32_t)idx * 8u : kOOB;
+    const uint32_t i4 = valid ? (uint32_t)idx * 4u : kOOB;
+    if (phase == 0) {
+      w0 = __builtin_amdgcn_raw_buffer_load_b32(descR, i8, 0, 0);
+      w1 = __builtin_amdgcn_raw_buffer_load_b32(descR, i8 + (valid ? 4u : 0u), 0, 0);
+    } else if (phase == 1) {
+      w0 = __builtin_amdgcn_raw_buffer_load_b32(slotR, kOOB, 0, 0);
+      w1 = __builtin_amdgcn_raw_buffer_load_b32(slotR, DENSE ? kOOB : i4, 0, 0);
+    } else if (phase == 2) {
+      w0 = __builtin_amdgcn_raw_buffer_load_b32(updR, i8, 0, 0);
+      w1 = __builtin_amdgcn_raw_buffer_load_b32(updR, i8 + (valid ? 4u : 0u), 0, 0);
+    } else {
+      w0 = __builtin_amdgcn_raw_buffer_load_b32(rowsR, phase == 3 ? i4 : kOOB, 0, 0);
+      w1 = __builtin_amdgcn_raw_buffer_load_b32(rowsR, kOOB, 0, 0);
+    }
+  };
+  auto store_desc = [=](int v, int w0, int w1) {
+    int idx;
+    bool valid;
+    const int phase = tile_phase(v, c32, idx, valid);
+    int cid = -1, row = -1, upd = 0;
+    if (valid) {
+      if (phase == 0) { cid = w0; row = w0; upd = w1 >= 0; }
+      else if (phase == 1) { cid = idx; row = idx; upd = !DENSE && w1 >= 0; }
+      else if (phase == 2) { cid = w0; row = w1; }
+      else { cid = w0; row = idx; }
+    }
     if (lane < kBN) {
-      int cid;
-      if (in_list) {
-        const int pos = tile * kBN + lane;
-        cid = pos < n_list ? colp[pos] : -1;
-      } else {
-        const int j = band_lo + (tile - n_list_tiles) * kBN + lane;
-        cid = j <= band_hi ? j : -1;
-      }
-      sm.cid[lane] = cid;
-      sm.nslot[lane] = (cid >= 0 && a.slot) ? a.slot[(int64_t)b * a.N + cid] : -1;
+      tcid[v & 7][c32] = cid;
+      trow[v & 7][c32] = row;
+      tupd[v & 7][c32] = upd;
     }
-    __syncthreads();
-    stage_tile<D>(a, sm, b, h, need_old);
-    __syncthreads();
+    const uint64_t any = __builtin_amdgcn_ballot_w64(lane < kBN && upd != 0);
+    if (lane == 0) tany[v & 7] = any != 0;
+  };
 
-    // validity of this lane's 16 (column, row) pairs: column 8j + 4hw + i
-    bool valid[16];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int cid = sm.cid[8 * j + 4 * hw + i];
-        bool v;
-        if (in_list) v = cid >= 0 && cid + a.window <= row_i;
-        else v = cid >= 0 && cid <= row_i && (a.dense || cid > row_i - a.window);
-        valid[4 * j + i] = v;
-      }
-    }
+  // buffer descriptors of the K/V tensors of this batch element
+  const uint32_t rb = (uint32_t)(HD * 2);
+  const uint32_t head_off = (uint32_t)(h * D * 2);
+  const rsrc_t kcR = make_rsrc(a.k_cache + (int64_t)b * a.N * HD, (uint32_t)a.N * rb);
+  const rsrc_t vcR = make_rsrc(a.v_cache + (int64_t)b * a.N * HD, (uint32_t)a.N * rb);
+  const rsrc_t knR = make_rsrc(DENSE ? a.k_cache : a.k_new + (int64_t)b * a.k * HD, DENSE ? 0u : (uint32_t)a.k * rb);
+  const rsrc_t vnR = make_rsrc(DENSE ? a.v_cache : a.v_new + (int64_t)b * a.k * HD, DENSE ? 0u : (uint32_t)a.k * rb);
 
+  // LDS-DMA of tile u into slot sl: each wave issues INST_PER_WAVE K and INST_PER_WAVE V instructions,
+  // always (a tile past the end loads nothing: every offset is out of range)
+  auto issue = [=](int u, Slot<D>& sl) {
+    const bool newer = u >= n_old;        // uniform: one of two scalar branches, same op count
+    const bool live = u < n_tiles;
 #pragma unroll
-    for (int pass = 0; pass < 2; ++pass) {
-      if (pass == 0 && !need_old) continue;
-      const int which = pass;   // 0 = subtract (loop r-1), 1 = add (loop r)
-      f32x16 s = f32x16{};
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const uint4 kw = *reinterpret_cast<const uint4*>(&sm.k[which][r32][ks * 16 + hw * 8]);
-        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kw),
-                                                    which ? qc[ks] : qp[ks], s, 0, 0, 0);
-      }
-      float pr[16];
-      if (which == 0) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          pr[v] = valid[v] ? __builtin_amdgcn_exp2f(s[v] * a.scale_log2 - lse2) : 0.0f;
-          msub += pr[v];
-        }
+    for (int t = 0; t < INST_PER_WAVE; ++t) {
+      const int inst = wave * INST_PER_WAVE + t;
+      const int c = inst * COLS_PER_INST + lane / CH;
+      const int ch = swz(c, lane % CH);
+      const int cid = tcid[u & 7][c], row = trow[u & 7][c];
+      const uint32_t off = (live && cid >= 0) ? (uint32_t)row * rb + head_off + (uint32_t)ch * 16 : kOOB;
+      if (newer) {
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(knR, FL_LDS(sl.k + inst * 512), 16, off, 0, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(vnR, FL_LDS(sl.v + inst * 512), 16, off, 0, 0, 0);
       } else {
-        float tmax = -INFINITY;
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          s[v] = valid[v] ? s[v] * a.scale_log2 : -INFINITY;
-          tmax = fmaxf(tmax, s[v]);
-        }
-        tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-        const float new_max = fmaxf(run_max, tmax);
-        float alpha = 1.0f;
-        if (new_max != -INFINITY) {
-          alpha = __builtin_amdgcn_exp2f(run_max - new_max);
-#pragma unroll
-          for (int v = 0; v < 16; ++v) pr[v] = valid[v] ? __builtin_amdgcn_exp2f(s[v] - new_max) : 0.0f;
-        } else {
-#pragma unroll
-          for (int v = 0; v < 16; ++v) pr[v] = 0.0f;
-        }
-        run_max = new_max;
-        float ts = 0.0f;
-#pragma unroll
-        for (int v = 0; v < 16; ++v) ts += pr[v];
-        lsum = lsum * alpha + ts;
-        if (alpha != 1.0f) {
-#pragma unroll
-          for (int db = 0; db < DB; ++db) acc_add[db] *= alpha;
-        }
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(kcR, FL_LDS(sl.k + inst * 512), 16, off, 0, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(vcR, FL_LDS(sl.v + inst * 512), 16, off, 0, 0, 0);
       }
-      // O^T += V^T P^T over two 16-column k-blocks
+    }
+  };
+
+  f32x16 acc[DB];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        const uint32_t b0 = pack_f16x2(pr[8 * kb + 0], pr[8 * kb + 1]);
-        const uint32_t b1 = pack_f16x2(pr[8 * kb + 2], pr[8 * kb + 3]);
-        const uint32_t b2 = pack_f16x2(pr[8 * kb + 4], pr[8 * kb + 5]);
-        const uint32_t b3 = pack_f16x2(pr[8 * kb + 6], pr[8 * kb + 7]);
-        const f16x8 pf = __builtin_bit_cast(f16x8, make_uint4(b0, b1, b2, b3));
+  for (int db = 0; db < DB; ++db) acc[db] = f32x16{};
+  float run_max = -INFINITY, lsum = 0.0f;   // add pass: running max (log2 units) and row sum
+  float msub = 0.0f;                        // subtract pass: mass of the columns seen
+
+  // wave w converts, in place, the V rows its own LDS-DMA wrote (bf16 -> fp16, exact for |v| in
+  // [2^-14, 65504]); the barrier of the next step publishes them to the other waves
+  auto convert_v = [=](Slot<D>& sl) {
 #pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          const uint2 lo = *reinterpret_cast<const uint2*>(&sm.vt[which][db * 32 + r32][16 * kb + 4 * hw]);
-          const uint2 hi = *reinterpret_cast<const uint2*>(&sm.vt[which][db * 32 + r32][16 * kb + 8 + 4 * hw]);
-          const f16x8 vf = __builtin_bit_cast(f16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
-          if (which) acc_add[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, pf, acc_add[db], 0, 0, 0);
-          else acc_sub[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, pf, acc_sub[db], 0, 0, 0);
+    for (int t = 0; t < INST_PER_WAVE; ++t) {
+      uint16_t* p = sl.v + (wave * INST_PER_WAVE + t) * 512 + lane * 8;
+      const u32x4 w = *reinterpret_cast<const u32x4*>(p);
+      u32x4 h;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        h[e] = pack_f16x2(__uint_as_float(w[e] << 16), __uint_as_float(w[e] & 0xFFFF0000u));
+      *reinterpret_cast<u32x4*>(p) = h;
+    }
+  };
+
+  auto compute = [=, &acc, &run_max, &lsum, &msub](int u, const Slot<D>& sl) {
+    const int ri = u & 7;
+    const bool newer = u >= n_old;
+    const bool is_list = u < tA || (newer && u < n_old + tC);
+    if (newer && !add_pass) return;
+    // does any row of this wave's group see any column of this tile?  (uniform)
+    const int c0 = tcid[ri][0];
+    const int clast = tcid[ri][kBN - 1];
+    const bool drop_upd = !DENSE && add_pass && !newer;
+    bool active, full;
+    if (is_list) {
+      active = group_has_rows && c0 >= 0 && c0 + a.window <= gmax;
+      full = clast >= 0 && clast + a.window <= gmin;
+    } else {
+      const int t_hi = clast >= 0 ? clast : bandHi;
+      const int g_lo = DENSE ? 0 : gmin - a.window + 1;
+      active = group_has_rows && c0 >= 0 && c0 <= gmax && t_hi >= g_lo;
+      full = clast >= 0 && clast <= gmin && (DENSE || c0 > gmax - a.window);
+    }
+    if (!active) return;
+    full = full && !(drop_upd && tany[ri]);   // every (row, column) pair of the tile counts
+    // S^T = K Q^T: lane holds columns 8j + 4hw + i of row r32
+    f32x16 s = f32x16{};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const u32x4 kw = *reinterpret_cast<const u32x4*>(&sl.k[r32 * D + swz(r32, 2 * ks + hw) * 8]);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kw), qf[ks], s, 0, 0, 0);
+    }
+    if (!full) {
+      // column masks, branch-free: list columns need j + window <= i; band columns i - window < j <= i
+      // (any j <= i in the dense loop); the add pass takes updated columns from phases C/D instead
+      const int lim_list = row_i - a.window;
+      const int lim_band = DENSE ? INT_MIN : row_i - a.window;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int4 c4 = *reinterpret_cast<const int4*>(&tcid[ri][8 * j + 4 * hw]);
+        const int4 u4 = *reinterpret_cast<const int4*>(&tupd[ri][8 * j + 4 * hw]);
+        const int cc[4] = {c4.x, c4.y, c4.z, c4.w};
+        const int uu[4] = {u4.x, u4.y, u4.z, u4.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int cid = cc[i];
+          const bool ok_list = (cid >= 0) & (cid <= lim_list);
+          const bool ok_band = (cid >= 0) & (cid <= row_i) & (cid > lim_band);
+          const bool ok = (is_list ? ok_list : ok_band) & !(drop_upd & (uu[i] != 0));
+          s[4 * j + i] = ok ? s[4 * j + i] : -INFINITY;
         }
       }
     }
-    __syncthreads();
+    float pr[16];
+    if (!add_pass) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        pr[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], a.scale_log2, -lse2));   // masked: exp2(-inf) = 0
+        msub += pr[v];
+      }
+    } else {
+      // online softmax with a lazily raised reference: the reference (run_max, log2 units) only moves
+      // when a score exceeds it by more than 8, so probabilities stay <= 256 and the accumulators are
+      // rescaled rarely; the final normaliser uses the same reference
+      float tmax = s[0];
+#pragma unroll
+      for (int v = 1; v < 16; ++v) tmax = fmaxf(tmax, s[v]);
+      tmax = xor32_max(tmax) * a.scale_log2;
+      const bool raise = tmax > run_max + 8.0f;          // false while both are -inf
+      if (__builtin_amdgcn_ballot_w64(raise) != 0) {      // uniform: rescale the rows that need it
+        const float nm = raise ? tmax : run_max;
+        const float alpha = raise ? __builtin_amdgcn_exp2f(run_max - nm) : 1.0f;   // exp2(-inf) = 0
+        lsum *= alpha;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) acc[db] *= alpha;
+        run_max = nm;
+      }
+      const float ref = run_max == -INFINITY ? 0.0f : run_max;
+      float ts = 0.0f;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        pr[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], a.scale_log2, -ref));
+        ts += pr[v];
+      }
+      lsum += ts;
+    }
+    // O^T += V^T P^T over two 16-column k-blocks, fp16 operands
+    const int g16 = lane >> 4, m16 = lane & 15;
+    const int tq = m16 >> 2, q = m16 & 3;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      const u32x4 pw = {pack_f16x2(pr[8 * kb + 0], pr[8 * kb + 1]), pack_f16x2(pr[8 * kb + 2], pr[8 * kb + 3]),
+                        pack_f16x2(pr[8 * kb + 4], pr[8 * kb + 5]), pack_f16x2(pr[8 * kb + 6], pr[8 * kb + 7])};
+      const f16x8 pf = __builtin_bit_cast(f16x8, pw);
+      // lane (16g + 4t + q) points at V[col_t][dim0 + 4q]; the transpose read hands lane m of the group
+      // V[col_t][dim0 + m] for t = 0..3 (columns 16kb + 4(g/2) + t, then the same + 8)
+      const int colA = 16 * kb + 4 * (g16 >> 1) + tq;
+      const int colB = colA + 8;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const int dim = db * 32 + 16 * (g16 & 1) + 4 * q;
+        const i16x4 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            FL_LDS4(&sl.v[colA * D + swz(colA, dim >> 3) * 8 + (dim & 7)]));
+        const i16x4 vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            FL_LDS4(&sl.v[colB * D + swz(colB, dim >> 3) * 8 + (dim & 7)]));
+        const i16x8 v8 = __builtin_shufflevector(va, vb, 0, 1, 2, 3, 4, 5, 6, 7);
+        acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, v8), pf, acc[db], 0, 0, 0);
+      }
+    }
+  };
+
+  // ---- pipeline --------------------------------------------------------------------------------------
+  // step s: wait for tile s+1; finalize the descriptors of tile s+4; barrier (tile s, converted at
+  // step s-1, is now visible); load the descriptors of tile s+6; LDS-DMA tile s+3 into the slot tile
+  // s-1 used; convert the V rows of tile s+1; compute tile s.  Every step issues the same number of
+  // VMEM ops (2 descriptor words + 2 * INST_PER_WAVE DMA), so "tile s+1 has landed" is exactly
+  // vmcnt(OPS_PER_STEP) and the count is the same on every path.
+  constexpr int OPS_PER_STEP = 2 + 2 * INST_PER_WAVE;
+  int dA0, dA1, dB0, dB1;                 // descriptor words in flight (even / odd tiles)
+  {
+    int w0, w1;
+    for (int v = 0; v < 4; ++v) {
+      load_desc(v, w0, w1);
+      FL_WAIT_VM(0);
+      store_desc(v, w0, w1);
+    }
   }
+  FL_WAIT_VM(0);                          // query fragments and the first descriptors have arrived
+  lds_barrier();
+  issue(0, s0);                           // as step -3
+  load_desc(4, dA0, dA1);                 // as step -2
+  issue(1, s1);
+  load_desc(5, dB0, dB1);                 // as step -1
+  issue(2, s2);
+  FL_WAIT_VM(2 * OPS_PER_STEP);           // tile 0 has landed (tiles 1 and 2 may be in flight)
+  convert_v(s0);
+
+  auto step = [&](int u, Slot<D>& cur, Slot<D>& nxt, Slot<D>& following, int& w0, int& w1) {
+    FL_WAIT_VM(OPS_PER_STEP);
+    store_desc(u + 4, w0, w1);
+    lds_barrier();
+    load_desc(u + 6, w0, w1);
+    issue(u + 3, nxt);
+    convert_v(following);
+    if (u < n_tiles) compute(u, cur);
+  };
+  const int n_steps = (n_tiles + kRing - 1) / kRing * kRing;
+  for (int u = 0; u < n_steps; u += kRing) {
+    step(u, s0, s3, s1, dA0, dA1);
+    step(u + 1, s1, s0, s2, dB0, dB1);
+    step(u + 2, s2, s1, s3, dA0, dA1);
+    step(u + 3, s3, s2, s0, dB0, dB1);
+  }
+  FL_WAIT_VM(0);
+  lds_barrier();
 
   // the two half-waves hold disjoint columns of the same row
-  lsum += __shfl_xor(lsum, 32, 64);
-  msub += __shfl_xor(msub, 32, 64);
+  lsum = xor32_add(lsum);
+  msub = xor32_add(msub);
+  // subtract-pass hand-off: group g uses ring slot g (D * 128 bytes >= 32 rows x D floats; ring is idle)
+  float4* xacc = reinterpret_cast<float4*>(group == 0 ? &s0 : &s1);
+  if constexpr (!DENSE) {
+    if (!add_pass) {
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          xacc[(db * 4 + j) * 64 + lane] =
+              make_float4(acc[db][4 * j], acc[db][4 * j + 1], acc[db][4 * j + 2], acc[db][4 * j + 3]);
+      xm[group][lane] = msub;
+    }
+    lds_barrier();
+    if (!add_pass) return;
+    msub = xm[group][lane];
+  }
   if (!row_ok) return;
   const int64_t orow = ((int64_t)b * a.N + row_i) * HD + (int64_t)h * D;
   const int64_t lrow = ((int64_t)b * a.N + row_i) * a.H + h;
-  if (a.dense) {
+  if constexpr (DENSE) {
     if (!(lsum > 0.0f)) return;    // unreachable: column 0 is always causal
     const float inv = 1.0f / lsum;
 #pragma unroll
@@ -296,38 +504,88 @@ __global__ __launch_bounds__(64) void loop_attn_kernel(AttnArgs a) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int dim = db * 32 + 8 * j + 4 * hw;
-        float4 out = make_float4(acc_add[db][4 * j] * inv, acc_add[db][4 * j + 1] * inv,
-                                 acc_add[db][4 * j + 2] * inv, acc_add[db][4 * j + 3] * inv);
+        float4 out = make_float4(acc[db][4 * j] * inv, acc[db][4 * j + 1] * inv,
+                                 acc[db][4 * j + 2] * inv, acc[db][4 * j + 3] * inv);
         *reinterpret_cast<float4*>(a.o + orow + dim) = out;
       }
     if (hw == 0) a.lse_ref[lrow] = (run_max + log2f(lsum)) * 0.6931471805599453f;
-    return;
+  } else {
+    if (!(msub > 0.0f) || !(lsum > 0.0f)) return;     // empty column set or vanished mass: unchanged
+    const float f = msub / lsum;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int dim = db * 32 + 8 * j + 4 * hw;
+        const float4 sub = xacc[(db * 4 + j) * 64 + lane];
+        float4 prev = *reinterpret_cast<const float4*>(a.o + orow + dim);
+        prev.x = prev.x - sub.x + acc[db][4 * j + 0] * f;
+        prev.y = prev.y - sub.y + acc[db][4 * j + 1] * f;
+        prev.z = prev.z - sub.z + acc[db][4 * j + 2] * f;
+        prev.w = prev.w - sub.w + acc[db][4 * j + 3] * f;
+        *reinterpret_cast<float4*>(a.o + orow + dim) = prev;
+      }
+    if (hw == 0) a.lse_ref[lrow] = (run_max + log2f(lsum)) * 0.6931471805599453f - logf(msub);
   }
-  if (!(msub > 0.0f) || !(lsum > 0.0f)) return;     // empty column set or vanished mass: unchanged
-  const float f = msub / lsum;
-#pragma unroll
-  for (int db = 0; db < DB; ++db)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int dim = db * 32 + 8 * j + 4 * hw;
-      float4 prev = *reinterpret_cast<const float4*>(a.o + orow + dim);
-      prev.x = prev.x - acc_sub[db][4 * j + 0] + acc_add[db][4 * j + 0] * f;
-      prev.y = prev.y - acc_sub[db][4 * j + 1] + acc_add[db][4 * j + 1] * f;
-      prev.z = prev.z - acc_sub[db][4 * j + 2] + acc_add[db][4 * j + 2] * f;
-      prev.w = prev.w - acc_sub[db][4 * j + 3] + acc_add[db][4 * j + 3] * f;
-      *reinterpret_cast<float4*>(a.o + orow + dim) = prev;
+}
+
+// Per (batch, head): (column, slot) of every list entry, and the entries updated this loop compacted in
+// ascending order, with their count.
+__global__ __launch_bounds__(256) void attn_prep_kernel(const int32_t* __restrict__ cols,
+                                                        const int32_t* __restrict__ slot, int c_list,
+                                                        int N, int H, int2* __restrict__ desc,
+                                                        int2* __restrict__ upd, int32_t* __restrict__ n_upd) {
+  __shared__ int wsum[4];
+  const int bh = blockIdx.x, b = bh / H;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int32_t* cp = cols + (int64_t)bh * c_list;
+  int2* dp = desc + (int64_t)bh * c_list;
+  int2* up = upd + (int64_t)bh * c_list;
+  int base = 0;
+  for (int p0 = 0; p0 < c_list; p0 += 256) {
+    const int pos = p0 + tid;
+    int cid = -1, s = -1;
+    if (pos < c_list) {
+      cid = cp[pos];
+      s = slot[(int64_t)b * N + cid];
+      dp[pos] = make_int2(cid, s);
     }
-  if (hw == 0) a.lse_ref[lrow] = (run_max + log2f(lsum)) * 0.6931471805599453f - logf(msub);
+    const int flag = (pos < c_list && s >= 0) ? 1 : 0;
+    int incl = flag;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int t = __shfl_up(incl, off, 64);
+      if (lane >= off) incl += t;
+    }
+    __syncthreads();
+    if (lane == 63) wsum[wave] = incl;
+    __syncthreads();
+    int before = 0, total = 0;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      before += (w < wave) ? wsum[w] : 0;
+      total += wsum[w];
+    }
+    if (flag) up[base + before + incl - 1] = make_int2(cid, s);
+    base += total;
+  }
+  if (tid == 0) n_upd[bh] = base;
 }
 
 }  // namespace fl
 
 using namespace fl;
 
+static size_t attn_ws_bytes(int B, int H, int c_list, bool dense) {
+  if (dense || B < 1 || H < 1 || c_list < 0) return 0;
+  const size_t n = (size_t)B * (size_t)H;
+  return n * (size_t)c_list * sizeof(int2) * 2 + n * sizeof(int32_t);
+}
+
 extern "C" size_t fl_loop_sparse_attn_ws(int B, int N, int H, int d, int k, int c_list, int window,
                                          int flags) {
-  (void)B; (void)N; (void)H; (void)d; (void)k; (void)c_list; (void)window; (void)flags;
-  return 0;
+  (void)N; (void)d; (void)k; (void)window;
+  return attn_ws_bytes(B, H, c_list, (flags & FL_ATTN_DENSE) != 0);
 }
 
 extern "C" int fl_loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev,
@@ -338,17 +596,15 @@ extern "C" int fl_loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev
                                    int d, float sm_scale, int flags, float* lse_ref, float* o,
                                    void* ws, size_t ws_bytes, void* stream) {
   FL_API_BEGIN
-  (void)ws;
   const bool dense = (flags & FL_ATTN_DENSE) != 0;
   FL_REQUIRE((flags & ~FL_ATTN_DENSE) == 0, FL_E_UNSUPPORTED, "fl_loop_sparse_attn: unknown flags 0x%x", flags);
   FL_REQUIRE(q_cur && k_cache && v_cache && lse_ref && o, FL_E_NULL,
              "fl_loop_sparse_attn: q_cur, k_cache, v_cache, lse_ref and o are required");
   FL_REQUIRE(B >= 1 && N >= 1 && H >= 1, FL_E_SHAPE, "fl_loop_sparse_attn: need B, N, H >= 1");
   FL_REQUIRE(d == 64 || d == 128, FL_E_SHAPE, "fl_loop_sparse_attn: head dim %d not in {64, 128}", d);
-  FL_REQUIRE((int64_t)N * H * d < ((int64_t)1 << 31), FL_E_SHAPE, "fl_loop_sparse_attn: N * H * d too large");
+  FL_REQUIRE((int64_t)N * H * d <= ((int64_t)1 << 30), FL_E_SHAPE,
+             "fl_loop_sparse_attn: N * H * d above 2^30 (byte offsets must stay below 2^31)");
   FL_REQUIRE(sm_scale > 0.0f && std::isfinite(sm_scale), FL_E_RANGE, "fl_loop_sparse_attn: sm_scale must be > 0");
-  FL_REQUIRE(ws_bytes >= fl_loop_sparse_attn_ws(B, N, H, d, k, c_list, window, flags), FL_E_WORKSPACE,
-             "fl_loop_sparse_attn: workspace too small");
   if (dense) {
     FL_REQUIRE(rows == nullptr && k == N, FL_E_SHAPE, "fl_loop_sparse_attn: DENSE needs rows == NULL and k == N");
   } else {
@@ -359,15 +615,54 @@ extern "C" int fl_loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev
     FL_REQUIRE(c_list == 0 || cols, FL_E_NULL, "fl_loop_sparse_attn: cols is required when c_list > 0");
     FL_REQUIRE(window >= 0, FL_E_RANGE, "fl_loop_sparse_attn: window must be >= 0");
   }
+  const size_t need = attn_ws_bytes(B, H, c_list, dense);
+  FL_REQUIRE(need == 0 || (ws && ws_bytes >= need), FL_E_WORKSPACE,
+             "fl_loop_sparse_attn: workspace of %zu bytes required", need);
   if (k == 0) return FL_OK;
-  AttnArgs a{q_cur, q_prev, k_cache, v_cache, k_new, v_new, slot, dense ? nullptr : rows,
-             dense ? nullptr : cols, lse_ref, o, k, dense ? 0 : c_list, dense ? 0 : window, N, H,
-             sm_scale * 1.4426950408889634f, dense ? 1 : 0};
-  if (dense) { a.slot = nullptr; a.q_prev = nullptr; a.k_new = nullptr; a.v_new = nullptr; }
-  dim3 grid((k + kBM - 1) / kBM, H, B);
   hipStream_t st = as_stream(stream);
-  if (d == 128) loop_attn_kernel<128><<<grid, 64, 0, st>>>(a);
-  else loop_attn_kernel<64><<<grid, 64, 0, st>>>(a);
+  AttnArgs a{};
+  a.q_cur = q_cur;
+  a.q_prev = dense ? nullptr : q_prev;
+  a.k_cache = k_cache;
+  a.v_cache = v_cache;
+  a.k_new = dense ? nullptr : k_new;
+  a.v_new = dense ? nullptr : v_new;
+  a.slot = dense ? nullptr : slot;
+  a.rows = dense ? nullptr : rows;
+  a.cols = dense ? nullptr : cols;
+  a.lse_ref = lse_ref;
+  a.o = o;
+  a.k = k;
+  a.c_list = dense ? 0 : c_list;
+  a.window = dense ? 0 : window;
+  a.B = B;
+  a.N = N;
+  a.H = H;
+  a.scale_log2 = sm_scale * 1.4426950408889634f;
+  if (!dense) {
+    char* w = static_cast<char*>(ws);
+    const size_t n = (size_t)B * H * (size_t)c_list;
+    int2* desc = reinterpret_cast<int2*>(w);
+    int2* upd = reinterpret_cast<int2*>(w + n * sizeof(int2));
+    int32_t* n_upd = reinterpret_cast<int32_t*>(w + 2 * n * sizeof(int2));
+    a.desc = desc;
+    a.upd = upd;
+    a.n_upd = n_upd;
+    if (c_list > 0) {
+      attn_prep_kernel<<<B * H, 256, 0, st>>>(cols, slot, c_list, N, H, desc, upd, n_upd);
+      int rc = check_launch("attn_prep_kernel");
+      if (rc != FL_OK) return rc;
+    }
+  }
+  const int bm = dense ? 128 : 64;          // rows per workgroup
+  dim3 grid(((k + bm - 1) / bm) * B * H);
+  if (d == 128) {
+    if (dense) loop_attn_kernel<128, true><<<grid, 256, 0, st>>>(a);
+    else loop_attn_kernel<128, false><<<grid, 256, 0, st>>>(a);
+  } else {
+    if (dense) loop_attn_kernel<64, true><<<grid, 256, 0, st>>>(a);
+    else loop_attn_kernel<64, false><<<grid, 256, 0, st>>>(a);
+  }
   return check_launch("loop_attn_kernel");
   FL_API_END
 }
