@@ -228,7 +228,7 @@ def copy_calib():
     dst = torch.empty_like(src)
     torch.cuda.synchronize()
     for _ in range(5):
-        dst.copy_(src)
+        torch.mul(src, 1.0, out=dst)      # one elementwise kernel: reads and writes nbytes each
     torch.cuda.synchronize()
     print(json.dumps({"copy_bytes_read": nbytes, "copy_bytes_written": nbytes, "dispatches": 5}), flush=True)
 

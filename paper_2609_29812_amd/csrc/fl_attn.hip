@@ -45,9 +45,10 @@ struct AttnArgs {
   const int32_t* slot;
   const int32_t* rows;
   const int32_t* cols;
-  const int2* desc;          // [B, H, c_list] (column, slot) of the list (prep kernel)
-  const int2* upd;           // [B, H, c_list] compacted updated list columns (prep kernel)
-  const int32_t* n_upd;      // [B, H]
+  const int2* rec;           // tile records written by the prep kernel (see attn_prep_kernel)
+  const int32_t* n_upd;      // [B, H] updated list entries per (batch, head)
+  int off_upd, off_band, off_rows, off_sent;   // record offsets of the regions and the sentinel
+  uint32_t rec_bytes;        // bytes of the record array, sentinel included
   float* lse_ref;
   float* o;
   int k, c_list, window, B, N, H;
@@ -60,7 +61,9 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef short i16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 constexpr uint32_t kOOB = 0x80000000u;   // beyond every descriptor's range (ranges stay <= 2^31)
+constexpr int kPad = INT_MAX;            // column id of a padding entry: fails every visibility test
 #define FL_LDS(p) ((__attribute__((address_space(3))) void*)(p))
 #define FL_LDS4(p) ((__attribute__((address_space(3))) i16x4*)(p))
 
@@ -111,9 +114,10 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
   constexpr int INST_PER_TILE = kBN / COLS_PER_INST;
   constexpr int INST_PER_WAVE = INST_PER_TILE / 4;   // per tensor (K and V each)
   __shared__ Slot<D> s0, s1, s2, s3;
-  __shared__ int tcid[8][kBN];            // column ids of tile v in entry v % 8 (-1 = padding)
-  __shared__ int trow[8][kBN];            // the row each column is loaded from (cache or new rows)
-  __shared__ int tupd[8][kBN];            // 1 when that column was updated this loop (phases A/B)
+  // column ids of tile v in entry v % 8 (kPad = padding): view 0 for the subtract pass and the dense
+  // loop, view 1 for the add pass, where the columns updated this loop are padding in phases A/B
+  __shared__ int tcv[2][8][kBN];
+  __shared__ uint32_t toff[8][kBN];       // byte offset of each column's row in its source (kOOB: none)
   __shared__ int tany[8];                 // some column of tile v was updated (phases A/B)
   __shared__ float xm[2][64];
   __shared__ int s_meta[2];
@@ -168,8 +172,12 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
   if (!DENSE && !add_pass && row_ok) lse2 = a.lse_ref[((int64_t)b * a.N + row_i) * a.H + h] * 1.4426950408889634f;
 
   // ---- phase extents (uniform) ----------------------------------------------------------------------
-  const int2* descp = DENSE ? nullptr : a.desc + ((int64_t)b * a.H + h) * a.c_list;
-  const int2* updp = DENSE ? nullptr : a.upd + ((int64_t)b * a.H + h) * a.c_list;
+  const int recA = bh * a.c_list;                  // record offsets of the four phases
+  const int recC = a.off_upd + bh * a.c_list;
+  const int recB = a.off_band + b * a.N;
+  const int recD = a.off_rows + b * a.k;
+  const int2* descp = DENSE ? nullptr : a.rec + recA;
+  const int2* updp = DENSE ? nullptr : a.rec + recC;
   if (tid < 2) {
     int n = 0;
     if (!DENSE && a.c_list > 0) {
@@ -212,65 +220,24 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
   const int n_tiles = n_old + tC + tD;
 
   // ---- tile descriptors ----------------------------------------------------------------------------
-  // For tile v every lane c < 32 loads two words per step (always two VMEM ops, out-of-range offsets for
-  // words a phase does not need) six tiles ahead; two steps later they are finalized into the LDS ring
-  // tcid/trow/tupd[v % 8], and three steps after that the tile's LDS-DMA reads its row offsets there.
+  // Every tile is described by 32 records (column, aux): list entries (column, slot), band columns
+  // (j, slot[j]), updated list entries (column, slot) and updated band rows (rows[p], p), all in one
+  // array so that one 8-byte load per lane fetches them for any phase; entries past a phase's end read
+  // a sentinel (kPad, -1).  Records are loaded six tiles ahead and two steps later turned into the LDS
+  // tables of entry v % 8: column ids for the masks and the byte offset of the row the DMA reads.
   const int c32 = lane & 31;
-  const rsrc_t descR = make_rsrc(DENSE ? (const void*)a.k_cache : (const void*)descp, DENSE ? 0u : (uint32_t)a.c_list * 8u);
-  const rsrc_t updR = make_rsrc(DENSE ? (const void*)a.k_cache : (const void*)updp, DENSE ? 0u : (uint32_t)a.c_list * 8u);
-  const rsrc_t slotR = make_rsrc(DENSE ? (const void*)a.k_cache : (const void*)(a.slot + (int64_t)b * a.N),
-                                 DENSE ? 0u : (uint32_t)a.N * 4u);
-  const rsrc_t rowsR = make_rsrc(DENSE ? (const void*)a.k_cache : (const void*)rowp, DENSE ? 0u : (uint32_t)a.k * 4u);
-  // phase of tile v: 0 = A, 1 = B, 2 = C, 3 = D, 4 = past the end; idx = position within the phase
-  auto tile_phase = [=](int v, int c, int& idx, bool& valid) {
-    int phase;
-    if (v < tA) { phase = 0; idx = v * kBN + c; valid = idx < nA; }
-    else if (v < n_old) { phase = 1; idx = bandLo + (v - tA) * kBN + c; valid = idx <= bandHi; }
-    else if (v < n_old + tC) { phase = 2; idx = (v - n_old) * kBN + c; valid = idx < nC; }
-    else if (v < n_tiles) { phase = 3; idx = pa + (v - n_old - tC) * kBN + c; valid = idx < pb; }
-    else { phase = 4; idx = 0; valid = false; }
-    return phase;
+  const rsrc_t recR = make_rsrc(DENSE ? (const void*)a.k_cache : (const void*)a.rec, DENSE ? 0u : a.rec_bytes);
+  const uint32_t sentinel = (uint32_t)a.off_sent * 8u;
+  auto load_desc = [=](int v) -> u32x2 {
+    if constexpr (DENSE) return u32x2{0u, 0u};
+    const bool inA = v < tA, inB = v < n_old, inC = v < n_old + tC;   // uniform
+    const int start = inA ? 0 : inB ? tA : inC ? n_old : n_old + tC;
+    const int base = inA ? recA : inB ? recB + bandLo : inC ? recC : recD + pa;
+    const int cnt = inA ? nA : inB ? bandHi - bandLo + 1 : inC ? nC : pb - pa;
+    const int i = (v - start) * kBN + c32;
+    const uint32_t off = lane >= kBN ? kOOB : i < cnt ? (uint32_t)(base + i) * 8u : sentinel;
+    return __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(recR, off, 0, 0));
   };
-  auto load_desc = [=](int v, int& w0, int& w1) {
-    int idx;
-    bool valid;
-    const int phase = tile_phase(v, c32, idx, valid);   // uniform: the branches below are scalar
-    const uint32_t i8 = valid ? (uint32_t)idx * 8u : kOOB;
-    const uint32_t i4 = valid ? (uint32_t)idx * 4u : kOOB;
-    if (phase == 0) {
-      w0 = __builtin_amdgcn_raw_buffer_load_b32(descR, i8, 0, 0);
-      w1 = __builtin_amdgcn_raw_buffer_load_b32(descR, i8 + (valid ? 4u : 0u), 0, 0);
-    } else if (phase == 1) {
-      w0 = __builtin_amdgcn_raw_buffer_load_b32(slotR, kOOB, 0, 0);
-      w1 = __builtin_amdgcn_raw_buffer_load_b32(slotR, DENSE ? kOOB : i4, 0, 0);
-    } else if (phase == 2) {
-      w0 = __builtin_amdgcn_raw_buffer_load_b32(updR, i8, 0, 0);
-      w1 = __builtin_amdgcn_raw_buffer_load_b32(updR, i8 + (valid ? 4u : 0u), 0, 0);
-    } else {
-      w0 = __builtin_amdgcn_raw_buffer_load_b32(rowsR, phase == 3 ? i4 : kOOB, 0, 0);
-      w1 = __builtin_amdgcn_raw_buffer_load_b32(rowsR, kOOB, 0, 0);
-    }
-  };
-  auto store_desc = [=](int v, int w0, int w1) {
-    int idx;
-    bool valid;
-    const int phase = tile_phase(v, c32, idx, valid);
-    int cid = -1, row = -1, upd = 0;
-    if (valid) {
-      if (phase == 0) { cid = w0; row = w0; upd = w1 >= 0; }
-      else if (phase == 1) { cid = idx; row = idx; upd = !DENSE && w1 >= 0; }
-      else if (phase == 2) { cid = w0; row = w1; }
-      else { cid = w0; row = idx; }
-    }
-    if (lane < kBN) {
-      tcid[v & 7][c32] = cid;
-      trow[v & 7][c32] = row;
-      tupd[v & 7][c32] = upd;
-    }
-    const uint64_t any = __builtin_amdgcn_ballot_w64(lane < kBN && upd != 0);
-    if (lane == 0) tany[v & 7] = any != 0;
-  };
-
   // buffer descriptors of the K/V tensors of this batch element
   const uint32_t rb = (uint32_t)(HD * 2);
   const uint32_t head_off = (uint32_t)(h * D * 2);
@@ -279,18 +246,41 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
   const rsrc_t knR = make_rsrc(DENSE ? a.k_cache : a.k_new + (int64_t)b * a.k * HD, DENSE ? 0u : (uint32_t)a.k * rb);
   const rsrc_t vnR = make_rsrc(DENSE ? a.v_cache : a.v_new + (int64_t)b * a.k * HD, DENSE ? 0u : (uint32_t)a.k * rb);
 
+  auto store_desc = [=](int v, u32x2 w) {
+    int cid, row;
+    bool upd;
+    if constexpr (DENSE) {
+      cid = v * kBN + c32;                 // the band from column 0
+      if (cid > bandHi) cid = kPad;
+      row = cid;
+      upd = false;
+    } else {
+      const bool newer = v >= n_old;
+      cid = (int)w[0];
+      const int aux = (int)w[1];
+      upd = !newer && aux >= 0;            // updated this loop but staged from the cache
+      row = newer ? aux : cid;
+    }
+    const bool valid = cid != kPad;
+    if (lane < kBN) {
+      tcv[0][v & 7][c32] = cid;
+      tcv[1][v & 7][c32] = upd ? kPad : cid;
+      toff[v & 7][c32] = valid ? (uint32_t)row * rb + head_off : kOOB;
+    }
+    const uint64_t any = __builtin_amdgcn_ballot_w64(lane < kBN && valid && upd);
+    if (lane == 0) tany[v & 7] = any != 0;
+  };
+
   // LDS-DMA of tile u into slot sl: each wave issues INST_PER_WAVE K and INST_PER_WAVE V instructions,
-  // always (a tile past the end loads nothing: every offset is out of range)
+  // always (padding and tiles past the end load nothing: their offsets are out of range)
   auto issue = [=](int u, Slot<D>& sl) {
     const bool newer = u >= n_old;        // uniform: one of two scalar branches, same op count
-    const bool live = u < n_tiles;
 #pragma unroll
     for (int t = 0; t < INST_PER_WAVE; ++t) {
       const int inst = wave * INST_PER_WAVE + t;
       const int c = inst * COLS_PER_INST + lane / CH;
       const int ch = swz(c, lane % CH);
-      const int cid = tcid[u & 7][c], row = trow[u & 7][c];
-      const uint32_t off = (live && cid >= 0) ? (uint32_t)row * rb + head_off + (uint32_t)ch * 16 : kOOB;
+      const uint32_t off = toff[u & 7][c] + (uint32_t)ch * 16;   // kOOB + 240 is still out of range
       if (newer) {
         __builtin_amdgcn_raw_ptr_buffer_load_lds(knR, FL_LDS(sl.k + inst * 512), 16, off, 0, 0, 0);
         __builtin_amdgcn_raw_ptr_buffer_load_lds(vnR, FL_LDS(sl.v + inst * 512), 16, off, 0, 0, 0);
@@ -308,7 +298,7 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
   float msub = 0.0f;                        // subtract pass: mass of the columns seen
 
   // wave w converts, in place, the V rows its own LDS-DMA wrote (bf16 -> fp16, exact for |v| in
-  // [2^-14, 65504]); the barrier of the next step publishes them to the other waves
+  // [2^-14, 65504]); the barrier that follows publishes them to the other waves
   auto convert_v = [=](Slot<D>& sl) {
 #pragma unroll
     for (int t = 0; t < INST_PER_WAVE; ++t) {
@@ -327,22 +317,21 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
     const bool newer = u >= n_old;
     const bool is_list = u < tA || (newer && u < n_old + tC);
     if (newer && !add_pass) return;
-    // does any row of this wave's group see any column of this tile?  (uniform)
-    const int c0 = tcid[ri][0];
-    const int clast = tcid[ri][kBN - 1];
-    const bool drop_upd = !DENSE && add_pass && !newer;
+    // does any row of this wave's group see any column of this tile, and do all rows see all of it?
+    // (uniform; column ids ascend within a tile and padding, kPad, sits at the end)
+    const int c0 = tcv[0][ri][0];
+    const int clast = tcv[0][ri][kBN - 1];
     bool active, full;
     if (is_list) {
-      active = group_has_rows && c0 >= 0 && c0 + a.window <= gmax;
-      full = clast >= 0 && clast + a.window <= gmin;
+      active = group_has_rows && c0 <= gmax - a.window;
+      full = clast <= gmin - a.window;
     } else {
-      const int t_hi = clast >= 0 ? clast : bandHi;
-      const int g_lo = DENSE ? 0 : gmin - a.window + 1;
-      active = group_has_rows && c0 >= 0 && c0 <= gmax && t_hi >= g_lo;
-      full = clast >= 0 && clast <= gmin && (DENSE || c0 > gmax - a.window);
+      const int t_hi = clast != kPad ? clast : bandHi;
+      active = group_has_rows && c0 <= gmax && (DENSE || t_hi > gmin - a.window);
+      full = clast <= gmin && (DENSE || c0 > gmax - a.window);
     }
     if (!active) return;
-    full = full && !(drop_upd && tany[ri]);   // every (row, column) pair of the tile counts
+    if (!DENSE && add_pass && !newer && tany[ri]) full = false;   // updated columns drop out
     // S^T = K Q^T: lane holds columns 8j + 4hw + i of row r32
     f32x16 s = f32x16{};
 #pragma unroll
@@ -351,24 +340,26 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
       s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kw), qf[ks], s, 0, 0, 0);
     }
     if (!full) {
-      // column masks, branch-free: list columns need j + window <= i; band columns i - window < j <= i
-      // (any j <= i in the dense loop); the add pass takes updated columns from phases C/D instead
-      const int lim_list = row_i - a.window;
-      const int lim_band = DENSE ? INT_MIN : row_i - a.window;
+      // column masks: list columns need j + window <= i, band columns i - window < j <= i (any j <= i in
+      // the dense loop); padding and, for the add pass, the columns updated this loop carry kPad
+      const int view = (!DENSE && add_pass) ? 1 : 0;
+      int cc[16];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int4 c4 = *reinterpret_cast<const int4*>(&tcid[ri][8 * j + 4 * hw]);
-        const int4 u4 = *reinterpret_cast<const int4*>(&tupd[ri][8 * j + 4 * hw]);
-        const int cc[4] = {c4.x, c4.y, c4.z, c4.w};
-        const int uu[4] = {u4.x, u4.y, u4.z, u4.w};
+        const int4 c4 = *reinterpret_cast<const int4*>(&tcv[view][ri][8 * j + 4 * hw]);
+        cc[4 * j] = c4.x; cc[4 * j + 1] = c4.y; cc[4 * j + 2] = c4.z; cc[4 * j + 3] = c4.w;
+      }
+      if (is_list) {
+        const int lim = row_i - a.window;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int cid = cc[i];
-          const bool ok_list = (cid >= 0) & (cid <= lim_list);
-          const bool ok_band = (cid >= 0) & (cid <= row_i) & (cid > lim_band);
-          const bool ok = (is_list ? ok_list : ok_band) & !(drop_upd & (uu[i] != 0));
-          s[4 * j + i] = ok ? s[4 * j + i] : -INFINITY;
-        }
+        for (int v = 0; v < 16; ++v) s[v] = cc[v] <= lim ? s[v] : -INFINITY;
+      } else if (DENSE) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) s[v] = cc[v] <= row_i ? s[v] : -INFINITY;
+      } else {
+        const uint32_t w = (uint32_t)a.window;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) s[v] = (uint32_t)row_i - (uint32_t)cc[v] < w ? s[v] : -INFINITY;
       }
     }
     float pr[16];
@@ -430,46 +421,42 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
   };
 
   // ---- pipeline --------------------------------------------------------------------------------------
-  // step s: wait for tile s+1; finalize the descriptors of tile s+4; barrier (tile s, converted at
-  // step s-1, is now visible); load the descriptors of tile s+6; LDS-DMA tile s+3 into the slot tile
-  // s-1 used; convert the V rows of tile s+1; compute tile s.  Every step issues the same number of
-  // VMEM ops (2 descriptor words + 2 * INST_PER_WAVE DMA), so "tile s+1 has landed" is exactly
-  // vmcnt(OPS_PER_STEP) and the count is the same on every path.
-  constexpr int OPS_PER_STEP = 2 + 2 * INST_PER_WAVE;
-  int dA0, dA1, dB0, dB1;                 // descriptor words in flight (even / odd tiles)
-  {
-    int w0, w1;
-    for (int v = 0; v < 4; ++v) {
-      load_desc(v, w0, w1);
-      FL_WAIT_VM(0);
-      store_desc(v, w0, w1);
-    }
-  }
-  FL_WAIT_VM(0);                          // query fragments and the first descriptors have arrived
+  // step s: wait for tile s; convert this wave's V rows of it; finalize the records of tile s+4;
+  // barrier; load the records of tile s+6; LDS-DMA tile s+3 into the slot tile s-1 used; compute tile
+  // s.  Every step issues the same number of VMEM ops (one record load in the sparse update and
+  // 2 * INST_PER_WAVE DMA), so "tile s has landed" is exactly vmcnt(2 * OPS_PER_STEP) on every path.
+  constexpr int OPS_PER_STEP = (DENSE ? 0 : 1) + 2 * INST_PER_WAVE;
+  u32x2 dA, dB;                           // records in flight (even / odd tiles)
+#pragma unroll
+  for (int v = 0; v < 4; ++v) store_desc(v, load_desc(v));
+  FL_WAIT_VM(0);                          // query fragments have arrived
   lds_barrier();
+  // the scheduling barriers keep this order, which the wait counts of the first steps assume
   issue(0, s0);                           // as step -3
-  load_desc(4, dA0, dA1);                 // as step -2
+  __builtin_amdgcn_sched_barrier(0);
+  dA = load_desc(4);                      // as step -2
+  __builtin_amdgcn_sched_barrier(0);
   issue(1, s1);
-  load_desc(5, dB0, dB1);                 // as step -1
+  __builtin_amdgcn_sched_barrier(0);
+  dB = load_desc(5);                      // as step -1
+  __builtin_amdgcn_sched_barrier(0);
   issue(2, s2);
-  FL_WAIT_VM(2 * OPS_PER_STEP);           // tile 0 has landed (tiles 1 and 2 may be in flight)
-  convert_v(s0);
 
-  auto step = [&](int u, Slot<D>& cur, Slot<D>& nxt, Slot<D>& following, int& w0, int& w1) {
-    FL_WAIT_VM(OPS_PER_STEP);
-    store_desc(u + 4, w0, w1);
+  auto step = [&](int u, Slot<D>& cur, Slot<D>& nxt, u32x2& w) {
+    FL_WAIT_VM(2 * OPS_PER_STEP);
+    convert_v(cur);
+    store_desc(u + 4, w);
     lds_barrier();
-    load_desc(u + 6, w0, w1);
+    w = load_desc(u + 6);
     issue(u + 3, nxt);
-    convert_v(following);
     if (u < n_tiles) compute(u, cur);
   };
   const int n_steps = (n_tiles + kRing - 1) / kRing * kRing;
   for (int u = 0; u < n_steps; u += kRing) {
-    step(u, s0, s3, s1, dA0, dA1);
-    step(u + 1, s1, s0, s2, dB0, dB1);
-    step(u + 2, s2, s1, s3, dA0, dA1);
-    step(u + 3, s3, s2, s0, dB0, dB1);
+    step(u, s0, s3, dA);
+    step(u + 1, s1, s0, dB);
+    step(u + 2, s2, s1, dA);
+    step(u + 3, s3, s2, dB);
   }
   FL_WAIT_VM(0);
   lds_barrier();
@@ -529,18 +516,35 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
   }
 }
 
-// Per (batch, head): (column, slot) of every list entry, and the entries updated this loop compacted in
-// ascending order, with their count.
+// Tile records of the sparse update, each an int2 (column, aux):
+//   [0, BH*c)                         list of (b, h): (column, slot of the column)
+//   [off_upd + bh*c, ...)             its entries updated this loop, compacted in order: (column, slot)
+//   [off_band + b*N, ... + N)         every column j of batch b: (j, slot[j])
+//   [off_rows + b*k, ... + k)         the updated rows of batch b: (rows[p], p)
+//   off_sent                          sentinel (kPad, -1)
+// followed by n_upd[B*H].  Blocks [0, B*H) build the lists, the remaining ones the per-batch regions.
 __global__ __launch_bounds__(256) void attn_prep_kernel(const int32_t* __restrict__ cols,
-                                                        const int32_t* __restrict__ slot, int c_list,
-                                                        int N, int H, int2* __restrict__ desc,
-                                                        int2* __restrict__ upd, int32_t* __restrict__ n_upd) {
+                                                        const int32_t* __restrict__ slot,
+                                                        const int32_t* __restrict__ rows, int c_list,
+                                                        int N, int H, int B, int k, int per_batch,
+                                                        int off_upd, int off_band, int off_rows, int off_sent,
+                                                        int2* __restrict__ rec, int32_t* __restrict__ n_upd) {
   __shared__ int wsum[4];
-  const int bh = blockIdx.x, b = bh / H;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if ((int)blockIdx.x >= B * H) {
+    const int e = blockIdx.x - B * H;
+    const int b = e / per_batch, part = e % per_batch;
+    for (int j = part * 256 + tid; j < N; j += per_batch * 256)
+      rec[off_band + (int64_t)b * N + j] = make_int2(j, slot[(int64_t)b * N + j]);
+    for (int p = part * 256 + tid; p < k; p += per_batch * 256)
+      rec[off_rows + (int64_t)b * k + p] = make_int2(rows[(int64_t)b * k + p], p);
+    if (e == 0 && tid == 0) rec[off_sent] = make_int2(kPad, -1);
+    return;
+  }
+  const int bh = blockIdx.x, b = bh / H;
   const int32_t* cp = cols + (int64_t)bh * c_list;
-  int2* dp = desc + (int64_t)bh * c_list;
-  int2* up = upd + (int64_t)bh * c_list;
+  int2* dp = rec + (int64_t)bh * c_list;
+  int2* up = rec + off_upd + (int64_t)bh * c_list;
   int base = 0;
   for (int p0 = 0; p0 < c_list; p0 += 256) {
     const int pos = p0 + tid;
@@ -576,16 +580,31 @@ __global__ __launch_bounds__(256) void attn_prep_kernel(const int32_t* __restric
 
 using namespace fl;
 
-static size_t attn_ws_bytes(int B, int H, int c_list, bool dense) {
-  if (dense || B < 1 || H < 1 || c_list < 0) return 0;
-  const size_t n = (size_t)B * (size_t)H;
-  return n * (size_t)c_list * sizeof(int2) * 2 + n * sizeof(int32_t);
+// record counts of the workspace regions (see attn_prep_kernel)
+struct RecLayout {
+  size_t off_upd, off_band, off_rows, off_sent, n_rec;
+};
+static RecLayout rec_layout(int B, int N, int H, int k, int c_list) {
+  RecLayout L;
+  const size_t list = (size_t)B * H * (size_t)c_list;
+  L.off_upd = list;
+  L.off_band = 2 * list;
+  L.off_rows = L.off_band + (size_t)B * N;
+  L.off_sent = L.off_rows + (size_t)B * k;
+  L.n_rec = L.off_sent + 1;
+  return L;
+}
+
+static size_t attn_ws_bytes(int B, int N, int H, int k, int c_list, bool dense) {
+  if (dense || B < 1 || N < 1 || H < 1 || k < 0 || c_list < 0) return 0;
+  const RecLayout L = rec_layout(B, N, H, k, c_list);
+  return L.n_rec * sizeof(int2) + (size_t)B * H * sizeof(int32_t);
 }
 
 extern "C" size_t fl_loop_sparse_attn_ws(int B, int N, int H, int d, int k, int c_list, int window,
                                          int flags) {
-  (void)N; (void)d; (void)k; (void)window;
-  return attn_ws_bytes(B, H, c_list, (flags & FL_ATTN_DENSE) != 0);
+  (void)d; (void)window;
+  return attn_ws_bytes(B, N, H, k, c_list, (flags & FL_ATTN_DENSE) != 0);
 }
 
 extern "C" int fl_loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev,
@@ -615,7 +634,9 @@ extern "C" int fl_loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev
     FL_REQUIRE(c_list == 0 || cols, FL_E_NULL, "fl_loop_sparse_attn: cols is required when c_list > 0");
     FL_REQUIRE(window >= 0, FL_E_RANGE, "fl_loop_sparse_attn: window must be >= 0");
   }
-  const size_t need = attn_ws_bytes(B, H, c_list, dense);
+  const size_t need = attn_ws_bytes(B, N, H, k, c_list, dense);
+  FL_REQUIRE(dense || rec_layout(B, N, H, k, c_list).n_rec * sizeof(int2) <= ((size_t)1 << 31) - 8, FL_E_SHAPE,
+             "fl_loop_sparse_attn: tile records above 2^31 bytes (reduce B * H * c_list + B * (N + k))");
   FL_REQUIRE(need == 0 || (ws && ws_bytes >= need), FL_E_WORKSPACE,
              "fl_loop_sparse_attn: workspace of %zu bytes required", need);
   if (k == 0) return FL_OK;
@@ -640,19 +661,22 @@ extern "C" int fl_loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev
   a.H = H;
   a.scale_log2 = sm_scale * 1.4426950408889634f;
   if (!dense) {
-    char* w = static_cast<char*>(ws);
-    const size_t n = (size_t)B * H * (size_t)c_list;
-    int2* desc = reinterpret_cast<int2*>(w);
-    int2* upd = reinterpret_cast<int2*>(w + n * sizeof(int2));
-    int32_t* n_upd = reinterpret_cast<int32_t*>(w + 2 * n * sizeof(int2));
-    a.desc = desc;
-    a.upd = upd;
+    const RecLayout L = rec_layout(B, N, H, k, c_list);
+    int2* rec = static_cast<int2*>(ws);
+    int32_t* n_upd = reinterpret_cast<int32_t*>(rec + L.n_rec);
+    a.rec = rec;
     a.n_upd = n_upd;
-    if (c_list > 0) {
-      attn_prep_kernel<<<B * H, 256, 0, st>>>(cols, slot, c_list, N, H, desc, upd, n_upd);
-      int rc = check_launch("attn_prep_kernel");
-      if (rc != FL_OK) return rc;
-    }
+    a.off_upd = (int)L.off_upd;
+    a.off_band = (int)L.off_band;
+    a.off_rows = (int)L.off_rows;
+    a.off_sent = (int)L.off_sent;
+    a.rec_bytes = (uint32_t)(L.n_rec * sizeof(int2));
+    const int per_batch = std::min(64, (N + k + 4095) / 4096);
+    attn_prep_kernel<<<B * H + B * per_batch, 256, 0, st>>>(cols, slot, rows, c_list, N, H, B, k, per_batch,
+                                                          a.off_upd, a.off_band, a.off_rows, a.off_sent, rec,
+                                                          n_upd);
+    int rc = check_launch("attn_prep_kernel");
+    if (rc != FL_OK) return rc;
   }
   const int bm = dense ? 128 : 64;          // rows per workgroup
   dim3 grid(((k + bm - 1) / bm) * B * H);
