@@ -97,11 +97,14 @@ __device__ __forceinline__ float xor32_add(float x) {
 // a DMA target), so the compiler's LDS-DMA tracking does not order them behind pending tile loads.
 template <int D>
 struct Slot {
-  uint16_t k[kBN * D];     // row c at c*D; its 16-byte chunk ch sits at chunk position ch ^ (c & 7)
+  uint16_t k[kBN * D];     // row c at c*D, 16-byte chunks permuted by swz
   uint16_t v[kBN * D];     // same layout; converted in place from bf16 to fp16 before use
 };
 
-__device__ __forceinline__ int swz(int c, int ch) { return ch ^ (c & 7); }
+// 16-byte chunk ch of row c sits at chunk position ch ^ f(c), f = (0,2,4,6,1,3,5,7)[c % 8]: the K reads
+// (8 rows x 16 B per LDS cycle) and the transposed V reads (4 columns x 32 B) both hit 32 distinct banks
+__device__ __forceinline__ int swz_f(int c) { return ((c & 3) << 1) | ((c >> 2) & 1); }
+__device__ __forceinline__ int swz(int c, int ch) { return ch ^ swz_f(c); }
 
 template <int D, bool DENSE>
 __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
@@ -312,6 +315,24 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
     }
   };
 
+  // LDS read offsets (elements) that depend on the lane; the rest of each read address is a constant.
+  // K (A operand of S^T = K Q^T): row r32, chunk 2ks + hw = 8 (ks >> 2) + (2 (ks & 3) + hw), and the
+  // swizzle only permutes the low three bits of a chunk index.  V (transposed reads for O^T += V^T P^T):
+  // lane (16g + 4t + q) points at V[col][dim0 + 4q] of column 16kb + 4(g >> 1) + t (and the same + 8),
+  // dims 32db + 16(g & 1) + 4q, so the transpose read hands lane m of the group V[col_t][dim0 + m]; the
+  // swizzle of those columns is the same for every kb and for the + 8 column.
+  int koff[4], voff[2];
+  {
+    const int g16 = lane >> 4, m16 = lane & 15;
+    const int tq = m16 >> 2, q = m16 & 3;
+    const int col0 = 4 * (g16 >> 1) + tq;
+    const int c_lo = 2 * (g16 & 1) + (q >> 1);
+#pragma unroll
+    for (int m = 0; m < 4; ++m) koff[m] = r32 * D + ((2 * m + hw) ^ swz_f(r32)) * 8;
+#pragma unroll
+    for (int e = 0; e < 2; ++e) voff[e] = col0 * D + ((4 * e + c_lo) ^ swz_f(col0)) * 8 + 4 * (q & 1);
+  }
+
   auto compute = [=, &acc, &run_max, &lsum, &msub](int u, const Slot<D>& sl) {
     const int ri = u & 7;
     const bool newer = u >= n_old;
@@ -336,7 +357,7 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
     f32x16 s = f32x16{};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      const u32x4 kw = *reinterpret_cast<const u32x4*>(&sl.k[r32 * D + swz(r32, 2 * ks + hw) * 8]);
+      const u32x4 kw = *reinterpret_cast<const u32x4*>(&sl.k[koff[ks & 3] + 64 * (ks >> 2)]);
       s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kw), qf[ks], s, 0, 0, 0);
     }
     if (!full) {
@@ -396,24 +417,16 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
       lsum += ts;
     }
     // O^T += V^T P^T over two 16-column k-blocks, fp16 operands
-    const int g16 = lane >> 4, m16 = lane & 15;
-    const int tq = m16 >> 2, q = m16 & 3;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
       const u32x4 pw = {pack_f16x2(pr[8 * kb + 0], pr[8 * kb + 1]), pack_f16x2(pr[8 * kb + 2], pr[8 * kb + 3]),
                         pack_f16x2(pr[8 * kb + 4], pr[8 * kb + 5]), pack_f16x2(pr[8 * kb + 6], pr[8 * kb + 7])};
       const f16x8 pf = __builtin_bit_cast(f16x8, pw);
-      // lane (16g + 4t + q) points at V[col_t][dim0 + 4q]; the transpose read hands lane m of the group
-      // V[col_t][dim0 + m] for t = 0..3 (columns 16kb + 4(g/2) + t, then the same + 8)
-      const int colA = 16 * kb + 4 * (g16 >> 1) + tq;
-      const int colB = colA + 8;
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        const int dim = db * 32 + 16 * (g16 & 1) + 4 * q;
-        const i16x4 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            FL_LDS4(&sl.v[colA * D + swz(colA, dim >> 3) * 8 + (dim & 7)]));
-        const i16x4 vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            FL_LDS4(&sl.v[colB * D + swz(colB, dim >> 3) * 8 + (dim & 7)]));
+        const int o = voff[db & 1] + 64 * (db >> 1) + 16 * kb * D;
+        const i16x4 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(FL_LDS4(&sl.v[o]));
+        const i16x4 vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(FL_LDS4(&sl.v[o + 8 * D]));
         const i16x8 v8 = __builtin_shufflevector(va, vb, 0, 1, 2, 3, 4, 5, 6, 7);
         acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, v8), pf, acc[db], 0, 0, 0);
       }
