@@ -28,7 +28,8 @@
  *     a launch was rejected by the runtime; faults inside kernels surface at the caller's next
  *     synchronization.  fl_last_error() returns a thread-local message for the last non-OK return.
  *   - Results are deterministic: the same inputs give bitwise-identical outputs (no float atomics).
- *   - Supported sizes: head dim d in {64, 128}; B, N, H >= 1; N < 2^31 / (H * d).
+ *   - Supported sizes: head dim d in {64, 128}; B, N, H >= 1; N < 2^31 / (H * d), and for
+ *     fl_loop_sparse_attn N * H * d <= 2^30 (byte offsets of one batch element stay below 2^31).
  */
 #ifndef FLASHLOOP_H
 #define FLASHLOOP_H
@@ -161,6 +162,8 @@ int fl_kv_residual_dequant(const uint8_t* codes, const uint16_t* scale, const ui
  *   lse_ref           : fp32 [B, N, H]     in/out
  *   o                 : fp32 [B, N, H, d]  in/out
  *   ws, ws_bytes      : workspace of at least fl_loop_sparse_attn_ws(...) bytes (may be NULL if 0).
+ *                       Scratch: a prep kernel fills it with the column records of every tile on each
+ *                       call (about 8 * (2 B H c_list + B (N + k)) bytes; FL_E_SHAPE above 2^31).
  * Attention products use bf16 MFMA with fp32 accumulation for q.k and fp16 MFMA for p.v (values are
  * converted bf16 -> fp16, exact for |v| in [2^-14, 65504]); softmax and the update are fp32.
  * ---------------------------------------------------------------------------------------------- */
