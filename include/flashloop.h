@@ -180,6 +180,34 @@ int fl_loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev,
                         float* lse_ref, float* o, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------------------------------
+ * (3b) The same update keeping the add term for the next loop -- Appendix D.2, Eq. 7.
+ *
+ * After the update of loop r, lse_ref_i = L - log m_i, so the next loop's subtract term over the same
+ * S_i and the same (q^(r), X_hat^(r)) is sum_j exp(sigma q^(r)_i . k_j - lse_ref_i) v_j = add, with mass
+ * m_i: it equals this loop's add term in exact arithmetic, as long as the column sets stay fixed and
+ * every row of loop r+1 was updated in loop r (nested selection).  This call
+ *   - with term_out/mass_out: also writes add (fp32 [B, k, H, d], row p of `rows`) and m_i
+ *     (fp32 [B, k, H]); rows left unchanged get 0 and 0;
+ *   - with term_prev (mass_prev, slot_prev, k_prev): takes the subtract term and m_i of row i from row
+ *     slot_prev[b, i] of the previous loop's term_out/mass_out (k_prev rows) instead of recomputing the
+ *     subtract pass, so q_prev is unused (may be NULL).  Every row of `rows` must have
+ *     slot_prev[b, i] >= 0; a row without one is left unchanged.  The kernel then runs the add pass
+ *     only, with two waves per row group splitting each tile's columns.
+ * term_prev and term_out may not alias.  Other arguments as fl_loop_sparse_attn (never DENSE).
+ * ---------------------------------------------------------------------------------------------- */
+int fl_loop_sparse_attn_terms(const uint16_t* q_cur, const uint16_t* q_prev,
+                              const uint16_t* k_cache, const uint16_t* v_cache,
+                              const uint16_t* k_new, const uint16_t* v_new,
+                              const int32_t* slot, const int32_t* rows, int k,
+                              const int32_t* cols, int c_list, int window,
+                              int B, int N, int H, int d, float sm_scale,
+                              float* lse_ref, float* o,
+                              const float* term_prev, const float* mass_prev,
+                              const int32_t* slot_prev, int k_prev,
+                              float* term_out, float* mass_out,
+                              void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------------------------------
  * (4) Column statistic of a dense source loop -- Appendix D.2, Eq. 6 with all causal keys and cached
  * mass 1, summed over all rows of a prefill:
  *     col_key[b, h, j] = fp32( sum_{i >= j} exp(l_ij - lse_i) ),  l_ij = sigma * sum_e q_ie k_je,

@@ -51,7 +51,12 @@ struct AttnArgs {
   uint32_t rec_bytes;        // bytes of the record array, sentinel included
   float* lse_ref;
   float* o;
-  int k, c_list, window, B, N, H;
+  const float* term_prev;    // reuse: [B, k_prev, H, d] add term of the previous loop, by its row position
+  const float* mass_prev;    // reuse: [B, k_prev, H] cached mass of the previous loop
+  const int32_t* slot_prev;  // reuse: [B, N] position of each row in the previous loop's rows
+  float* term_out;           // optional [B, k, H, d]: this loop's add term (the next loop's subtract term)
+  float* mass_out;           // optional [B, k, H]: the cached mass m of each updated row
+  int k, k_prev, c_list, window, B, N, H;
   float scale_log2;          // sm_scale * log2(e)
 };
 
@@ -106,8 +111,15 @@ struct Slot {
 __device__ __forceinline__ int swz_f(int c) { return ((c & 3) << 1) | ((c >> 2) & 1); }
 __device__ __forceinline__ int swz(int c, int ch) { return ch ^ swz_f(c); }
 
-template <int D, bool DENSE>
+// MODE: kDense (loop 1, every row over all causal columns), kFull (subtract and add passes), kReuse (the
+// subtract term is the previous loop's stored add term; the two spare waves of each row group take half
+// of every tile's columns).
+constexpr int kDense = 0, kFull = 1, kReuse = 2;
+
+template <int D, int MODE>
 __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
+  constexpr bool DENSE = MODE == kDense;
+  constexpr bool REUSE = MODE == kReuse;
   constexpr int GROUPS = DENSE ? 4 : 2;
   constexpr int BM = 32 * GROUPS;
   constexpr int KS = D / 16;              // k-steps of QK^T
@@ -117,12 +129,14 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
   constexpr int INST_PER_TILE = kBN / COLS_PER_INST;
   constexpr int INST_PER_WAVE = INST_PER_TILE / 4;   // per tensor (K and V each)
   __shared__ Slot<D> s0, s1, s2, s3;
-  // column ids of tile v in entry v % 8 (kPad = padding): view 0 for the subtract pass and the dense
-  // loop, view 1 for the add pass, where the columns updated this loop are padding in phases A/B
+  // column ids of tile v in entry v % 8 (kPad = padding).  Dense and full modes: view 0 plain (dense
+  // loop, subtract pass), view 1 for the add pass, where the columns updated this loop are padding in
+  // phases A/B.  Reuse mode: view h holds the add view rotated by 16h columns, for the waves of half h.
   __shared__ int tcv[2][8][kBN];
   __shared__ uint32_t toff[8][kBN];       // byte offset of each column's row in its source (kOOB: none)
-  __shared__ int tany[8];                 // some column of tile v was updated (phases A/B)
-  __shared__ float xm[2][64];
+  // tile v: first and last (plain) column id, whether some column was updated this loop (phases A/B)
+  __shared__ int thd[8][4];
+  __shared__ float xm[2][2][64];          // end-of-loop hand-off per group: sum or mass, running max
   __shared__ int s_meta[2];
 
   const int tid = threadIdx.x;
@@ -130,7 +144,8 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
   const int hw = lane >> 5;
   const int r32 = lane & 31;
   const int group = wave % GROUPS;
-  const bool add_pass = DENSE || wave >= 2;
+  const bool add_pass = MODE != kFull || wave >= 2;
+  const int half = REUSE ? __builtin_amdgcn_readfirstlane(wave) >> 1 : 0;   // reuse: columns 16*half .. +15
 
   // work item -> (batch*head, row tile); the row tiles of one (batch, head) stay on one XCD
   const int n_rt = (a.k + BM - 1) / BM;
@@ -246,8 +261,6 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
   const uint32_t head_off = (uint32_t)(h * D * 2);
   const rsrc_t kcR = make_rsrc(a.k_cache + (int64_t)b * a.N * HD, (uint32_t)a.N * rb);
   const rsrc_t vcR = make_rsrc(a.v_cache + (int64_t)b * a.N * HD, (uint32_t)a.N * rb);
-  const rsrc_t knR = make_rsrc(DENSE ? a.k_cache : a.k_new + (int64_t)b * a.k * HD, DENSE ? 0u : (uint32_t)a.k * rb);
-  const rsrc_t vnR = make_rsrc(DENSE ? a.v_cache : a.v_new + (int64_t)b * a.k * HD, DENSE ? 0u : (uint32_t)a.k * rb);
 
   auto store_desc = [=](int v, u32x2 w) {
     int cid, row;
@@ -266,30 +279,85 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
     }
     const bool valid = cid != kPad;
     if (lane < kBN) {
-      tcv[0][v & 7][c32] = cid;
-      tcv[1][v & 7][c32] = upd ? kPad : cid;
+      const int cid_add = upd ? kPad : cid;
+      tcv[0][v & 7][c32] = REUSE ? cid_add : cid;
+      tcv[1][v & 7][REUSE ? (c32 + 16) & 31 : c32] = cid_add;
+      if (c32 == 0) thd[v & 7][0] = cid;
+      if (c32 == kBN - 1) thd[v & 7][1] = cid;
       toff[v & 7][c32] = valid ? (uint32_t)row * rb + head_off : kOOB;
     }
     const uint64_t any = __builtin_amdgcn_ballot_w64(lane < kBN && valid && upd);
-    if (lane == 0) tany[v & 7] = any != 0;
+    if (lane == 0) thd[v & 7][2] = any != 0;
   };
 
   // LDS-DMA of tile u into slot sl: each wave issues INST_PER_WAVE K and INST_PER_WAVE V instructions,
   // always (padding and tiles past the end load nothing: their offsets are out of range)
-  auto issue = [=](int u, Slot<D>& sl) {
-    const bool newer = u >= n_old;        // uniform: one of two scalar branches, same op count
+  // DMA plan: every wave issues NI = 2 * INST_PER_WAVE one-kilobyte instructions per tile.  In the
+  // sparse update the subtract waves (0-1) load all of V and convert it, the add waves (2-3) load all
+  // of K; in the dense loop every wave loads its share of both.  inst_of(t) is the instruction (row
+  // block of the tile) of the wave's t-th op, is_v_op(t) whether it targets V.
+  constexpr int NI = 2 * INST_PER_WAVE;
+  constexpr bool SPLIT_KV = MODE == kFull;
+  const bool v_wave = SPLIT_KV && __builtin_amdgcn_readfirstlane(wave) < 2;
+  // the sparse update's per-wave source tensors (cache state and new rows)
+  const rsrc_t srcC = make_rsrc((v_wave ? a.v_cache : a.k_cache) + (int64_t)b * a.N * HD, (uint32_t)a.N * rb);
+  const rsrc_t srcN = make_rsrc(DENSE ? a.k_cache : (v_wave ? a.v_new : a.k_new) + (int64_t)b * a.k * HD,
+                                DENSE ? 0u : (uint32_t)a.k * rb);
+  const rsrc_t knR = make_rsrc(DENSE ? a.k_cache : a.k_new + (int64_t)b * a.k * HD, DENSE ? 0u : (uint32_t)a.k * rb);
+  const rsrc_t vnR = make_rsrc(DENSE ? a.v_cache : a.v_new + (int64_t)b * a.k * HD, DENSE ? 0u : (uint32_t)a.k * rb);
+  auto inst_of = [=](int t) { return SPLIT_KV ? (wave & 1) * NI + t : wave * INST_PER_WAVE + (t % INST_PER_WAVE); };
+  auto is_v_op = [=](int t) { return SPLIT_KV ? v_wave : t >= INST_PER_WAVE; };
+  // source byte offsets of this lane's chunks of tile u (read from the tables ahead of the barrier)
+  struct Offs { uint32_t o[NI]; };
+  auto tile_offs = [=](int u) {
+    Offs r;
 #pragma unroll
-    for (int t = 0; t < INST_PER_WAVE; ++t) {
-      const int inst = wave * INST_PER_WAVE + t;
-      const int c = inst * COLS_PER_INST + lane / CH;
-      const int ch = swz(c, lane % CH);
-      const uint32_t off = toff[u & 7][c] + (uint32_t)ch * 16;   // kOOB + 240 is still out of range
+    for (int t = 0; t < NI; ++t) {
+      const int c = inst_of(t) * COLS_PER_INST + lane / CH;
+      r.o[t] = toff[u & 7][c] + (uint32_t)swz(c, lane % CH) * 16;   // kOOB + 240 is still out of range
+    }
+    return r;
+  };
+  // (each offset goes through a local: handing the struct member straight to the builtin makes the
+  // host compilation drop the kernel's launch stub)
+  auto issue = [=](int u, Slot<D>& sl, const Offs& of) {
+    if constexpr (!SPLIT_KV) {
+      const bool newer = !DENSE && u >= n_old;   // uniform: one of two scalar branches, same op count
       if (newer) {
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(knR, FL_LDS(sl.k + inst * 512), 16, off, 0, 0, 0);
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(vnR, FL_LDS(sl.v + inst * 512), 16, off, 0, 0, 0);
+#pragma unroll
+        for (int t = 0; t < NI; ++t) {
+          const int inst = inst_of(t);
+          const uint32_t off = of.o[t];
+          if (t < INST_PER_WAVE)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(knR, FL_LDS(sl.k + inst * 512), 16, off, 0, 0, 0);
+          else
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(vnR, FL_LDS(sl.v + inst * 512), 16, off, 0, 0, 0);
+        }
       } else {
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(kcR, FL_LDS(sl.k + inst * 512), 16, off, 0, 0, 0);
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(vcR, FL_LDS(sl.v + inst * 512), 16, off, 0, 0, 0);
+#pragma unroll
+        for (int t = 0; t < NI; ++t) {
+          const int inst = inst_of(t);
+          const uint32_t off = of.o[t];
+          if (t < INST_PER_WAVE)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(kcR, FL_LDS(sl.k + inst * 512), 16, off, 0, 0, 0);
+          else
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(vcR, FL_LDS(sl.v + inst * 512), 16, off, 0, 0, 0);
+        }
+      }
+    } else {
+      uint16_t* dst = v_wave ? sl.v : sl.k;
+      if (u >= n_old) {                   // uniform: one of two scalar branches, same op count
+#pragma unroll
+        for (int t = 0; t < NI; ++t) {
+          const uint32_t off = of.o[t];
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(srcN, FL_LDS(dst + inst_of(t) * 512), 16, off, 0, 0, 0);
+        }
+      } else {
+#pragma unroll
+        for (int t = 0; t < NI; ++t) {
+          const uint32_t off = of.o[t];
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(srcC, FL_LDS(dst + inst_of(t) * 512), 16, off, 0, 0, 0);
+        }
       }
     }
   };
@@ -303,15 +371,18 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
   // wave w converts, in place, the V rows its own LDS-DMA wrote (bf16 -> fp16, exact for |v| in
   // [2^-14, 65504]); the barrier that follows publishes them to the other waves
   auto convert_v = [=](Slot<D>& sl) {
+    u32x4 w[NI];
 #pragma unroll
-    for (int t = 0; t < INST_PER_WAVE; ++t) {
-      uint16_t* p = sl.v + (wave * INST_PER_WAVE + t) * 512 + lane * 8;
-      const u32x4 w = *reinterpret_cast<const u32x4*>(p);
+    for (int t = 0; t < NI; ++t)           // all reads first: one LDS round trip for the batch
+      if (is_v_op(t)) w[t] = *reinterpret_cast<const u32x4*>(sl.v + inst_of(t) * 512 + lane * 8);
+#pragma unroll
+    for (int t = 0; t < NI; ++t) {
+      if (!is_v_op(t)) continue;
       u32x4 h;
 #pragma unroll
       for (int e = 0; e < 4; ++e)
-        h[e] = pack_f16x2(__uint_as_float(w[e] << 16), __uint_as_float(w[e] & 0xFFFF0000u));
-      *reinterpret_cast<u32x4*>(p) = h;
+        h[e] = pack_f16x2(__uint_as_float(w[t][e] << 16), __uint_as_float(w[t][e] & 0xFFFF0000u));
+      *reinterpret_cast<u32x4*>(sl.v + inst_of(t) * 512 + lane * 8) = h;
     }
   };
 
@@ -330,18 +401,26 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
 #pragma unroll
     for (int m = 0; m < 4; ++m) koff[m] = r32 * D + ((2 * m + hw) ^ swz_f(r32)) * 8;
 #pragma unroll
-    for (int e = 0; e < 2; ++e) voff[e] = col0 * D + ((4 * e + c_lo) ^ swz_f(col0)) * 8 + 4 * (q & 1);
+    for (int e = 0; e < 2; ++e)            // (+ 16 columns for the reuse mode's second-half waves)
+      voff[e] = (col0 + 16 * half) * D + ((4 * e + c_lo) ^ swz_f(col0)) * 8 + 4 * (q & 1);
   }
 
-  auto compute = [=, &acc, &run_max, &lsum, &msub](int u, const Slot<D>& sl) {
+  // first and last column id of tile u and whether it holds an updated column (uniform; read ahead of
+  // the barrier, the entries were written four steps earlier)
+  struct TileHead { int c0, clast, any; };
+  auto tile_head = [=](int u) {
+    return TileHead{thd[u & 7][0], thd[u & 7][1], thd[u & 7][2]};
+  };
+
+  auto compute = [=, &acc, &run_max, &lsum, &msub](int u, const Slot<D>& sl, const TileHead& th) {
     const int ri = u & 7;
     const bool newer = u >= n_old;
     const bool is_list = u < tA || (newer && u < n_old + tC);
     if (newer && !add_pass) return;
     // does any row of this wave's group see any column of this tile, and do all rows see all of it?
-    // (uniform; column ids ascend within a tile and padding, kPad, sits at the end)
-    const int c0 = tcv[0][ri][0];
-    const int clast = tcv[0][ri][kBN - 1];
+    // (column ids ascend within a tile and padding, kPad, sits at the end)
+    const int c0 = th.c0;
+    const int clast = th.clast;
     bool active, full;
     if (is_list) {
       active = group_has_rows && c0 <= gmax - a.window;
@@ -352,7 +431,7 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
       full = clast <= gmin && (DENSE || c0 > gmax - a.window);
     }
     if (!active) return;
-    if (!DENSE && add_pass && !newer && tany[ri]) full = false;   // updated columns drop out
+    if (!DENSE && add_pass && !newer && th.any) full = false;   // updated columns drop out
     // S^T = K Q^T: lane holds columns 8j + 4hw + i of row r32
     f32x16 s = f32x16{};
 #pragma unroll
@@ -360,33 +439,41 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
       const u32x4 kw = *reinterpret_cast<const u32x4*>(&sl.k[koff[ks & 3] + 64 * (ks >> 2)]);
       s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kw), qf[ks], s, 0, 0, 0);
     }
+    // masks, softmax and O^T += V^T P^T over the lane's first NE elements, fp16 operands.  In the reuse
+    // mode every wave takes one 16-column half of the tile: the second half's scores move down first,
+    // and its column ids (the rotated table view) and V rows (voff) are those of the second half.
+    constexpr int NE = REUSE ? 8 : 16;
+    if (REUSE && half != 0) {              // uniform
+#pragma unroll
+      for (int v = 0; v < 8; ++v) s[v] = s[v + 8];
+    }
     if (!full) {
       // column masks: list columns need j + window <= i, band columns i - window < j <= i (any j <= i in
       // the dense loop); padding and, for the add pass, the columns updated this loop carry kPad
-      const int view = (!DENSE && add_pass) ? 1 : 0;
+      const int view = REUSE ? half : (!DENSE && add_pass) ? 1 : 0;
       int cc[16];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < NE / 4; ++j) {
         const int4 c4 = *reinterpret_cast<const int4*>(&tcv[view][ri][8 * j + 4 * hw]);
         cc[4 * j] = c4.x; cc[4 * j + 1] = c4.y; cc[4 * j + 2] = c4.z; cc[4 * j + 3] = c4.w;
       }
       if (is_list) {
         const int lim = row_i - a.window;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) s[v] = cc[v] <= lim ? s[v] : -INFINITY;
+        for (int v = 0; v < NE; ++v) s[v] = cc[v] <= lim ? s[v] : -INFINITY;
       } else if (DENSE) {
 #pragma unroll
-        for (int v = 0; v < 16; ++v) s[v] = cc[v] <= row_i ? s[v] : -INFINITY;
+        for (int v = 0; v < NE; ++v) s[v] = cc[v] <= row_i ? s[v] : -INFINITY;
       } else {
         const uint32_t w = (uint32_t)a.window;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) s[v] = (uint32_t)row_i - (uint32_t)cc[v] < w ? s[v] : -INFINITY;
+        for (int v = 0; v < NE; ++v) s[v] = (uint32_t)row_i - (uint32_t)cc[v] < w ? s[v] : -INFINITY;
       }
     }
     float pr[16];
     if (!add_pass) {
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
+      for (int v = 0; v < NE; ++v) {
         pr[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], a.scale_log2, -lse2));   // masked: exp2(-inf) = 0
         msub += pr[v];
       }
@@ -396,7 +483,7 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
       // rescaled rarely; the final normaliser uses the same reference
       float tmax = s[0];
 #pragma unroll
-      for (int v = 1; v < 16; ++v) tmax = fmaxf(tmax, s[v]);
+      for (int v = 1; v < NE; ++v) tmax = fmaxf(tmax, s[v]);
       tmax = xor32_max(tmax) * a.scale_log2;
       const bool raise = tmax > run_max + 8.0f;          // false while both are -inf
       if (__builtin_amdgcn_ballot_w64(raise) != 0) {      // uniform: rescale the rows that need it
@@ -410,15 +497,14 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
       const float ref = run_max == -INFINITY ? 0.0f : run_max;
       float ts = 0.0f;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
+      for (int v = 0; v < NE; ++v) {
         pr[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], a.scale_log2, -ref));
         ts += pr[v];
       }
       lsum += ts;
     }
-    // O^T += V^T P^T over two 16-column k-blocks, fp16 operands
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < NE / 8; ++kb) {
       const u32x4 pw = {pack_f16x2(pr[8 * kb + 0], pr[8 * kb + 1]), pack_f16x2(pr[8 * kb + 2], pr[8 * kb + 3]),
                         pack_f16x2(pr[8 * kb + 4], pr[8 * kb + 5]), pack_f16x2(pr[8 * kb + 6], pr[8 * kb + 7])};
       const f16x8 pf = __builtin_bit_cast(f16x8, pw);
@@ -434,35 +520,44 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
   };
 
   // ---- pipeline --------------------------------------------------------------------------------------
-  // step s: wait for tile s; convert this wave's V rows of it; finalize the records of tile s+4;
-  // barrier; load the records of tile s+6; LDS-DMA tile s+3 into the slot tile s-1 used; compute tile
-  // s.  Every step issues the same number of VMEM ops (one record load in the sparse update and
+  // step s: read the table entries of tiles s+3 and s; wait for tile s; convert this wave's V rows of
+  // it; finalize the records of tile s+4; barrier; load the records of tile s+6; LDS-DMA tile s+3 into
+  // the slot tile s-1 used; compute tile s.  Every step issues the same number of VMEM ops (one record load in the sparse update and
   // 2 * INST_PER_WAVE DMA), so "tile s has landed" is exactly vmcnt(2 * OPS_PER_STEP) on every path.
-  constexpr int OPS_PER_STEP = (DENSE ? 0 : 1) + 2 * INST_PER_WAVE;
+  // Every wave loads the records (equal op counts keep every wait exact); one wave writes the tables:
+  // an add wave when the subtract waves convert all of V.
+  const bool rec_wave = __builtin_amdgcn_readfirstlane(wave) == (SPLIT_KV ? 2 : 0);
+  constexpr int OPS_PER_STEP = (DENSE ? 0 : 1) + NI;
   u32x2 dA, dB;                           // records in flight (even / odd tiles)
 #pragma unroll
-  for (int v = 0; v < 4; ++v) store_desc(v, load_desc(v));
+  for (int v = 0; v < 4; ++v) {
+    const u32x2 r = load_desc(v);
+    if (rec_wave) store_desc(v, r);
+  }
   FL_WAIT_VM(0);                          // query fragments have arrived
   lds_barrier();
   // the scheduling barriers keep this order, which the wait counts of the first steps assume
-  issue(0, s0);                           // as step -3
+  issue(0, s0, tile_offs(0));             // as step -3
   __builtin_amdgcn_sched_barrier(0);
   dA = load_desc(4);                      // as step -2
   __builtin_amdgcn_sched_barrier(0);
-  issue(1, s1);
+  issue(1, s1, tile_offs(1));
   __builtin_amdgcn_sched_barrier(0);
   dB = load_desc(5);                      // as step -1
   __builtin_amdgcn_sched_barrier(0);
-  issue(2, s2);
+  issue(2, s2, tile_offs(2));
 
   auto step = [&](int u, Slot<D>& cur, Slot<D>& nxt, u32x2& w) {
+    const Offs of = tile_offs(u + 3);     // tables of tiles u+3 and u were published by earlier barriers
+    const TileHead th = tile_head(u);
     FL_WAIT_VM(2 * OPS_PER_STEP);
     convert_v(cur);
-    store_desc(u + 4, w);
+    if (rec_wave) store_desc(u + 4, w);
     lds_barrier();
     w = load_desc(u + 6);
-    issue(u + 3, nxt);
-    if (u < n_tiles) compute(u, cur);
+    __builtin_amdgcn_sched_barrier(0);    // keep the record load ahead of the DMA (the waits count on it)
+    issue(u + 3, nxt, of);
+    if (u < n_tiles) compute(u, cur, th);
   };
   const int n_steps = (n_tiles + kRing - 1) / kRing * kRing;
   for (int u = 0; u < n_steps; u += kRing) {
@@ -477,21 +572,44 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
   // the two half-waves hold disjoint columns of the same row
   lsum = xor32_add(lsum);
   msub = xor32_add(msub);
-  // subtract-pass hand-off: group g uses ring slot g (D * 128 bytes >= 32 rows x D floats; ring is idle)
+  // hand-off through the idle ring: group g uses slot g (D * 128 bytes >= 32 rows x D floats).  The full
+  // mode's subtract waves hand over (sub, m); the reuse mode's second-half waves hand over their
+  // (acc, running max, sum), which the first-half waves merge into theirs.
   float4* xacc = reinterpret_cast<float4*>(group == 0 ? &s0 : &s1);
   if constexpr (!DENSE) {
-    if (!add_pass) {
+    const bool giver = REUSE ? half == 1 : !add_pass;
+    if (giver) {
 #pragma unroll
       for (int db = 0; db < DB; ++db)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
           xacc[(db * 4 + j) * 64 + lane] =
               make_float4(acc[db][4 * j], acc[db][4 * j + 1], acc[db][4 * j + 2], acc[db][4 * j + 3]);
-      xm[group][lane] = msub;
+      xm[group][0][lane] = REUSE ? lsum : msub;
+      if (REUSE) xm[group][1][lane] = run_max;
     }
     lds_barrier();
-    if (!add_pass) return;
-    msub = xm[group][lane];
+    if (giver) return;
+    if constexpr (REUSE) {
+      const float m1 = xm[group][1][lane], l1 = xm[group][0][lane];
+      const float mm = fmaxf(run_max, m1);
+      const float a0 = mm == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(run_max - mm);
+      const float a1 = mm == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m1 - mm);
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float4 x = xacc[(db * 4 + j) * 64 + lane];
+          acc[db][4 * j + 0] = acc[db][4 * j + 0] * a0 + x.x * a1;
+          acc[db][4 * j + 1] = acc[db][4 * j + 1] * a0 + x.y * a1;
+          acc[db][4 * j + 2] = acc[db][4 * j + 2] * a0 + x.z * a1;
+          acc[db][4 * j + 3] = acc[db][4 * j + 3] * a0 + x.w * a1;
+        }
+      lsum = lsum * a0 + l1 * a1;
+      run_max = mm;
+    } else {
+      msub = xm[group][0][lane];
+    }
   }
   if (!row_ok) return;
   const int64_t orow = ((int64_t)b * a.N + row_i) * HD + (int64_t)h * D;
@@ -510,22 +628,48 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
       }
     if (hw == 0) a.lse_ref[lrow] = (run_max + log2f(lsum)) * 0.6931471805599453f;
   } else {
-    if (!(msub > 0.0f) || !(lsum > 0.0f)) return;     // empty column set or vanished mass: unchanged
+    // the subtract term: recomputed (full) or the previous loop's add term of this row (reuse)
+    const float* subp = nullptr;
+    if constexpr (REUSE) {
+      const int pp = a.slot_prev[(int64_t)b * a.N + row_i];
+      const int64_t tp = ((int64_t)b * a.k_prev + pp) * a.H + h;
+      msub = pp >= 0 ? a.mass_prev[tp] : 0.0f;
+      subp = a.term_prev + tp * D;
+    }
+    const int64_t trow = ((int64_t)b * a.k + p) * a.H + h;
+    const bool keep = a.term_out != nullptr;
+    if (!(msub > 0.0f) || !(lsum > 0.0f)) {     // empty column set or vanished mass: unchanged
+      if (keep) {
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            *reinterpret_cast<float4*>(a.term_out + trow * D + db * 32 + 8 * j + 4 * hw) = make_float4(0, 0, 0, 0);
+        if (hw == 0) a.mass_out[trow] = 0.0f;
+      }
+      return;
+    }
     const float f = msub / lsum;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int dim = db * 32 + 8 * j + 4 * hw;
-        const float4 sub = xacc[(db * 4 + j) * 64 + lane];
+        const float4 sub = REUSE ? *reinterpret_cast<const float4*>(subp + dim) : xacc[(db * 4 + j) * 64 + lane];
+        const float4 add = make_float4(acc[db][4 * j + 0] * f, acc[db][4 * j + 1] * f,
+                                       acc[db][4 * j + 2] * f, acc[db][4 * j + 3] * f);
         float4 prev = *reinterpret_cast<const float4*>(a.o + orow + dim);
-        prev.x = prev.x - sub.x + acc[db][4 * j + 0] * f;
-        prev.y = prev.y - sub.y + acc[db][4 * j + 1] * f;
-        prev.z = prev.z - sub.z + acc[db][4 * j + 2] * f;
-        prev.w = prev.w - sub.w + acc[db][4 * j + 3] * f;
+        prev.x = prev.x - sub.x + add.x;
+        prev.y = prev.y - sub.y + add.y;
+        prev.z = prev.z - sub.z + add.z;
+        prev.w = prev.w - sub.w + add.w;
         *reinterpret_cast<float4*>(a.o + orow + dim) = prev;
+        if (keep) *reinterpret_cast<float4*>(a.term_out + trow * D + dim) = add;
       }
-    if (hw == 0) a.lse_ref[lrow] = (run_max + log2f(lsum)) * 0.6931471805599453f - logf(msub);
+    if (hw == 0) {
+      a.lse_ref[lrow] = (run_max + log2f(lsum)) * 0.6931471805599453f - logf(msub);
+      if (keep) a.mass_out[trow] = msub;
+    }
   }
 }
 
@@ -620,15 +764,15 @@ extern "C" size_t fl_loop_sparse_attn_ws(int B, int N, int H, int d, int k, int 
   return attn_ws_bytes(B, N, H, k, c_list, (flags & FL_ATTN_DENSE) != 0);
 }
 
-extern "C" int fl_loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev,
-                                   const uint16_t* k_cache, const uint16_t* v_cache,
-                                   const uint16_t* k_new, const uint16_t* v_new,
-                                   const int32_t* slot, const int32_t* rows, int k,
-                                   const int32_t* cols, int c_list, int window, int B, int N, int H,
-                                   int d, float sm_scale, int flags, float* lse_ref, float* o,
-                                   void* ws, size_t ws_bytes, void* stream) {
-  FL_API_BEGIN
+static int loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev, const uint16_t* k_cache,
+                            const uint16_t* v_cache, const uint16_t* k_new, const uint16_t* v_new,
+                            const int32_t* slot, const int32_t* rows, int k, const int32_t* cols, int c_list,
+                            int window, int B, int N, int H, int d, float sm_scale, int flags, float* lse_ref,
+                            float* o, const float* term_prev, const float* mass_prev, const int32_t* slot_prev,
+                            int k_prev, float* term_out, float* mass_out, void* ws, size_t ws_bytes,
+                            void* stream) {
   const bool dense = (flags & FL_ATTN_DENSE) != 0;
+  const bool reuse = term_prev != nullptr;
   FL_REQUIRE((flags & ~FL_ATTN_DENSE) == 0, FL_E_UNSUPPORTED, "fl_loop_sparse_attn: unknown flags 0x%x", flags);
   FL_REQUIRE(q_cur && k_cache && v_cache && lse_ref && o, FL_E_NULL,
              "fl_loop_sparse_attn: q_cur, k_cache, v_cache, lse_ref and o are required");
@@ -637,15 +781,22 @@ extern "C" int fl_loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev
   FL_REQUIRE((int64_t)N * H * d <= ((int64_t)1 << 30), FL_E_SHAPE,
              "fl_loop_sparse_attn: N * H * d above 2^30 (byte offsets must stay below 2^31)");
   FL_REQUIRE(sm_scale > 0.0f && std::isfinite(sm_scale), FL_E_RANGE, "fl_loop_sparse_attn: sm_scale must be > 0");
+  FL_REQUIRE((term_out == nullptr) == (mass_out == nullptr), FL_E_NULL,
+             "fl_loop_sparse_attn: term_out and mass_out go together");
   if (dense) {
     FL_REQUIRE(rows == nullptr && k == N, FL_E_SHAPE, "fl_loop_sparse_attn: DENSE needs rows == NULL and k == N");
+    FL_REQUIRE(!reuse && term_out == nullptr, FL_E_UNSUPPORTED, "fl_loop_sparse_attn: DENSE keeps no terms");
   } else {
-    FL_REQUIRE(q_prev && k_new && v_new && slot && rows, FL_E_NULL,
-               "fl_loop_sparse_attn: q_prev, k_new, v_new, slot and rows are required");
+    FL_REQUIRE(k_new && v_new && slot && rows && (reuse || q_prev), FL_E_NULL,
+               "fl_loop_sparse_attn: q_prev (unless reusing terms), k_new, v_new, slot and rows are required");
     FL_REQUIRE(k >= 0 && k <= N, FL_E_RANGE, "fl_loop_sparse_attn: k=%d outside [0, N]", k);
     FL_REQUIRE(c_list >= 0 && c_list <= N, FL_E_RANGE, "fl_loop_sparse_attn: c_list=%d outside [0, N]", c_list);
     FL_REQUIRE(c_list == 0 || cols, FL_E_NULL, "fl_loop_sparse_attn: cols is required when c_list > 0");
     FL_REQUIRE(window >= 0, FL_E_RANGE, "fl_loop_sparse_attn: window must be >= 0");
+    if (reuse) {
+      FL_REQUIRE(mass_prev && slot_prev, FL_E_NULL, "fl_loop_sparse_attn: term_prev needs mass_prev and slot_prev");
+      FL_REQUIRE(k_prev >= k && k_prev <= N, FL_E_RANGE, "fl_loop_sparse_attn: k_prev=%d outside [k, N]", k_prev);
+    }
   }
   const size_t need = attn_ws_bytes(B, N, H, k, c_list, dense);
   FL_REQUIRE(dense || rec_layout(B, N, H, k, c_list).n_rec * sizeof(int2) <= ((size_t)1 << 31) - 8, FL_E_SHAPE,
@@ -656,7 +807,7 @@ extern "C" int fl_loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev
   hipStream_t st = as_stream(stream);
   AttnArgs a{};
   a.q_cur = q_cur;
-  a.q_prev = dense ? nullptr : q_prev;
+  a.q_prev = (dense || reuse) ? nullptr : q_prev;
   a.k_cache = k_cache;
   a.v_cache = v_cache;
   a.k_new = dense ? nullptr : k_new;
@@ -666,7 +817,13 @@ extern "C" int fl_loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev
   a.cols = dense ? nullptr : cols;
   a.lse_ref = lse_ref;
   a.o = o;
+  a.term_prev = term_prev;
+  a.mass_prev = mass_prev;
+  a.slot_prev = slot_prev;
+  a.term_out = term_out;
+  a.mass_out = mass_out;
   a.k = k;
+  a.k_prev = reuse ? k_prev : 0;
   a.c_list = dense ? 0 : c_list;
   a.window = dense ? 0 : window;
   a.B = B;
@@ -684,7 +841,7 @@ extern "C" int fl_loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev
     a.off_rows = (int)L.off_rows;
     a.off_sent = (int)L.off_sent;
     a.rec_bytes = (uint32_t)(L.n_rec * sizeof(int2));
-    const int per_batch = std::min(64, (N + k + 4095) / 4096);
+    const int per_batch = std::min(256, (N + k + 1023) / 1024);
     attn_prep_kernel<<<B * H + B * per_batch, 256, 0, st>>>(cols, slot, rows, c_list, N, H, B, k, per_batch,
                                                           a.off_upd, a.off_band, a.off_rows, a.off_sent, rec,
                                                           n_upd);
@@ -694,12 +851,43 @@ extern "C" int fl_loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev
   const int bm = dense ? 128 : 64;          // rows per workgroup
   dim3 grid(((k + bm - 1) / bm) * B * H);
   if (d == 128) {
-    if (dense) loop_attn_kernel<128, true><<<grid, 256, 0, st>>>(a);
-    else loop_attn_kernel<128, false><<<grid, 256, 0, st>>>(a);
+    if (dense) loop_attn_kernel<128, kDense><<<grid, 256, 0, st>>>(a);
+    else if (reuse) loop_attn_kernel<128, kReuse><<<grid, 256, 0, st>>>(a);
+    else loop_attn_kernel<128, kFull><<<grid, 256, 0, st>>>(a);
   } else {
-    if (dense) loop_attn_kernel<64, true><<<grid, 256, 0, st>>>(a);
-    else loop_attn_kernel<64, false><<<grid, 256, 0, st>>>(a);
+    if (dense) loop_attn_kernel<64, kDense><<<grid, 256, 0, st>>>(a);
+    else if (reuse) loop_attn_kernel<64, kReuse><<<grid, 256, 0, st>>>(a);
+    else loop_attn_kernel<64, kFull><<<grid, 256, 0, st>>>(a);
   }
   return check_launch("loop_attn_kernel");
+}
+
+extern "C" int fl_loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev,
+                                   const uint16_t* k_cache, const uint16_t* v_cache,
+                                   const uint16_t* k_new, const uint16_t* v_new,
+                                   const int32_t* slot, const int32_t* rows, int k,
+                                   const int32_t* cols, int c_list, int window, int B, int N, int H,
+                                   int d, float sm_scale, int flags, float* lse_ref, float* o,
+                                   void* ws, size_t ws_bytes, void* stream) {
+  FL_API_BEGIN
+  return loop_sparse_attn(q_cur, q_prev, k_cache, v_cache, k_new, v_new, slot, rows, k, cols, c_list, window, B,
+                          N, H, d, sm_scale, flags, lse_ref, o, nullptr, nullptr, nullptr, 0, nullptr, nullptr, ws,
+                          ws_bytes, stream);
+  FL_API_END
+}
+
+extern "C" int fl_loop_sparse_attn_terms(const uint16_t* q_cur, const uint16_t* q_prev,
+                                         const uint16_t* k_cache, const uint16_t* v_cache,
+                                         const uint16_t* k_new, const uint16_t* v_new,
+                                         const int32_t* slot, const int32_t* rows, int k,
+                                         const int32_t* cols, int c_list, int window, int B, int N, int H,
+                                         int d, float sm_scale, float* lse_ref, float* o,
+                                         const float* term_prev, const float* mass_prev,
+                                         const int32_t* slot_prev, int k_prev, float* term_out,
+                                         float* mass_out, void* ws, size_t ws_bytes, void* stream) {
+  FL_API_BEGIN
+  return loop_sparse_attn(q_cur, q_prev, k_cache, v_cache, k_new, v_new, slot, rows, k, cols, c_list, window, B,
+                          N, H, d, sm_scale, 0, lse_ref, o, term_prev, mass_prev, slot_prev, k_prev, term_out,
+                          mass_out, ws, ws_bytes, stream);
   FL_API_END
 }

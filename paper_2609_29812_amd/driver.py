@@ -6,6 +6,8 @@ setup()       dense source loop 1: base codec of K (per-channel groups) and V (p
 sparse_step() one sparse loop r >= 2: select the active rows among the previous loop's (Eq. 5), quantize
               their K/V residuals against the caches and reconstruct the new rows (Eq. 8), apply the
               mass-corrected update to their outputs (Eq. 7), then commit the new rows into the caches.
+              Each loop keeps its add terms; from the second sparse loop on they serve as the subtract
+              terms (equal in exact arithmetic: the column sets are fixed and the active rows nested).
 """
 from __future__ import annotations
 
@@ -27,6 +29,10 @@ class LayerState:
     window: int = 0
     group: int = 64
     base: dict = field(default_factory=dict)
+    reuse: bool = True                  # keep add terms and reuse them as the next loop's subtract terms
+    term: torch.Tensor | None = None    # fp32 [B, k, H, d] add terms of the last loop (row order of cand)
+    mass: torch.Tensor | None = None    # fp32 [B, k, H]
+    slot_prev: torch.Tensor | None = None   # int32 [B, N] slot map of the last loop
 
 
 def setup(q1, k1, v1, base_bits, group, n_sink, t, window):
@@ -48,7 +54,19 @@ def sparse_step(st: LayerState, qr, qp, kr, kp, vr, vp, k_r, bits, keep=False):
     idx, slot, key = fl.select_tokens(kr, kp, vr, vp, k_r, cand=st.cand)
     ck, sk, zk, k_new = fl.kv_residual_quant(kr, st.k_hat, idx, bits, st.group, fl.AXIS_TOKEN)
     cv, sv, zv, v_new = fl.kv_residual_quant(vr, st.v_hat, idx, bits, st.group, fl.AXIS_CHANNEL)
-    fl.loop_sparse_attn(qr, qp, st.k_hat, st.v_hat, k_new, v_new, slot, idx, st.cols, st.window, st.lse, st.o)
+    term = mass = None
+    if st.reuse:
+        B, k, H, d = k_new.shape
+        term = torch.empty(B, k, H, d, dtype=torch.float32, device=k_new.device)
+        mass = torch.empty(B, k, H, dtype=torch.float32, device=k_new.device)
+    if st.reuse and st.term is not None:
+        fl.loop_sparse_attn(qr, None, st.k_hat, st.v_hat, k_new, v_new, slot, idx, st.cols, st.window, st.lse,
+                            st.o, term_prev=st.term, mass_prev=st.mass, slot_prev=st.slot_prev, term_out=term,
+                            mass_out=mass)
+    else:
+        fl.loop_sparse_attn(qr, qp, st.k_hat, st.v_hat, k_new, v_new, slot, idx, st.cols, st.window, st.lse,
+                            st.o, term_out=term, mass_out=mass)
+    st.term, st.mass, st.slot_prev = term, mass, slot
     fl.kv_residual_dequant(ck, sk, zk, idx, bits, st.group, fl.AXIS_TOKEN, st.k_hat, mode=fl.DQ_COMMIT)
     fl.kv_residual_dequant(cv, sv, zv, idx, bits, st.group, fl.AXIS_CHANNEL, st.v_hat, mode=fl.DQ_COMMIT)
     st.cand = idx

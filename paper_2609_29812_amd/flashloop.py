@@ -41,6 +41,9 @@ _SIGNATURES = {
     "fl_loop_sparse_attn_ws": (_c_sz, [_c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i]),
     "fl_loop_sparse_attn": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_i, _c_p, _c_i, _c_i,
                                    _c_i, _c_i, _c_i, _c_i, _c_f, _c_i, _c_p, _c_p, _c_p, _c_sz, _c_p]),
+    "fl_loop_sparse_attn_terms": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_i, _c_p, _c_i, _c_i,
+                                         _c_i, _c_i, _c_i, _c_i, _c_f, _c_p, _c_p, _c_p, _c_p, _c_p, _c_i, _c_p,
+                                         _c_p, _c_p, _c_sz, _c_p]),
     "fl_column_scores_ws": (_c_sz, [_c_i, _c_i, _c_i]),
     "fl_column_scores": (_c_i, [_c_p, _c_p, _c_i, _c_i, _c_i, _c_i, _c_p, _c_p, _c_sz, _c_p]),
     "fl_select_columns": (_c_i, [_c_p, _c_i, _c_i, _c_i, _c_i, _c_i, _c_p, _c_p]),
@@ -175,10 +178,16 @@ def kv_residual_dequant(codes, scale, zero, idx, bits, group, axis, x_hat, mode=
 
 # ---- (3) attention ----------------------------------------------------------------------------------
 def loop_sparse_attn(q_cur, q_prev, k_cache, v_cache, k_new, v_new, slot, rows, cols, window, lse_ref, o,
-                     sm_scale=None, ws=None):
-    """Mass-corrected update of rows `rows` (in place on lse_ref and o)."""
+                     sm_scale=None, ws=None, term_prev=None, mass_prev=None, slot_prev=None, term_out=None,
+                     mass_out=None):
+    """Mass-corrected update of rows `rows` (in place on lse_ref and o).
+
+    term_out/mass_out (fp32 [B, k, H, d] / [B, k, H]) also keep this loop's add terms; term_prev/mass_prev with
+    slot_prev (the previous loop's slot map) reuse the previous loop's add terms as the subtract terms, in
+    which case q_prev may be None."""
     B, N, H, d = q_cur.shape
     k = rows.shape[1]
+    reuse = term_prev is not None
     for name, t in (("q_cur", q_cur), ("q_prev", q_prev), ("k_cache", k_cache), ("v_cache", v_cache)):
         _dev(t, torch.bfloat16, name, q_cur.shape)
     _dev(k_new, torch.bfloat16, "k_new", (B, k, H, d))
@@ -189,15 +198,30 @@ def loop_sparse_attn(q_cur, q_prev, k_cache, v_cache, k_new, v_new, slot, rows, 
     _dev(cols, torch.int32, "cols", None if cols is None else (B, H, c_list))
     _dev(lse_ref, torch.float32, "lse_ref", (B, N, H))
     _dev(o, torch.float32, "o", (B, N, H, d))
+    k_prev = 0
+    if reuse:
+        k_prev = term_prev.shape[1]
+        _dev(term_prev, torch.float32, "term_prev", (B, k_prev, H, d))
+        _dev(mass_prev, torch.float32, "mass_prev", (B, k_prev, H))
+        _dev(slot_prev, torch.int32, "slot_prev", (B, N))
+    _dev(term_out, torch.float32, "term_out", (B, k, H, d))
+    _dev(mass_out, torch.float32, "mass_out", (B, k, H))
     sm_scale = 1.0 / math.sqrt(d) if sm_scale is None else sm_scale
     lib = load()
     need = lib.fl_loop_sparse_attn_ws(B, N, H, d, k, c_list, window, 0)
     if need and (ws is None or ws.numel() < need):
         ws = torch.empty(need, dtype=torch.uint8, device=q_cur.device)
-    rc = lib.fl_loop_sparse_attn(_p(q_cur), _p(q_prev), _p(k_cache), _p(v_cache), _p(k_new), _p(v_new),
-                                 _p(slot), _p(rows), k, _p(cols), c_list, window, B, N, H, d, sm_scale, 0,
-                                 _p(lse_ref), _p(o), _p(ws) if need else None, need, _stream())
-    _check(rc, "fl_loop_sparse_attn")
+    if reuse or term_out is not None:
+        rc = lib.fl_loop_sparse_attn_terms(_p(q_cur), _p(q_prev), _p(k_cache), _p(v_cache), _p(k_new), _p(v_new),
+                                           _p(slot), _p(rows), k, _p(cols), c_list, window, B, N, H, d, sm_scale,
+                                           _p(lse_ref), _p(o), _p(term_prev), _p(mass_prev), _p(slot_prev), k_prev,
+                                           _p(term_out), _p(mass_out), _p(ws) if need else None, need, _stream())
+        _check(rc, "fl_loop_sparse_attn_terms")
+    else:
+        rc = lib.fl_loop_sparse_attn(_p(q_cur), _p(q_prev), _p(k_cache), _p(v_cache), _p(k_new), _p(v_new),
+                                     _p(slot), _p(rows), k, _p(cols), c_list, window, B, N, H, d, sm_scale, 0,
+                                     _p(lse_ref), _p(o), _p(ws) if need else None, need, _stream())
+        _check(rc, "fl_loop_sparse_attn")
     return o, lse_ref
 
 

@@ -1,0 +1,103 @@
+"""The C ABI on the host: the built library loads, exports every function include/flashloop.h declares,
+and rejects bad arguments with the documented status before anything is enqueued (no GPU needed: every
+call here fails host-side validation, and pointers are never dereferenced on the host)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_29812_amd import flashloop as fl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "flashloop.h")
+
+FL_OK, FL_E_NULL, FL_E_SHAPE, FL_E_RANGE, FL_E_UNSUPPORTED, FL_E_WORKSPACE = 0, 1, 2, 3, 4, 5
+DUMMY = ctypes.c_void_p(0x1000)     # a non-NULL device pointer stand-in, never dereferenced on the host
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\**\s*(fl_\w+)\s*\(", text, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(fl.LIB_PATH):
+        from paper_2609_29812_amd import build
+        build.build(verbose=False)
+    return fl.load()
+
+
+def test_library_loads_and_exports_every_declared_function(lib):
+    names = declared_functions()
+    assert len(names) >= 11
+    missing = [n for n in names if not hasattr(lib, n)]
+    assert not missing, missing
+    assert sorted(fl.EXPORTS) == names        # the binding covers exactly the header
+
+
+def test_version_and_status_strings(lib):
+    assert lib.fl_abi_version() == 1
+    for code in range(8):
+        assert lib.fl_status_str(code)
+    assert b"OK" in lib.fl_status_str(FL_OK).upper()
+
+
+def test_workspace_queries(lib):
+    # records: list + compacted updated list per (b, h), every column and every row per batch, a sentinel;
+    # then one count per (b, h)
+    B, N, H, d, k, c, w = 2, 100, 3, 64, 10, 8, 4
+    want = (2 * B * H * c + B * N + B * k + 1) * 8 + B * H * 4
+    assert lib.fl_loop_sparse_attn_ws(B, N, H, d, k, c, w, 0) == want
+    assert lib.fl_loop_sparse_attn_ws(B, N, H, d, N, 0, 0, fl.ATTN_DENSE) == 0
+
+
+def _attn(lib, **kw):
+    a = dict(q_cur=DUMMY, q_prev=DUMMY, k_cache=DUMMY, v_cache=DUMMY, k_new=DUMMY, v_new=DUMMY, slot=DUMMY,
+             rows=DUMMY, k=4, cols=DUMMY, c_list=8, window=4, B=1, N=64, H=2, d=64, scale=0.125, flags=0,
+             lse=DUMMY, o=DUMMY, ws=DUMMY, ws_bytes=1 << 20)
+    a.update(kw)
+    return lib.fl_loop_sparse_attn(a["q_cur"], a["q_prev"], a["k_cache"], a["v_cache"], a["k_new"], a["v_new"],
+                                   a["slot"], a["rows"], a["k"], a["cols"], a["c_list"], a["window"], a["B"], a["N"],
+                                   a["H"], a["d"], a["scale"], a["flags"], a["lse"], a["o"], a["ws"], a["ws_bytes"],
+                                   None)
+
+
+def test_attention_rejects_bad_arguments(lib):
+    assert _attn(lib, flags=8) == FL_E_UNSUPPORTED
+    assert _attn(lib, q_cur=None) == FL_E_NULL
+    assert _attn(lib, d=96) == FL_E_SHAPE
+    assert _attn(lib, N=1 << 20, H=16, d=128) == FL_E_SHAPE      # N * H * d above 2^30
+    assert _attn(lib, scale=0.0) == FL_E_RANGE
+    assert _attn(lib, k=65) == FL_E_RANGE
+    assert _attn(lib, q_prev=None) == FL_E_NULL
+    assert _attn(lib, window=-1) == FL_E_RANGE
+    assert _attn(lib, ws=None) == FL_E_WORKSPACE
+    assert _attn(lib, ws_bytes=16) == FL_E_WORKSPACE
+    assert _attn(lib, flags=fl.ATTN_DENSE, rows=DUMMY, k=64) == FL_E_SHAPE   # dense takes rows == NULL
+    assert b"fl_loop_sparse_attn" in lib.fl_last_error()
+
+
+def test_select_and_codec_reject_bad_arguments(lib):
+    sel = lambda **kw: lib.fl_select_tokens(
+        kw.get("kc", DUMMY), DUMMY, kw.get("vc", DUMMY), DUMMY, 1, 64, kw.get("D", 128), None, 64, kw.get("k", 8),
+        1, 1e-6, DUMMY, DUMMY, DUMMY, None)
+    assert sel(kc=None) == FL_E_NULL
+    assert sel(vc=None) == FL_E_NULL          # one pair half-given
+    assert sel(D=12) == FL_E_SHAPE
+    assert sel(k=65) == FL_E_RANGE
+    assert b"fl_select_tokens" in lib.fl_last_error()
+
+    q = lambda **kw: lib.fl_kv_residual_quant(DUMMY, DUMMY, DUMMY, 8, 1, 64, 2, kw.get("d", 64), kw.get("bits", 4),
+                                              kw.get("G", 32), kw.get("axis", fl.AXIS_TOKEN), DUMMY, DUMMY, DUMMY,
+                                              None, None)
+    assert q(bits=3) == FL_E_UNSUPPORTED
+    assert q(axis=2) == FL_E_UNSUPPORTED
+    assert q(G=48) == FL_E_UNSUPPORTED
+    assert q(d=96) == FL_E_SHAPE
+    assert q(d=64, G=128, axis=fl.AXIS_CHANNEL) == FL_E_SHAPE    # CHANNEL groups must divide d
+    dq = lib.fl_kv_residual_dequant(DUMMY, DUMMY, DUMMY, DUMMY, 8, 1, 64, 2, 64, 4, 32, fl.AXIS_TOKEN, 7, DUMMY,
+                                    None, None)
+    assert dq == FL_E_UNSUPPORTED                                   # unknown mode

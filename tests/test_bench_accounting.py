@@ -1,5 +1,6 @@
-"""Host logic of bench.py: the algorithmic flop and byte counts of one attention launch, checked against
-a brute-force construction of every S_i with the oracle's own set definition."""
+"""Host logic of bench.py: the algorithmic flop and byte counts of one attention launch (both passes, or
+the add pass with stored subtract terms), checked against a brute-force construction of every S_i with the
+oracle's own set definition."""
 import numpy as np
 
 import bench
@@ -15,7 +16,12 @@ def test_attention_work_counts_match_brute_force():
         slot[b, idx[b]] = np.arange(40)
     cols = np.stack([np.stack([np.sort(np.concatenate([np.arange(4), rng.choice(np.arange(4, N), 30, replace=False)]))
                                for _ in range(H)]) for _ in range(B)]).astype(np.int32)
-    nbytes, flops = bench.attn_work(idx, cols, slot, N, H, d, w, B)
+    for reuse in (False, True):
+        check(idx, cols, slot, N, H, d, w, B, reuse)
+
+
+def check(idx, cols, slot, N, H, d, w, B, reuse):
+    nbytes, flops = bench.attn_work(idx, cols, slot, N, H, d, w, B, reuse=reuse, keep_terms=True)
     want_flops = 0
     want_bytes = 0
     for b in range(B):
@@ -23,11 +29,16 @@ def test_attention_work_counts_match_brute_force():
             used = set()
             for i in idx[b]:
                 S = att.row_columns(cols[b, h], int(i), w)
-                want_flops += 8 * d * S.size
+                want_flops += (4 if reuse else 8) * d * S.size
                 used |= set(S.tolist())
             n_new = sum(1 for j in used if slot[b, j] >= 0)
             want_bytes += (len(used) + n_new) * d * 4 + len(used) * 4 + cols.shape[2] * 4
         k = idx.shape[1]
-        want_bytes += k * H * d * 4 + k * H * d * 8 + k * H * 8 + k * 4
+        q_rows = 1 if reuse else 2
+        lse_io = 1 if reuse else 2
+        want_bytes += q_rows * k * H * d * 2 + k * H * d * 8 + lse_io * k * H * 4 + k * 4
+        want_bytes += k * H * d * 4 + k * H * 4                              # terms kept
+        if reuse:
+            want_bytes += k * H * d * 4 + k * H * 4 + k * 4                  # previous terms read
     assert flops == want_flops
     assert nbytes == want_bytes

@@ -238,6 +238,56 @@ def test_sparse_attn_stepwise_from_oracle_state(F, name, over):
         v_hat = codec.reconstruct(v_hat, st.v[r - 1], lr.idx, lr.enc_v, w.bits_at(r), w.group, codec.AXIS_CHANNEL)[0]
 
 
+@pytest.mark.parametrize("name,over", [("C4", dict(seq=2000, heads=2, window=128, col_budget=4 + 128 + 300)),
+                                       ("C5", dict(seq=1200, heads=2, batch=2, col_budget=200)),
+                                       ("C2", dict(seq=900, heads=2, head_dim=64, col_budget=100))])
+def test_reused_subtract_terms_match_recomputed_ones(F, name, over):
+    """Loops >= 3 with the previous loop's add terms as subtract terms against the same loops with the
+    subtract pass recomputed: equal up to fp32 rounding (Eq. 7 with fixed S and nested rows)."""
+    from paper_2609_29812_amd import driver
+    w = get(name).replace(**over)
+    st = make_layer(w)
+    say(f"reuse {w.name} B={w.batch} N={w.seq} H={w.heads} d={w.head_dim} R={w.loops}")
+    dev = {n: [up_bf16(a) for a in getattr(st, n)] for n in "qkv"}
+    runs = []
+    for reuse in (False, True):
+        gs = driver.setup(dev["q"][0], dev["k"][0], dev["v"][0], w.base_bits, w.group, w.n_sink, w.top_cols,
+                          w.window)
+        gs.reuse = reuse
+        outs = []
+        for r in range(2, w.loops + 1):
+            driver.sparse_step(gs, dev["q"][r - 1], dev["q"][r - 2], dev["k"][r - 1], dev["k"][r - 2],
+                               dev["v"][r - 1], dev["v"][r - 2], w.k(r), w.bits_at(r))
+            torch.cuda.synchronize()
+            outs.append((down(gs.o), down(gs.lse), down(gs.cand)))
+        runs.append(outs)
+    for r, (full, reu) in enumerate(zip(*runs), start=2):
+        assert np.array_equal(full[2], reu[2]), f"loop {r} active rows"
+        assert_close(reu[0], full[0], f"loop {r} o: reused vs recomputed subtract terms")
+        assert_close(reu[1], full[1], f"loop {r} lse: reused vs recomputed subtract terms")
+
+
+def test_reuse_leaves_rows_without_a_previous_term_unchanged(F):
+    from paper_2609_29812_amd import driver
+    w = get("C2").replace(seq=600, heads=2, col_budget=80)
+    st = make_layer(w)
+    dev = {n: [up_bf16(a) for a in getattr(st, n)] for n in "qkv"}
+    gs = driver.setup(dev["q"][0], dev["k"][0], dev["v"][0], w.base_bits, w.group, w.n_sink, w.top_cols,
+                      w.window)
+    driver.sparse_step(gs, dev["q"][1], dev["q"][0], dev["k"][1], dev["k"][0], dev["v"][1], dev["v"][0],
+                       w.k(2), w.bits_at(2))
+    torch.cuda.synchronize()
+    dropped = int(down(gs.cand)[0, 3])
+    gs.slot_prev[0, dropped] = -1
+    o_before = down(gs.o)[0, dropped].copy()
+    driver.sparse_step(gs, dev["q"][2], dev["q"][1], dev["k"][2], dev["k"][1], dev["v"][2], dev["v"][1],
+                       w.k(3), w.bits_at(3))
+    torch.cuda.synchronize()
+    assert dropped in down(gs.cand)[0]
+    assert np.array_equal(down(gs.o)[0, dropped], o_before)
+    assert not down(gs.mass)[0, list(down(gs.cand)[0]).index(dropped)].any()
+
+
 def test_all_rows_all_columns_no_quantization_is_dense_attention(F):
     """The special case that reduces the chain to exact dense attention of each loop, on the GPU."""
     from paper_2609_29812_amd import driver
