@@ -4,9 +4,11 @@
 //   with 16-byte loads, forms fp32 differences, accumulates squared norms in fp64, reduces across the
 //   wave and writes the fp32 key.  HBM-bound: 4 * D * 2 bytes per candidate.
 // topk_select: one 1024-thread workgroup per segment.  Keys are mapped to order-preserving uint32 and
-//   held in registers (M per thread); the k-th largest key is found bit by bit from the MSB with block
-//   counts (32 passes, no atomics), then the selected positions are compacted in candidate order with
-//   two block scans, which emits rows ascending and breaks ties by the lower index.
+//   held in registers (M per thread).  The k-th largest key is found in two stages: an LDS histogram
+//   of the top 12 bits and a block scan over its 4096 bins give the bin that holds it; the keys of
+//   that bin are compacted into LDS and the remaining 20 bits are resolved bit by bit from the MSB
+//   with block counts over that (small) set.  The selected positions are then compacted in candidate
+//   order with two block scans, which emits rows ascending and breaks ties by the lower index.
 #include "fl_common.h"
 
 namespace fl {
@@ -98,6 +100,52 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int* scratch /* [16] 
   return before + incl - v;
 }
 
+// hist[bin] += 1 for every lane with want set.  Lanes that share the bin of the first such lane add
+// once, as a count (keys crowd into few bins, and same-address LDS atomics serialize); the others add
+// one by one.
+__device__ __forceinline__ void hist_add(int* hist, uint32_t bin, bool want) {
+  const uint64_t live = __builtin_amdgcn_ballot_w64(want);
+  if (live == 0) return;                                  // uniform
+  const int leader = __builtin_ctzll(live);
+  const uint32_t lb = __shfl(bin, leader, 64);
+  const bool same = want && bin == lb;
+  const uint64_t group = __builtin_amdgcn_ballot_w64(same);
+  if ((int)(threadIdx.x & 63) == leader) atomicAdd(&hist[lb], (int)__builtin_popcountll(group));
+  if (want && !same) atomicAdd(&hist[bin], 1);
+}
+
+// The bin, scanning bins from the highest, where the running count of keys first reaches krem.
+// hist holds nbins counts (nbins <= 4 * kTopkThreads); result in meta[0..2] = (bin, krem left in it,
+// its count).  Block-wide; ends with a barrier.
+__device__ __forceinline__ void find_bin(const int* hist, int nbins, int krem, int* scratch, int* meta) {
+  const int t = threadIdx.x;
+  const int per = nbins > kTopkThreads ? nbins / kTopkThreads : 1;   // 4 or 1
+  int hb[4] = {0, 0, 0, 0}, local = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int bin = nbins - 1 - per * t - q;
+    if (q < per && bin >= 0) {
+      hb[q] = hist[bin];
+      local += hb[q];
+    }
+  }
+  int total;
+  const int above = block_exclusive_scan(local, scratch, &total);
+  if (above < krem && above + local >= krem) {
+    int acc = above;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (q < per && acc < krem && acc + hb[q] >= krem) {
+        meta[0] = nbins - 1 - per * t - q;
+        meta[1] = krem - acc;
+        meta[2] = hb[q];
+      }
+      acc += hb[q];
+    }
+  }
+  __syncthreads();
+}
+
 __device__ __forceinline__ uint32_t orderable(float f) {
   uint32_t u = __float_as_uint(f + 0.0f);   // -0 and +0 are the same key
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
@@ -112,8 +160,14 @@ __global__ __launch_bounds__(kTopkThreads) void topk_select_kernel(
     const int32_t* __restrict__ cand, int64_t cand_stride, int id_base,
     int32_t* __restrict__ out, int64_t out_stride, int n_prefix,
     int32_t* __restrict__ slot, int slot_n) {
+  constexpr int kHistBits = 12, kBins = 1 << kHistBits;
+  static_assert(kBins == 4 * kTopkThreads, "each thread owns four histogram bins");
+  constexpr int kCap = M * kTopkThreads < 32768 ? M * kTopkThreads : 32768;
   __shared__ int red[2 * kTopkWaves];
   __shared__ int scan_scratch[kTopkWaves];
+  __shared__ int hist[kBins];
+  __shared__ uint32_t cbuf[kCap];          // keys of the threshold's bin
+  __shared__ int meta[3];                  // that bin, keys still to take from it, its size
   const int s = blockIdx.x;
   const int t = threadIdx.x;
   const float* kp = keys + (int64_t)s * key_stride;
@@ -133,18 +187,60 @@ __global__ __launch_bounds__(kTopkThreads) void topk_select_kernel(
     u[j] = (p < n) ? orderable(kp[p]) : 0u;
   }
 
-  // k-th largest key, one bit at a time from the MSB
+  // k-th largest key: (1) histogram of the top kHistBits bits and the bin that holds it
   uint32_t prefix = 0, mask = 0;
   int krem = k;
-  if (k > 0) {
-    for (int bit = 31; bit >= 0; --bit) {
-      const uint32_t want = prefix | (1u << bit), m2 = mask | (1u << bit);
-      int cnt = 0;
+  if (k > 0) {                                            // uniform
+    for (int i = t; i < kBins; i += kTopkThreads) hist[i] = 0;
+    __syncthreads();
 #pragma unroll
-      for (int j = 0; j < M; ++j) cnt += ((t * M + j) < n && (u[j] & m2) == want) ? 1 : 0;
-      cnt = block_sum(cnt, red, bit & 1);
-      if (cnt >= krem) prefix = want; else krem -= cnt;
-      mask = m2;
+    for (int j = 0; j < M; ++j) hist_add(hist, u[j] >> (32 - kHistBits), t * M + j < n);
+    __syncthreads();
+    find_bin(hist, kBins, k, scan_scratch, meta);
+    const uint32_t bin = (uint32_t)meta[0];
+    const int cnt = meta[2];
+    krem = meta[1];
+    prefix = bin << (32 - kHistBits);
+    mask = ~0u << (32 - kHistBits);
+    if (cnt <= kCap) {
+      // (2) compact that bin's keys into LDS, then resolve the low 20 bits with digit histograms of
+      // 8, 8 and 4 bits over them
+      int n_in = 0;
+#pragma unroll
+      for (int j = 0; j < M; ++j) n_in += (t * M + j < n && (u[j] >> (32 - kHistBits)) == bin) ? 1 : 0;
+      int tot;
+      int off = block_exclusive_scan(n_in, scan_scratch, &tot);
+#pragma unroll
+      for (int j = 0; j < M; ++j)
+        if (t * M + j < n && (u[j] >> (32 - kHistBits)) == bin) cbuf[off++] = u[j];
+      int shift = 32 - kHistBits;
+      for (int pass = 0; pass < 3; ++pass) {
+        const int nb = pass < 2 ? 8 : 4;
+        shift -= nb;
+        for (int i = t; i < (1 << nb); i += kTopkThreads) hist[i] = 0;
+        __syncthreads();                                  // also orders the compaction writes
+        for (int i0 = 0; i0 < cnt; i0 += kTopkThreads) {
+          const int i = i0 + t;
+          const uint32_t v = i < cnt ? cbuf[i] : 0u;
+          hist_add(hist, (v >> shift) & ((1u << nb) - 1), i < cnt && (v & mask) == prefix);
+        }
+        __syncthreads();
+        find_bin(hist, 1 << nb, krem, scan_scratch, meta);
+        prefix |= (uint32_t)meta[0] << shift;
+        mask |= ((1u << nb) - 1) << shift;
+        krem = meta[1];
+      }
+    } else {
+      // (2b) too many keys in one bin for the LDS buffer: resolve the low bits over the registers
+      for (int bit = 31 - kHistBits; bit >= 0; --bit) {
+        const uint32_t want = prefix | (1u << bit), m2 = mask | (1u << bit);
+        int c = 0;
+#pragma unroll
+        for (int j = 0; j < M; ++j) c += ((t * M + j) < n && (u[j] & m2) == want) ? 1 : 0;
+        c = block_sum(c, red, bit & 1);
+        if (c >= krem) prefix = want; else krem -= c;
+        mask = m2;
+      }
     }
   }
   // krem = how many keys equal to the threshold are taken, lowest positions first

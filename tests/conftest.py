@@ -26,3 +26,11 @@ def pytest_collection_modifyitems(config, items):
     for item in items:
         if "gpu" in item.keywords:
             item.add_marker(skip)
+
+
+@pytest.fixture(scope="module")
+def F():
+    """The HIP library's binding (loaded; raises if the library is missing)."""
+    from paper_2609_29812_amd import flashloop
+    flashloop.load()
+    return flashloop

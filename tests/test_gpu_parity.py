@@ -18,13 +18,6 @@ from workloads import get, make_layer
 pytestmark = pytest.mark.gpu
 
 
-@pytest.fixture(scope="module")
-def F():
-    from paper_2609_29812_amd import flashloop
-    flashloop.load()
-    return flashloop
-
-
 def _bf16(rng, shape, scale=1.0):
     return f32_to_bf16((rng.standard_normal(shape) * scale).astype(np.float32))
 
@@ -286,6 +279,23 @@ def test_reuse_leaves_rows_without_a_previous_term_unchanged(F):
     assert dropped in down(gs.cand)[0]
     assert np.array_equal(down(gs.o)[0, dropped], o_before)
     assert not down(gs.mass)[0, list(down(gs.cand)[0]).index(dropped)].any()
+
+
+@pytest.mark.parametrize("n,kind", [(40004, "equal"), (40004, "few_values"), (40004, "random"),
+                                    (32772, "random"), (1700, "few_values"), (5000, "one_bin")])
+def test_topk_threshold_search_matches_oracle(F, n, kind):
+    """The shared top-k kernel (through fl_select_columns) on large, tied and single-bin key sets: above
+    32K keys a histogram bin can exceed the LDS buffer (register fallback); ties go to lower indices."""
+    rng = np.random.default_rng(n)
+    keys = {"equal": np.full(n, 0.25, np.float32),
+            "few_values": rng.choice(np.float32([0.0, 1e-3, 0.5, 0.5000001, 3.0]), n).astype(np.float32),
+            "random": rng.random(n, dtype=np.float32) ** 3,
+            "one_bin": (1.0 + rng.integers(0, 64, n) * 2.0 ** -20).astype(np.float32)}[kind]
+    say(f"top-k n={n} kind={kind}")
+    for t in (1, 777, (n - 4) // 2, n - 4):
+        got = down(F.select_columns(up(keys[None, None, :]), 4, t))[0, 0]
+        want = att.select_columns(keys, 4, t)
+        assert np.array_equal(got, want), f"n={n} kind={kind} t={t}"
 
 
 def test_all_rows_all_columns_no_quantization_is_dense_attention(F):
