@@ -680,20 +680,22 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
 //   [off_rows + b*k, ... + k)         the updated rows of batch b: (rows[p], p)
 //   off_sent                          sentinel (kPad, -1)
 // followed by n_upd[B*H].  Blocks [0, B*H) build the lists, the remaining ones the per-batch regions.
-__global__ __launch_bounds__(256) void attn_prep_kernel(const int32_t* __restrict__ cols,
+constexpr int kPrepThreads = 1024;
+__global__ __launch_bounds__(kPrepThreads) void attn_prep_kernel(const int32_t* __restrict__ cols,
                                                         const int32_t* __restrict__ slot,
                                                         const int32_t* __restrict__ rows, int c_list,
                                                         int N, int H, int B, int k, int per_batch,
                                                         int off_upd, int off_band, int off_rows, int off_sent,
                                                         int2* __restrict__ rec, int32_t* __restrict__ n_upd) {
-  __shared__ int wsum[4];
+  constexpr int kWaves = kPrepThreads / 64;
+  __shared__ int wsum[kWaves];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if ((int)blockIdx.x >= B * H) {
     const int e = blockIdx.x - B * H;
     const int b = e / per_batch, part = e % per_batch;
-    for (int j = part * 256 + tid; j < N; j += per_batch * 256)
+    for (int j = part * kPrepThreads + tid; j < N; j += per_batch * kPrepThreads)
       rec[off_band + (int64_t)b * N + j] = make_int2(j, slot[(int64_t)b * N + j]);
-    for (int p = part * 256 + tid; p < k; p += per_batch * 256)
+    for (int p = part * kPrepThreads + tid; p < k; p += per_batch * kPrepThreads)
       rec[off_rows + (int64_t)b * k + p] = make_int2(rows[(int64_t)b * k + p], p);
     if (e == 0 && tid == 0) rec[off_sent] = make_int2(kPad, -1);
     return;
@@ -703,7 +705,7 @@ __global__ __launch_bounds__(256) void attn_prep_kernel(const int32_t* __restric
   int2* dp = rec + (int64_t)bh * c_list;
   int2* up = rec + off_upd + (int64_t)bh * c_list;
   int base = 0;
-  for (int p0 = 0; p0 < c_list; p0 += 256) {
+  for (int p0 = 0; p0 < c_list; p0 += kPrepThreads) {
     const int pos = p0 + tid;
     int cid = -1, s = -1;
     if (pos < c_list) {
@@ -723,7 +725,7 @@ __global__ __launch_bounds__(256) void attn_prep_kernel(const int32_t* __restric
     __syncthreads();
     int before = 0, total = 0;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
+    for (int w = 0; w < kWaves; ++w) {
       before += (w < wave) ? wsum[w] : 0;
       total += wsum[w];
     }
@@ -841,8 +843,8 @@ static int loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev, const
     a.off_rows = (int)L.off_rows;
     a.off_sent = (int)L.off_sent;
     a.rec_bytes = (uint32_t)(L.n_rec * sizeof(int2));
-    const int per_batch = std::min(256, (N + k + 1023) / 1024);
-    attn_prep_kernel<<<B * H + B * per_batch, 256, 0, st>>>(cols, slot, rows, c_list, N, H, B, k, per_batch,
+    const int per_batch = std::min(64, (N + k + 4 * kPrepThreads - 1) / (4 * kPrepThreads));
+    attn_prep_kernel<<<B * H + B * per_batch, kPrepThreads, 0, st>>>(cols, slot, rows, c_list, N, H, B, k, per_batch,
                                                           a.off_upd, a.off_band, a.off_rows, a.off_sent, rec,
                                                           n_upd);
     int rc = check_launch("attn_prep_kernel");

@@ -86,22 +86,23 @@ __device__ __forceinline__ void group_meta(float mn, float mx, int qmax, double&
 }
 
 // ---- keys: per-channel groups along packed rows ----------------------------------------------------
-constexpr int kTokSlices = 8;
-constexpr int kTokChunks = 32;      // 32 threads x 8 channels = 256 channels per workgroup
+// A workgroup of 256 threads = S row slices x CH chunks of 8 channels; each slice holds RPS = G/S rows.
+// S = min(G, 32), so a group of 64 rows spreads over 32 slices and a workgroup covers 64 channels.
 
-template <int BITS, int RPS>
-__global__ __launch_bounds__(kTokSlices * kTokChunks) void quant_token_kernel(
+template <int BITS, int S, int RPS>
+__global__ __launch_bounds__(256) void quant_token_kernel(
     const uint16_t* __restrict__ x_cur, const uint16_t* __restrict__ x_ref,
     const int32_t* __restrict__ idx, int k, int N, int HD, int G, uint8_t* __restrict__ codes,
     uint16_t* __restrict__ scale, uint16_t* __restrict__ zero, uint16_t* __restrict__ out_rows) {
-  __shared__ float s_mn[kTokSlices][kTokChunks * 8];
-  __shared__ float s_mx[kTokSlices][kTokChunks * 8];
-  __shared__ float s_z[kTokChunks * 8];
-  __shared__ float s_s[kTokChunks * 8];
+  constexpr int CH = 256 / S;          // chunks of 8 channels per workgroup
+  __shared__ float s_mn[S][CH * 8];
+  __shared__ float s_mx[S][CH * 8];
+  __shared__ float s_z[CH * 8];
+  __shared__ float s_s[CH * 8];
   constexpr int qmax = (1 << BITS) - 1;
-  const int slice = threadIdx.x / kTokChunks, chunk = threadIdx.x % kTokChunks;
+  const int slice = threadIdx.x / CH, chunk = threadIdx.x % CH;
   const int g = blockIdx.y, b = blockIdx.z;
-  const int c0 = blockIdx.x * (kTokChunks * 8) + chunk * 8;
+  const int c0 = blockIdx.x * (CH * 8) + chunk * 8;
   const bool ch_ok = c0 < HD;
   const int ng = (k + G - 1) / G;
 
@@ -137,12 +138,12 @@ __global__ __launch_bounds__(kTokSlices * kTokChunks) void quant_token_kernel(
     s_mx[slice][chunk * 8 + t] = mx[t];
   }
   __syncthreads();
-  {
-    const int ch = threadIdx.x;   // 256 threads, one channel each
-    const int c = blockIdx.x * (kTokChunks * 8) + ch;
+  if (threadIdx.x < CH * 8) {
+    const int ch = threadIdx.x;   // one thread per channel
+    const int c = blockIdx.x * (CH * 8) + ch;
     float a = INFINITY, bb = -INFINITY;
 #pragma unroll
-    for (int sl = 0; sl < kTokSlices; ++sl) {
+    for (int sl = 0; sl < S; ++sl) {
       a = fminf(a, s_mn[sl][ch]);
       bb = fmaxf(bb, s_mx[sl][ch]);
     }
@@ -360,17 +361,19 @@ extern "C" int fl_kv_residual_quant(const uint16_t* x_cur, const uint16_t* x_ref
     return check_launch("passthrough_kernel");
   }
   if (axis == FL_AXIS_TOKEN) {
-    dim3 grid((HD + 255) / 256, (k + group - 1) / group, B);
-#define FL_QT(BB, RR)                                                                          \
-  quant_token_kernel<BB, RR><<<grid, 256, 0, st>>>(x_cur, x_ref, idx, k, N, HD, group, codes, \
-                                                   scale, zero, out_rows)
+    const int slices = group < 32 ? group : 32;
+    const int cw = 256 / slices * 8;                      // channels per workgroup
+    dim3 grid((HD + cw - 1) / cw, (k + group - 1) / group, B);
+#define FL_QT(BB, SS, RR)                                                                          \
+  quant_token_kernel<BB, SS, RR><<<grid, 256, 0, st>>>(x_cur, x_ref, idx, k, N, HD, group, codes, \
+                                                       scale, zero, out_rows)
 #define FL_QT_BITS(BB)                                   \
-  switch (group / 8) {                                   \
-    case 1: FL_QT(BB, 1); break;                         \
-    case 2: FL_QT(BB, 2); break;                         \
-    case 4: FL_QT(BB, 4); break;                         \
-    case 8: FL_QT(BB, 8); break;                         \
-    default: FL_QT(BB, 16); break;                       \
+  switch (group) {                                       \
+    case 8: FL_QT(BB, 8, 1); break;                      \
+    case 16: FL_QT(BB, 16, 1); break;                    \
+    case 32: FL_QT(BB, 32, 1); break;                    \
+    case 64: FL_QT(BB, 32, 2); break;                    \
+    default: FL_QT(BB, 32, 4); break;                    \
   }
     if (bits == 2) { FL_QT_BITS(2) } else if (bits == 4) { FL_QT_BITS(4) } else { FL_QT_BITS(8) }
 #undef FL_QT_BITS
