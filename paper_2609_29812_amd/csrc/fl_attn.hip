@@ -15,7 +15,9 @@
 // Work decomposition.  A workgroup of 4 waves takes consecutive updated rows of one (batch, head): 64
 // rows in the sparse update, where waves 0-1 run the subtract pass and waves 2-3 the add pass for the
 // same two groups of 32 rows, and 128 rows in the dense loop, where every wave runs the softmax pass.
-// The row tiles of one (batch, head) map to one XCD so its list columns stay in that XCD's L2.
+// When the subtract term is the previous loop's stored add term (loops >= 3), reuse_attn_kernel runs the
+// add pass alone with one 16-row group per wave.  The row tiles of one (batch, head) map to one XCD so
+// its list columns stay in that XCD's L2.
 //
 // Data movement.  Column tiles of 32 are gathered straight from HBM into a ring of 4 LDS slots with
 // buffer_load ... lds (no registers), three tiles ahead of the one being computed; out-of-range offsets
@@ -29,6 +31,7 @@
 #include "fl_common.h"
 
 #include <climits>
+#include <type_traits>
 
 namespace fl {
 
@@ -111,15 +114,12 @@ struct Slot {
 __device__ __forceinline__ int swz_f(int c) { return ((c & 3) << 1) | ((c >> 2) & 1); }
 __device__ __forceinline__ int swz(int c, int ch) { return ch ^ swz_f(c); }
 
-// MODE: kDense (loop 1, every row over all causal columns), kFull (subtract and add passes), kReuse (the
-// subtract term is the previous loop's stored add term; the two spare waves of each row group take half
-// of every tile's columns).
-constexpr int kDense = 0, kFull = 1, kReuse = 2;
+// MODE: kDense (loop 1, every row over all causal columns) or kFull (a sparse loop with both passes).
+constexpr int kDense = 0, kFull = 1;
 
 template <int D, int MODE>
 __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
   constexpr bool DENSE = MODE == kDense;
-  constexpr bool REUSE = MODE == kReuse;
   constexpr int GROUPS = DENSE ? 4 : 2;
   constexpr int BM = 32 * GROUPS;
   constexpr int KS = D / 16;              // k-steps of QK^T
@@ -129,14 +129,13 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
   constexpr int INST_PER_TILE = kBN / COLS_PER_INST;
   constexpr int INST_PER_WAVE = INST_PER_TILE / 4;   // per tensor (K and V each)
   __shared__ Slot<D> s0, s1, s2, s3;
-  // column ids of tile v in entry v % 8 (kPad = padding).  Dense and full modes: view 0 plain (dense
-  // loop, subtract pass), view 1 for the add pass, where the columns updated this loop are padding in
-  // phases A/B.  Reuse mode: view h holds the add view rotated by 16h columns, for the waves of half h.
+  // column ids of tile v in entry v % 8 (kPad = padding): view 0 plain (dense loop, subtract pass), view 1
+  // for the add pass, where the columns updated this loop are padding in phases A/B.
   __shared__ int tcv[2][8][kBN];
   __shared__ uint32_t toff[8][kBN];       // byte offset of each column's row in its source (kOOB: none)
   // tile v: first and last (plain) column id, whether some column was updated this loop (phases A/B)
   __shared__ int thd[8][4];
-  __shared__ float xm[2][2][64];          // end-of-loop hand-off per group: sum or mass, running max
+  __shared__ float xm[2][64];             // end-of-loop hand-off per group: the subtract pass's mass
   __shared__ int s_meta[2];
 
   const int tid = threadIdx.x;
@@ -145,7 +144,6 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
   const int r32 = lane & 31;
   const int group = wave % GROUPS;
   const bool add_pass = MODE != kFull || wave >= 2;
-  const int half = REUSE ? __builtin_amdgcn_readfirstlane(wave) >> 1 : 0;   // reuse: columns 16*half .. +15
 
   // work item -> (batch*head, row tile); the row tiles of one (batch, head) stay on one XCD
   const int n_rt = (a.k + BM - 1) / BM;
@@ -280,8 +278,8 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
     const bool valid = cid != kPad;
     if (lane < kBN) {
       const int cid_add = upd ? kPad : cid;
-      tcv[0][v & 7][c32] = REUSE ? cid_add : cid;
-      tcv[1][v & 7][REUSE ? (c32 + 16) & 31 : c32] = cid_add;
+      tcv[0][v & 7][c32] = cid;
+      tcv[1][v & 7][c32] = cid_add;
       if (c32 == 0) thd[v & 7][0] = cid;
       if (c32 == kBN - 1) thd[v & 7][1] = cid;
       toff[v & 7][c32] = valid ? (uint32_t)row * rb + head_off : kOOB;
@@ -401,8 +399,7 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
 #pragma unroll
     for (int m = 0; m < 4; ++m) koff[m] = r32 * D + ((2 * m + hw) ^ swz_f(r32)) * 8;
 #pragma unroll
-    for (int e = 0; e < 2; ++e)            // (+ 16 columns for the reuse mode's second-half waves)
-      voff[e] = (col0 + 16 * half) * D + ((4 * e + c_lo) ^ swz_f(col0)) * 8 + 4 * (q & 1);
+    for (int e = 0; e < 2; ++e) voff[e] = col0 * D + ((4 * e + c_lo) ^ swz_f(col0)) * 8 + 4 * (q & 1);
   }
 
   // first and last column id of tile u and whether it holds an updated column (uniform; read ahead of
@@ -439,18 +436,12 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
       const u32x4 kw = *reinterpret_cast<const u32x4*>(&sl.k[koff[ks & 3] + 64 * (ks >> 2)]);
       s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kw), qf[ks], s, 0, 0, 0);
     }
-    // masks, softmax and O^T += V^T P^T over the lane's first NE elements, fp16 operands.  In the reuse
-    // mode every wave takes one 16-column half of the tile: the second half's scores move down first,
-    // and its column ids (the rotated table view) and V rows (voff) are those of the second half.
-    constexpr int NE = REUSE ? 8 : 16;
-    if (REUSE && half != 0) {              // uniform
-#pragma unroll
-      for (int v = 0; v < 8; ++v) s[v] = s[v + 8];
-    }
+    // masks, softmax and O^T += V^T P^T over the lane's 16 elements, fp16 operands
+    constexpr int NE = 16;
     if (!full) {
       // column masks: list columns need j + window <= i, band columns i - window < j <= i (any j <= i in
       // the dense loop); padding and, for the add pass, the columns updated this loop carry kPad
-      const int view = REUSE ? half : (!DENSE && add_pass) ? 1 : 0;
+      const int view = (!DENSE && add_pass) ? 1 : 0;
       int cc[16];
 #pragma unroll
       for (int j = 0; j < NE / 4; ++j) {
@@ -572,44 +563,22 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
   // the two half-waves hold disjoint columns of the same row
   lsum = xor32_add(lsum);
   msub = xor32_add(msub);
-  // hand-off through the idle ring: group g uses slot g (D * 128 bytes >= 32 rows x D floats).  The full
-  // mode's subtract waves hand over (sub, m); the reuse mode's second-half waves hand over their
-  // (acc, running max, sum), which the first-half waves merge into theirs.
+  // hand-off through the idle ring: group g uses slot g (D * 128 bytes >= 32 rows x D floats); the
+  // subtract waves hand their term and mass to the add waves of the same rows
   float4* xacc = reinterpret_cast<float4*>(group == 0 ? &s0 : &s1);
   if constexpr (!DENSE) {
-    const bool giver = REUSE ? half == 1 : !add_pass;
-    if (giver) {
+    if (!add_pass) {
 #pragma unroll
       for (int db = 0; db < DB; ++db)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
           xacc[(db * 4 + j) * 64 + lane] =
               make_float4(acc[db][4 * j], acc[db][4 * j + 1], acc[db][4 * j + 2], acc[db][4 * j + 3]);
-      xm[group][0][lane] = REUSE ? lsum : msub;
-      if (REUSE) xm[group][1][lane] = run_max;
+      xm[group][lane] = msub;
     }
     lds_barrier();
-    if (giver) return;
-    if constexpr (REUSE) {
-      const float m1 = xm[group][1][lane], l1 = xm[group][0][lane];
-      const float mm = fmaxf(run_max, m1);
-      const float a0 = mm == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(run_max - mm);
-      const float a1 = mm == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m1 - mm);
-#pragma unroll
-      for (int db = 0; db < DB; ++db)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const float4 x = xacc[(db * 4 + j) * 64 + lane];
-          acc[db][4 * j + 0] = acc[db][4 * j + 0] * a0 + x.x * a1;
-          acc[db][4 * j + 1] = acc[db][4 * j + 1] * a0 + x.y * a1;
-          acc[db][4 * j + 2] = acc[db][4 * j + 2] * a0 + x.z * a1;
-          acc[db][4 * j + 3] = acc[db][4 * j + 3] * a0 + x.w * a1;
-        }
-      lsum = lsum * a0 + l1 * a1;
-      run_max = mm;
-    } else {
-      msub = xm[group][0][lane];
-    }
+    if (!add_pass) return;
+    msub = xm[group][lane];
   }
   if (!row_ok) return;
   const int64_t orow = ((int64_t)b * a.N + row_i) * HD + (int64_t)h * D;
@@ -628,14 +597,6 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
       }
     if (hw == 0) a.lse_ref[lrow] = (run_max + log2f(lsum)) * 0.6931471805599453f;
   } else {
-    // the subtract term: recomputed (full) or the previous loop's add term of this row (reuse)
-    const float* subp = nullptr;
-    if constexpr (REUSE) {
-      const int pp = a.slot_prev[(int64_t)b * a.N + row_i];
-      const int64_t tp = ((int64_t)b * a.k_prev + pp) * a.H + h;
-      msub = pp >= 0 ? a.mass_prev[tp] : 0.0f;
-      subp = a.term_prev + tp * D;
-    }
     const int64_t trow = ((int64_t)b * a.k + p) * a.H + h;
     const bool keep = a.term_out != nullptr;
     if (!(msub > 0.0f) || !(lsum > 0.0f)) {     // empty column set or vanished mass: unchanged
@@ -655,7 +616,7 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int dim = db * 32 + 8 * j + 4 * hw;
-        const float4 sub = REUSE ? *reinterpret_cast<const float4*>(subp + dim) : xacc[(db * 4 + j) * 64 + lane];
+        const float4 sub = xacc[(db * 4 + j) * 64 + lane];
         const float4 add = make_float4(acc[db][4 * j + 0] * f, acc[db][4 * j + 1] * f,
                                        acc[db][4 * j + 2] * f, acc[db][4 * j + 3] * f);
         float4 prev = *reinterpret_cast<const float4*>(a.o + orow + dim);
@@ -670,6 +631,435 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
       a.lse_ref[lrow] = (run_max + log2f(lsum)) * 0.6931471805599453f - logf(msub);
       if (keep) a.mass_out[trow] = msub;
     }
+  }
+}
+
+// ---- sparse update with the previous loop's add term as the subtract term (loops >= 3) -----------------
+// Only the add pass remains.  A workgroup of 4 waves takes 64 consecutive updated rows of one (batch,
+// head) and wave w owns rows 16w .. 16w+15, so every wave does the same kind of work and a wave's band is
+// that of 16 rows (the 32-row groups of loop_attn_kernel would need two waves per group here and compute
+// S twice).  The tiles, records and LDS pipeline are those of loop_attn_kernel.  The contractions use
+// v_mfma_f32_16x16x32: S^T = K Q^T per 16-column block leaves lane (j, g) = (lane % 16,
+// lane / 16) with columns 16c + 4g .. +3 of row j, which is exactly the B-operand layout of
+// O^T += V^T P^T when the k order of a 32-column tile is (4g .. 4g+3, 16+4g .. 16+4g+3) for lane group
+// g; the transposed V reads follow that order.  The accumulators of a lane belong to the same row j,
+// so the softmax state never leaves the lane (row reductions are two cross-row swaps).
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float xor16_max(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float xor16_add(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+// max / sum over the four 16-lane rows of the wave (the lanes that hold one query row)
+__device__ __forceinline__ float row4_max(float x) { return xor32_max(xor16_max(x)); }
+__device__ __forceinline__ float row4_add(float x) { return xor32_add(xor16_add(x)); }
+
+template <int D>
+__global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
+  constexpr int BM = 64;                  // rows per workgroup (4 waves x 16)
+  constexpr int KS = D / 32;              // k-steps of QK^T (32 dims each)
+  constexpr int DB = D / 16;              // 16-dim output blocks
+  constexpr int CH = D / 8;               // 16-byte chunks per row
+  constexpr int COLS_PER_INST = 64 / CH;  // rows covered by one 1 KB LDS-DMA instruction
+  constexpr int INST_PER_TILE = kBN / COLS_PER_INST;
+  constexpr int INST_PER_WAVE = INST_PER_TILE / 4;   // per tensor (K and V each)
+  constexpr int NI = 2 * INST_PER_WAVE;
+  __shared__ Slot<D> s0, s1, s2, s3;
+  // column ids of tile v in entry v % 8 for the add pass (kPad = padding; in phases A/B the columns
+  // updated this loop are padding too)
+  __shared__ int tcv[8][kBN];
+  __shared__ uint32_t toff[8][kBN];       // byte offset of each column's row in its source (kOOB: none)
+  __shared__ int thd[8][4];               // tile v: first and last column id, any column updated
+  __shared__ int s_meta[2];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int j16 = lane & 15, g4 = lane >> 4;
+
+  // work item -> (batch*head, row tile); the row tiles of one (batch, head) stay on one XCD
+  const int n_rt = (a.k + BM - 1) / BM;
+  const int n_bh = a.B * a.H;
+  int bh, rt;
+  if ((n_bh & 7) == 0) {
+    const int g = blockIdx.x & 7, s = blockIdx.x >> 3;
+    bh = g + 8 * (s / n_rt);
+    rt = n_rt - 1 - (s % n_rt);
+  } else {
+    bh = blockIdx.x / n_rt;
+    rt = n_rt - 1 - (blockIdx.x % n_rt);
+  }
+  const int b = bh / a.H, h = bh % a.H;
+  const int64_t HD = (int64_t)a.H * D;
+  const int32_t* rowp = a.rows + (int64_t)b * a.k;
+
+  const int p0 = rt * BM;
+  const int last_p = min(p0 + BM, a.k) - 1;
+  const int min_row = rowp[p0], max_row = rowp[last_p];
+  const int gp0 = p0 + 16 * wave;
+  const bool group_has_rows = gp0 < a.k;
+  const int gmin = group_has_rows ? rowp[gp0] : 0;
+  const int gmax = group_has_rows ? rowp[min(gp0 + 16, a.k) - 1] : -1;
+  const int p = gp0 + j16;
+  const bool row_ok = p < a.k;
+  const int row_i = row_ok ? rowp[p] : -1;
+
+  // query fragments (B operand of S^T = K Q^T): row j16, dims 32 ks + 8 g4 .. +7
+  bf16x8 qa[KS];
+  {
+    const int64_t qoff = ((int64_t)b * a.N + (row_ok ? row_i : 0)) * HD + (int64_t)h * D + g4 * 8;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const uint4 w = row_ok ? *reinterpret_cast<const uint4*>(a.q_cur + qoff + ks * 32) : make_uint4(0, 0, 0, 0);
+      qa[ks] = __builtin_bit_cast(bf16x8, w);
+    }
+  }
+
+  // ---- phase extents (uniform) ----------------------------------------------------------------------
+  const int recA = bh * a.c_list;
+  const int recC = a.off_upd + bh * a.c_list;
+  const int recB = a.off_band + b * a.N;
+  const int recD = a.off_rows + b * a.k;
+  const int2* descp = a.rec + recA;
+  const int2* updp = a.rec + recC;
+  if (tid < 2) {
+    int n = 0;
+    if (a.c_list > 0) {
+      // tid 0: list entries with j + window <= max_row; tid 1: the same among the updated entries
+      const int2* lp = tid == 0 ? descp : updp;
+      const int len = tid == 0 ? a.c_list : a.n_upd[(int64_t)b * a.H + h];
+      const int lim = max_row - a.window;
+      int lo = 0, hi = len;
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (lp[mid].x <= lim) lo = mid + 1; else hi = mid;
+      }
+      n = lo;
+    }
+    s_meta[tid] = n;
+  }
+  const int bandLo = a.window > 0 ? max(0, min_row - a.window + 1) : 0;
+  const int bandHi = a.window > 0 ? max_row : -1;
+  int pa = 0, pb = 0;
+  if (a.window > 0) {
+    int lo = 0, hi = a.k;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (rowp[mid] < bandLo) lo = mid + 1; else hi = mid;
+    }
+    pa = lo;
+    pb = last_p + 1;
+  }
+  __syncthreads();
+  const int nA = s_meta[0];
+  const int nC = s_meta[1];
+  const int tA = (nA + kBN - 1) / kBN;
+  const int tB = bandHi >= bandLo ? (bandHi - bandLo + kBN) / kBN : 0;
+  const int tC = (nC + kBN - 1) / kBN;
+  const int tD = (pb - pa + kBN - 1) / kBN;
+  const int n_old = tA + tB;
+  const int n_tiles = n_old + tC + tD;
+
+  // ---- tile descriptors (records as in the four-phase layout; see attn_prep_kernel) -----------------
+  const int c32 = lane & 31;
+  const rsrc_t recR = make_rsrc(a.rec, a.rec_bytes);
+  const uint32_t sentinel = (uint32_t)a.off_sent * 8u;
+  auto load_desc = [=](int v) -> u32x2 {
+    const bool inA = v < tA, inB = v < n_old, inC = v < n_old + tC;   // uniform
+    const int start = inA ? 0 : inB ? tA : inC ? n_old : n_old + tC;
+    const int base = inA ? recA : inB ? recB + bandLo : inC ? recC : recD + pa;
+    const int cnt = inA ? nA : inB ? bandHi - bandLo + 1 : inC ? nC : pb - pa;
+    const int i = (v - start) * kBN + c32;
+    const uint32_t off = lane >= kBN ? kOOB : i < cnt ? (uint32_t)(base + i) * 8u : sentinel;
+    return __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(recR, off, 0, 0));
+  };
+  const uint32_t rb = (uint32_t)(HD * 2);
+  const uint32_t head_off = (uint32_t)(h * D * 2);
+  const rsrc_t kcR = make_rsrc(a.k_cache + (int64_t)b * a.N * HD, (uint32_t)a.N * rb);
+  const rsrc_t vcR = make_rsrc(a.v_cache + (int64_t)b * a.N * HD, (uint32_t)a.N * rb);
+  const rsrc_t knR = make_rsrc(a.k_new + (int64_t)b * a.k * HD, (uint32_t)a.k * rb);
+  const rsrc_t vnR = make_rsrc(a.v_new + (int64_t)b * a.k * HD, (uint32_t)a.k * rb);
+
+  auto store_desc = [=](int v, u32x2 w) {
+    const bool newer = v >= n_old;
+    const int cid = (int)w[0];
+    const int aux = (int)w[1];
+    const bool upd = !newer && aux >= 0;   // updated this loop but staged from the cache
+    const int row = newer ? aux : cid;
+    const bool valid = cid != kPad;
+    if (lane < kBN) {
+      tcv[v & 7][c32] = upd ? kPad : cid;
+      if (c32 == 0) thd[v & 7][0] = cid;
+      if (c32 == kBN - 1) thd[v & 7][1] = cid;
+      toff[v & 7][c32] = valid ? (uint32_t)row * rb + head_off : kOOB;
+    }
+    const uint64_t any = __builtin_amdgcn_ballot_w64(lane < kBN && valid && upd);
+    if (lane == 0) thd[v & 7][2] = any != 0;
+  };
+
+  // LDS-DMA plan: every wave issues INST_PER_WAVE K and INST_PER_WAVE V one-kilobyte instructions per
+  // tile (row block inst_of(t) of the tile), always; padding and tiles past the end load nothing
+  auto inst_of = [=](int t) { return wave * INST_PER_WAVE + (t % INST_PER_WAVE); };
+  struct Offs { uint32_t o[NI]; };
+  auto tile_offs = [=](int u) {
+    Offs r;
+#pragma unroll
+    for (int t = 0; t < NI; ++t) {
+      const int c = inst_of(t) * COLS_PER_INST + lane / CH;
+      r.o[t] = toff[u & 7][c] + (uint32_t)swz(c, lane % CH) * 16;   // kOOB + 240 is still out of range
+    }
+    return r;
+  };
+  // (each offset goes through a local: handing the struct member straight to the builtin makes the
+  // host compilation drop the kernel's launch stub)
+  auto issue = [=](int u, Slot<D>& sl, const Offs& of) {
+    if (u >= n_old) {                     // uniform: one of two scalar branches, same op count
+#pragma unroll
+      for (int t = 0; t < NI; ++t) {
+        const int inst = inst_of(t);
+        const uint32_t off = of.o[t];
+        if (t < INST_PER_WAVE)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(knR, FL_LDS(sl.k + inst * 512), 16, off, 0, 0, 0);
+        else
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(vnR, FL_LDS(sl.v + inst * 512), 16, off, 0, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int t = 0; t < NI; ++t) {
+        const int inst = inst_of(t);
+        const uint32_t off = of.o[t];
+        if (t < INST_PER_WAVE)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(kcR, FL_LDS(sl.k + inst * 512), 16, off, 0, 0, 0);
+        else
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(vcR, FL_LDS(sl.v + inst * 512), 16, off, 0, 0, 0);
+      }
+    }
+  };
+  // each wave converts, in place, the V rows its own LDS-DMA wrote (bf16 -> fp16, exact for |v| in
+  // [2^-14, 65504]); the barrier that follows publishes them
+  auto convert_v = [=](Slot<D>& sl) {
+    u32x4 w[INST_PER_WAVE];
+#pragma unroll
+    for (int t = 0; t < INST_PER_WAVE; ++t)
+      w[t] = *reinterpret_cast<const u32x4*>(sl.v + inst_of(t) * 512 + lane * 8);
+#pragma unroll
+    for (int t = 0; t < INST_PER_WAVE; ++t) {
+      u32x4 hv;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        hv[e] = pack_f16x2(__uint_as_float(w[t][e] << 16), __uint_as_float(w[t][e] & 0xFFFF0000u));
+      *reinterpret_cast<u32x4*>(sl.v + inst_of(t) * 512 + lane * 8) = hv;
+    }
+  };
+
+  // LDS read offsets (elements) that depend on the lane.  K (A operand): row j16 (+16 for the second
+  // column block), chunk 4 ks + g4 = 8 (ks >> 1) + (4 (ks & 1) + g4).  V (transposed reads): lane
+  // (g4, t, q) points at dims 16 db + 4q of column 4 g4 + t (+16 for the second half of the k order);
+  // chunk 2 db + (q >> 1) = 8 (db >> 2) + (2 (db & 3) + (q >> 1)).  The swizzle permutes only the low
+  // three bits of a chunk index and depends on the column mod 8.
+  int koff[2], voff[4];
+  {
+    const int t4 = j16 >> 2, q = lane & 3;
+    const int colv = 4 * g4 + t4;
+#pragma unroll
+    for (int e = 0; e < 2; ++e) koff[e] = j16 * D + ((4 * e + g4) ^ swz_f(j16)) * 8;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) voff[e] = colv * D + ((2 * e + (q >> 1)) ^ swz_f(colv)) * 8 + 4 * (q & 1);
+  }
+
+  f32x4 acc[DB];                          // add term, O^T blocks
+#pragma unroll
+  for (int db = 0; db < DB; ++db) acc[db] = f32x4{};
+  float run_max = -INFINITY, lsum = 0.0f;   // add pass: running reference (log2 units) and row sum
+
+  struct TileHead { int c0, clast, any; };
+  auto tile_head = [=](int u) { return TileHead{thd[u & 7][0], thd[u & 7][1], thd[u & 7][2]}; };
+
+  // column mask of the lane's 8 entries (ids cc, columns 16c + 4 g4 + v): list columns need
+  // j + window <= i, band columns i - window < j <= i; padding and the columns updated this loop (in the
+  // cache tiles) carry kPad
+  auto apply_mask = [=](f32x4 (&s)[2], const int4 (&cc)[2], bool is_list) {
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const int ci[4] = {cc[c].x, cc[c].y, cc[c].z, cc[c].w};
+      if (is_list) {
+        const int lim = row_i - a.window;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) s[c][v] = ci[v] <= lim ? s[c][v] : -INFINITY;
+      } else {
+        const uint32_t w = (uint32_t)a.window;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) s[c][v] = (uint32_t)row_i - (uint32_t)ci[v] < w ? s[c][v] : -INFINITY;
+      }
+    }
+  };
+
+  auto compute = [=, &acc, &run_max, &lsum](int u, const Slot<D>& sl, const TileHead& th) {
+    const int ri = u & 7;
+    const bool newer = u >= n_old;
+    const bool is_list = u < tA || (newer && u < n_old + tC);
+    // does any row of this wave's group see any column of this tile, and do all rows see all of it?
+    // (column ids ascend within a tile and padding, kPad, sits at the end)
+    const int c0 = th.c0, clast = th.clast;
+    bool active, full;
+    if (is_list) {
+      active = group_has_rows && c0 <= gmax - a.window;
+      full = clast <= gmin - a.window;
+    } else {
+      const int t_hi = clast != kPad ? clast : bandHi;
+      active = group_has_rows && c0 <= gmax && t_hi > gmin - a.window;
+      full = clast <= gmin && c0 > gmax - a.window;
+    }
+    if (!active) return;
+    if (!newer && th.any) full = false;    // updated columns drop out of the cache tiles
+    // every LDS read of the tile first, unconditionally (column ids, K and V fragments): a read under a
+    // branch can lose the information that tells it apart from the pending LDS-DMA writes
+    int4 ca_[2];
+#pragma unroll
+    for (int c = 0; c < 2; ++c) ca_[c] = *reinterpret_cast<const int4*>(&tcv[ri][16 * c + 4 * g4]);
+    u32x4 kw[KS][2];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+        kw[ks][c] = *reinterpret_cast<const u32x4*>(&sl.k[koff[ks & 1] + 16 * c * D + 64 * (ks >> 1)]);
+    i16x4 vr[DB][2];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const int o = voff[db & 3] + 64 * (db >> 2);
+      vr[db][0] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(FL_LDS4(&sl.v[o]));
+      vr[db][1] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(FL_LDS4(&sl.v[o + 16 * D]));
+    }
+    // S^T = K Q^T per 16-column block c: lane holds columns 16c + 4 g4 + v of row j16
+    f32x4 sa[2] = {f32x4{}, f32x4{}};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+        sa[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kw[ks][c]), qa[ks], sa[c], 0, 0, 0);
+    // online softmax with a lazily raised reference (it moves only when a score exceeds it by more than 8
+    // in log2 units, so probabilities stay <= 256 and rescaling is rare)
+    if (!full) apply_mask(sa, ca_, is_list);
+    float tmax = fmaxf(fmaxf(fmaxf(sa[0][0], sa[0][1]), fmaxf(sa[0][2], sa[0][3])),
+                       fmaxf(fmaxf(sa[1][0], sa[1][1]), fmaxf(sa[1][2], sa[1][3])));
+    tmax = row4_max(tmax) * a.scale_log2;
+    const bool raise = tmax > run_max + 8.0f;            // false while both are -inf
+    if (__builtin_amdgcn_ballot_w64(raise) != 0) {        // uniform: rescale the rows that need it
+      const float nm = raise ? tmax : run_max;
+      const float alpha = raise ? __builtin_amdgcn_exp2f(run_max - nm) : 1.0f;   // exp2(-inf) = 0
+      lsum *= alpha;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) acc[db] *= alpha;
+      run_max = nm;
+    }
+    const float ref = run_max == -INFINITY ? 0.0f : run_max;
+    float pr[8];
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        pr[4 * c + v] = __builtin_amdgcn_exp2f(__builtin_fmaf(sa[c][v], a.scale_log2, -ref));
+        lsum += pr[4 * c + v];
+      }
+    const u32x4 pa4 = {pack_f16x2(pr[0], pr[1]), pack_f16x2(pr[2], pr[3]), pack_f16x2(pr[4], pr[5]),
+                       pack_f16x2(pr[6], pr[7])};
+    // O^T += V^T P^T, 16 dims per block, k = the tile's 32 columns in the lane-group order above
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const f16x8 vf = __builtin_bit_cast(f16x8, __builtin_shufflevector(vr[db][0], vr[db][1], 0, 1, 2, 3, 4, 5, 6, 7));
+      acc[db] = __builtin_amdgcn_mfma_f32_16x16x32_f16(vf, __builtin_bit_cast(f16x8, pa4), acc[db], 0, 0, 0);
+    }
+  };
+
+  // ---- pipeline (as in loop_attn_kernel): step s reads the table entries of tiles s+3 and s, waits for
+  // tile s, converts this wave's V rows of it, finalizes the records of tile s+4, passes the barrier,
+  // loads the records of tile s+6, LDS-DMAs tile s+3 into the slot tile s-1 used and computes tile s.
+  // Every step issues the same number of VMEM ops (one record load + NI DMA), so "tile s has landed" is
+  // exactly vmcnt(2 * OPS_PER_STEP) on every path.
+  const bool rec_wave = wave == 0;
+  constexpr int OPS_PER_STEP = 1 + NI;
+  u32x2 dA, dB;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const u32x2 r = load_desc(v);
+    if (rec_wave) store_desc(v, r);
+  }
+  FL_WAIT_VM(0);                          // query fragments have arrived
+  lds_barrier();
+  issue(0, s0, tile_offs(0));
+  __builtin_amdgcn_sched_barrier(0);
+  dA = load_desc(4);
+  __builtin_amdgcn_sched_barrier(0);
+  issue(1, s1, tile_offs(1));
+  __builtin_amdgcn_sched_barrier(0);
+  dB = load_desc(5);
+  __builtin_amdgcn_sched_barrier(0);
+  issue(2, s2, tile_offs(2));
+
+  auto step = [&](int u, Slot<D>& cur, Slot<D>& nxt, u32x2& w) {
+    const Offs of = tile_offs(u + 3);
+    const TileHead th = tile_head(u);
+    FL_WAIT_VM(2 * OPS_PER_STEP);
+    convert_v(cur);
+    if (rec_wave) store_desc(u + 4, w);
+    lds_barrier();
+    w = load_desc(u + 6);
+    __builtin_amdgcn_sched_barrier(0);
+    issue(u + 3, nxt, of);
+    if (u < n_tiles) compute(u, cur, th);
+  };
+  const int n_steps = (n_tiles + kRing - 1) / kRing * kRing;
+  for (int u = 0; u < n_steps; u += kRing) {
+    step(u, s0, s3, dA);
+    step(u + 1, s1, s0, dB);
+    step(u + 2, s2, s1, dA);
+    step(u + 3, s3, s2, dB);
+  }
+  FL_WAIT_VM(0);
+  lds_barrier();
+
+  // ---- epilogue: lane (j16, g4) holds dims 16 db + 4 g4 .. +3 of row j16 ----------------------------
+  lsum = row4_add(lsum);
+  if (!row_ok) return;
+  const int64_t orow = ((int64_t)b * a.N + row_i) * HD + (int64_t)h * D;
+  const int64_t lrow = ((int64_t)b * a.N + row_i) * a.H + h;
+  // the subtract term and mass are the previous loop's add term and mass of this row
+  const int pp = a.slot_prev[(int64_t)b * a.N + row_i];
+  const int64_t tp = ((int64_t)b * a.k_prev + pp) * a.H + h;
+  const float msub = pp >= 0 ? a.mass_prev[tp] : 0.0f;
+  const float* subp = a.term_prev + tp * D;
+  const int64_t trow = ((int64_t)b * a.k + p) * a.H + h;
+  const bool keep = a.term_out != nullptr;
+  if (!(msub > 0.0f) || !(lsum > 0.0f)) {     // empty column set or vanished mass: unchanged
+    if (keep) {
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+        *reinterpret_cast<float4*>(a.term_out + trow * D + db * 16 + 4 * g4) = make_float4(0, 0, 0, 0);
+      if (g4 == 0) a.mass_out[trow] = 0.0f;
+    }
+    return;
+  }
+  const float f = msub / lsum;
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+    const int dim = db * 16 + 4 * g4;
+    const float4 sub = *reinterpret_cast<const float4*>(subp + dim);
+    const float4 add = make_float4(acc[db][0] * f, acc[db][1] * f, acc[db][2] * f, acc[db][3] * f);
+    float4 prev = *reinterpret_cast<const float4*>(a.o + orow + dim);
+    prev.x = prev.x - sub.x + add.x;
+    prev.y = prev.y - sub.y + add.y;
+    prev.z = prev.z - sub.z + add.z;
+    prev.w = prev.w - sub.w + add.w;
+    *reinterpret_cast<float4*>(a.o + orow + dim) = prev;
+    if (keep) *reinterpret_cast<float4*>(a.term_out + trow * D + dim) = add;
+  }
+  if (g4 == 0) {
+    a.lse_ref[lrow] = (run_max + log2f(lsum)) * 0.6931471805599453f - logf(msub);
+    if (keep) a.mass_out[trow] = msub;
   }
 }
 
@@ -852,16 +1242,19 @@ static int loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev, const
   }
   const int bm = dense ? 128 : 64;          // rows per workgroup
   dim3 grid(((k + bm - 1) / bm) * B * H);
-  if (d == 128) {
-    if (dense) loop_attn_kernel<128, kDense><<<grid, 256, 0, st>>>(a);
-    else if (reuse) loop_attn_kernel<128, kReuse><<<grid, 256, 0, st>>>(a);
-    else loop_attn_kernel<128, kFull><<<grid, 256, 0, st>>>(a);
-  } else {
-    if (dense) loop_attn_kernel<64, kDense><<<grid, 256, 0, st>>>(a);
-    else if (reuse) loop_attn_kernel<64, kReuse><<<grid, 256, 0, st>>>(a);
-    else loop_attn_kernel<64, kFull><<<grid, 256, 0, st>>>(a);
+  if (dense) {
+    if (d == 128) loop_attn_kernel<128, kDense><<<grid, 256, 0, st>>>(a);
+    else loop_attn_kernel<64, kDense><<<grid, 256, 0, st>>>(a);
+    return check_launch("loop_attn_kernel");
   }
-  return check_launch("loop_attn_kernel");
+  if (!reuse) {
+    if (d == 128) loop_attn_kernel<128, kFull><<<grid, 256, 0, st>>>(a);
+    else loop_attn_kernel<64, kFull><<<grid, 256, 0, st>>>(a);
+    return check_launch("loop_attn_kernel");
+  }
+  if (d == 128) reuse_attn_kernel<128><<<grid, 256, 0, st>>>(a);
+  else reuse_attn_kernel<64><<<grid, 256, 0, st>>>(a);
+  return check_launch("reuse_attn_kernel");
 }
 
 extern "C" int fl_loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev,

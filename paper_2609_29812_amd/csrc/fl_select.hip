@@ -6,9 +6,10 @@
 // topk_select: one 1024-thread workgroup per segment.  Keys are mapped to order-preserving uint32 and
 //   held in registers (M per thread).  The k-th largest key is found in two stages: an LDS histogram
 //   of the top 12 bits and a block scan over its 4096 bins give the bin that holds it; the keys of
-//   that bin are compacted into LDS and the remaining 20 bits are resolved bit by bit from the MSB
-//   with block counts over that (small) set.  The selected positions are then compacted in candidate
-//   order with two block scans, which emits rows ascending and breaks ties by the lower index.
+//   that bin are compacted into LDS and the remaining 20 bits are resolved with digit histograms of
+//   8, 8 and 4 bits over that (small) set (bit by bit over the registers if the bin overflows the LDS
+//   buffer).  The selected positions are then compacted in candidate order with two block scans, which
+//   emits rows ascending and breaks ties by the lower index.
 #include "fl_common.h"
 
 namespace fl {
