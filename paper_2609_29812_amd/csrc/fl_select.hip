@@ -101,19 +101,27 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int* scratch /* [16] 
   return before + incl - v;
 }
 
-// hist[bin] += 1 for every lane with want set.  Lanes that share the bin of the first such lane add
-// once, as a count (keys crowd into few bins, and same-address LDS atomics serialize); the others add
-// one by one.
-__device__ __forceinline__ void hist_add(int* hist, uint32_t bin, bool want) {
-  const uint64_t live = __builtin_amdgcn_ballot_w64(want);
-  if (live == 0) return;                                  // uniform
-  const int leader = __builtin_ctzll(live);
-  const uint32_t lb = __shfl(bin, leader, 64);
-  const bool same = want && bin == lb;
-  const uint64_t group = __builtin_amdgcn_ballot_w64(same);
-  if ((int)(threadIdx.x & 63) == leader) atomicAdd(&hist[lb], (int)__builtin_popcountll(group));
-  if (want && !same) atomicAdd(&hist[bin], 1);
-}
+// Histogram of one digit per lane and round, for keys that crowd into few bins: the bin of the wave's
+// first key of the first round is counted in a register with ballots (one LDS atomic at the end), the
+// other keys add with LDS atomics.  Same-address LDS atomics from many waves serialize; this keeps them
+// to one per wave for the crowded bin.
+struct WaveHist {
+  uint32_t lead = 0;
+  int count = 0;
+  bool started = false;
+  __device__ __forceinline__ void add(int* hist, uint32_t bin, bool want) {
+    if (!started) {                                        // uniform
+      lead = __builtin_amdgcn_readfirstlane(bin);
+      started = true;
+    }
+    const bool same = want && bin == lead;
+    count += (int)__builtin_popcountll(__builtin_amdgcn_ballot_w64(same));
+    if (want && !same) atomicAdd(&hist[bin], 1);
+  }
+  __device__ __forceinline__ void flush(int* hist) {
+    if ((threadIdx.x & 63) == 0 && count > 0) atomicAdd(&hist[lead], count);
+  }
+};
 
 // The bin, scanning bins from the highest, where the running count of keys first reaches krem.
 // hist holds nbins counts (nbins <= 4 * kTopkThreads); result in meta[0..2] = (bin, krem left in it,
@@ -155,6 +163,8 @@ __device__ __forceinline__ uint32_t orderable(float f) {
 // Segment s selects the top k of n keys.  Position p has id cand[p] (cand != NULL) or id_base + p.
 // Selected ids are written ascending at out[s * out_stride + n_prefix + pos]; ids 0..n_prefix-1 are
 // written first (column sinks).  Optional slot map: slot[s * slot_n + id] = pos (or -1).
+// Thread t holds the keys of positions t + 1024 j (coalesced loads; the threshold search does not care
+// about order); the ascending output comes from bitmaps of the selected positions.
 template <int M>
 __global__ __launch_bounds__(kTopkThreads) void topk_select_kernel(
     const float* __restrict__ keys, int64_t key_stride, int n, int k,
@@ -164,13 +174,17 @@ __global__ __launch_bounds__(kTopkThreads) void topk_select_kernel(
   constexpr int kHistBits = 12, kBins = 1 << kHistBits;
   static_assert(kBins == 4 * kTopkThreads, "each thread owns four histogram bins");
   constexpr int kCap = M * kTopkThreads < 32768 ? M * kTopkThreads : 32768;
+  constexpr int kWords = M * kTopkThreads / 32;            // bitmap words over all positions
+  constexpr int kWordsPerThread = (kWords + kTopkThreads - 1) / kTopkThreads;
+  static_assert(2 * kWords <= kCap, "the bitmaps reuse the compaction buffer");
   __shared__ int red[2 * kTopkWaves];
   __shared__ int scan_scratch[kTopkWaves];
   __shared__ int hist[kBins];
-  __shared__ uint32_t cbuf[kCap];          // keys of the threshold's bin
+  __shared__ uint32_t cbuf[kCap];          // keys of the threshold's bin, later the two bitmaps
   __shared__ int meta[3];                  // that bin, keys still to take from it, its size
   const int s = blockIdx.x;
   const int t = threadIdx.x;
+  const int lane = t & 63, wave = t >> 6;
   const float* kp = keys + (int64_t)s * key_stride;
   const int32_t* cp = cand ? cand + (int64_t)s * cand_stride : nullptr;
   int32_t* op = out + (int64_t)s * out_stride;
@@ -181,11 +195,18 @@ __global__ __launch_bounds__(kTopkThreads) void topk_select_kernel(
   }
   for (int i = t; i < n_prefix; i += kTopkThreads) op[i] = i;
 
+  // (buffer loads: out-of-range positions read 0 without a branch, so all M loads are in flight at once;
+  // a bounds-checked pointer load puts each one behind its own branch and wait)
   uint32_t u[M];
+  {
+    const __amdgpu_buffer_rsrc_t kr =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(kp), (short)0, n * 4, 0x00020000);
 #pragma unroll
-  for (int j = 0; j < M; ++j) {
-    int p = t * M + j;
-    u[j] = (p < n) ? orderable(kp[p]) : 0u;
+    for (int j = 0; j < M; ++j) {
+      const int p = t + kTopkThreads * j;
+      const float x = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(kr, (uint32_t)p * 4u, 0, 0));
+      u[j] = orderable(x) & (0u - (uint32_t)(p < n));    // padding: 0 (as a mask, not a branch)
+    }
   }
 
   // k-th largest key: (1) histogram of the top kHistBits bits and the bin that holds it
@@ -194,8 +215,10 @@ __global__ __launch_bounds__(kTopkThreads) void topk_select_kernel(
   if (k > 0) {                                            // uniform
     for (int i = t; i < kBins; i += kTopkThreads) hist[i] = 0;
     __syncthreads();
+    WaveHist wh;
 #pragma unroll
-    for (int j = 0; j < M; ++j) hist_add(hist, u[j] >> (32 - kHistBits), t * M + j < n);
+    for (int j = 0; j < M; ++j) wh.add(hist, u[j] >> (32 - kHistBits), t + kTopkThreads * j < n);
+    wh.flush(hist);
     __syncthreads();
     find_bin(hist, kBins, k, scan_scratch, meta);
     const uint32_t bin = (uint32_t)meta[0];
@@ -204,27 +227,29 @@ __global__ __launch_bounds__(kTopkThreads) void topk_select_kernel(
     prefix = bin << (32 - kHistBits);
     mask = ~0u << (32 - kHistBits);
     if (cnt <= kCap) {
-      // (2) compact that bin's keys into LDS, then resolve the low 20 bits with digit histograms of
-      // 8, 8 and 4 bits over them
+      // (2) compact that bin's keys into LDS (any order), then resolve the low 20 bits with digit
+      // histograms of 8, 8 and 4 bits over them
       int n_in = 0;
 #pragma unroll
-      for (int j = 0; j < M; ++j) n_in += (t * M + j < n && (u[j] >> (32 - kHistBits)) == bin) ? 1 : 0;
+      for (int j = 0; j < M; ++j) n_in += (t + kTopkThreads * j < n && (u[j] >> (32 - kHistBits)) == bin) ? 1 : 0;
       int tot;
       int off = block_exclusive_scan(n_in, scan_scratch, &tot);
 #pragma unroll
       for (int j = 0; j < M; ++j)
-        if (t * M + j < n && (u[j] >> (32 - kHistBits)) == bin) cbuf[off++] = u[j];
+        if (t + kTopkThreads * j < n && (u[j] >> (32 - kHistBits)) == bin) cbuf[off++] = u[j];
       int shift = 32 - kHistBits;
       for (int pass = 0; pass < 3; ++pass) {
         const int nb = pass < 2 ? 8 : 4;
         shift -= nb;
         for (int i = t; i < (1 << nb); i += kTopkThreads) hist[i] = 0;
         __syncthreads();                                  // also orders the compaction writes
+        WaveHist dh;
         for (int i0 = 0; i0 < cnt; i0 += kTopkThreads) {
           const int i = i0 + t;
           const uint32_t v = i < cnt ? cbuf[i] : 0u;
-          hist_add(hist, (v >> shift) & ((1u << nb) - 1), i < cnt && (v & mask) == prefix);
+          dh.add(hist, (v >> shift) & ((1u << nb) - 1), i < cnt && (v & mask) == prefix);
         }
+        dh.flush(hist);
         __syncthreads();
         find_bin(hist, 1 << nb, krem, scan_scratch, meta);
         prefix |= (uint32_t)meta[0] << shift;
@@ -237,42 +262,108 @@ __global__ __launch_bounds__(kTopkThreads) void topk_select_kernel(
         const uint32_t want = prefix | (1u << bit), m2 = mask | (1u << bit);
         int c = 0;
 #pragma unroll
-        for (int j = 0; j < M; ++j) c += ((t * M + j) < n && (u[j] & m2) == want) ? 1 : 0;
+        for (int j = 0; j < M; ++j) c += ((t + kTopkThreads * j) < n && (u[j] & m2) == want) ? 1 : 0;
         c = block_sum(c, red, bit & 1);
         if (c >= krem) prefix = want; else krem -= c;
         mask = m2;
       }
     }
   }
-  // krem = how many keys equal to the threshold are taken, lowest positions first
+  // (3) bitmaps of the positions with a key above the threshold and equal to it (bit p % 32 of word
+  // p / 32): positions t + 1024 j of a wave's lanes 0-31 and 32-63 form whole words, written by ballot
+  uint32_t* bm_gt = cbuf;
+  uint32_t* bm_eq = cbuf + kWords;
+  __syncthreads();                                        // cbuf is no longer read
+#pragma unroll
+  for (int j = 0; j < M; ++j) {
+    const bool valid = k > 0 && t + kTopkThreads * j < n;
+    const uint64_t g = __builtin_amdgcn_ballot_w64(valid && u[j] > prefix);
+    const uint64_t e = __builtin_amdgcn_ballot_w64(valid && u[j] == prefix);
+    const int w0 = (kTopkThreads * j + 64 * wave) >> 5;
+    if (lane == 0) { bm_gt[w0] = (uint32_t)g; bm_eq[w0] = (uint32_t)e; }
+    if (lane == 1) { bm_gt[w0 + 1] = (uint32_t)(g >> 32); bm_eq[w0 + 1] = (uint32_t)(e >> 32); }
+  }
+  __syncthreads();
+  // thread t owns words t * kWordsPerThread ..; the equal keys taken are the krem lowest positions
+  uint32_t gw[kWordsPerThread], ew[kWordsPerThread];
   int n_eq = 0;
 #pragma unroll
-  for (int j = 0; j < M; ++j) n_eq += (k > 0 && (t * M + j) < n && u[j] == prefix) ? 1 : 0;
+  for (int q = 0; q < kWordsPerThread; ++q) {
+    const int wd = t * kWordsPerThread + q;
+    gw[q] = wd < kWords ? bm_gt[wd] : 0u;
+    ew[q] = wd < kWords ? bm_eq[wd] : 0u;
+    n_eq += __builtin_popcount(ew[q]);
+  }
   int total;
-  int eq_rank = block_exclusive_scan(n_eq, scan_scratch, &total);
+  const int eq_before = block_exclusive_scan(n_eq, scan_scratch, &total);
+  int take = krem - eq_before;                          // equal keys this thread still takes
   int n_sel = 0;
-  bool sel[M];
 #pragma unroll
-  for (int j = 0; j < M; ++j) {
-    const bool valid = k > 0 && (t * M + j) < n;
-    const bool eq = valid && u[j] == prefix;
-    sel[j] = valid && (u[j] > prefix || (eq && eq_rank < krem));
-    eq_rank += eq ? 1 : 0;
-    n_sel += sel[j] ? 1 : 0;
+  for (int q = 0; q < kWordsPerThread; ++q) {
+    uint32_t e = ew[q], keep = 0;
+    while (e != 0 && take > 0) {
+      const uint32_t low = e & (0u - e);
+      keep |= low;
+      e ^= low;
+      --take;
+    }
+    gw[q] |= keep;
+    n_sel += __builtin_popcount(gw[q]);
   }
   int pos = block_exclusive_scan(n_sel, scan_scratch, &total);
-  if (slot) {
-    __threadfence();
-    __syncthreads();   // the -1 fill above is complete before positions are written
-  }
+  if constexpr (M <= 4) {
+    // few keys per thread: record each word's selected bits and first output position, then every thread
+    // writes the selected positions among its own (t + 1024 j: coalesced id loads)
+    uint32_t* sel_w = cbuf;                               // reuses the bitmaps' space (read above)
+    int* pos_w = reinterpret_cast<int*>(cbuf + kWords);
+    __syncthreads();
 #pragma unroll
-  for (int j = 0; j < M; ++j) {
-    if (sel[j] && pos < k) {      // exactly k positions are selected; the bound is a safety net
-      const int p = t * M + j;
-      const int id = cp ? cp[p] : id_base + p;
-      op[n_prefix + pos] = id;
-      if (slot) slot[(int64_t)s * slot_n + id] = pos;
-      ++pos;
+    for (int q = 0; q < kWordsPerThread; ++q) {
+      const int wd = t * kWordsPerThread + q;
+      if (wd < kWords) {
+        sel_w[wd] = gw[q];
+        pos_w[wd] = pos;
+      }
+      pos += __builtin_popcount(gw[q]);
+    }
+    // the -1 fill above is complete before positions are written (same workgroup: a workgroup-scope
+    // release suffices; a device-scope fence would also write back the L2)
+    if (slot) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < M; ++j) {
+      const int p = t + kTopkThreads * j;
+      if (p >= n) continue;
+      const uint32_t sw = sel_w[p >> 5];
+      if ((sw >> (p & 31)) & 1u) {
+        const int o = pos_w[p >> 5] + __builtin_popcount(sw & ((1u << (p & 31)) - 1u));
+        if (o < k) {                // exactly k positions are selected; the bound is a safety net
+          const int id = cp ? cp[p] : id_base + p;
+          op[n_prefix + o] = id;
+          if (slot) slot[(int64_t)s * slot_n + id] = o;
+        }
+      }
+    }
+  } else {
+    // many keys per thread, few selected per word: thread t writes the selected positions of its own
+    // words in order
+    if (slot) {   // the -1 fill above is complete before positions are written (workgroup scope suffices)
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+      __syncthreads();
+    }
+#pragma unroll
+    for (int q = 0; q < kWordsPerThread; ++q) {
+      uint32_t g = gw[q];
+      while (g != 0) {
+        const int p = 32 * (t * kWordsPerThread + q) + __builtin_ctz(g);
+        g &= g - 1;
+        if (pos < k) {              // exactly k positions are selected; the bound is a safety net
+          const int id = cp ? cp[p] : id_base + p;
+          op[n_prefix + pos] = id;
+          if (slot) slot[(int64_t)s * slot_n + id] = pos;
+        }
+        ++pos;
+      }
     }
   }
 }
