@@ -45,7 +45,7 @@ def log(*a):
 
 
 # ---- algorithmic work of each call (what the method itself must move / compute) ----------------------
-def attn_work(idx, cols, slot, N, H, d, window, B, reuse=False, keep_terms=True):
+def attn_work(idx, cols, slot, N, H, d, window, B, reuse=False, keep_terms=True, current=False):
     """Exact algorithmic bytes and flops of one sparse attention launch.
 
     flops = 8 d * sum over (b, h, i in A) |S_i|  (two passes, each q.k and p.v), or 4 d * ... when the
@@ -54,7 +54,8 @@ def attn_work(idx, cols, slot, N, H, d, window, B, reuse=False, keep_terms=True)
             of the updated rows, every distinct column of K/V touched by some S_i (cache rows, plus the
             new rows of updated columns), the column list and the slot entries of the touched columns;
             with reuse the previous terms, masses and slot entries of the rows are read, and with
-            keep_terms this loop's terms and masses are written.
+            keep_terms this loop's terms and masses are written.  current: the caches already hold the
+            new rows (reuse only), so every touched column is one cache row and no slot entry is read.
     """
     flops = 0.0
     nbytes = 0.0
@@ -76,9 +77,9 @@ def attn_work(idx, cols, slot, N, H, d, window, B, reuse=False, keep_terms=True)
                     np.add.at(diff, rows + 1, -1)
                     used |= np.cumsum(diff[:N]) > 0
             n_used = int(used.sum())
-            n_new = int((used & upd).sum())
+            n_new = 0 if current else int((used & upd).sum())
             nbytes += (n_used + n_new) * d * 2 * 2          # K and V rows, bf16
-            nbytes += n_used * 4 + g.size * 4               # slot lookups and the column list
+            nbytes += (0 if current else n_used * 4) + g.size * 4   # slot lookups and the column list
         nbytes += k * H * d * 2 * (1 if reuse else 2)       # q_cur (and q_prev) rows
         nbytes += k * H * d * 4 * 2 + k * H * 4 * (1 if reuse else 2)   # o in/out, lse (in/)out
         nbytes += k * 4
@@ -94,6 +95,11 @@ def codec_bytes(k, H, d, bits, group, axis_token, B):
     rows = B * k * H * d
     meta = B * (math.ceil(k / group) * H * d if axis_token else k * H * (d // group)) * 2 * 2
     return rows * 2 * 2 + rows * bits / 8 + meta + rows * 2 + B * k * 4
+
+
+def quant_commit_bytes(k, H, d, bits, group, axis_token, B):
+    """quantize and commit in place: read cur + cache rows, write codes + metadata + cache rows."""
+    return codec_bytes(k, H, d, bits, group, axis_token, B)
 
 
 def commit_bytes(k, H, d, bits, group, axis_token, B):
@@ -135,26 +141,32 @@ class Step:
             vr, vp = dev["v"][r - 1], dev["v"][r - 2]
             bits, kk = w.bits_at(r), w.k(r)
             idx, slot, _ = timed(f"select r{r}", lambda: fl.select_tokens(kr, kp, vr, vp, kk, cand=gs.cand))
-            ck, sk, zk, k_new = timed(f"quant_k r{r}", lambda: fl.kv_residual_quant(
-                kr, gs.k_hat, idx, bits, gs.group, fl.AXIS_TOKEN))
-            cv, sv, zv, v_new = timed(f"quant_v r{r}", lambda: fl.kv_residual_quant(
-                vr, gs.v_hat, idx, bits, gs.group, fl.AXIS_CHANNEL))
-            B, k, H, d = k_new.shape
-            term = torch.empty(B, k, H, d, dtype=torch.float32, device=k_new.device)
-            mass = torch.empty(B, k, H, dtype=torch.float32, device=k_new.device)
+            B, N, H, d = kr.shape
+            term = torch.empty(B, kk, H, d, dtype=torch.float32, device=kr.device)
+            mass = torch.empty(B, kk, H, dtype=torch.float32, device=kr.device)
             if r == 2:
+                # both passes: quantize (compact new rows), attend, then commit into the caches
+                ck, sk, zk, k_new = timed(f"quant_k r{r}", lambda: fl.kv_residual_quant(
+                    kr, gs.k_hat, idx, bits, gs.group, fl.AXIS_TOKEN))
+                cv, sv, zv, v_new = timed(f"quant_v r{r}", lambda: fl.kv_residual_quant(
+                    vr, gs.v_hat, idx, bits, gs.group, fl.AXIS_CHANNEL))
                 timed(f"attn r{r}", lambda: fl.loop_sparse_attn(
                     qr, qp, gs.k_hat, gs.v_hat, k_new, v_new, slot, idx, gs.cols, gs.window, gs.lse, gs.o,
                     term_out=term, mass_out=mass))
+                timed(f"commit_k r{r}", lambda: fl.kv_residual_dequant(
+                    ck, sk, zk, idx, bits, gs.group, fl.AXIS_TOKEN, gs.k_hat, mode=fl.DQ_COMMIT))
+                timed(f"commit_v r{r}", lambda: fl.kv_residual_dequant(
+                    cv, sv, zv, idx, bits, gs.group, fl.AXIS_CHANNEL, gs.v_hat, mode=fl.DQ_COMMIT))
             else:
+                # the add pass alone: quantize and commit in one pass, then attend over the caches
+                timed(f"quant_k r{r}", lambda: fl.kv_residual_quant_commit(
+                    kr, gs.k_hat, idx, bits, gs.group, fl.AXIS_TOKEN))
+                timed(f"quant_v r{r}", lambda: fl.kv_residual_quant_commit(
+                    vr, gs.v_hat, idx, bits, gs.group, fl.AXIS_CHANNEL))
                 timed(f"attn r{r}", lambda: fl.loop_sparse_attn(
-                    qr, None, gs.k_hat, gs.v_hat, k_new, v_new, slot, idx, gs.cols, gs.window, gs.lse, gs.o,
+                    qr, None, gs.k_hat, gs.v_hat, None, None, slot, idx, gs.cols, gs.window, gs.lse, gs.o,
                     term_prev=gs.term, mass_prev=gs.mass, slot_prev=gs.slot_prev, term_out=term, mass_out=mass))
             gs.term, gs.mass, gs.slot_prev = term, mass, slot
-            timed(f"commit_k r{r}", lambda: fl.kv_residual_dequant(ck, sk, zk, idx, bits, gs.group, fl.AXIS_TOKEN,
-                                                                    gs.k_hat, mode=fl.DQ_COMMIT))
-            timed(f"commit_v r{r}", lambda: fl.kv_residual_dequant(cv, sv, zv, idx, bits, gs.group,
-                                                                    fl.AXIS_CHANNEL, gs.v_hat, mode=fl.DQ_COMMIT))
             trace.append((r, idx, slot))
             gs.cand = idx
         return trace
@@ -325,20 +337,22 @@ def main():
     B, N, H, d = w.batch, w.seq, w.heads, w.head_dim
     kernels = {}
     attn_bytes = attn_flops = attn_us = 0.0
+    per_kernel = {}               # kernel -> [bytes, flops, us, launches]
     total_bytes = 0.0
     n_cand = N
     for r, idx_t, slot_t in trace:
         idx, slot = idx_t.cpu().numpy(), slot_t.cpu().numpy()
         kr, bits = w.k(r), w.bits_at(r)
-        by, fl_ = attn_work(idx, cols, slot, N, H, d, w.window, B, reuse=r > 2)
+        by, fl_ = attn_work(idx, cols, slot, N, H, d, w.window, B, reuse=r > 2, current=r > 2)
         work = {
             f"select r{r}": (select_bytes(n_cand, N, H * d, kr, B), 0.0),
             f"quant_k r{r}": (codec_bytes(kr, H, d, bits, w.group, True, B), 0.0),
             f"quant_v r{r}": (codec_bytes(kr, H, d, bits, w.group, False, B), 0.0),
             f"attn r{r}": (by, fl_),
-            f"commit_k r{r}": (commit_bytes(kr, H, d, bits, w.group, True, B), 0.0),
-            f"commit_v r{r}": (commit_bytes(kr, H, d, bits, w.group, False, B), 0.0),
         }
+        if r == 2:
+            work[f"commit_k r{r}"] = (commit_bytes(kr, H, d, bits, w.group, True, B), 0.0)
+            work[f"commit_v r{r}"] = (commit_bytes(kr, H, d, bits, w.group, False, B), 0.0)
         for name, (nb, nf) in work.items():
             us = dur_us[name]
             kernels[name] = {"us": round(us, 2), "GB/s": round(nb / us / 1e3, 1),
@@ -348,27 +362,37 @@ def main():
         attn_bytes += by
         attn_flops += fl_
         attn_us += dur_us[f"attn r{r}"]
+        kname = "loop_attn_kernel" if r == 2 else "reuse_attn_kernel"
+        acc = per_kernel.setdefault(kname, [0.0, 0.0, 0.0, 0])
+        acc[0] += by
+        acc[1] += fl_
+        acc[2] += dur_us[f"attn r{r}"]
+        acc[3] += 1
         n_cand = kr
     for name, kv in kernels.items():
         log(f"  {name:12s} {kv['us']:9.2f} us  {kv['GB/s']:8.1f} GB/s  alg {kv['alg_MB']:8.2f} MB"
             + (f"  {kv['TFLOP/s']:7.2f} TFLOP/s" if kv["TFLOP/s"] else ""))
-    n_loops = w.loops - 1
-    t_hbm = attn_bytes / (HBM_PEAK_GBS * 1e9)
-    t_mfma = attn_flops / (MFMA_BF16_TFLOPS * 1e12)
-    bound = "hbm" if t_hbm >= t_mfma else "mfma"
-    if bound == "hbm":
-        achieved = attn_bytes / n_loops / (attn_us / n_loops * 1e-6) / 1e9
-        peak, unit = HBM_PEAK_GBS, "GB/s"
-    else:
-        achieved = attn_flops / n_loops / (attn_us / n_loops * 1e-6) / 1e12
-        peak, unit = MFMA_BF16_TFLOPS, "TFLOP/s"
-    traffic = load_traffic("loop_attn_kernel", w.name)
-    roofline = {"kernel": "loop_attn_kernel", "bound": bound, "achieved": round(achieved, 2), "peak": peak,
-                "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic,
-                "alg_bytes_per_launch": round(attn_bytes / n_loops), "alg_flops_per_launch": round(attn_flops / n_loops),
-                "avg_launch_us": round(attn_us / n_loops, 2),
-                "mfma_frac": round(attn_flops / (attn_us * 1e-6) / 1e12 / MFMA_BF16_TFLOPS, 4),
-                "hbm_frac": round(attn_bytes / (attn_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+
+    def roofline_of(kname):
+        nb, nf, us, n = per_kernel[kname]
+        t_hbm = nb / (HBM_PEAK_GBS * 1e9)
+        t_mfma = nf / (MFMA_BF16_TFLOPS * 1e12)
+        bound = "hbm" if t_hbm >= t_mfma else "mfma"
+        if bound == "hbm":
+            achieved, peak, unit = nb / (us * 1e-6) / 1e9, HBM_PEAK_GBS, "GB/s"
+        else:
+            achieved, peak, unit = nf / (us * 1e-6) / 1e12, MFMA_BF16_TFLOPS, "TFLOP/s"
+        return {"kernel": kname, "bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
+                "frac": round(achieved / peak, 4), "traffic": load_traffic(kname, w.name),
+                "launches_per_step": n, "alg_bytes_per_launch": round(nb / n), "alg_flops_per_launch": round(nf / n),
+                "avg_launch_us": round(us / n, 2),
+                "mfma_frac": round(nf / (us * 1e-6) / 1e12 / MFMA_BF16_TFLOPS, 4),
+                "hbm_frac": round(nb / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+
+    # the dominant kernel is the one with the most time per step
+    order = sorted(per_kernel, key=lambda kn: -per_kernel[kn][2])
+    roofline = roofline_of(order[0])
+    others = {kn: roofline_of(kn) for kn in order[1:]}
 
     result = {
         "metric": METRIC,
@@ -390,6 +414,7 @@ def main():
         "step_hbm_GBps": round(total_bytes / (ms_step * 1e-3) / 1e9, 1),
         "attn_rows_per_s": round(rows_per_step / (attn_us * 1e-6), 1),
         "roofline": roofline,
+        "roofline_other_kernels": others,
         "kernels": kernels,
     }
     if not args.no_cpu_baseline:

@@ -117,6 +117,16 @@ int fl_kv_residual_quant(const uint16_t* x_cur, const uint16_t* x_ref, const int
                          uint8_t* codes, uint16_t* scale, uint16_t* zero, uint16_t* out_rows,
                          void* stream);
 
+/* (2a') The same quantization with the reconstruction committed in place -- Eq. 4 and Appendix D.3,
+ * Eq. 8: x_hat holds X_hat^(r-1) and is the reference; codes, scale and zero are written as by
+ * fl_kv_residual_quant(x_cur, x_hat, idx, ...), and rows idx of x_hat become X_hat^(r) (what
+ * fl_kv_residual_dequant FL_DQ_COMMIT would write from those codes).  One pass instead of two, for a
+ * loop whose attention update reads the new state from the cache (fl_loop_sparse_attn_terms with
+ * k_new = v_new = NULL).  x_hat must not be NULL; other arguments as fl_kv_residual_quant. */
+int fl_kv_residual_quant_commit(const uint16_t* x_cur, uint16_t* x_hat, const int32_t* idx, int k,
+                                int B, int N, int H, int d, int bits, int group, int axis,
+                                uint8_t* codes, uint16_t* scale, uint16_t* zero, void* stream);
+
 /* ------------------------------------------------------------------------------------------------
  * (2b) Residual dequantization and reconstruction -- Eq. 4 and Appendix D.3, Eq. 8:
  *     X_hat^(r)[i] = bf16(fp32(X_hat^(r-1)[i]) + fp32(z + q * s))   for i = idx[b, p], p < k;
@@ -154,7 +164,8 @@ int fl_kv_residual_dequant(const uint8_t* codes, const uint16_t* scale, const ui
  *
  *   q_cur, q_prev     : bf16 [B, N, H, d]  (queries of loop r and r-1)
  *   k_cache, v_cache  : bf16 [B, N, H, d]  X_hat^(r-1)
- *   k_new, v_new      : bf16 [B, k, H, d]  X_hat^(r) of the rows, in `rows` order
+ *   k_new, v_new      : bf16 [B, k, H, d]  X_hat^(r) of the rows, in `rows` order (both or neither;
+ *                                          neither only with term_prev, see (3b))
  *   slot              : int32 [B, N]       position in rows, or -1
  *   rows              : int32 [B, k]       ascending updated rows
  *   cols              : int32 [B, H, c_list] ascending column list (0 <= c_list <= N)
@@ -192,7 +203,10 @@ int fl_loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev,
  *     slot_prev[b, i] of the previous loop's term_out/mass_out (k_prev rows) instead of recomputing the
  *     subtract pass, so q_prev is unused (may be NULL).  Every row of `rows` must have
  *     slot_prev[b, i] >= 0; a row without one is left unchanged.  The kernel then runs the add pass
- *     only, with two waves per row group splitting each tile's columns.
+ *     only, with one 16-row group per wave;
+ *   - with term_prev and k_new = v_new = NULL: k_cache and v_cache already hold X_hat^(r) of the updated
+ *     rows (committed before this call, e.g. by fl_kv_residual_quant_commit), and every column is read
+ *     from them.
  * term_prev and term_out may not alias.  Other arguments as fl_loop_sparse_attn (never DENSE).
  * ---------------------------------------------------------------------------------------------- */
 int fl_loop_sparse_attn_terms(const uint16_t* q_cur, const uint16_t* q_prev,

@@ -61,6 +61,7 @@ struct AttnArgs {
   float* mass_out;           // optional [B, k, H]: the cached mass m of each updated row
   int k, k_prev, c_list, window, B, N, H;
   float scale_log2;          // sm_scale * log2(e)
+  int cache_current;         // reuse: the caches already hold X_hat^(r) of the updated rows (no new rows)
 };
 
 typedef __amdgpu_buffer_rsrc_t rsrc_t;
@@ -740,7 +741,7 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
       }
       n = lo;
     }
-    s_meta[tid] = n;
+    s_meta[tid] = (tid == 1 && a.cache_current) ? 0 : n;   // current caches: no new-row tiles
   }
   const int bandLo = a.window > 0 ? max(0, min_row - a.window + 1) : 0;
   const int bandHi = a.window > 0 ? max_row : -1;
@@ -752,7 +753,7 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
       if (rowp[mid] < bandLo) lo = mid + 1; else hi = mid;
     }
     pa = lo;
-    pb = last_p + 1;
+    pb = a.cache_current ? lo : last_p + 1;
   }
   __syncthreads();
   const int nA = s_meta[0];
@@ -781,14 +782,16 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
   const uint32_t head_off = (uint32_t)(h * D * 2);
   const rsrc_t kcR = make_rsrc(a.k_cache + (int64_t)b * a.N * HD, (uint32_t)a.N * rb);
   const rsrc_t vcR = make_rsrc(a.v_cache + (int64_t)b * a.N * HD, (uint32_t)a.N * rb);
-  const rsrc_t knR = make_rsrc(a.k_new + (int64_t)b * a.k * HD, (uint32_t)a.k * rb);
-  const rsrc_t vnR = make_rsrc(a.v_new + (int64_t)b * a.k * HD, (uint32_t)a.k * rb);
+  // (with current caches there are no new rows: an empty range makes every access to them read zero)
+  const uint32_t new_bytes = a.cache_current ? 0u : (uint32_t)a.k * rb;
+  const rsrc_t knR = make_rsrc(a.cache_current ? a.k_cache : a.k_new + (int64_t)b * a.k * HD, new_bytes);
+  const rsrc_t vnR = make_rsrc(a.cache_current ? a.v_cache : a.v_new + (int64_t)b * a.k * HD, new_bytes);
 
   auto store_desc = [=](int v, u32x2 w) {
     const bool newer = v >= n_old;
     const int cid = (int)w[0];
     const int aux = (int)w[1];
-    const bool upd = !newer && aux >= 0;   // updated this loop but staged from the cache
+    const bool upd = !newer && aux >= 0 && !a.cache_current;   // updated this loop, staged from the cache
     const int row = newer ? aux : cid;
     const bool valid = cid != kPad;
     if (lane < kBN) {
@@ -1179,8 +1182,12 @@ static int loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev, const
     FL_REQUIRE(rows == nullptr && k == N, FL_E_SHAPE, "fl_loop_sparse_attn: DENSE needs rows == NULL and k == N");
     FL_REQUIRE(!reuse && term_out == nullptr, FL_E_UNSUPPORTED, "fl_loop_sparse_attn: DENSE keeps no terms");
   } else {
-    FL_REQUIRE(k_new && v_new && slot && rows && (reuse || q_prev), FL_E_NULL,
-               "fl_loop_sparse_attn: q_prev (unless reusing terms), k_new, v_new, slot and rows are required");
+    FL_REQUIRE(slot && rows && (reuse || q_prev), FL_E_NULL,
+               "fl_loop_sparse_attn: q_prev (unless reusing terms), slot and rows are required");
+    FL_REQUIRE((k_new == nullptr) == (v_new == nullptr), FL_E_NULL,
+               "fl_loop_sparse_attn: k_new and v_new go together");
+    FL_REQUIRE(reuse || k_new, FL_E_NULL,
+               "fl_loop_sparse_attn: k_new and v_new are required unless reusing terms with current caches");
     FL_REQUIRE(k >= 0 && k <= N, FL_E_RANGE, "fl_loop_sparse_attn: k=%d outside [0, N]", k);
     FL_REQUIRE(c_list >= 0 && c_list <= N, FL_E_RANGE, "fl_loop_sparse_attn: c_list=%d outside [0, N]", c_list);
     FL_REQUIRE(c_list == 0 || cols, FL_E_NULL, "fl_loop_sparse_attn: cols is required when c_list > 0");
@@ -1222,6 +1229,7 @@ static int loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev, const
   a.N = N;
   a.H = H;
   a.scale_log2 = sm_scale * 1.4426950408889634f;
+  a.cache_current = (!dense && reuse && k_new == nullptr) ? 1 : 0;
   if (!dense) {
     const RecLayout L = rec_layout(B, N, H, k, c_list);
     int2* rec = static_cast<int2*>(ws);

@@ -89,11 +89,13 @@ __device__ __forceinline__ void group_meta(float mn, float mx, int qmax, double&
 // A workgroup of 256 threads = S row slices x CH chunks of 8 channels; each slice holds RPS = G/S rows.
 // S = min(G, 32), so a group of 64 rows spreads over 32 slices and a workgroup covers 64 channels.
 
+// out_rows: compact [B, k, HD] rows, or (commit) the cache rows idx of x_ref itself, written in place
+// (every element is read before the same thread writes it, after the workgroup's reduction).
 template <int BITS, int S, int RPS>
 __global__ __launch_bounds__(256) void quant_token_kernel(
-    const uint16_t* __restrict__ x_cur, const uint16_t* __restrict__ x_ref,
+    const uint16_t* __restrict__ x_cur, const uint16_t* x_ref,
     const int32_t* __restrict__ idx, int k, int N, int HD, int G, uint8_t* __restrict__ codes,
-    uint16_t* __restrict__ scale, uint16_t* __restrict__ zero, uint16_t* __restrict__ out_rows) {
+    uint16_t* __restrict__ scale, uint16_t* __restrict__ zero, uint16_t* out_rows, bool commit) {
   constexpr int CH = 256 / S;          // chunks of 8 channels per workgroup
   __shared__ float s_mn[S][CH * 8];
   __shared__ float s_mx[S][CH * 8];
@@ -108,6 +110,7 @@ __global__ __launch_bounds__(256) void quant_token_kernel(
 
   float dl[RPS][8];
   uint4 ref_raw[RPS];
+  int64_t roff[RPS];                   // element offset of each row in x_ref
   float mn[8], mx[8];
 #pragma unroll
   for (int t = 0; t < 8; ++t) { mn[t] = INFINITY; mx[t] = -INFINITY; }
@@ -115,9 +118,11 @@ __global__ __launch_bounds__(256) void quant_token_kernel(
   for (int j = 0; j < RPS; ++j) {
     const int p = g * G + slice * RPS + j;
     ref_raw[j] = make_uint4(0, 0, 0, 0);
+    roff[j] = 0;
     if (ch_ok && p < k) {
       const int64_t i = idx ? (int64_t)idx[(int64_t)b * k + p] : (int64_t)p;
       const int64_t off = ((int64_t)b * N + i) * HD + c0;
+      roff[j] = off;
       Row8 c = load_bf16x8(x_cur + off);
       Row8 r{};
       if (x_ref) {
@@ -183,17 +188,18 @@ __global__ __launch_bounds__(256) void quant_token_kernel(
         float dq = z8[t] + (float)q[t] * s8[t];     // q * s exact in fp32: one rounding
         o.v[t] = ref + dq;
       }
-      store_bf16x8(out_rows + ((int64_t)b * k + p) * HD + c0, o);
+      store_bf16x8(out_rows + (commit ? roff[j] : ((int64_t)b * k + p) * HD + c0), o);
     }
   }
 }
 
 // ---- values: per-token groups of G channels ----------------------------------------------------------
+// out_rows as for quant_token_kernel (each element is read and written by one thread).
 template <int BITS>
 __global__ __launch_bounds__(256) void quant_channel_kernel(
-    const uint16_t* __restrict__ x_cur, const uint16_t* __restrict__ x_ref,
+    const uint16_t* __restrict__ x_cur, const uint16_t* x_ref,
     const int32_t* __restrict__ idx, int k, int N, int HD, int G, uint8_t* __restrict__ codes,
-    uint16_t* __restrict__ scale, uint16_t* __restrict__ zero, uint16_t* __restrict__ out_rows) {
+    uint16_t* __restrict__ scale, uint16_t* __restrict__ zero, uint16_t* out_rows, bool commit) {
   constexpr int qmax = (1 << BITS) - 1;
   const int chunks = HD / 8;
   const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -208,9 +214,11 @@ __global__ __launch_bounds__(256) void quant_channel_kernel(
   float dl[8];
   uint4 ref_raw = make_uint4(0, 0, 0, 0);
   float mn = INFINITY, mx = -INFINITY;
+  int64_t roff = 0;
   if (ok) {
     const int64_t i = idx ? (int64_t)idx[(int64_t)b * k + p] : (int64_t)p;
     const int64_t off = ((int64_t)b * N + i) * HD + c0;
+    roff = off;
     Row8 c = load_bf16x8(x_cur + off);
     Row8 r{};
     if (x_ref) {
@@ -250,7 +258,7 @@ __global__ __launch_bounds__(256) void quant_channel_kernel(
       float ref = (t & 1) ? __uint_as_float(rw[t >> 1] & 0xFFFF0000u) : __uint_as_float(rw[t >> 1] << 16);
       o.v[t] = ref + (z32 + (float)q[t] * s32);
     }
-    store_bf16x8(out_rows + ((int64_t)b * k + p) * HD + c0, o);
+    store_bf16x8(out_rows + (commit ? roff : ((int64_t)b * k + p) * HD + c0), o);
   }
 }
 
@@ -258,7 +266,7 @@ __global__ __launch_bounds__(256) void quant_channel_kernel(
 __global__ __launch_bounds__(256) void passthrough_kernel(const uint16_t* __restrict__ x_cur,
                                                           const int32_t* __restrict__ idx, int k,
                                                           int N, int HD, uint8_t* __restrict__ codes,
-                                                          uint16_t* __restrict__ out_rows) {
+                                                          uint16_t* __restrict__ out_rows, bool commit) {
   const int chunks = HD / 8;
   const int64_t local = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int b = blockIdx.y;
@@ -267,7 +275,8 @@ __global__ __launch_bounds__(256) void passthrough_kernel(const uint16_t* __rest
   const int64_t i = idx ? (int64_t)idx[(int64_t)b * k + p] : (int64_t)p;
   uint4 w = *reinterpret_cast<const uint4*>(x_cur + ((int64_t)b * N + i) * HD + c0);
   *reinterpret_cast<uint4*>(codes + (((int64_t)b * k + p) * HD + c0) * 2) = w;
-  if (out_rows) *reinterpret_cast<uint4*>(out_rows + ((int64_t)b * k + p) * HD + c0) = w;
+  if (out_rows)
+    *reinterpret_cast<uint4*>(out_rows + (commit ? ((int64_t)b * N + i) * HD : ((int64_t)b * k + p) * HD) + c0) = w;
 }
 
 // ---- dequantization / reconstruction ------------------------------------------------------------------
@@ -338,26 +347,17 @@ static int check_codec_args(const char* fn, const void* codes, const void* a, in
   return FL_OK;
 }
 
-}  // namespace fl
-
-using namespace fl;
-
-extern "C" int fl_kv_residual_quant(const uint16_t* x_cur, const uint16_t* x_ref, const int32_t* idx,
-                                    int k, int B, int N, int H, int d, int bits, int group, int axis,
-                                    uint8_t* codes, uint16_t* scale, uint16_t* zero,
-                                    uint16_t* out_rows, void* stream) {
-  FL_API_BEGIN
-  int rc = check_codec_args("fl_kv_residual_quant", codes, x_cur, k, B, N, H, d, bits, group, axis,
-                            true, scale, zero, idx);
+static int residual_quant(const char* fn, const uint16_t* x_cur, const uint16_t* x_ref, const int32_t* idx,
+                          int k, int B, int N, int H, int d, int bits, int group, int axis, uint8_t* codes,
+                          uint16_t* scale, uint16_t* zero, uint16_t* out_rows, bool commit, void* stream) {
+  int rc = check_codec_args(fn, codes, x_cur, k, B, N, H, d, bits, group, axis, true, scale, zero, idx);
   if (rc != FL_OK) return rc;
-  FL_REQUIRE(!(out_rows && out_rows == x_ref && idx), FL_E_SHAPE,
-             "fl_kv_residual_quant: out_rows may alias x_ref only when idx is NULL");
   if (k == 0) return FL_OK;
   hipStream_t st = as_stream(stream);
   const int HD = H * d;
   if (bits == 16) {
     dim3 grid((unsigned)(((int64_t)k * (HD / 8) + 255) / 256), B);
-    passthrough_kernel<<<grid, 256, 0, st>>>(x_cur, idx, k, N, HD, codes, out_rows);
+    passthrough_kernel<<<grid, 256, 0, st>>>(x_cur, idx, k, N, HD, codes, out_rows, commit);
     return check_launch("passthrough_kernel");
   }
   if (axis == FL_AXIS_TOKEN) {
@@ -366,7 +366,7 @@ extern "C" int fl_kv_residual_quant(const uint16_t* x_cur, const uint16_t* x_ref
     dim3 grid((HD + cw - 1) / cw, (k + group - 1) / group, B);
 #define FL_QT(BB, SS, RR)                                                                          \
   quant_token_kernel<BB, SS, RR><<<grid, 256, 0, st>>>(x_cur, x_ref, idx, k, N, HD, group, codes, \
-                                                       scale, zero, out_rows)
+                                                       scale, zero, out_rows, commit)
 #define FL_QT_BITS(BB)                                   \
   switch (group) {                                       \
     case 8: FL_QT(BB, 8, 1); break;                      \
@@ -381,10 +381,38 @@ extern "C" int fl_kv_residual_quant(const uint16_t* x_cur, const uint16_t* x_ref
     return check_launch("quant_token_kernel");
   }
   dim3 grid((unsigned)(((int64_t)k * (HD / 8) + 255) / 256), B);
-  if (bits == 2) quant_channel_kernel<2><<<grid, 256, 0, st>>>(x_cur, x_ref, idx, k, N, HD, group, codes, scale, zero, out_rows);
-  else if (bits == 4) quant_channel_kernel<4><<<grid, 256, 0, st>>>(x_cur, x_ref, idx, k, N, HD, group, codes, scale, zero, out_rows);
-  else quant_channel_kernel<8><<<grid, 256, 0, st>>>(x_cur, x_ref, idx, k, N, HD, group, codes, scale, zero, out_rows);
+#define FL_QC(BB) \
+  quant_channel_kernel<BB><<<grid, 256, 0, st>>>(x_cur, x_ref, idx, k, N, HD, group, codes, scale, zero, out_rows, commit)
+  if (bits == 2) FL_QC(2);
+  else if (bits == 4) FL_QC(4);
+  else FL_QC(8);
+#undef FL_QC
   return check_launch("quant_channel_kernel");
+}
+
+}  // namespace fl
+
+using namespace fl;
+
+extern "C" int fl_kv_residual_quant(const uint16_t* x_cur, const uint16_t* x_ref, const int32_t* idx,
+                                    int k, int B, int N, int H, int d, int bits, int group, int axis,
+                                    uint8_t* codes, uint16_t* scale, uint16_t* zero,
+                                    uint16_t* out_rows, void* stream) {
+  FL_API_BEGIN
+  FL_REQUIRE(!(out_rows && out_rows == x_ref && idx), FL_E_SHAPE,
+             "fl_kv_residual_quant: out_rows may alias x_ref only when idx is NULL");
+  return residual_quant("fl_kv_residual_quant", x_cur, x_ref, idx, k, B, N, H, d, bits, group, axis, codes,
+                        scale, zero, out_rows, false, stream);
+  FL_API_END
+}
+
+extern "C" int fl_kv_residual_quant_commit(const uint16_t* x_cur, uint16_t* x_hat, const int32_t* idx, int k,
+                                           int B, int N, int H, int d, int bits, int group, int axis,
+                                           uint8_t* codes, uint16_t* scale, uint16_t* zero, void* stream) {
+  FL_API_BEGIN
+  FL_REQUIRE(x_hat != nullptr, FL_E_NULL, "fl_kv_residual_quant_commit: x_hat is required");
+  return residual_quant("fl_kv_residual_quant_commit", x_cur, x_hat, idx, k, B, N, H, d, bits, group, axis,
+                        codes, scale, zero, x_hat, true, stream);
   FL_API_END
 }
 

@@ -8,6 +8,8 @@ sparse_step() one sparse loop r >= 2: select the active rows among the previous 
               mass-corrected update to their outputs (Eq. 7), then commit the new rows into the caches.
               Each loop keeps its add terms; from the second sparse loop on they serve as the subtract
               terms (equal in exact arithmetic: the column sets are fixed and the active rows nested).
+              Such a loop needs only the new state, so the quantizers commit the new rows straight into
+              the caches and the attention reads every column from them.
 """
 from __future__ import annotations
 
@@ -52,25 +54,31 @@ def setup(q1, k1, v1, base_bits, group, n_sink, t, window):
 def sparse_step(st: LayerState, qr, qp, kr, kp, vr, vp, k_r, bits, keep=False):
     """Advance the layer by one sparse loop.  Returns the loop's outputs when keep=True."""
     idx, slot, key = fl.select_tokens(kr, kp, vr, vp, k_r, cand=st.cand)
-    ck, sk, zk, k_new = fl.kv_residual_quant(kr, st.k_hat, idx, bits, st.group, fl.AXIS_TOKEN)
-    cv, sv, zv, v_new = fl.kv_residual_quant(vr, st.v_hat, idx, bits, st.group, fl.AXIS_CHANNEL)
+    B, N, H, d = kr.shape
+    k = idx.shape[1]
     term = mass = None
     if st.reuse:
-        B, k, H, d = k_new.shape
-        term = torch.empty(B, k, H, d, dtype=torch.float32, device=k_new.device)
-        mass = torch.empty(B, k, H, dtype=torch.float32, device=k_new.device)
+        term = torch.empty(B, k, H, d, dtype=torch.float32, device=kr.device)
+        mass = torch.empty(B, k, H, dtype=torch.float32, device=kr.device)
+    k_new = v_new = None
     if st.reuse and st.term is not None:
-        fl.loop_sparse_attn(qr, None, st.k_hat, st.v_hat, k_new, v_new, slot, idx, st.cols, st.window, st.lse,
+        # the add pass alone: commit the new rows first, then attend over the caches
+        ck, sk, zk = fl.kv_residual_quant_commit(kr, st.k_hat, idx, bits, st.group, fl.AXIS_TOKEN)
+        cv, sv, zv = fl.kv_residual_quant_commit(vr, st.v_hat, idx, bits, st.group, fl.AXIS_CHANNEL)
+        fl.loop_sparse_attn(qr, None, st.k_hat, st.v_hat, None, None, slot, idx, st.cols, st.window, st.lse,
                             st.o, term_prev=st.term, mass_prev=st.mass, slot_prev=st.slot_prev, term_out=term,
                             mass_out=mass)
     else:
+        # both passes: the subtract pass needs the loop r-1 caches, so commit after the attention
+        ck, sk, zk, k_new = fl.kv_residual_quant(kr, st.k_hat, idx, bits, st.group, fl.AXIS_TOKEN)
+        cv, sv, zv, v_new = fl.kv_residual_quant(vr, st.v_hat, idx, bits, st.group, fl.AXIS_CHANNEL)
         fl.loop_sparse_attn(qr, qp, st.k_hat, st.v_hat, k_new, v_new, slot, idx, st.cols, st.window, st.lse,
                             st.o, term_out=term, mass_out=mass)
+        fl.kv_residual_dequant(ck, sk, zk, idx, bits, st.group, fl.AXIS_TOKEN, st.k_hat, mode=fl.DQ_COMMIT)
+        fl.kv_residual_dequant(cv, sv, zv, idx, bits, st.group, fl.AXIS_CHANNEL, st.v_hat, mode=fl.DQ_COMMIT)
     st.term, st.mass, st.slot_prev = term, mass, slot
-    fl.kv_residual_dequant(ck, sk, zk, idx, bits, st.group, fl.AXIS_TOKEN, st.k_hat, mode=fl.DQ_COMMIT)
-    fl.kv_residual_dequant(cv, sv, zv, idx, bits, st.group, fl.AXIS_CHANNEL, st.v_hat, mode=fl.DQ_COMMIT)
     st.cand = idx
-    if keep:
+    if keep:   # (k_new / v_new are None when the loop committed straight into the caches)
         return dict(idx=idx, slot=slot, key=key, codes_k=ck, scale_k=sk, zero_k=zk, codes_v=cv,
                     scale_v=sv, zero_v=zv, k_new=k_new, v_new=v_new)
     return None

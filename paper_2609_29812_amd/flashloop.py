@@ -36,6 +36,8 @@ _SIGNATURES = {
                                 _c_p, _c_p, _c_p, _c_p]),
     "fl_kv_residual_quant": (_c_i, [_c_p, _c_p, _c_p, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i,
                                     _c_p, _c_p, _c_p, _c_p, _c_p]),
+    "fl_kv_residual_quant_commit": (_c_i, [_c_p, _c_p, _c_p, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i,
+                                           _c_p, _c_p, _c_p, _c_p]),
     "fl_kv_residual_dequant": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i,
                                       _c_i, _c_i, _c_p, _c_p, _c_p]),
     "fl_loop_sparse_attn_ws": (_c_sz, [_c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i]),
@@ -156,6 +158,30 @@ def kv_residual_quant(x_cur, x_ref, idx, bits, group, axis, rows=True, out=None)
     return codes, scale, zero, out_rows
 
 
+def kv_residual_quant_commit(x_cur, x_hat, idx, bits, group, axis, out=None):
+    """Quantize the residual of rows idx against x_hat and commit the reconstruction into x_hat in place.
+    Returns (codes, scale, zero)."""
+    B, N, H, d = x_cur.shape
+    _dev(x_cur, torch.bfloat16, "x_cur")
+    _dev(x_hat, torch.bfloat16, "x_hat", x_cur.shape)
+    k = N if idx is None else idx.shape[1]
+    _dev(idx, torch.int32, "idx", None if idx is None else (B, k))
+    dev = x_cur.device
+    o = out or {}
+    codes = o.get("codes")
+    if codes is None:
+        codes = torch.empty(B, k, H, d * bits // 8, dtype=torch.uint8, device=dev)
+    scale = zero = None
+    if bits != 16:
+        shp = meta_shape(B, k, H, d, group, axis)
+        scale = o.get("scale") if o.get("scale") is not None else torch.empty(shp, dtype=torch.float16, device=dev)
+        zero = o.get("zero") if o.get("zero") is not None else torch.empty(shp, dtype=torch.float16, device=dev)
+    rc = load().fl_kv_residual_quant_commit(_p(x_cur), _p(x_hat), _p(idx), k, B, N, H, d, bits, group, axis,
+                                            _p(codes), _p(scale), _p(zero), _stream())
+    _check(rc, "fl_kv_residual_quant_commit")
+    return codes, scale, zero
+
+
 def kv_residual_dequant(codes, scale, zero, idx, bits, group, axis, x_hat, mode=DQ_COMPACT):
     """COMPACT: returns the reconstructed rows [B, k, H, d]; COMMIT: updates x_hat in place."""
     B, N, H, d = x_hat.shape
@@ -184,7 +210,7 @@ def loop_sparse_attn(q_cur, q_prev, k_cache, v_cache, k_new, v_new, slot, rows, 
 
     term_out/mass_out (fp32 [B, k, H, d] / [B, k, H]) also keep this loop's add terms; term_prev/mass_prev with
     slot_prev (the previous loop's slot map) reuse the previous loop's add terms as the subtract terms, in
-    which case q_prev may be None."""
+    which case q_prev may be None, and k_new/v_new may be None when the caches already hold this loop's rows."""
     B, N, H, d = q_cur.shape
     k = rows.shape[1]
     reuse = term_prev is not None

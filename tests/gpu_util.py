@@ -63,3 +63,13 @@ def assert_keys_close(got, want, what):
     n_off = int(np.sum(diff > 0))
     say(f"  {what}: {n_off} of {want.size} keys differ (<= 1 ulp allowed)")
     assert np.all(diff <= ulp), f"{what}: key differs by more than one ulp"
+
+
+def new_rows(out, name, cache):
+    """The loop's reconstructed rows X_hat^(r)[idx] as [B, k, H, d] bf16 bits: the compact rows the quantizer
+    wrote, or (a loop that committed straight into the caches) the cache rows at idx."""
+    if out[name] is not None:
+        return down_bits16(out[name])
+    idx = down(out["idx"])
+    c = down_bits16(cache)
+    return np.stack([c[b, idx[b]] for b in range(idx.shape[0])])

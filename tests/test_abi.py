@@ -77,6 +77,8 @@ def test_attention_rejects_bad_arguments(lib):
     assert _attn(lib, ws=None) == FL_E_WORKSPACE
     assert _attn(lib, ws_bytes=16) == FL_E_WORKSPACE
     assert _attn(lib, flags=fl.ATTN_DENSE, rows=DUMMY, k=64) == FL_E_SHAPE   # dense takes rows == NULL
+    assert _attn(lib, k_new=None, v_new=None) == FL_E_NULL   # no new rows: only with reused terms
+    assert _attn(lib, v_new=None) == FL_E_NULL               # new rows come in pairs
     assert b"fl_loop_sparse_attn" in lib.fl_last_error()
 
 
@@ -98,6 +100,12 @@ def test_select_and_codec_reject_bad_arguments(lib):
     assert q(G=48) == FL_E_UNSUPPORTED
     assert q(d=96) == FL_E_SHAPE
     assert q(d=64, G=128, axis=fl.AXIS_CHANNEL) == FL_E_SHAPE    # CHANNEL groups must divide d
+    qc = lambda **kw: lib.fl_kv_residual_quant_commit(DUMMY, kw.get("x_hat", DUMMY), DUMMY, 8, 1, 64, 2, 64,
+                                                      kw.get("bits", 4), 32, fl.AXIS_TOKEN, DUMMY, DUMMY, DUMMY,
+                                                      None)
+    assert qc(x_hat=None) == FL_E_NULL
+    assert qc(bits=3) == FL_E_UNSUPPORTED
+    assert b"fl_kv_residual_quant_commit" in lib.fl_last_error()
     dq = lib.fl_kv_residual_dequant(DUMMY, DUMMY, DUMMY, DUMMY, 8, 1, 64, 2, 64, 4, 32, fl.AXIS_TOKEN, 7, DUMMY,
                                     None, None)
     assert dq == FL_E_UNSUPPORTED                                   # unknown mode

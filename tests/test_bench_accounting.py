@@ -1,6 +1,6 @@
 """Host logic of bench.py: the algorithmic flop and byte counts of one attention launch (both passes, or
-the add pass with stored subtract terms), checked against a brute-force construction of every S_i with the
-oracle's own set definition."""
+the add pass with stored subtract terms, reading new rows from the compact buffers or from the updated
+caches), checked against a brute-force construction of every S_i with the oracle's own set definition."""
 import numpy as np
 
 import bench
@@ -16,12 +16,12 @@ def test_attention_work_counts_match_brute_force():
         slot[b, idx[b]] = np.arange(40)
     cols = np.stack([np.stack([np.sort(np.concatenate([np.arange(4), rng.choice(np.arange(4, N), 30, replace=False)]))
                                for _ in range(H)]) for _ in range(B)]).astype(np.int32)
-    for reuse in (False, True):
-        check(idx, cols, slot, N, H, d, w, B, reuse)
+    for reuse, current in ((False, False), (True, False), (True, True)):
+        check(idx, cols, slot, N, H, d, w, B, reuse, current)
 
 
-def check(idx, cols, slot, N, H, d, w, B, reuse):
-    nbytes, flops = bench.attn_work(idx, cols, slot, N, H, d, w, B, reuse=reuse, keep_terms=True)
+def check(idx, cols, slot, N, H, d, w, B, reuse, current):
+    nbytes, flops = bench.attn_work(idx, cols, slot, N, H, d, w, B, reuse=reuse, keep_terms=True, current=current)
     want_flops = 0
     want_bytes = 0
     for b in range(B):
@@ -31,8 +31,9 @@ def check(idx, cols, slot, N, H, d, w, B, reuse):
                 S = att.row_columns(cols[b, h], int(i), w)
                 want_flops += (4 if reuse else 8) * d * S.size
                 used |= set(S.tolist())
-            n_new = sum(1 for j in used if slot[b, j] >= 0)
-            want_bytes += (len(used) + n_new) * d * 4 + len(used) * 4 + cols.shape[2] * 4
+            n_new = 0 if current else sum(1 for j in used if slot[b, j] >= 0)
+            slots = 0 if current else len(used) * 4
+            want_bytes += (len(used) + n_new) * d * 4 + slots + cols.shape[2] * 4
         k = idx.shape[1]
         q_rows = 1 if reuse else 2
         lse_io = 1 if reuse else 2

@@ -12,7 +12,7 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_util import assert_close, assert_keys_close, down, down_bits16, f16_bits, say, up_bf16
+from gpu_util import assert_close, assert_keys_close, down, down_bits16, f16_bits, new_rows, say, up_bf16
 from oracle import chain
 from workloads import get, make_layer
 
@@ -70,8 +70,8 @@ def test_full_size_chain_matches_oracle(F, name, layer, heads):
             assert np.array_equal(down(out["zero_k"]).view(np.uint16), f16_bits(lr.enc_k["zero"]))
             assert np.array_equal(down(out["scale_v"]).view(np.uint16), f16_bits(lr.enc_v["scale"]))
             assert np.array_equal(down(out["zero_v"]).view(np.uint16), f16_bits(lr.enc_v["zero"]))
-        assert np.array_equal(down_bits16(out["k_new"]), lr.k_new), f"loop {r} new K rows"
-        assert np.array_equal(down_bits16(out["v_new"]), lr.v_new), f"loop {r} new V rows"
+        assert np.array_equal(new_rows(out, "k_new", gs.k_hat), lr.k_new), f"loop {r} new K rows"
+        assert np.array_equal(new_rows(out, "v_new", gs.v_hat), lr.v_new), f"loop {r} new V rows"
         go, gl = down(gs.o), down(gs.lse)
         for b in range(B):
             rows = lr.idx[b]

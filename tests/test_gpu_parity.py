@@ -9,7 +9,7 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_util import (assert_close, assert_keys_close, down, down_bits16, f16_bits, say, up, up_bf16)
+from gpu_util import (assert_close, assert_keys_close, down, down_bits16, f16_bits, new_rows, say, up, up_bf16)
 from oracle import attention as att
 from oracle import chain, codec, select
 from oracle.numerics import bf16_to_f64, f32_to_bf16
@@ -80,7 +80,7 @@ def test_codec_matches_oracle(F, bits, axis, d, G):
                       .astype(np.float32))
     idx = np.stack([np.sort(rng.choice(N, k, replace=False)) for _ in range(B)]).astype(np.int32)
     enc = codec.quantize(cur, ref, idx, bits, G, axis)
-    x_hat, new_rows = codec.reconstruct(ref, cur, idx, enc, bits, G, axis)
+    x_hat, want_rows = codec.reconstruct(ref, cur, idx, enc, bits, G, axis)
     d_ref = up_bf16(ref)
     codes, scale, zero, rows = F.kv_residual_quant(up_bf16(cur), d_ref, up(idx), bits, G, axis)
     torch.cuda.synchronize()
@@ -88,13 +88,22 @@ def test_codec_matches_oracle(F, bits, axis, d, G):
     if bits != 16:
         assert np.array_equal(down(scale).view(np.uint16), f16_bits(enc["scale"])), "scale differs"
         assert np.array_equal(down(zero).view(np.uint16), f16_bits(enc["zero"])), "zero differs"
-    assert np.array_equal(down_bits16(rows), new_rows), "reconstructed rows differ"
+    assert np.array_equal(down_bits16(rows), want_rows), "reconstructed rows differ"
     compact = F.kv_residual_dequant(codes, scale, zero, up(idx), bits, G, axis, d_ref, mode=F.DQ_COMPACT)
     torch.cuda.synchronize()
-    assert np.array_equal(down_bits16(compact), new_rows), "COMPACT dequant differs"
+    assert np.array_equal(down_bits16(compact), want_rows), "COMPACT dequant differs"
     F.kv_residual_dequant(codes, scale, zero, up(idx), bits, G, axis, d_ref, mode=F.DQ_COMMIT)
     torch.cuda.synchronize()
     assert np.array_equal(down_bits16(d_ref), x_hat), "COMMIT dequant differs"
+    # quantize and commit in one pass: same codes and metadata, the cache updated in place
+    d_hat = up_bf16(ref)
+    codes2, scale2, zero2 = F.kv_residual_quant_commit(up_bf16(cur), d_hat, up(idx), bits, G, axis)
+    torch.cuda.synchronize()
+    assert np.array_equal(down(codes2), enc["codes"]), "fused commit: codes differ"
+    if bits != 16:
+        assert np.array_equal(down(scale2).view(np.uint16), f16_bits(enc["scale"])), "fused commit: scale differs"
+        assert np.array_equal(down(zero2).view(np.uint16), f16_bits(enc["zero"])), "fused commit: zero differs"
+    assert np.array_equal(down_bits16(d_hat), x_hat), "fused commit: cache differs"
 
 
 @pytest.mark.parametrize("axis", [codec.AXIS_TOKEN, codec.AXIS_CHANNEL])
@@ -193,8 +202,8 @@ def test_chain_matches_oracle(F, name, over):
             assert np.array_equal(down(out["zero_k"]).view(np.uint16), f16_bits(lr.enc_k["zero"]))
             assert np.array_equal(down(out["scale_v"]).view(np.uint16), f16_bits(lr.enc_v["scale"]))
             assert np.array_equal(down(out["zero_v"]).view(np.uint16), f16_bits(lr.enc_v["zero"]))
-        assert np.array_equal(down_bits16(out["k_new"]), lr.k_new), f"loop {r} new K rows"
-        assert np.array_equal(down_bits16(out["v_new"]), lr.v_new), f"loop {r} new V rows"
+        assert np.array_equal(new_rows(out, "k_new", gs.k_hat), lr.k_new), f"loop {r} new K rows"
+        assert np.array_equal(new_rows(out, "v_new", gs.v_hat), lr.v_new), f"loop {r} new V rows"
         assert_close(down(gs.o), _dict_to_array(lr.o, B, H), f"loop {r} o (chained)")
         assert_close(down(gs.lse), _dict_to_array(lr.lse, B, H), f"loop {r} lse (chained)")
     assert np.array_equal(down_bits16(gs.k_hat), rec.k_hat), "final K cache differs"
