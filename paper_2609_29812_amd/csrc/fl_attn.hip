@@ -91,6 +91,11 @@ __device__ __forceinline__ void lds_barrier() {
 __device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){a, b}, f16x2));
 }
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+// two fp32 values to bf16 (round to nearest even), packed low | high << 16
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){a, b}, bf16x2));
+}
 
 // max / sum of a lane and lane ^ 32 (the two half-waves hold disjoint columns of the same row)
 __device__ __forceinline__ float xor32_max(float x) {
@@ -644,7 +649,9 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
 // lane / 16) with columns 16c + 4g .. +3 of row j, which is exactly the B-operand layout of
 // O^T += V^T P^T when the k order of a 32-column tile is (4g .. 4g+3, 16+4g .. 16+4g+3) for lane group
 // g; the transposed V reads follow that order.  The accumulators of a lane belong to the same row j,
-// so the softmax state never leaves the lane (row reductions are two cross-row swaps).
+// so the softmax state never leaves the lane (row reductions are two cross-row swaps).  V stays bf16 as
+// the LDS-DMA wrote it (no conversion step in the pipeline): P goes in as two bf16 parts, hi = bf16(p)
+// and lo = bf16(p - hi), so p.v takes two bf16 MFMAs and P keeps about 16 significant bits.
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float xor16_max(float x) {
@@ -842,23 +849,6 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
       }
     }
   };
-  // each wave converts, in place, the V rows its own LDS-DMA wrote (bf16 -> fp16, exact for |v| in
-  // [2^-14, 65504]); the barrier that follows publishes them
-  auto convert_v = [=](Slot<D>& sl) {
-    u32x4 w[INST_PER_WAVE];
-#pragma unroll
-    for (int t = 0; t < INST_PER_WAVE; ++t)
-      w[t] = *reinterpret_cast<const u32x4*>(sl.v + inst_of(t) * 512 + lane * 8);
-#pragma unroll
-    for (int t = 0; t < INST_PER_WAVE; ++t) {
-      u32x4 hv;
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        hv[e] = pack_f16x2(__uint_as_float(w[t][e] << 16), __uint_as_float(w[t][e] & 0xFFFF0000u));
-      *reinterpret_cast<u32x4*>(sl.v + inst_of(t) * 512 + lane * 8) = hv;
-    }
-  };
-
   // LDS read offsets (elements) that depend on the lane.  K (A operand): row j16 (+16 for the second
   // column block), chunk 4 ks + g4 = 8 (ks >> 1) + (4 (ks & 1) + g4).  V (transposed reads): lane
   // (g4, t, q) points at dims 16 db + 4q of column 4 g4 + t (+16 for the second half of the k order);
@@ -968,18 +958,29 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
         pr[4 * c + v] = __builtin_amdgcn_exp2f(__builtin_fmaf(sa[c][v], a.scale_log2, -ref));
         lsum += pr[4 * c + v];
       }
-    const u32x4 pa4 = {pack_f16x2(pr[0], pr[1]), pack_f16x2(pr[2], pr[3]), pack_f16x2(pr[4], pr[5]),
-                       pack_f16x2(pr[6], pr[7])};
+    // P as two bf16 parts, p = hi + lo with hi = bf16(p) and lo = bf16(p - hi) (p - hi is exact in fp32), so
+    // V stays bf16 as loaded (no conversion pass) and P keeps about 16 significant bits
+    u32x4 ph, pl;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      ph[e] = pack_bf16x2(pr[2 * e], pr[2 * e + 1]);
+      pl[e] = pack_bf16x2(pr[2 * e] - __uint_as_float(ph[e] << 16), pr[2 * e + 1] - __uint_as_float(ph[e] & 0xFFFF0000u));
+    }
     // O^T += V^T P^T, 16 dims per block, k = the tile's 32 columns in the lane-group order above
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
-      const f16x8 vf = __builtin_bit_cast(f16x8, __builtin_shufflevector(vr[db][0], vr[db][1], 0, 1, 2, 3, 4, 5, 6, 7));
-      acc[db] = __builtin_amdgcn_mfma_f32_16x16x32_f16(vf, __builtin_bit_cast(f16x8, pa4), acc[db], 0, 0, 0);
+      const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(vr[db][0], vr[db][1], 0, 1, 2, 3, 4, 5, 6, 7));
+      acc[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, __builtin_bit_cast(bf16x8, ph), acc[db], 0, 0, 0);
+    }
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(vr[db][0], vr[db][1], 0, 1, 2, 3, 4, 5, 6, 7));
+      acc[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, __builtin_bit_cast(bf16x8, pl), acc[db], 0, 0, 0);
     }
   };
 
-  // ---- pipeline (as in loop_attn_kernel): step s reads the table entries of tiles s+3 and s, waits for
-  // tile s, converts this wave's V rows of it, finalizes the records of tile s+4, passes the barrier,
+  // ---- pipeline (as in loop_attn_kernel, without the V conversion): step s reads the table entries of
+  // tiles s+3 and s, waits for tile s, finalizes the records of tile s+4, passes the barrier,
   // loads the records of tile s+6, LDS-DMAs tile s+3 into the slot tile s-1 used and computes tile s.
   // Every step issues the same number of VMEM ops (one record load + NI DMA), so "tile s has landed" is
   // exactly vmcnt(2 * OPS_PER_STEP) on every path.
@@ -1007,7 +1008,6 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
     const Offs of = tile_offs(u + 3);
     const TileHead th = tile_head(u);
     FL_WAIT_VM(2 * OPS_PER_STEP);
-    convert_v(cur);
     if (rec_wave) store_desc(u + 4, w);
     lds_barrier();
     w = load_desc(u + 6);
