@@ -91,15 +91,11 @@ def attn_work(idx, cols, slot, N, H, d, window, B, reuse=False, keep_terms=True,
 
 
 def codec_bytes(k, H, d, bits, group, axis_token, B):
-    """quantize: read cur + ref rows, write codes + metadata + reconstructed rows."""
+    """quantize: read cur + ref rows, write codes + metadata + reconstructed rows (compact, or committed
+    into the cache in place: the same bytes)."""
     rows = B * k * H * d
     meta = B * (math.ceil(k / group) * H * d if axis_token else k * H * (d // group)) * 2 * 2
     return rows * 2 * 2 + rows * bits / 8 + meta + rows * 2 + B * k * 4
-
-
-def quant_commit_bytes(k, H, d, bits, group, axis_token, B):
-    """quantize and commit in place: read cur + cache rows, write codes + metadata + cache rows."""
-    return codec_bytes(k, H, d, bits, group, axis_token, B)
 
 
 def commit_bytes(k, H, d, bits, group, axis_token, B):
@@ -146,10 +142,8 @@ class Step:
             mass = torch.empty(B, kk, H, dtype=torch.float32, device=kr.device)
             if r == 2:
                 # both passes: quantize (compact new rows), attend, then commit into the caches
-                ck, sk, zk, k_new = timed(f"quant_k r{r}", lambda: fl.kv_residual_quant(
-                    kr, gs.k_hat, idx, bits, gs.group, fl.AXIS_TOKEN))
-                cv, sv, zv, v_new = timed(f"quant_v r{r}", lambda: fl.kv_residual_quant(
-                    vr, gs.v_hat, idx, bits, gs.group, fl.AXIS_CHANNEL))
+                (ck, sk, zk, k_new), (cv, sv, zv, v_new) = timed(f"quant_kv r{r}", lambda: fl.kv_residual_quant_kv(
+                    kr, gs.k_hat, vr, gs.v_hat, idx, bits, gs.group))
                 timed(f"attn r{r}", lambda: fl.loop_sparse_attn(
                     qr, qp, gs.k_hat, gs.v_hat, k_new, v_new, slot, idx, gs.cols, gs.window, gs.lse, gs.o,
                     term_out=term, mass_out=mass))
@@ -159,10 +153,8 @@ class Step:
                     cv, sv, zv, idx, bits, gs.group, fl.AXIS_CHANNEL, gs.v_hat, mode=fl.DQ_COMMIT))
             else:
                 # the add pass alone: quantize and commit in one pass, then attend over the caches
-                timed(f"quant_k r{r}", lambda: fl.kv_residual_quant_commit(
-                    kr, gs.k_hat, idx, bits, gs.group, fl.AXIS_TOKEN))
-                timed(f"quant_v r{r}", lambda: fl.kv_residual_quant_commit(
-                    vr, gs.v_hat, idx, bits, gs.group, fl.AXIS_CHANNEL))
+                timed(f"quant_kv r{r}", lambda: fl.kv_residual_quant_kv(
+                    kr, gs.k_hat, vr, gs.v_hat, idx, bits, gs.group, mode=fl.DQ_COMMIT))
                 timed(f"attn r{r}", lambda: fl.loop_sparse_attn(
                     qr, None, gs.k_hat, gs.v_hat, None, None, slot, idx, gs.cols, gs.window, gs.lse, gs.o,
                     term_prev=gs.term, mass_prev=gs.mass, slot_prev=gs.slot_prev, term_out=term, mass_out=mass))
@@ -346,8 +338,8 @@ def main():
         by, fl_ = attn_work(idx, cols, slot, N, H, d, w.window, B, reuse=r > 2, current=r > 2)
         work = {
             f"select r{r}": (select_bytes(n_cand, N, H * d, kr, B), 0.0),
-            f"quant_k r{r}": (codec_bytes(kr, H, d, bits, w.group, True, B), 0.0),
-            f"quant_v r{r}": (codec_bytes(kr, H, d, bits, w.group, False, B), 0.0),
+            f"quant_kv r{r}": (codec_bytes(kr, H, d, bits, w.group, True, B)
+                               + codec_bytes(kr, H, d, bits, w.group, False, B) - B * kr * 4, 0.0),
             f"attn r{r}": (by, fl_),
         }
         if r == 2:

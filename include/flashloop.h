@@ -109,6 +109,7 @@ int fl_select_tokens(const uint16_t* k_cur, const uint16_t* k_prev,
  *   out_rows : optional bf16 [B, k, H, d]: also write the reconstructed rows
  *              bf16(fp32(x_ref[b,i]) + fp32(z + q*s)) (what fl_kv_residual_dequant COMPACT returns).
  *              May alias x_ref only when idx is NULL (in-place base reconstruction).
+ * With k = 0 nothing is read or written, and codes, scale and zero may be NULL.
  * ---------------------------------------------------------------------------------------------- */
 enum fl_axis { FL_AXIS_TOKEN = 0, FL_AXIS_CHANNEL = 1 };
 
@@ -141,6 +142,24 @@ int fl_kv_residual_dequant(const uint8_t* codes, const uint16_t* scale, const ui
                            const int32_t* idx, int k, int B, int N, int H, int d,
                            int bits, int group, int axis, int mode,
                            uint16_t* x_hat, uint16_t* out_rows, void* stream);
+
+/* (2c) Keys and values of one loop in one call -- Eq. 4 and Appendix D.3, Eq. 8 with the Appendix E
+ * axes: keys on FL_AXIS_TOKEN, values on FL_AXIS_CHANNEL, one bits and group for both.  The outputs
+ * are bitwise those of two fl_kv_residual_quant calls (mode FL_DQ_COMPACT) or of two
+ * fl_kv_residual_quant_commit calls (mode FL_DQ_COMMIT); the two tensors share one kernel launch.
+ *   k_cur, v_cur     : bf16 [B, N, H, d] loop-r keys and values.
+ *   k_ref, v_ref     : bf16 [B, N, H, d] previous reconstructions (NULL for zeros in COMPACT mode);
+ *                      in COMMIT mode both are required, distinct, and rows idx are updated in place.
+ *   k_codes, k_scale, k_zero / v_codes, v_scale, v_zero : as fl_kv_residual_quant for each axis
+ *                      (distinct code buffers).
+ *   k_rows, v_rows   : COMPACT: optional bf16 [B, k, H, d] reconstructed rows (may alias the reference
+ *                      only when idx is NULL).  COMMIT: must be NULL.
+ * Other arguments as fl_kv_residual_quant. */
+int fl_kv_residual_quant_kv(const uint16_t* k_cur, uint16_t* k_ref, const uint16_t* v_cur, uint16_t* v_ref,
+                            const int32_t* idx, int k, int B, int N, int H, int d, int bits, int group,
+                            uint8_t* k_codes, uint16_t* k_scale, uint16_t* k_zero,
+                            uint8_t* v_codes, uint16_t* v_scale, uint16_t* v_zero,
+                            uint16_t* k_rows, uint16_t* v_rows, int mode, void* stream);
 
 /* ------------------------------------------------------------------------------------------------
  * (3) Mass-corrected sparse attention update -- Sections 3.2 and 4.2, Eq. 3; Appendix D.2, Eq. 7.

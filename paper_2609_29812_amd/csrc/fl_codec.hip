@@ -91,11 +91,13 @@ __device__ __forceinline__ void group_meta(float mn, float mx, int qmax, double&
 
 // out_rows: compact [B, k, HD] rows, or (commit) the cache rows idx of x_ref itself, written in place
 // (every element is read before the same thread writes it, after the workgroup's reduction).
+// Body of one workgroup: channel block bx, row group g, batch b.
 template <int BITS, int S, int RPS>
-__global__ __launch_bounds__(256) void quant_token_kernel(
+__device__ __forceinline__ void quant_token_body(
     const uint16_t* __restrict__ x_cur, const uint16_t* x_ref,
     const int32_t* __restrict__ idx, int k, int N, int HD, int G, uint8_t* __restrict__ codes,
-    uint16_t* __restrict__ scale, uint16_t* __restrict__ zero, uint16_t* out_rows, bool commit) {
+    uint16_t* __restrict__ scale, uint16_t* __restrict__ zero, uint16_t* out_rows, bool commit,
+    int bx, int g, int b) {
   constexpr int CH = 256 / S;          // chunks of 8 channels per workgroup
   __shared__ float s_mn[S][CH * 8];
   __shared__ float s_mx[S][CH * 8];
@@ -103,8 +105,7 @@ __global__ __launch_bounds__(256) void quant_token_kernel(
   __shared__ float s_s[CH * 8];
   constexpr int qmax = (1 << BITS) - 1;
   const int slice = threadIdx.x / CH, chunk = threadIdx.x % CH;
-  const int g = blockIdx.y, b = blockIdx.z;
-  const int c0 = blockIdx.x * (CH * 8) + chunk * 8;
+  const int c0 = bx * (CH * 8) + chunk * 8;
   const bool ch_ok = c0 < HD;
   const int ng = (k + G - 1) / G;
 
@@ -145,7 +146,7 @@ __global__ __launch_bounds__(256) void quant_token_kernel(
   __syncthreads();
   if (threadIdx.x < CH * 8) {
     const int ch = threadIdx.x;   // one thread per channel
-    const int c = blockIdx.x * (CH * 8) + ch;
+    const int c = bx * (CH * 8) + ch;
     float a = INFINITY, bb = -INFINITY;
 #pragma unroll
     for (int sl = 0; sl < S; ++sl) {
@@ -193,23 +194,29 @@ __global__ __launch_bounds__(256) void quant_token_kernel(
   }
 }
 
-// ---- values: per-token groups of G channels ----------------------------------------------------------
-// out_rows as for quant_token_kernel (each element is read and written by one thread).
-template <int BITS>
-__global__ __launch_bounds__(256) void quant_channel_kernel(
+template <int BITS, int S, int RPS>
+__global__ __launch_bounds__(256) void quant_token_kernel(
     const uint16_t* __restrict__ x_cur, const uint16_t* x_ref,
     const int32_t* __restrict__ idx, int k, int N, int HD, int G, uint8_t* __restrict__ codes,
     uint16_t* __restrict__ scale, uint16_t* __restrict__ zero, uint16_t* out_rows, bool commit) {
+  quant_token_body<BITS, S, RPS>(x_cur, x_ref, idx, k, N, HD, G, codes, scale, zero, out_rows, commit,
+                                 blockIdx.x, blockIdx.y, blockIdx.z);
+}
+
+// ---- values: per-token groups of G channels ----------------------------------------------------------
+// out_rows as for quant_token_kernel (each element is read and written by one thread).
+// Body of one thread: 8-channel chunk `local` of the k * HD / 8 chunks of batch b.
+template <int BITS>
+__device__ __forceinline__ void quant_channel_body(
+    const uint16_t* __restrict__ x_cur, const uint16_t* x_ref,
+    const int32_t* __restrict__ idx, int k, int N, int HD, int G, uint8_t* __restrict__ codes,
+    uint16_t* __restrict__ scale, uint16_t* __restrict__ zero, uint16_t* out_rows, bool commit,
+    int64_t local, int b) {
   constexpr int qmax = (1 << BITS) - 1;
   const int chunks = HD / 8;
-  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t total = (int64_t)gridDim.y * k * chunks;   // gridDim.y == B
-  const int b = blockIdx.y;
-  const int64_t local = tid;                               // within batch b
   const bool ok = local < (int64_t)k * chunks;
   const int p = ok ? (int)(local / chunks) : 0;
   const int chunk = ok ? (int)(local % chunks) : 0;
-  (void)total;
   const int c0 = chunk * 8;
   float dl[8];
   uint4 ref_raw = make_uint4(0, 0, 0, 0);
@@ -259,6 +266,52 @@ __global__ __launch_bounds__(256) void quant_channel_kernel(
       o.v[t] = ref + (z32 + (float)q[t] * s32);
     }
     store_bf16x8(out_rows + (commit ? roff : ((int64_t)b * k + p) * HD + c0), o);
+  }
+}
+
+template <int BITS>
+__global__ __launch_bounds__(256) void quant_channel_kernel(
+    const uint16_t* __restrict__ x_cur, const uint16_t* x_ref,
+    const int32_t* __restrict__ idx, int k, int N, int HD, int G, uint8_t* __restrict__ codes,
+    uint16_t* __restrict__ scale, uint16_t* __restrict__ zero, uint16_t* out_rows, bool commit) {
+  quant_channel_body<BITS>(x_cur, x_ref, idx, k, N, HD, G, codes, scale, zero, out_rows, commit,
+                           (int64_t)blockIdx.x * blockDim.x + threadIdx.x, blockIdx.y);
+}
+
+// ---- keys and values in one launch -------------------------------------------------------------------
+// The first kx * ky * B workgroups run the key body (token axis), the rest the value body (channel
+// axis), so the two short streams share one launch instead of two dependent ones.
+struct QuantKV {
+  const uint16_t* k_cur;
+  const uint16_t* k_ref;
+  const uint16_t* v_cur;
+  const uint16_t* v_ref;
+  const int32_t* idx;
+  uint8_t* k_codes;
+  uint16_t* k_scale;
+  uint16_t* k_zero;
+  uint8_t* v_codes;
+  uint16_t* v_scale;
+  uint16_t* v_zero;
+  uint16_t* k_rows;
+  uint16_t* v_rows;
+  int k, N, HD, G;
+  int kx, ky, vx;      // key workgroups per (row group, batch) and row groups; value workgroups per batch
+  int commit;
+};
+
+template <int BITS, int S, int RPS>
+__global__ __launch_bounds__(256) void quant_kv_kernel(QuantKV a) {
+  const int nkb = a.kx * a.ky;
+  const int blk = blockIdx.x;
+  const int b = blk / (nkb + a.vx);
+  const int r = blk - b * (nkb + a.vx);
+  if (r < nkb) {
+    quant_token_body<BITS, S, RPS>(a.k_cur, a.k_ref, a.idx, a.k, a.N, a.HD, a.G, a.k_codes, a.k_scale,
+                                   a.k_zero, a.k_rows, a.commit != 0, r % a.kx, r / a.kx, b);
+  } else {
+    quant_channel_body<BITS>(a.v_cur, a.v_ref, a.idx, a.k, a.N, a.HD, a.G, a.v_codes, a.v_scale, a.v_zero,
+                             a.v_rows, a.commit != 0, (int64_t)(r - nkb) * 256 + threadIdx.x, b);
   }
 }
 
@@ -328,11 +381,11 @@ __global__ __launch_bounds__(256) void dequant_kernel(
 static int check_codec_args(const char* fn, const void* codes, const void* a, int k, int B, int N,
                             int H, int d, int bits, int group, int axis, bool need_meta,
                             const void* scale, const void* zero, const void* idx) {
-  FL_REQUIRE(codes && a, FL_E_NULL, "%s: codes and the state pointer are required", fn);
+  FL_REQUIRE((codes || k == 0) && a, FL_E_NULL, "%s: codes and the state pointer are required", fn);
   FL_REQUIRE(B >= 1 && N >= 1 && H >= 1, FL_E_SHAPE, "%s: need B, N, H >= 1", fn);
   FL_REQUIRE(d == 64 || d == 128, FL_E_SHAPE, "%s: head dim %d not in {64, 128}", fn, d);
   FL_REQUIRE((int64_t)N * H * d < ((int64_t)1 << 31), FL_E_SHAPE, "%s: N * H * d too large", fn);
-  FL_REQUIRE(idx != nullptr || k == N, FL_E_SHAPE, "%s: without idx, k must equal N", fn);
+  FL_REQUIRE(idx != nullptr || k == N || k == 0, FL_E_SHAPE, "%s: without idx, k must equal N", fn);
   FL_REQUIRE(k >= 0 && k <= N, FL_E_RANGE, "%s: k=%d outside [0, N]", fn, k);
   FL_REQUIRE(bits == 2 || bits == 4 || bits == 8 || bits == 16, FL_E_UNSUPPORTED,
              "%s: bits=%d not in {2, 4, 8, 16}", fn, bits);
@@ -342,7 +395,7 @@ static int check_codec_args(const char* fn, const void* codes, const void* a, in
                FL_E_UNSUPPORTED, "%s: group=%d must be a power of two in [8, 128]", fn, group);
     FL_REQUIRE(axis == FL_AXIS_TOKEN || d % group == 0, FL_E_SHAPE,
                "%s: CHANNEL axis needs group | d (group=%d, d=%d)", fn, group, d);
-    if (need_meta) FL_REQUIRE(scale && zero, FL_E_NULL, "%s: scale and zero are required", fn);
+    if (need_meta && k > 0) FL_REQUIRE(scale && zero, FL_E_NULL, "%s: scale and zero are required", fn);
   }
   return FL_OK;
 }
@@ -390,6 +443,59 @@ static int residual_quant(const char* fn, const uint16_t* x_cur, const uint16_t*
   return check_launch("quant_channel_kernel");
 }
 
+// Keys (token axis) and values (channel axis) with one bit width and group size.  out rows: compact
+// k_rows / v_rows (each optional), or with commit the rows idx of k_ref / v_ref in place.
+static int residual_quant_kv(const char* fn, const uint16_t* k_cur, uint16_t* k_ref, const uint16_t* v_cur,
+                             uint16_t* v_ref, const int32_t* idx, int k, int B, int N, int H, int d, int bits,
+                             int group, uint8_t* k_codes, uint16_t* k_scale, uint16_t* k_zero, uint8_t* v_codes,
+                             uint16_t* v_scale, uint16_t* v_zero, uint16_t* k_rows, uint16_t* v_rows, bool commit,
+                             void* stream) {
+  int rc = check_codec_args(fn, k_codes, k_cur, k, B, N, H, d, bits, group, FL_AXIS_TOKEN, true, k_scale,
+                            k_zero, idx);
+  if (rc != FL_OK) return rc;
+  rc = check_codec_args(fn, v_codes, v_cur, k, B, N, H, d, bits, group, FL_AXIS_CHANNEL, true, v_scale, v_zero,
+                        idx);
+  if (rc != FL_OK) return rc;
+  if (k == 0) return FL_OK;
+  if (bits == 16) {   // raw payload: two copy launches
+    rc = residual_quant(fn, k_cur, k_ref, idx, k, B, N, H, d, bits, group, FL_AXIS_TOKEN, k_codes, k_scale,
+                        k_zero, commit ? k_ref : k_rows, commit, stream);
+    if (rc != FL_OK) return rc;
+    return residual_quant(fn, v_cur, v_ref, idx, k, B, N, H, d, bits, group, FL_AXIS_CHANNEL, v_codes, v_scale,
+                          v_zero, commit ? v_ref : v_rows, commit, stream);
+  }
+  const int HD = H * d;
+  const int slices = group < 32 ? group : 32;
+  const int cw = 256 / slices * 8;
+  QuantKV a;
+  a.k_cur = k_cur; a.k_ref = k_ref; a.v_cur = v_cur; a.v_ref = v_ref; a.idx = idx;
+  a.k_codes = k_codes; a.k_scale = k_scale; a.k_zero = k_zero;
+  a.v_codes = v_codes; a.v_scale = v_scale; a.v_zero = v_zero;
+  a.k_rows = commit ? k_ref : k_rows;
+  a.v_rows = commit ? v_ref : v_rows;
+  a.k = k; a.N = N; a.HD = HD; a.G = group;
+  a.kx = (HD + cw - 1) / cw;
+  a.ky = (k + group - 1) / group;
+  a.vx = (int)(((int64_t)k * (HD / 8) + 255) / 256);
+  a.commit = commit ? 1 : 0;
+  const int64_t blocks = ((int64_t)a.kx * a.ky + a.vx) * B;
+  FL_REQUIRE(blocks < ((int64_t)1 << 31), FL_E_SHAPE, "%s: grid too large", fn);
+  hipStream_t st = as_stream(stream);
+#define FL_QKV(BB, SS, RR) quant_kv_kernel<BB, SS, RR><<<(unsigned)blocks, 256, 0, st>>>(a)
+#define FL_QKV_BITS(BB)                                   \
+  switch (group) {                                        \
+    case 8: FL_QKV(BB, 8, 1); break;                      \
+    case 16: FL_QKV(BB, 16, 1); break;                    \
+    case 32: FL_QKV(BB, 32, 1); break;                    \
+    case 64: FL_QKV(BB, 32, 2); break;                    \
+    default: FL_QKV(BB, 32, 4); break;                    \
+  }
+  if (bits == 2) { FL_QKV_BITS(2) } else if (bits == 4) { FL_QKV_BITS(4) } else { FL_QKV_BITS(8) }
+#undef FL_QKV_BITS
+#undef FL_QKV
+  return check_launch("quant_kv_kernel");
+}
+
 }  // namespace fl
 
 using namespace fl;
@@ -413,6 +519,28 @@ extern "C" int fl_kv_residual_quant_commit(const uint16_t* x_cur, uint16_t* x_ha
   FL_REQUIRE(x_hat != nullptr, FL_E_NULL, "fl_kv_residual_quant_commit: x_hat is required");
   return residual_quant("fl_kv_residual_quant_commit", x_cur, x_hat, idx, k, B, N, H, d, bits, group, axis,
                         codes, scale, zero, x_hat, true, stream);
+  FL_API_END
+}
+
+extern "C" int fl_kv_residual_quant_kv(const uint16_t* k_cur, uint16_t* k_ref, const uint16_t* v_cur,
+                                       uint16_t* v_ref, const int32_t* idx, int k, int B, int N, int H, int d,
+                                       int bits, int group, uint8_t* k_codes, uint16_t* k_scale, uint16_t* k_zero,
+                                       uint8_t* v_codes, uint16_t* v_scale, uint16_t* v_zero, uint16_t* k_rows,
+                                       uint16_t* v_rows, int mode, void* stream) {
+  FL_API_BEGIN
+  const char* fn = "fl_kv_residual_quant_kv";
+  FL_REQUIRE(mode == FL_DQ_COMPACT || mode == FL_DQ_COMMIT, FL_E_UNSUPPORTED, "%s: bad mode %d", fn, mode);
+  if (mode == FL_DQ_COMMIT) {
+    FL_REQUIRE(k_ref && v_ref, FL_E_NULL, "%s: COMMIT needs k_ref and v_ref", fn);
+    FL_REQUIRE(!k_rows && !v_rows, FL_E_NULL, "%s: COMMIT needs k_rows == v_rows == NULL", fn);
+    FL_REQUIRE(k_ref != v_ref, FL_E_SHAPE, "%s: COMMIT needs distinct key and value caches", fn);
+  } else {
+    FL_REQUIRE(!(k_rows && k_rows == k_ref && idx) && !(v_rows && v_rows == v_ref && idx), FL_E_SHAPE,
+               "%s: rows may alias the reference only when idx is NULL", fn);
+  }
+  FL_REQUIRE(k == 0 || k_codes != v_codes, FL_E_SHAPE, "%s: key and value codes must be distinct buffers", fn);
+  return residual_quant_kv(fn, k_cur, k_ref, v_cur, v_ref, idx, k, B, N, H, d, bits, group, k_codes, k_scale,
+                           k_zero, v_codes, v_scale, v_zero, k_rows, v_rows, mode == FL_DQ_COMMIT, stream);
   FL_API_END
 }
 

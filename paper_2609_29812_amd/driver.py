@@ -63,15 +63,15 @@ def sparse_step(st: LayerState, qr, qp, kr, kp, vr, vp, k_r, bits, keep=False):
     k_new = v_new = None
     if st.reuse and st.term is not None:
         # the add pass alone: commit the new rows first, then attend over the caches
-        ck, sk, zk = fl.kv_residual_quant_commit(kr, st.k_hat, idx, bits, st.group, fl.AXIS_TOKEN)
-        cv, sv, zv = fl.kv_residual_quant_commit(vr, st.v_hat, idx, bits, st.group, fl.AXIS_CHANNEL)
+        (ck, sk, zk, _), (cv, sv, zv, _) = fl.kv_residual_quant_kv(kr, st.k_hat, vr, st.v_hat, idx, bits,
+                                                                   st.group, mode=fl.DQ_COMMIT)
         fl.loop_sparse_attn(qr, None, st.k_hat, st.v_hat, None, None, slot, idx, st.cols, st.window, st.lse,
                             st.o, term_prev=st.term, mass_prev=st.mass, slot_prev=st.slot_prev, term_out=term,
                             mass_out=mass)
     else:
         # both passes: the subtract pass needs the loop r-1 caches, so commit after the attention
-        ck, sk, zk, k_new = fl.kv_residual_quant(kr, st.k_hat, idx, bits, st.group, fl.AXIS_TOKEN)
-        cv, sv, zv, v_new = fl.kv_residual_quant(vr, st.v_hat, idx, bits, st.group, fl.AXIS_CHANNEL)
+        (ck, sk, zk, k_new), (cv, sv, zv, v_new) = fl.kv_residual_quant_kv(kr, st.k_hat, vr, st.v_hat, idx, bits,
+                                                                           st.group)
         fl.loop_sparse_attn(qr, qp, st.k_hat, st.v_hat, k_new, v_new, slot, idx, st.cols, st.window, st.lse,
                             st.o, term_out=term, mass_out=mass)
         fl.kv_residual_dequant(ck, sk, zk, idx, bits, st.group, fl.AXIS_TOKEN, st.k_hat, mode=fl.DQ_COMMIT)

@@ -40,6 +40,8 @@ _SIGNATURES = {
                                            _c_p, _c_p, _c_p, _c_p]),
     "fl_kv_residual_dequant": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i,
                                       _c_i, _c_i, _c_p, _c_p, _c_p]),
+    "fl_kv_residual_quant_kv": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_p, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i,
+                                       _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_i, _c_p]),
     "fl_loop_sparse_attn_ws": (_c_sz, [_c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i]),
     "fl_loop_sparse_attn": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_i, _c_p, _c_i, _c_i,
                                    _c_i, _c_i, _c_i, _c_i, _c_f, _c_i, _c_p, _c_p, _c_p, _c_sz, _c_p]),
@@ -180,6 +182,39 @@ def kv_residual_quant_commit(x_cur, x_hat, idx, bits, group, axis, out=None):
                                             _p(codes), _p(scale), _p(zero), _stream())
     _check(rc, "fl_kv_residual_quant_commit")
     return codes, scale, zero
+
+
+def kv_residual_quant_kv(k_cur, k_ref, v_cur, v_ref, idx, bits, group, mode=DQ_COMPACT, rows=True):
+    """Keys (token axis) and values (channel axis) in one call.  COMPACT: returns
+    ((codes, scale, zero, rows) for keys, the same for values), rows None unless rows=True;
+    COMMIT: rows idx of k_ref / v_ref are updated in place and the rows entries are None."""
+    B, N, H, d = k_cur.shape
+    _dev(k_cur, torch.bfloat16, "k_cur")
+    _dev(v_cur, torch.bfloat16, "v_cur", k_cur.shape)
+    _dev(k_ref, torch.bfloat16, "k_ref", k_cur.shape)
+    _dev(v_ref, torch.bfloat16, "v_ref", k_cur.shape)
+    k = N if idx is None else idx.shape[1]
+    _dev(idx, torch.int32, "idx", None if idx is None else (B, k))
+    dev = k_cur.device
+
+    def outputs(axis):
+        codes = torch.empty(B, k, H, d * bits // 8, dtype=torch.uint8, device=dev)
+        scale = zero = None
+        if bits != 16:
+            shp = meta_shape(B, k, H, d, group, axis)
+            scale = torch.empty(shp, dtype=torch.float16, device=dev)
+            zero = torch.empty(shp, dtype=torch.float16, device=dev)
+        out_rows = None
+        if mode == DQ_COMPACT and rows:
+            out_rows = torch.empty(B, k, H, d, dtype=torch.bfloat16, device=dev)
+        return codes, scale, zero, out_rows
+
+    ko, vo = outputs(AXIS_TOKEN), outputs(AXIS_CHANNEL)
+    rc = load().fl_kv_residual_quant_kv(_p(k_cur), _p(k_ref), _p(v_cur), _p(v_ref), _p(idx), k, B, N, H, d, bits,
+                                        group, _p(ko[0]), _p(ko[1]), _p(ko[2]), _p(vo[0]), _p(vo[1]), _p(vo[2]),
+                                        _p(ko[3]), _p(vo[3]), mode, _stream())
+    _check(rc, "fl_kv_residual_quant_kv")
+    return ko, vo
 
 
 def kv_residual_dequant(codes, scale, zero, idx, bits, group, axis, x_hat, mode=DQ_COMPACT):

@@ -14,6 +14,7 @@ HEADER = os.path.join(ROOT, "include", "flashloop.h")
 
 FL_OK, FL_E_NULL, FL_E_SHAPE, FL_E_RANGE, FL_E_UNSUPPORTED, FL_E_WORKSPACE = 0, 1, 2, 3, 4, 5
 DUMMY = ctypes.c_void_p(0x1000)     # a non-NULL device pointer stand-in, never dereferenced on the host
+DUMMY2 = ctypes.c_void_p(0x2000)    # a second, distinct stand-in
 
 
 def declared_functions():
@@ -106,6 +107,18 @@ def test_select_and_codec_reject_bad_arguments(lib):
     assert qc(x_hat=None) == FL_E_NULL
     assert qc(bits=3) == FL_E_UNSUPPORTED
     assert b"fl_kv_residual_quant_commit" in lib.fl_last_error()
+    qkv = lambda **kw: lib.fl_kv_residual_quant_kv(
+        DUMMY, kw.get("kr", DUMMY), DUMMY, kw.get("vr", DUMMY2), DUMMY, 8, 1, 64, 2, 64, kw.get("bits", 4), 32,
+        DUMMY, DUMMY, DUMMY, kw.get("vc", DUMMY2), DUMMY, DUMMY, kw.get("krows"), kw.get("vrows"),
+        kw.get("mode", fl.DQ_COMPACT), None)
+    assert qkv(mode=2) == FL_E_UNSUPPORTED
+    assert qkv(bits=3) == FL_E_UNSUPPORTED
+    assert qkv(mode=fl.DQ_COMMIT, vr=None) == FL_E_NULL           # commit needs both caches
+    assert qkv(mode=fl.DQ_COMMIT, krows=DUMMY2) == FL_E_NULL      # commit takes no compact rows
+    assert qkv(mode=fl.DQ_COMMIT, vr=DUMMY) == FL_E_SHAPE         # one cache for keys and values
+    assert qkv(krows=DUMMY) == FL_E_SHAPE                         # rows alias the reference with idx
+    assert qkv(vc=DUMMY) == FL_E_SHAPE                            # shared code buffer
+    assert b"fl_kv_residual_quant_kv" in lib.fl_last_error()
     dq = lib.fl_kv_residual_dequant(DUMMY, DUMMY, DUMMY, DUMMY, 8, 1, 64, 2, 64, 4, 32, fl.AXIS_TOKEN, 7, DUMMY,
                                     None, None)
     assert dq == FL_E_UNSUPPORTED                                   # unknown mode

@@ -106,6 +106,62 @@ def test_codec_matches_oracle(F, bits, axis, d, G):
     assert np.array_equal(down_bits16(d_hat), x_hat), "fused commit: cache differs"
 
 
+def _check_enc(got, enc, bits, what):
+    codes, scale, zero = got[:3]
+    assert np.array_equal(down(codes), enc["codes"]), f"{what}: codes differ"
+    if bits != 16:
+        assert np.array_equal(down(scale).view(np.uint16), f16_bits(enc["scale"])), f"{what}: scale differs"
+        assert np.array_equal(down(zero).view(np.uint16), f16_bits(enc["zero"])), f"{what}: zero differs"
+
+
+@pytest.mark.parametrize("bits", [2, 4, 8, 16])
+@pytest.mark.parametrize("d,G,k", [(64, 8, 77), (64, 16, 150), (64, 32, 1), (128, 64, 150), (128, 128, 300)])
+def test_codec_kv_pair_matches_oracle(F, bits, d, G, k):
+    """Keys on the token axis and values on the channel axis in one launch, compact and committed."""
+    rng = np.random.default_rng(bits * 1000 + d + G + k)
+    B, N, H = 2, 300, 3
+    kref, vref = _bf16(rng, (B, N, H, d)), _bf16(rng, (B, N, H, d))
+    step = lambda x: f32_to_bf16(bf16_to_f64(x).astype(np.float32)
+                                 + (rng.standard_normal((B, N, H, d)) * 0.05).astype(np.float32))
+    kcur, vcur = step(kref), step(vref)
+    idx = np.stack([np.sort(rng.choice(N, k, replace=False)) for _ in range(B)]).astype(np.int32)
+    want = {}
+    for name, cur, ref, axis in (("k", kcur, kref, codec.AXIS_TOKEN), ("v", vcur, vref, codec.AXIS_CHANNEL)):
+        enc = codec.quantize(cur, ref, idx, bits, G, axis)
+        want[name] = (enc,) + tuple(codec.reconstruct(ref, cur, idx, enc, bits, G, axis))
+    dk, dv = up_bf16(kref), up_bf16(vref)
+    ko, vo = F.kv_residual_quant_kv(up_bf16(kcur), dk, up_bf16(vcur), dv, up(idx), bits, G)
+    torch.cuda.synchronize()
+    for name, got in (("k", ko), ("v", vo)):
+        enc, _, rows = want[name]
+        _check_enc(got, enc, bits, f"pair {name}")
+        assert np.array_equal(down_bits16(got[3]), rows), f"pair {name}: reconstructed rows differ"
+    assert np.array_equal(down_bits16(dk), kref) and np.array_equal(down_bits16(dv), vref), "COMPACT wrote refs"
+    ko, vo = F.kv_residual_quant_kv(up_bf16(kcur), dk, up_bf16(vcur), dv, up(idx), bits, G, rows=False)
+    torch.cuda.synchronize()
+    assert ko[3] is None and vo[3] is None
+    _check_enc(ko, want["k"][0], bits, "pair k (no rows)")
+    _check_enc(vo, want["v"][0], bits, "pair v (no rows)")
+    ko, vo = F.kv_residual_quant_kv(up_bf16(kcur), dk, up_bf16(vcur), dv, up(idx), bits, G, mode=F.DQ_COMMIT)
+    torch.cuda.synchronize()
+    _check_enc(ko, want["k"][0], bits, "pair commit k")
+    _check_enc(vo, want["v"][0], bits, "pair commit v")
+    assert np.array_equal(down_bits16(dk), want["k"][1]), "pair commit: key cache differs"
+    assert np.array_equal(down_bits16(dv), want["v"][1]), "pair commit: value cache differs"
+
+
+def test_codec_kv_pair_empty_selection(F):
+    rng = np.random.default_rng(9)
+    B, N, H, d = 1, 40, 2, 64
+    kref, vref = _bf16(rng, (B, N, H, d)), _bf16(rng, (B, N, H, d))
+    dk, dv = up_bf16(kref), up_bf16(vref)
+    idx = torch.empty(B, 0, dtype=torch.int32, device="cuda")
+    ko, vo = F.kv_residual_quant_kv(up_bf16(kref), dk, up_bf16(vref), dv, idx, 4, 32, mode=F.DQ_COMMIT)
+    torch.cuda.synchronize()
+    assert ko[0].numel() == 0 and vo[0].numel() == 0
+    assert np.array_equal(down_bits16(dk), kref) and np.array_equal(down_bits16(dv), vref)
+
+
 @pytest.mark.parametrize("axis", [codec.AXIS_TOKEN, codec.AXIS_CHANNEL])
 def test_base_codec_all_rows(F, axis):
     rng = np.random.default_rng(5 + axis)
