@@ -240,6 +240,9 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
   const int tD = (pb - pa + kBN - 1) / kBN;
   const int n_old = tA + tB;             // tiles staged from the cache state
   const int n_tiles = n_old + tC + tD;
+  // band tiles run upward in even row tiles and downward in odd ones, so two neighbouring row tiles
+  // (dispatched together on one XCD) read the band columns they share at about the same time
+  const bool band_down = (rt & 1) != 0;
 
   // ---- tile descriptors ----------------------------------------------------------------------------
   // Every tile is described by 32 records (column, aux): list entries (column, slot), band columns
@@ -256,7 +259,8 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
     const int start = inA ? 0 : inB ? tA : inC ? n_old : n_old + tC;
     const int base = inA ? recA : inB ? recB + bandLo : inC ? recC : recD + pa;
     const int cnt = inA ? nA : inB ? bandHi - bandLo + 1 : inC ? nC : pb - pa;
-    const int i = (v - start) * kBN + c32;
+    const int t = (band_down && inB && !inA) ? tB - 1 - (v - start) : v - start;
+    const int i = t * kBN + c32;
     const uint32_t off = lane >= kBN ? kOOB : i < cnt ? (uint32_t)(base + i) * 8u : sentinel;
     return __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(recR, off, 0, 0));
   };
@@ -771,6 +775,7 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
   const int tD = (pb - pa + kBN - 1) / kBN;
   const int n_old = tA + tB;
   const int n_tiles = n_old + tC + tD;
+  const bool band_down = (rt & 1) != 0;   // band tile order as in loop_attn_kernel
 
   // ---- tile descriptors (records as in the four-phase layout; see attn_prep_kernel) -----------------
   const int c32 = lane & 31;
@@ -781,7 +786,8 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
     const int start = inA ? 0 : inB ? tA : inC ? n_old : n_old + tC;
     const int base = inA ? recA : inB ? recB + bandLo : inC ? recC : recD + pa;
     const int cnt = inA ? nA : inB ? bandHi - bandLo + 1 : inC ? nC : pb - pa;
-    const int i = (v - start) * kBN + c32;
+    const int t = (band_down && inB && !inA) ? tB - 1 - (v - start) : v - start;
+    const int i = t * kBN + c32;
     const uint32_t off = lane >= kBN ? kOOB : i < cnt ? (uint32_t)(base + i) * 8u : sentinel;
     return __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(recR, off, 0, 0));
   };
