@@ -670,7 +670,9 @@ __device__ __forceinline__ float xor16_add(float x) {
 __device__ __forceinline__ float row4_max(float x) { return xor32_max(xor16_max(x)); }
 __device__ __forceinline__ float row4_add(float x) { return xor32_add(xor16_add(x)); }
 
-template <int D>
+// CUR: the caches already hold this loop's rows (no new-row tiles and no updated columns), so tiles are
+// described straight from the column list and the band range, without the prep kernel's records.
+template <int D, bool CUR>
 __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
   constexpr int BM = 64;                  // rows per workgroup (4 waves x 16)
   constexpr int KS = D / 32;              // k-steps of QK^T (32 dims each)
@@ -736,23 +738,30 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
   const int recC = a.off_upd + bh * a.c_list;
   const int recB = a.off_band + b * a.N;
   const int recD = a.off_rows + b * a.k;
-  const int2* descp = a.rec + recA;
-  const int2* updp = a.rec + recC;
+  const int2* descp = CUR ? nullptr : a.rec + recA;
+  const int2* updp = CUR ? nullptr : a.rec + recC;
   if (tid < 2) {
     int n = 0;
-    if (a.c_list > 0) {
+    if (a.c_list > 0 && !(CUR && tid == 1)) {
       // tid 0: list entries with j + window <= max_row; tid 1: the same among the updated entries
-      const int2* lp = tid == 0 ? descp : updp;
-      const int len = tid == 0 ? a.c_list : a.n_upd[(int64_t)b * a.H + h];
       const int lim = max_row - a.window;
-      int lo = 0, hi = len;
-      while (lo < hi) {
-        const int mid = (lo + hi) >> 1;
-        if (lp[mid].x <= lim) lo = mid + 1; else hi = mid;
+      int lo = 0, hi = tid == 0 ? a.c_list : a.n_upd[(int64_t)b * a.H + h];
+      if constexpr (CUR) {
+        const int32_t* cp = a.cols + (int64_t)bh * a.c_list;
+        while (lo < hi) {
+          const int mid = (lo + hi) >> 1;
+          if (cp[mid] <= lim) lo = mid + 1; else hi = mid;
+        }
+      } else {
+        const int2* lp = tid == 0 ? descp : updp;
+        while (lo < hi) {
+          const int mid = (lo + hi) >> 1;
+          if (lp[mid].x <= lim) lo = mid + 1; else hi = mid;
+        }
       }
       n = lo;
     }
-    s_meta[tid] = (tid == 1 && a.cache_current) ? 0 : n;   // current caches: no new-row tiles
+    s_meta[tid] = n;                      // (current caches: no new-row tiles)
   }
   const int bandLo = a.window > 0 ? max(0, min_row - a.window + 1) : 0;
   const int bandHi = a.window > 0 ? max_row : -1;
@@ -764,7 +773,7 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
       if (rowp[mid] < bandLo) lo = mid + 1; else hi = mid;
     }
     pa = lo;
-    pb = a.cache_current ? lo : last_p + 1;
+    pb = CUR ? lo : last_p + 1;
   }
   __syncthreads();
   const int nA = s_meta[0];
@@ -781,7 +790,23 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
   const int c32 = lane & 31;
   const rsrc_t recR = make_rsrc(a.rec, a.rec_bytes);
   const uint32_t sentinel = (uint32_t)a.off_sent * 8u;
+  // CUR: entry i of tile v is list entry i of (b, h) or band column bandLo + i (kPad past the end); the
+  // list entry is loaded here and the id formed when the tile is described, so the load stays in flight
+  const rsrc_t colR = make_rsrc(a.cols, CUR ? (uint32_t)a.B * a.H * a.c_list * 4u : 0u);
+  auto cur_entry = [=](int v, int& i, bool& list, bool& ok) {
+    list = v < tA;
+    const int t = list ? v : band_down ? tB - 1 - (v - tA) : v - tA;
+    i = t * kBN + c32;
+    ok = lane < kBN && v < n_old && i < (list ? nA : bandHi - bandLo + 1);
+  };
   auto load_desc = [=](int v) -> u32x2 {
+    if constexpr (CUR) {
+      int i;
+      bool list, ok;
+      cur_entry(v, i, list, ok);
+      const uint32_t off = ok && list ? (uint32_t)(recA + i) * 4u : kOOB;
+      return u32x2{(uint32_t)__builtin_amdgcn_raw_buffer_load_b32(colR, off, 0, 0), 0u};
+    }
     const bool inA = v < tA, inB = v < n_old, inC = v < n_old + tC;   // uniform
     const int start = inA ? 0 : inB ? tA : inC ? n_old : n_old + tC;
     const int base = inA ? recA : inB ? recB + bandLo : inC ? recC : recD + pa;
@@ -796,15 +821,21 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
   const rsrc_t kcR = make_rsrc(a.k_cache + (int64_t)b * a.N * HD, (uint32_t)a.N * rb);
   const rsrc_t vcR = make_rsrc(a.v_cache + (int64_t)b * a.N * HD, (uint32_t)a.N * rb);
   // (with current caches there are no new rows: an empty range makes every access to them read zero)
-  const uint32_t new_bytes = a.cache_current ? 0u : (uint32_t)a.k * rb;
-  const rsrc_t knR = make_rsrc(a.cache_current ? a.k_cache : a.k_new + (int64_t)b * a.k * HD, new_bytes);
-  const rsrc_t vnR = make_rsrc(a.cache_current ? a.v_cache : a.v_new + (int64_t)b * a.k * HD, new_bytes);
+  const uint32_t new_bytes = CUR ? 0u : (uint32_t)a.k * rb;
+  const rsrc_t knR = make_rsrc(CUR ? a.k_cache : a.k_new + (int64_t)b * a.k * HD, new_bytes);
+  const rsrc_t vnR = make_rsrc(CUR ? a.v_cache : a.v_new + (int64_t)b * a.k * HD, new_bytes);
 
   auto store_desc = [=](int v, u32x2 w) {
     const bool newer = v >= n_old;
-    const int cid = (int)w[0];
+    int cid = (int)w[0];
     const int aux = (int)w[1];
-    const bool upd = !newer && aux >= 0 && !a.cache_current;   // updated this loop, staged from the cache
+    if constexpr (CUR) {
+      int i;
+      bool list, ok;
+      cur_entry(v, i, list, ok);
+      cid = !ok ? kPad : list ? cid : bandLo + i;
+    }
+    const bool upd = !CUR && !newer && aux >= 0;   // updated this loop, staged from the cache
     const int row = newer ? aux : cid;
     const bool valid = cid != kPad;
     if (lane < kBN) {
@@ -1236,7 +1267,7 @@ static int loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev, const
   a.H = H;
   a.scale_log2 = sm_scale * 1.4426950408889634f;
   a.cache_current = (!dense && reuse && k_new == nullptr) ? 1 : 0;
-  if (!dense) {
+  if (!dense && !a.cache_current) {       // (current caches: tiles come straight from cols and the band)
     const RecLayout L = rec_layout(B, N, H, k, c_list);
     int2* rec = static_cast<int2*>(ws);
     int32_t* n_upd = reinterpret_cast<int32_t*>(rec + L.n_rec);
@@ -1266,8 +1297,13 @@ static int loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev, const
     else loop_attn_kernel<64, kFull><<<grid, 256, 0, st>>>(a);
     return check_launch("loop_attn_kernel");
   }
-  if (d == 128) reuse_attn_kernel<128><<<grid, 256, 0, st>>>(a);
-  else reuse_attn_kernel<64><<<grid, 256, 0, st>>>(a);
+#define FL_REUSE(DD, CC) reuse_attn_kernel<DD, CC><<<grid, 256, 0, st>>>(a)
+  if (a.cache_current) {
+    if (d == 128) FL_REUSE(128, true); else FL_REUSE(64, true);
+  } else {
+    if (d == 128) FL_REUSE(128, false); else FL_REUSE(64, false);
+  }
+#undef FL_REUSE
   return check_launch("reuse_attn_kernel");
 }
 
