@@ -147,10 +147,8 @@ class Step:
                 timed(f"attn r{r}", lambda: fl.loop_sparse_attn(
                     qr, qp, gs.k_hat, gs.v_hat, k_new, v_new, slot, idx, gs.cols, gs.window, gs.lse, gs.o,
                     term_out=term, mass_out=mass))
-                timed(f"commit_k r{r}", lambda: fl.kv_residual_dequant(
-                    ck, sk, zk, idx, bits, gs.group, fl.AXIS_TOKEN, gs.k_hat, mode=fl.DQ_COMMIT))
-                timed(f"commit_v r{r}", lambda: fl.kv_residual_dequant(
-                    cv, sv, zv, idx, bits, gs.group, fl.AXIS_CHANNEL, gs.v_hat, mode=fl.DQ_COMMIT))
+                timed(f"commit_kv r{r}", lambda: fl.kv_residual_dequant_kv(
+                    (ck, sk, zk), (cv, sv, zv), idx, bits, gs.group, gs.k_hat, gs.v_hat, mode=fl.DQ_COMMIT))
             else:
                 # the add pass alone: quantize and commit in one pass, then attend over the caches
                 timed(f"quant_kv r{r}", lambda: fl.kv_residual_quant_kv(
@@ -343,8 +341,8 @@ def main():
             f"attn r{r}": (by, fl_),
         }
         if r == 2:
-            work[f"commit_k r{r}"] = (commit_bytes(kr, H, d, bits, w.group, True, B), 0.0)
-            work[f"commit_v r{r}"] = (commit_bytes(kr, H, d, bits, w.group, False, B), 0.0)
+            work[f"commit_kv r{r}"] = (commit_bytes(kr, H, d, bits, w.group, True, B)
+                                       + commit_bytes(kr, H, d, bits, w.group, False, B) - B * kr * 4, 0.0)
         for name, (nb, nf) in work.items():
             us = dur_us[name]
             kernels[name] = {"us": round(us, 2), "GB/s": round(nb / us / 1e3, 1),

@@ -161,6 +161,18 @@ int fl_kv_residual_quant_kv(const uint16_t* k_cur, uint16_t* k_ref, const uint16
                             uint8_t* v_codes, uint16_t* v_scale, uint16_t* v_zero,
                             uint16_t* k_rows, uint16_t* v_rows, int mode, void* stream);
 
+/* (2d) Reconstruction of keys and values in one call -- Eq. 4 and Appendix D.3, Eq. 8 with the axes of
+ * (2c).  Bitwise the results of fl_kv_residual_dequant for the keys (FL_AXIS_TOKEN) and the values
+ * (FL_AXIS_CHANNEL) with the same bits, group and mode; one kernel launch.
+ *   mode FL_DQ_COMPACT : k_rows and v_rows (bf16 [B, k, H, d]) are required; k_hat, v_hat are read only.
+ *   mode FL_DQ_COMMIT  : rows idx of k_hat and v_hat (distinct) are updated in place; k_rows = v_rows = NULL.
+ * Other arguments as fl_kv_residual_dequant. */
+int fl_kv_residual_dequant_kv(const uint8_t* k_codes, const uint16_t* k_scale, const uint16_t* k_zero,
+                              const uint8_t* v_codes, const uint16_t* v_scale, const uint16_t* v_zero,
+                              const int32_t* idx, int k, int B, int N, int H, int d, int bits, int group,
+                              int mode, uint16_t* k_hat, uint16_t* v_hat, uint16_t* k_rows,
+                              uint16_t* v_rows, void* stream);
+
 /* ------------------------------------------------------------------------------------------------
  * (3) Mass-corrected sparse attention update -- Sections 3.2 and 4.2, Eq. 3; Appendix D.2, Eq. 7.
  *

@@ -333,14 +333,13 @@ __global__ __launch_bounds__(256) void passthrough_kernel(const uint16_t* __rest
 }
 
 // ---- dequantization / reconstruction ------------------------------------------------------------------
+// One thread: 8-channel chunk `local` of the k * HD / 8 chunks of batch b.
 template <int BITS, int AXIS>
-__global__ __launch_bounds__(256) void dequant_kernel(
+__device__ __forceinline__ void dequant_body(
     const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scale,
     const uint16_t* __restrict__ zero, const int32_t* __restrict__ idx, int k, int N, int HD, int G,
-    uint16_t* x_hat, uint16_t* out_rows) {
+    uint16_t* x_hat, uint16_t* out_rows, int64_t local, int b) {
   const int chunks = HD / 8;
-  const int64_t local = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int b = blockIdx.y;
   if (local >= (int64_t)k * chunks) return;
   const int p = (int)(local / chunks), c0 = (int)(local % chunks) * 8;
   const int64_t i = idx ? (int64_t)idx[(int64_t)b * k + p] : (int64_t)p;
@@ -376,6 +375,42 @@ __global__ __launch_bounds__(256) void dequant_kernel(
     for (int t = 0; t < 8; ++t) o.v[t] = x.v[t] + (z8[t] + (float)q[t] * s8[t]);
     store_bf16x8(dst, o);
   }
+}
+
+template <int BITS, int AXIS>
+__global__ __launch_bounds__(256) void dequant_kernel(
+    const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scale,
+    const uint16_t* __restrict__ zero, const int32_t* __restrict__ idx, int k, int N, int HD, int G,
+    uint16_t* x_hat, uint16_t* out_rows) {
+  dequant_body<BITS, AXIS>(codes, scale, zero, idx, k, N, HD, G, x_hat, out_rows,
+                           (int64_t)blockIdx.x * blockDim.x + threadIdx.x, blockIdx.y);
+}
+
+// Keys (token axis) in workgroups [0, half) and values (channel axis) in [half, 2 half) of one launch.
+struct DequantKV {
+  const uint8_t* k_codes;
+  const uint16_t* k_scale;
+  const uint16_t* k_zero;
+  const uint8_t* v_codes;
+  const uint16_t* v_scale;
+  const uint16_t* v_zero;
+  const int32_t* idx;
+  uint16_t* k_hat;
+  uint16_t* v_hat;
+  uint16_t* k_rows;
+  uint16_t* v_rows;
+  int k, N, HD, G, half;
+};
+
+template <int BITS>
+__global__ __launch_bounds__(256) void dequant_kv_kernel(DequantKV a) {
+  const int bx = blockIdx.x;
+  if (bx < a.half)
+    dequant_body<BITS, FL_AXIS_TOKEN>(a.k_codes, a.k_scale, a.k_zero, a.idx, a.k, a.N, a.HD, a.G, a.k_hat,
+                                      a.k_rows, (int64_t)bx * 256 + threadIdx.x, blockIdx.y);
+  else
+    dequant_body<BITS, FL_AXIS_CHANNEL>(a.v_codes, a.v_scale, a.v_zero, a.idx, a.k, a.N, a.HD, a.G, a.v_hat,
+                                        a.v_rows, (int64_t)(bx - a.half) * 256 + threadIdx.x, blockIdx.y);
 }
 
 static int check_codec_args(const char* fn, const void* codes, const void* a, int k, int B, int N,
@@ -541,6 +576,47 @@ extern "C" int fl_kv_residual_quant_kv(const uint16_t* k_cur, uint16_t* k_ref, c
   FL_REQUIRE(k == 0 || k_codes != v_codes, FL_E_SHAPE, "%s: key and value codes must be distinct buffers", fn);
   return residual_quant_kv(fn, k_cur, k_ref, v_cur, v_ref, idx, k, B, N, H, d, bits, group, k_codes, k_scale,
                            k_zero, v_codes, v_scale, v_zero, k_rows, v_rows, mode == FL_DQ_COMMIT, stream);
+  FL_API_END
+}
+
+extern "C" int fl_kv_residual_dequant_kv(const uint8_t* k_codes, const uint16_t* k_scale, const uint16_t* k_zero,
+                                         const uint8_t* v_codes, const uint16_t* v_scale, const uint16_t* v_zero,
+                                         const int32_t* idx, int k, int B, int N, int H, int d, int bits, int group,
+                                         int mode, uint16_t* k_hat, uint16_t* v_hat, uint16_t* k_rows,
+                                         uint16_t* v_rows, void* stream) {
+  FL_API_BEGIN
+  const char* fn = "fl_kv_residual_dequant_kv";
+  int rc = check_codec_args(fn, k_codes, k_hat, k, B, N, H, d, bits, group, FL_AXIS_TOKEN, true, k_scale, k_zero,
+                            idx);
+  if (rc != FL_OK) return rc;
+  rc = check_codec_args(fn, v_codes, v_hat, k, B, N, H, d, bits, group, FL_AXIS_CHANNEL, true, v_scale, v_zero, idx);
+  if (rc != FL_OK) return rc;
+  FL_REQUIRE(mode == FL_DQ_COMPACT || mode == FL_DQ_COMMIT, FL_E_UNSUPPORTED, "%s: bad mode %d", fn, mode);
+  FL_REQUIRE(mode == FL_DQ_COMMIT ? (!k_rows && !v_rows) : (k_rows && v_rows), FL_E_NULL,
+             "%s: COMPACT needs k_rows and v_rows, COMMIT needs both NULL", fn);
+  FL_REQUIRE(mode == FL_DQ_COMPACT || k_hat != v_hat, FL_E_SHAPE, "%s: COMMIT needs distinct caches", fn);
+  if (k == 0) return FL_OK;
+  const int64_t half = ((int64_t)k * (H * d / 8) + 255) / 256;
+  FL_REQUIRE(2 * half < ((int64_t)1 << 31), FL_E_SHAPE, "%s: grid too large", fn);
+  DequantKV a;
+  a.k_codes = k_codes; a.k_scale = k_scale; a.k_zero = k_zero;
+  a.v_codes = v_codes; a.v_scale = v_scale; a.v_zero = v_zero;
+  a.idx = idx; a.k_hat = k_hat; a.v_hat = v_hat;
+  a.k_rows = mode == FL_DQ_COMMIT ? nullptr : k_rows;
+  a.v_rows = mode == FL_DQ_COMMIT ? nullptr : v_rows;
+  a.k = k; a.N = N; a.HD = H * d; a.G = group; a.half = (int)half;
+  dim3 grid((unsigned)(2 * half), B);
+  hipStream_t st = as_stream(stream);
+  if (bits == 16) {   // raw payload: both axes copy the same way
+    dequant_kv_kernel<16><<<grid, 256, 0, st>>>(a);
+  } else if (bits == 2) {
+    dequant_kv_kernel<2><<<grid, 256, 0, st>>>(a);
+  } else if (bits == 4) {
+    dequant_kv_kernel<4><<<grid, 256, 0, st>>>(a);
+  } else {
+    dequant_kv_kernel<8><<<grid, 256, 0, st>>>(a);
+  }
+  return check_launch("dequant_kv_kernel");
   FL_API_END
 }
 

@@ -209,10 +209,12 @@ __global__ __launch_bounds__(kTopkThreads) void topk_select_kernel(
     }
   }
 
-  // k-th largest key: (1) histogram of the top kHistBits bits and the bin that holds it
+  // k-th largest key: (1) histogram of the top kHistBits bits and the bin that holds it.  With k == n
+  // every position is taken and no threshold is needed.
+  const bool take_all = k == n;
   uint32_t prefix = 0, mask = 0;
-  int krem = k;
-  if (k > 0) {                                            // uniform
+  int krem = take_all ? 0 : k;
+  if (k > 0 && !take_all) {                               // uniform
     for (int i = t; i < kBins; i += kTopkThreads) hist[i] = 0;
     __syncthreads();
     WaveHist wh;
@@ -277,8 +279,8 @@ __global__ __launch_bounds__(kTopkThreads) void topk_select_kernel(
 #pragma unroll
   for (int j = 0; j < M; ++j) {
     const bool valid = k > 0 && t + kTopkThreads * j < n;
-    const uint64_t g = __builtin_amdgcn_ballot_w64(valid && u[j] > prefix);
-    const uint64_t e = __builtin_amdgcn_ballot_w64(valid && u[j] == prefix);
+    const uint64_t g = __builtin_amdgcn_ballot_w64(valid && (take_all || u[j] > prefix));
+    const uint64_t e = __builtin_amdgcn_ballot_w64(valid && !take_all && u[j] == prefix);
     const int w0 = (kTopkThreads * j + 64 * wave) >> 5;
     if (lane == 0) { bm_gt[w0] = (uint32_t)g; bm_eq[w0] = (uint32_t)e; }
     if (lane == 1) { bm_gt[w0 + 1] = (uint32_t)(g >> 32); bm_eq[w0 + 1] = (uint32_t)(e >> 32); }

@@ -74,8 +74,8 @@ def sparse_step(st: LayerState, qr, qp, kr, kp, vr, vp, k_r, bits, keep=False):
                                                                            st.group)
         fl.loop_sparse_attn(qr, qp, st.k_hat, st.v_hat, k_new, v_new, slot, idx, st.cols, st.window, st.lse,
                             st.o, term_out=term, mass_out=mass)
-        fl.kv_residual_dequant(ck, sk, zk, idx, bits, st.group, fl.AXIS_TOKEN, st.k_hat, mode=fl.DQ_COMMIT)
-        fl.kv_residual_dequant(cv, sv, zv, idx, bits, st.group, fl.AXIS_CHANNEL, st.v_hat, mode=fl.DQ_COMMIT)
+        fl.kv_residual_dequant_kv((ck, sk, zk), (cv, sv, zv), idx, bits, st.group, st.k_hat, st.v_hat,
+                                  mode=fl.DQ_COMMIT)
     st.term, st.mass, st.slot_prev = term, mass, slot
     st.cand = idx
     if keep:   # (k_new / v_new are None when the loop committed straight into the caches)

@@ -40,6 +40,8 @@ _SIGNATURES = {
                                            _c_p, _c_p, _c_p, _c_p]),
     "fl_kv_residual_dequant": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i,
                                       _c_i, _c_i, _c_p, _c_p, _c_p]),
+    "fl_kv_residual_dequant_kv": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_i, _c_i, _c_i, _c_i, _c_i,
+                                         _c_i, _c_i, _c_i, _c_p, _c_p, _c_p, _c_p, _c_p]),
     "fl_kv_residual_quant_kv": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_p, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i,
                                        _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_i, _c_p]),
     "fl_loop_sparse_attn_ws": (_c_sz, [_c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i]),
@@ -215,6 +217,31 @@ def kv_residual_quant_kv(k_cur, k_ref, v_cur, v_ref, idx, bits, group, mode=DQ_C
                                         _p(ko[3]), _p(vo[3]), mode, _stream())
     _check(rc, "fl_kv_residual_quant_kv")
     return ko, vo
+
+
+def kv_residual_dequant_kv(k_enc, v_enc, idx, bits, group, k_hat, v_hat, mode=DQ_COMPACT):
+    """Keys (token axis) and values (channel axis) in one call; k_enc / v_enc = (codes, scale, zero).
+    COMPACT: returns (key rows, value rows) [B, k, H, d]; COMMIT: updates k_hat and v_hat in place."""
+    B, N, H, d = k_hat.shape
+    _dev(k_hat, torch.bfloat16, "k_hat")
+    _dev(v_hat, torch.bfloat16, "v_hat", k_hat.shape)
+    k = N if idx is None else idx.shape[1]
+    _dev(idx, torch.int32, "idx", None if idx is None else (B, k))
+    for name, enc, axis in (("k", k_enc, AXIS_TOKEN), ("v", v_enc, AXIS_CHANNEL)):
+        _dev(enc[0], torch.uint8, f"{name} codes", (B, k, H, d * bits // 8))
+        if bits != 16:
+            shp = meta_shape(B, k, H, d, group, axis)
+            _dev(enc[1], torch.float16, f"{name} scale", shp)
+            _dev(enc[2], torch.float16, f"{name} zero", shp)
+    k_rows = v_rows = None
+    if mode == DQ_COMPACT:
+        k_rows = torch.empty(B, k, H, d, dtype=torch.bfloat16, device=k_hat.device)
+        v_rows = torch.empty(B, k, H, d, dtype=torch.bfloat16, device=k_hat.device)
+    rc = load().fl_kv_residual_dequant_kv(_p(k_enc[0]), _p(k_enc[1]), _p(k_enc[2]), _p(v_enc[0]), _p(v_enc[1]),
+                                          _p(v_enc[2]), _p(idx), k, B, N, H, d, bits, group, mode, _p(k_hat),
+                                          _p(v_hat), _p(k_rows), _p(v_rows), _stream())
+    _check(rc, "fl_kv_residual_dequant_kv")
+    return k_rows, v_rows
 
 
 def kv_residual_dequant(codes, scale, zero, idx, bits, group, axis, x_hat, mode=DQ_COMPACT):

@@ -119,6 +119,15 @@ def test_select_and_codec_reject_bad_arguments(lib):
     assert qkv(krows=DUMMY) == FL_E_SHAPE                         # rows alias the reference with idx
     assert qkv(vc=DUMMY) == FL_E_SHAPE                            # shared code buffer
     assert b"fl_kv_residual_quant_kv" in lib.fl_last_error()
+    dqkv = lambda **kw: lib.fl_kv_residual_dequant_kv(
+        DUMMY, DUMMY, DUMMY, DUMMY2, DUMMY2, DUMMY2, DUMMY, 8, 1, 64, 2, 64, kw.get("bits", 4), 32,
+        kw.get("mode", fl.DQ_COMMIT), DUMMY, kw.get("vh", DUMMY2), kw.get("kr"), kw.get("vr"), None)
+    assert dqkv(mode=5) == FL_E_UNSUPPORTED
+    assert dqkv(bits=3) == FL_E_UNSUPPORTED
+    assert dqkv(kr=DUMMY2) == FL_E_NULL                           # commit takes no compact rows
+    assert dqkv(mode=fl.DQ_COMPACT, kr=DUMMY2) == FL_E_NULL       # compact needs both row buffers
+    assert dqkv(vh=DUMMY) == FL_E_SHAPE                           # one cache for keys and values
+    assert b"fl_kv_residual_dequant_kv" in lib.fl_last_error()
     dq = lib.fl_kv_residual_dequant(DUMMY, DUMMY, DUMMY, DUMMY, 8, 1, 64, 2, 64, 4, 32, fl.AXIS_TOKEN, 7, DUMMY,
                                     None, None)
     assert dq == FL_E_UNSUPPORTED                                   # unknown mode

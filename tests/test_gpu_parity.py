@@ -142,6 +142,16 @@ def test_codec_kv_pair_matches_oracle(F, bits, d, G, k):
     assert ko[3] is None and vo[3] is None
     _check_enc(ko, want["k"][0], bits, "pair k (no rows)")
     _check_enc(vo, want["v"][0], bits, "pair v (no rows)")
+    # the pair reconstruction from those codes: compact rows, then committed in place
+    kr_, vr_ = F.kv_residual_dequant_kv(ko[:3], vo[:3], up(idx), bits, G, dk, dv)
+    torch.cuda.synchronize()
+    assert np.array_equal(down_bits16(kr_), want["k"][2]), "pair dequant: key rows differ"
+    assert np.array_equal(down_bits16(vr_), want["v"][2]), "pair dequant: value rows differ"
+    dk2, dv2 = up_bf16(kref), up_bf16(vref)
+    F.kv_residual_dequant_kv(ko[:3], vo[:3], up(idx), bits, G, dk2, dv2, mode=F.DQ_COMMIT)
+    torch.cuda.synchronize()
+    assert np.array_equal(down_bits16(dk2), want["k"][1]), "pair dequant commit: key cache differs"
+    assert np.array_equal(down_bits16(dv2), want["v"][1]), "pair dequant commit: value cache differs"
     ko, vo = F.kv_residual_quant_kv(up_bf16(kcur), dk, up_bf16(vcur), dv, up(idx), bits, G, mode=F.DQ_COMMIT)
     torch.cuda.synchronize()
     _check_enc(ko, want["k"][0], bits, "pair commit k")
