@@ -37,6 +37,9 @@ namespace fl {
 
 constexpr int kBN = 32;            // columns per tile
 constexpr int kRing = 4;           // LDS ring slots
+// cache policy of the tile loads: non-temporal (the "nt" bit, 2 on gfx950); measured a few percent
+// faster than the default policy on the 32K workload
+constexpr int kDmaPolicy = 2;
 
 struct AttnArgs {
   const uint16_t* q_cur;
@@ -337,9 +340,9 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
           const int inst = inst_of(t);
           const uint32_t off = of.o[t];
           if (t < INST_PER_WAVE)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(knR, FL_LDS(sl.k + inst * 512), 16, off, 0, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(knR, FL_LDS(sl.k + inst * 512), 16, off, 0, 0, kDmaPolicy);
           else
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(vnR, FL_LDS(sl.v + inst * 512), 16, off, 0, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(vnR, FL_LDS(sl.v + inst * 512), 16, off, 0, 0, kDmaPolicy);
         }
       } else {
 #pragma unroll
@@ -347,9 +350,9 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
           const int inst = inst_of(t);
           const uint32_t off = of.o[t];
           if (t < INST_PER_WAVE)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(kcR, FL_LDS(sl.k + inst * 512), 16, off, 0, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(kcR, FL_LDS(sl.k + inst * 512), 16, off, 0, 0, kDmaPolicy);
           else
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(vcR, FL_LDS(sl.v + inst * 512), 16, off, 0, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(vcR, FL_LDS(sl.v + inst * 512), 16, off, 0, 0, kDmaPolicy);
         }
       }
     } else {
@@ -358,13 +361,13 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
 #pragma unroll
         for (int t = 0; t < NI; ++t) {
           const uint32_t off = of.o[t];
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(srcN, FL_LDS(dst + inst_of(t) * 512), 16, off, 0, 0, 0);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(srcN, FL_LDS(dst + inst_of(t) * 512), 16, off, 0, 0, kDmaPolicy);
         }
       } else {
 #pragma unroll
         for (int t = 0; t < NI; ++t) {
           const uint32_t off = of.o[t];
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(srcC, FL_LDS(dst + inst_of(t) * 512), 16, off, 0, 0, 0);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(srcC, FL_LDS(dst + inst_of(t) * 512), 16, off, 0, 0, kDmaPolicy);
         }
       }
     }
@@ -870,9 +873,9 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
         const int inst = inst_of(t);
         const uint32_t off = of.o[t];
         if (t < INST_PER_WAVE)
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(knR, FL_LDS(sl.k + inst * 512), 16, off, 0, 0, 0);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(knR, FL_LDS(sl.k + inst * 512), 16, off, 0, 0, kDmaPolicy);
         else
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(vnR, FL_LDS(sl.v + inst * 512), 16, off, 0, 0, 0);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(vnR, FL_LDS(sl.v + inst * 512), 16, off, 0, 0, kDmaPolicy);
       }
     } else {
 #pragma unroll
@@ -880,9 +883,9 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
         const int inst = inst_of(t);
         const uint32_t off = of.o[t];
         if (t < INST_PER_WAVE)
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(kcR, FL_LDS(sl.k + inst * 512), 16, off, 0, 0, 0);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(kcR, FL_LDS(sl.k + inst * 512), 16, off, 0, 0, kDmaPolicy);
         else
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(vcR, FL_LDS(sl.v + inst * 512), 16, off, 0, 0, 0);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(vcR, FL_LDS(sl.v + inst * 512), 16, off, 0, 0, kDmaPolicy);
       }
     }
   };
