@@ -280,18 +280,33 @@ __global__ __launch_bounds__(kTopkThreads) void topk_select_kernel(
     }
   }
   // (3) bitmaps of the positions with a key above the threshold and equal to it (bit p % 32 of word
-  // p / 32): positions t + 1024 j of a wave's lanes 0-31 and 32-63 form whole words, written by ballot
+  // p / 32): positions t + 1024 j of a wave's lanes 0-31 and 32-63 form words 32 j + 2 wave and
+  // 32 j + 2 wave + 1, taken by ballot.  The wave gathers its 2 M words per map into lanes (word
+  // 2 j + h in lane (2 j + h) % 64 of register (2 j + h) / 64) and stores them without branches.
   uint32_t* bm_gt = cbuf;
   uint32_t* bm_eq = cbuf + kWords;
-  __syncthreads();                                        // cbuf is no longer read
+  constexpr int kRegs = (2 * M + 63) / 64;
+  uint32_t gv[kRegs], ev[kRegs];
+#pragma unroll
+  for (int r = 0; r < kRegs; ++r) gv[r] = ev[r] = 0u;
 #pragma unroll
   for (int j = 0; j < M; ++j) {
     const bool valid = k > 0 && t + kTopkThreads * j < n;
     const uint64_t g = __builtin_amdgcn_ballot_w64(valid && (take_all || u[j] > prefix));
     const uint64_t e = __builtin_amdgcn_ballot_w64(valid && !take_all && u[j] == prefix);
-    const int w0 = (kTopkThreads * j + 64 * wave) >> 5;
-    if (lane == 0) { bm_gt[w0] = (uint32_t)g; bm_eq[w0] = (uint32_t)e; }
-    if (lane == 1) { bm_gt[w0 + 1] = (uint32_t)(g >> 32); bm_eq[w0 + 1] = (uint32_t)(e >> 32); }
+    const int r = (2 * j) / 64, l0 = (2 * j) % 64;
+    gv[r] = lane == l0 ? (uint32_t)g : lane == l0 + 1 ? (uint32_t)(g >> 32) : gv[r];
+    ev[r] = lane == l0 ? (uint32_t)e : lane == l0 + 1 ? (uint32_t)(e >> 32) : ev[r];
+  }
+  __syncthreads();                                        // cbuf is no longer read
+#pragma unroll
+  for (int r = 0; r < kRegs; ++r) {
+    const int wj = 64 * r + lane;                         // word 2 j + h of this wave
+    if (wj < 2 * M) {
+      const int wd = 32 * (wj >> 1) + 2 * wave + (wj & 1);
+      bm_gt[wd] = gv[r];
+      bm_eq[wd] = ev[r];
+    }
   }
   __syncthreads();
   // thread t owns words t * kWordsPerThread ..; the equal keys taken are the krem lowest positions
