@@ -251,7 +251,7 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
   // Every tile is described by 32 records (column, aux): list entries (column, slot), band columns
   // (j, slot[j]), updated list entries (column, slot) and updated band rows (rows[p], p), all in one
   // array so that one 8-byte load per lane fetches them for any phase; entries past a phase's end read
-  // a sentinel (kPad, -1).  Records are loaded six tiles ahead and two steps later turned into the LDS
+  // a sentinel (kPad, -1).  Records are loaded eight tiles ahead and four steps later turned into the LDS
   // tables of entry v % 8: column ids for the masks and the byte offset of the row the DMA reads.
   const int c32 = lane & 31;
   const rsrc_t recR = make_rsrc(DENSE ? (const void*)a.k_cache : (const void*)a.rec, DENSE ? 0u : a.rec_bytes);
@@ -525,14 +525,18 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
 
   // ---- pipeline --------------------------------------------------------------------------------------
   // step s: read the table entries of tiles s+3 and s; wait for tile s; convert this wave's V rows of
-  // it; finalize the records of tile s+4; barrier; load the records of tile s+6; LDS-DMA tile s+3 into
-  // the slot tile s-1 used; compute tile s.  Every step issues the same number of VMEM ops (one record load in the sparse update and
-  // 2 * INST_PER_WAVE DMA), so "tile s has landed" is exactly vmcnt(2 * OPS_PER_STEP) on every path.
+  // it; finalize the records of tile s+4; barrier; load the records of tile s+8; LDS-DMA tile s+3 into
+  // the slot tile s-1 used; compute tile s.  Every step issues the same number of VMEM ops (one record
+  // load in the sparse update and 2 * INST_PER_WAVE DMA), so "tile s has landed" is exactly
+  // vmcnt(2 * OPS_PER_STEP) on every path.
   // Every wave loads the records (equal op counts keep every wait exact); one wave writes the tables:
   // an add wave when the subtract waves convert all of V.
   const bool rec_wave = __builtin_amdgcn_readfirstlane(wave) == (SPLIT_KV ? 2 : 0);
   constexpr int OPS_PER_STEP = (DENSE ? 0 : 1) + NI;
-  u32x2 dA, dB;                           // records in flight (even / odd tiles)
+  // Records are loaded four steps before they are turned into tables (step s loads tile s + 8 and
+  // describes tile s + 4), so the wave that writes the tables never waits for them: a record load is
+  // always older than the tile load the step waits for.
+  u32x2 dA, dB, dC, dD;                   // records in flight, by tile mod 4
 #pragma unroll
   for (int v = 0; v < 4; ++v) {
     const u32x2 r = load_desc(v);
@@ -541,13 +545,17 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
   FL_WAIT_VM(0);                          // query fragments have arrived
   lds_barrier();
   // the scheduling barriers keep this order, which the wait counts of the first steps assume
-  issue(0, s0, tile_offs(0));             // as step -3
+  dA = load_desc(4);                      // as step -4
   __builtin_amdgcn_sched_barrier(0);
-  dA = load_desc(4);                      // as step -2
+  dB = load_desc(5);                      // as step -3
+  __builtin_amdgcn_sched_barrier(0);
+  issue(0, s0, tile_offs(0));
+  __builtin_amdgcn_sched_barrier(0);
+  dC = load_desc(6);                      // as step -2
   __builtin_amdgcn_sched_barrier(0);
   issue(1, s1, tile_offs(1));
   __builtin_amdgcn_sched_barrier(0);
-  dB = load_desc(5);                      // as step -1
+  dD = load_desc(7);                      // as step -1
   __builtin_amdgcn_sched_barrier(0);
   issue(2, s2, tile_offs(2));
 
@@ -558,7 +566,7 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
     convert_v(cur);
     if (rec_wave) store_desc(u + 4, w);
     lds_barrier();
-    w = load_desc(u + 6);
+    w = load_desc(u + 8);
     __builtin_amdgcn_sched_barrier(0);    // keep the record load ahead of the DMA (the waits count on it)
     issue(u + 3, nxt, of);
     if (u < n_tiles) compute(u, cur, th);
@@ -567,8 +575,8 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
   for (int u = 0; u < n_steps; u += kRing) {
     step(u, s0, s3, dA);
     step(u + 1, s1, s0, dB);
-    step(u + 2, s2, s1, dA);
-    step(u + 3, s3, s2, dB);
+    step(u + 2, s2, s1, dC);
+    step(u + 3, s3, s2, dD);
   }
   FL_WAIT_VM(0);
   lds_barrier();
@@ -686,10 +694,10 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
   constexpr int INST_PER_WAVE = INST_PER_TILE / 4;   // per tensor (K and V each)
   constexpr int NI = 2 * INST_PER_WAVE;
   __shared__ Slot<D> s0, s1, s2, s3;
-  // column ids of tile v in entry v % 8 for the add pass (kPad = padding; in phases A/B the columns
-  // updated this loop are padding too)
-  __shared__ int tcv[8][kBN];
-  __shared__ uint32_t toff[8][kBN];       // byte offset of each column's row in its source (kOOB: none)
+  // tables of tile v in entry v % 8: [0, kBN) column ids for the add pass (kPad = padding; in phases A/B
+  // the columns updated this loop are padding too), [kBN, 2 kBN) byte offset of each column's row in its
+  // source (kOOB: none), so with current caches one 64-lane LDS write stores both halves
+  __shared__ uint32_t tab[8][2 * kBN];
   __shared__ int thd[8][4];               // tile v: first and last column id, any column updated
   __shared__ int s_meta[2];
 
@@ -829,23 +837,29 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
   const rsrc_t vnR = make_rsrc(CUR ? a.v_cache : a.v_new + (int64_t)b * a.k * HD, new_bytes);
 
   auto store_desc = [=](int v, u32x2 w) {
-    const bool newer = v >= n_old;
-    int cid = (int)w[0];
-    const int aux = (int)w[1];
     if constexpr (CUR) {
+      // lanes 0-31 form the column ids and offsets; lanes 32-63 take the offsets across the half-swap and
+      // store them beside the ids, in one write with no branch (the tile's head comes from the ids)
       int i;
       bool list, ok;
       cur_entry(v, i, list, ok);
-      cid = !ok ? kPad : list ? cid : bandLo + i;
+      const int cid = !ok ? kPad : list ? (int)w[0] : bandLo + i;
+      const uint32_t off = ok ? (uint32_t)cid * rb + head_off : kOOB;
+      const auto sw = __builtin_amdgcn_permlane32_swap(off, off, false, false);
+      tab[v & 7][lane] = lane < kBN ? (uint32_t)cid : (uint32_t)sw[0];
+      return;
     }
-    const bool upd = !CUR && !newer && aux >= 0;   // updated this loop, staged from the cache
+    const bool newer = v >= n_old;
+    const int cid = (int)w[0];
+    const int aux = (int)w[1];
+    const bool upd = !newer && aux >= 0;  // updated this loop, staged from the cache
     const int row = newer ? aux : cid;
     const bool valid = cid != kPad;
     if (lane < kBN) {
-      tcv[v & 7][c32] = upd ? kPad : cid;
+      tab[v & 7][c32] = (uint32_t)(upd ? kPad : cid);
       if (c32 == 0) thd[v & 7][0] = cid;
       if (c32 == kBN - 1) thd[v & 7][1] = cid;
-      toff[v & 7][c32] = valid ? (uint32_t)row * rb + head_off : kOOB;
+      tab[v & 7][kBN + c32] = valid ? (uint32_t)row * rb + head_off : kOOB;
     }
     const uint64_t any = __builtin_amdgcn_ballot_w64(lane < kBN && valid && upd);
     if (lane == 0) thd[v & 7][2] = any != 0;
@@ -860,7 +874,7 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
 #pragma unroll
     for (int t = 0; t < NI; ++t) {
       const int c = inst_of(t) * COLS_PER_INST + lane / CH;
-      r.o[t] = toff[u & 7][c] + (uint32_t)swz(c, lane % CH) * 16;   // kOOB + 240 is still out of range
+      r.o[t] = tab[u & 7][kBN + c] + (uint32_t)swz(c, lane % CH) * 16;   // kOOB + 240 is still out of range
     }
     return r;
   };
@@ -910,7 +924,10 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
   float run_max = -INFINITY, lsum = 0.0f;   // add pass: running reference (log2 units) and row sum
 
   struct TileHead { int c0, clast, any; };
-  auto tile_head = [=](int u) { return TileHead{thd[u & 7][0], thd[u & 7][1], thd[u & 7][2]}; };
+  auto tile_head = [=](int u) {
+    if constexpr (CUR) return TileHead{(int)tab[u & 7][0], (int)tab[u & 7][kBN - 1], 0};
+    return TileHead{thd[u & 7][0], thd[u & 7][1], thd[u & 7][2]};
+  };
 
   // column mask of the lane's 8 entries (ids cc, columns 16c + 4 g4 + v): list columns need
   // j + window <= i, band columns i - window < j <= i; padding and the columns updated this loop (in the
@@ -953,7 +970,7 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
     // branch can lose the information that tells it apart from the pending LDS-DMA writes
     int4 ca_[2];
 #pragma unroll
-    for (int c = 0; c < 2; ++c) ca_[c] = *reinterpret_cast<const int4*>(&tcv[ri][16 * c + 4 * g4]);
+    for (int c = 0; c < 2; ++c) ca_[c] = *reinterpret_cast<const int4*>(&tab[ri][16 * c + 4 * g4]);
     u32x4 kw[KS][2];
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
@@ -1021,12 +1038,12 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
 
   // ---- pipeline (as in loop_attn_kernel, without the V conversion): step s reads the table entries of
   // tiles s+3 and s, waits for tile s, finalizes the records of tile s+4, passes the barrier,
-  // loads the records of tile s+6, LDS-DMAs tile s+3 into the slot tile s-1 used and computes tile s.
+  // loads the records of tile s+8, LDS-DMAs tile s+3 into the slot tile s-1 used and computes tile s.
   // Every step issues the same number of VMEM ops (one record load + NI DMA), so "tile s has landed" is
   // exactly vmcnt(2 * OPS_PER_STEP) on every path.
   const bool rec_wave = wave == 0;
   constexpr int OPS_PER_STEP = 1 + NI;
-  u32x2 dA, dB;
+  u32x2 dA, dB, dC, dD;                   // records loaded four steps ahead, as in loop_attn_kernel
 #pragma unroll
   for (int v = 0; v < 4; ++v) {
     const u32x2 r = load_desc(v);
@@ -1034,13 +1051,17 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
   }
   FL_WAIT_VM(0);                          // query fragments have arrived
   lds_barrier();
+  dA = load_desc(4);
+  __builtin_amdgcn_sched_barrier(0);
+  dB = load_desc(5);
+  __builtin_amdgcn_sched_barrier(0);
   issue(0, s0, tile_offs(0));
   __builtin_amdgcn_sched_barrier(0);
-  dA = load_desc(4);
+  dC = load_desc(6);
   __builtin_amdgcn_sched_barrier(0);
   issue(1, s1, tile_offs(1));
   __builtin_amdgcn_sched_barrier(0);
-  dB = load_desc(5);
+  dD = load_desc(7);
   __builtin_amdgcn_sched_barrier(0);
   issue(2, s2, tile_offs(2));
 
@@ -1050,7 +1071,7 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
     FL_WAIT_VM(2 * OPS_PER_STEP);
     if (rec_wave) store_desc(u + 4, w);
     lds_barrier();
-    w = load_desc(u + 6);
+    w = load_desc(u + 8);
     __builtin_amdgcn_sched_barrier(0);
     issue(u + 3, nxt, of);
     if (u < n_tiles) compute(u, cur, th);
@@ -1059,8 +1080,8 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
   for (int u = 0; u < n_steps; u += kRing) {
     step(u, s0, s3, dA);
     step(u + 1, s1, s0, dB);
-    step(u + 2, s2, s1, dA);
-    step(u + 3, s3, s2, dB);
+    step(u + 2, s2, s1, dC);
+    step(u + 3, s3, s2, dD);
   }
   FL_WAIT_VM(0);
   lds_barrier();
