@@ -275,6 +275,37 @@ int fl_column_scores(const uint16_t* q, const uint16_t* k_cache, int B, int N, i
 int fl_select_columns(const float* col_key, int B, int H, int N, int n_sink, int t,
                       int32_t* cols, void* stream);
 
+/* ------------------------------------------------------------------------------------------------
+ * (6) Decode step of one loop for the newest position -- Appendix D.2, Eqs. 6 and 7 for one query row.
+ * For each (b, h), the query of position t = T - 1 attends over the columns S selected by the previous
+ * loop with their cached mass m, or over every column 0 .. T-1 with m = 1 (a dense source loop):
+ *     p_j = m * exp(l_j - L),  l_j = sm_scale * q . K_j (fp64),  L = log sum_{j in S} exp(l_j),
+ *     o <- o - sub + sum_{j in S} p_j V_j          (dense: o = sum_j p_j V_j),
+ * then selects the next loop's S' of c_next columns: columns j < n_sink and j >= T - window first
+ * (lower columns first if they alone exceed c_next), then fp32(p_j) descending, ties to the lower column,
+ * emitted ascending; m' = sum_{j in S'} p_j and sub' = sum_{j in S'} p_j V_j (the next loop's subtract
+ * term p_S'^(r) V_S'^(r)).
+ *   q                 : bf16 [B, H, d] the query of position T - 1 at this loop.
+ *   k_cache, v_cache  : bf16 [B, T, H, d] this loop's K_hat, V_hat of positions 0 .. T-1.
+ *   cols, c           : int32 [B, H, c] ascending S (1 <= c <= T), with mass fp32 [B, H] and sub fp32
+ *                       [B, H, d] from the loop that selected it; or cols = NULL (dense, c = 0 or T;
+ *                       mass and sub unused and may be NULL).
+ *   o                 : fp32 [B, H, d] the previous loop's output in (unused when dense), this loop's out.
+ *   lse               : optional fp32 [B, H]: L.
+ *   c_next            : 0 <= c_next <= |S| (0: no selection; the outputs below may then be NULL).
+ *   cols_next         : int32 [B, H, c_next];  mass_next : fp32 [B, H];  sub_next : fp32 [B, H, d].
+ *   ws                : at least fl_decode_step_ws(B, T, H, d, c, c_next) bytes (|S| <= 65536).
+ * Four launches: chunked logits and weighted V rows, their merge with the ranking keys, the top-k, and
+ * the next loop's mass and subtract term.  fp64 logits and probabilities make the selection exact.
+ * ---------------------------------------------------------------------------------------------- */
+size_t fl_decode_step_ws(int B, int T, int H, int d, int c, int c_next);
+
+int fl_decode_step(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                   const int32_t* cols, int c, const float* mass, const float* sub, int B, int T, int H,
+                   int d, float sm_scale, float* o, float* lse, int n_sink, int window, int c_next,
+                   int32_t* cols_next, float* mass_next, float* sub_next, void* ws, size_t ws_bytes,
+                   void* stream);
+
 #ifdef __cplusplus
 }
 #endif

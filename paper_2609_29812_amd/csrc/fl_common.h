@@ -30,6 +30,13 @@ int check_launch(const char* what);
 
 inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
+// Top-k of `segments` key rows (fl_select.hip): segment s selects the k largest of keys[s * key_stride +
+// 0..n-1] (ties to the lower position), writes their ids (cand[s * cand_stride + p], or id_base + p)
+// ascending at out[s * out_stride + n_prefix ..], ids 0..n_prefix-1 first, and optionally the slot map.
+int launch_topk(int segments, const float* keys, int64_t key_stride, int n, int k, const int32_t* cand,
+                int64_t cand_stride, int id_base, int32_t* out, int64_t out_stride, int n_prefix,
+                int32_t* slot, int slot_n, hipStream_t st);
+
 // ---- device numerics -------------------------------------------------------------------------------
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));

@@ -1,0 +1,344 @@
+// Decode step of one loop for the newest position (Appendix D.2, Eqs. (6) and (7) for one query row).
+//
+// For each (batch, head) the query of position t = T-1 attends over the column set S that the previous
+// loop selected (or over every column 0..T-1 for a dense source loop), with the cached mass m:
+//   p_j = m * exp(l_j - L), l_j = sm_scale * q . K_j, L = logsumexp over S,
+//   o <- o - sub + sum_j p_j V_j          (dense: o = sum_j p_j V_j, m = 1),
+// then selects the next loop's S' (sinks and window forced, then p descending, ties to the lower column)
+// and forms its mass m' = sum_{S'} p_j and subtract term sub' = sum_{S'} p_j V_j.
+//
+// One row per (b, h) is a GEMV: HBM-bound, split over columns.
+//   decode_partial  chunks of 256 positions: fp64 logits (exact bf16 products, fp64 sums), the chunk's
+//                   max and exp-sum, and the exp-weighted sum of its V rows (fp32); K and V rows are
+//                   each read once, 16 bytes per lane, D/8 lanes per row.
+//   decode_combine  one workgroup per (b, h): merges the chunks into L and the output, and writes the
+//                   fp32 ranking keys (probabilities in fp64, rounded; forced columns +inf).
+//   topk_select     the radix top-k of fl_select.hip over the keys (positions, ascending).
+//   decode_finalize one workgroup per (b, h): the selected columns, their mass and subtract term.
+#include "fl_common.h"
+
+namespace fl {
+
+constexpr int kDecChunk = 256;           // positions per partial workgroup
+
+struct DecodeArgs {
+  const uint16_t* q;         // [B, H, D]
+  const uint16_t* k;         // [B, T, H, D]
+  const uint16_t* v;
+  const int32_t* cols;       // [B, H, c] or NULL (dense)
+  const float* mass;         // [B, H]
+  const float* sub;          // [B, H, D]
+  float* o;                  // [B, H, D]
+  float* lse;                // [B, H] optional
+  double* logit;             // ws [B*H, n]
+  double* pmax;              // ws [B*H, nch] chunk max
+  double* psum;              // ws [B*H, nch] chunk exp-sum
+  float* pacc;               // ws [B*H, nch, D]
+  double* ltot;              // ws [B*H] log-normaliser
+  float* key;                // ws [B*H, n]
+  const int32_t* sel;        // ws [B*H, c_next] selected positions
+  int32_t* cols_next;        // [B, H, c_next]
+  float* mass_next;          // [B, H]
+  float* sub_next;           // [B, H, D]
+  int B, T, H, n, nch, c_next, n_sink, window;
+  double scale;
+};
+
+__device__ __forceinline__ int dec_col(const DecodeArgs& a, int bh, int p) {
+  return a.cols ? a.cols[(int64_t)bh * a.n + p] : p;
+}
+
+__device__ __forceinline__ double wave_max_f64(double x) {
+  for (int off = 32; off > 0; off >>= 1) x = fmax(x, __shfl_xor(x, off, 64));
+  return x;
+}
+__device__ __forceinline__ double wave_sum_f64_dec(double x) {
+  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
+  return x;
+}
+
+// ---- partial: one chunk of positions of one (b, h) -------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void decode_partial_kernel(DecodeArgs a) {
+  constexpr int LPC = D / 8;                 // lanes per row (16 bytes each)
+  constexpr int CPW = 64 / LPC;              // rows per wave instruction
+  constexpr int PER_WAVE = kDecChunk / 4;    // positions per wave
+  constexpr int IT = PER_WAVE / CPW;
+  __shared__ double s_red[4];
+  __shared__ float s_acc[4][D];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int sl = lane % LPC, grp = lane / LPC;
+  const int chunk = blockIdx.x, bh = blockIdx.y;
+  const int b = bh / a.H, h = bh % a.H;
+  const int64_t HD = (int64_t)a.H * D;
+  double qd[8];
+  {
+    const uint4 w = *reinterpret_cast<const uint4*>(a.q + (int64_t)bh * D + 8 * sl);
+    const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      qd[2 * t] = (double)bf16_to_f32(ws[t] & 0xFFFFu);
+      qd[2 * t + 1] = (double)bf16_to_f32(ws[t] >> 16);
+    }
+  }
+  // pass 1: logits (every lane of a row group ends with the row's full dot product)
+  double lg[IT];
+  int colv[IT];
+  double mx = -INFINITY;
+#pragma unroll
+  for (int it = 0; it < IT; ++it) {
+    const int p = chunk * kDecChunk + wave * PER_WAVE + it * CPW + grp;
+    const bool ok = p < a.n;
+    const int col = ok ? dec_col(a, bh, p) : 0;
+    colv[it] = col;
+    const uint4 w = *reinterpret_cast<const uint4*>(a.k + ((int64_t)b * a.T + col) * HD + (int64_t)h * D + 8 * sl);
+    const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+    double acc = 0.0;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      acc = fma((double)bf16_to_f32(ws[t] & 0xFFFFu), qd[2 * t], acc);
+      acc = fma((double)bf16_to_f32(ws[t] >> 16), qd[2 * t + 1], acc);
+    }
+#pragma unroll
+    for (int off = 1; off < LPC; off <<= 1) acc += __shfl_xor(acc, off, 64);
+    const double l = ok ? a.scale * acc : -INFINITY;
+    lg[it] = l;
+    mx = fmax(mx, l);
+    if (ok && sl == 0) a.logit[(int64_t)bh * a.n + p] = l;
+  }
+  mx = wave_max_f64(mx);
+  if (lane == 0) s_red[wave] = mx;
+  __syncthreads();
+  mx = fmax(fmax(s_red[0], s_red[1]), fmax(s_red[2], s_red[3]));
+  __syncthreads();
+  // pass 2: exp-weights against the chunk max, exp-sum and the weighted V rows
+  double es = 0.0;
+  float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+  for (int it = 0; it < IT; ++it) {
+    const double e = exp(lg[it] - mx);          // 0 for positions past the end
+    if (sl == 0) es += e;
+    const float wf = (float)e;
+    const uint4 w = *reinterpret_cast<const uint4*>(a.v + ((int64_t)b * a.T + colv[it]) * HD + (int64_t)h * D + 8 * sl);
+    const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      acc[2 * t] = fmaf(wf, bf16_to_f32(ws[t] & 0xFFFFu), acc[2 * t]);
+      acc[2 * t + 1] = fmaf(wf, bf16_to_f32(ws[t] >> 16), acc[2 * t + 1]);
+    }
+  }
+  es = wave_sum_f64_dec(es);
+  // rows of a wave -> lanes 0..LPC-1, then the four waves through LDS
+#pragma unroll
+  for (int t = 0; t < 8; ++t)
+    for (int off = LPC; off < 64; off <<= 1) acc[t] += __shfl_xor(acc[t], off, 64);
+  if (lane < LPC) {
+#pragma unroll
+    for (int t = 0; t < 8; ++t) s_acc[wave][8 * sl + t] = acc[t];
+  }
+  if (lane == 0) s_red[wave] = es;
+  __syncthreads();
+  const int64_t slot = (int64_t)bh * a.nch + chunk;
+  if (threadIdx.x < D) {
+    const int dd = threadIdx.x;
+    a.pacc[slot * D + dd] = s_acc[0][dd] + s_acc[1][dd] + s_acc[2][dd] + s_acc[3][dd];
+  }
+  if (threadIdx.x == 0) {
+    a.pmax[slot] = mx;
+    a.psum[slot] = s_red[0] + s_red[1] + s_red[2] + s_red[3];
+  }
+}
+
+// ---- combine: the output and the ranking keys of one (b, h) ------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a) {
+  __shared__ double s_m[4];
+  __shared__ double s_l;
+  const int bh = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const bool dense = a.cols == nullptr;
+  const double m = dense ? 1.0 : (double)a.mass[bh];
+  double mx = -INFINITY;
+  for (int c = tid; c < a.nch; c += 256) mx = fmax(mx, a.pmax[(int64_t)bh * a.nch + c]);
+  mx = wave_max_f64(mx);
+  if (lane == 0) s_m[wave] = mx;
+  __syncthreads();
+  const double M = fmax(fmax(s_m[0], s_m[1]), fmax(s_m[2], s_m[3]));
+  __syncthreads();
+  double es = 0.0;
+  for (int c = tid; c < a.nch; c += 256) {
+    const int64_t sidx = (int64_t)bh * a.nch + c;
+    es += a.psum[sidx] * exp(a.pmax[sidx] - M);
+  }
+  es = wave_sum_f64_dec(es);
+  if (lane == 0) s_m[wave] = es;
+  __syncthreads();
+  if (tid == 0) s_l = s_m[0] + s_m[1] + s_m[2] + s_m[3];
+  __syncthreads();
+  const double S = s_l;
+  const double L = M + log(S);
+  if (tid < D) {
+    float add = 0.0f;
+    for (int c = 0; c < a.nch; ++c) {
+      const int64_t sidx = (int64_t)bh * a.nch + c;
+      const float f = (float)(m * exp(a.pmax[sidx] - M) / S);
+      add = fmaf(f, a.pacc[sidx * D + tid], add);
+    }
+    const int64_t od = (int64_t)bh * D + tid;
+    a.o[od] = dense ? add : a.o[od] - a.sub[od] + add;
+  }
+  if (tid == 0) {
+    a.ltot[bh] = L;
+    if (a.lse) a.lse[bh] = (float)L;
+  }
+  if (a.c_next > 0) {
+    for (int p = tid; p < a.n; p += 256) {
+      const int col = dec_col(a, bh, p);
+      const bool forced = col < a.n_sink || (a.window > 0 && col >= a.T - a.window);
+      const double pr = m * exp(a.logit[(int64_t)bh * a.n + p] - L);
+      a.key[(int64_t)bh * a.n + p] = forced ? INFINITY : (float)pr;
+    }
+  }
+}
+
+// ---- finalize: the next loop's columns, mass and subtract term of one (b, h) ------------------------
+template <int D>
+__global__ __launch_bounds__(256) void decode_finalize_kernel(DecodeArgs a) {
+  constexpr int LPC = D / 8;
+  constexpr int CPW = 64 / LPC;
+  __shared__ double s_red[4];
+  __shared__ float s_acc[4][D];
+  const int bh = blockIdx.x;
+  const int b = bh / a.H, h = bh % a.H;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int sl = lane % LPC, grp = lane / LPC;
+  const int64_t HD = (int64_t)a.H * D;
+  const double m = a.cols == nullptr ? 1.0 : (double)a.mass[bh];
+  const double L = a.ltot[bh];
+  double ms = 0.0;
+  float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  for (int i0 = wave * CPW; i0 < a.c_next; i0 += 4 * CPW) {
+    const int i = i0 + grp;
+    const bool ok = i < a.c_next;
+    const int p = ok ? a.sel[(int64_t)bh * a.c_next + i] : 0;
+    const int col = dec_col(a, bh, p);
+    const double pr = ok ? m * exp(a.logit[(int64_t)bh * a.n + p] - L) : 0.0;
+    if (ok && sl == 0) {
+      a.cols_next[(int64_t)bh * a.c_next + i] = col;
+      ms += pr;
+    }
+    const float wf = (float)pr;
+    const uint4 w = *reinterpret_cast<const uint4*>(a.v + ((int64_t)b * a.T + col) * HD + (int64_t)h * D + 8 * sl);
+    const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      acc[2 * t] = fmaf(wf, bf16_to_f32(ws[t] & 0xFFFFu), acc[2 * t]);
+      acc[2 * t + 1] = fmaf(wf, bf16_to_f32(ws[t] >> 16), acc[2 * t + 1]);
+    }
+  }
+  ms = wave_sum_f64_dec(ms);
+#pragma unroll
+  for (int t = 0; t < 8; ++t)
+    for (int off = LPC; off < 64; off <<= 1) acc[t] += __shfl_xor(acc[t], off, 64);
+  if (lane < LPC) {
+#pragma unroll
+    for (int t = 0; t < 8; ++t) s_acc[wave][8 * sl + t] = acc[t];
+  }
+  if (lane == 0) s_red[wave] = ms;
+  __syncthreads();
+  if (threadIdx.x < D) {
+    const int dd = threadIdx.x;
+    a.sub_next[(int64_t)bh * D + dd] = s_acc[0][dd] + s_acc[1][dd] + s_acc[2][dd] + s_acc[3][dd];
+  }
+  if (threadIdx.x == 0) a.mass_next[bh] = (float)(s_red[0] + s_red[1] + s_red[2] + s_red[3]);
+}
+
+// workspace regions, each 256-byte aligned
+struct DecodeWs {
+  size_t logit, pmax, psum, pacc, ltot, key, sel, total;
+};
+static DecodeWs decode_ws(int B, int H, int d, int n, int c_next) {
+  auto al = [](size_t x) { return (x + 255) / 256 * 256; };
+  const size_t bh = (size_t)B * H;
+  const size_t nch = ((size_t)n + kDecChunk - 1) / kDecChunk;
+  DecodeWs w;
+  size_t off = 0;
+  w.logit = off; off += al(bh * n * sizeof(double));
+  w.pmax = off; off += al(bh * nch * sizeof(double));
+  w.psum = off; off += al(bh * nch * sizeof(double));
+  w.pacc = off; off += al(bh * nch * d * sizeof(float));
+  w.ltot = off; off += al(bh * sizeof(double));
+  w.key = off; off += al(bh * n * sizeof(float));
+  w.sel = off; off += al(bh * (size_t)c_next * sizeof(int32_t));
+  w.total = off;
+  return w;
+}
+
+}  // namespace fl
+
+using namespace fl;
+
+extern "C" size_t fl_decode_step_ws(int B, int T, int H, int d, int c, int c_next) {
+  if (B < 1 || T < 1 || H < 1 || (d != 64 && d != 128) || c < 0 || c_next < 0) return 0;
+  const int n = c > 0 ? c : T;
+  return decode_ws(B, H, d, n, c_next).total;
+}
+
+extern "C" int fl_decode_step(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                              const int32_t* cols, int c, const float* mass, const float* sub, int B, int T,
+                              int H, int d, float sm_scale, float* o, float* lse, int n_sink, int window,
+                              int c_next, int32_t* cols_next, float* mass_next, float* sub_next, void* ws,
+                              size_t ws_bytes, void* stream) {
+  FL_API_BEGIN
+  const char* fn = "fl_decode_step";
+  FL_REQUIRE(q && k_cache && v_cache && o, FL_E_NULL, "%s: q, k_cache, v_cache and o are required", fn);
+  FL_REQUIRE(B >= 1 && T >= 1 && H >= 1, FL_E_SHAPE, "%s: need B, T, H >= 1", fn);
+  FL_REQUIRE(d == 64 || d == 128, FL_E_SHAPE, "%s: head dim %d not in {64, 128}", fn, d);
+  FL_REQUIRE((int64_t)T * H * d < ((int64_t)1 << 31), FL_E_SHAPE, "%s: T * H * d too large", fn);
+  FL_REQUIRE(sm_scale > 0.0f && std::isfinite(sm_scale), FL_E_RANGE, "%s: sm_scale must be > 0", fn);
+  const bool dense = cols == nullptr;
+  if (dense) {
+    FL_REQUIRE(c == 0 || c == T, FL_E_SHAPE, "%s: without cols, c must be 0 or T", fn);
+  } else {
+    FL_REQUIRE(c >= 1 && c <= T, FL_E_RANGE, "%s: c=%d outside [1, T]", fn, c);
+    FL_REQUIRE(mass && sub, FL_E_NULL, "%s: a sparse loop needs its cached mass and subtract term", fn);
+  }
+  const int n = dense ? T : c;
+  FL_REQUIRE(n <= 65536, FL_E_SHAPE, "%s: %d columns exceed the 65536 the selection supports", fn, n);
+  FL_REQUIRE(c_next >= 0 && c_next <= n, FL_E_RANGE, "%s: c_next=%d outside [0, %d]", fn, c_next, n);
+  FL_REQUIRE(c_next == 0 || (cols_next && mass_next && sub_next), FL_E_NULL,
+             "%s: cols_next, mass_next and sub_next are required when c_next > 0", fn);
+  FL_REQUIRE(n_sink >= 0 && window >= 0, FL_E_RANGE, "%s: n_sink and window must be >= 0", fn);
+  const DecodeWs L = decode_ws(B, H, d, n, c_next);
+  FL_REQUIRE(ws && ws_bytes >= L.total, FL_E_WORKSPACE, "%s: workspace of %zu bytes required", fn, L.total);
+  hipStream_t st = as_stream(stream);
+  char* base = static_cast<char*>(ws);
+  DecodeArgs a{};
+  a.q = q; a.k = k_cache; a.v = v_cache; a.cols = cols; a.mass = mass; a.sub = sub; a.o = o; a.lse = lse;
+  a.logit = reinterpret_cast<double*>(base + L.logit);
+  a.pmax = reinterpret_cast<double*>(base + L.pmax);
+  a.psum = reinterpret_cast<double*>(base + L.psum);
+  a.pacc = reinterpret_cast<float*>(base + L.pacc);
+  a.ltot = reinterpret_cast<double*>(base + L.ltot);
+  a.key = reinterpret_cast<float*>(base + L.key);
+  a.sel = reinterpret_cast<const int32_t*>(base + L.sel);
+  a.cols_next = cols_next; a.mass_next = mass_next; a.sub_next = sub_next;
+  a.B = B; a.T = T; a.H = H; a.n = n; a.nch = (n + kDecChunk - 1) / kDecChunk; a.c_next = c_next;
+  a.n_sink = n_sink; a.window = window; a.scale = (double)sm_scale;
+  const int BH = B * H;
+  dim3 gp(a.nch, BH);
+  if (d == 128) decode_partial_kernel<128><<<gp, 256, 0, st>>>(a);
+  else decode_partial_kernel<64><<<gp, 256, 0, st>>>(a);
+  int rc = check_launch("decode_partial_kernel");
+  if (rc != FL_OK) return rc;
+  if (d == 128) decode_combine_kernel<128><<<BH, 256, 0, st>>>(a);
+  else decode_combine_kernel<64><<<BH, 256, 0, st>>>(a);
+  rc = check_launch("decode_combine_kernel");
+  if (rc != FL_OK || c_next == 0) return rc;
+  rc = launch_topk(BH, a.key, n, n, c_next, nullptr, 0, 0, const_cast<int32_t*>(a.sel), c_next, 0, nullptr, 0, st);
+  if (rc != FL_OK) return rc;
+  if (d == 128) decode_finalize_kernel<128><<<BH, 256, 0, st>>>(a);
+  else decode_finalize_kernel<64><<<BH, 256, 0, st>>>(a);
+  return check_launch("decode_finalize_kernel");
+  FL_API_END
+}

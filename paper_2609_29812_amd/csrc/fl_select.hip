@@ -393,7 +393,7 @@ __global__ __launch_bounds__(kTopkThreads) void topk_select_kernel(
   }
 }
 
-static int launch_topk(int segments, const float* keys, int64_t key_stride, int n, int k,
+int launch_topk(int segments, const float* keys, int64_t key_stride, int n, int k,
                        const int32_t* cand, int64_t cand_stride, int id_base, int32_t* out,
                        int64_t out_stride, int n_prefix, int32_t* slot, int slot_n,
                        hipStream_t st) {

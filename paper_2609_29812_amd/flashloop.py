@@ -53,6 +53,9 @@ _SIGNATURES = {
     "fl_column_scores_ws": (_c_sz, [_c_i, _c_i, _c_i]),
     "fl_column_scores": (_c_i, [_c_p, _c_p, _c_i, _c_i, _c_i, _c_i, _c_p, _c_p, _c_sz, _c_p]),
     "fl_select_columns": (_c_i, [_c_p, _c_i, _c_i, _c_i, _c_i, _c_i, _c_p, _c_p]),
+    "fl_decode_step_ws": (_c_sz, [_c_i, _c_i, _c_i, _c_i, _c_i, _c_i]),
+    "fl_decode_step": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_i, _c_p, _c_p, _c_i, _c_i, _c_i, _c_i, _c_f, _c_p, _c_p,
+                              _c_i, _c_i, _c_i, _c_p, _c_p, _c_p, _c_p, _c_sz, _c_p]),
 }
 
 EXPORTS = tuple(_SIGNATURES)
@@ -353,3 +356,36 @@ def select_columns(col_key, n_sink, t):
     rc = load().fl_select_columns(_p(col_key), B, H, N, n_sink, t, _p(cols), _stream())
     _check(rc, "fl_select_columns")
     return cols
+
+
+# ---- (6) decode ---------------------------------------------------------------------------------------
+def decode_step(q, k_cache, v_cache, cols, mass, sub, o, c_next, n_sink=0, window=0, sm_scale=None, lse=None):
+    """One loop of the decode position T-1.  q bf16 [B, H, d]; caches bf16 [B, T, H, d]; cols int32 [B, H, c]
+    (or None for a dense source loop, then mass and sub are unused); o fp32 [B, H, d] updated in place.
+    Returns (cols_next [B, H, c_next], mass_next [B, H], sub_next [B, H, d]) or Nones when c_next == 0."""
+    B, T, H, d = k_cache.shape
+    _dev(q, torch.bfloat16, "q", (B, H, d))
+    _dev(k_cache, torch.bfloat16, "k_cache")
+    _dev(v_cache, torch.bfloat16, "v_cache", k_cache.shape)
+    _dev(o, torch.float32, "o", (B, H, d))
+    c = 0 if cols is None else cols.shape[2]
+    if cols is not None:
+        _dev(cols, torch.int32, "cols", (B, H, c))
+        _dev(mass, torch.float32, "mass", (B, H))
+        _dev(sub, torch.float32, "sub", (B, H, d))
+    _dev(lse, torch.float32, "lse", (B, H))
+    dev = q.device
+    cols_next = mass_next = sub_next = None
+    if c_next > 0:
+        cols_next = torch.empty(B, H, c_next, dtype=torch.int32, device=dev)
+        mass_next = torch.empty(B, H, dtype=torch.float32, device=dev)
+        sub_next = torch.empty(B, H, d, dtype=torch.float32, device=dev)
+    sm_scale = 1.0 / math.sqrt(d) if sm_scale is None else sm_scale
+    lib = load()
+    need = lib.fl_decode_step_ws(B, T, H, d, c, c_next)
+    ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    rc = lib.fl_decode_step(_p(q), _p(k_cache), _p(v_cache), _p(cols), c, _p(mass), _p(sub), B, T, H, d, sm_scale,
+                            _p(o), _p(lse), n_sink, window, c_next, _p(cols_next), _p(mass_next), _p(sub_next),
+                            _p(ws), need, _stream())
+    _check(rc, "fl_decode_step")
+    return cols_next, mass_next, sub_next
