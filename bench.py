@@ -266,6 +266,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="C4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--copy-calib", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -407,9 +408,61 @@ def main():
         "roofline_other_kernels": others,
         "kernels": kernels,
     }
+    if not args.no_decode:
+        result["decode"] = decode_bench(w, gs, fl, torch)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, st, blas_threads())
     print(json.dumps(result), flush=True)
+
+
+def decode_work(B, T, H, d, c, c_next):
+    """Algorithmic bytes of one decode step: the K and V rows of the attended columns, the query, the
+    output (read unless dense, written), the column list, the cached subtract term, and the V rows and
+    outputs of the next loop's subtract term."""
+    n = T if c == 0 else c
+    nb = B * H * n * d * 2 * 2 + B * H * d * 2 + B * H * d * 4 * (1 if c == 0 else 3) + B * H * 4 * 2
+    if c:
+        nb += B * H * c * 4
+    nb += B * H * c_next * (d * 2 + 4) + B * H * d * 4
+    return nb
+
+
+def decode_bench(w, gs, fl, torch):
+    """The decode step for one new position of the workload's context: a dense source loop over every
+    position, then the sparse loops over the column budget (sinks and window forced), timed per loop with
+    HIP events (separate from the prefill step above)."""
+    B, T, H, d = gs.k_hat.shape
+    c = w.col_budget
+    g = torch.Generator(device="cuda").manual_seed(11)
+    q = torch.randn(B, H, d, device="cuda", generator=g).to(torch.bfloat16)
+    o = torch.zeros(B, H, d, dtype=torch.float32, device="cuda")
+    reps = 20
+
+    def timed(fn):
+        for _ in range(3):
+            out = fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            out = fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e3, out
+
+    us_dense, (cols, mass, sub) = timed(lambda: fl.decode_step(q, gs.k_hat, gs.v_hat, None, None, None, o, c,
+                                                               n_sink=w.n_sink, window=w.window))
+    us_sparse, _ = timed(lambda: fl.decode_step(q, gs.k_hat, gs.v_hat, cols, mass, sub, o, c,
+                                                n_sink=w.n_sink, window=w.window))
+    nb_dense = decode_work(B, T, H, d, 0, c)
+    nb_sparse = decode_work(B, T, H, d, c, c)
+    log(f"[bench] decode: dense loop {us_dense:.1f} us ({nb_dense / us_dense / 1e3:.0f} GB/s), "
+        f"sparse loop {us_sparse:.1f} us ({nb_sparse / us_sparse / 1e3:.0f} GB/s)")
+    return {"workload": f"{w.name} decode position {T - 1}", "columns_dense": T, "columns_sparse": c,
+            "dense_loop_us": round(us_dense, 2), "sparse_loop_us": round(us_sparse, 2),
+            "dense_alg_MB": round(nb_dense / 1e6, 2), "sparse_alg_MB": round(nb_sparse / 1e6, 2),
+            "dense_GBps": round(nb_dense / us_dense / 1e3, 1), "sparse_GBps": round(nb_sparse / us_sparse / 1e3, 1),
+            "timing": f"HIP events, mean of {reps} calls (five launches each)"}
 
 
 if __name__ == "__main__":

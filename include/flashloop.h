@@ -282,7 +282,7 @@ int fl_select_columns(const float* col_key, int B, int H, int N, int n_sink, int
  *     p_j = m * exp(l_j - L),  l_j = sm_scale * q . K_j (fp64),  L = log sum_{j in S} exp(l_j),
  *     o <- o - sub + sum_{j in S} p_j V_j          (dense: o = sum_j p_j V_j),
  * then selects the next loop's S' of c_next columns: columns j < n_sink and j >= T - window first
- * (lower columns first if they alone exceed c_next), then fp32(p_j) descending, ties to the lower column,
+ * (lower columns first if they alone exceed c_next), then fp32(l_j) descending, ties to the lower column,
  * emitted ascending; m' = sum_{j in S'} p_j and sub' = sum_{j in S'} p_j V_j (the next loop's subtract
  * term p_S'^(r) V_S'^(r)).
  *   q                 : bf16 [B, H, d] the query of position T - 1 at this loop.
@@ -295,8 +295,9 @@ int fl_select_columns(const float* col_key, int B, int H, int N, int n_sink, int
  *   c_next            : 0 <= c_next <= |S| (0: no selection; the outputs below may then be NULL).
  *   cols_next         : int32 [B, H, c_next];  mass_next : fp32 [B, H];  sub_next : fp32 [B, H, d].
  *   ws                : at least fl_decode_step_ws(B, T, H, d, c, c_next) bytes (|S| <= 65536).
- * Four launches: chunked logits and weighted V rows, their merge with the ranking keys, the top-k, and
- * the next loop's mass and subtract term.  fp64 logits and probabilities make the selection exact.
+ * Five launches: chunked logits (with their fp32 ranking keys) and weighted V rows, their merge, the
+ * top-k, and the next loop's mass and subtract term in parts and their ordered sum.  Within a row p_j
+ * grows with l_j, so S' is ranked by fp32(l_j) (fp64 logits keep the selection exact).
  * ---------------------------------------------------------------------------------------------- */
 size_t fl_decode_step_ws(int B, int T, int H, int d, int c, int c_next);
 

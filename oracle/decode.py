@@ -17,8 +17,9 @@ Readings (where the paper is silent):
 * the selection keeps the n_sink leading columns and the `window` most recent ones, as the prefill
   path does (they rank above every other column; if the budget is smaller than their number, the lower
   columns win), then the highest probabilities, ties to the lower column; S is emitted ascending;
-* probabilities are fp64 and ranked by their fp32 rounding (the GPU ranks fp32 keys formed from fp64
-  probabilities);
+* within one row p_j = m * exp(l_j - L) increases with the logit l_j, so the top probabilities are the
+  top logits: columns are ranked by the fp32 rounding of their fp64 logit (the GPU ranks the same fp32
+  keys, formed before L is known);
 * the decode position t = T - 1 is the last cached row and is causal for itself.
 Everything is fp64.
 """
@@ -48,8 +49,8 @@ def decode_step(q, k, v, S, m, sub, o_prev, sm_scale, n_sink, window, c_next):
     p = m * np.exp(logits - L)                        # p_S^(r) = m * softmax over S
     add = p @ v[S]
     o = add if dense else o_prev - sub + add
-    # next loop: forced columns first, then probability (fp32) descending, then column ascending
-    key = p.astype(np.float32).astype(np.float64)
+    # next loop: forced columns first, then the logit (fp32) descending, then column ascending
+    key = logits.astype(np.float32).astype(np.float64)
     forced = S < n_sink
     if window > 0:
         forced |= S >= T - window

@@ -4,17 +4,19 @@
 // loop selected (or over every column 0..T-1 for a dense source loop), with the cached mass m:
 //   p_j = m * exp(l_j - L), l_j = sm_scale * q . K_j, L = logsumexp over S,
 //   o <- o - sub + sum_j p_j V_j          (dense: o = sum_j p_j V_j, m = 1),
-// then selects the next loop's S' (sinks and window forced, then p descending, ties to the lower column)
-// and forms its mass m' = sum_{S'} p_j and subtract term sub' = sum_{S'} p_j V_j.
+// then selects the next loop's S' (sinks and window forced, then the largest p, ties to the lower
+// column) and forms its mass m' = sum_{S'} p_j and subtract term sub' = sum_{S'} p_j V_j.  Within a row
+// p_j grows with l_j, so the ranking key is fp32(l_j), available before L is known.
 //
 // One row per (b, h) is a GEMV: HBM-bound, split over columns.
-//   decode_partial  chunks of 256 positions: fp64 logits (exact bf16 products, fp64 sums), the chunk's
-//                   max and exp-sum, and the exp-weighted sum of its V rows (fp32); K and V rows are
-//                   each read once, 16 bytes per lane, D/8 lanes per row.
-//   decode_combine  one workgroup per (b, h): merges the chunks into L and the output, and writes the
-//                   fp32 ranking keys (probabilities in fp64, rounded; forced columns +inf).
+//   decode_partial  chunks of 256 positions: fp64 logits (exact bf16 products, fp64 sums) and their fp32
+//                   ranking keys (forced columns +inf), the chunk's max and exp-sum, and the
+//                   exp-weighted sum of its V rows (fp32); K and V rows are each read once, 16 bytes per
+//                   lane, D/8 lanes per row.
+//   decode_combine  one workgroup per (b, h): merges the chunks into L and the output.
 //   topk_select     the radix top-k of fl_select.hip over the keys (positions, ascending).
-//   decode_finalize one workgroup per (b, h): the selected columns, their mass and subtract term.
+//   decode_select  workgroups of 256 selected positions: the selected columns and their parts of the
+//                   mass and subtract term; then one workgroup per (b, h) adds the parts in order.
 #include "fl_common.h"
 
 namespace fl {
@@ -37,10 +39,12 @@ struct DecodeArgs {
   double* ltot;              // ws [B*H] log-normaliser
   float* key;                // ws [B*H, n]
   const int32_t* sel;        // ws [B*H, c_next] selected positions
+  double* fmass;             // ws [B*H, nfc] parts of the next mass
+  float* fsub;               // ws [B*H, nfc, D] parts of the next subtract term
   int32_t* cols_next;        // [B, H, c_next]
   float* mass_next;          // [B, H]
   float* sub_next;           // [B, H, D]
-  int B, T, H, n, nch, c_next, n_sink, window;
+  int B, T, H, n, nch, c_next, nfc, n_sink, window;
   double scale;
 };
 
@@ -81,17 +85,27 @@ __global__ __launch_bounds__(256) void decode_partial_kernel(DecodeArgs a) {
       qd[2 * t + 1] = (double)bf16_to_f32(ws[t] >> 16);
     }
   }
-  // pass 1: logits (every lane of a row group ends with the row's full dot product)
+  // pass 1: logits (every lane of a row group ends with the row's full dot product).  All column ids,
+  // then all K loads, are issued before any use, so a chunk costs two load latencies, not 2 * IT.
   double lg[IT];
   int colv[IT];
+  uint4 kw[IT];
   double mx = -INFINITY;
+  const int p0 = chunk * kDecChunk + wave * PER_WAVE + grp;
 #pragma unroll
   for (int it = 0; it < IT; ++it) {
-    const int p = chunk * kDecChunk + wave * PER_WAVE + it * CPW + grp;
+    const int p = p0 + it * CPW;
+    colv[it] = p < a.n ? dec_col(a, bh, p) : 0;
+  }
+#pragma unroll
+  for (int it = 0; it < IT; ++it)
+    kw[it] = *reinterpret_cast<const uint4*>(a.k + ((int64_t)b * a.T + colv[it]) * HD + (int64_t)h * D + 8 * sl);
+#pragma unroll
+  for (int it = 0; it < IT; ++it) {
+    const int p = p0 + it * CPW;
     const bool ok = p < a.n;
-    const int col = ok ? dec_col(a, bh, p) : 0;
-    colv[it] = col;
-    const uint4 w = *reinterpret_cast<const uint4*>(a.k + ((int64_t)b * a.T + col) * HD + (int64_t)h * D + 8 * sl);
+    const int col = colv[it];
+    const uint4 w = kw[it];
     const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
     double acc = 0.0;
 #pragma unroll
@@ -104,22 +118,31 @@ __global__ __launch_bounds__(256) void decode_partial_kernel(DecodeArgs a) {
     const double l = ok ? a.scale * acc : -INFINITY;
     lg[it] = l;
     mx = fmax(mx, l);
-    if (ok && sl == 0) a.logit[(int64_t)bh * a.n + p] = l;
+    if (ok && sl == 0) {
+      a.logit[(int64_t)bh * a.n + p] = l;
+      if (a.c_next > 0) {
+        const bool forced = col < a.n_sink || (a.window > 0 && col >= a.T - a.window);
+        a.key[(int64_t)bh * a.n + p] = forced ? INFINITY : (float)l;
+      }
+    }
   }
   mx = wave_max_f64(mx);
   if (lane == 0) s_red[wave] = mx;
   __syncthreads();
   mx = fmax(fmax(s_red[0], s_red[1]), fmax(s_red[2], s_red[3]));
   __syncthreads();
-  // pass 2: exp-weights against the chunk max, exp-sum and the weighted V rows
+  // pass 2: exp-weights against the chunk max, exp-sum and the weighted V rows (loads first again)
   double es = 0.0;
   float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+  for (int it = 0; it < IT; ++it)
+    kw[it] = *reinterpret_cast<const uint4*>(a.v + ((int64_t)b * a.T + colv[it]) * HD + (int64_t)h * D + 8 * sl);
 #pragma unroll
   for (int it = 0; it < IT; ++it) {
     const double e = exp(lg[it] - mx);          // 0 for positions past the end
     if (sl == 0) es += e;
     const float wf = (float)e;
-    const uint4 w = *reinterpret_cast<const uint4*>(a.v + ((int64_t)b * a.T + colv[it]) * HD + (int64_t)h * D + 8 * sl);
+    const uint4 w = kw[it];
     const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
@@ -149,11 +172,12 @@ __global__ __launch_bounds__(256) void decode_partial_kernel(DecodeArgs a) {
   }
 }
 
-// ---- combine: the output and the ranking keys of one (b, h) ------------------------------------------
+// ---- combine: the output of one (b, h) from its chunks (nch <= 256) -------------------------------------
 template <int D>
 __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a) {
   __shared__ double s_m[4];
   __shared__ double s_l;
+  __shared__ float s_f[256];
   const int bh = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const bool dense = a.cols == nullptr;
@@ -177,13 +201,11 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a) {
   __syncthreads();
   const double S = s_l;
   const double L = M + log(S);
+  if (tid < a.nch) s_f[tid] = (float)(m * exp(a.pmax[(int64_t)bh * a.nch + tid] - M) / S);   // chunk weights
+  __syncthreads();
   if (tid < D) {
     float add = 0.0f;
-    for (int c = 0; c < a.nch; ++c) {
-      const int64_t sidx = (int64_t)bh * a.nch + c;
-      const float f = (float)(m * exp(a.pmax[sidx] - M) / S);
-      add = fmaf(f, a.pacc[sidx * D + tid], add);
-    }
+    for (int c = 0; c < a.nch; ++c) add = fmaf(s_f[c], a.pacc[((int64_t)bh * a.nch + c) * D + tid], add);
     const int64_t od = (int64_t)bh * D + tid;
     a.o[od] = dense ? add : a.o[od] - a.sub[od] + add;
   }
@@ -191,45 +213,56 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a) {
     a.ltot[bh] = L;
     if (a.lse) a.lse[bh] = (float)L;
   }
-  if (a.c_next > 0) {
-    for (int p = tid; p < a.n; p += 256) {
-      const int col = dec_col(a, bh, p);
-      const bool forced = col < a.n_sink || (a.window > 0 && col >= a.T - a.window);
-      const double pr = m * exp(a.logit[(int64_t)bh * a.n + p] - L);
-      a.key[(int64_t)bh * a.n + p] = forced ? INFINITY : (float)pr;
-    }
-  }
 }
 
-// ---- finalize: the next loop's columns, mass and subtract term of one (b, h) ------------------------
+// ---- finalize: the next loop's columns, mass and subtract term ---------------------------------------
+// decode_select_partial: a workgroup takes 256 selected positions of one (b, h) (ids, probabilities and
+// weighted V rows, every load of a stage issued before any use); decode_select_reduce adds the
+// workgroups' parts in order (deterministic) into the mass and subtract term.
 template <int D>
-__global__ __launch_bounds__(256) void decode_finalize_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(256) void decode_select_partial_kernel(DecodeArgs a) {
   constexpr int LPC = D / 8;
   constexpr int CPW = 64 / LPC;
+  constexpr int IT = (kDecChunk / 4) / CPW;
   __shared__ double s_red[4];
   __shared__ float s_acc[4][D];
-  const int bh = blockIdx.x;
+  const int chunk = blockIdx.x, bh = blockIdx.y;
   const int b = bh / a.H, h = bh % a.H;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int sl = lane % LPC, grp = lane / LPC;
   const int64_t HD = (int64_t)a.H * D;
   const double m = a.cols == nullptr ? 1.0 : (double)a.mass[bh];
   const double L = a.ltot[bh];
+  const int i0 = chunk * kDecChunk + wave * (kDecChunk / 4) + grp;
+  int p[IT], col[IT];
+  double l[IT];
+  uint4 w[IT];
+#pragma unroll
+  for (int it = 0; it < IT; ++it) {
+    const int i = i0 + it * CPW;
+    p[it] = i < a.c_next ? a.sel[(int64_t)bh * a.c_next + i] : 0;
+  }
+#pragma unroll
+  for (int it = 0; it < IT; ++it) {
+    col[it] = dec_col(a, bh, p[it]);
+    l[it] = a.logit[(int64_t)bh * a.n + p[it]];
+  }
+#pragma unroll
+  for (int it = 0; it < IT; ++it)
+    w[it] = *reinterpret_cast<const uint4*>(a.v + ((int64_t)b * a.T + col[it]) * HD + (int64_t)h * D + 8 * sl);
   double ms = 0.0;
   float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  for (int i0 = wave * CPW; i0 < a.c_next; i0 += 4 * CPW) {
-    const int i = i0 + grp;
+#pragma unroll
+  for (int it = 0; it < IT; ++it) {
+    const int i = i0 + it * CPW;
     const bool ok = i < a.c_next;
-    const int p = ok ? a.sel[(int64_t)bh * a.c_next + i] : 0;
-    const int col = dec_col(a, bh, p);
-    const double pr = ok ? m * exp(a.logit[(int64_t)bh * a.n + p] - L) : 0.0;
+    const double pr = ok ? m * exp(l[it] - L) : 0.0;
     if (ok && sl == 0) {
-      a.cols_next[(int64_t)bh * a.c_next + i] = col;
+      a.cols_next[(int64_t)bh * a.c_next + i] = col[it];
       ms += pr;
     }
     const float wf = (float)pr;
-    const uint4 w = *reinterpret_cast<const uint4*>(a.v + ((int64_t)b * a.T + col) * HD + (int64_t)h * D + 8 * sl);
-    const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+    const uint32_t ws[4] = {w[it].x, w[it].y, w[it].z, w[it].w};
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       acc[2 * t] = fmaf(wf, bf16_to_f32(ws[t] & 0xFFFFu), acc[2 * t]);
@@ -246,16 +279,32 @@ __global__ __launch_bounds__(256) void decode_finalize_kernel(DecodeArgs a) {
   }
   if (lane == 0) s_red[wave] = ms;
   __syncthreads();
+  const int64_t slot = (int64_t)bh * a.nfc + chunk;
   if (threadIdx.x < D) {
     const int dd = threadIdx.x;
-    a.sub_next[(int64_t)bh * D + dd] = s_acc[0][dd] + s_acc[1][dd] + s_acc[2][dd] + s_acc[3][dd];
+    a.fsub[slot * D + dd] = s_acc[0][dd] + s_acc[1][dd] + s_acc[2][dd] + s_acc[3][dd];
   }
-  if (threadIdx.x == 0) a.mass_next[bh] = (float)(s_red[0] + s_red[1] + s_red[2] + s_red[3]);
+  if (threadIdx.x == 0) a.fmass[slot] = s_red[0] + s_red[1] + s_red[2] + s_red[3];
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void decode_select_reduce_kernel(DecodeArgs a) {
+  const int bh = blockIdx.x;
+  if (threadIdx.x < D) {
+    float sacc = 0.0f;
+    for (int c = 0; c < a.nfc; ++c) sacc += a.fsub[((int64_t)bh * a.nfc + c) * D + threadIdx.x];
+    a.sub_next[(int64_t)bh * D + threadIdx.x] = sacc;
+  }
+  if (threadIdx.x == 0) {
+    double ms = 0.0;
+    for (int c = 0; c < a.nfc; ++c) ms += a.fmass[(int64_t)bh * a.nfc + c];
+    a.mass_next[bh] = (float)ms;
+  }
 }
 
 // workspace regions, each 256-byte aligned
 struct DecodeWs {
-  size_t logit, pmax, psum, pacc, ltot, key, sel, total;
+  size_t logit, pmax, psum, pacc, ltot, key, sel, fmass, fsub, total;
 };
 static DecodeWs decode_ws(int B, int H, int d, int n, int c_next) {
   auto al = [](size_t x) { return (x + 255) / 256 * 256; };
@@ -270,6 +319,9 @@ static DecodeWs decode_ws(int B, int H, int d, int n, int c_next) {
   w.ltot = off; off += al(bh * sizeof(double));
   w.key = off; off += al(bh * n * sizeof(float));
   w.sel = off; off += al(bh * (size_t)c_next * sizeof(int32_t));
+  const size_t nfc = ((size_t)c_next + kDecChunk - 1) / kDecChunk;
+  w.fmass = off; off += al(bh * nfc * sizeof(double));
+  w.fsub = off; off += al(bh * nfc * d * sizeof(float));
   w.total = off;
   return w;
 }
@@ -322,8 +374,11 @@ extern "C" int fl_decode_step(const uint16_t* q, const uint16_t* k_cache, const 
   a.ltot = reinterpret_cast<double*>(base + L.ltot);
   a.key = reinterpret_cast<float*>(base + L.key);
   a.sel = reinterpret_cast<const int32_t*>(base + L.sel);
+  a.fmass = reinterpret_cast<double*>(base + L.fmass);
+  a.fsub = reinterpret_cast<float*>(base + L.fsub);
   a.cols_next = cols_next; a.mass_next = mass_next; a.sub_next = sub_next;
   a.B = B; a.T = T; a.H = H; a.n = n; a.nch = (n + kDecChunk - 1) / kDecChunk; a.c_next = c_next;
+  a.nfc = (c_next + kDecChunk - 1) / kDecChunk;
   a.n_sink = n_sink; a.window = window; a.scale = (double)sm_scale;
   const int BH = B * H;
   dim3 gp(a.nch, BH);
@@ -337,8 +392,13 @@ extern "C" int fl_decode_step(const uint16_t* q, const uint16_t* k_cache, const 
   if (rc != FL_OK || c_next == 0) return rc;
   rc = launch_topk(BH, a.key, n, n, c_next, nullptr, 0, 0, const_cast<int32_t*>(a.sel), c_next, 0, nullptr, 0, st);
   if (rc != FL_OK) return rc;
-  if (d == 128) decode_finalize_kernel<128><<<BH, 256, 0, st>>>(a);
-  else decode_finalize_kernel<64><<<BH, 256, 0, st>>>(a);
-  return check_launch("decode_finalize_kernel");
+  dim3 gf(a.nfc, BH);
+  if (d == 128) decode_select_partial_kernel<128><<<gf, 256, 0, st>>>(a);
+  else decode_select_partial_kernel<64><<<gf, 256, 0, st>>>(a);
+  rc = check_launch("decode_select_partial_kernel");
+  if (rc != FL_OK) return rc;
+  if (d == 128) decode_select_reduce_kernel<128><<<BH, 256, 0, st>>>(a);
+  else decode_select_reduce_kernel<64><<<BH, 256, 0, st>>>(a);
+  return check_launch("decode_select_reduce_kernel");
   FL_API_END
 }

@@ -7,8 +7,8 @@
 * with an unchanged state and a partial column set the update is the identity (the cached mass and
   subtract term must both be right for the correction to cancel);
 * with only V changing, the update is the closed form sum_S p_j (V^(r)_j - V^(r-1)_j);
-* the selection keeps the sinks and the window, then matches a brute-force ranking (fp32 keys, ties to
-  the lower column); it is nested and its mass is the sum of its probabilities.
+* the selection keeps the sinks and the window, then matches a brute-force ranking by probability (ties
+  to the lower column); it is nested and its mass is the sum of its probabilities.
 """
 import numpy as np
 import torch
@@ -94,8 +94,7 @@ def test_selection_forced_columns_ties_and_nesting():
     forced = set(range(n_sink)) | set(range(T - window, T))
     assert forced <= set(S.tolist())
     rest = [j for j in range(T) if j not in forced]
-    key = p.astype(np.float32)
-    ranked = sorted(rest, key=lambda j: (-float(key[j]), j))[:c - len(forced)]
+    ranked = sorted(rest, key=lambda j: (-float(p[j]), j))[:c - len(forced)]   # brute force on the probabilities
     assert S.tolist() == sorted(forced | set(ranked))
     assert abs(m - p[S].sum()) < 1e-14 and m <= 1.0
     np.testing.assert_allclose(sub, p[S] @ v[S], rtol=1e-13)
