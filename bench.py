@@ -267,6 +267,7 @@ def main():
     ap.add_argument("--workload", default="C4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--decode-only", action="store_true", help="only the decode measurement (for traces)")
     ap.add_argument("--copy-calib", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -299,6 +300,9 @@ def main():
     torch.cuda.synchronize()
     log(f"[bench] loop-1 setup on GPU {time.time() - t0:.2f}s")
     step = Step(w, dev, gs, fl, torch)
+    if args.decode_only:
+        print(json.dumps({"decode": decode_bench(w, gs, fl, torch)}), flush=True)
+        return
 
     for _ in range(args.warmup):
         step.run()

@@ -9,7 +9,7 @@
 // p_j grows with l_j, so the ranking key is fp32(l_j), available before L is known.
 //
 // One row per (b, h) is a GEMV: HBM-bound, split over columns.
-//   decode_partial  chunks of 256 positions: fp64 logits (exact bf16 products, fp64 sums) and their fp32
+//   decode_partial  chunks of 128 positions: fp64 logits (exact bf16 products, fp64 sums) and their fp32
 //                   ranking keys (forced columns +inf), the chunk's max and exp-sum, and the
 //                   exp-weighted sum of its V rows (fp32); K and V rows are each read once, 16 bytes per
 //                   lane, D/8 lanes per row.
@@ -21,7 +21,15 @@
 
 namespace fl {
 
-constexpr int kDecChunk = 256;           // positions per partial workgroup
+constexpr int kDecChunk = 128;           // positions per partial workgroup
+constexpr int kSelChunk = 256;           // selected positions per selection workgroup
+
+// 16-byte load marked non-temporal: the K and V rows of a step are streamed once
+typedef uint32_t u32x4d __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 stream16(const uint16_t* p) {
+  const u32x4d w = __builtin_nontemporal_load(reinterpret_cast<const u32x4d*>(p));
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
 
 struct DecodeArgs {
   const uint16_t* q;         // [B, H, D]
@@ -86,10 +94,10 @@ __global__ __launch_bounds__(256) void decode_partial_kernel(DecodeArgs a) {
     }
   }
   // pass 1: logits (every lane of a row group ends with the row's full dot product).  All column ids,
-  // then all K loads, are issued before any use, so a chunk costs two load latencies, not 2 * IT.
+  // then all K and V loads, are issued before any use, so a chunk costs two load latencies.
   double lg[IT];
   int colv[IT];
-  uint4 kw[IT];
+  uint4 kw[IT], vw[IT];
   double mx = -INFINITY;
   const int p0 = chunk * kDecChunk + wave * PER_WAVE + grp;
 #pragma unroll
@@ -98,8 +106,11 @@ __global__ __launch_bounds__(256) void decode_partial_kernel(DecodeArgs a) {
     colv[it] = p < a.n ? dec_col(a, bh, p) : 0;
   }
 #pragma unroll
-  for (int it = 0; it < IT; ++it)
-    kw[it] = *reinterpret_cast<const uint4*>(a.k + ((int64_t)b * a.T + colv[it]) * HD + (int64_t)h * D + 8 * sl);
+  for (int it = 0; it < IT; ++it) {
+    const int64_t off = ((int64_t)b * a.T + colv[it]) * HD + (int64_t)h * D + 8 * sl;
+    kw[it] = stream16(a.k + off);
+    vw[it] = stream16(a.v + off);
+  }
 #pragma unroll
   for (int it = 0; it < IT; ++it) {
     const int p = p0 + it * CPW;
@@ -131,18 +142,15 @@ __global__ __launch_bounds__(256) void decode_partial_kernel(DecodeArgs a) {
   __syncthreads();
   mx = fmax(fmax(s_red[0], s_red[1]), fmax(s_red[2], s_red[3]));
   __syncthreads();
-  // pass 2: exp-weights against the chunk max, exp-sum and the weighted V rows (loads first again)
+  // pass 2: exp-weights against the chunk max, exp-sum and the weighted V rows
   double es = 0.0;
   float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-#pragma unroll
-  for (int it = 0; it < IT; ++it)
-    kw[it] = *reinterpret_cast<const uint4*>(a.v + ((int64_t)b * a.T + colv[it]) * HD + (int64_t)h * D + 8 * sl);
 #pragma unroll
   for (int it = 0; it < IT; ++it) {
     const double e = exp(lg[it] - mx);          // 0 for positions past the end
     if (sl == 0) es += e;
     const float wf = (float)e;
-    const uint4 w = kw[it];
+    const uint4 w = vw[it];
     const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
@@ -172,12 +180,12 @@ __global__ __launch_bounds__(256) void decode_partial_kernel(DecodeArgs a) {
   }
 }
 
-// ---- combine: the output of one (b, h) from its chunks (nch <= 256) -------------------------------------
+// ---- combine: the output of one (b, h) from its chunks (nch <= 512) -------------------------------------
 template <int D>
 __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a) {
   __shared__ double s_m[4];
   __shared__ double s_l;
-  __shared__ float s_f[256];
+  __shared__ float s_f[512];
   const int bh = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const bool dense = a.cols == nullptr;
@@ -201,7 +209,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a) {
   __syncthreads();
   const double S = s_l;
   const double L = M + log(S);
-  if (tid < a.nch) s_f[tid] = (float)(m * exp(a.pmax[(int64_t)bh * a.nch + tid] - M) / S);   // chunk weights
+  for (int c = tid; c < a.nch; c += 256) s_f[c] = (float)(m * exp(a.pmax[(int64_t)bh * a.nch + c] - M) / S);
   __syncthreads();
   if (tid < D) {
     float add = 0.0f;
@@ -223,7 +231,7 @@ template <int D>
 __global__ __launch_bounds__(256) void decode_select_partial_kernel(DecodeArgs a) {
   constexpr int LPC = D / 8;
   constexpr int CPW = 64 / LPC;
-  constexpr int IT = (kDecChunk / 4) / CPW;
+  constexpr int IT = (kSelChunk / 4) / CPW;
   __shared__ double s_red[4];
   __shared__ float s_acc[4][D];
   const int chunk = blockIdx.x, bh = blockIdx.y;
@@ -233,7 +241,7 @@ __global__ __launch_bounds__(256) void decode_select_partial_kernel(DecodeArgs a
   const int64_t HD = (int64_t)a.H * D;
   const double m = a.cols == nullptr ? 1.0 : (double)a.mass[bh];
   const double L = a.ltot[bh];
-  const int i0 = chunk * kDecChunk + wave * (kDecChunk / 4) + grp;
+  const int i0 = chunk * kSelChunk + wave * (kSelChunk / 4) + grp;
   int p[IT], col[IT];
   double l[IT];
   uint4 w[IT];
@@ -319,7 +327,7 @@ static DecodeWs decode_ws(int B, int H, int d, int n, int c_next) {
   w.ltot = off; off += al(bh * sizeof(double));
   w.key = off; off += al(bh * n * sizeof(float));
   w.sel = off; off += al(bh * (size_t)c_next * sizeof(int32_t));
-  const size_t nfc = ((size_t)c_next + kDecChunk - 1) / kDecChunk;
+  const size_t nfc = ((size_t)c_next + kSelChunk - 1) / kSelChunk;
   w.fmass = off; off += al(bh * nfc * sizeof(double));
   w.fsub = off; off += al(bh * nfc * d * sizeof(float));
   w.total = off;
@@ -378,7 +386,7 @@ extern "C" int fl_decode_step(const uint16_t* q, const uint16_t* k_cache, const 
   a.fsub = reinterpret_cast<float*>(base + L.fsub);
   a.cols_next = cols_next; a.mass_next = mass_next; a.sub_next = sub_next;
   a.B = B; a.T = T; a.H = H; a.n = n; a.nch = (n + kDecChunk - 1) / kDecChunk; a.c_next = c_next;
-  a.nfc = (c_next + kDecChunk - 1) / kDecChunk;
+  a.nfc = (c_next + kSelChunk - 1) / kSelChunk;
   a.n_sink = n_sink; a.window = window; a.scale = (double)sm_scale;
   const int BH = B * H;
   dim3 gp(a.nch, BH);

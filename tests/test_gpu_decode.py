@@ -4,7 +4,7 @@ Each case runs a dense source loop and then sparse loops on both sides independe
 feeds itself its own selections, masses and subtract terms; the oracle chain its own), with the state
 of every loop perturbed on a subset of positions.  Bit-exact: the selected columns of every loop.
 Tolerance (max-abs 1e-2, relative Frobenius 2e-3 vs fp64): outputs, log-normalisers, masses and
-subtract terms.  Shapes: several 256-position chunks with a ragged tail, ties in the probabilities,
+subtract terms.  Shapes: several 128-position chunks with a ragged tail, ties in the probabilities,
 budgets that keep everything, shrink, or stop; and the 32K shape.
 """
 import numpy as np
@@ -80,7 +80,7 @@ def _run_chain(F, B, T, H, d, budgets, n_sink, window, seed, ties=False, check_h
 
 @pytest.mark.parametrize("d", [64, 128])
 def test_decode_chain_small(F, d):
-    # T = 700: three chunks, the last ragged; budgets shrink, keep all of S, then stop
+    # T = 700: six chunks, the last ragged; budgets shrink, keep all of S, then stop
     _run_chain(F, B=2, T=700, H=3, d=d, budgets=[180, 120, 120, 37, 0], n_sink=4, window=32, seed=d, ties=True)
 
 
