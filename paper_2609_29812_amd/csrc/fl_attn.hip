@@ -138,12 +138,12 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
   constexpr int INST_PER_TILE = kBN / COLS_PER_INST;
   constexpr int INST_PER_WAVE = INST_PER_TILE / 4;   // per tensor (K and V each)
   __shared__ Slot<D> s0, s1, s2, s3;
-  // column ids of tile v in entry v % 8 (kPad = padding): view 0 plain (dense loop, subtract pass), view 1
-  // for the add pass, where the columns updated this loop are padding in phases A/B.
-  __shared__ int tcv[2][8][kBN];
-  __shared__ uint32_t toff[8][kBN];       // byte offset of each column's row in its source (kOOB: none)
-  // tile v: first and last (plain) column id, whether some column was updated this loop (phases A/B)
-  __shared__ int thd[8][4];
+  // tables of tile v in entry v % 8, written by two 64-lane stores with no branch:
+  //   [0, kBN)        column ids, plain (dense loop, subtract pass; kPad = padding)
+  //   [kBN, 2 kBN)    column ids for the add pass, where the columns updated this loop are padding
+  //   [2 kBN, 3 kBN)  byte offset of each column's row in its source (kOOB: none)
+  //   [3 kBN, 4 kBN)  whether some column of the tile was updated this loop (every entry the same)
+  __shared__ uint32_t tab[8][4 * kBN];
   __shared__ float xm[2][64];             // end-of-loop hand-off per group: the subtract pass's mass
   __shared__ int s_meta[2];
 
@@ -289,16 +289,13 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
       row = newer ? aux : cid;
     }
     const bool valid = cid != kPad;
-    if (lane < kBN) {
-      const int cid_add = upd ? kPad : cid;
-      tcv[0][v & 7][c32] = cid;
-      tcv[1][v & 7][c32] = cid_add;
-      if (c32 == 0) thd[v & 7][0] = cid;
-      if (c32 == kBN - 1) thd[v & 7][1] = cid;
-      toff[v & 7][c32] = valid ? (uint32_t)row * rb + head_off : kOOB;
-    }
+    // lanes 0-31 hold the records; lanes 32-63 take their add-view ids across the half-swap
+    const uint32_t cid_add = upd ? (uint32_t)kPad : (uint32_t)cid;
+    const auto sw = __builtin_amdgcn_permlane32_swap(cid_add, cid_add, false, false);
+    const uint32_t off = valid ? (uint32_t)row * rb + head_off : kOOB;
     const uint64_t any = __builtin_amdgcn_ballot_w64(lane < kBN && valid && upd);
-    if (lane == 0) thd[v & 7][2] = any != 0;
+    tab[v & 7][lane] = lane < kBN ? (uint32_t)cid : (uint32_t)sw[0];
+    tab[v & 7][2 * kBN + lane] = lane < kBN ? off : (uint32_t)(any != 0);
   };
 
   // LDS-DMA of tile u into slot sl: each wave issues INST_PER_WAVE K and INST_PER_WAVE V instructions,
@@ -325,7 +322,7 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
 #pragma unroll
     for (int t = 0; t < NI; ++t) {
       const int c = inst_of(t) * COLS_PER_INST + lane / CH;
-      r.o[t] = toff[u & 7][c] + (uint32_t)swz(c, lane % CH) * 16;   // kOOB + 240 is still out of range
+      r.o[t] = tab[u & 7][2 * kBN + c] + (uint32_t)swz(c, lane % CH) * 16;   // kOOB + 240 is still out of range
     }
     return r;
   };
@@ -419,7 +416,7 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
   // the barrier, the entries were written four steps earlier)
   struct TileHead { int c0, clast, any; };
   auto tile_head = [=](int u) {
-    return TileHead{thd[u & 7][0], thd[u & 7][1], thd[u & 7][2]};
+    return TileHead{(int)tab[u & 7][0], (int)tab[u & 7][kBN - 1], (int)tab[u & 7][3 * kBN]};
   };
 
   auto compute = [=, &acc, &run_max, &lsum, &msub](int u, const Slot<D>& sl, const TileHead& th) {
@@ -458,7 +455,7 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
       int cc[16];
 #pragma unroll
       for (int j = 0; j < NE / 4; ++j) {
-        const int4 c4 = *reinterpret_cast<const int4*>(&tcv[view][ri][8 * j + 4 * hw]);
+        const int4 c4 = *reinterpret_cast<const int4*>(&tab[ri][kBN * view + 8 * j + 4 * hw]);
         cc[4 * j] = c4.x; cc[4 * j + 1] = c4.y; cc[4 * j + 2] = c4.z; cc[4 * j + 3] = c4.w;
       }
       if (is_list) {
