@@ -131,3 +131,31 @@ def test_select_and_codec_reject_bad_arguments(lib):
     dq = lib.fl_kv_residual_dequant(DUMMY, DUMMY, DUMMY, DUMMY, 8, 1, 64, 2, 64, 4, 32, fl.AXIS_TOKEN, 7, DUMMY,
                                     None, None)
     assert dq == FL_E_UNSUPPORTED                                   # unknown mode
+
+
+def test_decode_workspace_and_argument_checks(lib):
+    # workspace: fp64 logits, chunk parts, fp32 keys and selection parts; 0 for unsupported shapes
+    assert lib.fl_decode_step_ws(1, 4096, 16, 128, 0, 2048) > 4096 * 16 * 12
+    assert lib.fl_decode_step_ws(1, 4096, 16, 96, 0, 2048) == 0
+    assert lib.fl_decode_step_ws(0, 4096, 16, 128, 0, 2048) == 0
+    WS = ctypes.c_size_t(1 << 40)
+
+    def dec(**kw):
+        return lib.fl_decode_step(
+            kw.get("q", DUMMY), DUMMY, DUMMY, kw.get("cols"), kw.get("c", 0), kw.get("mass"), kw.get("sub"),
+            1, kw.get("T", 64), 2, kw.get("d", 64), ctypes.c_float(kw.get("scale", 0.125)), DUMMY, None,
+            kw.get("n_sink", 4), 8, kw.get("c_next", 16), kw.get("cn", DUMMY), DUMMY, DUMMY,
+            kw.get("ws", DUMMY), kw.get("wsb", WS), None)
+    assert dec(q=None) == FL_E_NULL
+    assert dec(d=96) == FL_E_SHAPE
+    assert dec(scale=0.0) == FL_E_RANGE
+    assert dec(c=5) == FL_E_SHAPE                               # dense: c must be 0 or T
+    assert dec(cols=DUMMY, c=65, mass=DUMMY, sub=DUMMY) == FL_E_RANGE
+    assert dec(cols=DUMMY, c=10) == FL_E_NULL                    # sparse needs mass and sub
+    assert dec(c_next=65) == FL_E_RANGE
+    assert dec(cn=None) == FL_E_NULL                             # a selection needs its outputs
+    assert dec(n_sink=-1) == FL_E_RANGE
+    assert dec(T=70000) == FL_E_SHAPE                            # more columns than the selection takes
+    assert dec(ws=None) == FL_E_WORKSPACE
+    assert dec(wsb=ctypes.c_size_t(16)) == FL_E_WORKSPACE
+    assert b"fl_decode_step" in lib.fl_last_error()
