@@ -3,6 +3,8 @@
 // score_rows: one wave per candidate row streams the four bf16 rows (K and V, current and previous)
 //   with non-temporal 16-byte loads, forms fp32 differences, accumulates squared norms in fp64,
 //   reduces across the wave and writes the fp32 key.  HBM-bound: 4 * D * 2 bytes per candidate.
+//   When the budget keeps every candidate (k = n_cand, nested loops with a constant budget), extra
+//   workgroups of the same launch write the selection itself: the candidates and their slot map.
 // topk_select: one 1024-thread workgroup per segment.  Keys are mapped to order-preserving uint32 and
 //   held in registers (M per thread).  The k-th largest key is found in two stages: an LDS histogram
 //   of the top 12 bits and a block scan over its 4096 bins give the bin that holds it; the keys of
@@ -39,14 +41,35 @@ __device__ __forceinline__ void accum_pair(uint4 c, uint4 p, double& num, double
   }
 }
 
+// take_all (k == n_cand): workgroups past the scoring ones write the selection itself, which keeps every
+// candidate: idx = the candidates, and slot[j] = j's position among them (binary search) or -1.
 __global__ __launch_bounds__(64 * kScoreWaves) void score_rows_kernel(
     const uint16_t* __restrict__ k_cur, const uint16_t* __restrict__ k_prev,
     const uint16_t* __restrict__ v_cur, const uint16_t* __restrict__ v_prev, int N, int D,
     const int32_t* __restrict__ cand, int n_cand, int normalize, double eps,
-    float* __restrict__ out_key) {
+    float* __restrict__ out_key, int score_blocks, int32_t* __restrict__ take_idx,
+    int32_t* __restrict__ take_slot) {
   const int lane = threadIdx.x & 63;
-  const int p = blockIdx.x * kScoreWaves + (threadIdx.x >> 6);
   const int b = blockIdx.y;
+  if ((int)blockIdx.x >= score_blocks) {
+    const int64_t t = (int64_t)(blockIdx.x - score_blocks) * blockDim.x + threadIdx.x;
+    const int32_t* cp = cand ? cand + (int64_t)b * n_cand : nullptr;
+    if (t < n_cand) take_idx[(int64_t)b * n_cand + t] = cp ? cp[t] : (int32_t)t;
+    if (take_slot && t < N) {
+      int pos = (int)t;                    // all rows are candidates without a list
+      if (cp) {
+        int lo = 0, hi = n_cand;
+        while (lo < hi) {
+          const int mid = (lo + hi) >> 1;
+          if (cp[mid] < (int)t) lo = mid + 1; else hi = mid;
+        }
+        pos = (lo < n_cand && cp[lo] == (int)t) ? lo : -1;
+      }
+      take_slot[(int64_t)b * N + t] = pos;
+    }
+    return;
+  }
+  const int p = blockIdx.x * kScoreWaves + (threadIdx.x >> 6);
   if (p >= n_cand) return;
   const int64_t row = cand ? (int64_t)cand[(int64_t)b * n_cand + p] : (int64_t)p;
   const int64_t base = ((int64_t)b * N + row) * D;
@@ -438,13 +461,18 @@ extern "C" int fl_select_tokens(const uint16_t* k_cur, const uint16_t* k_prev,
   FL_REQUIRE(k == 0 || out_idx, FL_E_NULL, "fl_select_tokens: out_idx is required when k > 0");
   FL_REQUIRE(eps >= 0.0, FL_E_RANGE, "fl_select_tokens: eps must be >= 0");
   hipStream_t st = as_stream(stream);
+  // k == n_cand keeps every candidate: the scoring launch also writes the selection (no top-k launch)
+  const bool take_all = k == n_cand && k > 0;
   if (n_cand > 0) {
-    dim3 grid((n_cand + kScoreWaves - 1) / kScoreWaves, B), block(64 * kScoreWaves);
+    const int score_blocks = (n_cand + kScoreWaves - 1) / kScoreWaves;
+    const int fill_blocks = take_all ? (N + 64 * kScoreWaves - 1) / (64 * kScoreWaves) : 0;
+    dim3 grid(score_blocks + fill_blocks, B), block(64 * kScoreWaves);
     score_rows_kernel<<<grid, block, 0, st>>>(k_cur, k_prev, v_cur, v_prev, N, D, cand, n_cand,
-                                              normalize, eps, out_key);
+                                              normalize, eps, out_key, score_blocks, out_idx, out_slot);
     int rc = check_launch("score_rows_kernel");
     if (rc != FL_OK) return rc;
   }
+  if (take_all) return FL_OK;
   if (k == 0 && !out_slot) return FL_OK;
   return launch_topk(B, out_key, n_cand, n_cand, k, cand, n_cand, 0, out_idx, k, 0, out_slot, N, st);
   FL_API_END
