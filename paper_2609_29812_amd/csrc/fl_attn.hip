@@ -65,6 +65,7 @@ struct AttnArgs {
   int k, k_prev, c_list, window, B, N, H;
   float scale_log2;          // sm_scale * log2(e)
   int cache_current;         // reuse: the caches already hold X_hat^(r) of the updated rows (no new rows)
+  float pinf;                // +inf
 };
 
 typedef __amdgpu_buffer_rsrc_t rsrc_t;
@@ -235,8 +236,8 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
     pb = last_p + 1;
   }
   __syncthreads();
-  const int nA = s_meta[0];
-  const int nC = s_meta[1];
+  const int nA = __builtin_amdgcn_readfirstlane(s_meta[0]);   // (uniform: scalar tests and branches below)
+  const int nC = __builtin_amdgcn_readfirstlane(s_meta[1]);
   const int tA = (nA + kBN - 1) / kBN;
   const int tB = bandHi >= bandLo ? (bandHi - bandLo + kBN) / kBN : 0;
   const int tC = (nC + kBN - 1) / kBN;
@@ -416,7 +417,9 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
   // the barrier, the entries were written four steps earlier)
   struct TileHead { int c0, clast, any; };
   auto tile_head = [=](int u) {
-    return TileHead{(int)tab[u & 7][0], (int)tab[u & 7][kBN - 1], (int)tab[u & 7][3 * kBN]};
+    return TileHead{__builtin_amdgcn_readfirstlane((int)tab[u & 7][0]),
+                    __builtin_amdgcn_readfirstlane((int)tab[u & 7][kBN - 1]),
+                    __builtin_amdgcn_readfirstlane((int)tab[u & 7][3 * kBN])};
   };
 
   auto compute = [=, &acc, &run_max, &lsum, &msub](int u, const Slot<D>& sl, const TileHead& th) {
@@ -784,8 +787,8 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
     pb = CUR ? lo : last_p + 1;
   }
   __syncthreads();
-  const int nA = s_meta[0];
-  const int nC = s_meta[1];
+  const int nA = __builtin_amdgcn_readfirstlane(s_meta[0]);   // (uniform: scalar tests and branches below)
+  const int nC = __builtin_amdgcn_readfirstlane(s_meta[1]);
   const int tA = (nA + kBN - 1) / kBN;
   const int tB = bandHi >= bandLo ? (bandHi - bandLo + kBN) / kBN : 0;
   const int tC = (nC + kBN - 1) / kBN;
@@ -922,8 +925,11 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
 
   struct TileHead { int c0, clast, any; };
   auto tile_head = [=](int u) {
-    if constexpr (CUR) return TileHead{(int)tab[u & 7][0], (int)tab[u & 7][kBN - 1], 0};
-    return TileHead{thd[u & 7][0], thd[u & 7][1], thd[u & 7][2]};
+    if constexpr (CUR)
+      return TileHead{__builtin_amdgcn_readfirstlane((int)tab[u & 7][0]),
+                      __builtin_amdgcn_readfirstlane((int)tab[u & 7][kBN - 1]), 0};
+    return TileHead{__builtin_amdgcn_readfirstlane(thd[u & 7][0]), __builtin_amdgcn_readfirstlane(thd[u & 7][1]),
+                    __builtin_amdgcn_readfirstlane(thd[u & 7][2])};
   };
 
   // column mask of the lane's 8 entries (ids cc, columns 16c + 4 g4 + v): list columns need
@@ -1124,6 +1130,335 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
   }
 }
 
+// ---- add pass over current caches with the column list in LDS ------------------------------------------
+// With the caches already holding this loop's rows, a tile is either 32 consecutive entries of the
+// (b, h) column list or 32 consecutive band columns.  A workgroup copies the list entries into LDS once
+// (up to kListCap of them), so every wave forms its own DMA offsets, column ids and tile bounds from that
+// copy or from the band range: the pipeline has no record loads and no per-step table writes, and each
+// step is one wait, one barrier, the DMA of tile s+3 and the math of tile s.  Rows, tiles, masks, the
+// online softmax and the epilogue are those of reuse_attn_kernel.
+constexpr int kListCap = 3072;
+
+// max(x, y) for non-NaN inputs (-inf included) as a median with +inf; pinf holds +inf as a kernel
+// argument, so the median is not folded back into a maximum with its NaN-quieting steps
+__device__ __forceinline__ float fmax_nn(float x, float y, float pinf) { return __builtin_amdgcn_fmed3f(x, y, pinf); }
+
+template <int D>
+__global__ __launch_bounds__(256, 2) void cur_attn_kernel(AttnArgs a) {
+  constexpr int BM = 64;                  // rows per workgroup (4 waves x 16)
+  constexpr int KS = D / 32;              // k-steps of QK^T (32 dims each)
+  constexpr int DB = D / 16;              // 16-dim output blocks
+  constexpr int CH = D / 8;               // 16-byte chunks per row
+  constexpr int COLS_PER_INST = 64 / CH;  // rows covered by one 1 KB LDS-DMA instruction
+  constexpr int INST_PER_TILE = kBN / COLS_PER_INST;
+  constexpr int INST_PER_WAVE = INST_PER_TILE / 4;   // per tensor (K and V each)
+  constexpr int NI = 2 * INST_PER_WAVE;
+  __shared__ Slot<D> s0, s1, s2, s3;
+  __shared__ __attribute__((aligned(16))) int lst[kListCap + kBN];   // list entries of (b, h), kPad-padded to whole tiles
+  __shared__ int s_meta[1];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int j16 = lane & 15, g4 = lane >> 4;
+
+  // work item -> (batch*head, row tile); the row tiles of one (batch, head) stay on one XCD
+  const int n_rt = (a.k + BM - 1) / BM;
+  const int n_bh = a.B * a.H;
+  int bh, rt;
+  if ((n_bh & 7) == 0) {
+    const int g = blockIdx.x & 7, s = blockIdx.x >> 3;
+    bh = g + 8 * (s / n_rt);
+    rt = n_rt - 1 - (s % n_rt);
+  } else {
+    bh = blockIdx.x / n_rt;
+    rt = n_rt - 1 - (blockIdx.x % n_rt);
+  }
+  const int b = bh / a.H, h = bh % a.H;
+  const int64_t HD = (int64_t)a.H * D;
+  const int32_t* rowp = a.rows + (int64_t)b * a.k;
+
+  const int p0 = rt * BM;
+  const int last_p = min(p0 + BM, a.k) - 1;
+  const int min_row = rowp[p0], max_row = rowp[last_p];
+  const int gp0 = p0 + 16 * wave;
+  const bool group_has_rows = gp0 < a.k;
+  const int gmin = group_has_rows ? rowp[gp0] : 0;
+  const int gmax = group_has_rows ? rowp[min(gp0 + 16, a.k) - 1] : -1;
+  const int p = gp0 + j16;
+  const bool row_ok = p < a.k;
+  const int row_i = row_ok ? rowp[p] : -1;
+
+  // query fragments (B operand of S^T = K Q^T): row j16, dims 32 ks + 8 g4 .. +7
+  bf16x8 qa[KS];
+  {
+    const int64_t qoff = ((int64_t)b * a.N + (row_ok ? row_i : 0)) * HD + (int64_t)h * D + g4 * 8;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const uint4 w = row_ok ? *reinterpret_cast<const uint4*>(a.q_cur + qoff + ks * 32) : make_uint4(0, 0, 0, 0);
+      qa[ks] = __builtin_bit_cast(bf16x8, w);
+    }
+  }
+
+  // ---- the list in LDS and the phase extents (uniform) --------------------------------------------------
+  // nA = list entries j with j + window <= max_row (the only ones a row of this workgroup can see); the
+  // list ascends, so thread i finds the boundary between entries i and i + 1
+  const int32_t* cp = a.cols + (int64_t)bh * a.c_list;
+  const int lim = max_row - a.window;
+  if (tid == 0) s_meta[0] = 0;
+  for (int i = tid; i < a.c_list; i += 256) lst[i] = cp[i];
+  __syncthreads();
+  for (int i = tid; i < a.c_list; i += 256)
+    if (lst[i] <= lim && (i + 1 == a.c_list || lst[i + 1] > lim)) s_meta[0] = i + 1;
+  __syncthreads();
+  const int nA = __builtin_amdgcn_readfirstlane(s_meta[0]);
+  if (tid < kBN) lst[nA + tid] = kPad;    // the last list tile's padding (entries nA .. are not read before)
+  const int bandLo = a.window > 0 ? max(0, min_row - a.window + 1) : 0;
+  const int bandHi = a.window > 0 ? max_row : -1;
+  const int tA = (nA + kBN - 1) / kBN;
+  const int tB = bandHi >= bandLo ? (bandHi - bandLo + kBN) / kBN : 0;
+  const int n_tiles = tA + tB;
+  const bool band_down = (rt & 1) != 0;   // neighbouring row tiles meet in the band columns they share
+  // tile v: list entries [kBN v, kBN v + kBN) or band columns [first, first + kBN) (ascending columns in
+  // both); returns the first entry index (list) or first column (band)
+  auto tile_first = [=](int v) {
+    const int tb = band_down ? tA + tB - 1 - v : v - tA;
+    return v < tA ? v * kBN : bandLo + tb * kBN;
+  };
+
+  // ---- LDS-DMA offsets: lane column c of instruction t (same for K and V) -------------------------------
+  const uint32_t rb = (uint32_t)(HD * 2);
+  const uint32_t head_off = (uint32_t)(h * D * 2);
+  const rsrc_t kcR = make_rsrc(a.k_cache + (int64_t)b * a.N * HD, (uint32_t)a.N * rb);
+  const rsrc_t vcR = make_rsrc(a.v_cache + (int64_t)b * a.N * HD, (uint32_t)a.N * rb);
+  auto inst_of = [=](int t) { return wave * INST_PER_WAVE + (t % INST_PER_WAVE); };
+  int lcol[INST_PER_WAVE];                // tile column of this lane in instruction t
+  uint32_t lsw[INST_PER_WAVE];            // its swizzled chunk offset
+#pragma unroll
+  for (int t = 0; t < INST_PER_WAVE; ++t) {
+    lcol[t] = inst_of(t) * COLS_PER_INST + lane / CH;
+    lsw[t] = (uint32_t)swz(lcol[t], lane % CH) * 16 + head_off;
+  }
+  struct Offs { uint32_t o[INST_PER_WAVE]; };
+  // (no branches: the list copy is read at a valid index for band tiles too, and the choice is a select)
+  auto tile_offs = [=](int v) {
+    Offs r;
+    const int f = tile_first(v);
+    const bool in_list = v < tA;
+    const int fl = in_list ? f : 0;
+    const int hi = in_list ? kBN - 1 : v < n_tiles ? bandHi - f : -1;   // tile columns c <= hi exist
+#pragma unroll
+    for (int t = 0; t < INST_PER_WAVE; ++t) {
+      const int idl = lst[fl + lcol[t]];
+      const int id = in_list ? idl : f + lcol[t];
+      r.o[t] = ((id != kPad) & (lcol[t] <= hi)) ? (uint32_t)id * rb + lsw[t] : kOOB;
+    }
+    return r;
+  };
+  // (each offset goes through a local: handing the struct member straight to the builtin makes the
+  // host compilation drop the kernel's launch stub)
+  auto issue = [=](Slot<D>& sl, const Offs& of) {
+#pragma unroll
+    for (int t = 0; t < NI; ++t) {
+      const int inst = inst_of(t);
+      const uint32_t off = of.o[t % INST_PER_WAVE];
+      if (t < INST_PER_WAVE)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(kcR, FL_LDS(sl.k + inst * 512), 16, off, 0, 0, kDmaPolicy);
+      else
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(vcR, FL_LDS(sl.v + inst * 512), 16, off, 0, 0, kDmaPolicy);
+    }
+  };
+  // LDS read offsets of the fragments, as in reuse_attn_kernel
+  int koff[2], voff[4];
+  {
+    const int t4 = j16 >> 2, q = lane & 3;
+    const int colv = 4 * g4 + t4;
+#pragma unroll
+    for (int e = 0; e < 2; ++e) koff[e] = j16 * D + ((4 * e + g4) ^ swz_f(j16)) * 8;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) voff[e] = colv * D + ((2 * e + (q >> 1)) ^ swz_f(colv)) * 8 + 4 * (q & 1);
+  }
+
+  f32x4 acc[DB];                          // add term, O^T blocks
+#pragma unroll
+  for (int db = 0; db < DB; ++db) acc[db] = f32x4{};
+  float run_max = -INFINITY, lsum = 0.0f;   // running reference (log2 units) and row sum
+
+  // the lane's 8 column ids (16c + 4 g4 + v) come from the list copy or the band range
+  auto compute = [=, &acc, &run_max, &lsum](int u, const Slot<D>& sl) {
+    const bool is_list = u < tA;          // uniform
+    const int f = tile_first(u);
+    const int fl = is_list ? f : 0;
+    // first and last column of the tile (kPad past the list's end; the band's last tile ends at bandHi)
+    const int l0 = __builtin_amdgcn_readfirstlane(lst[fl]);
+    const int l1 = __builtin_amdgcn_readfirstlane(lst[fl + kBN - 1]);
+    const int c0 = is_list ? l0 : f;
+    const int clast = is_list ? l1 : min(f + kBN - 1, bandHi);
+    // (bitwise, so the tests stay scalar arithmetic without branches)
+    const bool active = group_has_rows & (c0 <= (is_list ? gmax - a.window : gmax)) &
+                        (is_list | (clast > gmin - a.window));
+    const bool full = is_list ? clast <= gmin - a.window
+                              : (f + kBN - 1 <= bandHi) & (clast <= gmin) & (c0 > gmax - a.window);
+    if (!active) return;
+    // every LDS read of the tile first, unconditionally (a read under a branch can lose the information
+    // that tells it apart from the pending LDS-DMA writes)
+    int4 ca_[2];
+#pragma unroll
+    for (int c = 0; c < 2; ++c) ca_[c] = *reinterpret_cast<const int4*>(&lst[fl + 16 * c + 4 * g4]);
+    u32x4 kw[KS][2];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+        kw[ks][c] = *reinterpret_cast<const u32x4*>(&sl.k[koff[ks & 1] + 16 * c * D + 64 * (ks >> 1)]);
+    i16x4 vr[DB][2];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const int o = voff[db & 3] + 64 * (db >> 2);
+      vr[db][0] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(FL_LDS4(&sl.v[o]));
+      vr[db][1] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(FL_LDS4(&sl.v[o + 16 * D]));
+    }
+    f32x4 sa[2] = {f32x4{}, f32x4{}};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+        sa[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kw[ks][c]), qa[ks], sa[c], 0, 0, 0);
+    // scores in log2 units first (the products are canonical, so the maximum needs no quieting step)
+#pragma unroll
+    for (int c = 0; c < 2; ++c) sa[c] *= a.scale_log2;
+    if (!full) {
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        if (is_list) {                    // list columns: j + window <= i
+          const int ci[4] = {ca_[c].x, ca_[c].y, ca_[c].z, ca_[c].w};
+          const int lim_i = row_i - a.window;
+#pragma unroll
+          for (int v = 0; v < 4; ++v) sa[c][v] = ci[v] <= lim_i ? sa[c][v] : -INFINITY;
+        } else {                          // band columns f + 16c + 4 g4 + v: i - window < j <= i
+          const uint32_t w = (uint32_t)a.window;
+          const uint32_t d0 = (uint32_t)(row_i - f - 16 * c - 4 * g4);
+#pragma unroll
+          for (int v = 0; v < 4; ++v) sa[c][v] = d0 - (uint32_t)v < w ? sa[c][v] : -INFINITY;
+        }
+      }
+    }
+    const float pinf = a.pinf;
+    float tmax = fmax_nn(fmax_nn(fmax_nn(sa[0][0], sa[0][1], pinf), fmax_nn(sa[0][2], sa[0][3], pinf), pinf),
+                         fmax_nn(fmax_nn(sa[1][0], sa[1][1], pinf), fmax_nn(sa[1][2], sa[1][3], pinf), pinf), pinf);
+    {
+      auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(tmax), __float_as_uint(tmax), false, false);
+      tmax = fmax_nn(__uint_as_float(r[0]), __uint_as_float(r[1]), pinf);
+      r = __builtin_amdgcn_permlane32_swap(__float_as_uint(tmax), __float_as_uint(tmax), false, false);
+      tmax = fmax_nn(__uint_as_float(r[0]), __uint_as_float(r[1]), pinf);
+    }
+    // online softmax with a lazily raised reference (it moves only when a score exceeds it by more than 8
+    // in log2 units, so probabilities stay <= 256 and rescaling is rare)
+    const bool raise = tmax > run_max + 8.0f;            // false while both are -inf
+    if (__builtin_amdgcn_ballot_w64(raise) != 0) {        // uniform: rescale the rows that need it
+      const float nm = raise ? tmax : run_max;
+      const float alpha = raise ? __builtin_amdgcn_exp2f(run_max - nm) : 1.0f;   // exp2(-inf) = 0
+      lsum *= alpha;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) acc[db] *= alpha;
+      run_max = nm;
+    }
+    const float ref = run_max == -INFINITY ? 0.0f : run_max;
+    float pr[8];
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        pr[4 * c + v] = __builtin_amdgcn_exp2f(sa[c][v] - ref);
+        lsum += pr[4 * c + v];
+      }
+    // P as two bf16 parts, p = hi + lo with hi = bf16(p) and lo = bf16(p - hi) (p - hi is exact in fp32)
+    u32x4 ph, pl;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      ph[e] = pack_bf16x2(pr[2 * e], pr[2 * e + 1]);
+      pl[e] = pack_bf16x2(pr[2 * e] - __uint_as_float(ph[e] << 16), pr[2 * e + 1] - __uint_as_float(ph[e] & 0xFFFF0000u));
+    }
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(vr[db][0], vr[db][1], 0, 1, 2, 3, 4, 5, 6, 7));
+      acc[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, __builtin_bit_cast(bf16x8, ph), acc[db], 0, 0, 0);
+    }
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(vr[db][0], vr[db][1], 0, 1, 2, 3, 4, 5, 6, 7));
+      acc[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, __builtin_bit_cast(bf16x8, pl), acc[db], 0, 0, 0);
+    }
+  };
+
+  // ---- pipeline: step s waits for tile s (issued three steps earlier: tiles s+1 and s+2 may still be in
+  // flight, 2 NI operations), passes the barrier (every wave is done with tile s-1), LDS-DMAs tile s+3
+  // into the slot tile s-1 used and computes tile s.  Every step issues exactly NI VMEM operations.
+  __syncthreads();                        // the padding entries
+  FL_WAIT_VM(0);                          // query fragments have arrived
+  issue(s0, tile_offs(0));
+  __builtin_amdgcn_sched_barrier(0);
+  issue(s1, tile_offs(1));
+  __builtin_amdgcn_sched_barrier(0);
+  issue(s2, tile_offs(2));
+  auto step = [&](int u, Slot<D>& cur, Slot<D>& nxt) {
+    const Offs of = tile_offs(u + 3);
+    FL_WAIT_VM(2 * NI);
+    lds_barrier();
+    issue(nxt, of);
+    if (u < n_tiles) compute(u, cur);
+  };
+  const int n_steps = (n_tiles + kRing - 1) / kRing * kRing;
+  for (int u = 0; u < n_steps; u += kRing) {
+    step(u, s0, s3);
+    step(u + 1, s1, s0);
+    step(u + 2, s2, s1);
+    step(u + 3, s3, s2);
+  }
+  FL_WAIT_VM(0);
+  lds_barrier();
+
+  // ---- epilogue: lane (j16, g4) holds dims 16 db + 4 g4 .. +3 of row j16 ----------------------------
+  lsum = row4_add(lsum);
+  if (!row_ok) return;
+  const int64_t orow = ((int64_t)b * a.N + row_i) * HD + (int64_t)h * D;
+  const int64_t lrow = ((int64_t)b * a.N + row_i) * a.H + h;
+  // the subtract term and mass are the previous loop's add term and mass of this row
+  const int pp = a.slot_prev[(int64_t)b * a.N + row_i];
+  const int64_t tp = ((int64_t)b * a.k_prev + pp) * a.H + h;
+  const float msub = pp >= 0 ? a.mass_prev[tp] : 0.0f;
+  const float* subp = a.term_prev + tp * D;
+  const int64_t trow = ((int64_t)b * a.k + p) * a.H + h;
+  const bool keep = a.term_out != nullptr;
+  if (!(msub > 0.0f) || !(lsum > 0.0f)) {     // empty column set or vanished mass: unchanged
+    if (keep) {
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+        *reinterpret_cast<float4*>(a.term_out + trow * D + db * 16 + 4 * g4) = make_float4(0, 0, 0, 0);
+      if (g4 == 0) a.mass_out[trow] = 0.0f;
+    }
+    return;
+  }
+  const float fm = msub / lsum;
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+    const int dim = db * 16 + 4 * g4;
+    const float4 sub = *reinterpret_cast<const float4*>(subp + dim);
+    const float4 add = make_float4(acc[db][0] * fm, acc[db][1] * fm, acc[db][2] * fm, acc[db][3] * fm);
+    float4 prev = *reinterpret_cast<const float4*>(a.o + orow + dim);
+    prev.x = prev.x - sub.x + add.x;
+    prev.y = prev.y - sub.y + add.y;
+    prev.z = prev.z - sub.z + add.z;
+    prev.w = prev.w - sub.w + add.w;
+    *reinterpret_cast<float4*>(a.o + orow + dim) = prev;
+    if (keep) *reinterpret_cast<float4*>(a.term_out + trow * D + dim) = add;
+  }
+  if (g4 == 0) {
+    a.lse_ref[lrow] = (run_max + log2f(lsum)) * 0.6931471805599453f - logf(msub);
+    if (keep) a.mass_out[trow] = msub;
+  }
+}
+
 // Tile records of the sparse update, each an int2 (column, aux):
 //   [0, BH*c)                         list of (b, h): (column, slot of the column)
 //   [off_upd + bh*c, ...)             its entries updated this loop, compacted in order: (column, slot)
@@ -1288,6 +1623,7 @@ static int loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev, const
   a.H = H;
   a.scale_log2 = sm_scale * 1.4426950408889634f;
   a.cache_current = (!dense && reuse && k_new == nullptr) ? 1 : 0;
+  a.pinf = INFINITY;
   if (!dense && !a.cache_current) {       // (current caches: tiles come straight from cols and the band)
     const RecLayout L = rec_layout(B, N, H, k, c_list);
     int2* rec = static_cast<int2*>(ws);
@@ -1319,6 +1655,11 @@ static int loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev, const
     return check_launch("loop_attn_kernel");
   }
 #define FL_REUSE(DD, CC) reuse_attn_kernel<DD, CC><<<grid, 256, 0, st>>>(a)
+  if (a.cache_current && c_list <= kListCap) {
+    if (d == 128) cur_attn_kernel<128><<<grid, 256, 0, st>>>(a);
+    else cur_attn_kernel<64><<<grid, 256, 0, st>>>(a);
+    return check_launch("cur_attn_kernel");
+  }
   if (a.cache_current) {
     if (d == 128) FL_REUSE(128, true); else FL_REUSE(64, true);
   } else {
