@@ -115,14 +115,27 @@ __device__ __forceinline__ float xor32_add(float x) {
 // a DMA target), so the compiler's LDS-DMA tracking does not order them behind pending tile loads.
 template <int D>
 struct Slot {
-  uint16_t k[kBN * D];     // row c at c*D, 16-byte chunks permuted by swz
+  uint16_t k[kBN * D];     // row c at c*D, 16-byte chunks permuted (swz16_f, swz32_f)
   uint16_t v[kBN * D];     // same layout; converted in place from bf16 to fp16 before use
 };
 
-// 16-byte chunk ch of row c sits at chunk position ch ^ f(c), f = (0,2,4,6,1,3,5,7)[c % 8]: the K reads
-// (8 rows x 16 B per LDS cycle) and the transposed V reads (4 columns x 32 B) both hit 32 distinct banks
-__device__ __forceinline__ int swz_f(int c) { return ((c & 3) << 1) | ((c >> 2) & 1); }
-__device__ __forceinline__ int swz(int c, int ch) { return ch ^ swz_f(c); }
+// Tile rows in LDS: the 16-byte chunk ch of row c sits at chunk position ch ^ g(c) (the LDS-DMA lanes
+// fetch their global chunks in that order).  LDS reads are served 256 bytes (64 banks, 16 groups of 16
+// bytes) at a time, so g spreads the rows one read instruction touches over the 16 groups.  For the
+// 16x16x32 kernels: g is a bijection on 16 consecutive rows (the K reads: 16 rows x 16 B) whose halves
+// g(c) >> 1 are distinct on 8 consecutive rows (the transposed V reads: 8 rows x 32 B).
+template <int D>
+__device__ __forceinline__ int swz16_f(int c) {
+  if constexpr (D == 128) return ((c & 7) << 1) | ((c >> 3) & 1);
+  else return (((c >> 1) & 3) << 1) | ((c >> 3) & 1);   // 128-byte rows: two rows share a 256-byte line
+}
+// For the 32x32x16 reads of loop_attn_kernel: a bijection on 16 consecutive rows (K: 16 rows x 16 B) whose
+// quarters g(c) >> 2 are distinct on 4 consecutive rows (transposed V: 4 rows x 64 B).
+template <int D>
+__device__ __forceinline__ int swz32_f(int c) {
+  if constexpr (D == 128) return ((c & 3) << 2) | ((c >> 2) & 3);
+  else return (((c >> 1) & 1) << 2) | ((c >> 2) & 3);
+}
 
 // MODE: kDense (loop 1, every row over all causal columns) or kFull (a sparse loop with both passes).
 constexpr int kDense = 0, kFull = 1;
@@ -323,7 +336,7 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
 #pragma unroll
     for (int t = 0; t < NI; ++t) {
       const int c = inst_of(t) * COLS_PER_INST + lane / CH;
-      r.o[t] = tab[u & 7][2 * kBN + c] + (uint32_t)swz(c, lane % CH) * 16;   // kOOB + 240 is still out of range
+      r.o[t] = tab[u & 7][2 * kBN + c] + (uint32_t)((lane % CH) ^ swz32_f<D>(c)) * 16;   // kOOB + 240: still out of range
     }
     return r;
   };
@@ -396,21 +409,24 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
   };
 
   // LDS read offsets (elements) that depend on the lane; the rest of each read address is a constant.
-  // K (A operand of S^T = K Q^T): row r32, chunk 2ks + hw = 8 (ks >> 2) + (2 (ks & 3) + hw), and the
-  // swizzle only permutes the low three bits of a chunk index.  V (transposed reads for O^T += V^T P^T):
+  // K (A operand of S^T = K Q^T): row r32, data chunk 2ks + hw.  V (transposed reads for O^T += V^T P^T):
   // lane (16g + 4t + q) points at V[col][dim0 + 4q] of column 16kb + 4(g >> 1) + t (and the same + 8),
-  // dims 32db + 16(g & 1) + 4q, so the transpose read hands lane m of the group V[col_t][dim0 + m]; the
-  // swizzle of those columns is the same for every kb and for the + 8 column.
-  int koff[4], voff[2];
+  // dims 32db + 16(g & 1) + 4q (data chunk 4db + 2(g & 1) + (q >> 1)), so the transpose read hands lane m
+  // of the group V[col_t][dim0 + m]; the swizzle of those columns is the same for every kb (voff), and
+  // the + 8 columns have their own (voff8).
+  int koff[KS], voff[DB], voff8[DB];
   {
     const int g16 = lane >> 4, m16 = lane & 15;
     const int tq = m16 >> 2, q = m16 & 3;
     const int col0 = 4 * (g16 >> 1) + tq;
     const int c_lo = 2 * (g16 & 1) + (q >> 1);
 #pragma unroll
-    for (int m = 0; m < 4; ++m) koff[m] = r32 * D + ((2 * m + hw) ^ swz_f(r32)) * 8;
+    for (int ks = 0; ks < KS; ++ks) koff[ks] = r32 * D + ((2 * ks + hw) ^ swz32_f<D>(r32)) * 8;
 #pragma unroll
-    for (int e = 0; e < 2; ++e) voff[e] = col0 * D + ((4 * e + c_lo) ^ swz_f(col0)) * 8 + 4 * (q & 1);
+    for (int db = 0; db < DB; ++db) {
+      voff[db] = col0 * D + ((4 * db + c_lo) ^ swz32_f<D>(col0)) * 8 + 4 * (q & 1);
+      voff8[db] = (col0 + 8) * D + ((4 * db + c_lo) ^ swz32_f<D>(col0 + 8)) * 8 + 4 * (q & 1);
+    }
   }
 
   // first and last column id of tile u and whether it holds an updated column (uniform; read ahead of
@@ -446,7 +462,7 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
     f32x16 s = f32x16{};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      const u32x4 kw = *reinterpret_cast<const u32x4*>(&sl.k[koff[ks & 3] + 64 * (ks >> 2)]);
+      const u32x4 kw = *reinterpret_cast<const u32x4*>(&sl.k[koff[ks]]);
       s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kw), qf[ks], s, 0, 0, 0);
     }
     // masks, softmax and O^T += V^T P^T over the lane's 16 elements, fp16 operands
@@ -514,9 +530,8 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
       const f16x8 pf = __builtin_bit_cast(f16x8, pw);
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        const int o = voff[db & 1] + 64 * (db >> 1) + 16 * kb * D;
-        const i16x4 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(FL_LDS4(&sl.v[o]));
-        const i16x4 vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(FL_LDS4(&sl.v[o + 8 * D]));
+        const i16x4 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(FL_LDS4(&sl.v[voff[db] + 16 * kb * D]));
+        const i16x4 vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(FL_LDS4(&sl.v[voff8[db] + 16 * kb * D]));
         const i16x8 v8 = __builtin_shufflevector(va, vb, 0, 1, 2, 3, 4, 5, 6, 7);
         acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, v8), pf, acc[db], 0, 0, 0);
       }
@@ -874,7 +889,7 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
 #pragma unroll
     for (int t = 0; t < NI; ++t) {
       const int c = inst_of(t) * COLS_PER_INST + lane / CH;
-      r.o[t] = tab[u & 7][kBN + c] + (uint32_t)swz(c, lane % CH) * 16;   // kOOB + 240 is still out of range
+      r.o[t] = tab[u & 7][kBN + c] + (uint32_t)((lane % CH) ^ swz16_f<D>(c)) * 16;   // kOOB + 240: still out of range
     }
     return r;
   };
@@ -904,18 +919,16 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
     }
   };
   // LDS read offsets (elements) that depend on the lane.  K (A operand): row j16 (+16 for the second
-  // column block), chunk 4 ks + g4 = 8 (ks >> 1) + (4 (ks & 1) + g4).  V (transposed reads): lane
-  // (g4, t, q) points at dims 16 db + 4q of column 4 g4 + t (+16 for the second half of the k order);
-  // chunk 2 db + (q >> 1) = 8 (db >> 2) + (2 (db & 3) + (q >> 1)).  The swizzle permutes only the low
-  // three bits of a chunk index and depends on the column mod 8.
-  int koff[2], voff[4];
+  // column block), data chunk 4 ks + g4.  V (transposed reads): lane (g4, t, q) points at dims
+  // 16 db + 4q of column 4 g4 + t (+16 for the second half of the k order), data chunk 2 db + (q >> 1).
+  int koff[KS], voff[DB];
   {
     const int t4 = j16 >> 2, q = lane & 3;
     const int colv = 4 * g4 + t4;
 #pragma unroll
-    for (int e = 0; e < 2; ++e) koff[e] = j16 * D + ((4 * e + g4) ^ swz_f(j16)) * 8;
+    for (int ks = 0; ks < KS; ++ks) koff[ks] = j16 * D + ((4 * ks + g4) ^ swz16_f<D>(j16)) * 8;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) voff[e] = colv * D + ((2 * e + (q >> 1)) ^ swz_f(colv)) * 8 + 4 * (q & 1);
+    for (int db = 0; db < DB; ++db) voff[db] = colv * D + ((2 * db + (q >> 1)) ^ swz16_f<D>(colv)) * 8 + 4 * (q & 1);
   }
 
   f32x4 acc[DB];                          // add term, O^T blocks
@@ -979,11 +992,11 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
     for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
       for (int c = 0; c < 2; ++c)
-        kw[ks][c] = *reinterpret_cast<const u32x4*>(&sl.k[koff[ks & 1] + 16 * c * D + 64 * (ks >> 1)]);
+        kw[ks][c] = *reinterpret_cast<const u32x4*>(&sl.k[koff[ks] + 16 * c * D]);
     i16x4 vr[DB][2];
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
-      const int o = voff[db & 3] + 64 * (db >> 2);
+      const int o = voff[db];
       vr[db][0] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(FL_LDS4(&sl.v[o]));
       vr[db][1] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(FL_LDS4(&sl.v[o + 16 * D]));
     }
@@ -1237,7 +1250,7 @@ __global__ __launch_bounds__(256, 2) void cur_attn_kernel(AttnArgs a) {
 #pragma unroll
   for (int t = 0; t < INST_PER_WAVE; ++t) {
     lcol[t] = inst_of(t) * COLS_PER_INST + lane / CH;
-    lsw[t] = (uint32_t)swz(lcol[t], lane % CH) * 16 + head_off;
+    lsw[t] = (uint32_t)((lane % CH) ^ swz16_f<D>(lcol[t])) * 16 + head_off;
   }
   struct Offs { uint32_t o[INST_PER_WAVE]; };
   // (no branches: the list copy is read at a valid index for band tiles too, and the choice is a select)
@@ -1268,15 +1281,17 @@ __global__ __launch_bounds__(256, 2) void cur_attn_kernel(AttnArgs a) {
         __builtin_amdgcn_raw_ptr_buffer_load_lds(vcR, FL_LDS(sl.v + inst * 512), 16, off, 0, 0, kDmaPolicy);
     }
   };
-  // LDS read offsets of the fragments, as in reuse_attn_kernel
-  int koff[2], voff[4];
+  // LDS read offsets (elements) of the fragments.  K (A operand): row j16 (+16 for the second column
+  // block), data chunk 4 ks + g4.  V (transposed reads): lane (g4, t, q) reads dims 16 db + 4q of column
+  // 4 g4 + t (+16 for the second half of the k order), data chunk 2 db + (q >> 1).
+  int koff[KS], voff[DB];
   {
     const int t4 = j16 >> 2, q = lane & 3;
     const int colv = 4 * g4 + t4;
 #pragma unroll
-    for (int e = 0; e < 2; ++e) koff[e] = j16 * D + ((4 * e + g4) ^ swz_f(j16)) * 8;
+    for (int ks = 0; ks < KS; ++ks) koff[ks] = j16 * D + ((4 * ks + g4) ^ swz16_f<D>(j16)) * 8;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) voff[e] = colv * D + ((2 * e + (q >> 1)) ^ swz_f(colv)) * 8 + 4 * (q & 1);
+    for (int db = 0; db < DB; ++db) voff[db] = colv * D + ((2 * db + (q >> 1)) ^ swz16_f<D>(colv)) * 8 + 4 * (q & 1);
   }
 
   f32x4 acc[DB];                          // add term, O^T blocks
@@ -1310,11 +1325,11 @@ __global__ __launch_bounds__(256, 2) void cur_attn_kernel(AttnArgs a) {
     for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
       for (int c = 0; c < 2; ++c)
-        kw[ks][c] = *reinterpret_cast<const u32x4*>(&sl.k[koff[ks & 1] + 16 * c * D + 64 * (ks >> 1)]);
+        kw[ks][c] = *reinterpret_cast<const u32x4*>(&sl.k[koff[ks] + 16 * c * D]);
     i16x4 vr[DB][2];
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
-      const int o = voff[db & 3] + 64 * (db >> 2);
+      const int o = voff[db];
       vr[db][0] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(FL_LDS4(&sl.v[o]));
       vr[db][1] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(FL_LDS4(&sl.v[o + 16 * D]));
     }
