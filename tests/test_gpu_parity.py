@@ -308,7 +308,12 @@ def test_sparse_attn_stepwise_from_oracle_state(F, name, over):
 
 @pytest.mark.parametrize("name,over", [("C4", dict(seq=2000, heads=2, window=128, col_budget=4 + 128 + 300)),
                                        ("C5", dict(seq=1200, heads=2, batch=2, col_budget=200)),
-                                       ("C2", dict(seq=900, heads=2, head_dim=64, col_budget=100))])
+                                       ("C2", dict(seq=900, heads=2, head_dim=64, col_budget=100)),
+                                       # lists at the LDS copy's capacity (3072 entries) and beyond it (the
+                                       # record-table kernel), with and without a band
+                                       ("C5", dict(seq=4000, heads=2, col_budget=3072)),
+                                       ("C5", dict(seq=4500, heads=2, col_budget=3300)),
+                                       ("C4", dict(seq=5000, heads=2, window=256, col_budget=4 + 256 + 3200))])
 def test_reused_subtract_terms_match_recomputed_ones(F, name, over):
     """Loops >= 3 with the previous loop's add terms as subtract terms against the same loops with the
     subtract pass recomputed: equal up to fp32 rounding (Eq. 7 with fixed S and nested rows)."""
