@@ -12,7 +12,8 @@
  *                             with a mass-corrected correction over predicted key columns
  *                             (Sections 3.2, 4.2, Eq. 3; Appendix D.2, Eq. 7).
  * plus two set-up helpers for a dense source loop (Appendix D.2, Eq. 6 with all causal keys):
- *   fl_column_scores, fl_select_columns.
+ *   fl_column_scores, fl_select_columns; the decode step (fl_decode_step) and the list pruning for a
+ *   shrinking budget (fl_prune_columns).
  *
  * Conventions shared by every call
  *   - Every data pointer is a DEVICE pointer (HIP device memory).  The caller allocates and owns all
@@ -306,6 +307,31 @@ int fl_decode_step(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v
                    int d, float sm_scale, float* o, float* lse, int n_sink, int window, int c_next,
                    int32_t* cols_next, float* mass_next, float* sub_next, void* ws, size_t ws_bytes,
                    void* stream);
+
+/* ------------------------------------------------------------------------------------------------
+ * (7) Pruning the column list for a smaller budget -- Section 4.2 (later loops with smaller budgets
+ * prune the selected set by the preceding sparse loop's attention statistics) and Appendix D.2, Eq. 6
+ * with a sparse source.  After loop r has updated the rows A, for each (b, h) and each list entry
+ * j = cols[b, h, e], e >= ns (ns = min(n_sink, c_list)):
+ *     col_key[b, h, e - ns] = fp32( sum_{i in A, i >= j} exp(sm_scale * q_i . k_j - lse_ref_i) )   (fp64)
+ * the probability mass loop r gives column j, summed over the updated rows that attend to it, each row's
+ * probabilities recovered from its reference log-normaliser (the cached mass is folded into lse_ref).
+ * cols_next keeps the ns sinks and the t_next entries with the largest keys (ties to the lower column),
+ * ascending: a subset of cols.  The band is not pruned.  A following two-pass loop over cols_next
+ * subtracts the kept probabilities with the same lse_ref, so their mass m' needs no separate output.
+ *   q, k_cache : bf16 [B, N, H, d] loop r's queries and K_hat (rows A and the list columns are read).
+ *   rows, k    : int32 [B, k] ascending updated rows of loop r (NULL allowed when k = 0).
+ *   cols       : int32 [B, H, c_list] ascending, 1 <= c_list <= N, whose first ns entries are the sinks
+ *                0 .. ns-1 (as fl_select_columns and this call emit them).
+ *   lse_ref    : fp32 [B, N, H] after loop r (read at the rows A).
+ *   col_key    : fp32 [B, H, c_list - ns] out (may be NULL when c_list == ns);  c_list - ns <= 65536.
+ *   cols_next  : int32 [B, H, ns + t_next] out, 0 <= t_next <= c_list - ns.
+ * Two launches: the fp64 statistic (a thread pair per entry against staged query rows) and the top-k.
+ * ---------------------------------------------------------------------------------------------- */
+int fl_prune_columns(const uint16_t* q, const uint16_t* k_cache, const int32_t* rows, int k,
+                     const int32_t* cols, int c_list, const float* lse_ref, int B, int N, int H, int d,
+                     double sm_scale, int n_sink, int t_next, float* col_key, int32_t* cols_next,
+                     void* stream);
 
 #ifdef __cplusplus
 }

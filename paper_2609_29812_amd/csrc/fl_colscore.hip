@@ -100,6 +100,81 @@ __global__ __launch_bounds__(kCsThreads) void colscore_kernel(const uint16_t* __
   }
 }
 
+
+// Statistic of the list entries for pruning a shrinking list (Section 4.2; Appendix D.2, Eq. 6 with a
+// sparse source): entry j of the (b, h) list gets sum_{i updated, i >= j} exp(sigma q_i . k_j - lse_ref_i),
+// the loop-r probability mass it receives from the updated rows, each row's probabilities recovered from
+// its reference log-normaliser.  A thread pair owns one entry (the K row in registers, half the dims
+// each); the updated rows' queries and lse_ref are staged 32 at a time in ascending order, from the first
+// row that can see the workgroup's first entry.  fp64 throughout, fixed summation order.
+template <int D>
+__global__ __launch_bounds__(kCsThreads) void prune_mass_kernel(const uint16_t* __restrict__ q,
+                                                                const uint16_t* __restrict__ kc,
+                                                                const int32_t* __restrict__ rows, int k,
+                                                                const int32_t* __restrict__ cols, int c_list,
+                                                                int ns, const float* __restrict__ lse_ref,
+                                                                int N, int H, double sigma,
+                                                                float* __restrict__ key) {
+  __shared__ double tile[kCsTile][D];
+  __shared__ double tile_lse[kCsTile];
+  __shared__ int tile_row[kCsTile];
+  __shared__ int s_first;
+  constexpr int HALF = D / 2;
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int n_ent = c_list - ns;
+  const int e = blockIdx.x * kCsOwn + (threadIdx.x >> 1);
+  const int half = threadIdx.x & 1;
+  const bool ok = e < n_ent;
+  const int64_t stride = (int64_t)H * D;
+  const int32_t* cl = cols + ((int64_t)b * H + h) * c_list + ns;
+  const int32_t* rp = rows + (int64_t)b * k;
+  const int j = ok ? cl[e] : INT_MAX;
+
+  double v[HALF];
+  {
+    const uint16_t* src = kc + ((int64_t)b * N + (ok ? j : 0)) * stride + (int64_t)h * D + half * HALF;
+#pragma unroll
+    for (int t = 0; t < HALF; ++t) v[t] = ok ? (double)bf16_to_f32(src[t]) : 0.0;
+  }
+  if (threadIdx.x == 0) {                 // rows and entries ascend: skip the rows before the first entry
+    const int j0 = cl[blockIdx.x * kCsOwn];
+    int lo = 0, hi = k;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (rp[mid] < j0) lo = mid + 1; else hi = mid;
+    }
+    s_first = lo;
+  }
+  __syncthreads();
+  const int first = s_first;
+  double acc = 0.0;
+  for (int t0 = first; t0 < k; t0 += kCsTile) {
+    for (int x = threadIdx.x; x < kCsTile * D; x += kCsThreads) {
+      const int r = x / D, dd = x % D;
+      const int p = t0 + r;
+      tile[r][dd] = p < k ? (double)bf16_to_f32(q[((int64_t)b * N + rp[p]) * stride + (int64_t)h * D + dd]) : 0.0;
+    }
+    if (threadIdx.x < kCsTile) {
+      const int p = t0 + (int)threadIdx.x;
+      const int i = p < k ? rp[p] : -1;
+      tile_row[threadIdx.x] = i;
+      tile_lse[threadIdx.x] = p < k ? (double)lse_ref[((int64_t)b * N + i) * H + h] : 0.0;
+    }
+    __syncthreads();
+    for (int ii = 0; ii < kCsTile; ++ii) {
+      double dot = 0.0;
+#pragma unroll
+      for (int t = 0; t < HALF; ++t) dot = fma(v[t], tile[ii][half * HALF + t], dot);
+      const double other = __shfl_xor(dot, 1, 64);
+      const double full = half ? other + dot : dot + other;   // lower half first
+      const int i = tile_row[ii];                              // -1 past the last row: never >= j
+      if (ok && i >= j) acc += exp(sigma * full - tile_lse[ii]);
+    }
+    __syncthreads();
+  }
+  if (ok && half == 0) key[((int64_t)b * H + h) * n_ent + e] = (float)acc;
+}
+
 }  // namespace fl
 
 using namespace fl;
@@ -134,5 +209,47 @@ extern "C" int fl_column_scores(const uint16_t* q, const uint16_t* k_cache, int 
     colscore_kernel<64, true><<<grid, kCsThreads, 0, st>>>(q, k_cache, N, H, sigma, lse, col_key);
   }
   return check_launch("colscore_kernel(columns)");
+  FL_API_END
+}
+
+extern "C" int fl_prune_columns(const uint16_t* q, const uint16_t* k_cache, const int32_t* rows, int k,
+                                const int32_t* cols, int c_list, const float* lse_ref, int B, int N, int H,
+                                int d, double sm_scale, int n_sink, int t_next, float* col_key,
+                                int32_t* cols_next, void* stream) {
+  FL_API_BEGIN
+  FL_REQUIRE(q && k_cache && cols && lse_ref && cols_next, FL_E_NULL,
+             "fl_prune_columns: q, k_cache, cols, lse_ref and cols_next are required");
+  FL_REQUIRE(B >= 1 && N >= 1 && H >= 1, FL_E_SHAPE, "fl_prune_columns: need B, N, H >= 1");
+  FL_REQUIRE(d == 64 || d == 128, FL_E_SHAPE, "fl_prune_columns: head dim %d not in {64, 128}", d);
+  FL_REQUIRE((int64_t)N * H * d < ((int64_t)1 << 31), FL_E_SHAPE, "fl_prune_columns: N * H * d too large");
+  FL_REQUIRE(k >= 0 && k <= N, FL_E_RANGE, "fl_prune_columns: k=%d outside [0, N]", k);
+  FL_REQUIRE(k == 0 || rows, FL_E_NULL, "fl_prune_columns: rows are required when k > 0");
+  FL_REQUIRE(c_list >= 1 && c_list <= N, FL_E_RANGE, "fl_prune_columns: c_list=%d outside [1, N]", c_list);
+  FL_REQUIRE(n_sink >= 0, FL_E_RANGE, "fl_prune_columns: n_sink must be >= 0");
+  const int ns = std::min(n_sink, c_list);
+  const int n_ent = c_list - ns;
+  FL_REQUIRE(t_next >= 0 && t_next <= n_ent, FL_E_RANGE, "fl_prune_columns: t_next=%d outside [0, %d]", t_next,
+             n_ent);
+  FL_REQUIRE(n_ent <= 65536, FL_E_SHAPE, "fl_prune_columns: %d list entries after the sinks exceed 65536", n_ent);
+  FL_REQUIRE(n_ent == 0 || col_key, FL_E_NULL, "fl_prune_columns: col_key is required when entries follow the sinks");
+  FL_REQUIRE(sm_scale > 0.0 && std::isfinite(sm_scale), FL_E_RANGE, "fl_prune_columns: sm_scale must be > 0");
+  hipStream_t st = as_stream(stream);
+  if (n_ent == 0) {                       // the list is all sinks: it is kept as it is
+    if (hipMemcpyAsync(cols_next, cols, (size_t)B * H * ns * sizeof(int32_t), hipMemcpyDeviceToDevice, st) !=
+        hipSuccess)
+      return set_error(FL_E_HIP, "fl_prune_columns: copy of the sinks failed");
+    return FL_OK;
+  }
+  dim3 grid((n_ent + kCsOwn - 1) / kCsOwn, H, B);
+  if (d == 128)
+    prune_mass_kernel<128><<<grid, kCsThreads, 0, st>>>(q, k_cache, rows, k, cols, c_list, ns, lse_ref, N, H,
+                                                        sm_scale, col_key);
+  else
+    prune_mass_kernel<64><<<grid, kCsThreads, 0, st>>>(q, k_cache, rows, k, cols, c_list, ns, lse_ref, N, H,
+                                                       sm_scale, col_key);
+  int rc = check_launch("prune_mass_kernel");
+  if (rc != FL_OK) return rc;
+  return launch_topk(B * H, col_key, n_ent, n_ent, t_next, cols + ns, c_list, 0, cols_next, ns + t_next, ns,
+                     nullptr, 0, st);
   FL_API_END
 }

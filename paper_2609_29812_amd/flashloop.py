@@ -56,6 +56,8 @@ _SIGNATURES = {
     "fl_decode_step_ws": (_c_sz, [_c_i, _c_i, _c_i, _c_i, _c_i, _c_i]),
     "fl_decode_step": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_i, _c_p, _c_p, _c_i, _c_i, _c_i, _c_i, _c_f, _c_p, _c_p,
                               _c_i, _c_i, _c_i, _c_p, _c_p, _c_p, _c_p, _c_sz, _c_p]),
+    "fl_prune_columns": (_c_i, [_c_p, _c_p, _c_p, _c_i, _c_p, _c_i, _c_p, _c_i, _c_i, _c_i, _c_i, _c_d, _c_i, _c_i,
+                                _c_p, _c_p, _c_p]),
 }
 
 EXPORTS = tuple(_SIGNATURES)
@@ -389,3 +391,29 @@ def decode_step(q, k_cache, v_cache, cols, mass, sub, o, c_next, n_sink=0, windo
                             _p(ws), need, _stream())
     _check(rc, "fl_decode_step")
     return cols_next, mass_next, sub_next
+
+
+# ---- (7) list pruning for a smaller budget --------------------------------------------------------------
+def prune_columns(q, k_cache, rows, cols, lse_ref, n_sink, t_next, sm_scale=None):
+    """Keep the sinks and the t_next list entries that loop r's updated rows gave the most probability mass.
+    q, k_cache bf16 [B, N, H, d] (loop r); rows int32 [B, k] (or None when k = 0); cols int32 [B, H, c_list];
+    lse_ref fp32 [B, N, H].  Returns (cols_next int32 [B, H, ns + t_next], col_key fp32 [B, H, c_list - ns])."""
+    B, N, H, d = k_cache.shape
+    _dev(q, torch.bfloat16, "q", k_cache.shape)
+    _dev(k_cache, torch.bfloat16, "k_cache")
+    c_list = cols.shape[2]
+    _dev(cols, torch.int32, "cols", (B, H, c_list))
+    _dev(lse_ref, torch.float32, "lse_ref", (B, N, H))
+    k = 0 if rows is None else rows.shape[1]
+    if rows is not None:
+        _dev(rows, torch.int32, "rows", (B, k))
+    ns = min(n_sink, c_list)
+    dev = q.device
+    col_key = torch.empty(B, H, c_list - ns, dtype=torch.float32, device=dev)
+    cols_next = torch.empty(B, H, ns + t_next, dtype=torch.int32, device=dev)
+    sm_scale = 1.0 / math.sqrt(d) if sm_scale is None else sm_scale
+    rc = load().fl_prune_columns(_p(q), _p(k_cache), _p(rows), k, _p(cols), c_list, _p(lse_ref), B, N, H, d,
+                                 sm_scale, n_sink, t_next, _p(col_key) if c_list > ns else None, _p(cols_next),
+                                 _stream())
+    _check(rc, "fl_prune_columns")
+    return cols_next, col_key
