@@ -18,6 +18,7 @@ import numpy as np
 
 from . import attention as att
 from . import codec
+from . import prune
 from . import select
 from .numerics import bf16_to_f64
 
@@ -35,6 +36,7 @@ class LoopRecord:
     o: dict                   # (b, h) -> float64 [N, d] after loop r (valid rows: see `valid`)
     lse: dict                 # (b, h) -> float64 [N]
     mass: dict                # (b, h) -> float64 [N] (nan where not updated)
+    cols_next: dict = None    # (b, h) -> int32 list pruned after this loop for a smaller budget, if any
 
 
 @dataclass
@@ -123,7 +125,8 @@ def sparse_loop(states, r, cand, k_hat, v_hat, cols, o, lse, heads, rows=None):
 
 def run_layer(states, heads=None, rows=None, cols=None):
     """Loop 1 then sparse loops 2..R.  cols: optional dict (b, h) -> column list to use instead of the
-    loop-1 selection (e.g. to evaluate the update alone with all columns)."""
+    loop-1 selection (e.g. to evaluate the update alone with all columns).  With a decaying column budget
+    (workload.col_decay) the lists are pruned between loops (recorded as LoopRecord.cols_next)."""
     w = states.workload
     rec = loop1(states, heads)
     if cols is not None:
@@ -132,9 +135,22 @@ def run_layer(states, heads=None, rows=None, cols=None):
     lse = {key: val.copy() for key, val in rec.lse1.items()}
     k_hat, v_hat = rec.k_hat1, rec.v_hat1
     cand = None
+    cols_r = dict(rec.cols)
     for r in range(2, w.loops + 1):
-        lr, k_hat, v_hat = sparse_loop(states, r, cand, k_hat, v_hat, rec.cols, o, lse, rec.heads, rows)
+        lr, k_hat, v_hat = sparse_loop(states, r, cand, k_hat, v_hat, cols_r, o, lse, rec.heads, rows)
         rec.loops.append(lr)
         cand = lr.idx
+        if r < w.loops and w.top_cols_at(r + 1) < w.top_cols_at(r):
+            # a smaller budget next loop: prune each list by this loop's statistic (Section 4.2), with the
+            # reference log-normalisers as the state stores them (fp32)
+            assert rows is None, "pruning needs every updated row's log-normaliser"
+            lr.cols_next = {}
+            for b in range(w.batch):
+                for h in rec.heads:
+                    lse32 = lse[b, h].astype(np.float32).astype(np.float64)
+                    stat = prune.column_mass(cols_r[b, h], lr.idx[b], _f64(states.q[r - 1], b, h),
+                                             _f64(k_hat, b, h), lse32, w.sm_scale, w.n_sink)
+                    lr.cols_next[b, h] = prune.prune_columns(cols_r[b, h], stat, w.n_sink, w.top_cols_at(r + 1))
+            cols_r.update(lr.cols_next)
     rec.k_hat, rec.v_hat = k_hat, v_hat
     return rec

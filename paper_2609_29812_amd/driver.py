@@ -10,6 +10,9 @@ sparse_step() one sparse loop r >= 2: select the active rows among the previous 
               terms (equal in exact arithmetic: the column sets are fixed and the active rows nested).
               Such a loop needs only the new state, so the quantizers commit the new rows straight into
               the caches and the attention reads every column from them.
+prune_list()  a smaller column budget for the next loop (Section 4.2): keep the sinks and the entries the
+              last loop's updated rows gave the most probability mass.  The next loop then runs both passes
+              (its subtract pass recomputes the kept columns' share with the same lse_ref).
 """
 from __future__ import annotations
 
@@ -82,3 +85,9 @@ def sparse_step(st: LayerState, qr, qp, kr, kp, vr, vp, k_r, bits, keep=False):
         return dict(idx=idx, slot=slot, key=key, codes_k=ck, scale_k=sk, zero_k=zk, codes_v=cv,
                     scale_v=sv, zero_v=zv, k_new=k_new, v_new=v_new)
     return None
+
+
+def prune_list(st: LayerState, qr, t_next, n_sink):
+    """Shrink the column lists to the sinks plus t_next entries after the loop whose queries are qr."""
+    st.cols, _ = fl.prune_columns(qr, st.k_hat, st.cand, st.cols, st.lse, n_sink, t_next)
+    st.term = st.mass = None   # the stored add terms cover the old lists: the next loop recomputes

@@ -220,6 +220,11 @@ CHAIN_CASES = [
     ("C4", dict(seq=2000, heads=2, window=128, col_budget=4 + 128 + 300)),
     ("C5", dict(seq=1200, heads=2, batch=2, col_budget=200)),
     ("C3", dict(seq=1500, heads=2, col_budget=160)),
+    # a decaying column budget: lists pruned after loops 3 and 4, loops 4 and 5 recompute their subtract pass
+    ("C4", dict(seq=2000, heads=2, window=128, col_budget=4 + 128 + 300, loops=5, hot_frac=(0.1, 0.08, 0.06, 0.05),
+                topk_frac=(0.1, 0.08, 0.06, 0.05), bits=(4, 2, 2, 2),
+                col_decay=(4 + 128 + 300, 4 + 128 + 300, 4 + 128 + 150, 4 + 128 + 60))),
+    ("C5", dict(seq=1200, heads=2, batch=2, col_budget=200, col_decay=(200, 200, 160, 120, 80, 60, 40))),
 ]
 
 
@@ -272,6 +277,11 @@ def test_chain_matches_oracle(F, name, over):
         assert np.array_equal(new_rows(out, "v_new", gs.v_hat), lr.v_new), f"loop {r} new V rows"
         assert_close(down(gs.o), _dict_to_array(lr.o, B, H), f"loop {r} o (chained)")
         assert_close(down(gs.lse), _dict_to_array(lr.lse, B, H), f"loop {r} lse (chained)")
+        if lr.cols_next is not None:
+            driver.prune_list(gs, dev["q"][r - 1], w.top_cols_at(r + 1), w.n_sink)
+            want = np.stack([np.stack([lr.cols_next[b, h] for h in range(H)]) for b in range(B)])
+            assert np.array_equal(down(gs.cols), want), f"lists pruned after loop {r} differ"
+            say(f" pruned after loop {r} to {want.shape[2]} entries")
     assert np.array_equal(down_bits16(gs.k_hat), rec.k_hat), "final K cache differs"
     assert np.array_equal(down_bits16(gs.v_hat), rec.v_hat), "final V cache differs"
 

@@ -1,5 +1,6 @@
 """The seeded input generator: determinism, nesting of hot sets, and the derived budgets."""
 import numpy as np
+import pytest
 
 from workloads import CONFIGS, get, make_layer
 
@@ -35,3 +36,14 @@ def test_budgets_of_the_five_workloads():
     assert [get("C5").bits_at(r) for r in range(2, 9)] == [4, 4, 2, 2, 2, 2, 2]
     for w in CONFIGS.values():
         assert w.head_dim in (64, 128)
+
+
+def test_decaying_column_budget_is_nested_and_validated():
+    w = get("C4").replace(seq=2000, window=128, col_budget=4 + 128 + 300,
+                          col_decay=(4 + 128 + 300, 4 + 128 + 400, 4 + 128 + 100))
+    assert [w.top_cols_at(r) for r in (2, 3, 4)] == [300, 300, 100]     # a larger budget cannot regrow the list
+    assert get("C4").top_cols_at(4) == get("C4").top_cols                  # no schedule: constant
+    with pytest.raises(ValueError):
+        get("C4").replace(col_decay=(2048, 1024))                         # R - 1 = 3 entries needed
+    with pytest.raises(ValueError):
+        get("C4").replace(col_decay=(1024, 1024, 512))                    # must start at col_budget

@@ -31,6 +31,8 @@ class Workload:
     group: int           # quantization group size G
     seed: int
     delta: str = "normal"     # "normal" (std hot_scale) or "student_t" (df, scale hot_scale)
+    col_decay: tuple = ()     # optional per sparse loop r = 2..R: column budget c_r (c_2 = col_budget); a
+                              # smaller budget prunes the list after the loop before (Section 4.2)
     hot_scale: float = 0.5
     cold_std: float = 0.01
     df: float = 3.0
@@ -39,6 +41,8 @@ class Workload:
         nl = self.loops - 1
         if not (len(self.hot_frac) == len(self.topk_frac) == len(self.bits) == nl):
             raise ValueError(f"{self.name}: per-loop tuples must have R-1 = {nl} entries")
+        if self.col_decay and (len(self.col_decay) != nl or self.col_decay[0] != self.col_budget):
+            raise ValueError(f"{self.name}: col_decay needs R-1 = {nl} budgets starting at col_budget")
 
     # ---- derived sizes -------------------------------------------------------------------------
     def n_hot(self, r: int) -> int:
@@ -62,6 +66,15 @@ class Workload:
     def top_cols(self) -> int:
         """t: ranked columns beyond the sinks and the band, clamped to the available columns."""
         return max(0, min(self.col_budget - self.n_sink - self.window, self.seq - self.n_sink))
+
+    def top_cols_at(self, r: int) -> int:
+        """t_r of sparse loop r (2..R): ranked list entries under that loop's budget, never more than the
+        loop before (pruned lists are nested)."""
+        t = self.top_cols
+        for rr in range(3, r + 1):
+            if self.col_decay:
+                t = min(t, max(0, min(self.col_decay[rr - 2] - self.n_sink - self.window, self.seq - self.n_sink)))
+        return t
 
     @property
     def n_sink_eff(self) -> int:
