@@ -36,6 +36,7 @@ if ROOT not in sys.path:
 METRIC = "updated-token attn rows/s per layer-loop + achieved HBM GB/s & MFMA % at 32K"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 MFMA_BF16_TFLOPS = 2500.0      # dense bf16/fp16 MFMA
+FP64_VECTOR_TFLOPS = 78.6      # fp64 vector FMA (the pruning statistic)
 PROFILE_DIR = os.path.join(ROOT, "profiles")
 ATTN_SRC = os.path.join(ROOT, "paper_2609_29812_amd", "csrc", "fl_attn.hip")
 
@@ -267,11 +268,12 @@ def main():
     ap.add_argument("--workload", default="C4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-prune", action="store_true")
     ap.add_argument("--decode-only", action="store_true", help="only the decode measurement (for traces)")
     ap.add_argument("--copy-calib", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for {args.gpus}); "
+        print(f"bench.py runs on one GPU only; there is no multi-GPU path (asked for {args.gpus}): "
               "the step would shard by head with one small all-gather of row-score partials.", flush=True)
         sys.exit(2)
     import torch
@@ -414,6 +416,8 @@ def main():
     }
     if not args.no_decode:
         result["decode"] = decode_bench(w, gs, fl, torch)
+    if not args.no_prune:
+        result["prune"] = prune_bench(w, gs, dev["q"][w.loops - 1], fl, torch)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, st, blas_threads())
     print(json.dumps(result), flush=True)
@@ -467,6 +471,49 @@ def decode_bench(w, gs, fl, torch):
             "dense_alg_MB": round(nb_dense / 1e6, 2), "sparse_alg_MB": round(nb_sparse / 1e6, 2),
             "dense_GBps": round(nb_dense / us_dense / 1e3, 1), "sparse_GBps": round(nb_sparse / us_sparse / 1e3, 1),
             "timing": f"HIP events, mean of {reps} calls (five launches each)"}
+
+
+def prune_work(rows, cols, n_sink, H, d):
+    """Algorithmic work of one fl_prune_columns call: bytes = the list entries' K rows, the updated rows'
+    queries and lse_ref, the keys written, the lists read and written; fp64 flops = 2 d per (updated row i,
+    list entry j >= sinks) pair with i >= j (one dot product each; the exponentials are not counted)."""
+    B, k = rows.shape
+    c_list = cols.shape[2]
+    ns = min(n_sink, c_list)
+    nb = B * H * (c_list - ns) * (d * 2 + 4) + B * k * H * (d * 2 + 4) + B * H * c_list * 4 * 2
+    pairs = 0
+    for b in range(B):
+        rb = np.sort(rows[b])
+        for h in range(H):
+            js = cols[b, h, ns:]
+            pairs += int(np.sum(len(rb) - np.searchsorted(rb, js, side="left")))
+    return nb, 2.0 * d * pairs
+
+
+def prune_bench(w, gs, q_last, fl, torch):
+    """The list pruning after the last sparse loop of the step, to half the ranked entries (one step of a
+    decaying budget), timed with HIP events (not part of the step: the workload's budget is constant)."""
+    t_next = w.top_cols // 2
+    reps = 10
+    for _ in range(2):
+        fl.prune_columns(q_last, gs.k_hat, gs.cand, gs.cols, gs.lse, w.n_sink, t_next)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        fl.prune_columns(q_last, gs.k_hat, gs.cand, gs.cols, gs.lse, w.n_sink, t_next)
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) / reps * 1e3
+    B, N, H, d = gs.k_hat.shape
+    nb, nf = prune_work(gs.cand.cpu().numpy(), gs.cols.cpu().numpy(), w.n_sink, H, d)
+    achieved = nf / (us * 1e-6) / 1e12
+    log(f"[bench] prune: {us:.1f} us, {achieved:.2f} fp64 TFLOP/s")
+    return {"workload": f"{w.name} list {gs.cols.shape[2]} -> {min(w.n_sink, gs.cols.shape[2]) + t_next} entries "
+                        f"over {gs.cand.shape[1]} updated rows", "us": round(us, 2),
+            "bound": "alu", "achieved": round(achieved, 2), "peak": FP64_VECTOR_TFLOPS, "unit": "TFLOP/s (fp64)",
+            "frac": round(achieved / FP64_VECTOR_TFLOPS, 4), "alg_MB": round(nb / 1e6, 2),
+            "alg_GF": round(nf / 1e9, 3), "timing": f"HIP events, mean of {reps} calls (two launches each)"}
 
 
 if __name__ == "__main__":

@@ -326,12 +326,17 @@ int fl_decode_step(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v
  *   lse_ref    : fp32 [B, N, H] after loop r (read at the rows A).
  *   col_key    : fp32 [B, H, c_list - ns] out (may be NULL when c_list == ns);  c_list - ns <= 65536.
  *   cols_next  : int32 [B, H, ns + t_next] out, 0 <= t_next <= c_list - ns.
- * Two launches: the fp64 statistic (a thread pair per entry against staged query rows) and the top-k.
+ *   ws         : at least fl_prune_columns_ws(B, H, k, c_list, n_sink) bytes (fp64 partial sums of
+ *                256-row chunks; H * ceil(k / 256) <= 65535).
+ * Three launches: the fp64 statistic per chunk of updated rows (a thread pair per entry against staged
+ * query rows), the ordered sum of the chunks, and the top-k.
  * ---------------------------------------------------------------------------------------------- */
+size_t fl_prune_columns_ws(int B, int H, int k, int c_list, int n_sink);
+
 int fl_prune_columns(const uint16_t* q, const uint16_t* k_cache, const int32_t* rows, int k,
                      const int32_t* cols, int c_list, const float* lse_ref, int B, int N, int H, int d,
                      double sm_scale, int n_sink, int t_next, float* col_key, int32_t* cols_next,
-                     void* stream);
+                     void* ws, size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -105,22 +105,26 @@ __global__ __launch_bounds__(kCsThreads) void colscore_kernel(const uint16_t* __
 // sparse source): entry j of the (b, h) list gets sum_{i updated, i >= j} exp(sigma q_i . k_j - lse_ref_i),
 // the loop-r probability mass it receives from the updated rows, each row's probabilities recovered from
 // its reference log-normaliser.  A thread pair owns one entry (the K row in registers, half the dims
-// each); the updated rows' queries and lse_ref are staged 32 at a time in ascending order, from the first
-// row that can see the workgroup's first entry.  fp64 throughout, fixed summation order.
+// each); a workgroup takes 128 entries and one chunk of kPruneChunk updated rows, staged 32 at a time in
+// ascending order from the first row that can see its first entry, and writes its fp64 partial sums;
+// the partials of the chunks are added in chunk order afterwards.  The two threads of a pair take the
+// exponentials of alternate rows.  fp64 throughout, fixed summation order.
+constexpr int kPruneChunk = 256;
+
 template <int D>
 __global__ __launch_bounds__(kCsThreads) void prune_mass_kernel(const uint16_t* __restrict__ q,
                                                                 const uint16_t* __restrict__ kc,
                                                                 const int32_t* __restrict__ rows, int k,
                                                                 const int32_t* __restrict__ cols, int c_list,
                                                                 int ns, const float* __restrict__ lse_ref,
-                                                                int N, int H, double sigma,
-                                                                float* __restrict__ key) {
+                                                                int N, int H, double sigma, int n_chunks,
+                                                                double* __restrict__ part) {
   __shared__ double tile[kCsTile][D];
   __shared__ double tile_lse[kCsTile];
   __shared__ int tile_row[kCsTile];
   __shared__ int s_first;
   constexpr int HALF = D / 2;
-  const int h = blockIdx.y, b = blockIdx.z;
+  const int h = blockIdx.y % H, chunk = blockIdx.y / H, b = blockIdx.z;
   const int n_ent = c_list - ns;
   const int e = blockIdx.x * kCsOwn + (threadIdx.x >> 1);
   const int half = threadIdx.x & 1;
@@ -129,6 +133,7 @@ __global__ __launch_bounds__(kCsThreads) void prune_mass_kernel(const uint16_t* 
   const int32_t* cl = cols + ((int64_t)b * H + h) * c_list + ns;
   const int32_t* rp = rows + (int64_t)b * k;
   const int j = ok ? cl[e] : INT_MAX;
+  const int p_end = min(k, (chunk + 1) * kPruneChunk);
 
   double v[HALF];
   {
@@ -138,7 +143,7 @@ __global__ __launch_bounds__(kCsThreads) void prune_mass_kernel(const uint16_t* 
   }
   if (threadIdx.x == 0) {                 // rows and entries ascend: skip the rows before the first entry
     const int j0 = cl[blockIdx.x * kCsOwn];
-    int lo = 0, hi = k;
+    int lo = chunk * kPruneChunk, hi = p_end;
     while (lo < hi) {
       const int mid = (lo + hi) >> 1;
       if (rp[mid] < j0) lo = mid + 1; else hi = mid;
@@ -148,17 +153,17 @@ __global__ __launch_bounds__(kCsThreads) void prune_mass_kernel(const uint16_t* 
   __syncthreads();
   const int first = s_first;
   double acc = 0.0;
-  for (int t0 = first; t0 < k; t0 += kCsTile) {
+  for (int t0 = first; t0 < p_end; t0 += kCsTile) {
     for (int x = threadIdx.x; x < kCsTile * D; x += kCsThreads) {
       const int r = x / D, dd = x % D;
       const int p = t0 + r;
-      tile[r][dd] = p < k ? (double)bf16_to_f32(q[((int64_t)b * N + rp[p]) * stride + (int64_t)h * D + dd]) : 0.0;
+      tile[r][dd] = p < p_end ? (double)bf16_to_f32(q[((int64_t)b * N + rp[p]) * stride + (int64_t)h * D + dd]) : 0.0;
     }
     if (threadIdx.x < kCsTile) {
       const int p = t0 + (int)threadIdx.x;
-      const int i = p < k ? rp[p] : -1;
+      const int i = p < p_end ? rp[p] : -1;
       tile_row[threadIdx.x] = i;
-      tile_lse[threadIdx.x] = p < k ? (double)lse_ref[((int64_t)b * N + i) * H + h] : 0.0;
+      tile_lse[threadIdx.x] = p < p_end ? (double)lse_ref[((int64_t)b * N + i) * H + h] : 0.0;
     }
     __syncthreads();
     for (int ii = 0; ii < kCsTile; ++ii) {
@@ -167,12 +172,24 @@ __global__ __launch_bounds__(kCsThreads) void prune_mass_kernel(const uint16_t* 
       for (int t = 0; t < HALF; ++t) dot = fma(v[t], tile[ii][half * HALF + t], dot);
       const double other = __shfl_xor(dot, 1, 64);
       const double full = half ? other + dot : dot + other;   // lower half first
-      const int i = tile_row[ii];                              // -1 past the last row: never >= j
-      if (ok && i >= j) acc += exp(sigma * full - tile_lse[ii]);
+      const int i = tile_row[ii];                              // -1 past the chunk's last row: never >= j
+      if (ok && (ii & 1) == half && i >= j) acc += exp(sigma * full - tile_lse[ii]);
     }
     __syncthreads();
   }
-  if (ok && half == 0) key[((int64_t)b * H + h) * n_ent + e] = (float)acc;
+  const double pair = __shfl_xor(acc, 1, 64);
+  if (ok && half == 0) part[(((int64_t)b * H + h) * n_chunks + chunk) * n_ent + e] = acc + pair;
+}
+
+// key[b, h, e] = fp32 of the chunks' partial sums of entry e, added in chunk order
+__global__ __launch_bounds__(256) void prune_sum_kernel(const double* __restrict__ part, int n_chunks, int n_ent,
+                                                        int64_t n_seg, float* __restrict__ key) {
+  const int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (x >= n_seg * n_ent) return;
+  const int64_t seg = x / n_ent, e = x % n_ent;
+  double s = 0.0;
+  for (int c = 0; c < n_chunks; ++c) s += part[(seg * n_chunks + c) * n_ent + e];
+  key[x] = (float)s;
 }
 
 }  // namespace fl
@@ -212,10 +229,17 @@ extern "C" int fl_column_scores(const uint16_t* q, const uint16_t* k_cache, int 
   FL_API_END
 }
 
+extern "C" size_t fl_prune_columns_ws(int B, int H, int k, int c_list, int n_sink) {
+  if (B < 1 || H < 1 || k < 0 || c_list < 1 || n_sink < 0) return 0;
+  const int n_ent = c_list - std::min(n_sink, c_list);
+  const int n_chunks = std::max(1, (k + kPruneChunk - 1) / kPruneChunk);
+  return (size_t)B * H * n_chunks * n_ent * sizeof(double);
+}
+
 extern "C" int fl_prune_columns(const uint16_t* q, const uint16_t* k_cache, const int32_t* rows, int k,
                                 const int32_t* cols, int c_list, const float* lse_ref, int B, int N, int H,
                                 int d, double sm_scale, int n_sink, int t_next, float* col_key,
-                                int32_t* cols_next, void* stream) {
+                                int32_t* cols_next, void* ws, size_t ws_bytes, void* stream) {
   FL_API_BEGIN
   FL_REQUIRE(q && k_cache && cols && lse_ref && cols_next, FL_E_NULL,
              "fl_prune_columns: q, k_cache, cols, lse_ref and cols_next are required");
@@ -233,6 +257,9 @@ extern "C" int fl_prune_columns(const uint16_t* q, const uint16_t* k_cache, cons
   FL_REQUIRE(n_ent <= 65536, FL_E_SHAPE, "fl_prune_columns: %d list entries after the sinks exceed 65536", n_ent);
   FL_REQUIRE(n_ent == 0 || col_key, FL_E_NULL, "fl_prune_columns: col_key is required when entries follow the sinks");
   FL_REQUIRE(sm_scale > 0.0 && std::isfinite(sm_scale), FL_E_RANGE, "fl_prune_columns: sm_scale must be > 0");
+  const size_t need = fl_prune_columns_ws(B, H, k, c_list, n_sink);
+  FL_REQUIRE(need == 0 || (ws && ws_bytes >= need), FL_E_WORKSPACE,
+             "fl_prune_columns: workspace of %zu bytes required", need);
   hipStream_t st = as_stream(stream);
   if (n_ent == 0) {                       // the list is all sinks: it is kept as it is
     if (hipMemcpyAsync(cols_next, cols, (size_t)B * H * ns * sizeof(int32_t), hipMemcpyDeviceToDevice, st) !=
@@ -240,14 +267,22 @@ extern "C" int fl_prune_columns(const uint16_t* q, const uint16_t* k_cache, cons
       return set_error(FL_E_HIP, "fl_prune_columns: copy of the sinks failed");
     return FL_OK;
   }
-  dim3 grid((n_ent + kCsOwn - 1) / kCsOwn, H, B);
+  const int n_chunks = std::max(1, (k + kPruneChunk - 1) / kPruneChunk);
+  FL_REQUIRE((int64_t)H * n_chunks <= 65535, FL_E_SHAPE, "fl_prune_columns: H * ceil(k / %d) above 65535",
+             kPruneChunk);
+  double* part = static_cast<double*>(ws);
+  dim3 grid((n_ent + kCsOwn - 1) / kCsOwn, H * n_chunks, B);
   if (d == 128)
     prune_mass_kernel<128><<<grid, kCsThreads, 0, st>>>(q, k_cache, rows, k, cols, c_list, ns, lse_ref, N, H,
-                                                        sm_scale, col_key);
+                                                        sm_scale, n_chunks, part);
   else
     prune_mass_kernel<64><<<grid, kCsThreads, 0, st>>>(q, k_cache, rows, k, cols, c_list, ns, lse_ref, N, H,
-                                                       sm_scale, col_key);
+                                                       sm_scale, n_chunks, part);
   int rc = check_launch("prune_mass_kernel");
+  if (rc != FL_OK) return rc;
+  const int64_t total = (int64_t)B * H * n_ent;
+  prune_sum_kernel<<<(unsigned)((total + 255) / 256), 256, 0, st>>>(part, n_chunks, n_ent, (int64_t)B * H, col_key);
+  rc = check_launch("prune_sum_kernel");
   if (rc != FL_OK) return rc;
   return launch_topk(B * H, col_key, n_ent, n_ent, t_next, cols + ns, c_list, 0, cols_next, ns + t_next, ns,
                      nullptr, 0, st);

@@ -56,8 +56,9 @@ _SIGNATURES = {
     "fl_decode_step_ws": (_c_sz, [_c_i, _c_i, _c_i, _c_i, _c_i, _c_i]),
     "fl_decode_step": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_i, _c_p, _c_p, _c_i, _c_i, _c_i, _c_i, _c_f, _c_p, _c_p,
                               _c_i, _c_i, _c_i, _c_p, _c_p, _c_p, _c_p, _c_sz, _c_p]),
+    "fl_prune_columns_ws": (_c_sz, [_c_i, _c_i, _c_i, _c_i, _c_i]),
     "fl_prune_columns": (_c_i, [_c_p, _c_p, _c_p, _c_i, _c_p, _c_i, _c_p, _c_i, _c_i, _c_i, _c_i, _c_d, _c_i, _c_i,
-                                _c_p, _c_p, _c_p]),
+                                _c_p, _c_p, _c_p, _c_sz, _c_p]),
 }
 
 EXPORTS = tuple(_SIGNATURES)
@@ -412,8 +413,11 @@ def prune_columns(q, k_cache, rows, cols, lse_ref, n_sink, t_next, sm_scale=None
     col_key = torch.empty(B, H, c_list - ns, dtype=torch.float32, device=dev)
     cols_next = torch.empty(B, H, ns + t_next, dtype=torch.int32, device=dev)
     sm_scale = 1.0 / math.sqrt(d) if sm_scale is None else sm_scale
-    rc = load().fl_prune_columns(_p(q), _p(k_cache), _p(rows), k, _p(cols), c_list, _p(lse_ref), B, N, H, d,
-                                 sm_scale, n_sink, t_next, _p(col_key) if c_list > ns else None, _p(cols_next),
-                                 _stream())
+    lib = load()
+    need = lib.fl_prune_columns_ws(B, H, k, c_list, n_sink)
+    ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    rc = lib.fl_prune_columns(_p(q), _p(k_cache), _p(rows), k, _p(cols), c_list, _p(lse_ref), B, N, H, d,
+                              sm_scale, n_sink, t_next, _p(col_key) if c_list > ns else None, _p(cols_next),
+                              _p(ws), need, _stream())
     _check(rc, "fl_prune_columns")
     return cols_next, col_key

@@ -53,6 +53,9 @@ def test_workspace_queries(lib):
     want = (2 * B * H * c + B * N + B * k + 1) * 8 + B * H * 4
     assert lib.fl_loop_sparse_attn_ws(B, N, H, d, k, c, w, 0) == want
     assert lib.fl_loop_sparse_attn_ws(B, N, H, d, N, 0, 0, fl.ATTN_DENSE) == 0
+    # list pruning: fp64 partial sums per 256-row chunk of the updated rows and per non-sink entry
+    assert lib.fl_prune_columns_ws(1, 16, 1638, 1536, 4) == 16 * 7 * 1532 * 8
+    assert lib.fl_prune_columns_ws(2, 3, 0, 10, 20) == 0          # all sinks: nothing to rank
 
 
 def _attn(lib, **kw):

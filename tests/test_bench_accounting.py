@@ -43,3 +43,16 @@ def check(idx, cols, slot, N, H, d, w, B, reuse, current):
             want_bytes += k * H * d * 4 + k * H * 4 + k * 4                  # previous terms read
     assert flops == want_flops
     assert nbytes == want_bytes
+
+
+def test_prune_work_counts_match_brute_force():
+    """fl_prune_columns: one d-long fp64 dot product per (updated row i, non-sink entry j) with i >= j."""
+    rng = np.random.default_rng(1)
+    B, N, H, d, ns = 2, 400, 3, 64, 4
+    rows = np.stack([np.sort(rng.choice(N, 50, replace=False)) for _ in range(B)]).astype(np.int32)
+    cols = np.stack([np.stack([np.concatenate([np.arange(ns), np.sort(rng.choice(np.arange(ns, N), 70, replace=False))])
+                               for _ in range(H)]) for _ in range(B)]).astype(np.int32)
+    nb, nf = bench.prune_work(rows, cols, ns, H, d)
+    pairs = sum(1 for b in range(B) for h in range(H) for j in cols[b, h, ns:] for i in rows[b] if i >= j)
+    assert nf == 2.0 * d * pairs
+    assert nb == B * H * 70 * (2 * d + 4) + B * 50 * H * (2 * d + 4) + B * H * 74 * 8
