@@ -104,81 +104,129 @@ __global__ __launch_bounds__(kCsThreads) void colscore_kernel(const uint16_t* __
 // Statistic of the list entries for pruning a shrinking list (Section 4.2; Appendix D.2, Eq. 6 with a
 // sparse source): entry j of the (b, h) list gets sum_{i updated, i >= j} exp(sigma q_i . k_j - lse_ref_i),
 // the loop-r probability mass it receives from the updated rows, each row's probabilities recovered from
-// its reference log-normaliser.  A thread pair owns one entry (the K row in registers, half the dims
-// each); a workgroup takes 128 entries and one chunk of kPruneChunk updated rows, staged 32 at a time in
-// ascending order from the first row that can see its first entry, and writes its fp64 partial sums;
-// the partials of the chunks are added in chunk order afterwards.  The two threads of a pair take the
-// exponentials of alternate rows.  fp64 throughout, fixed summation order.
+// its reference log-normaliser.  The dot products are fp64 MFMAs (v_mfma_f64_16x16x4): a wave owns 16
+// entries (their K rows as the B operand, in registers: lane l holds dim 4s + l / 16 of entry l % 16 for
+// step s), a workgroup 64 entries and one chunk of kPruneChunk updated rows, staged 32 rows at a time in
+// LDS as fp64 (the A operand: row l % 16, dim 4s + l / 16).  Which accumulator element is which (row,
+// entry) is read off two index products at the start, so the epilogue does not depend on the output
+// layout.  The chunk partials (fp64, fixed order) are added in chunk order by prune_sum_kernel.
 constexpr int kPruneChunk = 256;
+constexpr int kPruneEnt = 64;             // entries per workgroup (16 per wave)
+constexpr int kPruneRows = 32;            // rows staged per step
+typedef double f64x4 __attribute__((ext_vector_type(4)));
 
 template <int D>
-__global__ __launch_bounds__(kCsThreads) void prune_mass_kernel(const uint16_t* __restrict__ q,
-                                                                const uint16_t* __restrict__ kc,
-                                                                const int32_t* __restrict__ rows, int k,
-                                                                const int32_t* __restrict__ cols, int c_list,
-                                                                int ns, const float* __restrict__ lse_ref,
-                                                                int N, int H, double sigma, int n_chunks,
-                                                                double* __restrict__ part) {
-  __shared__ double tile[kCsTile][D];
-  __shared__ double tile_lse[kCsTile];
-  __shared__ int tile_row[kCsTile];
-  __shared__ int s_first;
-  constexpr int HALF = D / 2;
+__global__ __launch_bounds__(256) void prune_mass_kernel(const uint16_t* __restrict__ q,
+                                                         const uint16_t* __restrict__ kc,
+                                                         const int32_t* __restrict__ rows, int k,
+                                                         const int32_t* __restrict__ cols, int c_list, int ns,
+                                                         const float* __restrict__ lse_ref, int N, int H,
+                                                         double sigma, int n_chunks, double* __restrict__ part) {
+  constexpr int QS = D + 1;               // padded row stride (doubles): the 16 rows of a read spread over banks
+  constexpr int KSTEPS = D / 4;
+  __shared__ double qt[kPruneRows * QS];
+  __shared__ double q_lse[kPruneRows];
+  __shared__ int q_row[kPruneRows];
+  __shared__ double red[4][16][17];       // per wave: accumulators by (entry, row) for the ordered sum
+  __shared__ int s_rows[kPruneChunk];     // the chunk's updated rows
+  __shared__ int s_cnt[4];
   const int h = blockIdx.y % H, chunk = blockIdx.y / H, b = blockIdx.z;
   const int n_ent = c_list - ns;
-  const int e = blockIdx.x * kCsOwn + (threadIdx.x >> 1);
-  const int half = threadIdx.x & 1;
-  const bool ok = e < n_ent;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int l16 = lane & 15, kq = lane >> 4;
   const int64_t stride = (int64_t)H * D;
   const int32_t* cl = cols + ((int64_t)b * H + h) * c_list + ns;
   const int32_t* rp = rows + (int64_t)b * k;
-  const int j = ok ? cl[e] : INT_MAX;
   const int p_end = min(k, (chunk + 1) * kPruneChunk);
+  const int e_wave = blockIdx.x * kPruneEnt + wave * 16;     // first entry of this wave
+  const bool wave_ok = e_wave < n_ent;
+  const int j_first = wave_ok ? cl[e_wave] : INT_MAX;        // entries ascend
 
-  double v[HALF];
+  // B operand: dims 4s + kq of entry e_wave + l16 (zero past the list's end)
+  double kb[KSTEPS];
   {
-    const uint16_t* src = kc + ((int64_t)b * N + (ok ? j : 0)) * stride + (int64_t)h * D + half * HALF;
+    const int e = e_wave + l16;
+    const bool ok = e < n_ent;
+    const uint16_t* src = kc + ((int64_t)b * N + (ok ? cl[e] : 0)) * stride + (int64_t)h * D + kq;
 #pragma unroll
-    for (int t = 0; t < HALF; ++t) v[t] = ok ? (double)bf16_to_f32(src[t]) : 0.0;
+    for (int s = 0; s < KSTEPS; ++s) kb[s] = ok ? (double)bf16_to_f32(src[4 * s]) : 0.0;
   }
-  if (threadIdx.x == 0) {                 // rows and entries ascend: skip the rows before the first entry
-    const int j0 = cl[blockIdx.x * kCsOwn];
-    int lo = chunk * kPruneChunk, hi = p_end;
-    while (lo < hi) {
-      const int mid = (lo + hi) >> 1;
-      if (rp[mid] < j0) lo = mid + 1; else hi = mid;
+  // which (row, entry) each accumulator element holds: D = A B with A = row index in k-column 0, B = 1 in
+  // k-row 0 gives the row; the transposed pair gives the entry
+  int el_row[4], el_ent[4];
+  {
+    const f64x4 zero = {0.0, 0.0, 0.0, 0.0};
+    const f64x4 r = __builtin_amdgcn_mfma_f64_16x16x4f64(kq == 0 ? (double)l16 : 0.0, kq == 0 ? 1.0 : 0.0, zero, 0, 0, 0);
+    const f64x4 c = __builtin_amdgcn_mfma_f64_16x16x4f64(kq == 0 ? 1.0 : 0.0, kq == 0 ? (double)l16 : 0.0, zero, 0, 0, 0);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {           // (clamped: indices stay in range whatever the products hold)
+      el_row[t] = min(max((int)r[t], 0), 15);
+      el_ent[t] = min(max((int)c[t], 0), 15);
     }
-    s_first = lo;
+  }
+  int el_j[4];                             // column id of each element's entry (INT_MAX past the end)
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int e = e_wave + el_ent[t];
+    el_j[t] = e < n_ent ? cl[e] : INT_MAX;
+  }
+  // the chunk's rows into LDS, and the first one that can see the workgroup's first entry (rows and
+  // entries ascend: the rows before it are counted with one ballot per wave)
+  const int p0 = chunk * kPruneChunk;
+  static_assert(kPruneChunk == 256, "one row of the chunk per thread");
+  {
+    const int j0 = cl[blockIdx.x * kPruneEnt];
+    const int p = p0 + (int)threadIdx.x;
+    const int i = p < p_end ? rp[p] : INT_MAX;
+    s_rows[threadIdx.x] = i;
+    const uint64_t before = __builtin_amdgcn_ballot_w64(i < j0);
+    if (lane == 0) s_cnt[wave] = __builtin_popcountll(before);
   }
   __syncthreads();
-  const int first = s_first;
-  double acc = 0.0;
-  for (int t0 = first; t0 < p_end; t0 += kCsTile) {
-    for (int x = threadIdx.x; x < kCsTile * D; x += kCsThreads) {
+  const int first = p0 + s_cnt[0] + s_cnt[1] + s_cnt[2] + s_cnt[3];
+  double acc[4] = {0.0, 0.0, 0.0, 0.0};
+  for (int t0 = first; t0 < p_end; t0 += kPruneRows) {
+    for (int x = threadIdx.x; x < kPruneRows * D; x += 256) {
       const int r = x / D, dd = x % D;
       const int p = t0 + r;
-      tile[r][dd] = p < p_end ? (double)bf16_to_f32(q[((int64_t)b * N + rp[p]) * stride + (int64_t)h * D + dd]) : 0.0;
+      qt[r * QS + dd] = p < p_end ? (double)bf16_to_f32(q[((int64_t)b * N + s_rows[p - p0]) * stride + (int64_t)h * D + dd]) : 0.0;
     }
-    if (threadIdx.x < kCsTile) {
+    if (threadIdx.x < kPruneRows) {
       const int p = t0 + (int)threadIdx.x;
-      const int i = p < p_end ? rp[p] : -1;
-      tile_row[threadIdx.x] = i;
-      tile_lse[threadIdx.x] = p < p_end ? (double)lse_ref[((int64_t)b * N + i) * H + h] : 0.0;
+      const int i = p < p_end ? s_rows[p - p0] : -1;
+      q_row[threadIdx.x] = i;
+      q_lse[threadIdx.x] = p < p_end ? (double)lse_ref[((int64_t)b * N + i) * H + h] : 0.0;
     }
     __syncthreads();
-    for (int ii = 0; ii < kCsTile; ++ii) {
-      double dot = 0.0;
 #pragma unroll
-      for (int t = 0; t < HALF; ++t) dot = fma(v[t], tile[ii][half * HALF + t], dot);
-      const double other = __shfl_xor(dot, 1, 64);
-      const double full = half ? other + dot : dot + other;   // lower half first
-      const int i = tile_row[ii];                              // -1 past the chunk's last row: never >= j
-      if (ok && (ii & 1) == half && i >= j) acc += exp(sigma * full - tile_lse[ii]);
+    for (int half = 0; half < kPruneRows / 16; ++half) {
+      // uniform: skip 16 rows that all come before this wave's first entry
+      const int last_row = q_row[min(16 * half + 15, p_end - t0 - 1)];
+      if (wave_ok && last_row >= j_first) {
+        f64x4 d4 = {0.0, 0.0, 0.0, 0.0};
+        const double* qa = qt + (16 * half + l16) * QS + kq;
+#pragma unroll
+        for (int s = 0; s < KSTEPS; ++s) d4 = __builtin_amdgcn_mfma_f64_16x16x4f64(qa[4 * s], kb[s], d4, 0, 0, 0);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const int r = 16 * half + el_row[t];
+          const int i = q_row[r];                                // -1 past the chunk's last row
+          if (i >= el_j[t]) acc[t] += exp(sigma * d4[t] - q_lse[r]);
+        }
+      }
     }
     __syncthreads();
   }
-  const double pair = __shfl_xor(acc, 1, 64);
-  if (ok && half == 0) part[(((int64_t)b * H + h) * n_chunks + chunk) * n_ent + e] = acc + pair;
+  // ordered sum over the rows held by the wave's lanes: accumulators by (entry, row group), then entry-wise
+#pragma unroll
+  for (int t = 0; t < 4; ++t) red[wave][el_ent[t]][el_row[t]] = acc[t];
+  __syncthreads();
+  if (lane < 16 && wave_ok && e_wave + lane < n_ent) {
+    double s = 0.0;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s += red[wave][lane][r];
+    part[(((int64_t)b * H + h) * n_chunks + chunk) * n_ent + e_wave + lane] = s;
+  }
 }
 
 // key[b, h, e] = fp32 of the chunks' partial sums of entry e, added in chunk order
@@ -271,13 +319,13 @@ extern "C" int fl_prune_columns(const uint16_t* q, const uint16_t* k_cache, cons
   FL_REQUIRE((int64_t)H * n_chunks <= 65535, FL_E_SHAPE, "fl_prune_columns: H * ceil(k / %d) above 65535",
              kPruneChunk);
   double* part = static_cast<double*>(ws);
-  dim3 grid((n_ent + kCsOwn - 1) / kCsOwn, H * n_chunks, B);
+  dim3 grid((n_ent + kPruneEnt - 1) / kPruneEnt, H * n_chunks, B);
   if (d == 128)
-    prune_mass_kernel<128><<<grid, kCsThreads, 0, st>>>(q, k_cache, rows, k, cols, c_list, ns, lse_ref, N, H,
-                                                        sm_scale, n_chunks, part);
+    prune_mass_kernel<128><<<grid, 256, 0, st>>>(q, k_cache, rows, k, cols, c_list, ns, lse_ref, N, H, sm_scale,
+                                                 n_chunks, part);
   else
-    prune_mass_kernel<64><<<grid, kCsThreads, 0, st>>>(q, k_cache, rows, k, cols, c_list, ns, lse_ref, N, H,
-                                                       sm_scale, n_chunks, part);
+    prune_mass_kernel<64><<<grid, 256, 0, st>>>(q, k_cache, rows, k, cols, c_list, ns, lse_ref, N, H, sm_scale,
+                                                n_chunks, part);
   int rc = check_launch("prune_mass_kernel");
   if (rc != FL_OK) return rc;
   const int64_t total = (int64_t)B * H * n_ent;
