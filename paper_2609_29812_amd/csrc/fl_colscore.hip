@@ -1,105 +1,146 @@
-// Column statistic of a dense source loop (Appendix D.2, Eq. 6 with all causal keys and cached mass 1,
-// summed over the rows of a prefill), in fp64 so that the fp32 keys the column top-k ranks are the
-// correctly rounded values of the exact statistic up to fp64 rounding.
-//
-// Two passes, both "a register-resident vector against LDS-staged vectors":
-//   pass 1 (rows)    : a thread pair owns query row i (each thread half of the dims); K rows are staged
-//                      32 at a time; l_ij = sigma * sum_e q_ie k_je and an online fp64 logsumexp over
-//                      j <= i give lse_i (stored in the workspace);
-//   pass 2 (columns) : a thread pair owns key column j; Q rows and their lse are staged 32 at a time and
-//                      col_j = sum_{i >= j} exp(l_ij - lse_i) is accumulated in ascending i.
-// Products of bf16 values are exact in fp64; every sum runs in a fixed order (deterministic).
+// Column statistics in fp64, so that the fp32 keys a top-k ranks are the correctly rounded values of the
+// exact statistic up to fp64 rounding:
+//   * the dense source loop's statistic (Appendix D.2, Eq. 6 with all causal keys and cached mass 1, summed
+//     over the rows of a prefill), in two passes: the rows' log-normalisers, then the column sums;
+//   * the statistic that prunes a list for a smaller budget (Section 4.2): the mass the updated rows give
+//     each list entry, from their stored reference log-normalisers.
+// The dot products run on v_mfma_f64_16x16x4 (products of bf16 values are exact in fp64); every sum runs
+// in a fixed order (deterministic).
 #include "fl_common.h"
 
 namespace fl {
 
-constexpr int kCsThreads = 256;
-constexpr int kCsOwn = kCsThreads / 2;   // rows (pass 1) or columns (pass 2) per workgroup
-constexpr int kCsTile = 32;
+constexpr int kCsRows = 32;               // vectors staged per step
+typedef double f64x4 __attribute__((ext_vector_type(4)));
 
-template <int D>
-__device__ __forceinline__ void stage_f64(double (*tile)[D], const uint16_t* src, int64_t row_stride,
-                                          int first, int N) {
-  for (int q = threadIdx.x; q < kCsTile * D; q += kCsThreads) {
-    const int r = q / D, e = q % D;
-    const int idx = first + r;
-    tile[r][e] = idx < N ? (double)bf16_to_f32(src[(int64_t)idx * row_stride + e]) : 0.0;
+// Which (row, column) of a v_mfma_f64_16x16x4 product each of a lane's four accumulator elements holds,
+// read off two index products (A = row index in k-column 0 against B = 1 in k-row 0, and the transposed
+// pair), clamped so that the indices stay in range whatever the products hold.
+__device__ __forceinline__ void mfma_f64_layout(int l16, int kq, int (&row)[4], int (&col)[4]) {
+  const f64x4 zero = {0.0, 0.0, 0.0, 0.0};
+  const f64x4 r = __builtin_amdgcn_mfma_f64_16x16x4f64(kq == 0 ? (double)l16 : 0.0, kq == 0 ? 1.0 : 0.0, zero, 0, 0, 0);
+  const f64x4 c = __builtin_amdgcn_mfma_f64_16x16x4f64(kq == 0 ? 1.0 : 0.0, kq == 0 ? (double)l16 : 0.0, zero, 0, 0, 0);
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    row[t] = min(max((int)r[t], 0), 15);
+    col[t] = min(max((int)c[t], 0), 15);
   }
 }
 
-template <int D, bool COLUMNS>
-__global__ __launch_bounds__(kCsThreads) void colscore_kernel(const uint16_t* __restrict__ q,
-                                                              const uint16_t* __restrict__ kc, int N,
-                                                              int H, double sigma,
-                                                              double* __restrict__ lse,
-                                                              float* __restrict__ col_key) {
-  __shared__ double tile[kCsTile][D];
-  __shared__ double tile_lse[kCsTile];
-  constexpr int HALF = D / 2;
+// Dense column statistic in two passes, the fp64 dot products on v_mfma_f64_16x16x4 (products of bf16 values
+// are exact in fp64).  A wave owns 16 vectors of one side in registers (lane l holds dim 4s + l / 16 of vector
+// l % 16 for step s), a workgroup 64 of them; the other side is staged 32 vectors at a time in LDS as fp64.
+//   pass 1 (ROWS)  : the wave's 16 query rows against the staged K columns j <= i: per accumulator element
+//                    an online (max, sum) in fp64; the 16 partial pairs of a row are merged in column order;
+//   pass 2 (!ROWS) : the wave's 16 K columns against the staged query rows i >= j and their lse_i:
+//                    col_j = sum exp(l_ij - lse_i), the 16 partials of a column added in row order.
+// Every sum runs in a fixed order (deterministic).
+template <int D, bool ROWS>
+__global__ __launch_bounds__(256) void colscore_kernel(const uint16_t* __restrict__ q,
+                                                       const uint16_t* __restrict__ kc, int N, int H,
+                                                       double sigma, double* __restrict__ lse,
+                                                       float* __restrict__ col_key) {
+  constexpr int QS = D + 1;               // padded stride (doubles): the 16 vectors of a read spread over banks
+  constexpr int KSTEPS = D / 4;
+  __shared__ double st[kCsRows * QS];
+  __shared__ double st_lse[kCsRows];
+  __shared__ double red_m[4][16][17];
+  __shared__ double red_s[4][16][17];
   const int h = blockIdx.y, b = blockIdx.z;
-  const int me = blockIdx.x * kCsOwn + (threadIdx.x >> 1);
-  const int half = threadIdx.x & 1;
-  const bool ok = me < N;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int l16 = lane & 15, kq = lane >> 4;
   const int64_t stride = (int64_t)H * D;
   const uint16_t* qbase = q + (int64_t)b * N * stride + (int64_t)h * D;
   const uint16_t* kbase = kc + (int64_t)b * N * stride + (int64_t)h * D;
   double* lse_bh = lse + ((int64_t)b * H + h) * N;
+  const int v0 = blockIdx.x * 64 + wave * 16;          // first of the wave's own vectors
+  const bool wave_ok = v0 < N;
 
-  double v[HALF];
+  double reg[KSTEPS];                                   // own vectors (query rows or key columns)
   {
-    const uint16_t* src = (COLUMNS ? kbase : qbase) + (int64_t)(ok ? me : 0) * stride + half * HALF;
+    const int v = v0 + l16;
+    const uint16_t* src = (ROWS ? qbase : kbase) + (int64_t)(v < N ? v : 0) * stride + kq;
 #pragma unroll
-    for (int e = 0; e < HALF; ++e) v[e] = ok ? (double)bf16_to_f32(src[e]) : 0.0;
+    for (int s = 0; s < KSTEPS; ++s) reg[s] = v < N ? (double)bf16_to_f32(src[4 * s]) : 0.0;
   }
-
-  if (!COLUMNS) {
-    const int last = min(N, (int)(blockIdx.x + 1) * kCsOwn) - 1;
-    double m = -INFINITY, s = 0.0;
-    for (int t0 = 0; t0 <= last; t0 += kCsTile) {
-      stage_f64<D>(tile, kbase, stride, t0, N);
-      __syncthreads();
-      for (int jj = 0; jj < kCsTile; ++jj) {
-        const int j = t0 + jj;
-        double dot = 0.0;
+  int el_r[4], el_c[4];                   // element t: staged vector el_r (A side), own vector el_c (B side)
+  mfma_f64_layout(l16, kq, el_r, el_c);
+  // staged range: pass 1 columns 0 .. last own row; pass 2 rows from the workgroup's first column on
+  const int wg_first = blockIdx.x * 64;
+  const int s_begin = ROWS ? 0 : wg_first;
+  const int s_end = ROWS ? min(N, wg_first + 64) : N;
+  double m[4], acc[4];
 #pragma unroll
-        for (int e = 0; e < HALF; ++e) dot = fma(v[e], tile[jj][half * HALF + e], dot);
-        const double other = __shfl_xor(dot, 1, 64);
-        const double full = half ? other + dot : dot + other;   // lower half first
-        if (ok && j <= me) {
-          const double l = sigma * full;
-          if (l > m) {
-            s = s * exp(m - l) + 1.0;
-            m = l;
+  for (int t = 0; t < 4; ++t) { m[t] = -INFINITY; acc[t] = 0.0; }
+  for (int t0 = s_begin; t0 < s_end; t0 += kCsRows) {
+    for (int x = threadIdx.x; x < kCsRows * D; x += 256) {
+      const int r = x / D, dd = x % D;
+      const int v = t0 + r;
+      st[r * QS + dd] = v < s_end ? (double)bf16_to_f32((ROWS ? kbase : qbase)[(int64_t)v * stride + dd]) : 0.0;
+    }
+    if (!ROWS && threadIdx.x < kCsRows) {
+      const int v = t0 + (int)threadIdx.x;
+      st_lse[threadIdx.x] = v < s_end ? lse_bh[v] : 0.0;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int half = 0; half < kCsRows / 16; ++half) {
+      const int sv0 = t0 + 16 * half;                   // first staged vector of this 16
+      // uniform: pass 1 needs staged columns <= the wave's last row, pass 2 staged rows >= its first column
+      const bool useful = wave_ok && sv0 < s_end && (ROWS ? sv0 <= v0 + 15 : sv0 + 15 >= v0);
+      if (useful) {
+        f64x4 d4 = {0.0, 0.0, 0.0, 0.0};
+        const double* sa = st + (16 * half + l16) * QS + kq;
+#pragma unroll
+        for (int s = 0; s < KSTEPS; ++s) d4 = __builtin_amdgcn_mfma_f64_16x16x4f64(sa[4 * s], reg[s], d4, 0, 0, 0);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const int sv = sv0 + el_r[t];                  // staged vector
+          const int ov = v0 + el_c[t];                   // own vector
+          const double l = sigma * d4[t];
+          if (ROWS) {
+            if (sv < s_end && ov < N && sv <= ov) {      // column sv of row ov
+              if (l > m[t]) {
+                acc[t] = acc[t] * exp(m[t] - l) + 1.0;
+                m[t] = l;
+              } else {
+                acc[t] += exp(l - m[t]);
+              }
+            }
           } else {
-            s += exp(l - m);
+            if (sv < s_end && ov < N && sv >= ov) acc[t] += exp(l - st_lse[16 * half + el_r[t]]);   // row sv
           }
         }
       }
-      __syncthreads();
     }
-    if (ok && half == 0) lse_bh[me] = m + log(s);
-  } else {
-    const int first = blockIdx.x * kCsOwn;
-    double acc = 0.0;
-    for (int t0 = first; t0 < N; t0 += kCsTile) {
-      stage_f64<D>(tile, qbase, stride, t0, N);
-      if (threadIdx.x < kCsTile) tile_lse[threadIdx.x] = (t0 + (int)threadIdx.x) < N ? lse_bh[t0 + threadIdx.x] : 0.0;
-      __syncthreads();
-      for (int ii = 0; ii < kCsTile; ++ii) {
-        const int i = t0 + ii;
-        double dot = 0.0;
+    __syncthreads();
+  }
+  // merge the 16 partials of each own vector in staged-slot order
 #pragma unroll
-        for (int e = 0; e < HALF; ++e) dot = fma(v[e], tile[ii][half * HALF + e], dot);
-        const double other = __shfl_xor(dot, 1, 64);
-        const double full = half ? other + dot : dot + other;
-        if (ok && i < N && i >= me) acc += exp(sigma * full - tile_lse[ii]);
-      }
-      __syncthreads();
+  for (int t = 0; t < 4; ++t) {
+    red_m[wave][el_c[t]][el_r[t]] = m[t];
+    red_s[wave][el_c[t]][el_r[t]] = acc[t];
+  }
+  __syncthreads();
+  const int v = v0 + lane;
+  if (lane < 16 && v < N) {
+    if (ROWS) {
+      double mm = -INFINITY;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mm = fmax(mm, red_m[wave][lane][r]);
+      double ss = 0.0;
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        if (red_s[wave][lane][r] > 0.0) ss += red_s[wave][lane][r] * exp(red_m[wave][lane][r] - mm);
+      lse_bh[v] = mm + log(ss);
+    } else {
+      double ss = 0.0;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) ss += red_s[wave][lane][r];
+      col_key[((int64_t)b * H + h) * N + v] = (float)ss;
     }
-    if (ok && half == 0) col_key[((int64_t)b * H + h) * N + me] = (float)acc;
   }
 }
-
 
 // Statistic of the list entries for pruning a shrinking list (Section 4.2; Appendix D.2, Eq. 6 with a
 // sparse source): entry j of the (b, h) list gets sum_{i updated, i >= j} exp(sigma q_i . k_j - lse_ref_i),
@@ -113,7 +154,6 @@ __global__ __launch_bounds__(kCsThreads) void colscore_kernel(const uint16_t* __
 constexpr int kPruneChunk = 256;
 constexpr int kPruneEnt = 64;             // entries per workgroup (16 per wave)
 constexpr int kPruneRows = 32;            // rows staged per step
-typedef double f64x4 __attribute__((ext_vector_type(4)));
 
 template <int D>
 __global__ __launch_bounds__(256) void prune_mass_kernel(const uint16_t* __restrict__ q,
@@ -154,16 +194,7 @@ __global__ __launch_bounds__(256) void prune_mass_kernel(const uint16_t* __restr
   // which (row, entry) each accumulator element holds: D = A B with A = row index in k-column 0, B = 1 in
   // k-row 0 gives the row; the transposed pair gives the entry
   int el_row[4], el_ent[4];
-  {
-    const f64x4 zero = {0.0, 0.0, 0.0, 0.0};
-    const f64x4 r = __builtin_amdgcn_mfma_f64_16x16x4f64(kq == 0 ? (double)l16 : 0.0, kq == 0 ? 1.0 : 0.0, zero, 0, 0, 0);
-    const f64x4 c = __builtin_amdgcn_mfma_f64_16x16x4f64(kq == 0 ? 1.0 : 0.0, kq == 0 ? (double)l16 : 0.0, zero, 0, 0, 0);
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {           // (clamped: indices stay in range whatever the products hold)
-      el_row[t] = min(max((int)r[t], 0), 15);
-      el_ent[t] = min(max((int)c[t], 0), 15);
-    }
-  }
+  mfma_f64_layout(l16, kq, el_row, el_ent);
   int el_j[4];                             // column id of each element's entry (INT_MAX past the end)
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
@@ -261,17 +292,17 @@ extern "C" int fl_column_scores(const uint16_t* q, const uint16_t* k_cache, int 
   hipStream_t st = as_stream(stream);
   const double sigma = 1.0 / std::sqrt((double)d);
   double* lse = static_cast<double*>(ws);
-  dim3 grid((N + kCsOwn - 1) / kCsOwn, H, B);
+  dim3 grid((N + 63) / 64, H, B);
   if (d == 128) {
-    colscore_kernel<128, false><<<grid, kCsThreads, 0, st>>>(q, k_cache, N, H, sigma, lse, col_key);
+    colscore_kernel<128, true><<<grid, 256, 0, st>>>(q, k_cache, N, H, sigma, lse, col_key);
     int rc = check_launch("colscore_kernel(rows)");
     if (rc != FL_OK) return rc;
-    colscore_kernel<128, true><<<grid, kCsThreads, 0, st>>>(q, k_cache, N, H, sigma, lse, col_key);
+    colscore_kernel<128, false><<<grid, 256, 0, st>>>(q, k_cache, N, H, sigma, lse, col_key);
   } else {
-    colscore_kernel<64, false><<<grid, kCsThreads, 0, st>>>(q, k_cache, N, H, sigma, lse, col_key);
+    colscore_kernel<64, true><<<grid, 256, 0, st>>>(q, k_cache, N, H, sigma, lse, col_key);
     int rc = check_launch("colscore_kernel(rows)");
     if (rc != FL_OK) return rc;
-    colscore_kernel<64, true><<<grid, kCsThreads, 0, st>>>(q, k_cache, N, H, sigma, lse, col_key);
+    colscore_kernel<64, false><<<grid, 256, 0, st>>>(q, k_cache, N, H, sigma, lse, col_key);
   }
   return check_launch("colscore_kernel(columns)");
   FL_API_END
