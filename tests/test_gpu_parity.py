@@ -68,6 +68,25 @@ def test_select_tokens_ties_edges_and_one_pair(F):
     assert_keys_close(down(key), want_key, "unnormalized keys")
 
 
+def test_select_tokens_on_hidden_states(F):
+    """Eq. (5) scored on the layer's hidden states instead of K and V: one pair of [B, N, D_model] states
+    (D_model = 2048, the 16 x 128 model width), two nested loops (candidates = the previous selection)."""
+    rng = np.random.default_rng(22)
+    B, N, Dm = 2, 3000, 2048
+    h0, h1, h2 = (_bf16(rng, (B, N, Dm)) for _ in range(3))
+    idx_prev = None
+    for (cur, prev), k in (((h1, h0), 900), ((h2, h1), 300)):
+        want_key = select.token_keys([(cur, prev)], idx_prev)
+        want_idx, want_slot = select.nested_topk(want_key, idx_prev, k, N)
+        cand = None if idx_prev is None else torch.from_numpy(idx_prev).cuda()
+        idx, slot, key = F.select_tokens(up_bf16(cur), up_bf16(prev), None, None, k, cand=cand)
+        torch.cuda.synchronize()
+        assert_keys_close(down(key), want_key, f"hidden-state keys k={k}")
+        assert np.array_equal(down(idx), want_idx), k
+        assert np.array_equal(down(slot), want_slot), k
+        idx_prev = want_idx
+
+
 # ---------------------------------------------------------------------------------------------------
 @pytest.mark.parametrize("bits", [2, 4, 8, 16])
 @pytest.mark.parametrize("axis", [codec.AXIS_TOKEN, codec.AXIS_CHANNEL])
