@@ -69,6 +69,8 @@ def loop1(states, heads=None, cols_only=False):
     k_hat, _ = codec.reconstruct(None, K1, None, enc_k, w.base_bits, w.group, codec.AXIS_TOKEN)
     enc_v = codec.quantize(V1, None, None, w.base_bits, w.group, codec.AXIS_CHANNEL)
     v_hat, _ = codec.reconstruct(None, V1, None, enc_v, w.base_bits, w.group, codec.AXIS_CHANNEL)
+    k_hat, _ = codec.keep_recent(k_hat, None, K1, None, w.tail)
+    v_hat, _ = codec.keep_recent(v_hat, None, V1, None, w.tail)
     heads = list(range(w.heads)) if heads is None else list(heads)
     rec = LayerRecord(w, heads, k_hat, v_hat, enc_k, enc_v, {}, {}, {}, {}, {})
     for b in range(w.batch):
@@ -100,6 +102,8 @@ def sparse_loop(states, r, cand, k_hat, v_hat, cols, o, lse, heads, rows=None):
     k_hat_r, k_new = codec.reconstruct(k_hat, Kr, idx, enc_k, bits, w.group, codec.AXIS_TOKEN)
     enc_v = codec.quantize(Vr, v_hat, idx, bits, w.group, codec.AXIS_CHANNEL)
     v_hat_r, v_new = codec.reconstruct(v_hat, Vr, idx, enc_v, bits, w.group, codec.AXIS_CHANNEL)
+    k_hat_r, k_new = codec.keep_recent(k_hat_r, k_new, Kr, idx, w.tail)
+    v_hat_r, v_new = codec.keep_recent(v_hat_r, v_new, Vr, idx, w.tail)
     mass = {}
     for b in range(w.batch):
         active = idx[b].astype(np.int64)

@@ -157,3 +157,27 @@ def reconstruct(x_hat_prev, x_cur, idx, enc, bits, group, axis):
         rows = np.arange(N) if idx is None else np.asarray(idx[b], dtype=np.int64)
         x_hat[b, rows] = new_rows[b]
     return x_hat, new_rows
+
+
+def keep_recent(x_hat, new_rows, x_cur, idx, tail):
+    """Appendix E keeps the most recent `tail` tokens in bf16: every stored row i >= N - tail is the exact
+    X^(r) row instead of its reconstruction.  Reading: the rows are still encoded with the others (the groups
+    and codes are unchanged); only what the state stores for them is exact.  x_hat [B, N, H, d] and the
+    compact new_rows [B, k, H, d] (either may be None) are returned as updated copies."""
+    if tail <= 0:
+        return x_hat, new_rows
+    B, N = x_cur.shape[:2]
+    lo = max(0, N - tail)
+    if x_hat is not None:
+        x_hat = x_hat.copy()
+        for b in range(B):
+            rows = np.arange(N) if idx is None else np.asarray(idx[b], dtype=np.int64)
+            rows = rows[rows >= lo]
+            x_hat[b, rows] = x_cur[b, rows]
+    if new_rows is not None:
+        new_rows = new_rows.copy()
+        for b in range(B):
+            rows = np.arange(N) if idx is None else np.asarray(idx[b], dtype=np.int64)
+            sel = np.nonzero(rows >= lo)[0]
+            new_rows[b, sel] = x_cur[b, rows[sel]]
+    return x_hat, new_rows

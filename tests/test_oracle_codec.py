@@ -11,7 +11,7 @@ import numpy as np
 import pytest
 
 from oracle import codec
-from oracle.numerics import bf16_to_f32, f16_down, f16_up, f32_to_bf16
+from oracle.numerics import bf16_to_f32, bf16_to_f64, f16_down, f16_up, f32_to_bf16
 from workloads import get, make_layer
 
 # every finite binary16 value, ascending (as float64)
@@ -192,3 +192,32 @@ def test_residual_coding_beats_full_state_coding_on_lazy_deltas():
         err_res = np.linalg.norm(bf16_to_f32(hr) - ref)
         err_full = np.linalg.norm(bf16_to_f32(hf) - ref)
         assert err_res < err_full
+
+
+def test_recent_tail_keeps_exact_rows_and_only_those():
+    """Appendix E's bf16 tail: with tail = N and 4-bit codecs every stored row is exact, so the chain over
+    all rows and columns is exact attention in every loop (as without quantization); with a 64-row tail
+    the base codes are unchanged, the rows before the tail are the plain reconstructions, the tail rows
+    are the exact inputs."""
+    from oracle import attention as att
+    from oracle import chain
+    from workloads import get, make_layer
+    w = get("C2").replace(seq=200, heads=2, head_dim=32, topk_frac=(1.0, 1.0, 1.0), bits=(4, 4, 4),
+                          base_bits=4, group=32, tail=200)
+    st = make_layer(w)
+    cols = {(0, h): np.arange(w.seq, dtype=np.int32) for h in range(w.heads)}
+    rec = chain.run_layer(st, cols=cols)
+    for lr in rec.loops:
+        for h in range(w.heads):
+            q, k, v = (bf16_to_f64(getattr(st, n)[lr.r - 1][0, :, h, :]) for n in "qkv")
+            o, _, _ = att.dense_loop(q, k, v, w.sm_scale, want_colscore=False)
+            assert np.max(np.abs(lr.o[0, h] - o)) < 1e-11, (lr.r, h)
+    w64 = get("C2").replace(seq=300, heads=2, head_dim=32, group=32, tail=64)
+    st = make_layer(w64)
+    with_tail = chain.loop1(st)
+    without = chain.loop1(make_layer(w64.replace(tail=0)))
+    assert np.array_equal(with_tail.enc_k1["codes"], without.enc_k1["codes"])
+    assert np.array_equal(with_tail.k_hat1[:, :236], without.k_hat1[:, :236])
+    assert np.array_equal(with_tail.k_hat1[:, 236:], st.k[0][:, 236:])
+    assert np.array_equal(with_tail.v_hat1[:, 236:], st.v[0][:, 236:])
+    assert not np.array_equal(without.k_hat1[:, 236:], st.k[0][:, 236:])

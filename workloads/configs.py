@@ -33,6 +33,7 @@ class Workload:
     delta: str = "normal"     # "normal" (std hot_scale) or "student_t" (df, scale hot_scale)
     col_decay: tuple = ()     # optional per sparse loop r = 2..R: column budget c_r (c_2 = col_budget); a
                               # smaller budget prunes the list after the loop before (Section 4.2)
+    tail: int = 0             # the most recent `tail` positions are stored exactly in bf16 (Appendix E: 64)
     hot_scale: float = 0.5
     cold_std: float = 0.01
     df: float = 3.0
