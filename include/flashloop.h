@@ -12,8 +12,8 @@
  *                             with a mass-corrected correction over predicted key columns
  *                             (Sections 3.2, 4.2, Eq. 3; Appendix D.2, Eq. 7).
  * plus two set-up helpers for a dense source loop (Appendix D.2, Eq. 6 with all causal keys):
- *   fl_column_scores, fl_select_columns; the decode step (fl_decode_step) and the list pruning for a
- *   shrinking budget (fl_prune_columns).
+ *   fl_column_scores, fl_select_columns; the decode step (fl_decode_step), the list pruning for a
+ *   shrinking budget (fl_prune_columns) and the recent-token bf16 tail (fl_kv_keep_recent).
  *
  * Conventions shared by every call
  *   - Every data pointer is a DEVICE pointer (HIP device memory).  The caller allocates and owns all
@@ -337,6 +337,19 @@ int fl_prune_columns(const uint16_t* q, const uint16_t* k_cache, const int32_t* 
                      const int32_t* cols, int c_list, const float* lse_ref, int B, int N, int H, int d,
                      double sm_scale, int n_sink, int t_next, float* col_key, int32_t* cols_next,
                      void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------------------------------
+ * (8) Recent tokens kept in bf16 -- Appendix E (the most recent 64 tokens stay in BF16).  For every active
+ * row i = idx[b, p] (or every row when idx == NULL) with i >= N - tail, the stored row becomes the exact
+ * input row:  cache[b, i] = x_cur[b, i]  and/or  rows[b, p] = x_cur[b, i].  The rows are still encoded
+ * with the others by the codec calls; this call replaces what the state stores for them, after those calls.
+ *   x_cur       : bf16 [B, N, H, d], d a positive multiple of 8 (16-byte aligned rows).
+ *   idx, k      : int32 [B, k] ascending active rows (NULL: every row, k = N).
+ *   cache       : bf16 [B, N, H, d] or NULL;  rows : bf16 [B, k, H, d] compact rows or NULL (not both NULL).
+ *   tail = 0 does nothing.  One launch over the last min(k, tail) entries of idx.
+ * ---------------------------------------------------------------------------------------------- */
+int fl_kv_keep_recent(const uint16_t* x_cur, const int32_t* idx, int k, int B, int N, int H, int d, int tail,
+                      uint16_t* cache, uint16_t* rows, void* stream);
 
 #ifdef __cplusplus
 }

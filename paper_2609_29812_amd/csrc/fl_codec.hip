@@ -531,6 +531,26 @@ static int residual_quant_kv(const char* fn, const uint16_t* k_cur, uint16_t* k_
   return check_launch("quant_kv_kernel");
 }
 
+
+// The most recent tokens stay in bf16 (Appendix E): rows i >= N - tail among the active rows are stored as
+// the exact X^(r) rows, in the caches and/or the compact rows (their codes are formed with the others).
+// idx ascends, so only its last min(k, tail) entries can be tail rows: one thread per 16-byte chunk of those.
+__global__ __launch_bounds__(256) void keep_recent_kernel(const uint16_t* __restrict__ x_cur,
+                                                          const int32_t* __restrict__ idx, int k, int N, int HD,
+                                                          int lo, int n_last, uint16_t* cache, uint16_t* rows) {
+  const int b = blockIdx.y;
+  const int chunks = HD / 8;
+  const int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (x >= (int64_t)n_last * chunks) return;
+  const int p = k - n_last + (int)(x / chunks);
+  const int c = (int)(x % chunks);
+  const int i = idx ? idx[(int64_t)b * k + p] : p;
+  if (i < lo) return;
+  const uint4 v = *reinterpret_cast<const uint4*>(x_cur + ((int64_t)b * N + i) * HD + c * 8);
+  if (cache) *reinterpret_cast<uint4*>(cache + ((int64_t)b * N + i) * HD + c * 8) = v;
+  if (rows) *reinterpret_cast<uint4*>(rows + ((int64_t)b * k + p) * HD + c * 8) = v;
+}
+
 }  // namespace fl
 
 using namespace fl;
@@ -646,5 +666,27 @@ extern "C" int fl_kv_residual_dequant(const uint8_t* codes, const uint16_t* scal
   }
 #undef FL_DQ
   return check_launch("dequant_kernel");
+  FL_API_END
+}
+
+extern "C" int fl_kv_keep_recent(const uint16_t* x_cur, const int32_t* idx, int k, int B, int N, int H, int d,
+                                 int tail, uint16_t* cache, uint16_t* rows, void* stream) {
+  FL_API_BEGIN
+  FL_REQUIRE(x_cur, FL_E_NULL, "fl_kv_keep_recent: x_cur is required");
+  FL_REQUIRE(cache || rows, FL_E_NULL, "fl_kv_keep_recent: cache or rows is required");
+  FL_REQUIRE(B >= 1 && N >= 1 && H >= 1, FL_E_SHAPE, "fl_kv_keep_recent: need B, N, H >= 1");
+  FL_REQUIRE(d >= 8 && d % 8 == 0, FL_E_SHAPE, "fl_kv_keep_recent: d=%d must be a positive multiple of 8", d);
+  FL_REQUIRE((int64_t)N * H * d < ((int64_t)1 << 40), FL_E_SHAPE, "fl_kv_keep_recent: N * H * d too large");
+  FL_REQUIRE(k >= 0 && k <= N, FL_E_RANGE, "fl_kv_keep_recent: k=%d outside [0, N]", k);
+  FL_REQUIRE(idx || k == N, FL_E_SHAPE, "fl_kv_keep_recent: without idx, k must equal N");
+  FL_REQUIRE(tail >= 0, FL_E_RANGE, "fl_kv_keep_recent: tail must be >= 0");
+  const int n_last = std::min(k, tail);
+  if (n_last == 0) return FL_OK;
+  const int HD = H * d;
+  const int64_t work = (int64_t)n_last * (HD / 8);
+  dim3 grid((unsigned)((work + 255) / 256), B);
+  keep_recent_kernel<<<grid, 256, 0, as_stream(stream)>>>(x_cur, idx, k, N, HD, std::max(0, N - tail), n_last,
+                                                          cache, rows);
+  return check_launch("keep_recent_kernel");
   FL_API_END
 }

@@ -1,7 +1,8 @@
 """Per-layer sequencing of the FlashLoop step on one GPU (device tensors only; all math is in the library).
 
 setup()       dense source loop 1: base codec of K (per-channel groups) and V (per-token groups) with the
-              reconstruction written straight into the caches, dense causal attention over the
+              reconstruction written straight into the caches (the most recent `tail` rows stored exactly,
+              Appendix E), dense causal attention over the
               reconstructed base, fp64 column statistic and the column list (Appendix D.2, Eq. 6).
 sparse_step() one sparse loop r >= 2: select the active rows among the previous loop's (Eq. 5), quantize
               their K/V residuals against the caches and reconstruct the new rows (Eq. 8), apply the
@@ -38,18 +39,23 @@ class LayerState:
     term: torch.Tensor | None = None    # fp32 [B, k, H, d] add terms of the last loop (row order of cand)
     mass: torch.Tensor | None = None    # fp32 [B, k, H]
     slot_prev: torch.Tensor | None = None   # int32 [B, N] slot map of the last loop
+    tail: int = 0                       # the most recent positions stored exactly in bf16 (Appendix E)
 
 
-def setup(q1, k1, v1, base_bits, group, n_sink, t, window):
+def setup(q1, k1, v1, base_bits, group, n_sink, t, window, tail=0):
     B, N, H, d = k1.shape
     k_hat = torch.empty_like(k1)
     v_hat = torch.empty_like(v1)
     ck, sk, zk, _ = fl.kv_residual_quant(k1, None, None, base_bits, group, fl.AXIS_TOKEN, rows=k_hat)
     cv, sv, zv, _ = fl.kv_residual_quant(v1, None, None, base_bits, group, fl.AXIS_CHANNEL, rows=v_hat)
+    if tail:
+        fl.kv_keep_recent(k1, None, tail, cache=k_hat)
+        fl.kv_keep_recent(v1, None, tail, cache=v_hat)
     o, lse = fl.dense_attn(q1, k_hat, v_hat)
     col_key = fl.column_scores(q1, k_hat)
     cols = fl.select_columns(col_key, n_sink, t)
     st = LayerState(k_hat, v_hat, o, lse, cols, None, window, group)
+    st.tail = tail
     st.base = dict(codes_k=ck, scale_k=sk, zero_k=zk, codes_v=cv, scale_v=sv, zero_v=zv, col_key=col_key)
     return st
 
@@ -68,6 +74,9 @@ def sparse_step(st: LayerState, qr, qp, kr, kp, vr, vp, k_r, bits, keep=False):
         # the add pass alone: commit the new rows first, then attend over the caches
         (ck, sk, zk, _), (cv, sv, zv, _) = fl.kv_residual_quant_kv(kr, st.k_hat, vr, st.v_hat, idx, bits,
                                                                    st.group, mode=fl.DQ_COMMIT)
+        if st.tail:
+            fl.kv_keep_recent(kr, idx, st.tail, cache=st.k_hat)
+            fl.kv_keep_recent(vr, idx, st.tail, cache=st.v_hat)
         fl.loop_sparse_attn(qr, None, st.k_hat, st.v_hat, None, None, slot, idx, st.cols, st.window, st.lse,
                             st.o, term_prev=st.term, mass_prev=st.mass, slot_prev=st.slot_prev, term_out=term,
                             mass_out=mass)
@@ -75,10 +84,16 @@ def sparse_step(st: LayerState, qr, qp, kr, kp, vr, vp, k_r, bits, keep=False):
         # both passes: the subtract pass needs the loop r-1 caches, so commit after the attention
         (ck, sk, zk, k_new), (cv, sv, zv, v_new) = fl.kv_residual_quant_kv(kr, st.k_hat, vr, st.v_hat, idx, bits,
                                                                            st.group)
+        if st.tail:
+            fl.kv_keep_recent(kr, idx, st.tail, rows=k_new)
+            fl.kv_keep_recent(vr, idx, st.tail, rows=v_new)
         fl.loop_sparse_attn(qr, qp, st.k_hat, st.v_hat, k_new, v_new, slot, idx, st.cols, st.window, st.lse,
                             st.o, term_out=term, mass_out=mass)
         fl.kv_residual_dequant_kv((ck, sk, zk), (cv, sv, zv), idx, bits, st.group, st.k_hat, st.v_hat,
                                   mode=fl.DQ_COMMIT)
+        if st.tail:
+            fl.kv_keep_recent(kr, idx, st.tail, cache=st.k_hat)
+            fl.kv_keep_recent(vr, idx, st.tail, cache=st.v_hat)
     st.term, st.mass, st.slot_prev = term, mass, slot
     st.cand = idx
     if keep:   # (k_new / v_new are None when the loop committed straight into the caches)

@@ -57,6 +57,7 @@ _SIGNATURES = {
     "fl_decode_step": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_i, _c_p, _c_p, _c_i, _c_i, _c_i, _c_i, _c_f, _c_p, _c_p,
                               _c_i, _c_i, _c_i, _c_p, _c_p, _c_p, _c_p, _c_sz, _c_p]),
     "fl_prune_columns_ws": (_c_sz, [_c_i, _c_i, _c_i, _c_i, _c_i]),
+    "fl_kv_keep_recent": (_c_i, [_c_p, _c_p, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_p, _c_p, _c_p]),
     "fl_prune_columns": (_c_i, [_c_p, _c_p, _c_p, _c_i, _c_p, _c_i, _c_p, _c_i, _c_i, _c_i, _c_i, _c_d, _c_i, _c_i,
                                 _c_p, _c_p, _c_p, _c_sz, _c_p]),
 }
@@ -421,3 +422,17 @@ def prune_columns(q, k_cache, rows, cols, lse_ref, n_sink, t_next, sm_scale=None
                               _p(ws), need, _stream())
     _check(rc, "fl_prune_columns")
     return cols_next, col_key
+
+
+# ---- (8) recent tokens kept in bf16 --------------------------------------------------------------------
+def kv_keep_recent(x_cur, idx, tail, cache=None, rows=None):
+    """Store the active rows i >= N - tail exactly: cache [B, N, H, d] at i and/or the compact rows
+    [B, k, H, d] at their position (x_cur bf16 [B, N, H, d]; idx int32 [B, k] or None for every row)."""
+    B, N, H, d = x_cur.shape
+    _dev(x_cur, torch.bfloat16, "x_cur")
+    k = N if idx is None else idx.shape[1]
+    _dev(idx, torch.int32, "idx", None if idx is None else (B, k))
+    _dev(cache, torch.bfloat16, "cache", None if cache is None else x_cur.shape)
+    _dev(rows, torch.bfloat16, "rows", None if rows is None else (B, k, H, d))
+    rc = load().fl_kv_keep_recent(_p(x_cur), _p(idx), k, B, N, H, d, tail, _p(cache), _p(rows), _stream())
+    _check(rc, "fl_kv_keep_recent")

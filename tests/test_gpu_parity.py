@@ -179,6 +179,27 @@ def test_codec_kv_pair_matches_oracle(F, bits, d, G, k):
     assert np.array_equal(down_bits16(dv), want["v"][1]), "pair commit: value cache differs"
 
 
+def test_keep_recent_matches_oracle(F):
+    """fl_kv_keep_recent against codec.keep_recent: tails longer and shorter than the active set, rows with
+    no active tail row, every row (idx = NULL), the caches and the compact rows, tail = 0."""
+    rng = np.random.default_rng(31)
+    B, N, H, d = 2, 500, 3, 64
+    x = _bf16(rng, (B, N, H, d))
+    for k, tail in ((40, 64), (200, 16), (30, 0), (N, 70)):
+        idx = None if k == N else np.stack([np.sort(rng.choice(N, k, replace=False)) for _ in range(B)]).astype(np.int32)
+        if idx is not None:
+            idx[0, -3:] = [N - 3, N - 2, N - 1]                # batch 0 ends in the tail
+            idx[1] = np.sort(rng.choice(N - 100, k, replace=False))   # batch 1 has no tail row
+        cache = _bf16(rng, (B, N, H, d))
+        rows = _bf16(rng, (B, k, H, d))
+        want_c, want_r = codec.keep_recent(cache, rows, x, idx, tail)
+        dc, dr = up_bf16(cache), up_bf16(rows)
+        F.kv_keep_recent(up_bf16(x), None if idx is None else torch.from_numpy(idx).cuda(), tail, cache=dc, rows=dr)
+        torch.cuda.synchronize()
+        assert np.array_equal(down_bits16(dc), want_c), (k, tail)
+        assert np.array_equal(down_bits16(dr), want_r), (k, tail)
+
+
 def test_codec_kv_pair_empty_selection(F):
     rng = np.random.default_rng(9)
     B, N, H, d = 1, 40, 2, 64
@@ -244,6 +265,9 @@ CHAIN_CASES = [
                 topk_frac=(0.1, 0.08, 0.06, 0.05), bits=(4, 2, 2, 2),
                 col_decay=(4 + 128 + 300, 4 + 128 + 300, 4 + 128 + 150, 4 + 128 + 60))),
     ("C5", dict(seq=1200, heads=2, batch=2, col_budget=200, col_decay=(200, 200, 160, 120, 80, 60, 40))),
+    # the most recent 64 positions stored exactly in bf16 (Appendix E), with a band and with a batch
+    ("C4", dict(seq=2000, heads=2, window=128, col_budget=4 + 128 + 300, tail=64)),
+    ("C5", dict(seq=1200, heads=2, batch=2, col_budget=200, tail=64)),
 ]
 
 
@@ -262,7 +286,7 @@ def test_chain_matches_oracle(F, name, over):
     B, H = w.batch, w.heads
     dev = {n: [up_bf16(a) for a in getattr(st, n)] for n in "qkv"}
     gs = driver.setup(dev["q"][0], dev["k"][0], dev["v"][0], w.base_bits, w.group, w.n_sink, w.top_cols,
-                      w.window)
+                      w.window, tail=w.tail)
     torch.cuda.synchronize()
     assert np.array_equal(down_bits16(gs.k_hat), rec.k_hat1), "base K reconstruction differs"
     assert np.array_equal(down_bits16(gs.v_hat), rec.v_hat1), "base V reconstruction differs"
