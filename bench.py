@@ -418,6 +418,7 @@ def main():
         result["decode"] = decode_bench(w, gs, fl, torch)
     if not args.no_prune:
         result["prune"] = prune_bench(w, gs, dev["q"][w.loops - 1], fl, torch)
+        result["keep_recent"] = tail_bench(w, gs, dev["k"][w.loops - 1], fl, torch)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, st, blas_threads())
     print(json.dumps(result), flush=True)
@@ -514,6 +515,29 @@ def prune_bench(w, gs, q_last, fl, torch):
             "bound": "alu", "achieved": round(achieved, 2), "peak": FP64_VECTOR_TFLOPS, "unit": "TFLOP/s (fp64)",
             "frac": round(achieved / FP64_VECTOR_TFLOPS, 4), "alg_MB": round(nb / 1e6, 2),
             "alg_GF": round(nf / 1e9, 3), "timing": f"HIP events, mean of {reps} calls (two launches each)"}
+
+
+def tail_bench(w, gs, k_last, fl, torch, tail=64):
+    """The recent-token bf16 tail (Appendix E, 64 positions) applied to the cache after the step's last
+    loop, for its active rows; timed with HIP events (the workload itself runs without a tail)."""
+    reps = 20
+    cache = gs.k_hat.clone()
+    for _ in range(2):
+        fl.kv_keep_recent(k_last, gs.cand, tail, cache=cache)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        fl.kv_keep_recent(k_last, gs.cand, tail, cache=cache)
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) / reps * 1e3
+    B, N, H, d = cache.shape
+    idx = gs.cand.cpu().numpy()
+    n_tail = int(np.sum(idx >= N - tail))
+    nb = n_tail * H * d * 2 * 2 + B * min(idx.shape[1], tail) * 4
+    return {"workload": f"{w.name} tail {tail}: {n_tail} active tail rows of one tensor", "us": round(us, 2),
+            "alg_KB": round(nb / 1e3, 2), "timing": f"HIP events, mean of {reps} calls (launch-bound)"}
 
 
 if __name__ == "__main__":
