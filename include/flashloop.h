@@ -271,7 +271,8 @@ int fl_column_scores(const uint16_t* q, const uint16_t* k_cache, int B, int N, i
  * (5) Column list -- Appendix D.2, Eq. 6: S = {0 .. n_sink-1} U TopK_t(col_key over j >= n_sink),
  * ties broken by the lower column index, emitted ascending.
  *   col_key : fp32 [B, H, N];  cols : int32 [B, H, ns + t] with ns = min(n_sink, N);
- *   0 <= t <= N - ns, else FL_E_RANGE;  N - ns <= 65536.
+ *   0 <= t <= N - ns, else FL_E_RANGE;  N - ns <= 65536.  An empty list (ns + t = 0) writes nothing and
+ *   takes NULL pointers.
  * ---------------------------------------------------------------------------------------------- */
 int fl_select_columns(const float* col_key, int B, int H, int N, int n_sink, int t,
                       int32_t* cols, void* stream);

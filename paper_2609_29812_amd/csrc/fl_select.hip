@@ -481,13 +481,13 @@ extern "C" int fl_select_tokens(const uint16_t* k_cur, const uint16_t* k_prev,
 extern "C" int fl_select_columns(const float* col_key, int B, int H, int N, int n_sink, int t,
                                  int32_t* cols, void* stream) {
   FL_API_BEGIN
-  FL_REQUIRE(col_key && cols, FL_E_NULL, "fl_select_columns: col_key and cols are required");
   FL_REQUIRE(B >= 1 && H >= 1 && N >= 1, FL_E_SHAPE, "fl_select_columns: need B, H, N >= 1");
   FL_REQUIRE(n_sink >= 0, FL_E_RANGE, "fl_select_columns: n_sink must be >= 0");
   const int ns = n_sink < N ? n_sink : N;
   FL_REQUIRE(t >= 0 && t <= N - ns, FL_E_RANGE, "fl_select_columns: t=%d outside [0, N - n_sink]", t);
   FL_REQUIRE(N - ns <= 65536, FL_E_SHAPE, "fl_select_columns: N - n_sink exceeds 65536");
-  if (ns + t == 0) return FL_OK;
+  if (ns + t == 0) return FL_OK;          // an empty list: nothing to write (cols may be NULL)
+  FL_REQUIRE(col_key && cols, FL_E_NULL, "fl_select_columns: col_key and cols are required");
   return launch_topk(B * H, col_key + ns, N, N - ns, t, nullptr, 0, ns, cols, ns + t, ns, nullptr, 0,
                      as_stream(stream));
   FL_API_END

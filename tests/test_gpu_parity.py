@@ -366,7 +366,10 @@ def test_sparse_attn_stepwise_from_oracle_state(F, name, over):
                                        # record-table kernel), with and without a band
                                        ("C5", dict(seq=4000, heads=2, col_budget=3072)),
                                        ("C5", dict(seq=4500, heads=2, col_budget=3300)),
-                                       ("C4", dict(seq=5000, heads=2, window=256, col_budget=4 + 256 + 3200))])
+                                       ("C4", dict(seq=5000, heads=2, window=256, col_budget=4 + 256 + 3200)),
+                                       # the band alone (an empty list), and fewer rows than one 64-row tile
+                                       ("C4", dict(seq=1500, heads=2, window=128, n_sink=0, col_budget=128)),
+                                       ("C4", dict(seq=600, heads=2, window=64, col_budget=4 + 64 + 50))])
 def test_reused_subtract_terms_match_recomputed_ones(F, name, over):
     """Loops >= 3 with the previous loop's add terms as subtract terms against the same loops with the
     subtract pass recomputed: equal up to fp32 rounding (Eq. 7 with fixed S and nested rows)."""
