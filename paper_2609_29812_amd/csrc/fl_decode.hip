@@ -143,11 +143,18 @@ __global__ __launch_bounds__(256) void decode_partial_kernel(DecodeArgs a) {
   mx = fmax(fmax(s_red[0], s_red[1]), fmax(s_red[2], s_red[3]));
   __syncthreads();
   // pass 2: exp-weights against the chunk max, exp-sum and the weighted V rows
+  // (every lane of a row group holds the same logits: lane sl of the group takes the exponential of the
+  // group's position sl and the group shares them by shuffles, one fp64 exp per lane instead of IT)
+  static_assert(IT <= LPC, "one position per lane of a row group");
+  double mine = 0.0;
+#pragma unroll
+  for (int it = 0; it < IT; ++it) mine = sl % IT == it ? lg[it] : mine;
+  mine = exp(mine - mx);                        // 0 for positions past the end
   double es = 0.0;
   float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
 #pragma unroll
   for (int it = 0; it < IT; ++it) {
-    const double e = exp(lg[it] - mx);          // 0 for positions past the end
+    const double e = __shfl(mine, grp * LPC + it, 64);
     if (sl == 0) es += e;
     const float wf = (float)e;
     const uint4 w = vw[it];
