@@ -37,6 +37,7 @@ class LoopRecord:
     lse: dict                 # (b, h) -> float64 [N]
     mass: dict                # (b, h) -> float64 [N] (nan where not updated)
     cols_next: dict = None    # (b, h) -> int32 list pruned after this loop for a smaller budget, if any
+    stat_next: dict = None    # (b, h) -> float64 statistic of the non-sink entries that ranked cols_next
 
 
 @dataclass
@@ -148,12 +149,13 @@ def run_layer(states, heads=None, rows=None, cols=None):
             # a smaller budget next loop: prune each list by this loop's statistic (Section 4.2), with the
             # reference log-normalisers as the state stores them (fp32)
             assert rows is None, "pruning needs every updated row's log-normaliser"
-            lr.cols_next = {}
+            lr.cols_next, lr.stat_next = {}, {}
             for b in range(w.batch):
                 for h in rec.heads:
                     lse32 = lse[b, h].astype(np.float32).astype(np.float64)
                     stat = prune.column_mass(cols_r[b, h], lr.idx[b], _f64(states.q[r - 1], b, h),
                                              _f64(k_hat, b, h), lse32, w.sm_scale, w.n_sink)
+                    lr.stat_next[b, h] = stat
                     lr.cols_next[b, h] = prune.prune_columns(cols_r[b, h], stat, w.n_sink, w.top_cols_at(r + 1))
             cols_r.update(lr.cols_next)
     rec.k_hat, rec.v_hat = k_hat, v_hat

@@ -82,3 +82,66 @@ def test_loop_over_the_pruned_list_with_an_unchanged_state_is_the_identity():
         np.testing.assert_allclose(o3, o[i], rtol=0, atol=1e-13)
         # the kept mass is the sum of the row's loop-2 probabilities over the pruned set
         assert abs(m3 - np.exp(sc * (k1[S2] @ q1[i]) - lse[i]).sum()) < 1e-14
+
+
+def _brute_stat(cols, ns, rows, q, k, lse32, sc):
+    """The statistic written out entry by entry: for list entry j, the sum over updated rows i >= j of
+    exp(sc * q_i . k_j - lse_i) (a scalar loop, no shared helper)."""
+    out = []
+    for j in cols[ns:]:
+        s = 0.0
+        for i in rows:
+            if i >= j:
+                s += float(np.exp(sc * float(np.dot(q[i], k[j])) - lse32[i]))
+        out.append(s)
+    return np.array(out)
+
+
+def test_run_layer_prunes_with_loop_r_queries_keys_and_stored_lse():
+    """run_layer's pruning branch (Section 4.2) wired by hand: after sparse loop r the statistic uses loop
+    r's queries Q^(r), its reconstructed keys K_hat^(r), and lse_ref after loop r as the state stores it
+    (fp32); the list is then the sinks plus the top t_(r+1) entries by fp32 statistic, ties to the lower
+    column.  The hand-wired chain advances with chain.loop1 / chain.sparse_loop (pinned elsewhere) and
+    computes the statistic and ranking by brute force, so a wrong loop's queries or keys, an fp64
+    log-normaliser, or a skipped pruning changes the statistic beyond the 1e-12 bound."""
+    from oracle import chain
+    from workloads import get, make_layer
+
+    w = get("C5").replace(name="prune-wiring", batch=2, seq=160, heads=2, head_dim=32, loops=4,
+                          hot_frac=(0.4, 0.3, 0.2), topk_frac=(0.45, 0.35, 0.25), col_budget=48, window=8,
+                          col_decay=(48, 36, 24), bits=(4, 4, 2), group=16, delta="normal", hot_scale=0.5)
+    st = make_layer(w)
+    rec = chain.run_layer(st)
+    # hand-wired chain
+    ref = chain.loop1(st)
+    o = {key: val.copy() for key, val in ref.o1.items()}
+    lse = {key: val.copy() for key, val in ref.lse1.items()}
+    k_hat, v_hat, cand, cols_r = ref.k_hat1, ref.v_hat1, None, dict(ref.cols)
+    pruned = 0
+    for r in range(2, w.loops + 1):
+        lr, k_hat, v_hat = chain.sparse_loop(st, r, cand, k_hat, v_hat, cols_r, o, lse, ref.heads)
+        got = rec.loops[r - 2]
+        np.testing.assert_array_equal(got.idx, lr.idx)
+        cand = lr.idx
+        t_next = w.top_cols_at(r + 1) if r < w.loops else None
+        if t_next is None or t_next >= w.top_cols_at(r):
+            assert got.cols_next is None
+            continue
+        for b in range(w.batch):
+            for h in ref.heads:
+                q = bf16_to_f64(st.q[r - 1][b, :, h, :])
+                kk = bf16_to_f64(k_hat[b, :, h, :])
+                lse32 = lse[b, h].astype(np.float32).astype(np.float64)
+                ns = min(w.n_sink, len(cols_r[b, h]))
+                stat = _brute_stat(cols_r[b, h], ns, lr.idx[b], q, kk, lse32, w.sm_scale)
+                np.testing.assert_allclose(got.stat_next[b, h], stat, rtol=1e-12, atol=1e-300)
+                js = [int(j) for j in cols_r[b, h][ns:]]
+                order = sorted(range(len(js)), key=lambda e: (-float(np.float32(stat[e])), js[e]))[:t_next]
+                want = [int(j) for j in cols_r[b, h][:ns]] + sorted(js[e] for e in order)
+                assert got.cols_next[b, h].tolist() == want
+                cols_r[b, h] = np.asarray(want, dtype=np.int32)
+                pruned += 1
+    assert pruned == 2 * w.batch * w.heads
+    # and the final outputs of both chains agree (the pruned lists were used by the loops after)
+    for key in o:
+        np.testing.assert_allclose(rec.loops[-1].o[key], o[key], rtol=0, atol=1e-12)
