@@ -309,6 +309,25 @@ int fl_decode_step(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v
                    int32_t* cols_next, float* mass_next, float* sub_next, void* ws, size_t ws_bytes,
                    void* stream);
 
+/* (6b) The decode step without a workspace argument, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).  Arguments and
+ * results are those of fl_decode_step; the workspace is a library-owned device array of
+ * FL_DECODE_SCRATCH_BYTES per GPU (allocated with the code object when the library is loaded on that
+ * GPU, held until the process ends).  The call itself allocates and frees nothing.
+ *   - FL_E_RANGE when fl_decode_step_ws(B, T, H, d, c, c_next) exceeds FL_DECODE_SCRATCH_BYTES (32 MiB:
+ *     about 1.9 million (batch, head, position) entries in a dense loop, e.g. B = 1, H = 16, T = 64K).
+ *   - Every call on one GPU shares that GPU's array: calls that overlap on one GPU (two streams, two
+ *     threads) race on it and must be ordered by the caller.  Nothing in the array needs clearing between
+ *     calls; the last call's contents stay there.
+ *   - The first call on a device looks up that device's copy of the array (hipGetSymbolAddress); the
+ *     current device must be the one `stream` belongs to. */
+#define FL_DECODE_SCRATCH_BYTES (32u << 20)
+
+int fl_decode_step_noalloc(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                           const int32_t* cols, int c, const float* mass, const float* sub, int B, int T, int H,
+                           int d, float sm_scale, float* o, float* lse, int n_sink, int window, int c_next,
+                           int32_t* cols_next, float* mass_next, float* sub_next, void* stream);
+
 /* ------------------------------------------------------------------------------------------------
  * (7) Pruning the column list for a smaller budget -- Section 4.2 (later loops with smaller budgets
  * prune the selected set by the preceding sparse loop's attention statistics) and Appendix D.2, Eq. 6

@@ -19,6 +19,8 @@
 //                   mass and subtract term; then one workgroup per (b, h) adds the parts in order.
 #include "fl_common.h"
 
+#include <mutex>
+
 namespace fl {
 
 constexpr int kDecChunk = 128;           // positions per partial workgroup
@@ -351,13 +353,14 @@ extern "C" size_t fl_decode_step_ws(int B, int T, int H, int d, int c, int c_nex
   return decode_ws(B, H, d, n, c_next).total;
 }
 
-extern "C" int fl_decode_step(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
-                              const int32_t* cols, int c, const float* mass, const float* sub, int B, int T,
-                              int H, int d, float sm_scale, float* o, float* lse, int n_sink, int window,
-                              int c_next, int32_t* cols_next, float* mass_next, float* sub_next, void* ws,
-                              size_t ws_bytes, void* stream) {
-  FL_API_BEGIN
-  const char* fn = "fl_decode_step";
+static int decode_scratch(void** out);
+
+// ws == nullptr with use_scratch: the library's own scratch array, looked up after the arguments pass
+static int decode_step(const char* fn, bool use_scratch, const uint16_t* q, const uint16_t* k_cache,
+                       const uint16_t* v_cache, const int32_t* cols, int c, const float* mass, const float* sub,
+                       int B, int T, int H, int d, float sm_scale, float* o, float* lse, int n_sink, int window, int c_next,
+                       int32_t* cols_next, float* mass_next, float* sub_next, void* ws, size_t ws_bytes,
+                       void* stream) {
   FL_REQUIRE(q && k_cache && v_cache && o, FL_E_NULL, "%s: q, k_cache, v_cache and o are required", fn);
   FL_REQUIRE(B >= 1 && T >= 1 && H >= 1, FL_E_SHAPE, "%s: need B, T, H >= 1", fn);
   FL_REQUIRE(d == 64 || d == 128, FL_E_SHAPE, "%s: head dim %d not in {64, 128}", fn, d);
@@ -377,6 +380,14 @@ extern "C" int fl_decode_step(const uint16_t* q, const uint16_t* k_cache, const 
              "%s: cols_next, mass_next and sub_next are required when c_next > 0", fn);
   FL_REQUIRE(n_sink >= 0 && window >= 0, FL_E_RANGE, "%s: n_sink and window must be >= 0", fn);
   const DecodeWs L = decode_ws(B, H, d, n, c_next);
+  if (use_scratch) {
+    FL_REQUIRE(L.total <= (size_t)FL_DECODE_SCRATCH_BYTES, FL_E_RANGE,
+               "%s: the step needs %zu bytes of scratch, above the %zu available (use fl_decode_step with a "
+               "workspace)", fn, L.total, (size_t)FL_DECODE_SCRATCH_BYTES);
+    const int rc = decode_scratch(&ws);
+    if (rc != FL_OK) return rc;
+    ws_bytes = (size_t)FL_DECODE_SCRATCH_BYTES;
+  }
   FL_REQUIRE(ws && ws_bytes >= L.total, FL_E_WORKSPACE, "%s: workspace of %zu bytes required", fn, L.total);
   hipStream_t st = as_stream(stream);
   char* base = static_cast<char*>(ws);
@@ -415,5 +426,57 @@ extern "C" int fl_decode_step(const uint16_t* q, const uint16_t* k_cache, const 
   if (d == 128) decode_select_reduce_kernel<128><<<BH, 256, 0, st>>>(a);
   else decode_select_reduce_kernel<64><<<BH, 256, 0, st>>>(a);
   return check_launch("decode_select_reduce_kernel");
+}
+
+extern "C" int fl_decode_step(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                              const int32_t* cols, int c, const float* mass, const float* sub, int B, int T,
+                              int H, int d, float sm_scale, float* o, float* lse, int n_sink, int window,
+                              int c_next, int32_t* cols_next, float* mass_next, float* sub_next, void* ws,
+                              size_t ws_bytes, void* stream) {
+  FL_API_BEGIN
+  return decode_step("fl_decode_step", false, q, k_cache, v_cache, cols, c, mass, sub, B, T, H, d, sm_scale, o, lse,
+                     n_sink, window, c_next, cols_next, mass_next, sub_next, ws, ws_bytes, stream);
+  FL_API_END
+}
+
+// ---- the decode step without a caller workspace ----------------------------------------------------------
+// The workspace lives in a file-scope device array of FL_DECODE_SCRATCH_BYTES, one copy per GPU, held
+// until the process ends.  Host code never passes the array's name to a kernel (on the host it is only a
+// stand-in for the symbol): the device address of each GPU's copy is looked up once with
+// hipGetSymbolAddress, with that GPU current, and that address is what the kernels receive.  Every region
+// of the workspace is written before it is read within one call, so nothing needs clearing between calls.
+static __device__ __align__(256) unsigned char scratch[FL_DECODE_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+}  // namespace
+
+static int decode_scratch(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  FL_REQUIRE(e == hipSuccess && dev >= 0 && dev < kMaxDevices, FL_E_HIP,
+             "fl_decode_step_noalloc: no current device (%s)", hipGetErrorString(e));
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    FL_REQUIRE(e == hipSuccess && p != nullptr, FL_E_HIP,
+               "fl_decode_step_noalloc: hipGetSymbolAddress failed on device %d (%s)", dev, hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return FL_OK;
+}
+
+extern "C" int fl_decode_step_noalloc(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                                      const int32_t* cols, int c, const float* mass, const float* sub, int B,
+                                      int T, int H, int d, float sm_scale, float* o, float* lse, int n_sink,
+                                      int window, int c_next, int32_t* cols_next, float* mass_next,
+                                      float* sub_next, void* stream) {
+  FL_API_BEGIN
+  return decode_step("fl_decode_step_noalloc", true, q, k_cache, v_cache, cols, c, mass, sub, B, T, H, d, sm_scale,
+                     o, lse, n_sink, window, c_next, cols_next, mass_next, sub_next, nullptr, 0, stream);
   FL_API_END
 }

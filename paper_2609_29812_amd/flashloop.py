@@ -56,6 +56,8 @@ _SIGNATURES = {
     "fl_decode_step_ws": (_c_sz, [_c_i, _c_i, _c_i, _c_i, _c_i, _c_i]),
     "fl_decode_step": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_i, _c_p, _c_p, _c_i, _c_i, _c_i, _c_i, _c_f, _c_p, _c_p,
                               _c_i, _c_i, _c_i, _c_p, _c_p, _c_p, _c_p, _c_sz, _c_p]),
+    "fl_decode_step_noalloc": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_i, _c_p, _c_p, _c_i, _c_i, _c_i, _c_i, _c_f, _c_p,
+                                      _c_p, _c_i, _c_i, _c_i, _c_p, _c_p, _c_p, _c_p]),
     "fl_prune_columns_ws": (_c_sz, [_c_i, _c_i, _c_i, _c_i, _c_i]),
     "fl_kv_keep_recent": (_c_i, [_c_p, _c_p, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_p, _c_p, _c_p]),
     "fl_prune_columns": (_c_i, [_c_p, _c_p, _c_p, _c_i, _c_p, _c_i, _c_p, _c_i, _c_i, _c_i, _c_i, _c_d, _c_i, _c_i,
@@ -363,10 +365,15 @@ def select_columns(col_key, n_sink, t):
 
 
 # ---- (6) decode ---------------------------------------------------------------------------------------
-def decode_step(q, k_cache, v_cache, cols, mass, sub, o, c_next, n_sink=0, window=0, sm_scale=None, lse=None):
-    """One loop of the decode position T-1.  q bf16 [B, H, d]; caches bf16 [B, T, H, d]; cols int32 [B, H, c]
-    (or None for a dense source loop, then mass and sub are unused); o fp32 [B, H, d] updated in place.
-    Returns (cols_next [B, H, c_next], mass_next [B, H], sub_next [B, H, d]) or Nones when c_next == 0."""
+def decode_ws(k_cache, cols, c_next):
+    """A workspace for decode_step over these shapes (reusable across calls of the same or smaller size)."""
+    B, T, H, d = k_cache.shape
+    c = 0 if cols is None else cols.shape[2]
+    need = load().fl_decode_step_ws(B, T, H, d, c, c_next)
+    return torch.empty(max(need, 1), dtype=torch.uint8, device=k_cache.device)
+
+
+def _decode_args(q, k_cache, v_cache, cols, mass, sub, o, c_next, lse, out):
     B, T, H, d = k_cache.shape
     _dev(q, torch.bfloat16, "q", (B, H, d))
     _dev(k_cache, torch.bfloat16, "k_cache")
@@ -378,20 +385,53 @@ def decode_step(q, k_cache, v_cache, cols, mass, sub, o, c_next, n_sink=0, windo
         _dev(mass, torch.float32, "mass", (B, H))
         _dev(sub, torch.float32, "sub", (B, H, d))
     _dev(lse, torch.float32, "lse", (B, H))
-    dev = q.device
     cols_next = mass_next = sub_next = None
     if c_next > 0:
-        cols_next = torch.empty(B, H, c_next, dtype=torch.int32, device=dev)
-        mass_next = torch.empty(B, H, dtype=torch.float32, device=dev)
-        sub_next = torch.empty(B, H, d, dtype=torch.float32, device=dev)
+        if out is None:
+            dev = q.device
+            out = (torch.empty(B, H, c_next, dtype=torch.int32, device=dev),
+                   torch.empty(B, H, dtype=torch.float32, device=dev),
+                   torch.empty(B, H, d, dtype=torch.float32, device=dev))
+        cols_next, mass_next, sub_next = out
+        _dev(cols_next, torch.int32, "cols_next", (B, H, c_next))
+        _dev(mass_next, torch.float32, "mass_next", (B, H))
+        _dev(sub_next, torch.float32, "sub_next", (B, H, d))
+    return B, T, H, d, c, cols_next, mass_next, sub_next
+
+
+def decode_step(q, k_cache, v_cache, cols, mass, sub, o, c_next, n_sink=0, window=0, sm_scale=None, lse=None,
+                out=None, ws=None):
+    """One loop of the decode position T-1.  q bf16 [B, H, d]; caches bf16 [B, T, H, d]; cols int32 [B, H, c]
+    (or None for a dense source loop, then mass and sub are unused); o fp32 [B, H, d] updated in place.
+    out: optional (cols_next, mass_next, sub_next) to write into; ws: optional workspace (decode_ws).  With
+    both given nothing is allocated.  Returns (cols_next [B, H, c_next], mass_next [B, H], sub_next
+    [B, H, d]) or Nones when c_next == 0."""
+    B, T, H, d, c, cols_next, mass_next, sub_next = _decode_args(q, k_cache, v_cache, cols, mass, sub, o, c_next,
+                                                                 lse, out)
     sm_scale = 1.0 / math.sqrt(d) if sm_scale is None else sm_scale
     lib = load()
     need = lib.fl_decode_step_ws(B, T, H, d, c, c_next)
-    ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    if ws is None:
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+    _dev(ws, torch.uint8, "ws")
     rc = lib.fl_decode_step(_p(q), _p(k_cache), _p(v_cache), _p(cols), c, _p(mass), _p(sub), B, T, H, d, sm_scale,
                             _p(o), _p(lse), n_sink, window, c_next, _p(cols_next), _p(mass_next), _p(sub_next),
-                            _p(ws), need, _stream())
+                            _p(ws), ws.numel(), _stream())
     _check(rc, "fl_decode_step")
+    return cols_next, mass_next, sub_next
+
+
+def decode_step_noalloc(q, k_cache, v_cache, cols, mass, sub, o, c_next, out=None, n_sink=0, window=0,
+                        sm_scale=None, lse=None):
+    """decode_step without a caller workspace: the library's own device scratch serves as the workspace
+    (calls overlapping on one GPU race on it).  Nothing is allocated when `out` is given (or c_next == 0)."""
+    B, T, H, d, c, cols_next, mass_next, sub_next = _decode_args(q, k_cache, v_cache, cols, mass, sub, o, c_next,
+                                                                 lse, out)
+    sm_scale = 1.0 / math.sqrt(d) if sm_scale is None else sm_scale
+    rc = load().fl_decode_step_noalloc(_p(q), _p(k_cache), _p(v_cache), _p(cols), c, _p(mass), _p(sub), B, T, H, d,
+                                       sm_scale, _p(o), _p(lse), n_sink, window, c_next, _p(cols_next),
+                                       _p(mass_next), _p(sub_next), _stream())
+    _check(rc, "fl_decode_step_noalloc")
     return cols_next, mass_next, sub_next
 
 

@@ -162,3 +162,21 @@ def test_decode_workspace_and_argument_checks(lib):
     assert dec(ws=None) == FL_E_WORKSPACE
     assert dec(wsb=ctypes.c_size_t(16)) == FL_E_WORKSPACE
     assert b"fl_decode_step" in lib.fl_last_error()
+
+
+def test_decode_noalloc_argument_checks(lib):
+    # the same host-side checks as fl_decode_step, before the scratch array is looked up, plus its size limit
+    assert lib.fl_decode_step_ws(1, 8192, 16, 128, 0, 2048) <= 32 << 20      # a dense 8K step fits
+    assert lib.fl_decode_step_ws(4, 65536, 16, 128, 0, 2048) > 32 << 20      # B * H * T = 4M does not
+
+    def dec(**kw):
+        return lib.fl_decode_step_noalloc(
+            kw.get("q", DUMMY), DUMMY, DUMMY, kw.get("cols"), kw.get("c", 0), kw.get("mass"), kw.get("sub"),
+            kw.get("B", 1), kw.get("T", 64), kw.get("H", 2), kw.get("d", 64), ctypes.c_float(0.125), DUMMY, None,
+            4, 8, kw.get("c_next", 16), kw.get("cn", DUMMY), DUMMY, DUMMY, None)
+    assert dec(q=None) == FL_E_NULL
+    assert dec(d=96) == FL_E_SHAPE
+    assert dec(c=5) == FL_E_SHAPE
+    assert dec(cn=None) == FL_E_NULL
+    assert dec(B=64, T=65536, H=16, d=128) == FL_E_RANGE                     # beyond the scratch array
+    assert b"scratch" in lib.fl_last_error()
