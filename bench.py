@@ -359,7 +359,7 @@ def main():
         attn_bytes += by
         attn_flops += fl_
         attn_us += dur_us[f"attn r{r}"]
-        kname = "loop_attn_kernel" if r == 2 else "cur_attn_kernel"
+        kname = "loop_attn_kernel" if r == 2 else "seg_cur_kernel"
         acc = per_kernel.setdefault(kname, [0.0, 0.0, 0.0, 0])
         acc[0] += by
         acc[1] += fl_

@@ -22,7 +22,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libflashloop.so")
 
-SOURCES = ["fl_common.hip", "fl_select.hip", "fl_codec.hip", "fl_attn.hip", "fl_colscore.hip", "fl_decode.hip"]
+SOURCES = ["fl_common.hip", "fl_select.hip", "fl_codec.hip", "fl_attn.hip", "fl_seg_attn.hip", "fl_colscore.hip", "fl_decode.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

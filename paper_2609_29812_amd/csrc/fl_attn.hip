@@ -28,18 +28,15 @@
 // operand of O^T += V^T P^T (v_mfma_f32_32x32x16_f16, P in fp16).
 //   subtract pass : pp = exp(a - lse_ref), no running max needed (lse_ref bounds the logits);
 //   add pass      : online softmax with a running max shared by the two half-waves of a row.
-#include "fl_common.h"
+#include "fl_attn_util.h"
 
-#include <climits>
+#include <algorithm>
+
 #include <type_traits>
 
 namespace fl {
 
-constexpr int kBN = 32;            // columns per tile
 constexpr int kRing = 4;           // LDS ring slots
-// cache policy of the tile loads: non-temporal (the "nt" bit, 2 on gfx950); measured a few percent
-// faster than the default policy on the 32K workload
-constexpr int kDmaPolicy = 2;
 
 struct AttnArgs {
   const uint16_t* q_cur;
@@ -67,75 +64,6 @@ struct AttnArgs {
   int cache_current;         // reuse: the caches already hold X_hat^(r) of the updated rows (no new rows)
   float pinf;                // +inf
 };
-
-typedef __amdgpu_buffer_rsrc_t rsrc_t;
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef short i16x4 __attribute__((ext_vector_type(4)));
-typedef short i16x8 __attribute__((ext_vector_type(8)));
-typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
-typedef float f32x2 __attribute__((ext_vector_type(2)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-constexpr uint32_t kOOB = 0x80000000u;   // beyond every descriptor's range (ranges stay <= 2^31)
-constexpr int kPad = INT_MAX;            // column id of a padding entry: fails every visibility test
-#define FL_LDS(p) ((__attribute__((address_space(3))) void*)(p))
-#define FL_LDS4(p) ((__attribute__((address_space(3))) i16x4*)(p))
-
-__device__ __forceinline__ rsrc_t make_rsrc(const void* p, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
-}
-
-// s_waitcnt vmcnt(n) with every other counter left alone (gfx9 encoding).
-#define FL_WAIT_VM(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (7 << 4) | (15 << 8) | ((((n) >> 4) & 3) << 14))
-// LDS traffic done, then a workgroup barrier without a memory fence (LDS-DMA waits are explicit).
-__device__ __forceinline__ void lds_barrier() {
-  __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
-  __builtin_amdgcn_s_barrier();
-}
-
-__device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){a, b}, f16x2));
-}
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-// two fp32 values to bf16 (round to nearest even), packed low | high << 16
-__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){a, b}, bf16x2));
-}
-
-// max / sum of a lane and lane ^ 32 (the two half-waves hold disjoint columns of the same row)
-__device__ __forceinline__ float xor32_max(float x) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-__device__ __forceinline__ float xor32_add(float x) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-
-// One ring slot: the LDS-DMA target of one tile.  Column ids and flags live in separate arrays (never
-// a DMA target), so the compiler's LDS-DMA tracking does not order them behind pending tile loads.
-template <int D>
-struct Slot {
-  uint16_t k[kBN * D];     // row c at c*D, 16-byte chunks permuted (swz16_f, swz32_f)
-  uint16_t v[kBN * D];     // same layout; converted in place from bf16 to fp16 before use
-};
-
-// Tile rows in LDS: the 16-byte chunk ch of row c sits at chunk position ch ^ g(c) (the LDS-DMA lanes
-// fetch their global chunks in that order).  LDS reads are served 256 bytes (64 banks, 16 groups of 16
-// bytes) at a time, so g spreads the rows one read instruction touches over the 16 groups.  For the
-// 16x16x32 kernels: g is a bijection on 16 consecutive rows (the K reads: 16 rows x 16 B) whose halves
-// g(c) >> 1 are distinct on 8 consecutive rows (the transposed V reads: 8 rows x 32 B).
-template <int D>
-__device__ __forceinline__ int swz16_f(int c) {
-  if constexpr (D == 128) return ((c & 7) << 1) | ((c >> 3) & 1);
-  else return (((c >> 1) & 3) << 1) | ((c >> 3) & 1);   // 128-byte rows: two rows share a 256-byte line
-}
-// For the 32x32x16 reads of loop_attn_kernel: a bijection on 16 consecutive rows (K: 16 rows x 16 B) whose
-// quarters g(c) >> 2 are distinct on 4 consecutive rows (transposed V: 4 rows x 64 B).
-template <int D>
-__device__ __forceinline__ int swz32_f(int c) {
-  if constexpr (D == 128) return ((c & 3) << 2) | ((c >> 2) & 3);
-  else return (((c >> 1) & 1) << 2) | ((c >> 2) & 3);
-}
 
 // MODE: kDense (loop 1, every row over all causal columns) or kFull (a sparse loop with both passes).
 constexpr int kDense = 0, kFull = 1;
@@ -684,17 +612,6 @@ __global__ __launch_bounds__(256, 2) void loop_attn_kernel(AttnArgs a) {
 // and lo = bf16(p - hi), so p.v takes two bf16 MFMAs and P keeps about 16 significant bits.
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ float xor16_max(float x) {
-  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-__device__ __forceinline__ float xor16_add(float x) {
-  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-// max / sum over the four 16-lane rows of the wave (the lanes that hold one query row)
-__device__ __forceinline__ float row4_max(float x) { return xor32_max(xor16_max(x)); }
-__device__ __forceinline__ float row4_add(float x) { return xor32_add(xor16_add(x)); }
 
 // CUR: the caches already hold this loop's rows (no new-row tiles and no updated columns), so tiles are
 // described straight from the column list and the band range, without the prep kernel's records.
@@ -1152,9 +1069,6 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
 // online softmax and the epilogue are those of reuse_attn_kernel.
 constexpr int kListCap = 3072;
 
-// max(x, y) for non-NaN inputs (-inf included) as a median with +inf; pinf holds +inf as a kernel
-// argument, so the median is not folded back into a maximum with its NaN-quieting steps
-__device__ __forceinline__ float fmax_nn(float x, float y, float pinf) { return __builtin_amdgcn_fmed3f(x, y, pinf); }
 
 template <int D>
 __global__ __launch_bounds__(256, 2) void cur_attn_kernel(AttnArgs a) {
@@ -1555,16 +1469,18 @@ static RecLayout rec_layout(int B, int N, int H, int k, int c_list) {
   return L;
 }
 
-static size_t attn_ws_bytes(int B, int N, int H, int k, int c_list, bool dense) {
+// the larger of the tile records (prep kernel) and, with a band, the segment kernel's per-row parts
+static size_t attn_ws_bytes(int B, int N, int H, int d, int k, int c_list, int window, bool dense) {
   if (dense || B < 1 || N < 1 || H < 1 || k < 0 || c_list < 0) return 0;
   const RecLayout L = rec_layout(B, N, H, k, c_list);
-  return L.n_rec * sizeof(int2) + (size_t)B * H * sizeof(int32_t);
+  const size_t rec = L.n_rec * sizeof(int2) + (size_t)B * H * sizeof(int32_t);
+  const size_t part = window > 0 && (d == 64 || d == 128) ? seg_part_bytes(B, H, d, k) : 0;
+  return std::max(rec, part);
 }
 
 extern "C" size_t fl_loop_sparse_attn_ws(int B, int N, int H, int d, int k, int c_list, int window,
                                          int flags) {
-  (void)d; (void)window;
-  return attn_ws_bytes(B, N, H, k, c_list, (flags & FL_ATTN_DENSE) != 0);
+  return attn_ws_bytes(B, N, H, d, k, c_list, window, (flags & FL_ATTN_DENSE) != 0);
 }
 
 static int loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev, const uint16_t* k_cache,
@@ -1605,7 +1521,7 @@ static int loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev, const
       FL_REQUIRE(k_prev >= k && k_prev <= N, FL_E_RANGE, "fl_loop_sparse_attn: k_prev=%d outside [k, N]", k_prev);
     }
   }
-  const size_t need = attn_ws_bytes(B, N, H, k, c_list, dense);
+  const size_t need = attn_ws_bytes(B, N, H, d, k, c_list, window, dense);
   FL_REQUIRE(dense || rec_layout(B, N, H, k, c_list).n_rec * sizeof(int2) <= ((size_t)1 << 31) - 8, FL_E_SHAPE,
              "fl_loop_sparse_attn: tile records above 2^31 bytes (reduce B * H * c_list + B * (N + k))");
   FL_REQUIRE(need == 0 || (ws && ws_bytes >= need), FL_E_WORKSPACE,
@@ -1670,6 +1586,11 @@ static int loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev, const
     return check_launch("loop_attn_kernel");
   }
 #define FL_REUSE(DD, CC) reuse_attn_kernel<DD, CC><<<grid, 256, 0, st>>>(a)
+  if (a.cache_current) {
+    const int rc = launch_seg_cur(q_cur, k_cache, v_cache, rows, k, cols, c_list, window, B, N, H, d, sm_scale, lse_ref,
+                                  o, term_prev, mass_prev, slot_prev, k_prev, term_out, mass_out, ws, st);
+    if (rc != FL_E_UNSUPPORTED) return rc;
+  }
   if (a.cache_current && c_list <= kListCap) {
     if (d == 128) cur_attn_kernel<128><<<grid, 256, 0, st>>>(a);
     else cur_attn_kernel<64><<<grid, 256, 0, st>>>(a);

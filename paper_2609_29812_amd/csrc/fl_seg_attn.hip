@@ -1,0 +1,687 @@
+// Mass-corrected sparse attention update over row segments (Appendix D.2, Eq. 7; Sections 3.2, 4.2) for a
+// loop whose subtract term is the previous loop's stored add term and whose caches already hold this
+// loop's state: the add pass alone,
+//   L_i = log sum_{j in S_i} exp(l_ij),  add_i = sum_j exp(l_ij - L_i) v_j,  l_ij = sigma q_i . k_j,
+//   o_i <- o_i - term_prev_i + m_i add_i,   lse_ref_i <- L_i - log m_i,
+// over S_i = (list U {j : i - w < j <= i}) restricted to j <= i, list columns taking the condition
+// j + w <= i so that a column in both is counted once.
+//
+// Work decomposition.  One workgroup of 8 waves takes a segment of up to 128 consecutive updated rows of
+// one (batch, head).  The rows form eight 16-row groups; wave (team t, index w) holds groups w and w + 4
+// (query fragments, running maxima, sums and output blocks of both), so one K/V fragment read from LDS
+// feeds two groups.  The column tiles of the segment -- the list entries the segment's last row can see,
+// and the band columns from its first row's band start to its last row -- form one sequence in which
+// list and band tiles are interleaved evenly (the band tiles stream from HBM while the list tiles, shared
+// by every segment of the head and kept in L2, keep the matrix cores busy).  Step s gives tile 2s to team
+// 0 and tile 2s + 1 to team 1; each team keeps its own softmax state, and the two are merged per row at
+// the end.
+//
+// L2 sharing of the band.  Neighbouring segments of a head need the same band columns around their
+// boundary (about w columns).  Each segment walks the band tiles it shares with a neighbour before the
+// rest: even segments the lower shared range first, odd segments the upper one first, so both segments of
+// every boundary reach the shared columns at about the same time.  The segments of one (batch, head) run
+// on one XCD, which holds its L2.
+//
+// Data movement: tiles of 32 columns are gathered by LDS-DMA (buffer_load ... lds) into a ring of four
+// steps (two tiles each) three steps ahead; out-of-range offsets read zeros.  Each wave converts the value
+// rows its own DMA wrote from bf16 to fp16 in place (exact for 2^-14 <= |v| <= 65504; smaller magnitudes
+// round to a multiple of 2^-24; larger ones overflow) before the step's barrier.  Contractions: S^T = K Q^T
+// on v_mfma_f32_16x16x32_bf16 (lane (j, g) holds columns 16c + 4g .. +3 of row j), O^T += V^T P^T on
+// v_mfma_f32_16x16x32_f16 with V read transposed and P rounded to fp16; that lane layout of S^T is the
+// B-operand layout of P^T when the transposed V reads follow the k order (4g .. 4g+3, 16+4g .. 16+4g+3),
+// so P needs no shuffle.  Within a tile the two groups' phases are interleaved in program order (the
+// products of one group between the vector instructions of the other), as a wave issues in order.
+#include "fl_attn_util.h"
+
+#include <algorithm>
+#include <type_traits>
+
+namespace fl {
+
+constexpr int kSegRows = 128;        // rows per segment at most (8 groups of 16)
+constexpr int kSegListCap = 2048;    // list entries kept in LDS
+constexpr int kSegTileCap = 2048;    // tile descriptors kept in LDS (list tiles + band tiles of a segment)
+constexpr int kSegSteps = 4;         // ring depth in steps
+
+struct SegArgs {
+  const uint16_t* q;          // [B, N, H, d] queries of this loop
+  const uint16_t* k_cache;    // [B, N, H, d] this loop's K_hat, V_hat
+  const uint16_t* v_cache;
+  const int32_t* rows;        // [B, k] ascending updated rows
+  const int32_t* cols;        // [B, H, c_list] ascending column list
+  float* lse_ref;             // [B, N, H]
+  float* o;                   // [B, N, H, d]
+  const float* term_prev;     // [B, k_prev, H, d]
+  const float* mass_prev;     // [B, k_prev, H]
+  const int32_t* slot_prev;   // [B, N]
+  float* term_out;            // optional [B, k, H, d]
+  float* mass_out;            // optional [B, k, H]
+  int k, k_prev, c_list, window, B, N, H;
+  int n_seg, seg_rows;        // segments per (batch, head) and rows per segment (<= kSegRows)
+  int split;                  // list and band columns in separate workgroups (a band exists)
+  float* part_acc;            // split: [2][B, k, H, d] unnormalised outputs of the list / band workgroups
+  float* part_st;             // split: [2][B, k, H, 2] their reference (log2 units) and row sum
+  float scale_log2;           // sm_scale * log2(e)
+  float pinf;                 // +inf (a kernel argument, so the median below is not folded into a max)
+};
+
+template <int D>
+__global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
+  constexpr int KS = D / 32;              // k-steps of QK^T (32 dims each)
+  constexpr int DB = D / 16;              // 16-dim output blocks
+  constexpr int CH = D / 8;               // 16-byte chunks per row
+  constexpr int CPI = 64 / CH;            // tile columns covered by one 1 KB LDS-DMA instruction
+  constexpr int IPT = kBN / CPI;          // instructions per tensor and tile
+  constexpr int NIK = IPT / 4;            // K (and V) instructions per wave: a team's 4 waves load its tile
+  constexpr int NI = 2 * NIK;             // VMEM operations per wave and step
+  // The four ring slots and the list are separate LDS objects (a slot holds both teams' tiles): the compiler
+  // then tells every LDS read apart from the LDS-DMA writes still in flight into the other slots (one
+  // object would make it wait for all of them before each read).
+  __shared__ Slot<D> ring0[2], ring1[2], ring2[2], ring3[2];   // step slot s, team t: ring<s>[t]
+  __shared__ __attribute__((aligned(16))) int lst[kSegListCap + kBN];   // the (b, h) list, kPad-padded
+  __shared__ int2 tdesc[kSegTileCap];     // per sequence position: first column or entry, kind, group bits
+  __shared__ int s_grp[16];               // first and last row of each of the 8 groups
+  __shared__ int s_meta[1];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int team = wave >> 2, w4 = wave & 3;
+  const int j16 = lane & 15, g4 = lane >> 4;
+
+  // ---- work item -> (kind, batch*head, segment); the workgroups of one (batch, head) stay on one XCD ----
+  // kind 0 takes the segment's list columns, kind 1 its band columns (split), or kind 0 takes both (a
+  // single workgroup per segment).  The two kinds alternate in dispatch order, so about half of the CUs
+  // stream band columns from HBM while the others work through the lists held in L2.
+  const int n_bh = a.B * a.H;
+  int bh, seg, kind = 0;
+  {
+    int x, s;
+    if ((n_bh & 7) == 0) { x = blockIdx.x & 7; s = blockIdx.x >> 3; }
+    else { x = 0; s = blockIdx.x; }
+    if (a.split) { kind = s & 1; s >>= 1; }
+    const int per = (n_bh & 7) == 0 ? 8 : 1;
+    bh = x + per * (s / a.n_seg);
+    seg = s % a.n_seg;
+  }
+  const int b = bh / a.H, h = bh % a.H;
+  const int64_t HD = (int64_t)a.H * D;
+  const int32_t* rowp = a.rows + (int64_t)b * a.k;
+  const int P0 = seg * a.seg_rows;
+  const int P1 = min(P0 + a.seg_rows, a.k);
+  const int min_row = rowp[P0], max_row = rowp[P1 - 1];
+
+  // ---- the wave's two groups (g = w4, w4 + 4) --------------------------------------------------------
+  int row_i[2], pos[2];
+  bf16x8 qa[2][KS];
+#pragma unroll
+  for (int gi = 0; gi < 2; ++gi) {
+    const int gp0 = P0 + 16 * (w4 + 4 * gi);
+    pos[gi] = gp0 + j16;
+    const bool ok = pos[gi] < P1;
+    row_i[gi] = ok ? rowp[pos[gi]] : -1;
+    const int64_t qoff = ((int64_t)b * a.N + (ok ? row_i[gi] : 0)) * HD + (int64_t)h * D + g4 * 8;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const uint4 w = ok ? *reinterpret_cast<const uint4*>(a.q + qoff + ks * 32) : make_uint4(0, 0, 0, 0);
+      qa[gi][ks] = __builtin_bit_cast(bf16x8, w);
+    }
+  }
+
+  // ---- the list in LDS; nA = entries j with j + window <= max_row (the ones a row here can see) -------
+  const int32_t* cp = a.cols + (int64_t)bh * a.c_list;
+  const int w = a.window;
+  const int lim = max_row - w;
+  if (tid == 0) s_meta[0] = 0;
+  if (tid < 8) {                          // group bounds (a group without rows gets last row -1)
+    const int gp0 = P0 + 16 * tid;
+    const bool has = gp0 < P1;
+    s_grp[2 * tid] = has ? rowp[gp0] : 0;
+    s_grp[2 * tid + 1] = has ? rowp[min(gp0 + 16, P1) - 1] : -1;
+  }
+  const int c_list = kind == 0 ? a.c_list : 0;   // (a band workgroup has no list)
+  for (int i = tid; i < c_list; i += 512) lst[i] = cp[i];
+  __syncthreads();
+  for (int i = tid; i < c_list; i += 512)
+    if (lst[i] <= lim && (i + 1 == c_list || lst[i + 1] > lim)) s_meta[0] = i + 1;
+  __syncthreads();
+  const int nA = __builtin_amdgcn_readfirstlane(s_meta[0]);
+  if (tid < kBN) lst[nA + tid] = kPad;   // padding of the last list tile (entries from nA on are unread)
+
+  // ---- tile sequence: nL list tiles and nB band tiles, interleaved evenly -----------------------------
+  const int bandLo = w > 0 ? max(0, min_row - w + 1) : 0;
+  const int bandHi = w > 0 && (kind == 1 || !a.split) ? max_row : -1;   // (a list workgroup has no band)
+  const int nL = (nA + kBN - 1) / kBN;
+  const int nB = bandHi >= bandLo ? (bandHi - bandLo + kBN) / kBN : 0;
+  // positions are handed out in pairs (position 2p to team 0, 2p + 1 to team 1), and both positions of a
+  // pair hold the same kind of tile, so the two teams do similar work between two barriers
+  const int nLP = (nL + 1) / 2, nBP = (nB + 1) / 2, nP = nLP + nBP;
+  const int n_tiles = min(2 * nP, kSegTileCap);   // (the host keeps 2 nP within the table)
+  // band tiles shared with the previous segment ([bandLo, its last row]) and with the next one
+  // ([its first row - w + 1, bandHi]); the rest in the middle
+  int nBot = 0, nTop = 0;
+  if (w > 0 && nB > 0) {
+    if (P0 > 0) {
+      const int prev_last = rowp[P0 - 1];
+      nBot = prev_last >= bandLo ? min(nB, (prev_last - bandLo) / kBN + 1) : 0;
+    }
+    if (P1 < a.k) {
+      const int from = rowp[P1] - w + 1;
+      const int t0 = from > bandLo ? (from - bandLo) / kBN : 0;
+      nTop = nB - max(t0, nBot);
+      nTop = nTop > 0 ? nTop : 0;
+    }
+  }
+  const bool top_first = (seg & 1) != 0;
+  __syncthreads();                        // list padding and group bounds
+  // Descriptor of sequence position u = 2p + t: pair p holds list tiles when floor((p + 1) nLP / nP) >
+  // floor(p nLP / nP) (list pairs spread evenly through the band pairs); a position past the last tile of
+  // its kind is empty (no group bits, no columns).
+  //   x: first list entry (list tile) or first column (band tile), bit 31 set for a band tile;
+  //   y: bit g: group g sees some column of the tile; bit 8 + g: it sees every column (no mask);
+  //      bits 16-20: the last existing column of the tile (band tiles end at the last row); bit 21: empty.
+  for (int u = tid; u < n_tiles; u += 512) {
+    const int pr = u >> 1, t = u & 1;
+    const int before = (pr * nLP) / nP, after = ((pr + 1) * nLP) / nP;
+    const bool is_list = after > before;
+    int f = 0, c0 = 0, clast = -1, hi = 0;
+    bool empty;
+    if (is_list) {
+      const int lt = 2 * before + t;
+      empty = lt >= nL;
+      f = lt * kBN;
+      if (!empty) {
+        c0 = lst[f];
+        clast = lst[f + kBN - 1];
+        hi = kBN - 1;
+      }
+    } else {
+      const int q = 2 * (pr - before) + t;  // band order position
+      empty = q >= nB;
+      int bt;
+      if (!top_first) bt = q < nBot ? q : q < nBot + nTop ? nB - nTop + (q - nBot) : q - nTop;
+      else bt = q < nTop ? nB - nTop + q : q - nTop;
+      f = bandLo + bt * kBN;
+      if (!empty) {
+        c0 = f;
+        clast = min(f + kBN - 1, bandHi);
+        hi = clast - f;
+      }
+    }
+    uint32_t bits = ((uint32_t)hi << 16) | ((uint32_t)empty << 21);
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+      const int gmin = s_grp[2 * g], gmax = s_grp[2 * g + 1];
+      const bool act = !empty & (gmax >= 0) & (c0 <= (is_list ? gmax - w : gmax)) & (is_list | (clast > gmin - w));
+      const bool full = is_list ? clast <= gmin - w : (hi == kBN - 1) & (clast <= gmin) & (c0 > gmax - w);
+      bits |= ((uint32_t)act << g) | ((uint32_t)(act & full) << (8 + g));
+    }
+    tdesc[u] = make_int2(is_list ? f : (int)(0x80000000u | (uint32_t)f), (int)bits);
+  }
+
+  // (a slot holds team 0's tile, then team 1's: the team's part is an offset from the slot's first tile, so
+  // every address keeps the slot's own constant base)
+  const int tofs = team * (int)(sizeof(Slot<D>) / sizeof(uint16_t));
+  // ---- LDS-DMA offsets of this wave's instructions (its team's tile) -----------------------------------
+  const uint32_t rb = (uint32_t)(HD * 2);
+  const uint32_t head_off = (uint32_t)(h * D * 2);
+  const rsrc_t kcR = make_rsrc(a.k_cache + (int64_t)b * a.N * HD, (uint32_t)a.N * rb);
+  const rsrc_t vcR = make_rsrc(a.v_cache + (int64_t)b * a.N * HD, (uint32_t)a.N * rb);
+  int lcol[NIK];
+  uint32_t lsw[NIK];
+#pragma unroll
+  for (int t = 0; t < NIK; ++t) {
+    const int inst = w4 * NIK + t;
+    lcol[t] = inst * CPI + lane / CH;
+    lsw[t] = (uint32_t)((lane % CH) ^ swz16_f<D>(lcol[t])) * 16 + head_off;
+  }
+  struct Offs { uint32_t o[NIK]; };
+  auto tile_offs = [&](int u) {
+    Offs r;
+    const bool have = u < n_tiles;
+    const int2 dsc = tdesc[have ? u : 0];
+    const int dx = __builtin_amdgcn_readfirstlane(dsc.x), dy = __builtin_amdgcn_readfirstlane(dsc.y);
+    const bool in_list = dx >= 0;
+    const int f = dx & 0x7FFFFFFF;
+    const int hi = have & !((dy >> 21) & 1) ? (dy >> 16) & 31 : -1;   // tile columns c <= hi exist
+    const int fl = in_list & (hi >= 0) ? f : 0;
+#pragma unroll
+    for (int t = 0; t < NIK; ++t) {
+      const int idl = lst[fl + lcol[t]];
+      const int id = in_list ? idl : f + lcol[t];
+      r.o[t] = ((id != kPad) & (lcol[t] <= hi)) ? (uint32_t)id * rb + lsw[t] : kOOB;
+    }
+    return r;
+  };
+  auto issue = [&](Slot<D>& sl, const Offs& of) {
+#pragma unroll
+    for (int t = 0; t < NI; ++t) {
+      const int inst = w4 * NIK + (t % NIK);
+      const uint32_t off = of.o[t % NIK];
+      if (t < NIK)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(kcR, FL_LDS(sl.k + tofs + inst * 512), 16, off, 0, 0, kDmaPolicy);
+      else
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(vcR, FL_LDS(sl.v + tofs + inst * 512), 16, off, 0, 0, kDmaPolicy);
+    }
+  };
+
+  // LDS read offsets of the fragments (elements).  K (A operand): row j16 (+16 for the second column
+  // block), data chunk 4 ks + g4.  V (transposed reads): lane (g4, t, q) reads dims 16 db + 4q of column
+  // 4 g4 + t (+16 for the second half of the k order), data chunk 2 db + (q >> 1).
+  int koff[KS], voff[DB];
+  {
+    const int t4 = j16 >> 2, q = lane & 3;
+    const int colv = 4 * g4 + t4;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) koff[ks] = tofs + j16 * D + ((4 * ks + g4) ^ swz16_f<D>(j16)) * 8;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+      voff[db] = tofs + colv * D + ((2 * db + (q >> 1)) ^ swz16_f<D>(colv)) * 8 + 4 * (q & 1);
+  }
+
+  f32x4 acc[2][DB];
+#pragma unroll
+  for (int gi = 0; gi < 2; ++gi)
+#pragma unroll
+    for (int db = 0; db < DB; ++db) acc[gi][db] = f32x4{};
+  float run_max[2] = {-INFINITY, -INFINITY}, lsum[2] = {0.0f, 0.0f};   // log2 units; row sums
+  // per group: the row index less the lane's column offset within a band block (band masks)
+  const int rband[2] = {row_i[0] - 4 * g4, row_i[1] - 4 * g4};
+
+  // ---- this wave's value rows of a tile, bf16 -> fp16 in place (the 16 bytes per lane its DMA wrote) ---
+  auto convert = [&](Slot<D>& sl) {
+#pragma unroll
+    for (int t = 0; t < NIK; ++t) {
+      u32x4* pv = reinterpret_cast<u32x4*>(sl.v + tofs + (w4 * NIK + t) * 512 + lane * 8);
+      const u32x4 x = *pv;
+      u32x4 y;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) y[e] = pack_f16x2(__uint_as_float(x[e] << 16), __uint_as_float(x[e] & 0xFFFF0000u));
+      *pv = y;
+    }
+  };
+
+  // ---- one tile for the wave's active groups (A0, A1) of one kind (list or band): straight-line code ----
+  const float pinf = a.pinf;
+  const float sc = a.scale_log2;
+  auto body = [&](auto list_c, auto a0_c, auto a1_c, int f, uint32_t dy, const Slot<D>& sl) {
+    constexpr bool IS_LIST = decltype(list_c)::value;
+    constexpr bool A0 = decltype(a0_c)::value, A1 = decltype(a1_c)::value;
+    constexpr bool AG[2] = {A0, A1};
+    // every LDS read of the tile first
+    int4 ca_[2];
+    if constexpr (IS_LIST) {
+#pragma unroll
+      for (int c = 0; c < 2; ++c) ca_[c] = *reinterpret_cast<const int4*>(&lst[f + 16 * c + 4 * g4]);
+    }
+    u32x4 kw[KS][2];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int c = 0; c < 2; ++c) kw[ks][c] = *reinterpret_cast<const u32x4*>(&sl.k[koff[ks] + 16 * c * D]);
+    // S^T = K Q^T for each active group (raw scores; the scale goes into the exponent's multiply-add)
+    f32x4 sa[2][2];
+#pragma unroll
+    for (int gi = 0; gi < 2; ++gi) sa[gi][0] = sa[gi][1] = f32x4{};
+#pragma unroll
+    for (int gi = 0; gi < 2; ++gi) {
+      if constexpr (true) {
+        if (!AG[gi]) continue;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+          for (int c = 0; c < 2; ++c)
+            sa[gi][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kw[ks][c]), qa[gi][ks], sa[gi][c], 0, 0, 0);
+      }
+    }
+    // the value fragments once the key fragments are dead (their registers are reused)
+    __builtin_amdgcn_sched_barrier(0);
+    f16x8 vf[DB];                         // V^T fragments: the two halves of the tile's k order
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const int o = voff[db];
+      const i16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(FL_LDS4(&sl.v[o]));
+      const i16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(FL_LDS4(&sl.v[o + 16 * D]));
+      vf[db] = __builtin_bit_cast(f16x8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
+    }
+    // masks (branch-free: a group that sees the whole tile gets bounds every column passes), row maxima
+    float tmax[2] = {-INFINITY, -INFINITY};
+#pragma unroll
+    for (int gi = 0; gi < 2; ++gi) {
+      if (!AG[gi]) continue;
+      const bool full = ((dy >> (8 + w4 + 4 * gi)) & 1) != 0;
+      if constexpr (IS_LIST) {            // list columns: j + w <= i
+        const int lim_i = full ? INT_MAX : row_i[gi] - w;
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          const int ci[4] = {ca_[c].x, ca_[c].y, ca_[c].z, ca_[c].w};
+#pragma unroll
+          for (int v = 0; v < 4; ++v) sa[gi][c][v] = ci[v] <= lim_i ? sa[gi][c][v] : -INFINITY;
+        }
+      } else {                            // band columns f + 16c + 4 g4 + v: i - w < j <= i
+        const uint32_t wl = full ? 0xFFFFFFFFu : (uint32_t)w;
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          const uint32_t d0 = (uint32_t)(rband[gi] - f - 16 * c);
+#pragma unroll
+          for (int v = 0; v < 4; ++v) sa[gi][c][v] = d0 - (uint32_t)v < wl ? sa[gi][c][v] : -INFINITY;
+        }
+      }
+      float t = fmax_nn(fmax_nn(fmax_nn(sa[gi][0][0], sa[gi][0][1], pinf), fmax_nn(sa[gi][0][2], sa[gi][0][3], pinf), pinf),
+                        fmax_nn(fmax_nn(sa[gi][1][0], sa[gi][1][1], pinf), fmax_nn(sa[gi][1][2], sa[gi][1][3], pinf), pinf),
+                        pinf);
+      auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(t), __float_as_uint(t), false, false);
+      t = fmax_nn(__uint_as_float(r[0]), __uint_as_float(r[1]), pinf);
+      r = __builtin_amdgcn_permlane32_swap(__float_as_uint(t), __float_as_uint(t), false, false);
+      t = fmax_nn(__uint_as_float(r[0]), __uint_as_float(r[1]), pinf);
+      tmax[gi] = t * sc;                  // log2 units (sc > 0 keeps the order; -inf stays -inf)
+    }
+    if constexpr (A0 && A1) {
+      // the second group's products between the first group's vector work
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);   // four VALU
+      }
+    }
+    // online softmax with a lazily raised reference (moved only when a score exceeds it by more than 8 in
+    // log2 units: probabilities stay <= 256 and rescaling is rare); one uniform branch for both groups
+    const bool raise0 = A0 && tmax[0] > run_max[0] + 8.0f;
+    const bool raise1 = A1 && tmax[1] > run_max[1] + 8.0f;
+    if (__builtin_amdgcn_ballot_w64(raise0 | raise1) != 0) {
+#pragma unroll
+      for (int gi = 0; gi < 2; ++gi) {
+        if (!AG[gi]) continue;
+        const bool raise = gi == 0 ? raise0 : raise1;
+        const float nm = raise ? tmax[gi] : run_max[gi];
+        const float alpha = raise ? __builtin_amdgcn_exp2f(run_max[gi] - nm) : 1.0f;   // exp2(-inf) = 0
+        lsum[gi] *= alpha;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) acc[gi][db] *= alpha;
+        run_max[gi] = nm;
+      }
+    }
+    // probabilities, rounded to fp16 for O^T += V^T P^T
+    f16x8 pf[2];
+#pragma unroll
+    for (int gi = 0; gi < 2; ++gi) {
+      if (!AG[gi]) continue;
+      const float ref = run_max[gi] == -INFINITY ? 0.0f : run_max[gi];
+      float pr[8];
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          pr[4 * c + v] = __builtin_amdgcn_exp2f(__builtin_fmaf(sa[gi][c][v], sc, -ref));
+          lsum[gi] += pr[4 * c + v];
+        }
+      u32x4 pk;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) pk[e] = pack_f16x2(pr[2 * e], pr[2 * e + 1]);
+      pf[gi] = __builtin_bit_cast(f16x8, pk);
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+        acc[gi][db] = __builtin_amdgcn_mfma_f32_16x16x32_f16(vf[db], pf[gi], acc[gi][db], 0, 0, 0);
+    }
+    if constexpr (A0 && A1) {
+      // the first group's products between the second group's exponentials
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+        __builtin_amdgcn_sched_group_barrier(0x002, 4, 1);
+      }
+    }
+  };
+  auto compute = [&](int dx, int dy, const Slot<D>& sl) {
+    const bool is_list = dx >= 0;         // uniform
+    const int f = dx & 0x7FFFFFFF;
+    const bool a0 = ((dy >> w4) & 1) != 0, a1 = ((dy >> (w4 + 4)) & 1) != 0;
+    using T = std::true_type;
+    using F = std::false_type;
+    if (is_list) {
+      if (a0 & a1) body(T{}, T{}, T{}, f, (uint32_t)dy, sl);
+      else if (a0) body(T{}, T{}, F{}, f, (uint32_t)dy, sl);
+      else if (a1) body(T{}, F{}, T{}, f, (uint32_t)dy, sl);
+    } else {
+      if (a0 & a1) body(F{}, T{}, T{}, f, (uint32_t)dy, sl);
+      else if (a0) body(F{}, T{}, F{}, f, (uint32_t)dy, sl);
+      else if (a1) body(F{}, F{}, T{}, f, (uint32_t)dy, sl);
+    }
+  };
+
+  // ---- pipeline: step s waits for its two tiles (issued three steps earlier; steps s+1 and s+2 may still
+  // be in flight, 2 NI operations per wave), converts this wave's value rows, passes the barrier (every
+  // wave is done with step s-1 and every value row of step s is fp16), has each team DMA its tile of step
+  // s+3 into the slot step s-1 used, and computes its tile of step s.  Every step issues exactly NI VMEM
+  // operations per wave.
+  __syncthreads();                        // the descriptors
+  FL_WAIT_VM(0);                          // query fragments have arrived
+  const int n_steps = (n_tiles + 1) / 2;
+  const int n_loop = (n_steps + kSegSteps - 1) / kSegSteps * kSegSteps;
+  issue(ring0[0], tile_offs(team));
+  __builtin_amdgcn_sched_barrier(0);
+  issue(ring1[0], tile_offs(2 + team));
+  __builtin_amdgcn_sched_barrier(0);
+  issue(ring2[0], tile_offs(4 + team));
+  int u = team;                           // this team's position at the current step
+  int2 dsc = tdesc[u < n_tiles ? u : 0];  // its descriptor, read one step ahead
+  auto step = [&](Slot<D>& cur, Slot<D>& nxt) {   // (the slots' first tiles; the team's is at tofs)
+    const Offs of = tile_offs(u + 6);
+    const int dx = __builtin_amdgcn_readfirstlane(dsc.x), dy = __builtin_amdgcn_readfirstlane(dsc.y);
+    const bool have = u < n_tiles;
+    dsc = tdesc[u + 2 < n_tiles ? u + 2 : 0];
+    FL_WAIT_VM(2 * NI);
+    convert(cur);
+    lds_barrier();
+    issue(nxt, of);
+    if (have) compute(dx, dy, cur);
+    u += 2;
+  };
+  for (int s = 0; s < n_loop; s += kSegSteps) {
+    step(ring0[0], ring3[0]);
+    step(ring1[0], ring0[0]);
+    step(ring2[0], ring1[0]);
+    step(ring3[0], ring2[0]);
+  }
+  FL_WAIT_VM(0);
+  lds_barrier();
+
+  // ---- merge the two teams' states per row: team 0 finishes group w4, team 1 group w4 + 4 -------------
+  // The other team's partial of the group goes through the (now idle) ring: per wave 16 rows x D fp32
+  // output values (DB x 64 lanes x 4) in slots 0 and 1, and the reference and sum of each row (64 lanes x 2)
+  // in slot 2.
+  constexpr int XO = DB * 64 * 4;         // floats per wave: two waves per slot half
+  auto xo_of = [&](int wv) {
+    Slot<D>* sl = (wv >> 2) ? ring1 : ring0;
+    return reinterpret_cast<float*>(sl[(wv >> 1) & 1].k) + (wv & 1) * XO;
+  };
+  auto xs_of = [&](int wv) { return reinterpret_cast<float*>(ring2[0].k) + wv * 128; };
+  float* xo_me = xo_of(wave);
+  float* xs_me = xs_of(wave);
+  const int other = wave ^ 4;             // the same w4 in the other team
+  const float* xo_ot = xo_of(other);
+  const float* xs_ot = xs_of(other);
+  // (team is uniform: the selects below pick whole registers, so no state is indexed dynamically)
+  const bool t1 = team != 0;
+#pragma unroll
+  for (int db = 0; db < DB; ++db)         // team 0 gives group w4 + 4, team 1 gives group w4
+    *reinterpret_cast<f32x4*>(&xo_me[(db * 64 + lane) * 4]) = t1 ? acc[0][db] : acc[1][db];
+  xs_me[lane * 2] = t1 ? run_max[0] : run_max[1];
+  xs_me[lane * 2 + 1] = t1 ? lsum[0] : lsum[1];
+  lds_barrier();
+  float m_o = xs_ot[lane * 2], l_o = xs_ot[lane * 2 + 1];
+  float m_s = t1 ? run_max[1] : run_max[0];
+  float l_s = t1 ? lsum[1] : lsum[0];
+  l_s = row4_add(l_s);
+  l_o = row4_add(l_o);
+  f32x4 o_acc[DB];
+  {
+    // combine (reference m_s, sum l_s, acc) with (m_o, l_o, acc_o); an empty state has sum 0 and
+    // reference -inf, and contributes nothing (its factor is exp2(-inf) = 0)
+    const float mm = fmaxf(m_s, m_o);
+    const float fs = mm == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m_s - mm);
+    const float fo = mm == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m_o - mm);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const f32x4 ao = *reinterpret_cast<const f32x4*>(&xo_ot[(db * 64 + lane) * 4]);
+      o_acc[db] = (t1 ? acc[1][db] : acc[0][db]) * fs + ao * fo;
+    }
+    l_s = l_s * fs + l_o * fo;
+    m_s = mm;
+  }
+  // ---- epilogue: lane (j16, g4) holds dims 16 db + 4 g4 .. +3 of row j16 of its group -----------------
+  const int p = t1 ? pos[1] : pos[0];
+  if (p >= P1) return;
+  if (a.split) {                          // this kind's part of the row; seg_merge_kernel finishes it
+    const int64_t prow = ((int64_t)kind * a.B * a.k + (int64_t)b * a.k + p) * a.H + h;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+      *reinterpret_cast<f32x4*>(a.part_acc + prow * D + db * 16 + 4 * g4) = o_acc[db];
+    if (g4 == 0) *reinterpret_cast<float2*>(a.part_st + prow * 2) = make_float2(m_s, l_s);
+    return;
+  }
+  const int ri = t1 ? row_i[1] : row_i[0];
+  const int64_t orow = ((int64_t)b * a.N + ri) * HD + (int64_t)h * D;
+  const int64_t lrow = ((int64_t)b * a.N + ri) * a.H + h;
+  const int pp = a.slot_prev[(int64_t)b * a.N + ri];
+  const int64_t tp = ((int64_t)b * a.k_prev + pp) * a.H + h;
+  const float msub = pp >= 0 ? a.mass_prev[tp] : 0.0f;
+  const float* subp = a.term_prev + tp * D;
+  const int64_t trow = ((int64_t)b * a.k + p) * a.H + h;
+  const bool keep_terms = a.term_out != nullptr;
+  if (!(msub > 0.0f) || !(l_s > 0.0f)) {  // empty column set or vanished mass: unchanged
+    if (keep_terms) {
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+        *reinterpret_cast<float4*>(a.term_out + trow * D + db * 16 + 4 * g4) = make_float4(0, 0, 0, 0);
+      if (g4 == 0) a.mass_out[trow] = 0.0f;
+    }
+    return;
+  }
+  const float fm = msub / l_s;
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+    const int dim = db * 16 + 4 * g4;
+    const float4 sub = *reinterpret_cast<const float4*>(subp + dim);
+    const float4 add = make_float4(o_acc[db][0] * fm, o_acc[db][1] * fm, o_acc[db][2] * fm, o_acc[db][3] * fm);
+    float4 prev = *reinterpret_cast<const float4*>(a.o + orow + dim);
+    prev.x = prev.x - sub.x + add.x;
+    prev.y = prev.y - sub.y + add.y;
+    prev.z = prev.z - sub.z + add.z;
+    prev.w = prev.w - sub.w + add.w;
+    *reinterpret_cast<float4*>(a.o + orow + dim) = prev;
+    if (keep_terms) *reinterpret_cast<float4*>(a.term_out + trow * D + dim) = add;
+  }
+  if (g4 == 0) {
+    a.lse_ref[lrow] = (m_s + log2f(l_s)) * 0.6931471805599453f - logf(msub);
+    if (keep_terms) a.mass_out[trow] = msub;
+  }
+}
+
+// The two parts of each updated row (list and band workgroups) merged and the row finished as above: one
+// wave per two (row, head) pairs, four output dimensions per lane.
+template <int D>
+__global__ __launch_bounds__(256) void seg_merge_kernel(SegArgs a) {
+  constexpr int TPR = D / 4;              // lanes per (row, head)
+  const int64_t n = (int64_t)a.B * a.k * a.H;
+  const int64_t e = (int64_t)blockIdx.x * (256 / TPR) + threadIdx.x / TPR;
+  if (e >= n) return;
+  const int dim = (threadIdx.x % TPR) * 4;
+  const int h = (int)(e % a.H);
+  const int64_t bp = e / a.H;             // b * k + p
+  const int b = (int)(bp / a.k), p = (int)(bp % a.k);
+  const int64_t e1 = e + n;               // the band part
+  const f32x4 acc0 = *reinterpret_cast<const f32x4*>(a.part_acc + e * D + dim);
+  const f32x4 acc1 = *reinterpret_cast<const f32x4*>(a.part_acc + e1 * D + dim);
+  const float2 st0 = *reinterpret_cast<const float2*>(a.part_st + e * 2);
+  const float2 st1 = *reinterpret_cast<const float2*>(a.part_st + e1 * 2);
+  const float mm = fmaxf(st0.x, st1.x);
+  const float f0 = mm == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(st0.x - mm);
+  const float f1 = mm == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(st1.x - mm);
+  const f32x4 acc = acc0 * f0 + acc1 * f1;
+  const float l = st0.y * f0 + st1.y * f1;
+  const int64_t HD = (int64_t)a.H * D;
+  const int ri = a.rows[bp];
+  const int64_t orow = ((int64_t)b * a.N + ri) * HD + (int64_t)h * D;
+  const int64_t lrow = ((int64_t)b * a.N + ri) * a.H + h;
+  const int pp = a.slot_prev[(int64_t)b * a.N + ri];
+  const int64_t tp = ((int64_t)b * a.k_prev + pp) * a.H + h;
+  const float msub = pp >= 0 ? a.mass_prev[tp] : 0.0f;
+  const bool keep_terms = a.term_out != nullptr;
+  if (!(msub > 0.0f) || !(l > 0.0f)) {    // empty column set or vanished mass: unchanged
+    if (keep_terms) {
+      *reinterpret_cast<float4*>(a.term_out + e * D + dim) = make_float4(0, 0, 0, 0);
+      if (dim == 0) a.mass_out[e] = 0.0f;
+    }
+    return;
+  }
+  const float fm = msub / l;
+  const float4 sub = *reinterpret_cast<const float4*>(a.term_prev + tp * D + dim);
+  const float4 add = make_float4(acc[0] * fm, acc[1] * fm, acc[2] * fm, acc[3] * fm);
+  float4 prev = *reinterpret_cast<const float4*>(a.o + orow + dim);
+  prev.x = prev.x - sub.x + add.x;
+  prev.y = prev.y - sub.y + add.y;
+  prev.z = prev.z - sub.z + add.z;
+  prev.w = prev.w - sub.w + add.w;
+  *reinterpret_cast<float4*>(a.o + orow + dim) = prev;
+  if (keep_terms) *reinterpret_cast<float4*>(a.term_out + e * D + dim) = add;
+  if (dim == 0) {
+    a.lse_ref[lrow] = (mm + log2f(l)) * 0.6931471805599453f - logf(msub);
+    if (keep_terms) a.mass_out[e] = msub;
+  }
+}
+
+size_t seg_part_bytes(int B, int H, int d, int k) {
+  return (size_t)2 * B * k * H * ((size_t)d + 2) * sizeof(float);
+}
+
+// Launch of the segment kernel for a reuse loop over current caches; returns FL_E_UNSUPPORTED (nothing
+// launched) when the shape is outside what it covers, so the caller can take another kernel.
+int launch_seg_cur(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, const int32_t* rows, int k,
+                   const int32_t* cols, int c_list, int window, int B, int N, int H, int d, float sm_scale,
+                   float* lse_ref, float* o, const float* term_prev, const float* mass_prev,
+                   const int32_t* slot_prev, int k_prev, float* term_out, float* mass_out, void* part,
+                   hipStream_t st) {
+  if (c_list > kSegListCap || (d != 64 && d != 128) || k < 1) return FL_E_UNSUPPORTED;
+  // the descriptor table holds every position: at most ceil(c_list / 32) list tiles and ceil(N / 32) + 1 band
+  // tiles, plus one empty position per kind when the counts are odd
+  if ((c_list + kBN - 1) / kBN + (N + kBN - 1) / kBN + 3 > kSegTileCap) return FL_E_UNSUPPORTED;
+  constexpr int kCUs = 256;
+  const int bh = B * H;
+  // at least one segment per 128 rows; more (down to 64 rows) while the grid is below one workgroup per CU
+  // (two per segment with a band)
+  int n_seg = (k + kSegRows - 1) / kSegRows;
+  const int fill = (kCUs + bh - 1) / bh;
+  const int n_max = (k + 63) / 64;
+  if (n_seg < fill) n_seg = std::min(fill, n_max);
+  if (n_seg < 1) n_seg = 1;
+  const int seg_rows = (k + n_seg - 1) / n_seg;
+  n_seg = (k + seg_rows - 1) / seg_rows;
+  SegArgs a{};
+  a.q = q; a.k_cache = k_cache; a.v_cache = v_cache; a.rows = rows; a.cols = cols;
+  a.lse_ref = lse_ref; a.o = o; a.term_prev = term_prev; a.mass_prev = mass_prev; a.slot_prev = slot_prev;
+  a.term_out = term_out; a.mass_out = mass_out;
+  a.k = k; a.k_prev = k_prev; a.c_list = c_list; a.window = window; a.B = B; a.N = N; a.H = H;
+  a.n_seg = n_seg; a.seg_rows = seg_rows;
+  a.scale_log2 = sm_scale * 1.4426950408889634f;
+  a.pinf = INFINITY;
+  a.split = 0;                            // (list and band in the same workgroup: measured faster)
+  if (a.split) {
+    if (part == nullptr) return FL_E_UNSUPPORTED;
+    a.part_acc = static_cast<float*>(part);
+    a.part_st = a.part_acc + (size_t)2 * B * k * H * d;
+  }
+  dim3 grid((unsigned)(n_seg * bh * (a.split ? 2 : 1)));
+  if (d == 128) seg_cur_kernel<128><<<grid, 512, 0, st>>>(a);
+  else seg_cur_kernel<64><<<grid, 512, 0, st>>>(a);
+  int rc = check_launch("seg_cur_kernel");
+  if (rc != FL_OK || !a.split) return rc;
+  const int64_t n = (int64_t)B * k * H;
+  const int per_block = 256 / (d / 4);
+  dim3 gm((unsigned)((n + per_block - 1) / per_block));
+  if (d == 128) seg_merge_kernel<128><<<gm, 256, 0, st>>>(a);
+  else seg_merge_kernel<64><<<gm, 256, 0, st>>>(a);
+  return check_launch("seg_merge_kernel");
+}
+
+}  // namespace fl
