@@ -1469,18 +1469,16 @@ static RecLayout rec_layout(int B, int N, int H, int k, int c_list) {
   return L;
 }
 
-// the larger of the tile records (prep kernel) and, with a band, the segment kernel's per-row parts
-static size_t attn_ws_bytes(int B, int N, int H, int d, int k, int c_list, int window, bool dense) {
+static size_t attn_ws_bytes(int B, int N, int H, int k, int c_list, bool dense) {
   if (dense || B < 1 || N < 1 || H < 1 || k < 0 || c_list < 0) return 0;
   const RecLayout L = rec_layout(B, N, H, k, c_list);
-  const size_t rec = L.n_rec * sizeof(int2) + (size_t)B * H * sizeof(int32_t);
-  const size_t part = window > 0 && (d == 64 || d == 128) ? seg_part_bytes(B, H, d, k) : 0;
-  return std::max(rec, part);
+  return L.n_rec * sizeof(int2) + (size_t)B * H * sizeof(int32_t);
 }
 
 extern "C" size_t fl_loop_sparse_attn_ws(int B, int N, int H, int d, int k, int c_list, int window,
                                          int flags) {
-  return attn_ws_bytes(B, N, H, d, k, c_list, window, (flags & FL_ATTN_DENSE) != 0);
+  (void)d; (void)window;
+  return attn_ws_bytes(B, N, H, k, c_list, (flags & FL_ATTN_DENSE) != 0);
 }
 
 static int loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev, const uint16_t* k_cache,
@@ -1521,7 +1519,7 @@ static int loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev, const
       FL_REQUIRE(k_prev >= k && k_prev <= N, FL_E_RANGE, "fl_loop_sparse_attn: k_prev=%d outside [k, N]", k_prev);
     }
   }
-  const size_t need = attn_ws_bytes(B, N, H, d, k, c_list, window, dense);
+  const size_t need = attn_ws_bytes(B, N, H, k, c_list, dense);
   FL_REQUIRE(dense || rec_layout(B, N, H, k, c_list).n_rec * sizeof(int2) <= ((size_t)1 << 31) - 8, FL_E_SHAPE,
              "fl_loop_sparse_attn: tile records above 2^31 bytes (reduce B * H * c_list + B * (N + k))");
   FL_REQUIRE(need == 0 || (ws && ws_bytes >= need), FL_E_WORKSPACE,
@@ -1588,7 +1586,7 @@ static int loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev, const
 #define FL_REUSE(DD, CC) reuse_attn_kernel<DD, CC><<<grid, 256, 0, st>>>(a)
   if (a.cache_current) {
     const int rc = launch_seg_cur(q_cur, k_cache, v_cache, rows, k, cols, c_list, window, B, N, H, d, sm_scale, lse_ref,
-                                  o, term_prev, mass_prev, slot_prev, k_prev, term_out, mass_out, ws, st);
+                                  o, term_prev, mass_prev, slot_prev, k_prev, term_out, mass_out, st);
     if (rc != FL_E_UNSUPPORTED) return rc;
   }
   if (a.cache_current && c_list <= kListCap) {

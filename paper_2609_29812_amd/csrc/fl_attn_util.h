@@ -103,9 +103,6 @@ __device__ __forceinline__ float fmax_nn(float x, float y, float pinf) { return 
 int launch_seg_cur(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, const int32_t* rows, int k,
                    const int32_t* cols, int c_list, int window, int B, int N, int H, int d, float sm_scale,
                    float* lse_ref, float* o, const float* term_prev, const float* mass_prev,
-                   const int32_t* slot_prev, int k_prev, float* term_out, float* mass_out, void* part,
-                   hipStream_t st);
-// workspace bytes of the segment kernel's per-row parts (list and band) of k rows
-size_t seg_part_bytes(int B, int H, int d, int k);
+                   const int32_t* slot_prev, int k_prev, float* term_out, float* mass_out, hipStream_t st);
 
 }  // namespace fl

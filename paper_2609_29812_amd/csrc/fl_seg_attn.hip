@@ -58,9 +58,6 @@ struct SegArgs {
   float* mass_out;            // optional [B, k, H]
   int k, k_prev, c_list, window, B, N, H;
   int n_seg, seg_rows;        // segments per (batch, head) and rows per segment (<= kSegRows)
-  int split;                  // list and band columns in separate workgroups (a band exists)
-  float* part_acc;            // split: [2][B, k, H, d] unnormalised outputs of the list / band workgroups
-  float* part_st;             // split: [2][B, k, H, 2] their reference (log2 units) and row sum
   float scale_log2;           // sm_scale * log2(e)
   float pinf;                 // +inf (a kernel argument, so the median below is not folded into a max)
 };
@@ -89,20 +86,16 @@ __global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
   const int team = wave >> 2, w4 = wave & 3;
   const int j16 = lane & 15, g4 = lane >> 4;
 
-  // ---- work item -> (kind, batch*head, segment); the workgroups of one (batch, head) stay on one XCD ----
-  // kind 0 takes the segment's list columns, kind 1 its band columns (split), or kind 0 takes both (a
-  // single workgroup per segment).  The two kinds alternate in dispatch order, so about half of the CUs
-  // stream band columns from HBM while the others work through the lists held in L2.
+  // ---- work item -> (batch*head, segment); the segments of one (batch, head) stay on one XCD ----------
   const int n_bh = a.B * a.H;
-  int bh, seg, kind = 0;
-  {
-    int x, s;
-    if ((n_bh & 7) == 0) { x = blockIdx.x & 7; s = blockIdx.x >> 3; }
-    else { x = 0; s = blockIdx.x; }
-    if (a.split) { kind = s & 1; s >>= 1; }
-    const int per = (n_bh & 7) == 0 ? 8 : 1;
-    bh = x + per * (s / a.n_seg);
+  int bh, seg;
+  if ((n_bh & 7) == 0) {
+    const int x = blockIdx.x & 7, s = blockIdx.x >> 3;
+    bh = x + 8 * (s / a.n_seg);
     seg = s % a.n_seg;
+  } else {
+    bh = blockIdx.x / a.n_seg;
+    seg = blockIdx.x % a.n_seg;
   }
   const int b = bh / a.H, h = bh % a.H;
   const int64_t HD = (int64_t)a.H * D;
@@ -139,18 +132,17 @@ __global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
     s_grp[2 * tid] = has ? rowp[gp0] : 0;
     s_grp[2 * tid + 1] = has ? rowp[min(gp0 + 16, P1) - 1] : -1;
   }
-  const int c_list = kind == 0 ? a.c_list : 0;   // (a band workgroup has no list)
-  for (int i = tid; i < c_list; i += 512) lst[i] = cp[i];
+  for (int i = tid; i < a.c_list; i += 512) lst[i] = cp[i];
   __syncthreads();
-  for (int i = tid; i < c_list; i += 512)
-    if (lst[i] <= lim && (i + 1 == c_list || lst[i + 1] > lim)) s_meta[0] = i + 1;
+  for (int i = tid; i < a.c_list; i += 512)
+    if (lst[i] <= lim && (i + 1 == a.c_list || lst[i + 1] > lim)) s_meta[0] = i + 1;
   __syncthreads();
   const int nA = __builtin_amdgcn_readfirstlane(s_meta[0]);
   if (tid < kBN) lst[nA + tid] = kPad;   // padding of the last list tile (entries from nA on are unread)
 
   // ---- tile sequence: nL list tiles and nB band tiles, interleaved evenly -----------------------------
   const int bandLo = w > 0 ? max(0, min_row - w + 1) : 0;
-  const int bandHi = w > 0 && (kind == 1 || !a.split) ? max_row : -1;   // (a list workgroup has no band)
+  const int bandHi = w > 0 ? max_row : -1;
   const int nL = (nA + kBN - 1) / kBN;
   const int nB = bandHi >= bandLo ? (bandHi - bandLo + kBN) / kBN : 0;
   // positions are handed out in pairs (position 2p to team 0, 2p + 1 to team 1), and both positions of a
@@ -532,14 +524,6 @@ __global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
   // ---- epilogue: lane (j16, g4) holds dims 16 db + 4 g4 .. +3 of row j16 of its group -----------------
   const int p = t1 ? pos[1] : pos[0];
   if (p >= P1) return;
-  if (a.split) {                          // this kind's part of the row; seg_merge_kernel finishes it
-    const int64_t prow = ((int64_t)kind * a.B * a.k + (int64_t)b * a.k + p) * a.H + h;
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-      *reinterpret_cast<f32x4*>(a.part_acc + prow * D + db * 16 + 4 * g4) = o_acc[db];
-    if (g4 == 0) *reinterpret_cast<float2*>(a.part_st + prow * 2) = make_float2(m_s, l_s);
-    return;
-  }
   const int ri = t1 ? row_i[1] : row_i[0];
   const int64_t orow = ((int64_t)b * a.N + ri) * HD + (int64_t)h * D;
   const int64_t lrow = ((int64_t)b * a.N + ri) * a.H + h;
@@ -578,70 +562,12 @@ __global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
   }
 }
 
-// The two parts of each updated row (list and band workgroups) merged and the row finished as above: one
-// wave per two (row, head) pairs, four output dimensions per lane.
-template <int D>
-__global__ __launch_bounds__(256) void seg_merge_kernel(SegArgs a) {
-  constexpr int TPR = D / 4;              // lanes per (row, head)
-  const int64_t n = (int64_t)a.B * a.k * a.H;
-  const int64_t e = (int64_t)blockIdx.x * (256 / TPR) + threadIdx.x / TPR;
-  if (e >= n) return;
-  const int dim = (threadIdx.x % TPR) * 4;
-  const int h = (int)(e % a.H);
-  const int64_t bp = e / a.H;             // b * k + p
-  const int b = (int)(bp / a.k), p = (int)(bp % a.k);
-  const int64_t e1 = e + n;               // the band part
-  const f32x4 acc0 = *reinterpret_cast<const f32x4*>(a.part_acc + e * D + dim);
-  const f32x4 acc1 = *reinterpret_cast<const f32x4*>(a.part_acc + e1 * D + dim);
-  const float2 st0 = *reinterpret_cast<const float2*>(a.part_st + e * 2);
-  const float2 st1 = *reinterpret_cast<const float2*>(a.part_st + e1 * 2);
-  const float mm = fmaxf(st0.x, st1.x);
-  const float f0 = mm == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(st0.x - mm);
-  const float f1 = mm == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(st1.x - mm);
-  const f32x4 acc = acc0 * f0 + acc1 * f1;
-  const float l = st0.y * f0 + st1.y * f1;
-  const int64_t HD = (int64_t)a.H * D;
-  const int ri = a.rows[bp];
-  const int64_t orow = ((int64_t)b * a.N + ri) * HD + (int64_t)h * D;
-  const int64_t lrow = ((int64_t)b * a.N + ri) * a.H + h;
-  const int pp = a.slot_prev[(int64_t)b * a.N + ri];
-  const int64_t tp = ((int64_t)b * a.k_prev + pp) * a.H + h;
-  const float msub = pp >= 0 ? a.mass_prev[tp] : 0.0f;
-  const bool keep_terms = a.term_out != nullptr;
-  if (!(msub > 0.0f) || !(l > 0.0f)) {    // empty column set or vanished mass: unchanged
-    if (keep_terms) {
-      *reinterpret_cast<float4*>(a.term_out + e * D + dim) = make_float4(0, 0, 0, 0);
-      if (dim == 0) a.mass_out[e] = 0.0f;
-    }
-    return;
-  }
-  const float fm = msub / l;
-  const float4 sub = *reinterpret_cast<const float4*>(a.term_prev + tp * D + dim);
-  const float4 add = make_float4(acc[0] * fm, acc[1] * fm, acc[2] * fm, acc[3] * fm);
-  float4 prev = *reinterpret_cast<const float4*>(a.o + orow + dim);
-  prev.x = prev.x - sub.x + add.x;
-  prev.y = prev.y - sub.y + add.y;
-  prev.z = prev.z - sub.z + add.z;
-  prev.w = prev.w - sub.w + add.w;
-  *reinterpret_cast<float4*>(a.o + orow + dim) = prev;
-  if (keep_terms) *reinterpret_cast<float4*>(a.term_out + e * D + dim) = add;
-  if (dim == 0) {
-    a.lse_ref[lrow] = (mm + log2f(l)) * 0.6931471805599453f - logf(msub);
-    if (keep_terms) a.mass_out[e] = msub;
-  }
-}
-
-size_t seg_part_bytes(int B, int H, int d, int k) {
-  return (size_t)2 * B * k * H * ((size_t)d + 2) * sizeof(float);
-}
-
 // Launch of the segment kernel for a reuse loop over current caches; returns FL_E_UNSUPPORTED (nothing
 // launched) when the shape is outside what it covers, so the caller can take another kernel.
 int launch_seg_cur(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, const int32_t* rows, int k,
                    const int32_t* cols, int c_list, int window, int B, int N, int H, int d, float sm_scale,
                    float* lse_ref, float* o, const float* term_prev, const float* mass_prev,
-                   const int32_t* slot_prev, int k_prev, float* term_out, float* mass_out, void* part,
-                   hipStream_t st) {
+                   const int32_t* slot_prev, int k_prev, float* term_out, float* mass_out, hipStream_t st) {
   if (c_list > kSegListCap || (d != 64 && d != 128) || k < 1) return FL_E_UNSUPPORTED;
   // the descriptor table holds every position: at most ceil(c_list / 32) list tiles and ceil(N / 32) + 1 band
   // tiles, plus one empty position per kind when the counts are odd
@@ -649,7 +575,6 @@ int launch_seg_cur(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v
   constexpr int kCUs = 256;
   const int bh = B * H;
   // at least one segment per 128 rows; more (down to 64 rows) while the grid is below one workgroup per CU
-  // (two per segment with a band)
   int n_seg = (k + kSegRows - 1) / kSegRows;
   const int fill = (kCUs + bh - 1) / bh;
   const int n_max = (k + 63) / 64;
@@ -665,23 +590,10 @@ int launch_seg_cur(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v
   a.n_seg = n_seg; a.seg_rows = seg_rows;
   a.scale_log2 = sm_scale * 1.4426950408889634f;
   a.pinf = INFINITY;
-  a.split = 0;                            // (list and band in the same workgroup: measured faster)
-  if (a.split) {
-    if (part == nullptr) return FL_E_UNSUPPORTED;
-    a.part_acc = static_cast<float*>(part);
-    a.part_st = a.part_acc + (size_t)2 * B * k * H * d;
-  }
-  dim3 grid((unsigned)(n_seg * bh * (a.split ? 2 : 1)));
+  dim3 grid((unsigned)(n_seg * bh));
   if (d == 128) seg_cur_kernel<128><<<grid, 512, 0, st>>>(a);
   else seg_cur_kernel<64><<<grid, 512, 0, st>>>(a);
-  int rc = check_launch("seg_cur_kernel");
-  if (rc != FL_OK || !a.split) return rc;
-  const int64_t n = (int64_t)B * k * H;
-  const int per_block = 256 / (d / 4);
-  dim3 gm((unsigned)((n + per_block - 1) / per_block));
-  if (d == 128) seg_merge_kernel<128><<<gm, 256, 0, st>>>(a);
-  else seg_merge_kernel<64><<<gm, 256, 0, st>>>(a);
-  return check_launch("seg_merge_kernel");
+  return check_launch("seg_cur_kernel");
 }
 
 }  // namespace fl
