@@ -38,7 +38,6 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 MFMA_BF16_TFLOPS = 2500.0      # dense bf16/fp16 MFMA
 FP64_VECTOR_TFLOPS = 78.6      # fp64 vector FMA (the pruning statistic)
 PROFILE_DIR = os.path.join(ROOT, "profiles")
-ATTN_SRC = os.path.join(ROOT, "paper_2609_29812_amd", "csrc", "fl_attn.hip")
 
 
 def log(*a):
@@ -168,16 +167,24 @@ def source_sha(path):
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def load_traffic(kernel, workload):
-    """HBM bytes per launch from committed rocprofv3 counter runs, if taken on the current source."""
-    path = os.path.join(PROFILE_DIR, f"{kernel}_{workload}_pmc.json")
+KERNEL_SRC = {"seg_cur_kernel": "fl_seg_attn.hip", "loop_attn_kernel": "fl_attn.hip", "cur_attn_kernel": "fl_attn.hip"}
+
+
+def load_counters(kernel, workload):
+    """HBM traffic and MFMA busy fraction per launch from committed rocprofv3 counter runs
+    (profiles/<kernel>_<workload>_counters.json), used only when taken on the kernel's current source."""
+    none = {"traffic": None, "traffic_read": None, "traffic_write": None, "mfma_busy": None}
+    path = os.path.join(PROFILE_DIR, f"{kernel}_{workload}_counters.json")
+    src = os.path.join(ROOT, "paper_2609_29812_amd", "csrc", KERNEL_SRC.get(kernel, "fl_attn.hip"))
     if not os.path.exists(path):
-        return None
+        return none
     with open(path) as f:
         rec = json.load(f)
-    if rec.get("source_sha") != source_sha(ATTN_SRC):
-        return None
-    return rec.get("hbm_bytes_per_launch")
+    if rec.get("source_sha") != source_sha(src):
+        return none
+    rd, wr = rec.get("dram_read_bytes_per_launch"), rec.get("dram_write_bytes_per_launch")
+    return {"traffic": None if rd is None or wr is None else int(rd + wr), "traffic_read": rd, "traffic_write": wr,
+            "mfma_busy": rec.get("mfma_busy")}
 
 
 # ---- CPU oracle leg ------------------------------------------------------------------------------------
@@ -229,6 +236,9 @@ def cpu_baseline(w, st, threads_note):
         "value": rows_total / t_est,
         "unit": "rows/s",
         "cores": threads_note,
+        "host_cores": len(os.sched_getaffinity(0)),
+        "cores_note": "cores = the BLAS threads the oracle's matrix products use; its elementwise numpy work is "
+                      "single-threaded; host_cores = the cores this process may run on",
         "kind": "oracle",
         "sample": (f"{w.name} loops 2-{w.loops}: token scoring, top-k and the K/V residual codec for all "
                    f"{w.heads} heads, the mass-corrected update for every active row of head 0 only "
@@ -259,71 +269,41 @@ def copy_calib():
     print(json.dumps({"copy_bytes_read": nbytes, "copy_bytes_written": nbytes, "dispatches": 5}), flush=True)
 
 
-# ---- main ----------------------------------------------------------------------------------------------
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="C4")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-decode", action="store_true")
-    ap.add_argument("--no-prune", action="store_true")
-    ap.add_argument("--decode-only", action="store_true", help="only the decode measurement (for traces)")
-    ap.add_argument("--copy-calib", action="store_true")
-    args = ap.parse_args()
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only; there is no multi-GPU path (asked for {args.gpus}): "
-              "the step would shard by head with one small all-gather of row-score partials.", flush=True)
-        sys.exit(2)
-    import torch
-    torch.cuda.set_device(0)
-    if args.copy_calib:
-        copy_calib()
-        return
+def workload_config(w):
+    return {"workload": w.name, "batch": w.batch, "seq": w.seq, "heads": w.heads, "head_dim": w.head_dim,
+            "loops": w.loops, "sparse_loops": f"2-{w.loops}",
+            "rows_per_step": sum(w.batch * w.k(r) for r in range(2, w.loops + 1)),
+            "k_per_loop": [w.k(r) for r in range(2, w.loops + 1)], "column_budget": w.col_budget,
+            "window": w.window, "residual_bits": list(w.bits), "group": w.group}
 
-    from paper_2609_29812_amd import driver
-    from paper_2609_29812_amd import flashloop as fl
-    from workloads import get, make_layer
 
-    fl.load()
-    w = get(args.workload)
-    t0 = time.time()
-    st = make_layer(w)
-    log(f"[bench] generated {w.name} in {time.time() - t0:.1f}s")
-
-    def up(a):
-        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda().view(torch.bfloat16)
-
-    dev = {n: [up(a) for a in getattr(st, n)] for n in "qkv"}
+def measure(w, dev, driver, fl, torch, steps, warmup, log_calls=False):
+    """Set-up, then W warm-up steps and K timed steps (HIP events on the launch stream around the K steps);
+    then a separate pass with events around every call, for the per-call durations and the rooflines."""
     t0 = time.time()
     gs = driver.setup(dev["q"][0], dev["k"][0], dev["v"][0], w.base_bits, w.group, w.n_sink, w.top_cols,
                       w.window)
     torch.cuda.synchronize()
-    log(f"[bench] loop-1 setup on GPU {time.time() - t0:.2f}s")
+    log(f"[bench] {w.name}: loop-1 setup on GPU {time.time() - t0:.2f}s")
     step = Step(w, dev, gs, fl, torch)
-    if args.decode_only:
-        print(json.dumps({"decode": decode_bench(w, gs, fl, torch)}), flush=True)
-        return
-
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         step.run()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t_wall = time.perf_counter()
     e0.record()
-    for _ in range(args.steps):
+    for _ in range(steps):
         step.run()
     e1.record()
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
-    ms_step = e0.elapsed_time(e1) / args.steps
+    ms_step = e0.elapsed_time(e1) / steps
     rows_per_step = sum(w.batch * w.k(r) for r in range(2, w.loops + 1))
-    log(f"[bench] {args.steps} steps: {ms_step:.4f} ms/step (wall {t_wall / args.steps * 1e3:.4f} ms)")
+    log(f"[bench] {w.name}: {steps} steps: {ms_step:.4f} ms/step (wall {t_wall / steps * 1e3:.4f} ms)")
 
     # per-call durations with events on the launch stream (a separate pass, same work)
     events = {}
-    reps = max(3, min(args.steps, 10))
+    reps = max(3, min(steps, 10))
     trace = None
     for _ in range(reps):
         trace = step.run(events)
@@ -333,7 +313,7 @@ def main():
     cols = gs.cols.cpu().numpy()
     B, N, H, d = w.batch, w.seq, w.heads, w.head_dim
     kernels = {}
-    attn_bytes = attn_flops = attn_us = 0.0
+    attn_us = 0.0
     per_kernel = {}               # kernel -> [bytes, flops, us, launches]
     total_bytes = 0.0
     n_cand = N
@@ -356,19 +336,18 @@ def main():
                              "TFLOP/s": round(nf / us / 1e6, 2) if nf else None,
                              "alg_MB": round(nb / 1e6, 2), "alg_GF": round(nf / 1e9, 3) if nf else None}
             total_bytes += nb
-        attn_bytes += by
-        attn_flops += fl_
         attn_us += dur_us[f"attn r{r}"]
-        kname = "loop_attn_kernel" if r == 2 else "seg_cur_kernel"
+        kname = "loop_attn_kernel" if r == 2 else ("seg_cur_kernel" if w.window > 0 else "cur_attn_kernel")
         acc = per_kernel.setdefault(kname, [0.0, 0.0, 0.0, 0])
         acc[0] += by
         acc[1] += fl_
         acc[2] += dur_us[f"attn r{r}"]
         acc[3] += 1
         n_cand = kr
-    for name, kv in kernels.items():
-        log(f"  {name:12s} {kv['us']:9.2f} us  {kv['GB/s']:8.1f} GB/s  alg {kv['alg_MB']:8.2f} MB"
-            + (f"  {kv['TFLOP/s']:7.2f} TFLOP/s" if kv["TFLOP/s"] else ""))
+    if log_calls:
+        for name, kv in kernels.items():
+            log(f"  {name:12s} {kv['us']:9.2f} us  {kv['GB/s']:8.1f} GB/s  alg {kv['alg_MB']:8.2f} MB"
+                + (f"  {kv['TFLOP/s']:7.2f} TFLOP/s" if kv["TFLOP/s"] else ""))
 
     def roofline_of(kname):
         nb, nf, us, n = per_kernel[kname]
@@ -379,18 +358,73 @@ def main():
             achieved, peak, unit = nb / (us * 1e-6) / 1e9, HBM_PEAK_GBS, "GB/s"
         else:
             achieved, peak, unit = nf / (us * 1e-6) / 1e12, MFMA_BF16_TFLOPS, "TFLOP/s"
-        return {"kernel": kname, "bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
-                "frac": round(achieved / peak, 4), "traffic": load_traffic(kname, w.name),
-                "launches_per_step": n, "alg_bytes_per_launch": round(nb / n), "alg_flops_per_launch": round(nf / n),
-                "avg_launch_us": round(us / n, 2),
-                "mfma_frac": round(nf / (us * 1e-6) / 1e12 / MFMA_BF16_TFLOPS, 4),
-                "hbm_frac": round(nb / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+        out = {"kernel": kname, "bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
+               "frac": round(achieved / peak, 4), "traffic": None,
+               "launches_per_step": n, "alg_bytes_per_launch": round(nb / n), "alg_flops_per_launch": round(nf / n),
+               "avg_launch_us": round(us / n, 2),
+               "mfma_frac": round(nf / (us * 1e-6) / 1e12 / MFMA_BF16_TFLOPS, 4),
+               "hbm_frac": round(nb / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+        out.update(load_counters(kname, w.name))
+        return out
 
     # the dominant kernel is the one with the most time per step
     order = sorted(per_kernel, key=lambda kn: -per_kernel[kn][2])
-    roofline = roofline_of(order[0])
-    others = {kn: roofline_of(kn) for kn in order[1:]}
+    return {"state": gs, "ms_per_step": ms_step, "rows_per_step": rows_per_step,
+            "step_hbm_GBps": round(total_bytes / (ms_step * 1e-3) / 1e9, 1),
+            "attn_rows_per_s": round(rows_per_step / (attn_us * 1e-6), 1),
+            "roofline": roofline_of(order[0]),
+            "roofline_other_kernels": {kn: roofline_of(kn) for kn in order[1:]},
+            "kernels": kernels}
 
+
+# ---- main ----------------------------------------------------------------------------------------------
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="C4")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-prune", action="store_true")
+    ap.add_argument("--no-configs", action="store_true", help="only the 32K workload (no per-workload summaries)")
+    ap.add_argument("--decode-only", action="store_true", help="only the decode measurement (for traces)")
+    ap.add_argument("--copy-calib", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; there is no multi-GPU path (asked for {args.gpus}): "
+              "the step would shard by head with one small all-gather of row-score partials.", flush=True)
+        sys.exit(2)
+    import torch
+    torch.cuda.set_device(0)
+    if args.copy_calib:
+        copy_calib()
+        return
+
+    from paper_2609_29812_amd import driver
+    from paper_2609_29812_amd import flashloop as fl
+    from workloads import get, make_layer
+    from workloads.gen_device import make_layer_device
+
+    fl.load()
+    w = get(args.workload)
+    t0 = time.time()
+    st = make_layer(w)
+    log(f"[bench] generated {w.name} in {time.time() - t0:.1f}s")
+
+    def up(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda().view(torch.bfloat16)
+
+    dev = {n: [up(a) for a in getattr(st, n)] for n in "qkv"}
+    if args.decode_only:
+        gs = driver.setup(dev["q"][0], dev["k"][0], dev["v"][0], w.base_bits, w.group, w.n_sink, w.top_cols,
+                          w.window)
+        print(json.dumps({"decode": decode_bench(w, gs, fl, torch)}), flush=True)
+        return
+    m = measure(w, dev, driver, fl, torch, args.steps, args.warmup, log_calls=True)
+    gs = m["state"]
+    ms_step = m["ms_per_step"]
+    rows_per_step = m["rows_per_step"]
     result = {
         "metric": METRIC,
         "value": round(rows_per_step / (ms_step * 1e-3), 1),
@@ -404,16 +438,37 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": w.name, "batch": B, "seq": N, "heads": H, "head_dim": d, "loops": w.loops,
-                   "sparse_loops": f"2-{w.loops}", "rows_per_step": rows_per_step,
-                   "k_per_loop": [w.k(r) for r in range(2, w.loops + 1)], "column_budget": w.col_budget,
-                   "window": w.window, "residual_bits": list(w.bits), "group": w.group},
-        "step_hbm_GBps": round(total_bytes / (ms_step * 1e-3) / 1e9, 1),
-        "attn_rows_per_s": round(rows_per_step / (attn_us * 1e-6), 1),
-        "roofline": roofline,
-        "roofline_other_kernels": others,
-        "kernels": kernels,
+        "config": workload_config(w),
+        "step_hbm_GBps": m["step_hbm_GBps"],
+        "attn_rows_per_s": m["attn_rows_per_s"],
+        "roofline": m["roofline"],
+        "roofline_other_kernels": m["roofline_other_kernels"],
+        "kernels": m["kernels"],
     }
+    if not args.no_configs:
+        result["configs"] = {}
+        for name in ("C1", "C2", "C3", "C5"):
+            wc = get(name)
+            t0 = time.time()
+            devc = make_layer_device(wc)
+            torch.cuda.synchronize()
+            log(f"[bench] generated {wc.name} on the device in {time.time() - t0:.1f}s")
+            mc = measure(wc, devc, driver, fl, torch, max(5, args.steps // 2), max(2, args.warmup // 2))
+            rec = {"workload": wc.name, "config": workload_config(wc), "rows_per_step": mc["rows_per_step"],
+                   "ms_per_step": round(mc["ms_per_step"], 4),
+                   "rows_per_s": round(mc["rows_per_step"] / (mc["ms_per_step"] * 1e-3), 1),
+                   "attn_rows_per_s": mc["attn_rows_per_s"], "step_hbm_GBps": mc["step_hbm_GBps"],
+                   "roofline": mc["roofline"], "roofline_other_kernels": mc["roofline_other_kernels"],
+                   "attn_us_per_loop": {k_: v_["us"] for k_, v_ in mc["kernels"].items() if k_.startswith("attn")},
+                   "data": "synthetic, drawn on the device with the same recipe (throughput does not depend on "
+                           "the values)"}
+            if wc.layers > 1:
+                rec["stack"] = {"layers": wc.layers, "ms_per_step": round(mc["ms_per_step"] * wc.layers, 3),
+                                "note": f"{wc.layers} x the layer-0 step (every layer has the same shapes and "
+                                        "budgets; only the seeds differ)"}
+            result["configs"][name] = rec
+            del devc, mc
+            torch.cuda.empty_cache()
     if not args.no_decode:
         result["decode"] = decode_bench(w, gs, fl, torch)
     if not args.no_prune:

@@ -568,7 +568,9 @@ int launch_seg_cur(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v
                    const int32_t* cols, int c_list, int window, int B, int N, int H, int d, float sm_scale,
                    float* lse_ref, float* o, const float* term_prev, const float* mass_prev,
                    const int32_t* slot_prev, int k_prev, float* term_out, float* mass_out, hipStream_t st) {
-  if (c_list > kSegListCap || (d != 64 && d != 128) || k < 1) return FL_E_UNSUPPORTED;
+  // (without a band, the 64-row kernel over the list alone measured faster: the segment layout pays off
+  // when the band's HBM stream is there to overlap)
+  if (window < 1 || c_list > kSegListCap || (d != 64 && d != 128) || k < 1) return FL_E_UNSUPPORTED;
   // the descriptor table holds every position: at most ceil(c_list / 32) list tiles and ceil(N / 32) + 1 band
   // tiles, plus one empty position per kind when the counts are odd
   if ((c_list + kBN - 1) / kBN + (N + kBN - 1) / kBN + 3 > kSegTileCap) return FL_E_UNSUPPORTED;
