@@ -59,6 +59,13 @@ const char* fl_status_str(int status);
 const char* fl_last_error(void);
 int fl_abi_version(void);
 
+/* Debugging aid: with on != 0 (or the environment variable FL_CHECK_INDICES set to a non-zero value when the
+ * library is first used), every call that takes index lists first synchronizes its stream, copies the lists
+ * to the host and returns FL_E_RANGE (launching nothing) if one is not strictly ascending or holds an entry
+ * outside its range (rows and columns in [0, N), or [0, T) for decode).  Off by default; not usable under
+ * stream capture.  Process-wide. */
+void fl_set_index_checks(int on);
+
 /* ------------------------------------------------------------------------------------------------
  * (1) Token selection -- Section 4.1; Appendix D.1, Eq. 5.
  *
@@ -207,8 +214,12 @@ int fl_kv_residual_dequant_kv(const uint8_t* k_codes, const uint16_t* k_scale, c
  *   ws, ws_bytes      : workspace of at least fl_loop_sparse_attn_ws(...) bytes (may be NULL if 0).
  *                       Scratch: a prep kernel fills it with the column records of every tile on each
  *                       call (about 8 * (2 B H c_list + B (N + k)) bytes; FL_E_SHAPE above 2^31).
- * Attention products use bf16 MFMA with fp32 accumulation for q.k and fp16 MFMA for p.v (values are
- * converted bf16 -> fp16, exact for |v| in [2^-14, 65504]); softmax and the update are fp32.
+ * Precision.  q.k is a bf16 MFMA product with fp32 accumulation; softmax and the update are fp32.  p.v
+ * depends on the path: the dense loop, the two-pass loop and the add pass over current caches with a band
+ * (window > 0) convert the value rows to fp16 and multiply fp16 probabilities (exact conversion for
+ * 2^-14 <= |v| <= 65504; smaller magnitudes round to a multiple of 2^-24; values beyond 65504 in magnitude
+ * overflow to infinity and are outside the supported input range); the other add-pass paths keep values
+ * in bf16 and split each probability into two bf16 parts (about 16 significant bits).
  * ---------------------------------------------------------------------------------------------- */
 enum fl_attn_flags { FL_ATTN_DENSE = 1 };
 
@@ -348,8 +359,9 @@ int fl_decode_step_noalloc(const uint16_t* q, const uint16_t* k_cache, const uin
  *   cols_next  : int32 [B, H, ns + t_next] out, 0 <= t_next <= c_list - ns.
  *   ws         : at least fl_prune_columns_ws(B, H, k, c_list, n_sink) bytes (fp64 partial sums of
  *                256-row chunks; H * ceil(k / 256) <= 65535).
- * Three launches: the fp64 statistic per chunk of updated rows (a thread pair per entry against staged
- * query rows), the ordered sum of the chunks, and the top-k.
+ * Three launches: the fp64 statistic per 256-row chunk of updated rows (dot products on fp64 matrix
+ * instructions, 16 list entries per wave against query rows staged in LDS), the ordered sum of the chunks,
+ * and the top-k.
  * ---------------------------------------------------------------------------------------------- */
 size_t fl_prune_columns_ws(int B, int H, int k, int c_list, int n_sink);
 

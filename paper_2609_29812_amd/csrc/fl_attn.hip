@@ -1526,6 +1526,10 @@ static int loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev, const
              "fl_loop_sparse_attn: workspace of %zu bytes required", need);
   if (k == 0) return FL_OK;
   hipStream_t st = as_stream(stream);
+  if (!dense) {
+    FL_CHECK_LIST("fl_loop_sparse_attn", "rows", rows, B, k, 0, N, st);
+    FL_CHECK_LIST("fl_loop_sparse_attn", "cols", cols, (int64_t)B * H, c_list, 0, N, st);
+  }
   AttnArgs a{};
   a.q_cur = q_cur;
   a.q_prev = (dense || reuse) ? nullptr : q_prev;

@@ -442,6 +442,7 @@ static int residual_quant(const char* fn, const uint16_t* x_cur, const uint16_t*
   if (rc != FL_OK) return rc;
   if (k == 0) return FL_OK;
   hipStream_t st = as_stream(stream);
+  FL_CHECK_LIST(fn, "idx", idx, B, k, 0, N, st);
   const int HD = H * d;
   if (bits == 16) {
     dim3 grid((unsigned)(((int64_t)k * (HD / 8) + 255) / 256), B);
@@ -516,6 +517,7 @@ static int residual_quant_kv(const char* fn, const uint16_t* k_cur, uint16_t* k_
   const int64_t blocks = ((int64_t)a.kx * a.ky + a.vx) * B;
   FL_REQUIRE(blocks < ((int64_t)1 << 31), FL_E_SHAPE, "%s: grid too large", fn);
   hipStream_t st = as_stream(stream);
+  FL_CHECK_LIST(fn, "idx", idx, B, k, 0, N, st);
 #define FL_QKV(BB, SS, RR) quant_kv_kernel<BB, SS, RR><<<(unsigned)blocks, 256, 0, st>>>(a)
 #define FL_QKV_BITS(BB)                                   \
   switch (group) {                                        \
@@ -627,6 +629,7 @@ extern "C" int fl_kv_residual_dequant_kv(const uint8_t* k_codes, const uint16_t*
   a.k = k; a.N = N; a.HD = H * d; a.G = group; a.half = (int)half;
   dim3 grid((unsigned)(2 * half), B);
   hipStream_t st = as_stream(stream);
+  FL_CHECK_LIST("fl_kv_residual_dequant_kv", "idx", idx, B, k, 0, N, st);
   if (bits == 16) {   // raw payload: both axes copy the same way
     dequant_kv_kernel<16><<<grid, 256, 0, st>>>(a);
   } else if (bits == 2) {
@@ -656,6 +659,7 @@ extern "C" int fl_kv_residual_dequant(const uint8_t* codes, const uint16_t* scal
   const int HD = H * d;
   dim3 grid((unsigned)(((int64_t)k * (HD / 8) + 255) / 256), B);
   hipStream_t st = as_stream(stream);
+  FL_CHECK_LIST("fl_kv_residual_dequant", "idx", idx, B, k, 0, N, st);
 #define FL_DQ(BB, AA) \
   dequant_kernel<BB, AA><<<grid, 256, 0, st>>>(codes, scale, zero, idx, k, N, HD, group, x_hat, out_rows)
   if (bits == 16) FL_DQ(16, 0);
@@ -685,6 +689,7 @@ extern "C" int fl_kv_keep_recent(const uint16_t* x_cur, const int32_t* idx, int 
   const int HD = H * d;
   const int64_t work = (int64_t)n_last * (HD / 8);
   dim3 grid((unsigned)((work + 255) / 256), B);
+  FL_CHECK_LIST("fl_kv_keep_recent", "idx", idx, B, k, 0, N, as_stream(stream));
   keep_recent_kernel<<<grid, 256, 0, as_stream(stream)>>>(x_cur, idx, k, N, HD, std::max(0, N - tail), n_last,
                                                           cache, rows);
   return check_launch("keep_recent_kernel");

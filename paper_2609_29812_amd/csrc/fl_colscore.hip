@@ -340,6 +340,8 @@ extern "C" int fl_prune_columns(const uint16_t* q, const uint16_t* k_cache, cons
   FL_REQUIRE(need == 0 || (ws && ws_bytes >= need), FL_E_WORKSPACE,
              "fl_prune_columns: workspace of %zu bytes required", need);
   hipStream_t st = as_stream(stream);
+  FL_CHECK_LIST("fl_prune_columns", "rows", rows, B, k, 0, N, st);
+  FL_CHECK_LIST("fl_prune_columns", "cols", cols, (int64_t)B * H, c_list, 0, N, st);
   if (n_ent == 0) {                       // the list is all sinks: it is kept as it is
     if (hipMemcpyAsync(cols_next, cols, (size_t)B * H * ns * sizeof(int32_t), hipMemcpyDeviceToDevice, st) !=
         hipSuccess)

@@ -30,6 +30,18 @@ int check_launch(const char* what);
 
 inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
+// The optional index-list check (fl_set_index_checks / FL_CHECK_INDICES): n_lists lists of len entries,
+// each strictly ascending within [lo, hi); FL_E_RANGE otherwise.  Synchronizes `st` and copies the lists to
+// the host, so it is a debugging aid; FL_OK without any work when the check is off.
+bool index_checks_on();
+int check_index_lists(const char* fn, const char* name, const int32_t* list, int64_t n_lists, int len, int lo,
+                      int hi, hipStream_t st);
+#define FL_CHECK_LIST(fn, name, list, n_lists, len, lo, hi, st)                                   \
+  do {                                                                                            \
+    const int fl_rc_ = ::fl::check_index_lists((fn), (name), (list), (n_lists), (len), (lo), (hi), (st)); \
+    if (fl_rc_ != FL_OK) return fl_rc_;                                                           \
+  } while (0)
+
 // Top-k of `segments` key rows (fl_select.hip): segment s selects the k largest of keys[s * key_stride +
 // 0..n-1] (ties to the lower position), writes their ids (cand[s * cand_stride + p], or id_base + p)
 // ascending at out[s * out_stride + n_prefix ..], ids 0..n_prefix-1 first, and optionally the slot map.

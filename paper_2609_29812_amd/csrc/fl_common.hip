@@ -1,9 +1,48 @@
 // Status strings, the thread-local error message and launch checking for the C ABI.
 #include "fl_common.h"
 
+#include <atomic>
+#include <cstdlib>
 #include <cstring>
+#include <vector>
 
 namespace fl {
+
+// index-list checks: off unless FL_CHECK_INDICES is set to a non-zero value, or fl_set_index_checks(1)
+static std::atomic<int> g_checks{-1};
+
+bool index_checks_on() {
+  int v = g_checks.load(std::memory_order_relaxed);
+  if (v < 0) {
+    const char* e = std::getenv("FL_CHECK_INDICES");
+    v = (e && *e && std::strcmp(e, "0") != 0) ? 1 : 0;
+    int expect = -1;
+    g_checks.compare_exchange_strong(expect, v);
+    v = g_checks.load(std::memory_order_relaxed);
+  }
+  return v > 0;
+}
+
+int check_index_lists(const char* fn, const char* name, const int32_t* list, int64_t n_lists, int len, int lo,
+                      int hi, hipStream_t st) {
+  if (!index_checks_on() || list == nullptr || n_lists <= 0 || len <= 0) return FL_OK;
+  hipError_t e = hipStreamSynchronize(st);
+  FL_REQUIRE(e == hipSuccess, FL_E_HIP, "%s: index check: stream synchronization failed: %s", fn,
+             hipGetErrorString(e));
+  std::vector<int32_t> h((size_t)n_lists * (size_t)len);
+  e = hipMemcpy(h.data(), list, h.size() * sizeof(int32_t), hipMemcpyDeviceToHost);
+  FL_REQUIRE(e == hipSuccess, FL_E_HIP, "%s: index check: copy of %s failed: %s", fn, name, hipGetErrorString(e));
+  for (int64_t r = 0; r < n_lists; ++r) {
+    const int32_t* p = h.data() + r * len;
+    for (int i = 0; i < len; ++i) {
+      FL_REQUIRE(p[i] >= lo && p[i] < hi, FL_E_RANGE, "%s: %s[%lld][%d] = %d outside [%d, %d)", fn, name,
+                 (long long)r, i, p[i], lo, hi);
+      FL_REQUIRE(i == 0 || p[i] > p[i - 1], FL_E_RANGE, "%s: %s[%lld] is not strictly ascending at %d (%d after %d)",
+                 fn, name, (long long)r, i, p[i], p[i - 1]);
+    }
+  }
+  return FL_OK;
+}
 
 static thread_local char g_last_error[512] = "";
 
@@ -41,3 +80,5 @@ extern "C" const char* fl_status_str(int status) {
 extern "C" const char* fl_last_error(void) { return fl::g_last_error; }
 
 extern "C" int fl_abi_version(void) { return FL_ABI_VERSION; }
+
+extern "C" void fl_set_index_checks(int on) { fl::g_checks.store(on ? 1 : 0, std::memory_order_relaxed); }

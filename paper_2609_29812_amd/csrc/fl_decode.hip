@@ -390,6 +390,7 @@ static int decode_step(const char* fn, bool use_scratch, const uint16_t* q, cons
   }
   FL_REQUIRE(ws && ws_bytes >= L.total, FL_E_WORKSPACE, "%s: workspace of %zu bytes required", fn, L.total);
   hipStream_t st = as_stream(stream);
+  FL_CHECK_LIST(fn, "cols", cols, (int64_t)B * H, c, 0, T, st);
   char* base = static_cast<char*>(ws);
   DecodeArgs a{};
   a.q = q; a.k = k_cache; a.v = v_cache; a.cols = cols; a.mass = mass; a.sub = sub; a.o = o; a.lse = lse;

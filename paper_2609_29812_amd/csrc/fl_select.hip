@@ -461,6 +461,7 @@ extern "C" int fl_select_tokens(const uint16_t* k_cur, const uint16_t* k_prev,
   FL_REQUIRE(k == 0 || out_idx, FL_E_NULL, "fl_select_tokens: out_idx is required when k > 0");
   FL_REQUIRE(eps >= 0.0, FL_E_RANGE, "fl_select_tokens: eps must be >= 0");
   hipStream_t st = as_stream(stream);
+  FL_CHECK_LIST("fl_select_tokens", "cand", cand, B, n_cand, 0, N, st);
   // k == n_cand keeps every candidate: the scoring launch also writes the selection (no top-k launch)
   const bool take_all = k == n_cand && k > 0;
   if (n_cand > 0) {

@@ -32,6 +32,7 @@ _SIGNATURES = {
     "fl_status_str": (ctypes.c_char_p, [_c_i]),
     "fl_last_error": (ctypes.c_char_p, []),
     "fl_abi_version": (_c_i, []),
+    "fl_set_index_checks": (None, [_c_i]),
     "fl_select_tokens": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_i, _c_i, _c_i, _c_p, _c_i, _c_i, _c_i, _c_d,
                                 _c_p, _c_p, _c_p, _c_p]),
     "fl_kv_residual_quant": (_c_i, [_c_p, _c_p, _c_p, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i,
@@ -87,6 +88,11 @@ def load(path: str = LIB_PATH):
         fn.argtypes = args
     _lib = lib
     return lib
+
+
+def set_index_checks(on: bool):
+    """Turn the library's index-list checks on or off (every call then validates its lists on the host)."""
+    load().fl_set_index_checks(1 if on else 0)
 
 
 def _check(rc: int, fn: str):

@@ -470,3 +470,42 @@ def test_results_are_deterministic(F):
         outs.append([down(gs.o), down(gs.lse), down_bits16(gs.k_hat), down(gs.cols), down(gs.base["col_key"])])
     for a, b in zip(*outs):
         assert np.array_equal(a.view(np.uint8), b.view(np.uint8))
+
+
+def test_ragged_batch_budgets_on_single_element_views(F):
+    """A token budget per batch element (Appendix D.1, Eq. 5 with its own k_b^(r) per element): every entry
+    point takes one k for the whole batch, so a ragged batch runs the per-loop step once per element on
+    B = 1 views of the batched tensors (batch is the leading dimension, so each view is contiguous) and
+    must match the oracle's chain run on that element alone, with that element's budgets."""
+    from paper_2609_29812_amd import driver
+    from workloads.gen import LoopStates
+    w = get("C5").replace(batch=3, seq=1500, heads=2, head_dim=64, loops=4, hot_frac=(0.3, 0.2, 0.1),
+                          topk_frac=(0.3, 0.2, 0.1), bits=(4, 4, 2), col_budget=4 + 120, group=32)
+    budgets = [(0.3, 0.2, 0.1), (0.15, 0.15, 0.05), (0.4, 0.1, 0.02)]
+    st = make_layer(w)
+    dev = {n: [up_bf16(a) for a in getattr(st, n)] for n in "qkv"}
+    for b, fr in enumerate(budgets):
+        wb = w.replace(name=f"ragged-b{b}", batch=1, topk_frac=fr)
+        sb = LoopStates(wb, 0, [a[b:b + 1] for a in st.q], [a[b:b + 1] for a in st.k], [a[b:b + 1] for a in st.v],
+                        [[hot[b]] for hot in st.hot])
+        rec = chain.run_layer(sb)
+        view = {n: [t[b:b + 1] for t in dev[n]] for n in "qkv"}
+        say(f"ragged element {b}: k per loop {[wb.k(r) for r in range(2, wb.loops + 1)]}")
+        gs = driver.setup(view["q"][0], view["k"][0], view["v"][0], wb.base_bits, wb.group, wb.n_sink,
+                          wb.top_cols, wb.window)
+        for lr in rec.loops:
+            r = lr.r
+            out = driver.sparse_step(gs, view["q"][r - 1], view["q"][r - 2], view["k"][r - 1], view["k"][r - 2],
+                                     view["v"][r - 1], view["v"][r - 2], wb.k(r), wb.bits_at(r), keep=True)
+            torch.cuda.synchronize()
+            assert np.array_equal(down(out["idx"]), lr.idx), f"element {b} loop {r}: active rows"
+            assert np.array_equal(down(out["codes_k"]), lr.enc_k["codes"]), f"element {b} loop {r}: K codes"
+            assert np.array_equal(down(out["codes_v"]), lr.enc_v["codes"]), f"element {b} loop {r}: V codes"
+            assert_close(down(gs.o), _dict_to_array(lr.o, 1, wb.heads), f"element {b} loop {r} o")
+            assert_close(down(gs.lse), _dict_to_array(lr.lse, 1, wb.heads), f"element {b} loop {r} lse")
+        assert np.array_equal(down_bits16(gs.k_hat), rec.k_hat), f"element {b}: final K cache"
+        assert np.array_equal(down_bits16(gs.v_hat), rec.v_hat), f"element {b}: final V cache"
+    # the views never wrote outside their element: the batched input tensors are untouched
+    for n in "qkv":
+        for r in range(w.loops):
+            assert np.array_equal(down_bits16(dev[n][r]), getattr(st, n)[r]), f"input {n}{r + 1} was modified"
