@@ -7,14 +7,13 @@
 // j + w <= i so that a column in both is counted once.
 //
 // Work decomposition.  One workgroup of 8 waves takes a segment of up to 128 consecutive updated rows of
-// one (batch, head).  The rows form eight 16-row groups; wave (team t, index w) holds groups w and w + 4
-// (query fragments, running maxima, sums and output blocks of both), so one K/V fragment read from LDS
-// feeds two groups.  The column tiles of the segment -- the list entries the segment's last row can see,
-// and the band columns from its first row's band start to its last row -- form one sequence in which
-// list and band tiles are interleaved evenly (the band tiles stream from HBM while the list tiles, shared
-// by every segment of the head and kept in L2, keep the matrix cores busy).  Step s gives tile 2s to team
-// 0 and tile 2s + 1 to team 1; each team keeps its own softmax state, and the two are merged per row at
-// the end.
+// one (batch, head).  The rows form four 32-row groups, each held by one wave of each team (query
+// fragments, running maximum, sum and output blocks).  The column tiles of the segment -- the
+// list entries the segment's last row can see, and the band columns from its first row's band start to
+// its last row -- form one sequence in which list and band tiles are interleaved evenly (the band tiles
+// stream from HBM while the list tiles, shared by every segment of the head and kept in L2, keep the
+// matrix cores busy).  Step s gives tile 2s to team 0 and tile 2s + 1 to team 1; each team keeps its own
+// softmax state, and the two are merged per row at the end.
 //
 // L2 sharing of the band.  Neighbouring segments of a head need the same band columns around their
 // boundary (about w columns).  Each segment walks the band tiles it shares with a neighbour before the
@@ -26,11 +25,9 @@
 // steps (two tiles each) three steps ahead; out-of-range offsets read zeros.  Each wave converts the value
 // rows its own DMA wrote from bf16 to fp16 in place (exact for 2^-14 <= |v| <= 65504; smaller magnitudes
 // round to a multiple of 2^-24; larger ones overflow) before the step's barrier.  Contractions: S^T = K Q^T
-// on v_mfma_f32_16x16x32_bf16 (lane (j, g) holds columns 16c + 4g .. +3 of row j), O^T += V^T P^T on
-// v_mfma_f32_16x16x32_f16 with V read transposed and P rounded to fp16; that lane layout of S^T is the
-// B-operand layout of P^T when the transposed V reads follow the k order (4g .. 4g+3, 16+4g .. 16+4g+3),
-// so P needs no shuffle.  Within a tile the two groups' phases are interleaved in program order (the
-// products of one group between the vector instructions of the other), as a wave issues in order.
+// on v_mfma_f32_32x32x16_bf16 (lane (r, h) holds columns 8j + 4h .. +3, j = 0..3, of row r of the group),
+// O^T += V^T P^T on v_mfma_f32_32x32x16_f16 with V read transposed and P rounded to fp16; the transposed V
+// reads take the columns in the order the lane already holds them, so P needs no shuffle.
 #include "fl_attn_util.h"
 
 #include <algorithm>
@@ -38,7 +35,7 @@
 
 namespace fl {
 
-constexpr int kSegRows = 128;        // rows per segment at most (8 groups of 16)
+constexpr int kSegRows = 128;        // rows per segment at most (4 groups of 32)
 constexpr int kSegListCap = 2048;    // list entries kept in LDS
 constexpr int kSegTileCap = 2048;    // tile descriptors kept in LDS (list tiles + band tiles of a segment)
 constexpr int kSegSteps = 4;         // ring depth in steps
@@ -64,8 +61,8 @@ struct SegArgs {
 
 template <int D>
 __global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
-  constexpr int KS = D / 32;              // k-steps of QK^T (32 dims each)
-  constexpr int DB = D / 16;              // 16-dim output blocks
+  constexpr int KS = D / 16;              // k-steps of QK^T (16 dims each)
+  constexpr int DB = D / 32;              // 32-dim output blocks
   constexpr int CH = D / 8;               // 16-byte chunks per row
   constexpr int CPI = 64 / CH;            // tile columns covered by one 1 KB LDS-DMA instruction
   constexpr int IPT = kBN / CPI;          // instructions per tensor and tile
@@ -77,14 +74,18 @@ __global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
   __shared__ Slot<D> ring0[2], ring1[2], ring2[2], ring3[2];   // step slot s, team t: ring<s>[t]
   __shared__ __attribute__((aligned(16))) int lst[kSegListCap + kBN];   // the (b, h) list, kPad-padded
   __shared__ int2 tdesc[kSegTileCap];     // per sequence position: first column or entry, kind, group bits
-  __shared__ int s_grp[16];               // first and last row of each of the 8 groups
+  __shared__ int s_grp[8];                // first and last row of each of the 4 groups
   __shared__ int s_meta[1];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int team = wave >> 2, w4 = wave & 3;
-  const int j16 = lane & 15, g4 = lane >> 4;
+  // the wave's row group: team 0 wave w takes group w, team 1 wave w group w + 2 (mod 4), so the two waves
+  // of one group sit on different SIMDs when waves w and w + 4 share one (a band tile is often seen by one
+  // or two neighbouring groups only)
+  const int grp = team ? (w4 + 2) & 3 : w4;
+  const int r32 = lane & 31, hw = lane >> 5;
 
   // ---- work item -> (batch*head, segment); the segments of one (batch, head) stay on one XCD ----------
   const int n_bh = a.B * a.H;
@@ -104,20 +105,17 @@ __global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
   const int P1 = min(P0 + a.seg_rows, a.k);
   const int min_row = rowp[P0], max_row = rowp[P1 - 1];
 
-  // ---- the wave's two groups (g = w4, w4 + 4) --------------------------------------------------------
-  int row_i[2], pos[2];
-  bf16x8 qa[2][KS];
-#pragma unroll
-  for (int gi = 0; gi < 2; ++gi) {
-    const int gp0 = P0 + 16 * (w4 + 4 * gi);
-    pos[gi] = gp0 + j16;
-    const bool ok = pos[gi] < P1;
-    row_i[gi] = ok ? rowp[pos[gi]] : -1;
-    const int64_t qoff = ((int64_t)b * a.N + (ok ? row_i[gi] : 0)) * HD + (int64_t)h * D + g4 * 8;
+  // ---- the wave's group: rows 32 grp .. +31 of the segment --------------------------------------------
+  const int pos = P0 + 32 * grp + r32;
+  const bool row_ok = pos < P1;
+  const int row_i = row_ok ? rowp[pos] : -1;
+  bf16x8 qf[KS];                          // B operand of S^T = K Q^T: row r32, dims 16 ks + 8 hw .. +7
+  {
+    const int64_t qoff = ((int64_t)b * a.N + (row_ok ? row_i : 0)) * HD + (int64_t)h * D + hw * 8;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      const uint4 w = ok ? *reinterpret_cast<const uint4*>(a.q + qoff + ks * 32) : make_uint4(0, 0, 0, 0);
-      qa[gi][ks] = __builtin_bit_cast(bf16x8, w);
+      const uint4 w = row_ok ? *reinterpret_cast<const uint4*>(a.q + qoff + ks * 16) : make_uint4(0, 0, 0, 0);
+      qf[ks] = __builtin_bit_cast(bf16x8, w);
     }
   }
 
@@ -126,11 +124,11 @@ __global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
   const int w = a.window;
   const int lim = max_row - w;
   if (tid == 0) s_meta[0] = 0;
-  if (tid < 8) {                          // group bounds (a group without rows gets last row -1)
-    const int gp0 = P0 + 16 * tid;
+  if (tid < 4) {                          // group bounds (a group without rows gets last row -1)
+    const int gp0 = P0 + 32 * tid;
     const bool has = gp0 < P1;
     s_grp[2 * tid] = has ? rowp[gp0] : 0;
-    s_grp[2 * tid + 1] = has ? rowp[min(gp0 + 16, P1) - 1] : -1;
+    s_grp[2 * tid + 1] = has ? rowp[min(gp0 + 32, P1) - 1] : -1;
   }
   for (int i = tid; i < a.c_list; i += 512) lst[i] = cp[i];
   __syncthreads();
@@ -170,7 +168,7 @@ __global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
   // floor(p nLP / nP) (list pairs spread evenly through the band pairs); a position past the last tile of
   // its kind is empty (no group bits, no columns).
   //   x: first list entry (list tile) or first column (band tile), bit 31 set for a band tile;
-  //   y: bit g: group g sees some column of the tile; bit 8 + g: it sees every column (no mask);
+  //   y: bit g: group g (rows 32 g .. +31) sees some column of the tile; bit 8 + g: it sees every column;
   //      bits 16-20: the last existing column of the tile (band tiles end at the last row); bit 21: empty.
   for (int u = tid; u < n_tiles; u += 512) {
     const int pr = u >> 1, t = u & 1;
@@ -202,7 +200,7 @@ __global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
     }
     uint32_t bits = ((uint32_t)hi << 16) | ((uint32_t)empty << 21);
 #pragma unroll
-    for (int g = 0; g < 8; ++g) {
+    for (int g = 0; g < 4; ++g) {
       const int gmin = s_grp[2 * g], gmax = s_grp[2 * g + 1];
       const bool act = !empty & (gmax >= 0) & (c0 <= (is_list ? gmax - w : gmax)) & (is_list | (clast > gmin - w));
       const bool full = is_list ? clast <= gmin - w : (hi == kBN - 1) & (clast <= gmin) & (c0 > gmax - w);
@@ -225,18 +223,18 @@ __global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
   for (int t = 0; t < NIK; ++t) {
     const int inst = w4 * NIK + t;
     lcol[t] = inst * CPI + lane / CH;
-    lsw[t] = (uint32_t)((lane % CH) ^ swz16_f<D>(lcol[t])) * 16 + head_off;
+    lsw[t] = (uint32_t)((lane % CH) ^ swz32_f<D>(lcol[t])) * 16 + head_off;
   }
   struct Offs { uint32_t o[NIK]; };
-  auto tile_offs = [&](int u) {
+  auto tile_offs = [&](int u) __attribute__((always_inline)) {
     Offs r;
     const bool have = u < n_tiles;
     const int2 dsc = tdesc[have ? u : 0];
     const int dx = __builtin_amdgcn_readfirstlane(dsc.x), dy = __builtin_amdgcn_readfirstlane(dsc.y);
     const bool in_list = dx >= 0;
     const int f = dx & 0x7FFFFFFF;
-    const int hi = have & !((dy >> 21) & 1) ? (dy >> 16) & 31 : -1;   // tile columns c <= hi exist
-    const int fl = in_list & (hi >= 0) ? f : 0;
+    const int hi = (have & !((dy >> 21) & 1)) ? (dy >> 16) & 31 : -1;   // tile columns c <= hi exist
+    const int fl = (in_list & (hi >= 0)) ? f : 0;
 #pragma unroll
     for (int t = 0; t < NIK; ++t) {
       const int idl = lst[fl + lcol[t]];
@@ -245,7 +243,7 @@ __global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
     }
     return r;
   };
-  auto issue = [&](Slot<D>& sl, const Offs& of) {
+  auto issue = [&](Slot<D>& sl, const Offs& of) __attribute__((always_inline)) {
 #pragma unroll
     for (int t = 0; t < NI; ++t) {
       const int inst = w4 * NIK + (t % NIK);
@@ -257,31 +255,33 @@ __global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
     }
   };
 
-  // LDS read offsets of the fragments (elements).  K (A operand): row j16 (+16 for the second column
-  // block), data chunk 4 ks + g4.  V (transposed reads): lane (g4, t, q) reads dims 16 db + 4q of column
-  // 4 g4 + t (+16 for the second half of the k order), data chunk 2 db + (q >> 1).
-  int koff[KS], voff[DB];
+  // LDS read offsets (elements).  K (A operand of S^T = K Q^T): row r32, data chunk 2 ks + hw.  V
+  // (transposed reads for O^T += V^T P^T): lane (16 g + 4 t + q) points at V[col][dim0 + 4 q] of column
+  // 16 kb + 4 (g >> 1) + t (and the same + 8), dims 32 db + 16 (g & 1) + 4 q, so the transpose hands lane
+  // m of the group V[col_t][dim0 + m] and P^T needs no shuffle.
+  int koff[KS], voff[DB], voff8[DB];
   {
-    const int t4 = j16 >> 2, q = lane & 3;
-    const int colv = 4 * g4 + t4;
+    const int g16 = lane >> 4, m16 = lane & 15;
+    const int tq = m16 >> 2, q = m16 & 3;
+    const int col0 = 4 * (g16 >> 1) + tq;
+    const int c_lo = 2 * (g16 & 1) + (q >> 1);
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) koff[ks] = tofs + j16 * D + ((4 * ks + g4) ^ swz16_f<D>(j16)) * 8;
+    for (int ks = 0; ks < KS; ++ks) koff[ks] = tofs + r32 * D + ((2 * ks + hw) ^ swz32_f<D>(r32)) * 8;
 #pragma unroll
-    for (int db = 0; db < DB; ++db)
-      voff[db] = tofs + colv * D + ((2 * db + (q >> 1)) ^ swz16_f<D>(colv)) * 8 + 4 * (q & 1);
+    for (int db = 0; db < DB; ++db) {
+      voff[db] = tofs + col0 * D + ((4 * db + c_lo) ^ swz32_f<D>(col0)) * 8 + 4 * (q & 1);
+      voff8[db] = tofs + (col0 + 8) * D + ((4 * db + c_lo) ^ swz32_f<D>(col0 + 8)) * 8 + 4 * (q & 1);
+    }
   }
 
-  f32x4 acc[2][DB];
+  f32x16 acc[DB];                         // O^T blocks: lane (r32, hw) holds dims 32 db + 8 j + 4 hw + i
 #pragma unroll
-  for (int gi = 0; gi < 2; ++gi)
-#pragma unroll
-    for (int db = 0; db < DB; ++db) acc[gi][db] = f32x4{};
-  float run_max[2] = {-INFINITY, -INFINITY}, lsum[2] = {0.0f, 0.0f};   // log2 units; row sums
-  // per group: the row index less the lane's column offset within a band block (band masks)
-  const int rband[2] = {row_i[0] - 4 * g4, row_i[1] - 4 * g4};
+  for (int db = 0; db < DB; ++db) acc[db] = f32x16{};
+  float run_max = -INFINITY, lsum = 0.0f; // log2 units; the lane's part of the row sum
+  const int rband = row_i - 4 * hw;       // the row less the lane's column offset within a block of 8
 
   // ---- this wave's value rows of a tile, bf16 -> fp16 in place (the 16 bytes per lane its DMA wrote) ---
-  auto convert = [&](Slot<D>& sl) {
+  auto convert = [&](Slot<D>& sl) __attribute__((always_inline)) {
 #pragma unroll
     for (int t = 0; t < NIK; ++t) {
       u32x4* pv = reinterpret_cast<u32x4*>(sl.v + tofs + (w4 * NIK + t) * 512 + lane * 8);
@@ -293,151 +293,82 @@ __global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
     }
   };
 
-  // ---- one tile for the wave's active groups (A0, A1) of one kind (list or band): straight-line code ----
+  // ---- one tile (list or band) for the wave's group: one code path for both kinds, so the accumulators
+  // keep their registers across tiles; only the mask differs, and a tile every row of the group sees in
+  // full skips it
   const float pinf = a.pinf;
   const float sc = a.scale_log2;
-  auto body = [&](auto list_c, auto a0_c, auto a1_c, int f, uint32_t dy, const Slot<D>& sl) {
-    constexpr bool IS_LIST = decltype(list_c)::value;
-    constexpr bool A0 = decltype(a0_c)::value, A1 = decltype(a1_c)::value;
-    constexpr bool AG[2] = {A0, A1};
-    // every LDS read of the tile first
-    int4 ca_[2];
-    if constexpr (IS_LIST) {
-#pragma unroll
-      for (int c = 0; c < 2; ++c) ca_[c] = *reinterpret_cast<const int4*>(&lst[f + 16 * c + 4 * g4]);
-    }
-    u32x4 kw[KS][2];
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-      for (int c = 0; c < 2; ++c) kw[ks][c] = *reinterpret_cast<const u32x4*>(&sl.k[koff[ks] + 16 * c * D]);
-    // S^T = K Q^T for each active group (raw scores; the scale goes into the exponent's multiply-add)
-    f32x4 sa[2][2];
-#pragma unroll
-    for (int gi = 0; gi < 2; ++gi) sa[gi][0] = sa[gi][1] = f32x4{};
-#pragma unroll
-    for (int gi = 0; gi < 2; ++gi) {
-      if constexpr (true) {
-        if (!AG[gi]) continue;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-          for (int c = 0; c < 2; ++c)
-            sa[gi][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kw[ks][c]), qa[gi][ks], sa[gi][c], 0, 0, 0);
-      }
-    }
-    // the value fragments once the key fragments are dead (their registers are reused)
-    __builtin_amdgcn_sched_barrier(0);
-    f16x8 vf[DB];                         // V^T fragments: the two halves of the tile's k order
-#pragma unroll
-    for (int db = 0; db < DB; ++db) {
-      const int o = voff[db];
-      const i16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(FL_LDS4(&sl.v[o]));
-      const i16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(FL_LDS4(&sl.v[o + 16 * D]));
-      vf[db] = __builtin_bit_cast(f16x8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
-    }
-    // masks (branch-free: a group that sees the whole tile gets bounds every column passes), row maxima
-    float tmax[2] = {-INFINITY, -INFINITY};
-#pragma unroll
-    for (int gi = 0; gi < 2; ++gi) {
-      if (!AG[gi]) continue;
-      const bool full = ((dy >> (8 + w4 + 4 * gi)) & 1) != 0;
-      if constexpr (IS_LIST) {            // list columns: j + w <= i
-        const int lim_i = full ? INT_MAX : row_i[gi] - w;
-#pragma unroll
-        for (int c = 0; c < 2; ++c) {
-          const int ci[4] = {ca_[c].x, ca_[c].y, ca_[c].z, ca_[c].w};
-#pragma unroll
-          for (int v = 0; v < 4; ++v) sa[gi][c][v] = ci[v] <= lim_i ? sa[gi][c][v] : -INFINITY;
-        }
-      } else {                            // band columns f + 16c + 4 g4 + v: i - w < j <= i
-        const uint32_t wl = full ? 0xFFFFFFFFu : (uint32_t)w;
-#pragma unroll
-        for (int c = 0; c < 2; ++c) {
-          const uint32_t d0 = (uint32_t)(rband[gi] - f - 16 * c);
-#pragma unroll
-          for (int v = 0; v < 4; ++v) sa[gi][c][v] = d0 - (uint32_t)v < wl ? sa[gi][c][v] : -INFINITY;
-        }
-      }
-      float t = fmax_nn(fmax_nn(fmax_nn(sa[gi][0][0], sa[gi][0][1], pinf), fmax_nn(sa[gi][0][2], sa[gi][0][3], pinf), pinf),
-                        fmax_nn(fmax_nn(sa[gi][1][0], sa[gi][1][1], pinf), fmax_nn(sa[gi][1][2], sa[gi][1][3], pinf), pinf),
-                        pinf);
-      auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(t), __float_as_uint(t), false, false);
-      t = fmax_nn(__uint_as_float(r[0]), __uint_as_float(r[1]), pinf);
-      r = __builtin_amdgcn_permlane32_swap(__float_as_uint(t), __float_as_uint(t), false, false);
-      t = fmax_nn(__uint_as_float(r[0]), __uint_as_float(r[1]), pinf);
-      tmax[gi] = t * sc;                  // log2 units (sc > 0 keeps the order; -inf stays -inf)
-    }
-    if constexpr (A0 && A1) {
-      // the second group's products between the first group's vector work
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
-        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);   // four VALU
-      }
-    }
-    // online softmax with a lazily raised reference (moved only when a score exceeds it by more than 8 in
-    // log2 units: probabilities stay <= 256 and rescaling is rare); one uniform branch for both groups
-    const bool raise0 = A0 && tmax[0] > run_max[0] + 8.0f;
-    const bool raise1 = A1 && tmax[1] > run_max[1] + 8.0f;
-    if (__builtin_amdgcn_ballot_w64(raise0 | raise1) != 0) {
-#pragma unroll
-      for (int gi = 0; gi < 2; ++gi) {
-        if (!AG[gi]) continue;
-        const bool raise = gi == 0 ? raise0 : raise1;
-        const float nm = raise ? tmax[gi] : run_max[gi];
-        const float alpha = raise ? __builtin_amdgcn_exp2f(run_max[gi] - nm) : 1.0f;   // exp2(-inf) = 0
-        lsum[gi] *= alpha;
-#pragma unroll
-        for (int db = 0; db < DB; ++db) acc[gi][db] *= alpha;
-        run_max[gi] = nm;
-      }
-    }
-    // probabilities, rounded to fp16 for O^T += V^T P^T
-    f16x8 pf[2];
-#pragma unroll
-    for (int gi = 0; gi < 2; ++gi) {
-      if (!AG[gi]) continue;
-      const float ref = run_max[gi] == -INFINITY ? 0.0f : run_max[gi];
-      float pr[8];
-#pragma unroll
-      for (int c = 0; c < 2; ++c)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          pr[4 * c + v] = __builtin_amdgcn_exp2f(__builtin_fmaf(sa[gi][c][v], sc, -ref));
-          lsum[gi] += pr[4 * c + v];
-        }
-      u32x4 pk;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) pk[e] = pack_f16x2(pr[2 * e], pr[2 * e + 1]);
-      pf[gi] = __builtin_bit_cast(f16x8, pk);
-#pragma unroll
-      for (int db = 0; db < DB; ++db)
-        acc[gi][db] = __builtin_amdgcn_mfma_f32_16x16x32_f16(vf[db], pf[gi], acc[gi][db], 0, 0, 0);
-    }
-    if constexpr (A0 && A1) {
-      // the first group's products between the second group's exponentials
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
-        __builtin_amdgcn_sched_group_barrier(0x002, 4, 1);
-      }
-    }
-  };
-  auto compute = [&](int dx, int dy, const Slot<D>& sl) {
+  auto compute = [&](int dx, int dy, const Slot<D>& sl) __attribute__((always_inline)) {
+    if (((dy >> grp) & 1) == 0) return;   // no row of the group sees a column of the tile
+    const bool full = ((dy >> (8 + grp)) & 1) != 0;
     const bool is_list = dx >= 0;         // uniform
     const int f = dx & 0x7FFFFFFF;
-    const bool a0 = ((dy >> w4) & 1) != 0, a1 = ((dy >> (w4 + 4)) & 1) != 0;
-    using T = std::true_type;
-    using F = std::false_type;
-    if (is_list) {
-      if (a0 & a1) body(T{}, T{}, T{}, f, (uint32_t)dy, sl);
-      else if (a0) body(T{}, T{}, F{}, f, (uint32_t)dy, sl);
-      else if (a1) body(T{}, F{}, T{}, f, (uint32_t)dy, sl);
-    } else {
-      if (a0 & a1) body(F{}, T{}, T{}, f, (uint32_t)dy, sl);
-      else if (a0) body(F{}, T{}, F{}, f, (uint32_t)dy, sl);
-      else if (a1) body(F{}, F{}, T{}, f, (uint32_t)dy, sl);
+    constexpr int NE = 16;                // scores per lane: columns 8 j + 4 hw + i of row r32
+    f32x16 sv = f32x16{};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const u32x4 kw = *reinterpret_cast<const u32x4*>(&sl.k[koff[ks]]);
+      sv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kw), qf[ks], sv, 0, 0, 0);
+    }
+    if (!full) {
+      if (is_list) {                      // list columns: j + w <= i
+        const int lim = row_i - w;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int4 c4 = *reinterpret_cast<const int4*>(&lst[f + 8 * j + 4 * hw]);
+          sv[4 * j + 0] = c4.x <= lim ? sv[4 * j + 0] : -INFINITY;
+          sv[4 * j + 1] = c4.y <= lim ? sv[4 * j + 1] : -INFINITY;
+          sv[4 * j + 2] = c4.z <= lim ? sv[4 * j + 2] : -INFINITY;
+          sv[4 * j + 3] = c4.w <= lim ? sv[4 * j + 3] : -INFINITY;
+        }
+      } else {                            // band columns f + 8 j + 4 hw + i: i - w < j <= i
+        const uint32_t d0 = (uint32_t)(rband - f);
+#pragma unroll
+        for (int v = 0; v < NE; ++v) {
+          const uint32_t off = (uint32_t)(8 * (v >> 2) + (v & 3));
+          sv[v] = d0 - off < (uint32_t)w ? sv[v] : -INFINITY;
+        }
+      }
+    }
+    float t = sv[0];
+#pragma unroll
+    for (int v = 1; v < NE; ++v) t = fmax_nn(t, sv[v], pinf);
+    {
+      const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(t), __float_as_uint(t), false, false);
+      t = fmax_nn(__uint_as_float(r[0]), __uint_as_float(r[1]), pinf);
+    }
+    const float tmax = t * sc;            // log2 units (sc > 0 keeps the order; -inf stays -inf)
+    // online softmax with a lazily raised reference (moved only when a score exceeds it by more than 8 in
+    // log2 units: probabilities stay <= 256 and rescaling is rare)
+    const bool raise = tmax > run_max + 8.0f;
+    if (__builtin_amdgcn_ballot_w64(raise) != 0) {
+      const float nm = raise ? tmax : run_max;
+      const float alpha = raise ? __builtin_amdgcn_exp2f(run_max - nm) : 1.0f;   // exp2(-inf) = 0
+      lsum *= alpha;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) acc[db] *= alpha;
+      run_max = nm;
+    }
+    const float ref = run_max == -INFINITY ? 0.0f : run_max;
+    float pr[NE];
+#pragma unroll
+    for (int v = 0; v < NE; ++v) {
+      pr[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[v], sc, -ref));
+      lsum += pr[v];
+    }
+    // O^T += V^T P^T, P rounded to fp16, two 16-column halves of the tile
+#pragma unroll
+    for (int kb = 0; kb < NE / 8; ++kb) {
+      const u32x4 pw = {pack_f16x2(pr[8 * kb + 0], pr[8 * kb + 1]), pack_f16x2(pr[8 * kb + 2], pr[8 * kb + 3]),
+                        pack_f16x2(pr[8 * kb + 4], pr[8 * kb + 5]), pack_f16x2(pr[8 * kb + 6], pr[8 * kb + 7])};
+      const f16x8 pf = __builtin_bit_cast(f16x8, pw);
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const i16x4 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(FL_LDS4(&sl.v[voff[db] + 16 * kb * D]));
+        const i16x4 vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(FL_LDS4(&sl.v[voff8[db] + 16 * kb * D]));
+        const i16x8 v8 = __builtin_shufflevector(va, vb, 0, 1, 2, 3, 4, 5, 6, 7);
+        acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, v8), pf, acc[db], 0, 0, 0);
+      }
     }
   };
 
@@ -457,7 +388,7 @@ __global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
   issue(ring2[0], tile_offs(4 + team));
   int u = team;                           // this team's position at the current step
   int2 dsc = tdesc[u < n_tiles ? u : 0];  // its descriptor, read one step ahead
-  auto step = [&](Slot<D>& cur, Slot<D>& nxt) {   // (the slots' first tiles; the team's is at tofs)
+  auto step = [&](Slot<D>& cur, Slot<D>& nxt) __attribute__((always_inline)) {   // (the slots' first tiles; the team's is at tofs)
     const Offs of = tile_offs(u + 6);
     const int dx = __builtin_amdgcn_readfirstlane(dsc.x), dy = __builtin_amdgcn_readfirstlane(dsc.y);
     const bool have = u < n_tiles;
@@ -478,53 +409,48 @@ __global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
   FL_WAIT_VM(0);
   lds_barrier();
 
-  // ---- merge the two teams' states per row: team 0 finishes group w4, team 1 group w4 + 4 -------------
-  // The other team's partial of the group goes through the (now idle) ring: per wave 16 rows x D fp32
-  // output values (DB x 64 lanes x 4) in slots 0 and 1, and the reference and sum of each row (64 lanes x 2)
-  // in slot 2.
-  constexpr int XO = DB * 64 * 4;         // floats per wave: two waves per slot half
-  auto xo_of = [&](int wv) {
-    Slot<D>* sl = (wv >> 2) ? ring1 : ring0;
-    return reinterpret_cast<float*>(sl[(wv >> 1) & 1].k) + (wv & 1) * XO;
-  };
-  auto xs_of = [&](int wv) { return reinterpret_cast<float*>(ring2[0].k) + wv * 128; };
-  float* xo_me = xo_of(wave);
-  float* xs_me = xs_of(wave);
-  const int other = wave ^ 4;             // the same w4 in the other team
-  const float* xo_ot = xo_of(other);
-  const float* xs_ot = xs_of(other);
-  // (team is uniform: the selects below pick whole registers, so no state is indexed dynamically)
-  const bool t1 = team != 0;
-#pragma unroll
-  for (int db = 0; db < DB; ++db)         // team 0 gives group w4 + 4, team 1 gives group w4
-    *reinterpret_cast<f32x4*>(&xo_me[(db * 64 + lane) * 4]) = t1 ? acc[0][db] : acc[1][db];
-  xs_me[lane * 2] = t1 ? run_max[0] : run_max[1];
-  xs_me[lane * 2 + 1] = t1 ? lsum[0] : lsum[1];
-  lds_barrier();
-  float m_o = xs_ot[lane * 2], l_o = xs_ot[lane * 2 + 1];
-  float m_s = t1 ? run_max[1] : run_max[0];
-  float l_s = t1 ? lsum[1] : lsum[0];
-  l_s = row4_add(l_s);
-  l_o = row4_add(l_o);
-  f32x4 o_acc[DB];
+  // ---- merge the two teams' states per row; team 0 finishes the group -------------------------------
+  // Team 1's partial goes through the (now idle) ring: per wave 32 rows x D fp32 output values (DB x 16 x
+  // 64 lanes) in slot grp of team 1's half, and the reference and sum of each lane's row (64 x 2) in slot
+  // 3 of team 0's half.
+  lsum = xor32_add(lsum);                 // the two half-waves hold disjoint columns of the same row
   {
-    // combine (reference m_s, sum l_s, acc) with (m_o, l_o, acc_o); an empty state has sum 0 and
-    // reference -inf, and contributes nothing (its factor is exp2(-inf) = 0)
-    const float mm = fmaxf(m_s, m_o);
-    const float fs = mm == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m_s - mm);
+    float* xs = reinterpret_cast<float*>(ring3[0].k) + grp * 128;
+    float* xo = reinterpret_cast<float*>(grp == 0 ? ring0[1].k : grp == 1 ? ring1[1].k : grp == 2 ? ring2[1].k
+                                                                                         : ring3[1].k);
+    if (team) {
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          *reinterpret_cast<f32x4*>(&xo[((db * 4 + j) * 64 + lane) * 4]) =
+              f32x4{acc[db][4 * j], acc[db][4 * j + 1], acc[db][4 * j + 2], acc[db][4 * j + 3]};
+      xs[lane * 2] = run_max;
+      xs[lane * 2 + 1] = lsum;
+    }
+    lds_barrier();
+    if (team) return;
+    const float m_o = xs[lane * 2], l_o = xs[lane * 2 + 1];
+    // combine (run_max, lsum, acc) with (m_o, l_o, team 1's acc); an empty state has sum 0 and reference
+    // -inf, and contributes nothing (its factor is exp2(-inf) = 0)
+    const float mm = fmaxf(run_max, m_o);
+    const float fs = mm == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(run_max - mm);
     const float fo = mm == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m_o - mm);
 #pragma unroll
-    for (int db = 0; db < DB; ++db) {
-      const f32x4 ao = *reinterpret_cast<const f32x4*>(&xo_ot[(db * 64 + lane) * 4]);
-      o_acc[db] = (t1 ? acc[1][db] : acc[0][db]) * fs + ao * fo;
-    }
-    l_s = l_s * fs + l_o * fo;
-    m_s = mm;
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const f32x4 ao = *reinterpret_cast<const f32x4*>(&xo[((db * 4 + j) * 64 + lane) * 4]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[db][4 * j + i] = acc[db][4 * j + i] * fs + ao[i] * fo;
+      }
+    lsum = lsum * fs + l_o * fo;
+    run_max = mm;
   }
-  // ---- epilogue: lane (j16, g4) holds dims 16 db + 4 g4 .. +3 of row j16 of its group -----------------
-  const int p = t1 ? pos[1] : pos[0];
-  if (p >= P1) return;
-  const int ri = t1 ? row_i[1] : row_i[0];
+  // ---- epilogue: lane (r32, hw) holds dims 32 db + 8 j + 4 hw .. +3 of row r32 of the group -------------
+  if (!row_ok) return;
+  const int p = pos;
+  const int ri = row_i;
   const int64_t orow = ((int64_t)b * a.N + ri) * HD + (int64_t)h * D;
   const int64_t lrow = ((int64_t)b * a.N + ri) * a.H + h;
   const int pp = a.slot_prev[(int64_t)b * a.N + ri];
@@ -533,31 +459,36 @@ __global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
   const float* subp = a.term_prev + tp * D;
   const int64_t trow = ((int64_t)b * a.k + p) * a.H + h;
   const bool keep_terms = a.term_out != nullptr;
-  if (!(msub > 0.0f) || !(l_s > 0.0f)) {  // empty column set or vanished mass: unchanged
+  if (!(msub > 0.0f) || !(lsum > 0.0f)) { // empty column set or vanished mass: unchanged
     if (keep_terms) {
 #pragma unroll
       for (int db = 0; db < DB; ++db)
-        *reinterpret_cast<float4*>(a.term_out + trow * D + db * 16 + 4 * g4) = make_float4(0, 0, 0, 0);
-      if (g4 == 0) a.mass_out[trow] = 0.0f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          *reinterpret_cast<float4*>(a.term_out + trow * D + db * 32 + 8 * j + 4 * hw) = make_float4(0, 0, 0, 0);
+      if (hw == 0) a.mass_out[trow] = 0.0f;
     }
     return;
   }
-  const float fm = msub / l_s;
+  const float fm = msub / lsum;
 #pragma unroll
-  for (int db = 0; db < DB; ++db) {
-    const int dim = db * 16 + 4 * g4;
-    const float4 sub = *reinterpret_cast<const float4*>(subp + dim);
-    const float4 add = make_float4(o_acc[db][0] * fm, o_acc[db][1] * fm, o_acc[db][2] * fm, o_acc[db][3] * fm);
-    float4 prev = *reinterpret_cast<const float4*>(a.o + orow + dim);
-    prev.x = prev.x - sub.x + add.x;
-    prev.y = prev.y - sub.y + add.y;
-    prev.z = prev.z - sub.z + add.z;
-    prev.w = prev.w - sub.w + add.w;
-    *reinterpret_cast<float4*>(a.o + orow + dim) = prev;
-    if (keep_terms) *reinterpret_cast<float4*>(a.term_out + trow * D + dim) = add;
-  }
-  if (g4 == 0) {
-    a.lse_ref[lrow] = (m_s + log2f(l_s)) * 0.6931471805599453f - logf(msub);
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int dim = db * 32 + 8 * j + 4 * hw;
+      const float4 sub = *reinterpret_cast<const float4*>(subp + dim);
+      const float4 add = make_float4(acc[db][4 * j] * fm, acc[db][4 * j + 1] * fm, acc[db][4 * j + 2] * fm,
+                                     acc[db][4 * j + 3] * fm);
+      float4 prev = *reinterpret_cast<const float4*>(a.o + orow + dim);
+      prev.x = prev.x - sub.x + add.x;
+      prev.y = prev.y - sub.y + add.y;
+      prev.z = prev.z - sub.z + add.z;
+      prev.w = prev.w - sub.w + add.w;
+      *reinterpret_cast<float4*>(a.o + orow + dim) = prev;
+      if (keep_terms) *reinterpret_cast<float4*>(a.term_out + trow * D + dim) = add;
+    }
+  if (hw == 0) {
+    a.lse_ref[lrow] = (run_max + log2f(lsum)) * 0.6931471805599453f - logf(msub);
     if (keep_terms) a.mass_out[trow] = msub;
   }
 }
