@@ -481,13 +481,17 @@ def main():
 
 def decode_work(B, T, H, d, c, c_next):
     """Algorithmic bytes of one decode step: the K and V rows of the attended columns, the query, the
-    output (read unless dense, written), the column list, the cached subtract term, and the V rows and
-    outputs of the next loop's subtract term."""
+    output (read unless dense, written), the column list, the cached subtract term, the next loop's
+    columns and subtract term, and the V rows of the selected columns when the next loop keeps fewer than
+    all of them (keeping all, its subtract term is this loop's add term)."""
     n = T if c == 0 else c
     nb = B * H * n * d * 2 * 2 + B * H * d * 2 + B * H * d * 4 * (1 if c == 0 else 3) + B * H * 4 * 2
     if c:
         nb += B * H * c * 4
-    nb += B * H * c_next * (d * 2 + 4) + B * H * d * 4
+    if c_next:
+        nb += B * H * c_next * 4 + B * H * d * 4
+        if c_next < n:
+            nb += B * H * c_next * d * 2
     return nb
 
 
@@ -514,10 +518,17 @@ def decode_bench(w, gs, fl, torch):
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / reps * 1e3, out
 
+    # outputs and workspaces allocated once: the timed calls allocate nothing
+    out_d = (torch.empty(B, H, c, dtype=torch.int32, device="cuda"), torch.empty(B, H, device="cuda"),
+             torch.empty(B, H, d, device="cuda"))
+    out_s = tuple(torch.empty_like(t) for t in out_d)
+    ws_d = fl.decode_ws(gs.k_hat, None, c)
     us_dense, (cols, mass, sub) = timed(lambda: fl.decode_step(q, gs.k_hat, gs.v_hat, None, None, None, o, c,
-                                                               n_sink=w.n_sink, window=w.window))
+                                                               n_sink=w.n_sink, window=w.window, out=out_d,
+                                                               ws=ws_d))
+    ws_s = fl.decode_ws(gs.k_hat, cols, c)
     us_sparse, _ = timed(lambda: fl.decode_step(q, gs.k_hat, gs.v_hat, cols, mass, sub, o, c,
-                                                n_sink=w.n_sink, window=w.window))
+                                                n_sink=w.n_sink, window=w.window, out=out_s, ws=ws_s))
     nb_dense = decode_work(B, T, H, d, 0, c)
     nb_sparse = decode_work(B, T, H, d, c, c)
     log(f"[bench] decode: dense loop {us_dense:.1f} us ({nb_dense / us_dense / 1e3:.0f} GB/s), "
@@ -526,7 +537,7 @@ def decode_bench(w, gs, fl, torch):
             "dense_loop_us": round(us_dense, 2), "sparse_loop_us": round(us_sparse, 2),
             "dense_alg_MB": round(nb_dense / 1e6, 2), "sparse_alg_MB": round(nb_sparse / 1e6, 2),
             "dense_GBps": round(nb_dense / us_dense / 1e3, 1), "sparse_GBps": round(nb_sparse / us_sparse / 1e3, 1),
-            "timing": f"HIP events, mean of {reps} calls (five launches each)"}
+            "timing": f"HIP events, mean of {reps} calls (two launches each, nothing allocated)"}
 
 
 def prune_work(rows, cols, n_sink, H, d):

@@ -308,9 +308,11 @@ int fl_select_columns(const float* col_key, int B, int H, int N, int n_sink, int
  *   c_next            : 0 <= c_next <= |S| (0: no selection; the outputs below may then be NULL).
  *   cols_next         : int32 [B, H, c_next];  mass_next : fp32 [B, H];  sub_next : fp32 [B, H, d].
  *   ws                : at least fl_decode_step_ws(B, T, H, d, c, c_next) bytes (|S| <= 65536).
- * Five launches: chunked logits (with their fp32 ranking keys) and weighted V rows, their merge, the
- * top-k, and the next loop's mass and subtract term in parts and their ordered sum.  Within a row p_j
- * grows with l_j, so S' is ranked by fp32(l_j) (fp64 logits keep the selection exact).
+ * Two launches: chunked logits (with their fp32 ranking keys) and weighted V rows; then one workgroup
+ * per (b, h) merges them into L and the output and forms S', m' and sub' (c_next = |S| keeps every
+ * column: S' = S, m' = m and sub' is the add term just formed; otherwise a top-k and a gather of the
+ * selected V rows).  Within a row p_j grows with l_j, so S' is ranked by fp32(l_j) (fp64 logits keep
+ * the selection exact).
  * ---------------------------------------------------------------------------------------------- */
 size_t fl_decode_step_ws(int B, int T, int H, int d, int c, int c_next);
 

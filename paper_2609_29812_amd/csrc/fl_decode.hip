@@ -8,23 +8,24 @@
 // column) and forms its mass m' = sum_{S'} p_j and subtract term sub' = sum_{S'} p_j V_j.  Within a row
 // p_j grows with l_j, so the ranking key is fp32(l_j), available before L is known.
 //
-// One row per (b, h) is a GEMV: HBM-bound, split over columns.
-//   decode_partial  chunks of 128 positions: fp64 logits (exact bf16 products, fp64 sums) and their fp32
-//                   ranking keys (forced columns +inf), the chunk's max and exp-sum, and the
-//                   exp-weighted sum of its V rows (fp32); K and V rows are each read once, 16 bytes per
-//                   lane, D/8 lanes per row.
-//   decode_combine  one workgroup per (b, h): merges the chunks into L and the output.
-//   topk_select     the radix top-k of fl_select.hip over the keys (positions, ascending).
-//   decode_select  workgroups of 256 selected positions: the selected columns and their parts of the
-//                   mass and subtract term; then one workgroup per (b, h) adds the parts in order.
+// One row per (b, h) is a GEMV: HBM-bound, split over columns.  Two launches:
+//   decode_partial   chunks of 128 positions: fp64 logits (exact bf16 products, fp64 sums) and their fp32
+//                    ranking keys (forced columns +inf), the chunk's max and exp-sum, and the
+//                    exp-weighted sum of its V rows (fp32); K and V rows are each read once, 16 bytes per
+//                    lane, D/8 lanes per row.
+//   decode_finalize  one 1024-thread workgroup per (b, h): merges the chunks into L and the output, and
+//                    forms the next loop's columns, mass and subtract term: directly when every column
+//                    is kept, else by the radix top-k of fl_topk.h over the keys and a gather of the
+//                    selected V rows (read once more).
 #include "fl_common.h"
+#include "fl_topk.h"
 
 #include <mutex>
 
 namespace fl {
 
 constexpr int kDecChunk = 128;           // positions per partial workgroup
-constexpr int kSelChunk = 256;           // selected positions per selection workgroup
+constexpr int kSelWin = 1024;            // selected positions gathered per round of the finalize
 
 // 16-byte load marked non-temporal: the K and V rows of a step are streamed once
 typedef uint32_t u32x4d __attribute__((ext_vector_type(4)));
@@ -46,15 +47,12 @@ struct DecodeArgs {
   double* pmax;              // ws [B*H, nch] chunk max
   double* psum;              // ws [B*H, nch] chunk exp-sum
   float* pacc;               // ws [B*H, nch, D]
-  double* ltot;              // ws [B*H] log-normaliser
   float* key;                // ws [B*H, n]
   const int32_t* sel;        // ws [B*H, c_next] selected positions
-  double* fmass;             // ws [B*H, nfc] parts of the next mass
-  float* fsub;               // ws [B*H, nfc, D] parts of the next subtract term
   int32_t* cols_next;        // [B, H, c_next]
   float* mass_next;          // [B, H]
   float* sub_next;           // [B, H, D]
-  int B, T, H, n, nch, c_next, nfc, n_sink, window;
+  int B, T, H, n, nch, c_next, n_sink, window;
   double scale;
 };
 
@@ -189,102 +187,130 @@ __global__ __launch_bounds__(256) void decode_partial_kernel(DecodeArgs a) {
   }
 }
 
-// ---- combine: the output of one (b, h) from its chunks (nch <= 512) -------------------------------------
-template <int D>
-__global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a) {
-  __shared__ double s_m[4];
+// ---- finalize: one 1024-thread workgroup per (b, h) ----------------------------------------------------
+// (1) merges the chunks into L and the output; (2) with c_next > 0, the next loop's columns, mass m' =
+// sum_{S'} p_j and subtract term sub' = sum_{S'} p_j V_j.  When the next loop keeps every column
+// (c_next = n) these are the columns themselves, m' = m (the probabilities over S sum to m) and sub' = the
+// add term just formed.  Otherwise the radix top-k of fl_topk.h writes the selected positions (ascending)
+// to the workspace, and windows of kSelWin of them are gathered: ids, logits and weights into LDS, then
+// their V rows (every load of a window issued before any use); the waves' sums are added in order
+// (deterministic).
+template <int D, int M>
+__global__ __launch_bounds__(kTopkThreads) void decode_finalize_kernel(DecodeArgs a) {
+  constexpr int NW = kTopkThreads / 64;      // waves
+  constexpr int PARTS = kTopkThreads / D;    // threads per output dimension in the merge
+  constexpr int LPC = D / 8;                 // lanes per V row (16 bytes each)
+  constexpr int CPW = 64 / LPC;              // rows per wave instruction
+  constexpr int IT = kSelWin / (NW * CPW);   // window rows per lane
+  static_assert(IT * NW * CPW == kSelWin && kSelWin == kTopkThreads, "one id per thread, IT rows per lane");
+  constexpr int BUF = NW * D > 2 * kSelWin ? NW * D : 2 * kSelWin;
+  __shared__ double s_m[NW];
   __shared__ double s_l;
-  __shared__ float s_f[512];
+  __shared__ float s_f[512];                 // chunk weights (nch <= 512)
+  __shared__ __attribute__((aligned(16))) float s_buf[BUF];   // partial sums; a window's ids and weights
+  float (*s_acc)[D] = reinterpret_cast<float (*)[D]>(s_buf);
+  int32_t* s_col = reinterpret_cast<int32_t*>(s_buf);
+  float* s_w = s_buf + kSelWin;
   const int bh = blockIdx.x;
+  const int b = bh / a.H, h = bh % a.H;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const bool dense = a.cols == nullptr;
   const double m = dense ? 1.0 : (double)a.mass[bh];
+  // (1) L = M + log S over the chunks' maxima and exp-sums; the add term and the output
   double mx = -INFINITY;
-  for (int c = tid; c < a.nch; c += 256) mx = fmax(mx, a.pmax[(int64_t)bh * a.nch + c]);
+  for (int c = tid; c < a.nch; c += kTopkThreads) mx = fmax(mx, a.pmax[(int64_t)bh * a.nch + c]);
   mx = wave_max_f64(mx);
   if (lane == 0) s_m[wave] = mx;
   __syncthreads();
-  const double M = fmax(fmax(s_m[0], s_m[1]), fmax(s_m[2], s_m[3]));
+  double Mx = s_m[0];
+#pragma unroll
+  for (int w = 1; w < NW; ++w) Mx = fmax(Mx, s_m[w]);
   __syncthreads();
   double es = 0.0;
-  for (int c = tid; c < a.nch; c += 256) {
+  for (int c = tid; c < a.nch; c += kTopkThreads) {
     const int64_t sidx = (int64_t)bh * a.nch + c;
-    es += a.psum[sidx] * exp(a.pmax[sidx] - M);
+    es += a.psum[sidx] * exp(a.pmax[sidx] - Mx);
   }
   es = wave_sum_f64_dec(es);
   if (lane == 0) s_m[wave] = es;
   __syncthreads();
-  if (tid == 0) s_l = s_m[0] + s_m[1] + s_m[2] + s_m[3];
+  if (tid == 0) {
+    double S = 0.0;
+    for (int w = 0; w < NW; ++w) S += s_m[w];
+    s_l = S;
+  }
   __syncthreads();
   const double S = s_l;
-  const double L = M + log(S);
-  for (int c = tid; c < a.nch; c += 256) s_f[c] = (float)(m * exp(a.pmax[(int64_t)bh * a.nch + c] - M) / S);
+  const double L = Mx + log(S);
+  for (int c = tid; c < a.nch; c += kTopkThreads) s_f[c] = (float)(m * exp(a.pmax[(int64_t)bh * a.nch + c] - Mx) / S);
   __syncthreads();
-  if (tid < D) {
+  {
+    // thread (part, dd) adds the chunks part, part + PARTS, ...; the parts are then added in order
+    const int dd = tid % D, part = tid / D;
     float add = 0.0f;
-    for (int c = 0; c < a.nch; ++c) add = fmaf(s_f[c], a.pacc[((int64_t)bh * a.nch + c) * D + tid], add);
+    for (int c = part; c < a.nch; c += PARTS) add = fmaf(s_f[c], a.pacc[((int64_t)bh * a.nch + c) * D + dd], add);
+    s_acc[part][dd] = add;
+  }
+  __syncthreads();
+  float o_add = 0.0f;
+  if (tid < D) {
+#pragma unroll
+    for (int q = 0; q < PARTS; ++q) o_add += s_acc[q][tid];
     const int64_t od = (int64_t)bh * D + tid;
-    a.o[od] = dense ? add : a.o[od] - a.sub[od] + add;
+    a.o[od] = dense ? o_add : a.o[od] - a.sub[od] + o_add;
   }
-  if (tid == 0) {
-    a.ltot[bh] = L;
-    if (a.lse) a.lse[bh] = (float)L;
+  if (tid == 0 && a.lse) a.lse[bh] = (float)L;
+  if (a.c_next == 0) return;               // uniform
+  if (a.c_next == a.n) {                   // every column kept
+    for (int i = tid; i < a.n; i += kTopkThreads) a.cols_next[(int64_t)bh * a.n + i] = dec_col(a, bh, i);
+    if (tid < D) a.sub_next[(int64_t)bh * D + tid] = o_add;
+    if (tid == 0) a.mass_next[bh] = (float)m;
+    return;
   }
-}
-
-// ---- finalize: the next loop's columns, mass and subtract term ---------------------------------------
-// decode_select_partial: a workgroup takes 256 selected positions of one (b, h) (ids, probabilities and
-// weighted V rows, every load of a stage issued before any use); decode_select_reduce adds the
-// workgroups' parts in order (deterministic) into the mass and subtract term.
-template <int D>
-__global__ __launch_bounds__(256) void decode_select_partial_kernel(DecodeArgs a) {
-  constexpr int LPC = D / 8;
-  constexpr int CPW = 64 / LPC;
-  constexpr int IT = (kSelChunk / 4) / CPW;
-  __shared__ double s_red[4];
-  __shared__ float s_acc[4][D];
-  const int chunk = blockIdx.x, bh = blockIdx.y;
-  const int b = bh / a.H, h = bh % a.H;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // (2) the selected positions, ascending, into the workspace; this workgroup's writes are visible to
+  // its own threads after a workgroup-scope release and acquire around the barrier
+  int32_t* sel = const_cast<int32_t*>(a.sel) + (int64_t)bh * a.c_next;
+  topk_block<M>(a.key + (int64_t)bh * a.n, a.n, a.c_next, nullptr, 0, sel, 0, nullptr, 0);
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __syncthreads();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
   const int sl = lane % LPC, grp = lane / LPC;
   const int64_t HD = (int64_t)a.H * D;
-  const double m = a.cols == nullptr ? 1.0 : (double)a.mass[bh];
-  const double L = a.ltot[bh];
-  const int i0 = chunk * kSelChunk + wave * (kSelChunk / 4) + grp;
-  int p[IT], col[IT];
-  double l[IT];
-  uint4 w[IT];
-#pragma unroll
-  for (int it = 0; it < IT; ++it) {
-    const int i = i0 + it * CPW;
-    p[it] = i < a.c_next ? a.sel[(int64_t)bh * a.c_next + i] : 0;
-  }
-#pragma unroll
-  for (int it = 0; it < IT; ++it) {
-    col[it] = dec_col(a, bh, p[it]);
-    l[it] = a.logit[(int64_t)bh * a.n + p[it]];
-  }
-#pragma unroll
-  for (int it = 0; it < IT; ++it)
-    w[it] = *reinterpret_cast<const uint4*>(a.v + ((int64_t)b * a.T + col[it]) * HD + (int64_t)h * D + 8 * sl);
   double ms = 0.0;
   float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-#pragma unroll
-  for (int it = 0; it < IT; ++it) {
-    const int i = i0 + it * CPW;
-    const bool ok = i < a.c_next;
-    const double pr = ok ? m * exp(l[it] - L) : 0.0;
-    if (ok && sl == 0) {
-      a.cols_next[(int64_t)bh * a.c_next + i] = col[it];
+  for (int lo = 0; lo < a.c_next; lo += kSelWin) {
+    // ids, weights p_j = m exp(l_j - L) and the next loop's columns of the window (thread t: entry t)
+    {
+      const int i = lo + tid;
+      const bool ok = i < a.c_next;
+      const int p = ok ? sel[i] : 0;
+      const int col = dec_col(a, bh, p);
+      const double pr = ok ? m * exp(a.logit[(int64_t)bh * a.n + p] - L) : 0.0;
+      if (ok) a.cols_next[(int64_t)bh * a.c_next + i] = col;
       ms += pr;
+      s_col[tid] = col;
+      s_w[tid] = (float)pr;
     }
-    const float wf = (float)pr;
-    const uint32_t ws[4] = {w[it].x, w[it].y, w[it].z, w[it].w};
+    __syncthreads();
+    // their V rows: wave w, row group g takes window entries (w * CPW + g) + it * NW * CPW
+    uint4 vw[IT];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      acc[2 * t] = fmaf(wf, bf16_to_f32(ws[t] & 0xFFFFu), acc[2 * t]);
-      acc[2 * t + 1] = fmaf(wf, bf16_to_f32(ws[t] >> 16), acc[2 * t + 1]);
+    for (int it = 0; it < IT; ++it) {
+      const int e = wave * CPW + grp + it * NW * CPW;
+      vw[it] = *reinterpret_cast<const uint4*>(a.v + ((int64_t)b * a.T + s_col[e]) * HD + (int64_t)h * D + 8 * sl);
     }
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int e = wave * CPW + grp + it * NW * CPW;
+      const float wf = s_w[e];             // 0 past the end of the selection
+      const uint32_t ws[4] = {vw[it].x, vw[it].y, vw[it].z, vw[it].w};
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        acc[2 * t] = fmaf(wf, bf16_to_f32(ws[t] & 0xFFFFu), acc[2 * t]);
+        acc[2 * t + 1] = fmaf(wf, bf16_to_f32(ws[t] >> 16), acc[2 * t + 1]);
+      }
+    }
+    __syncthreads();                       // the window's ids and weights are no longer read
   }
   ms = wave_sum_f64_dec(ms);
 #pragma unroll
@@ -294,34 +320,24 @@ __global__ __launch_bounds__(256) void decode_select_partial_kernel(DecodeArgs a
 #pragma unroll
     for (int t = 0; t < 8; ++t) s_acc[wave][8 * sl + t] = acc[t];
   }
-  if (lane == 0) s_red[wave] = ms;
+  if (lane == 0) s_m[wave] = ms;
   __syncthreads();
-  const int64_t slot = (int64_t)bh * a.nfc + chunk;
-  if (threadIdx.x < D) {
-    const int dd = threadIdx.x;
-    a.fsub[slot * D + dd] = s_acc[0][dd] + s_acc[1][dd] + s_acc[2][dd] + s_acc[3][dd];
-  }
-  if (threadIdx.x == 0) a.fmass[slot] = s_red[0] + s_red[1] + s_red[2] + s_red[3];
-}
-
-template <int D>
-__global__ __launch_bounds__(256) void decode_select_reduce_kernel(DecodeArgs a) {
-  const int bh = blockIdx.x;
-  if (threadIdx.x < D) {
+  if (tid < D) {
     float sacc = 0.0f;
-    for (int c = 0; c < a.nfc; ++c) sacc += a.fsub[((int64_t)bh * a.nfc + c) * D + threadIdx.x];
-    a.sub_next[(int64_t)bh * D + threadIdx.x] = sacc;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) sacc += s_acc[w][tid];
+    a.sub_next[(int64_t)bh * D + tid] = sacc;
   }
-  if (threadIdx.x == 0) {
-    double ms = 0.0;
-    for (int c = 0; c < a.nfc; ++c) ms += a.fmass[(int64_t)bh * a.nfc + c];
-    a.mass_next[bh] = (float)ms;
+  if (tid == 0) {
+    double mt = 0.0;
+    for (int w = 0; w < NW; ++w) mt += s_m[w];
+    a.mass_next[bh] = (float)mt;
   }
 }
 
 // workspace regions, each 256-byte aligned
 struct DecodeWs {
-  size_t logit, pmax, psum, pacc, ltot, key, sel, fmass, fsub, total;
+  size_t logit, pmax, psum, pacc, key, sel, total;
 };
 static DecodeWs decode_ws(int B, int H, int d, int n, int c_next) {
   auto al = [](size_t x) { return (x + 255) / 256 * 256; };
@@ -333,12 +349,8 @@ static DecodeWs decode_ws(int B, int H, int d, int n, int c_next) {
   w.pmax = off; off += al(bh * nch * sizeof(double));
   w.psum = off; off += al(bh * nch * sizeof(double));
   w.pacc = off; off += al(bh * nch * d * sizeof(float));
-  w.ltot = off; off += al(bh * sizeof(double));
   w.key = off; off += al(bh * n * sizeof(float));
   w.sel = off; off += al(bh * (size_t)c_next * sizeof(int32_t));
-  const size_t nfc = ((size_t)c_next + kSelChunk - 1) / kSelChunk;
-  w.fmass = off; off += al(bh * nfc * sizeof(double));
-  w.fsub = off; off += al(bh * nfc * d * sizeof(float));
   w.total = off;
   return w;
 }
@@ -398,14 +410,10 @@ static int decode_step(const char* fn, bool use_scratch, const uint16_t* q, cons
   a.pmax = reinterpret_cast<double*>(base + L.pmax);
   a.psum = reinterpret_cast<double*>(base + L.psum);
   a.pacc = reinterpret_cast<float*>(base + L.pacc);
-  a.ltot = reinterpret_cast<double*>(base + L.ltot);
   a.key = reinterpret_cast<float*>(base + L.key);
   a.sel = reinterpret_cast<const int32_t*>(base + L.sel);
-  a.fmass = reinterpret_cast<double*>(base + L.fmass);
-  a.fsub = reinterpret_cast<float*>(base + L.fsub);
   a.cols_next = cols_next; a.mass_next = mass_next; a.sub_next = sub_next;
   a.B = B; a.T = T; a.H = H; a.n = n; a.nch = (n + kDecChunk - 1) / kDecChunk; a.c_next = c_next;
-  a.nfc = (c_next + kSelChunk - 1) / kSelChunk;
   a.n_sink = n_sink; a.window = window; a.scale = (double)sm_scale;
   const int BH = B * H;
   dim3 gp(a.nch, BH);
@@ -413,20 +421,23 @@ static int decode_step(const char* fn, bool use_scratch, const uint16_t* q, cons
   else decode_partial_kernel<64><<<gp, 256, 0, st>>>(a);
   int rc = check_launch("decode_partial_kernel");
   if (rc != FL_OK) return rc;
-  if (d == 128) decode_combine_kernel<128><<<BH, 256, 0, st>>>(a);
-  else decode_combine_kernel<64><<<BH, 256, 0, st>>>(a);
-  rc = check_launch("decode_combine_kernel");
-  if (rc != FL_OK || c_next == 0) return rc;
-  rc = launch_topk(BH, a.key, n, n, c_next, nullptr, 0, 0, const_cast<int32_t*>(a.sel), c_next, 0, nullptr, 0, st);
-  if (rc != FL_OK) return rc;
-  dim3 gf(a.nfc, BH);
-  if (d == 128) decode_select_partial_kernel<128><<<gf, 256, 0, st>>>(a);
-  else decode_select_partial_kernel<64><<<gf, 256, 0, st>>>(a);
-  rc = check_launch("decode_select_partial_kernel");
-  if (rc != FL_OK) return rc;
-  if (d == 128) decode_select_reduce_kernel<128><<<BH, 256, 0, st>>>(a);
-  else decode_select_reduce_kernel<64><<<BH, 256, 0, st>>>(a);
-  return check_launch("decode_select_reduce_kernel");
+  // finalize: the top-k's register depth follows the number of keys (as in the selection kernels)
+  const int per = (n + kTopkThreads - 1) / kTopkThreads;
+  const dim3 gf(BH);
+#define FL_FIN(MM)                                                                        \
+  do {                                                                                    \
+    if (d == 128) decode_finalize_kernel<128, MM><<<gf, kTopkThreads, 0, st>>>(a);        \
+    else decode_finalize_kernel<64, MM><<<gf, kTopkThreads, 0, st>>>(a);                  \
+  } while (0)
+  if (per <= 1) FL_FIN(1);
+  else if (per <= 2) FL_FIN(2);
+  else if (per <= 4) FL_FIN(4);
+  else if (per <= 8) FL_FIN(8);
+  else if (per <= 16) FL_FIN(16);
+  else if (per <= 32) FL_FIN(32);
+  else FL_FIN(64);
+#undef FL_FIN
+  return check_launch("decode_finalize_kernel");
 }
 
 extern "C" int fl_decode_step(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
