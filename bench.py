@@ -172,8 +172,11 @@ KERNEL_SRC = {"seg_cur_kernel": "fl_seg_attn.hip", "loop_attn_kernel": "fl_attn.
 
 def load_counters(kernel, workload):
     """HBM traffic and MFMA busy fraction per launch from committed rocprofv3 counter runs
-    (profiles/<kernel>_<workload>_counters.json), used only when taken on the kernel's current source."""
-    none = {"traffic": None, "traffic_read": None, "traffic_write": None, "mfma_busy": None}
+    (profiles/<kernel>_<workload>_counters.json), used only when taken on the kernel's current source:
+    traffic = FETCH_SIZE and WRITE_SIZE scaled by a 1 GiB copy's; traffic_dram = the DRAM request counters
+    times their request sizes."""
+    none = {"traffic": None, "traffic_dram": None, "traffic_dram_read": None, "traffic_dram_write": None,
+            "mfma_busy": None}
     path = os.path.join(PROFILE_DIR, f"{kernel}_{workload}_counters.json")
     src = os.path.join(ROOT, "paper_2609_29812_amd", "csrc", KERNEL_SRC.get(kernel, "fl_attn.hip"))
     if not os.path.exists(path):
@@ -183,8 +186,9 @@ def load_counters(kernel, workload):
     if rec.get("source_sha") != source_sha(src):
         return none
     rd, wr = rec.get("dram_read_bytes_per_launch"), rec.get("dram_write_bytes_per_launch")
-    return {"traffic": None if rd is None or wr is None else int(rd + wr), "traffic_read": rd, "traffic_write": wr,
-            "mfma_busy": rec.get("mfma_busy")}
+    return {"traffic": rec.get("fetch_write_bytes_per_launch"),
+            "traffic_dram": None if rd is None or wr is None else int(rd + wr), "traffic_dram_read": rd,
+            "traffic_dram_write": wr, "mfma_busy": rec.get("mfma_busy")}
 
 
 # ---- CPU oracle leg ------------------------------------------------------------------------------------
@@ -267,6 +271,109 @@ def copy_calib():
         torch.mul(src, 1.0, out=dst)      # one elementwise kernel: reads and writes nbytes each
     torch.cuda.synchronize()
     print(json.dumps({"copy_bytes_read": nbytes, "copy_bytes_written": nbytes, "dispatches": 5}), flush=True)
+
+
+# ---- counter summaries -------------------------------------------------------------------------------------
+# Per-dispatch request sizes of the L2 -> memory interface: writes are 64-byte requests (a 1 GiB copy
+# writes exactly 2^24 of them); reads are 128-byte requests (the TCC_EA0_RDREQ_{32B,64B,128B} split of the
+# same runs), and a 1 GiB copy issues 0.83 GiB of them: the rest of its source is served from the
+# last-level cache (MALL) in front of HBM, whose hits are no HBM traffic.
+DRAM_READ_REQ_BYTES = 128
+DRAM_WRITE_REQ_BYTES = 64
+
+
+def _pmc_means(dirs, kernel):
+    import collections
+    import csv
+    import glob
+    per = collections.defaultdict(lambda: collections.defaultdict(float))   # counter -> dispatch -> sum
+    names = set()
+    for d in dirs:
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            with open(f) as fh:
+                for r in csv.DictReader(fh):
+                    if kernel not in r["Kernel_Name"]:
+                        continue
+                    names.add(r["Kernel_Name"])
+                    per[r["Counter_Name"]][(f, r["Dispatch_Id"])] += float(r["Counter_Value"])
+    return {c: sum(v.values()) / len(v) for c, v in per.items()}, {c: len(v) for c, v in per.items()}, names
+
+
+def pmc_summary(kernel, workload, dirs, commands, copy_dirs=()):
+    """Summarize rocprofv3 --pmc runs (counter_collection.csv under each dir) of one kernel into
+    profiles/<kernel>_<workload>_counters.json: per-dispatch means of every counter (summed over its
+    dimensions), the DRAM bytes they imply, and the MFMA busy fraction."""
+    mean, n_disp, names = _pmc_means(dirs, kernel)
+    if not mean:
+        raise SystemExit(f"no dispatches of {kernel} under {dirs}")
+    rec = {"kernel": sorted(names), "workload": workload,
+           "source_sha": source_sha(os.path.join(ROOT, "paper_2609_29812_amd", "csrc", KERNEL_SRC[kernel])),
+           "counters_per_dispatch": {c: round(v, 1) for c, v in sorted(mean.items())},
+           "dispatches": n_disp}
+    rd, wr = mean.get("TCC_EA0_RDREQ_DRAM_sum"), mean.get("TCC_EA0_WRREQ_DRAM_sum")
+    rec["dram_read_bytes_per_launch"] = None if rd is None else int(rd * DRAM_READ_REQ_BYTES)
+    rec["dram_write_bytes_per_launch"] = None if wr is None else int(wr * DRAM_WRITE_REQ_BYTES)
+    tot = mean.get("TCC_EA0_RDREQ_sum")
+    if tot:
+        rec["read_request_mix"] = {sz: round(mean.get(f"TCC_EA0_RDREQ_{sz}_sum", 0.0) / tot, 4)
+                                   for sz in ("32B", "64B", "128B")}
+    busy, active = mean.get("SQ_VALU_MFMA_BUSY_CYCLES"), mean.get("SQ_BUSY_CU_CYCLES")
+    # both sum over the chip: MFMA busy cycles over the SIMDs (four per CU), busy cycles over the CUs
+    rec["mfma_busy"] = None if not busy or not active else round(busy / (4 * active), 4)
+    if copy_dirs:
+        # FETCH_SIZE / WRITE_SIZE (KiB) scaled by what they read for a copy of 1 GiB each way
+        cm, _, _ = _pmc_means(copy_dirs, "elementwise")
+        fs, ws = cm.get("FETCH_SIZE"), cm.get("WRITE_SIZE")
+        rec["copy_calibration"] = {
+            "kernel": "elementwise copy (torch.mul(src, 1.0, out=dst)), 1 GiB read + 1 GiB written",
+            "counters_per_dispatch": {c: round(v, 1) for c, v in sorted(cm.items())}}
+        if fs and ws and "FETCH_SIZE" in mean and "WRITE_SIZE" in mean:
+            f_scale, w_scale = (1 << 20) / fs, (1 << 20) / ws
+            rec["copy_calibration"].update(fetch_scale=round(f_scale, 4), write_scale=round(w_scale, 4))
+            rec["fetch_write_bytes_per_launch"] = int((mean["FETCH_SIZE"] * f_scale + mean["WRITE_SIZE"] * w_scale) * 1024)
+    rec["commands"] = commands
+    rec["note"] = ("R = repository root.  dram bytes = TCC_EA0_RDREQ_DRAM_sum x 128 + TCC_EA0_WRREQ_DRAM_sum x 64 "
+                   "per dispatch; mfma_busy = SQ_VALU_MFMA_BUSY_CYCLES / (4 SIMDs per CU x SQ_BUSY_CU_CYCLES)")
+    out = os.path.join(PROFILE_DIR, f"{kernel}_{workload}_counters.json")
+    with open(out, "w") as fh:
+        json.dump(rec, fh, indent=1)
+    print(json.dumps({k: rec[k] for k in ("dram_read_bytes_per_launch", "dram_write_bytes_per_launch",
+                                          "mfma_busy")}), flush=True)
+
+
+def trace_summary(title, command, trace_dir, out_name):
+    """Markdown table of a rocprofv3 --kernel-trace run (kernel_trace.csv under trace_dir) into
+    profiles/<out_name>.md: per kernel and grid, the calls and their durations."""
+    import collections
+    import csv
+    import glob
+    files = glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no kernel_trace.csv under {trace_dir}")
+    groups = collections.defaultdict(list)
+    meta = {}
+    for f in files:
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                grid = "x".join(r.get(f"Grid_Size_{a}", "1") for a in "XYZ")
+                key = (r["Kernel_Name"], grid)
+                groups[key].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+                meta[key] = (r.get("Workgroup_Size_X", ""), r.get("Arch_VGPR_Count", r.get("VGPR_Count", "")),
+                             r.get("Accum_VGPR_Count", ""), r.get("LDS_Block_Size", r.get("Group_Segment_Size", "")),
+                             r.get("Scratch_Size", r.get("Private_Segment_Size", "")))
+    total = sum(sum(v) for v in groups.values())
+    lines = [f"# {title}", "", "Command (run from the repository root on the MI355X box; R = repository root):", "",
+             "```", command, "```", "",
+             "| kernel | grid (work-items) | wg | vgpr/agpr | LDS B | scratch | calls | avg us | min us | max us | % time |",
+             "|---|---|---|---|---|---|---|---|---|---|---|"]
+    for key, v in sorted(groups.items(), key=lambda kv: -sum(kv[1])):
+        wg, vg, ag, lds, scr = meta[key]
+        name = key[0].replace("void ", "").split("(")[0].replace("|", "\\|")
+        lines.append(f"| {name} | {key[1]} | {wg} | {vg}/{ag} | {lds} | {scr} | {len(v)} | {sum(v) / len(v):.2f} | "
+                     f"{min(v):.2f} | {max(v):.2f} | {100 * sum(v) / total:.1f} |")
+    with open(os.path.join(PROFILE_DIR, f"{out_name}.md"), "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines[8:]), flush=True)
 
 
 def workload_config(w):
@@ -390,7 +497,21 @@ def main():
     ap.add_argument("--no-configs", action="store_true", help="only the 32K workload (no per-workload summaries)")
     ap.add_argument("--decode-only", action="store_true", help="only the decode measurement (for traces)")
     ap.add_argument("--copy-calib", action="store_true")
+    ap.add_argument("--pmc-summary", nargs="+", metavar="ARG",
+                    help="KERNEL WORKLOAD DIR [DIR ...]: summarize rocprofv3 --pmc runs into profiles/ (no GPU)")
+    ap.add_argument("--pmc-command", action="append", default=[], help="a command recorded in the summary")
+    ap.add_argument("--pmc-copy", nargs="*", default=[], help="counter dirs of the copy calibration runs")
+    ap.add_argument("--trace-summary", nargs=4, metavar=("TITLE", "COMMAND", "TRACE_DIR", "OUT_NAME"),
+                    help="summarize a rocprofv3 --kernel-trace run into profiles/OUT_NAME.md (no GPU)")
     args = ap.parse_args()
+    if args.trace_summary:
+        trace_summary(*args.trace_summary)
+        return
+    if args.pmc_summary:
+        if len(args.pmc_summary) < 3:
+            ap.error("--pmc-summary needs KERNEL WORKLOAD DIR [DIR ...]")
+        pmc_summary(args.pmc_summary[0], args.pmc_summary[1], args.pmc_summary[2:], args.pmc_command, args.pmc_copy)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; there is no multi-GPU path (asked for {args.gpus}): "
               "the step would shard by head with one small all-gather of row-score partials.", flush=True)
