@@ -590,6 +590,7 @@ def main():
             result["configs"][name] = rec
             del devc, mc
             torch.cuda.empty_cache()
+    result["kv_footprint"] = kv_footprint(w)
     if not args.no_decode:
         result["decode"] = decode_bench(w, gs, fl, torch)
     if not args.no_prune:
@@ -598,6 +599,31 @@ def main():
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, st, blas_threads())
     print(json.dumps(result), flush=True)
+
+
+def kv_footprint(w):
+    """Bytes of one layer's K and V state after the workload's last loop, stored three ways (Section 4.3, Eq. 4;
+    Appendix E): a bf16 cache per loop (a looped model without the method); the packed streams the paper's
+    engine keeps (int4 base codes and fp16 metadata, then each sparse loop's residual codes and metadata);
+    and the one in-place bf16 cache pair this implementation keeps."""
+    B, N, H, d, G = w.batch, w.seq, w.heads, w.head_dim, w.group
+    el = B * N * H * d
+    per_loop_bf16 = w.loops * 2 * el * 2
+    base = 2 * el * w.base_bits // 8
+    base_meta = B * -(-N // G) * H * d * 4 + B * N * H * (d // G) * 4     # K per-channel, V per-token; z and s
+    res = res_meta = 0
+    for r in range(2, w.loops + 1):
+        k = w.k(r)
+        res += 2 * B * k * H * d * w.bits_at(r) // 8
+        res_meta += B * -(-k // G) * H * d * 4 + B * k * H * (d // G) * 4
+    packed = base + base_meta + res + res_meta
+    working = 2 * el * 2
+    mb = lambda x: round(x / 1e6, 1)
+    return {"workload": w.name, "bf16_cache_per_loop_MB": mb(per_loop_bf16),
+            "packed_MB": mb(packed), "packed_bytes": packed, "packed_parts_MB": {"base_codes": mb(base), "base_metadata": mb(base_meta),
+                                                       "residual_codes": mb(res), "residual_metadata": mb(res_meta)},
+            "working_caches_MB": mb(working), "packed_reduction": round(per_loop_bf16 / packed, 2),
+            "working_reduction": round(per_loop_bf16 / working, 2)}
 
 
 def decode_work(B, T, H, d, c, c_next):

@@ -56,3 +56,29 @@ def test_prune_work_counts_match_brute_force():
     pairs = sum(1 for b in range(B) for h in range(H) for j in cols[b, h, ns:] for i in rows[b] if i >= j)
     assert nf == 2.0 * d * pairs
     assert nb == B * H * 70 * (2 * d + 4) + B * 50 * H * (2 * d + 4) + B * H * 74 * 8
+
+
+def test_kv_footprint_matches_the_oracle_codec_outputs():
+    # the packed footprint of a small workload equals the bytes of the codes and fp16 metadata the oracle's
+    # codec actually produces for the base (all rows) and each sparse loop's active rows
+    from oracle import codec
+    from workloads import get, make_layer
+
+    w = get("C1")
+    st = make_layer(w)
+    B, N, H, d = st.k[0].shape
+    total = 0
+    for axis in (codec.AXIS_TOKEN, codec.AXIS_CHANNEL):
+        enc = codec.quantize(st.k[0], None, np.tile(np.arange(N, dtype=np.int32), (B, 1)), w.base_bits,
+                             w.group, axis)
+        total += enc["codes"].nbytes + enc["scale"].nbytes + enc["zero"].nbytes
+    rng = np.random.default_rng(1)
+    for r in range(2, w.loops + 1):
+        k = w.k(r)
+        idx = np.stack([np.sort(rng.choice(N, k, replace=False)) for _ in range(B)]).astype(np.int32)
+        for axis in (codec.AXIS_TOKEN, codec.AXIS_CHANNEL):
+            enc = codec.quantize(st.k[r - 1], st.k[r - 2], idx, w.bits_at(r), w.group, axis)
+            total += enc["codes"].nbytes + enc["scale"].nbytes + enc["zero"].nbytes
+    fp = bench.kv_footprint(w)
+    assert fp["packed_bytes"] == total
+    assert fp["bf16_cache_per_loop_MB"] == round(w.loops * 2 * B * N * H * d * 2 / 1e6, 1)
