@@ -160,39 +160,68 @@ __device__ __forceinline__ void topk_block(const float* __restrict__ kp, int n, 
     }
   }
 
-  // k-th largest key: (1) histogram of the top kHistBits bits and the bin that holds it.  With k == n
-  // every position is taken and no threshold is needed.
+  // k-th largest key.  (1) The keys' range [lo, hi]: the codes become offsets v = u - lo (order kept), and
+  // the first histogram takes the kHistBits bits of v from the highest bit the range needs (shift0 up),
+  // so the bins cover the keys' actual range and the bin that holds the k-th largest is small.  With
+  // k == n every position is taken and no threshold is needed.
   const bool take_all = k == n;
   uint32_t prefix = 0, mask = 0;
   int krem = take_all ? 0 : k;
   if (k > 0 && !take_all) {                               // uniform
+    uint32_t lo = 0xFFFFFFFFu, hi = 0u;
+#pragma unroll
+    for (int j = 0; j < M; ++j) {
+      const bool valid = t + kTopkThreads * j < n;
+      lo = valid ? min(lo, u[j]) : lo;
+      hi = valid ? max(hi, u[j]) : hi;
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      lo = min(lo, (uint32_t)__shfl_xor((int)lo, off, 64));
+      hi = max(hi, (uint32_t)__shfl_xor((int)hi, off, 64));
+    }
+    if (lane == 0) {
+      red[wave] = (int)lo;
+      red[kTopkWaves + wave] = (int)hi;
+    }
     for (int i = t; i < kBins; i += kTopkThreads) hist[i] = 0;
     __syncthreads();
+#pragma unroll
+    for (int w2 = 0; w2 < kTopkWaves; ++w2) {
+      lo = min(lo, (uint32_t)red[w2]);
+      hi = max(hi, (uint32_t)red[kTopkWaves + w2]);
+    }
+    const uint32_t span = hi - lo;
+    const int shift0 = span >> kHistBits ? 32 - __builtin_clz(span) - kHistBits : 0;   // span >> shift0 < kBins
+#pragma unroll
+    for (int j = 0; j < M; ++j) u[j] = (t + kTopkThreads * j < n) ? u[j] - lo : 0u;
     WaveHist wh;
 #pragma unroll
-    for (int j = 0; j < M; ++j) wh.add(hist, u[j] >> (32 - kHistBits), t + kTopkThreads * j < n);
+    for (int j = 0; j < M; ++j) wh.add(hist, u[j] >> shift0, t + kTopkThreads * j < n);
     wh.flush(hist);
-    __syncthreads();
+    __syncthreads();                                      // (also: every wave has read red)
     find_bin(hist, kBins, k, scan_scratch, meta);
     const uint32_t bin = (uint32_t)meta[0];
     const int cnt = meta[2];
     krem = meta[1];
-    prefix = bin << (32 - kHistBits);
-    mask = ~0u << (32 - kHistBits);
-    if (cnt <= kCap) {
-      // (2) compact that bin's keys into LDS (any order), then resolve the low 20 bits with digit
-      // histograms of 8, 8 and 4 bits over them
+    prefix = bin << shift0;
+    mask = shift0 < 32 ? ~0u << shift0 : 0u;
+    if (shift0 == 0) {
+      // every offset is its own bin: the threshold is known
+    } else if (cnt <= kCap) {
+      // (2) compact that bin's keys into LDS (any order), then resolve the low shift0 bits with digit
+      // histograms of up to 8 bits over them
       int n_in = 0;
 #pragma unroll
-      for (int j = 0; j < M; ++j) n_in += (t + kTopkThreads * j < n && (u[j] >> (32 - kHistBits)) == bin) ? 1 : 0;
+      for (int j = 0; j < M; ++j) n_in += (t + kTopkThreads * j < n && (u[j] & mask) == prefix) ? 1 : 0;
       int tot;
       int off = block_exclusive_scan(n_in, scan_scratch, &tot);
 #pragma unroll
       for (int j = 0; j < M; ++j)
-        if (t + kTopkThreads * j < n && (u[j] >> (32 - kHistBits)) == bin) cbuf[off++] = u[j];
-      int shift = 32 - kHistBits;
-      for (int pass = 0; pass < 3; ++pass) {
-        const int nb = pass < 2 ? 8 : 4;
+        if (t + kTopkThreads * j < n && (u[j] & mask) == prefix) cbuf[off++] = u[j];
+      int shift = shift0;
+      while (shift > 0) {                                 // uniform
+        const int nb = shift < 8 ? shift : 8;
         shift -= nb;
         for (int i = t; i < (1 << nb); i += kTopkThreads) hist[i] = 0;
         __syncthreads();                                  // also orders the compaction writes
@@ -211,7 +240,7 @@ __device__ __forceinline__ void topk_block(const float* __restrict__ kp, int n, 
       }
     } else {
       // (2b) too many keys in one bin for the LDS buffer: resolve the low bits over the registers
-      for (int bit = 31 - kHistBits; bit >= 0; --bit) {
+      for (int bit = shift0 - 1; bit >= 0; --bit) {
         const uint32_t want = prefix | (1u << bit), m2 = mask | (1u << bit);
         int c = 0;
 #pragma unroll
