@@ -62,8 +62,10 @@ int fl_abi_version(void);
 /* Debugging aid: with on != 0 (or the environment variable FL_CHECK_INDICES set to a non-zero value when the
  * library is first used), every call that takes index lists first synchronizes its stream, copies the lists
  * to the host and returns FL_E_RANGE (launching nothing) if one is not strictly ascending or holds an entry
- * outside its range (rows and columns in [0, N), or [0, T) for decode).  Off by default; not usable under
- * stream capture.  Process-wide. */
+ * outside its range (rows and columns in [0, N), or [0, T) for decode).  The same switch has
+ * fl_loop_sparse_attn check that every V value it reads (v_cache, and v_new when given) has magnitude
+ * <= 65504, since its products with V run in fp16 (a small reduction launch, then FL_E_RANGE).  Off by
+ * default; not usable under stream capture.  Process-wide. */
 void fl_set_index_checks(int on);
 
 /* ------------------------------------------------------------------------------------------------

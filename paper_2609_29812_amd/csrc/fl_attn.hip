@@ -1530,6 +1530,12 @@ static int loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev, const
     FL_CHECK_LIST("fl_loop_sparse_attn", "rows", rows, B, k, 0, N, st);
     FL_CHECK_LIST("fl_loop_sparse_attn", "cols", cols, (int64_t)B * H, c_list, 0, N, st);
   }
+  {
+    // the products with V run in fp16 on the dense, two-pass and band add-pass paths
+    int rc = check_f16_range("fl_loop_sparse_attn", "v_cache", v_cache, (int64_t)B * N * H * d, st);
+    if (rc == FL_OK && !dense && v_new) rc = check_f16_range("fl_loop_sparse_attn", "v_new", v_new, (int64_t)B * k * H * d, st);
+    if (rc != FL_OK) return rc;
+  }
   AttnArgs a{};
   a.q_cur = q_cur;
   a.q_prev = (dense || reuse) ? nullptr : q_prev;

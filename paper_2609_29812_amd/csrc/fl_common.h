@@ -36,6 +36,8 @@ inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s);
 bool index_checks_on();
 int check_index_lists(const char* fn, const char* name, const int32_t* list, int64_t n_lists, int len, int lo,
                       int hi, hipStream_t st);
+// With the checks on: FL_E_RANGE unless every bf16 value of x[0..n) has magnitude <= 65504 (fits fp16).
+int check_f16_range(const char* fn, const char* name, const uint16_t* x, int64_t n, hipStream_t st);
 #define FL_CHECK_LIST(fn, name, list, n_lists, len, lo, hi, st)                                   \
   do {                                                                                            \
     const int fl_rc_ = ::fl::check_index_lists((fn), (name), (list), (n_lists), (len), (lo), (hi), (st)); \

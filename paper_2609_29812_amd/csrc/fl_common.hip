@@ -44,6 +44,41 @@ int check_index_lists(const char* fn, const char* name, const int32_t* list, int
   return FL_OK;
 }
 
+// Largest bf16 magnitude pattern (sign cleared) seen by the range check below; patterns order like the
+// magnitudes they encode.
+static __device__ unsigned int g_bf16_max_mag;
+
+__global__ __launch_bounds__(256) void bf16_max_mag_kernel(const uint16_t* __restrict__ x, int64_t n) {
+  unsigned int m = 0;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+    m = max(m, (unsigned int)(x[i] & 0x7FFFu));
+  for (int off = 32; off > 0; off >>= 1) m = max(m, (unsigned int)__shfl_xor((int)m, off, 64));
+  if ((threadIdx.x & 63) == 0) atomicMax(&g_bf16_max_mag, m);
+}
+
+int check_f16_range(const char* fn, const char* name, const uint16_t* x, int64_t n, hipStream_t st) {
+  if (!index_checks_on() || x == nullptr || n <= 0) return FL_OK;
+  // (synchronous like the list checks: the stream is drained, the device word reset, the reduction run
+  // on the stream, and the word read back once the stream has finished)
+  hipError_t e = hipStreamSynchronize(st);
+  const unsigned int zero = 0;
+  if (e == hipSuccess) e = hipMemcpyToSymbol(HIP_SYMBOL(g_bf16_max_mag), &zero, sizeof(zero), 0, hipMemcpyHostToDevice);
+  FL_REQUIRE(e == hipSuccess, FL_E_HIP, "%s: range check: reset failed: %s", fn, hipGetErrorString(e));
+  const int64_t blocks64 = (n + 255) / 256;
+  const unsigned int blocks = (unsigned int)(blocks64 < 4096 ? blocks64 : 4096);
+  bf16_max_mag_kernel<<<blocks, 256, 0, st>>>(x, n);
+  int rc = check_launch("bf16_max_mag_kernel");
+  if (rc != FL_OK) return rc;
+  unsigned int m = 0;
+  e = hipStreamSynchronize(st);
+  if (e == hipSuccess) e = hipMemcpyFromSymbol(&m, HIP_SYMBOL(g_bf16_max_mag), sizeof(m), 0, hipMemcpyDeviceToHost);
+  FL_REQUIRE(e == hipSuccess, FL_E_HIP, "%s: range check: read-back failed: %s", fn, hipGetErrorString(e));
+  // 0x4780 is bf16 65536: every smaller finite bf16 magnitude is at most 65280 and fits fp16 (<= 65504)
+  FL_REQUIRE(m < 0x4780u, FL_E_RANGE, "%s: %s holds a value of magnitude %s (bf16 bits 0x%04x): the fp16 "
+             "product path needs |v| <= 65504", fn, name, m >= 0x7F80u ? "inf/NaN" : "> 65504", m);
+  return FL_OK;
+}
+
 static thread_local char g_last_error[512] = "";
 
 int set_error(int status, const char* fmt, ...) {

@@ -44,3 +44,29 @@ def test_unsorted_and_out_of_range_lists_are_rejected(F):
         F.set_index_checks(False)
     F.select_tokens(x, y, None, None, 2, cand=good)                           # checks off again
     torch.cuda.synchronize()
+
+
+def test_values_beyond_fp16_are_rejected_when_checking(F):
+    # the attention's products with V run in fp16: with the checks on, a V cache holding |v| > 65504 is
+    # rejected before any attention launch, and one within range is accepted
+    rng = np.random.default_rng(6)
+    B, N, H, d = 1, 200, 2, 64
+    q, k = _bf16(rng, (B, N, H, d)), _bf16(rng, (B, N, H, d))
+    v_ok = _bf16(rng, (B, N, H, d))
+    big = rng.standard_normal((B, N, H, d)).astype(np.float32)
+    big[0, 17, 1, 5] = 1.0e5
+    v_big = up_bf16(f32_to_bf16(big))
+    o = torch.zeros(B, N, H, d, dtype=torch.float32, device="cuda")
+    lse = torch.zeros(B, N, H, dtype=torch.float32, device="cuda")
+    F.set_index_checks(True)
+    try:
+        say("range check on: dense loop over a V cache with one value of 1e5, then one within range")
+        with pytest.raises(F.FlashLoopError, match="65504"):
+            F.dense_attn(q, k, v_big, o=o, lse=lse)
+        torch.cuda.synchronize()
+        assert float(o.abs().max()) == 0.0, "a rejected call wrote its output"
+        F.dense_attn(q, k, v_ok, o=o, lse=lse)
+        torch.cuda.synchronize()
+        assert bool(torch.isfinite(o).all())
+    finally:
+        F.set_index_checks(False)
