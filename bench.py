@@ -45,7 +45,7 @@ def log(*a):
 
 
 # ---- algorithmic work of each call (what the method itself must move / compute) ----------------------
-def attn_work(idx, cols, slot, N, H, d, window, B, reuse=False, keep_terms=True, current=False):
+def attn_work(idx, cols, slot, N, H, d, window, B, reuse=False, keep_terms=True, current=False, sub_only=False):
     """Exact algorithmic bytes and flops of one sparse attention launch.
 
     flops = 8 d * sum over (b, h, i in A) |S_i|  (two passes, each q.k and p.v), or 4 d * ... when the
@@ -56,7 +56,11 @@ def attn_work(idx, cols, slot, N, H, d, window, B, reuse=False, keep_terms=True,
             with reuse the previous terms, masses and slot entries of the rows are read, and with
             keep_terms this loop's terms and masses are written.  current: the caches already hold the
             new rows (reuse only), so every touched column is one cache row and no slot entry is read.
+            sub_only: the subtract pass alone over the previous loop's caches (4 d flops per column; q_prev
+            rows, lse in, the touched cache rows and the list read; the terms and masses written).
     """
+    if sub_only:
+        reuse, current = True, True
     flops = 0.0
     nbytes = 0.0
     for b in range(B):
@@ -81,8 +85,11 @@ def attn_work(idx, cols, slot, N, H, d, window, B, reuse=False, keep_terms=True,
             nbytes += (n_used + n_new) * d * 2 * 2          # K and V rows, bf16
             nbytes += (0 if current else n_used * 4) + g.size * 4   # slot lookups and the column list
         nbytes += k * H * d * 2 * (1 if reuse else 2)       # q_cur (and q_prev) rows
-        nbytes += k * H * d * 4 * 2 + k * H * 4 * (1 if reuse else 2)   # o in/out, lse (in/)out
         nbytes += k * 4
+        if sub_only:                                        # lse in, terms and masses out
+            nbytes += k * H * 4 + k * H * d * 4 + k * H * 4
+            continue
+        nbytes += k * H * d * 4 * 2 + k * H * 4 * (1 if reuse else 2)   # o in/out, lse (in/)out
         if reuse:
             nbytes += k * H * d * 4 + k * H * 4 + k * 4     # previous terms, masses, slot entries
         if keep_terms:
@@ -140,7 +147,18 @@ class Step:
             B, N, H, d = kr.shape
             term = torch.empty(B, kk, H, d, dtype=torch.float32, device=kr.device)
             mass = torch.empty(B, kk, H, dtype=torch.float32, device=kr.device)
-            if r == 2:
+            split = r == 2 and fl.subtract_terms_supported(kk, gs.cols.shape[2], gs.window, N, d)
+            if split:
+                # the subtract pass over the loop-1 state, then as loops 3, 4: quantize and commit in one
+                # pass, and the add pass over the caches with the just-computed subtract terms
+                sub, msub = timed(f"sub r{r}", lambda: fl.subtract_terms(qp, gs.k_hat, gs.v_hat, idx, gs.cols,
+                                                                         gs.window, gs.lse))
+                timed(f"quant_kv r{r}", lambda: fl.kv_residual_quant_kv(
+                    kr, gs.k_hat, vr, gs.v_hat, idx, bits, gs.group, mode=fl.DQ_COMMIT))
+                timed(f"attn r{r}", lambda: fl.loop_sparse_attn(
+                    qr, None, gs.k_hat, gs.v_hat, None, None, slot, idx, gs.cols, gs.window, gs.lse, gs.o,
+                    term_prev=sub, mass_prev=msub, slot_prev=slot, term_out=term, mass_out=mass))
+            elif r == 2:
                 # both passes: quantize (compact new rows), attend, then commit into the caches
                 (ck, sk, zk, k_new), (cv, sv, zv, v_new) = timed(f"quant_kv r{r}", lambda: fl.kv_residual_quant_kv(
                     kr, gs.k_hat, vr, gs.v_hat, idx, bits, gs.group))
@@ -167,7 +185,8 @@ def source_sha(path):
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-KERNEL_SRC = {"seg_cur_kernel": "fl_seg_attn.hip", "loop_attn_kernel": "fl_attn.hip", "cur_attn_kernel": "fl_attn.hip"}
+KERNEL_SRC = {"seg_cur_kernel": "fl_seg_attn.hip", "seg_sub_kernel": "fl_seg_attn.hip", "loop_attn_kernel": "fl_attn.hip",
+              "cur_attn_kernel": "fl_attn.hip"}
 
 
 def load_counters(kernel, workload):
@@ -427,14 +446,17 @@ def measure(w, dev, driver, fl, torch, steps, warmup, log_calls=False):
     for r, idx_t, slot_t in trace:
         idx, slot = idx_t.cpu().numpy(), slot_t.cpu().numpy()
         kr, bits = w.k(r), w.bits_at(r)
-        by, fl_ = attn_work(idx, cols, slot, N, H, d, w.window, B, reuse=r > 2, current=r > 2)
+        split = r == 2 and f"sub r{r}" in dur_us
+        by, fl_ = attn_work(idx, cols, slot, N, H, d, w.window, B, reuse=r > 2 or split, current=r > 2 or split)
         work = {
             f"select r{r}": (select_bytes(n_cand, N, H * d, kr, B), 0.0),
             f"quant_kv r{r}": (codec_bytes(kr, H, d, bits, w.group, True, B)
                                + codec_bytes(kr, H, d, bits, w.group, False, B) - B * kr * 4, 0.0),
             f"attn r{r}": (by, fl_),
         }
-        if r == 2:
+        if split:
+            work[f"sub r{r}"] = attn_work(idx, cols, slot, N, H, d, w.window, B, sub_only=True)
+        elif r == 2:
             work[f"commit_kv r{r}"] = (commit_bytes(kr, H, d, bits, w.group, True, B)
                                        + commit_bytes(kr, H, d, bits, w.group, False, B) - B * kr * 4, 0.0)
         for name, (nb, nf) in work.items():
@@ -444,12 +466,18 @@ def measure(w, dev, driver, fl, torch, steps, warmup, log_calls=False):
                              "alg_MB": round(nb / 1e6, 2), "alg_GF": round(nf / 1e9, 3) if nf else None}
             total_bytes += nb
         attn_us += dur_us[f"attn r{r}"]
-        kname = "loop_attn_kernel" if r == 2 else ("seg_cur_kernel" if w.window > 0 else "cur_attn_kernel")
-        acc = per_kernel.setdefault(kname, [0.0, 0.0, 0.0, 0])
-        acc[0] += by
-        acc[1] += fl_
-        acc[2] += dur_us[f"attn r{r}"]
-        acc[3] += 1
+        kname = "loop_attn_kernel" if (r == 2 and not split) else (
+            "seg_cur_kernel" if w.window > 0 else "cur_attn_kernel")
+        launches = [(kname, by, fl_, dur_us[f"attn r{r}"])]
+        if split:
+            attn_us += dur_us[f"sub r{r}"]
+            launches.append(("seg_sub_kernel", *work[f"sub r{r}"], dur_us[f"sub r{r}"]))
+        for kn, nb, nf, us in launches:
+            acc = per_kernel.setdefault(kn, [0.0, 0.0, 0.0, 0])
+            acc[0] += nb
+            acc[1] += nf
+            acc[2] += us
+            acc[3] += 1
         n_cand = kr
     if log_calls:
         for name, kv in kernels.items():

@@ -267,6 +267,30 @@ int fl_loop_sparse_attn_terms(const uint16_t* q_cur, const uint16_t* q_prev,
                               void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------------------------------
+ * (3c) The subtract pass alone -- Appendix D.2, Eq. 7 (the cached loop r-1 probabilities over S_i).
+ *
+ * For every updated row i = rows[b, p] and head h, over S_i as in (3):
+ *   term_out[b, p, h, :] = sum_{j in S_i} exp(sigma q_prev_i . k_cache_j - lse_ref_i) v_cache_j,
+ *   mass_out[b, p, h]    = sum_{j in S_i} exp(sigma q_prev_i . k_cache_j - lse_ref_i)   (m_i)
+ * with the loop r-1 queries, caches and lse_ref (read only).  A loop without stored add terms can then
+ * commit its new rows into the caches (fl_kv_residual_quant_commit) and run the add pass alone with
+ * fl_loop_sparse_attn_terms(term_prev = term_out, mass_prev = mass_out, slot_prev = this loop's slot map,
+ * k_prev = k, k_new = v_new = NULL): the same update as the two-pass fl_loop_sparse_attn, in exact
+ * arithmetic.  Covers shapes with a band (window >= 1), c_list <= 2048 and the segment kernel's tile table
+ * (fl_loop_subtract_terms_supported returns 1); FL_E_UNSUPPORTED otherwise, with nothing launched.
+ * Arrays as in (3): q_prev bf16 [B, N, H, d]; k_cache, v_cache bf16 [B, N, H, d]; rows int32 [B, k]
+ * ascending; cols int32 [B, H, c_list] ascending; lse_ref fp32 [B, N, H]; term_out fp32 [B, k, H, d];
+ * mass_out fp32 [B, k, H] (rows, term_out and mass_out may be NULL when k = 0: nothing to do).  Precision: q.k bf16 MFMA with fp32 accumulation, p.v with fp16 probabilities
+ * and values (the value rows are converted to fp16 as in (3)).
+ * ---------------------------------------------------------------------------------------------- */
+int fl_loop_subtract_terms_supported(int k, int c_list, int window, int N, int d);
+
+int fl_loop_subtract_terms(const uint16_t* q_prev, const uint16_t* k_cache, const uint16_t* v_cache,
+                           const int32_t* rows, int k, const int32_t* cols, int c_list, int window,
+                           int B, int N, int H, int d, float sm_scale, const float* lse_ref,
+                           float* term_out, float* mass_out, void* stream);
+
+/* ------------------------------------------------------------------------------------------------
  * (4) Column statistic of a dense source loop -- Appendix D.2, Eq. 6 with all causal keys and cached
  * mass 1, summed over all rows of a prefill:
  *     col_key[b, h, j] = fp32( sum_{i >= j} exp(l_ij - lse_i) ),  l_ij = sigma * sum_e q_ie k_je,

@@ -84,6 +84,16 @@ def row_columns(cols, i, window):
     return np.unique(lst)
 
 
+def subtract_row(S, q_prev, k_prev, v_prev, lse_ref, sm_scale):
+    """The subtract half of Eq. (7) for one row: the loop r-1 probabilities of the columns in S, recovered
+    from the cached log-normaliser, their value-weighted sum and their mass.  Returns (sub [d], m)."""
+    if S.size == 0:
+        return np.zeros(v_prev.shape[1]), 0.0
+    a = sm_scale * (k_prev[S] @ q_prev)
+    pp = np.exp(a - lse_ref)                     # cached loop r-1 probabilities of the columns in S
+    return pp @ v_prev[S], pp.sum()              # (their global mass m)
+
+
 def correct_row(S, q_cur, q_prev, k_prev, v_prev, k_cur, v_cur, lse_ref, o_prev, sm_scale):
     """One row of Eq. (7).  Returns (o_new [d], lse_ref_new, m).
 
@@ -91,12 +101,9 @@ def correct_row(S, q_cur, q_prev, k_prev, v_prev, k_cur, v_cur, lse_ref, o_prev,
     """
     if S.size == 0:
         return o_prev.copy(), lse_ref, 0.0
-    a = sm_scale * (k_prev[S] @ q_prev)
-    pp = np.exp(a - lse_ref)                     # cached loop r-1 probabilities of the columns in S
-    m = pp.sum()                                  # their global mass
+    sub, m = subtract_row(S, q_prev, k_prev, v_prev, lse_ref, sm_scale)
     if m == 0.0:
         return o_prev.copy(), lse_ref, 0.0
-    sub = pp @ v_prev[S]
     b = sm_scale * (k_cur[S] @ q_cur)
     bmax = b.max()
     L = bmax + np.log(np.exp(b - bmax).sum())

@@ -1642,3 +1642,38 @@ extern "C" int fl_loop_sparse_attn_terms(const uint16_t* q_cur, const uint16_t* 
                           mass_out, ws, ws_bytes, stream);
   FL_API_END
 }
+
+extern "C" int fl_loop_subtract_terms_supported(int k, int c_list, int window, int N, int d) {
+  return seg_supported(k, c_list, window, N, d) ? 1 : 0;
+}
+
+extern "C" int fl_loop_subtract_terms(const uint16_t* q_prev, const uint16_t* k_cache, const uint16_t* v_cache,
+                                      const int32_t* rows, int k, const int32_t* cols, int c_list, int window,
+                                      int B, int N, int H, int d, float sm_scale, const float* lse_ref,
+                                      float* term_out, float* mass_out, void* stream) {
+  FL_API_BEGIN
+  const char* fn = "fl_loop_subtract_terms";
+  FL_REQUIRE(q_prev && k_cache && v_cache && lse_ref, FL_E_NULL, "%s: q_prev, k_cache, v_cache and lse_ref are required",
+             fn);
+  FL_REQUIRE(k == 0 || (rows && term_out && mass_out), FL_E_NULL, "%s: rows, term_out and mass_out are required", fn);
+  FL_REQUIRE(B >= 1 && N >= 1 && H >= 1 && k >= 0 && k <= N, FL_E_SHAPE, "%s: need B, N, H >= 1 and 0 <= k <= N", fn);
+  FL_REQUIRE(d == 64 || d == 128, FL_E_SHAPE, "%s: head dim %d not in {64, 128}", fn, d);
+  FL_REQUIRE((int64_t)N * H * d <= ((int64_t)1 << 30), FL_E_SHAPE,
+             "%s: N * H * d above 2^30 (byte offsets must stay below 2^31)", fn);
+  FL_REQUIRE(c_list >= 0 && c_list <= N && (c_list == 0 || cols), FL_E_SHAPE, "%s: bad column list", fn);
+  FL_REQUIRE(window >= 0, FL_E_SHAPE, "%s: window must be >= 0", fn);
+  FL_REQUIRE(sm_scale > 0.0f && std::isfinite(sm_scale), FL_E_RANGE, "%s: sm_scale must be > 0", fn);
+  if (k == 0) return FL_OK;
+  FL_REQUIRE(seg_supported(k, c_list, window, N, d), FL_E_UNSUPPORTED,
+             "%s: shape outside the segment kernel (needs window >= 1, c_list <= 2048; "
+             "fl_loop_sparse_attn runs both passes for every shape)", fn);
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  FL_CHECK_LIST(fn, "rows", rows, B, k, 0, N, st);
+  FL_CHECK_LIST(fn, "cols", cols, (int64_t)B * H, c_list, 0, N, st);
+  const int rc = check_f16_range(fn, "v_cache", v_cache, (int64_t)B * N * H * d, st);
+  if (rc != FL_OK) return rc;
+  return launch_seg_sub(q_prev, k_cache, v_cache, rows, k, cols, c_list, window, B, N, H, d, sm_scale, lse_ref,
+                        term_out, mass_out, st);
+  FL_API_END
+}
+

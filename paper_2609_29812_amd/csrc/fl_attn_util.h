@@ -98,6 +98,15 @@ __device__ __forceinline__ float row4_add(float x) { return xor32_add(xor16_add(
 // argument, so the median is not folded back into a maximum with its NaN-quieting steps
 __device__ __forceinline__ float fmax_nn(float x, float y, float pinf) { return __builtin_amdgcn_fmed3f(x, y, pinf); }
 
+// Whether the segment kernels (fl_seg_attn.hip) cover a shape.
+bool seg_supported(int k, int c_list, int window, int N, int d);
+
+// Segment kernel of the subtract pass over the previous loop's state; FL_E_UNSUPPORTED without a launch
+// outside seg_supported.
+int launch_seg_sub(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, const int32_t* rows, int k,
+                   const int32_t* cols, int c_list, int window, int B, int N, int H, int d, float sm_scale,
+                   const float* lse_ref, float* term_out, float* mass_out, hipStream_t st);
+
 // Segment kernel of the add pass over current caches (fl_seg_attn.hip); FL_E_UNSUPPORTED without a launch
 // when the shape is outside what it covers.
 int launch_seg_cur(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, const int32_t* rows, int k,

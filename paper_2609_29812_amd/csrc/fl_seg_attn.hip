@@ -59,8 +59,8 @@ struct SegArgs {
   float pinf;                 // +inf (a kernel argument, so the median below is not folded into a max)
 };
 
-template <int D>
-__global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
+template <int D, bool SUB>
+__device__ __forceinline__ void seg_body(const SegArgs& a) {
   constexpr int KS = D / 16;              // k-steps of QK^T (16 dims each)
   constexpr int DB = D / 32;              // 32-dim output blocks
   constexpr int CH = D / 8;               // 16-byte chunks per row
@@ -298,6 +298,9 @@ __global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
   // full skips it
   const float pinf = a.pinf;
   const float sc = a.scale_log2;
+  // subtract pass: the previous loop's log-normaliser (log2 units) is the fixed reference
+  float lse2 = 0.0f;
+  if (SUB && row_ok) lse2 = a.lse_ref[((int64_t)b * a.N + row_i) * a.H + h] * 1.4426950408889634f;
   auto compute = [&](int dx, int dy, const Slot<D>& sl) __attribute__((always_inline)) {
     if (((dy >> grp) & 1) == 0) return;   // no row of the group sees a column of the tile
     const bool full = ((dy >> (8 + grp)) & 1) != 0;
@@ -330,31 +333,45 @@ __global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
         }
       }
     }
-    float t = sv[0];
+    // subtract pass: probabilities against the fixed reference (they are at most 1: the reference is the
+    // log-normaliser over a superset of the columns); add pass: the online softmax below
+    float ref = lse2;
+    if constexpr (!SUB) {
+      // row maximum and (below) row sum as trees: the tile's chain of dependent instructions is its latency
+      float m8[8];
 #pragma unroll
-    for (int v = 1; v < NE; ++v) t = fmax_nn(t, sv[v], pinf);
-    {
-      const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(t), __float_as_uint(t), false, false);
-      t = fmax_nn(__uint_as_float(r[0]), __uint_as_float(r[1]), pinf);
-    }
-    const float tmax = t * sc;            // log2 units (sc > 0 keeps the order; -inf stays -inf)
-    // online softmax with a lazily raised reference (moved only when a score exceeds it by more than 8 in
-    // log2 units: probabilities stay <= 256 and rescaling is rare)
-    const bool raise = tmax > run_max + 8.0f;
-    if (__builtin_amdgcn_ballot_w64(raise) != 0) {
-      const float nm = raise ? tmax : run_max;
-      const float alpha = raise ? __builtin_amdgcn_exp2f(run_max - nm) : 1.0f;   // exp2(-inf) = 0
-      lsum *= alpha;
+      for (int v = 0; v < 8; ++v) m8[v] = fmax_nn(sv[v], sv[v + 8], pinf);
 #pragma unroll
-      for (int db = 0; db < DB; ++db) acc[db] *= alpha;
-      run_max = nm;
+      for (int v = 0; v < 4; ++v) m8[v] = fmax_nn(m8[v], m8[v + 4], pinf);
+      m8[0] = fmax_nn(m8[0], m8[2], pinf);
+      m8[1] = fmax_nn(m8[1], m8[3], pinf);
+      float t = fmax_nn(m8[0], m8[1], pinf);
+      {
+        const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(t), __float_as_uint(t), false, false);
+        t = fmax_nn(__uint_as_float(r[0]), __uint_as_float(r[1]), pinf);
+      }
+      const float tmax = t * sc;            // log2 units (sc > 0 keeps the order; -inf stays -inf)
+      // online softmax with a lazily raised reference (moved only when a score exceeds it by more than 8 in
+      // log2 units: probabilities stay <= 256 and rescaling is rare)
+      const bool raise = tmax > run_max + 8.0f;
+      if (__builtin_amdgcn_ballot_w64(raise) != 0) {
+        const float nm = raise ? tmax : run_max;
+        const float alpha = raise ? __builtin_amdgcn_exp2f(run_max - nm) : 1.0f;   // exp2(-inf) = 0
+        lsum *= alpha;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) acc[db] *= alpha;
+        run_max = nm;
+      }
+      ref = run_max == -INFINITY ? 0.0f : run_max;
     }
-    const float ref = run_max == -INFINITY ? 0.0f : run_max;
     float pr[NE];
 #pragma unroll
-    for (int v = 0; v < NE; ++v) {
-      pr[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[v], sc, -ref));
-      lsum += pr[v];
+    for (int v = 0; v < NE; ++v) pr[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[v], sc, -ref));
+    {
+      float a4[4];
+#pragma unroll
+      for (int v = 0; v < 4; ++v) a4[v] = (pr[v] + pr[v + 4]) + (pr[v + 8] + pr[v + 12]);
+      lsum += (a4[0] + a4[1]) + (a4[2] + a4[3]);
     }
     // O^T += V^T P^T, P rounded to fp16, two 16-column halves of the tile
 #pragma unroll
@@ -374,9 +391,9 @@ __global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
 
   // ---- pipeline: step s waits for its two tiles (issued three steps earlier; steps s+1 and s+2 may still
   // be in flight, 2 NI operations per wave), converts this wave's value rows, passes the barrier (every
-  // wave is done with step s-1 and every value row of step s is fp16), has each team DMA its tile of step
-  // s+3 into the slot step s-1 used, and computes its tile of step s.  Every step issues exactly NI VMEM
-  // operations per wave.
+  // wave is done with step s-1 and every value row of step s is fp16), computes its tile of step s, and
+  // has each team DMA its tile of step s+3 into the slot step s-1 used (after the math, which the barrier
+  // releases first).  Every step issues exactly NI VMEM operations per wave.
   __syncthreads();                        // the descriptors
   FL_WAIT_VM(0);                          // query fragments have arrived
   const int n_steps = (n_tiles + 1) / 2;
@@ -396,8 +413,8 @@ __global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
     FL_WAIT_VM(2 * NI);
     convert(cur);
     lds_barrier();
-    issue(nxt, of);
     if (have) compute(dx, dy, cur);
+    issue(nxt, of);                       // (after the math: the step's critical path starts at the barrier)
     u += 2;
   };
   for (int s = 0; s < n_loop; s += kSegSteps) {
@@ -433,9 +450,10 @@ __global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
     const float m_o = xs[lane * 2], l_o = xs[lane * 2 + 1];
     // combine (run_max, lsum, acc) with (m_o, l_o, team 1's acc); an empty state has sum 0 and reference
     // -inf, and contributes nothing (its factor is exp2(-inf) = 0)
+    // (the subtract pass has one fixed reference: plain sums)
     const float mm = fmaxf(run_max, m_o);
-    const float fs = mm == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(run_max - mm);
-    const float fo = mm == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m_o - mm);
+    const float fs = SUB ? 1.0f : mm == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(run_max - mm);
+    const float fo = SUB ? 1.0f : mm == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m_o - mm);
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -449,6 +467,17 @@ __global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
   }
   // ---- epilogue: lane (r32, hw) holds dims 32 db + 8 j + 4 hw .. +3 of row r32 of the group -------------
   if (!row_ok) return;
+  if constexpr (SUB) {                    // the subtract term and the mass, at the row's position in rows
+    const int64_t srow = ((int64_t)b * a.k + pos) * a.H + h;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        *reinterpret_cast<float4*>(a.term_out + srow * D + db * 32 + 8 * j + 4 * hw) =
+            make_float4(acc[db][4 * j], acc[db][4 * j + 1], acc[db][4 * j + 2], acc[db][4 * j + 3]);
+    if (hw == 0) a.mass_out[srow] = lsum;
+    return;
+  }
   const int p = pos;
   const int ri = row_i;
   const int64_t orow = ((int64_t)b * a.N + ri) * HD + (int64_t)h * D;
@@ -493,6 +522,58 @@ __global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
   }
 }
 
+template <int D>
+__global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
+  seg_body<D, false>(a);
+}
+template <int D>
+__global__ __launch_bounds__(512, 2) void seg_sub_kernel(SegArgs a) {
+  seg_body<D, true>(a);
+}
+
+// Whether the segment kernels cover a shape (a band, a list that fits in LDS, the descriptor table).
+bool seg_supported(int k, int c_list, int window, int N, int d) {
+  if (window < 1 || c_list > kSegListCap || (d != 64 && d != 128) || k < 1) return false;
+  // the descriptor table holds every position: at most ceil(c_list / 32) list tiles and ceil(N / 32) + 1 band
+  // tiles, plus one empty position per kind when the counts are odd
+  return (c_list + kBN - 1) / kBN + (N + kBN - 1) / kBN + 3 <= kSegTileCap;
+}
+
+// Segments per (batch, head): at least one per 128 rows; more (down to 64 rows) while the grid is below one
+// workgroup per CU.  Sets a.n_seg and a.seg_rows.
+static void seg_grid(SegArgs& a, int k, int bh) {
+  constexpr int kCUs = 256;
+  int n_seg = (k + kSegRows - 1) / kSegRows;
+  const int fill = (kCUs + bh - 1) / bh;
+  const int n_max = (k + 63) / 64;
+  if (n_seg < fill) n_seg = std::min(fill, n_max);
+  if (n_seg < 1) n_seg = 1;
+  const int seg_rows = (k + n_seg - 1) / n_seg;
+  a.n_seg = (k + seg_rows - 1) / seg_rows;
+  a.seg_rows = seg_rows;
+}
+
+// Subtract pass over the previous loop's state (queries q of loop r-1, caches X_hat^(r-1), lse_ref of loop
+// r-1): per updated row the term sum_j exp(sigma q . k_j - lse_ref) v_j and its mass, written at the row's
+// position in rows.  FL_E_UNSUPPORTED (nothing launched) outside seg_supported.
+int launch_seg_sub(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, const int32_t* rows, int k,
+                   const int32_t* cols, int c_list, int window, int B, int N, int H, int d, float sm_scale,
+                   const float* lse_ref, float* term_out, float* mass_out, hipStream_t st) {
+  if (!seg_supported(k, c_list, window, N, d)) return FL_E_UNSUPPORTED;
+  SegArgs a{};
+  a.q = q; a.k_cache = k_cache; a.v_cache = v_cache; a.rows = rows; a.cols = cols;
+  a.lse_ref = const_cast<float*>(lse_ref);   // (read only in this pass)
+  a.term_out = term_out; a.mass_out = mass_out;
+  a.k = k; a.c_list = c_list; a.window = window; a.B = B; a.N = N; a.H = H;
+  seg_grid(a, k, B * H);
+  a.scale_log2 = sm_scale * 1.4426950408889634f;
+  a.pinf = INFINITY;
+  dim3 grid((unsigned)(a.n_seg * B * H));
+  if (d == 128) seg_sub_kernel<128><<<grid, 512, 0, st>>>(a);
+  else seg_sub_kernel<64><<<grid, 512, 0, st>>>(a);
+  return check_launch("seg_sub_kernel");
+}
+
 // Launch of the segment kernel for a reuse loop over current caches; returns FL_E_UNSUPPORTED (nothing
 // launched) when the shape is outside what it covers, so the caller can take another kernel.
 int launch_seg_cur(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, const int32_t* rows, int k,
@@ -501,29 +582,16 @@ int launch_seg_cur(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v
                    const int32_t* slot_prev, int k_prev, float* term_out, float* mass_out, hipStream_t st) {
   // (without a band, the 64-row kernel over the list alone measured faster: the segment layout pays off
   // when the band's HBM stream is there to overlap)
-  if (window < 1 || c_list > kSegListCap || (d != 64 && d != 128) || k < 1) return FL_E_UNSUPPORTED;
-  // the descriptor table holds every position: at most ceil(c_list / 32) list tiles and ceil(N / 32) + 1 band
-  // tiles, plus one empty position per kind when the counts are odd
-  if ((c_list + kBN - 1) / kBN + (N + kBN - 1) / kBN + 3 > kSegTileCap) return FL_E_UNSUPPORTED;
-  constexpr int kCUs = 256;
-  const int bh = B * H;
-  // at least one segment per 128 rows; more (down to 64 rows) while the grid is below one workgroup per CU
-  int n_seg = (k + kSegRows - 1) / kSegRows;
-  const int fill = (kCUs + bh - 1) / bh;
-  const int n_max = (k + 63) / 64;
-  if (n_seg < fill) n_seg = std::min(fill, n_max);
-  if (n_seg < 1) n_seg = 1;
-  const int seg_rows = (k + n_seg - 1) / n_seg;
-  n_seg = (k + seg_rows - 1) / seg_rows;
+  if (!seg_supported(k, c_list, window, N, d)) return FL_E_UNSUPPORTED;
   SegArgs a{};
   a.q = q; a.k_cache = k_cache; a.v_cache = v_cache; a.rows = rows; a.cols = cols;
   a.lse_ref = lse_ref; a.o = o; a.term_prev = term_prev; a.mass_prev = mass_prev; a.slot_prev = slot_prev;
   a.term_out = term_out; a.mass_out = mass_out;
   a.k = k; a.k_prev = k_prev; a.c_list = c_list; a.window = window; a.B = B; a.N = N; a.H = H;
-  a.n_seg = n_seg; a.seg_rows = seg_rows;
+  seg_grid(a, k, B * H);
   a.scale_log2 = sm_scale * 1.4426950408889634f;
   a.pinf = INFINITY;
-  dim3 grid((unsigned)(n_seg * bh));
+  dim3 grid((unsigned)(a.n_seg * B * H));
   if (d == 128) seg_cur_kernel<128><<<grid, 512, 0, st>>>(a);
   else seg_cur_kernel<64><<<grid, 512, 0, st>>>(a);
   return check_launch("seg_cur_kernel");

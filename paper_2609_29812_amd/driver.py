@@ -10,7 +10,10 @@ sparse_step() one sparse loop r >= 2: select the active rows among the previous 
               Each loop keeps its add terms; from the second sparse loop on they serve as the subtract
               terms (equal in exact arithmetic: the column sets are fixed and the active rows nested).
               Such a loop needs only the new state, so the quantizers commit the new rows straight into
-              the caches and the attention reads every column from them.
+              the caches and the attention reads every column from them.  A loop without stored terms
+              computes its subtract terms first, over the loop r-1 state, where the segment kernel covers
+              the shape, and then runs as such a loop; otherwise it runs both passes in one kernel and
+              commits after it.
 prune_list()  a smaller column budget for the next loop (Section 4.2): keep the sinks and the entries the
               last loop's updated rows gave the most probability mass.  The next loop then runs both passes
               (its subtract pass recomputes the kept columns' share with the same lse_ref).
@@ -70,7 +73,15 @@ def sparse_step(st: LayerState, qr, qp, kr, kp, vr, vp, k_r, bits, keep=False):
         term = torch.empty(B, k, H, d, dtype=torch.float32, device=kr.device)
         mass = torch.empty(B, k, H, dtype=torch.float32, device=kr.device)
     k_new = v_new = None
-    if st.reuse and st.term is not None:
+    reuse = st.reuse and st.term is not None
+    split = not reuse and fl.subtract_terms_supported(k, st.cols.shape[2], st.window, N, d)
+    if reuse or split:
+        term_prev, mass_prev, slot_prev = st.term, st.mass, st.slot_prev
+        if split:
+            # no stored terms: the subtract pass over the loop r-1 state first (its terms index this loop's
+            # rows), so that the new rows can be committed before the add pass
+            term_prev, mass_prev = fl.subtract_terms(qp, st.k_hat, st.v_hat, idx, st.cols, st.window, st.lse)
+            slot_prev = slot
         # the add pass alone: commit the new rows first, then attend over the caches
         (ck, sk, zk, _), (cv, sv, zv, _) = fl.kv_residual_quant_kv(kr, st.k_hat, vr, st.v_hat, idx, bits,
                                                                    st.group, mode=fl.DQ_COMMIT)
@@ -78,7 +89,7 @@ def sparse_step(st: LayerState, qr, qp, kr, kp, vr, vp, k_r, bits, keep=False):
             fl.kv_keep_recent(kr, idx, st.tail, cache=st.k_hat)
             fl.kv_keep_recent(vr, idx, st.tail, cache=st.v_hat)
         fl.loop_sparse_attn(qr, None, st.k_hat, st.v_hat, None, None, slot, idx, st.cols, st.window, st.lse,
-                            st.o, term_prev=st.term, mass_prev=st.mass, slot_prev=st.slot_prev, term_out=term,
+                            st.o, term_prev=term_prev, mass_prev=mass_prev, slot_prev=slot_prev, term_out=term,
                             mass_out=mass)
     else:
         # both passes: the subtract pass needs the loop r-1 caches, so commit after the attention

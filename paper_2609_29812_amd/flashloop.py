@@ -51,6 +51,9 @@ _SIGNATURES = {
     "fl_loop_sparse_attn_terms": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_i, _c_p, _c_i, _c_i,
                                          _c_i, _c_i, _c_i, _c_i, _c_f, _c_p, _c_p, _c_p, _c_p, _c_p, _c_i, _c_p,
                                          _c_p, _c_p, _c_sz, _c_p]),
+    "fl_loop_subtract_terms_supported": (_c_i, [_c_i, _c_i, _c_i, _c_i, _c_i]),
+    "fl_loop_subtract_terms": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_i, _c_p, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_f,
+                                      _c_p, _c_p, _c_p, _c_p]),
     "fl_column_scores_ws": (_c_sz, [_c_i, _c_i, _c_i]),
     "fl_column_scores": (_c_i, [_c_p, _c_p, _c_i, _c_i, _c_i, _c_i, _c_p, _c_p, _c_sz, _c_p]),
     "fl_select_columns": (_c_i, [_c_p, _c_i, _c_i, _c_i, _c_i, _c_i, _c_p, _c_p]),
@@ -326,6 +329,34 @@ def loop_sparse_attn(q_cur, q_prev, k_cache, v_cache, k_new, v_new, slot, rows, 
                                      _p(lse_ref), _p(o), _p(ws) if need else None, need, _stream())
         _check(rc, "fl_loop_sparse_attn")
     return o, lse_ref
+
+
+def subtract_terms_supported(k, c_list, window, N, d):
+    """Whether fl_loop_subtract_terms covers the shape (the segment kernel)."""
+    return bool(load().fl_loop_subtract_terms_supported(k, c_list, window, N, d))
+
+
+def subtract_terms(q_prev, k_cache, v_cache, rows, cols, window, lse_ref, term_out=None, mass_out=None,
+                   sm_scale=None):
+    """Subtract term and mass of Eq. 7 over the previous loop's state: (term fp32 [B, k, H, d], m fp32 [B, k, H])
+    in the row order of `rows` (fl_loop_subtract_terms)."""
+    B, N, H, d = q_prev.shape
+    k = rows.shape[1]
+    for name, t in (("q_prev", q_prev), ("k_cache", k_cache), ("v_cache", v_cache)):
+        _dev(t, torch.bfloat16, name, q_prev.shape)
+    _dev(rows, torch.int32, "rows", (B, k))
+    c_list = 0 if cols is None else cols.shape[2]
+    _dev(cols, torch.int32, "cols", None if cols is None else (B, H, c_list))
+    _dev(lse_ref, torch.float32, "lse_ref", (B, N, H))
+    term_out = torch.empty(B, k, H, d, dtype=torch.float32, device=q_prev.device) if term_out is None else term_out
+    mass_out = torch.empty(B, k, H, dtype=torch.float32, device=q_prev.device) if mass_out is None else mass_out
+    _dev(term_out, torch.float32, "term_out", (B, k, H, d))
+    _dev(mass_out, torch.float32, "mass_out", (B, k, H))
+    sm_scale = 1.0 / math.sqrt(d) if sm_scale is None else sm_scale
+    rc = load().fl_loop_subtract_terms(_p(q_prev), _p(k_cache), _p(v_cache), _p(rows), k, _p(cols), c_list, window,
+                                       B, N, H, d, sm_scale, _p(lse_ref), _p(term_out), _p(mass_out), _stream())
+    _check(rc, "fl_loop_subtract_terms")
+    return term_out, mass_out
 
 
 def dense_attn(q, k_cache, v_cache, o=None, lse=None, sm_scale=None):

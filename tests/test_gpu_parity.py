@@ -359,6 +359,90 @@ def test_sparse_attn_stepwise_from_oracle_state(F, name, over):
         v_hat = codec.reconstruct(v_hat, st.v[r - 1], lr.idx, lr.enc_v, w.bits_at(r), w.group, codec.AXIS_CHANNEL)[0]
 
 
+@pytest.mark.parametrize("name,over", [("C4", dict(seq=1100, heads=2, window=100, col_budget=4 + 100 + 150)),
+                                       # two batch elements; the band alone (an empty list); d = 64; fewer rows
+                                       # than one segment
+                                       ("C4", dict(seq=1500, heads=2, batch=2, window=128, col_budget=4 + 128 + 200)),
+                                       ("C4", dict(seq=1500, heads=2, window=128, n_sink=0, col_budget=128)),
+                                       ("C4", dict(seq=1300, heads=2, head_dim=64, window=96, col_budget=4 + 96 + 120)),
+                                       ("C4", dict(seq=600, heads=2, window=64, col_budget=4 + 64 + 50))])
+def test_subtract_pass_then_add_pass_from_oracle_state(F, name, over):
+    """fl_loop_subtract_terms on the oracle's loop r-1 state: every row's subtract term and mass against the
+    oracle's subtract half of Eq. 7; then the new rows committed and the add pass run with those terms
+    (fl_loop_sparse_attn_terms), against the oracle's loop r outputs."""
+    w = get(name).replace(**over)
+    st = make_layer(w)
+    rec = chain.run_layer(st)
+    B, H, d, N = w.batch, w.heads, w.head_dim, w.seq
+    sc = 1.0 / np.sqrt(d)
+    say(f"subtract pass {w.name} B={B} N={N} H={H} d={d} window={w.window}")
+    o_prev, l_prev = _dict_to_array(rec.o1, B, H), _dict_to_array(rec.lse1, B, H)
+    k_hat, v_hat = rec.k_hat1, rec.v_hat1
+    cols_np = np.stack([np.stack([rec.cols[b, h] for h in range(H)]) for b in range(B)])
+    cols = up(cols_np)
+    assert F.subtract_terms_supported(rec.loops[0].idx.shape[1], cols_np.shape[2], w.window, N, d)
+    for lr in rec.loops:
+        r = lr.r
+        k = lr.idx.shape[1]
+        l32 = l_prev.astype(np.float32)
+        qp = up_bf16(st.q[r - 2])
+        kc, vc = up_bf16(k_hat), up_bf16(v_hat)
+        term, mass = F.subtract_terms(qp, kc, vc, up(lr.idx), cols, w.window, up(l32))
+        torch.cuda.synchronize()
+        want_t = np.zeros((B, k, H, d))
+        want_m = np.zeros((B, k, H))
+        for b in range(B):
+            for h in range(H):
+                kp, vp = bf16_to_f64(k_hat[b, :, h]), bf16_to_f64(v_hat[b, :, h])
+                for p, i in enumerate(lr.idx[b]):
+                    S = att.row_columns(cols_np[b, h], int(i), w.window)
+                    want_t[b, p, h], want_m[b, p, h] = att.subtract_row(
+                        S, bf16_to_f64(st.q[r - 2][b, i, h]), kp, vp, float(l32[b, i, h]), sc)
+        assert_close(down(term), want_t, f"loop {r} subtract terms")
+        assert_close(down(mass), want_m, f"loop {r} masses")
+        # commit the new rows, then the add pass alone with these terms (slot_prev: this loop's slot map)
+        o = up(o_prev.astype(np.float32))
+        lse = up(l32)
+        F.kv_residual_quant_kv(up_bf16(st.k[r - 1]), kc, up_bf16(st.v[r - 1]), vc, up(lr.idx), w.bits_at(r),
+                               w.group, mode=F.DQ_COMMIT)
+        F.loop_sparse_attn(up_bf16(st.q[r - 1]), None, kc, vc, None, None, up(lr.slot), up(lr.idx), cols,
+                           w.window, lse, o, term_prev=term, mass_prev=mass, slot_prev=up(lr.slot))
+        torch.cuda.synchronize()
+        k_hat = codec.reconstruct(k_hat, st.k[r - 1], lr.idx, lr.enc_k, w.bits_at(r), w.group, codec.AXIS_TOKEN)[0]
+        v_hat = codec.reconstruct(v_hat, st.v[r - 1], lr.idx, lr.enc_v, w.bits_at(r), w.group, codec.AXIS_CHANNEL)[0]
+        assert np.array_equal(down_bits16(kc), k_hat) and np.array_equal(down_bits16(vc), v_hat), \
+            f"loop {r} committed caches"
+        want_o, want_l = _dict_to_array(lr.o, B, H), _dict_to_array(lr.lse, B, H)
+        for b in range(B):
+            rows = lr.idx[b]
+            assert_close(down(o)[b][rows], want_o[b][rows], f"loop {r} o (subtract pass, then add pass), b={b}")
+            assert_close(down(lse)[b][rows], want_l[b][rows], f"loop {r} lse (subtract pass, then add pass), b={b}")
+            others = np.setdiff1d(np.arange(N), rows)
+            assert np.array_equal(down(o)[b][others], o_prev.astype(np.float32)[b][others])
+        o_prev, l_prev = want_o, want_l
+
+
+def test_subtract_pass_coverage_and_arguments(F):
+    """The query follows the segment kernel's domain (a band, a list of at most 2048 entries); outside it the
+    call returns FL_E_UNSUPPORTED without a launch; k = 0 is a no-op."""
+    from paper_2609_29812_amd.flashloop import FlashLoopError
+    assert F.subtract_terms_supported(100, 512, 64, 4096, 128)
+    assert F.subtract_terms_supported(100, 2048, 1, 4096, 64)
+    assert not F.subtract_terms_supported(100, 512, 0, 4096, 128)       # no band
+    assert not F.subtract_terms_supported(100, 2049, 64, 4096, 128)     # list beyond the LDS copy
+    assert not F.subtract_terms_supported(100, 512, 64, 4096, 96)       # head dim
+    B, N, H, d = 1, 256, 2, 64
+    q = torch.zeros(B, N, H, d, dtype=torch.bfloat16, device="cuda")
+    rows = torch.arange(0, N, 4, dtype=torch.int32, device="cuda").view(1, -1)
+    cols = torch.arange(0, 32, dtype=torch.int32, device="cuda").view(1, 1, -1).repeat(1, H, 1).contiguous()
+    lse = torch.zeros(B, N, H, dtype=torch.float32, device="cuda")
+    with pytest.raises(FlashLoopError, match="outside the segment kernel"):
+        F.subtract_terms(q, q, q, rows, cols, 0, lse)
+    empty = torch.zeros(1, 0, dtype=torch.int32, device="cuda")
+    t, m = F.subtract_terms(q, q, q, empty, cols, 16, lse)
+    assert t.shape == (1, 0, H, d) and m.shape == (1, 0, H)
+
+
 @pytest.mark.parametrize("name,over", [("C4", dict(seq=2000, heads=2, window=128, col_budget=4 + 128 + 300)),
                                        ("C5", dict(seq=1200, heads=2, batch=2, col_budget=200)),
                                        ("C2", dict(seq=900, heads=2, head_dim=64, col_budget=100)),

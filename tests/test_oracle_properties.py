@@ -6,9 +6,10 @@ definitions fix independently of the code under test (brute force, closed forms,
 * codec (Section 4.3, Eq. 4; Appendix D.3, Eq. 8): codes stay in range, the dequantized residual is within
   half a step (plus fp32 rounding slack) of the residual, the packed bytes unpack to the codes, and rows
   outside the active set keep their previous reconstruction;
-* attention (Appendix D.2, Eqs. 6 and 7): after a dense loop, a sparse loop over every causal column equals
-  exact attention over the new state (the mass is 1), and over any column set the mass is the sum of the
-  previous loop's probabilities of those columns;
+* attention (Appendix D.2, Eqs. 6 and 7): after a dense loop, the subtract half over every causal column is
+  the dense output with mass 1, a sparse loop over every causal column equals exact attention over the new
+  state (the mass is 1), and over any column set the mass is the sum of the previous loop's probabilities of
+  those columns;
 * column lists: the sinks are kept, the list is ascending and of the budgeted size, and equals a brute-force
   ranking of the column keys.
 """
@@ -97,6 +98,10 @@ def test_sparse_loop_after_a_dense_loop(seed, N, d, window, n_list):
     want_o, want_lse = att.dense_rows(q1, k1, v1, np.arange(N), sc)
     for i in range(N):
         S = att.row_columns(full, i, 0)
+        # the subtract half over every causal column is the dense loop's own output, with mass 1
+        sub, m0 = att.subtract_row(S, q0[i], k0, v0, lse0[i], sc)
+        np.testing.assert_allclose(sub, o0[i], rtol=0, atol=1e-12)
+        assert abs(m0 - 1.0) < 1e-12
         o, lse, m = att.correct_row(S, q1[i], q0[i], k0, v0, k1, v1, lse0[i], o0[i], sc)
         assert abs(m - 1.0) < 1e-12
         np.testing.assert_allclose(o, want_o[i], rtol=0, atol=1e-11)
