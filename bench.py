@@ -180,6 +180,22 @@ class Step:
         return trace
 
 
+def capture_step(step, torch):
+    """One step captured in a HIP graph (torch.cuda.CUDAGraph on ROCm): every launch of loops 2..R on the
+    capture stream, its buffers from the graph's pool.  Replays redo the step on the layer state as it
+    stands, as the eager loop does.  None if capture fails (the eager number stands then)."""
+    try:
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step.run()
+        torch.cuda.synchronize()
+        return g
+    except Exception as e:   # (reported; the bench keeps the eager timing)
+        log(f"[bench] graph capture failed: {e}")
+        return None
+
+
 def source_sha(path):
     with open(path, "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
@@ -423,9 +439,26 @@ def measure(w, dev, driver, fl, torch, steps, warmup, log_calls=False):
     e1.record()
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
-    ms_step = e0.elapsed_time(e1) / steps
+    ms_eager = e0.elapsed_time(e1) / steps
     rows_per_step = sum(w.batch * w.k(r) for r in range(2, w.loops + 1))
-    log(f"[bench] {w.name}: {steps} steps: {ms_step:.4f} ms/step (wall {t_wall / steps * 1e3:.4f} ms)")
+    log(f"[bench] {w.name}: {steps} steps: {ms_eager:.4f} ms/step (wall {t_wall / steps * 1e3:.4f} ms)")
+
+    # the same step captured once in a graph and replayed (reported beside the eager step, which is the
+    # headline: on this stack the replay measured slower, and the eager launches keep ahead of the GPU)
+    ms_step = ms_eager
+    ms_graph = None
+    graph = capture_step(step, torch)
+    if graph is not None:
+        for _ in range(warmup):
+            graph.replay()
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(steps):
+            graph.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        ms_graph = e0.elapsed_time(e1) / steps
+        log(f"[bench] {w.name}: {steps} graph replays: {ms_graph:.4f} ms/step")
 
     # per-call durations with events on the launch stream (a separate pass, same work)
     events = {}
@@ -504,7 +537,8 @@ def measure(w, dev, driver, fl, torch, steps, warmup, log_calls=False):
 
     # the dominant kernel is the one with the most time per step
     order = sorted(per_kernel, key=lambda kn: -per_kernel[kn][2])
-    return {"state": gs, "ms_per_step": ms_step, "rows_per_step": rows_per_step,
+    return {"state": gs, "ms_per_step": ms_step, "ms_per_step_graph": ms_graph,
+            "rows_per_step": rows_per_step,
             "step_hbm_GBps": round(total_bytes / (ms_step * 1e-3) / 1e9, 1),
             "attn_rows_per_s": round(rows_per_step / (attn_us * 1e-6), 1),
             "roofline": roofline_of(order[0]),
@@ -582,6 +616,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4),
+        "ms_per_step_graph_replay": None if m["ms_per_step_graph"] is None else round(m["ms_per_step_graph"], 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -605,6 +640,8 @@ def main():
             mc = measure(wc, devc, driver, fl, torch, max(5, args.steps // 2), max(2, args.warmup // 2))
             rec = {"workload": wc.name, "config": workload_config(wc), "rows_per_step": mc["rows_per_step"],
                    "ms_per_step": round(mc["ms_per_step"], 4),
+                   "ms_per_step_graph_replay": (None if mc["ms_per_step_graph"] is None
+                                                else round(mc["ms_per_step_graph"], 4)),
                    "rows_per_s": round(mc["rows_per_step"] / (mc["ms_per_step"] * 1e-3), 1),
                    "attn_rows_per_s": mc["attn_rows_per_s"], "step_hbm_GBps": mc["step_hbm_GBps"],
                    "roofline": mc["roofline"], "roofline_other_kernels": mc["roofline_other_kernels"],
