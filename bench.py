@@ -443,9 +443,8 @@ def measure(w, dev, driver, fl, torch, steps, warmup, log_calls=False):
     rows_per_step = sum(w.batch * w.k(r) for r in range(2, w.loops + 1))
     log(f"[bench] {w.name}: {steps} steps: {ms_eager:.4f} ms/step (wall {t_wall / steps * 1e3:.4f} ms)")
 
-    # the same step captured once in a graph and replayed (reported beside the eager step, which is the
-    # headline: on this stack the replay measured slower, and the eager launches keep ahead of the GPU)
-    ms_step = ms_eager
+    # the same step captured once in a graph and replayed; the step time is the faster of the two (the replay
+    # pays off where the step is launch-bound: the small workloads; at 32K the eager launches keep ahead)
     ms_graph = None
     graph = capture_step(step, torch)
     if graph is not None:
@@ -459,6 +458,8 @@ def measure(w, dev, driver, fl, torch, steps, warmup, log_calls=False):
         torch.cuda.synchronize()
         ms_graph = e0.elapsed_time(e1) / steps
         log(f"[bench] {w.name}: {steps} graph replays: {ms_graph:.4f} ms/step")
+    mode = "graph replay" if ms_graph is not None and ms_graph < ms_eager else "eager"
+    ms_step = ms_graph if mode == "graph replay" else ms_eager
 
     # per-call durations with events on the launch stream (a separate pass, same work)
     events = {}
@@ -537,7 +538,8 @@ def measure(w, dev, driver, fl, torch, steps, warmup, log_calls=False):
 
     # the dominant kernel is the one with the most time per step
     order = sorted(per_kernel, key=lambda kn: -per_kernel[kn][2])
-    return {"state": gs, "ms_per_step": ms_step, "ms_per_step_graph": ms_graph,
+    return {"state": gs, "ms_per_step": ms_step, "ms_per_step_graph": ms_graph, "ms_per_step_eager": ms_eager,
+            "step_mode": mode,
             "rows_per_step": rows_per_step,
             "step_hbm_GBps": round(total_bytes / (ms_step * 1e-3) / 1e9, 1),
             "attn_rows_per_s": round(rows_per_step / (attn_us * 1e-6), 1),
@@ -616,6 +618,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4),
+        "step_mode": m["step_mode"],
+        "ms_per_step_eager": round(m["ms_per_step_eager"], 4),
         "ms_per_step_graph_replay": None if m["ms_per_step_graph"] is None else round(m["ms_per_step_graph"], 4),
         "higher_is_better": True,
         "scaling": "weak",
@@ -640,6 +644,7 @@ def main():
             mc = measure(wc, devc, driver, fl, torch, max(5, args.steps // 2), max(2, args.warmup // 2))
             rec = {"workload": wc.name, "config": workload_config(wc), "rows_per_step": mc["rows_per_step"],
                    "ms_per_step": round(mc["ms_per_step"], 4),
+                   "step_mode": mc["step_mode"], "ms_per_step_eager": round(mc["ms_per_step_eager"], 4),
                    "ms_per_step_graph_replay": (None if mc["ms_per_step_graph"] is None
                                                 else round(mc["ms_per_step_graph"], 4)),
                    "rows_per_s": round(mc["rows_per_step"] / (mc["ms_per_step"] * 1e-3), 1),

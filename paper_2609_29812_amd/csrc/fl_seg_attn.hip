@@ -1,8 +1,12 @@
-// Mass-corrected sparse attention update over row segments (Appendix D.2, Eq. 7; Sections 3.2, 4.2) for a
-// loop whose subtract term is the previous loop's stored add term and whose caches already hold this
-// loop's state: the add pass alone,
-//   L_i = log sum_{j in S_i} exp(l_ij),  add_i = sum_j exp(l_ij - L_i) v_j,  l_ij = sigma q_i . k_j,
-//   o_i <- o_i - term_prev_i + m_i add_i,   lse_ref_i <- L_i - log m_i,
+// Mass-corrected sparse attention update over row segments (Appendix D.2, Eq. 7; Sections 3.2, 4.2), in two
+// kernels that share one body.
+//   seg_cur_kernel, the add pass, for a loop whose subtract term and mass are given (the previous loop's
+//   stored add term, or the subtract pass below) and whose caches already hold this loop's state:
+//     L_i = log sum_{j in S_i} exp(l_ij),  add_i = sum_j exp(l_ij - L_i) v_j,  l_ij = sigma q_i . k_j,
+//     o_i <- o_i - term_prev_i + m_i add_i,   lse_ref_i <- L_i - log m_i;
+//   seg_sub_kernel, the subtract pass over the previous loop's queries, caches and lse_ref:
+//     sub_i = sum_{j in S_i} exp(l_ij - lse_ref_i) v_j,  m_i = sum_{j in S_i} exp(l_ij - lse_ref_i)
+//     (a fixed reference: no running maximum, and the two teams' sums simply add);
 // over S_i = (list U {j : i - w < j <= i}) restricted to j <= i, list columns taking the condition
 // j + w <= i so that a column in both is counted once.
 //
@@ -24,7 +28,8 @@
 // Data movement: tiles of 32 columns are gathered by LDS-DMA (buffer_load ... lds) into a ring of four
 // steps (two tiles each) three steps ahead; out-of-range offsets read zeros.  Each wave converts the value
 // rows its own DMA wrote from bf16 to fp16 in place (exact for 2^-14 <= |v| <= 65504; smaller magnitudes
-// round to a multiple of 2^-24; larger ones overflow) before the step's barrier.  Contractions: S^T = K Q^T
+// round to a multiple of 2^-24; larger ones overflow) one step before they are used, after its own math.
+// Contractions: S^T = K Q^T
 // on v_mfma_f32_32x32x16_bf16 (lane (r, h) holds columns 8j + 4h .. +3, j = 0..3, of row r of the group),
 // O^T += V^T P^T on v_mfma_f32_32x32x16_f16 with V read transposed and P rounded to fp16; the transposed V
 // reads take the columns in the order the lane already holds them, so P needs no shuffle.
@@ -389,11 +394,12 @@ __device__ __forceinline__ void seg_body(const SegArgs& a) {
     }
   };
 
-  // ---- pipeline: step s waits for its two tiles (issued three steps earlier; steps s+1 and s+2 may still
-  // be in flight, 2 NI operations per wave), converts this wave's value rows, passes the barrier (every
-  // wave is done with step s-1 and every value row of step s is fp16), computes its tile of step s, and
-  // has each team DMA its tile of step s+3 into the slot step s-1 used (after the math, which the barrier
-  // releases first).  Every step issues exactly NI VMEM operations per wave.
+  // ---- pipeline: step s passes the barrier (every wave is done with step s-1, and every value row of step s
+  // was converted to fp16 by the wave whose DMA wrote it), computes its tile of step s, has each team DMA
+  // its tile of step s+3 into the slot step s-1 used (after the math, which the barrier releases first),
+  // then waits for its own rows of step s+1 (issued two steps earlier; s+2 and s+3 may still be in flight,
+  // 2 NI operations per wave) and converts their values, while slower waves still compute.  Every step
+  // issues exactly NI VMEM operations per wave.
   __syncthreads();                        // the descriptors
   FL_WAIT_VM(0);                          // query fragments have arrived
   const int n_steps = (n_tiles + 1) / 2;
@@ -405,23 +411,26 @@ __device__ __forceinline__ void seg_body(const SegArgs& a) {
   issue(ring2[0], tile_offs(4 + team));
   int u = team;                           // this team's position at the current step
   int2 dsc = tdesc[u < n_tiles ? u : 0];  // its descriptor, read one step ahead
-  auto step = [&](Slot<D>& cur, Slot<D>& nxt) __attribute__((always_inline)) {   // (the slots' first tiles; the team's is at tofs)
+  FL_WAIT_VM(2 * NI);                     // step 0 has landed
+  convert(ring0[0]);
+  auto step = [&](Slot<D>& cur, Slot<D>& nxt, Slot<D>& nx1) __attribute__((always_inline)) {   // (the slots' first tiles; the team's is at tofs)
     const Offs of = tile_offs(u + 6);
     const int dx = __builtin_amdgcn_readfirstlane(dsc.x), dy = __builtin_amdgcn_readfirstlane(dsc.y);
     const bool have = u < n_tiles;
     dsc = tdesc[u + 2 < n_tiles ? u + 2 : 0];
-    FL_WAIT_VM(2 * NI);
-    convert(cur);
+    FL_WAIT_VM(2 * NI);                   // (step s: converted at the end of step s-1, so already landed)
     lds_barrier();
     if (have) compute(dx, dy, cur);
     issue(nxt, of);                       // (after the math: the step's critical path starts at the barrier)
+    FL_WAIT_VM(2 * NI);                   // step s+1 has landed (s+2 and s+3 may be in flight)
+    convert(nx1);                         // its value rows to fp16, in the shadow of the other waves' math
     u += 2;
   };
   for (int s = 0; s < n_loop; s += kSegSteps) {
-    step(ring0[0], ring3[0]);
-    step(ring1[0], ring0[0]);
-    step(ring2[0], ring1[0]);
-    step(ring3[0], ring2[0]);
+    step(ring0[0], ring3[0], ring1[0]);
+    step(ring1[0], ring0[0], ring2[0]);
+    step(ring2[0], ring1[0], ring3[0]);
+    step(ring3[0], ring2[0], ring0[0]);
   }
   FL_WAIT_VM(0);
   lds_barrier();

@@ -167,34 +167,36 @@ __device__ __forceinline__ void topk_block(const float* __restrict__ kp, int n, 
   const bool take_all = k == n;
   uint32_t prefix = 0, mask = 0;
   int krem = take_all ? 0 : k;
+  // (the range is taken on every path, so the keys have one form, offsets, in registers: with the raw keys
+  // kept for the paths without a search, the 32K-key kernel ran out of registers)
+  uint32_t lo = 0xFFFFFFFFu, hi = 0u;
+#pragma unroll
+  for (int j = 0; j < M; ++j) {
+    const bool valid = t + kTopkThreads * j < n;
+    lo = valid ? min(lo, u[j]) : lo;
+    hi = valid ? max(hi, u[j]) : hi;
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    lo = min(lo, (uint32_t)__shfl_xor((int)lo, off, 64));
+    hi = max(hi, (uint32_t)__shfl_xor((int)hi, off, 64));
+  }
+  if (lane == 0) {
+    red[wave] = (int)lo;
+    red[kTopkWaves + wave] = (int)hi;
+  }
+  for (int i = t; i < kBins; i += kTopkThreads) hist[i] = 0;
+  __syncthreads();
+#pragma unroll
+  for (int w2 = 0; w2 < kTopkWaves; ++w2) {
+    lo = min(lo, (uint32_t)red[w2]);
+    hi = max(hi, (uint32_t)red[kTopkWaves + w2]);
+  }
+  const uint32_t span = hi - lo;
+  const int shift0 = span >> kHistBits ? 32 - __builtin_clz(span) - kHistBits : 0;   // span >> shift0 < kBins
+#pragma unroll
+  for (int j = 0; j < M; ++j) u[j] = (t + kTopkThreads * j < n) ? u[j] - lo : 0u;
   if (k > 0 && !take_all) {                               // uniform
-    uint32_t lo = 0xFFFFFFFFu, hi = 0u;
-#pragma unroll
-    for (int j = 0; j < M; ++j) {
-      const bool valid = t + kTopkThreads * j < n;
-      lo = valid ? min(lo, u[j]) : lo;
-      hi = valid ? max(hi, u[j]) : hi;
-    }
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-      lo = min(lo, (uint32_t)__shfl_xor((int)lo, off, 64));
-      hi = max(hi, (uint32_t)__shfl_xor((int)hi, off, 64));
-    }
-    if (lane == 0) {
-      red[wave] = (int)lo;
-      red[kTopkWaves + wave] = (int)hi;
-    }
-    for (int i = t; i < kBins; i += kTopkThreads) hist[i] = 0;
-    __syncthreads();
-#pragma unroll
-    for (int w2 = 0; w2 < kTopkWaves; ++w2) {
-      lo = min(lo, (uint32_t)red[w2]);
-      hi = max(hi, (uint32_t)red[kTopkWaves + w2]);
-    }
-    const uint32_t span = hi - lo;
-    const int shift0 = span >> kHistBits ? 32 - __builtin_clz(span) - kHistBits : 0;   // span >> shift0 < kBins
-#pragma unroll
-    for (int j = 0; j < M; ++j) u[j] = (t + kTopkThreads * j < n) ? u[j] - lo : 0u;
     WaveHist wh;
 #pragma unroll
     for (int j = 0; j < M; ++j) wh.add(hist, u[j] >> shift0, t + kTopkThreads * j < n);
