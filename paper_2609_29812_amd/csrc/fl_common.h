@@ -90,15 +90,14 @@ __device__ __forceinline__ double f16_down_value(double x) {
   if (x >= 65504.0) return 65504.0;
   if (x <= -65504.0) return -65504.0;
   double a = fabs(x);
-  double quantum;
+  int sh = 24;                          // x * 2^sh counts fp16 spacings (2^-24 below the normal range)
   if (a >= 0x1p-14) {
     int e;
-    frexp(a, &e);                       // a in [2^(e-1), 2^e)
-    quantum = ldexp(1.0, e - 1 - 10);   // fp16 spacing in that binade
-  } else {
-    quantum = 0x1p-24;
+    frexp(a, &e);                       // a in [2^(e-1), 2^e): spacing 2^(e - 11) in that binade
+    sh = 11 - e;
   }
-  double v = floor(x / quantum) * quantum;   // exact: power-of-two scaling and an integer
+  // floor(x / spacing) * spacing with both scalings as exponent shifts (exact: no division)
+  const double v = ldexp(floor(ldexp(x, sh)), -sh);
   return v + 0.0;                            // -0 -> +0
 }
 
