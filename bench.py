@@ -119,11 +119,12 @@ def select_bytes(n_cand, N, D, k, B):
 # ---- the timed step ------------------------------------------------------------------------------------
 class Step:
     def __init__(self, w, dev, gs, fl, torch):
-        self.w, self.dev, self.gs, self.fl, self.torch = w, dev, gs, fl, torch
+        from paper_2609_29812_amd import driver
+        self.w, self.dev, self.gs, self.fl, self.torch, self.driver = w, dev, gs, fl, torch, driver
 
     def run(self, events=None):
         """One step (loops 2..R).  events: optional dict name -> list of (start, end) event pairs."""
-        w, dev, gs, fl = self.w, self.dev, self.gs, self.fl
+        w, dev, gs, fl, driver = self.w, self.dev, self.gs, self.fl, self.driver
         torch = self.torch
         gs.cand = None
         trace = []
@@ -147,7 +148,7 @@ class Step:
             B, N, H, d = kr.shape
             term = torch.empty(B, kk, H, d, dtype=torch.float32, device=kr.device)
             mass = torch.empty(B, kk, H, dtype=torch.float32, device=kr.device)
-            split = r == 2 and fl.subtract_terms_supported(kk, gs.cols.shape[2], gs.window, N, d)
+            split = r == 2 and driver.subtract_pass_first(kk, gs.cols.shape[2], gs.window, B, N, H, d)
             if split:
                 # the subtract pass over the loop-1 state, then as loops 3, 4: quantize and commit in one
                 # pass, and the add pass over the caches with the just-computed subtract terms
@@ -201,8 +202,9 @@ def source_sha(path):
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-KERNEL_SRC = {"seg_cur_kernel": "fl_seg_attn.hip", "seg_sub_kernel": "fl_seg_attn.hip", "loop_attn_kernel": "fl_attn.hip",
-              "cur_attn_kernel": "fl_attn.hip"}
+KERNEL_SRC = {"seg_cur_kernel": "fl_seg_attn.hip", "seg_sub_kernel": "fl_seg_attn.hip", "seg1_cur_kernel": "fl_seg_attn.hip",
+              "seg1_sub_kernel": "fl_seg_attn.hip", "loop_attn_kernel": "fl_attn.hip", "cur_attn_kernel": "fl_attn.hip",
+              "cur_sub_kernel": "fl_attn.hip", "reuse_attn_kernel": "fl_attn.hip"}
 
 
 def load_counters(kernel, workload):
@@ -399,13 +401,17 @@ def trace_summary(title, command, trace_dir, out_name):
     total = sum(sum(v) for v in groups.values())
     lines = [f"# {title}", "", "Command (run from the repository root on the MI355X box; R = repository root):", "",
              "```", command, "```", "",
-             "| kernel | grid (work-items) | wg | vgpr/agpr | LDS B | scratch | calls | avg us | min us | max us | % time |",
-             "|---|---|---|---|---|---|---|---|---|---|---|"]
+             "Durations of one kernel drift upward over a sustained run of back-to-back steps (the graph replays "
+             "come last) and recover after a pause, which is the chip's clock management; the minimum and the "
+             "median bracket what the benchmark's shorter per-kernel HIP-event pass measures.", "",
+             "| kernel | grid (work-items) | wg | vgpr/agpr | LDS B | scratch | calls | avg us | median us | min us | "
+             "max us | % time |",
+             "|---|---|---|---|---|---|---|---|---|---|---|---|"]
     for key, v in sorted(groups.items(), key=lambda kv: -sum(kv[1])):
         wg, vg, ag, lds, scr = meta[key]
         name = key[0].replace("void ", "").split("(")[0].replace("|", "\\|")
         lines.append(f"| {name} | {key[1]} | {wg} | {vg}/{ag} | {lds} | {scr} | {len(v)} | {sum(v) / len(v):.2f} | "
-                     f"{min(v):.2f} | {max(v):.2f} | {100 * sum(v) / total:.1f} |")
+                     f"{float(np.median(v)):.2f} | {min(v):.2f} | {max(v):.2f} | {100 * sum(v) / total:.1f} |")
     with open(os.path.join(PROFILE_DIR, f"{out_name}.md"), "w") as fh:
         fh.write("\n".join(lines) + "\n")
     print("\n".join(lines[8:]), flush=True)
@@ -500,12 +506,14 @@ def measure(w, dev, driver, fl, torch, steps, warmup, log_calls=False):
                              "alg_MB": round(nb / 1e6, 2), "alg_GF": round(nf / 1e9, 3) if nf else None}
             total_bytes += nb
         attn_us += dur_us[f"attn r{r}"]
-        kname = "loop_attn_kernel" if (r == 2 and not split) else (
-            "seg_cur_kernel" if w.window > 0 else "cur_attn_kernel")
+        c_list = cols.shape[2]
+        kname = fl.attn_kernel_name(fl.PASS_BOTH if (r == 2 and not split) else fl.PASS_ADD, kr, c_list, w.window,
+                                    B, N, H, d)
         launches = [(kname, by, fl_, dur_us[f"attn r{r}"])]
         if split:
             attn_us += dur_us[f"sub r{r}"]
-            launches.append(("seg_sub_kernel", *work[f"sub r{r}"], dur_us[f"sub r{r}"]))
+            launches.append((fl.attn_kernel_name(fl.PASS_SUBTRACT, kr, c_list, w.window, B, N, H, d),
+                             *work[f"sub r{r}"], dur_us[f"sub r{r}"]))
         for kn, nb, nf, us in launches:
             acc = per_kernel.setdefault(kn, [0.0, 0.0, 0.0, 0])
             acc[0] += nb

@@ -276,12 +276,15 @@ int fl_loop_sparse_attn_terms(const uint16_t* q_cur, const uint16_t* q_prev,
  * commit its new rows into the caches (fl_kv_residual_quant_commit) and run the add pass alone with
  * fl_loop_sparse_attn_terms(term_prev = term_out, mass_prev = mass_out, slot_prev = this loop's slot map,
  * k_prev = k, k_new = v_new = NULL): the same update as the two-pass fl_loop_sparse_attn, in exact
- * arithmetic.  Covers shapes with a band (window >= 1), c_list <= 2048 and the segment kernel's tile table
- * (fl_loop_subtract_terms_supported returns 1); FL_E_UNSUPPORTED otherwise, with nothing launched.
+ * arithmetic.  Covers c_list <= 3072, with or without a band (fl_loop_subtract_terms_supported returns 1):
+ * c_list <= 2048 (and, with a band, the segment kernel's tile table) runs the segment kernels, the others the
+ * 64-row kernel with the list in LDS.  FL_E_UNSUPPORTED otherwise, with nothing launched.
  * Arrays as in (3): q_prev bf16 [B, N, H, d]; k_cache, v_cache bf16 [B, N, H, d]; rows int32 [B, k]
  * ascending; cols int32 [B, H, c_list] ascending; lse_ref fp32 [B, N, H]; term_out fp32 [B, k, H, d];
- * mass_out fp32 [B, k, H] (rows, term_out and mass_out may be NULL when k = 0: nothing to do).  Precision: q.k bf16 MFMA with fp32 accumulation, p.v with fp16 probabilities
- * and values (the value rows are converted to fp16 as in (3)).
+ * mass_out fp32 [B, k, H] (rows, term_out and mass_out may be NULL when k = 0: nothing to do).
+ * Precision: q.k bf16 MFMA with fp32 accumulation; p.v with fp16 probabilities and values in the segment
+ * kernel (the value rows are converted to fp16 as in (3), and v_cache must fit fp16), with bf16 values and
+ * each probability split into two bf16 parts in the 64-row kernel.
  * ---------------------------------------------------------------------------------------------- */
 int fl_loop_subtract_terms_supported(int k, int c_list, int window, int N, int d);
 
@@ -289,6 +292,19 @@ int fl_loop_subtract_terms(const uint16_t* q_prev, const uint16_t* k_cache, cons
                            const int32_t* rows, int k, const int32_t* cols, int c_list, int window,
                            int B, int N, int H, int d, float sm_scale, const float* lse_ref,
                            float* term_out, float* mass_out, void* stream);
+
+/* ------------------------------------------------------------------------------------------------
+ * (3d) Which kernel an attention call launches -- for profilers that look the launch up in a trace.
+ * Host-only: no device call, no argument is dereferenced.  pass: FL_PASS_ADD, the add pass over caches
+ * that hold the loop's state (fl_loop_sparse_attn_terms with k_new = v_new = NULL); FL_PASS_SUBTRACT,
+ * fl_loop_subtract_terms; FL_PASS_BOTH, both passes (fl_loop_sparse_attn, and loop 2 without terms).
+ * Returns a static string naming the __global__ function (e.g. "seg_cur_kernel"), or NULL for a shape the
+ * pass does not cover or arguments outside 1 <= k <= N, 0 <= c_list <= N, window >= 0, d in {64, 128},
+ * B, H >= 1.
+ * ---------------------------------------------------------------------------------------------- */
+enum fl_attn_pass { FL_PASS_ADD = 0, FL_PASS_SUBTRACT = 1, FL_PASS_BOTH = 2 };
+
+const char* fl_attn_kernel_name(int pass, int k, int c_list, int window, int B, int N, int H, int d);
 
 /* ------------------------------------------------------------------------------------------------
  * (4) Column statistic of a dense source loop -- Appendix D.2, Eq. 6 with all causal keys and cached

@@ -1060,18 +1060,23 @@ __global__ __launch_bounds__(256, 2) void reuse_attn_kernel(AttnArgs a) {
   }
 }
 
-// ---- add pass over current caches with the column list in LDS ------------------------------------------
-// With the caches already holding this loop's rows, a tile is either 32 consecutive entries of the
-// (b, h) column list or 32 consecutive band columns.  A workgroup copies the list entries into LDS once
-// (up to kListCap of them), so every wave forms its own DMA offsets, column ids and tile bounds from that
-// copy or from the band range: the pipeline has no record loads and no per-step table writes, and each
-// step is one wait, one barrier, the DMA of tile s+3 and the math of tile s.  Rows, tiles, masks, the
-// online softmax and the epilogue are those of reuse_attn_kernel.
+// ---- one pass over caches that hold a single loop's state, the column list in LDS -----------------------
+// A tile is either 32 consecutive entries of the (b, h) column list or 32 consecutive band columns.  A
+// workgroup copies the list entries into LDS once (up to kListCap of them), so every wave forms its own DMA
+// offsets, column ids and tile bounds from that copy or from the band range: the pipeline has no record
+// loads and no per-step table writes, and each step is one wait, one barrier, the DMA of tile s+3 and the
+// math of tile s.  Rows, tiles and masks are those of reuse_attn_kernel.  Two kernels share the body:
+//   cur_attn_kernel (SUB false): the add pass of loop r over the caches after the commit, with the online
+//     softmax and the epilogue of reuse_attn_kernel (o_i <- o_i - term_prev_i + m_i add_i);
+//   cur_sub_kernel (SUB true): the subtract pass over loop r-1's queries, caches and lse_ref (Section 4.2,
+//     the removed part of the correction): probabilities against the fixed reference lse_ref (at most 1,
+//     it normalizes a superset of S_i), so no running maximum; the epilogue writes the term
+//     sum_{j in S_i} p_ij v_j and the mass sum_{j in S_i} p_ij at the row's position in rows.
 constexpr int kListCap = 3072;
 
 
-template <int D>
-__global__ __launch_bounds__(256, 2) void cur_attn_kernel(AttnArgs a) {
+template <int D, bool SUB>
+__device__ __forceinline__ void cur_body(const AttnArgs& a) {
   constexpr int BM = 64;                  // rows per workgroup (4 waves x 16)
   constexpr int KS = D / 32;              // k-steps of QK^T (32 dims each)
   constexpr int DB = D / 16;              // 16-dim output blocks
@@ -1122,7 +1127,8 @@ __global__ __launch_bounds__(256, 2) void cur_attn_kernel(AttnArgs a) {
     const int64_t qoff = ((int64_t)b * a.N + (row_ok ? row_i : 0)) * HD + (int64_t)h * D + g4 * 8;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      const uint4 w = row_ok ? *reinterpret_cast<const uint4*>(a.q_cur + qoff + ks * 32) : make_uint4(0, 0, 0, 0);
+      const uint4 w = row_ok ? *reinterpret_cast<const uint4*>((SUB ? a.q_prev : a.q_cur) + qoff + ks * 32)
+                             : make_uint4(0, 0, 0, 0);
       qa[ks] = __builtin_bit_cast(bf16x8, w);
     }
   }
@@ -1208,10 +1214,13 @@ __global__ __launch_bounds__(256, 2) void cur_attn_kernel(AttnArgs a) {
     for (int db = 0; db < DB; ++db) voff[db] = colv * D + ((2 * db + (q >> 1)) ^ swz16_f<D>(colv)) * 8 + 4 * (q & 1);
   }
 
-  f32x4 acc[DB];                          // add term, O^T blocks
+  f32x4 acc[DB];                          // add (or subtract) term, O^T blocks
 #pragma unroll
   for (int db = 0; db < DB; ++db) acc[db] = f32x4{};
   float run_max = -INFINITY, lsum = 0.0f;   // running reference (log2 units) and row sum
+  // subtract pass: the row's loop r-1 log-normaliser in log2 units, the fixed reference
+  float lse2 = 0.0f;
+  if (SUB && row_ok) lse2 = a.lse_ref[((int64_t)b * a.N + row_i) * a.H + h] * 1.4426950408889634f;
 
   // the lane's 8 column ids (16c + 4 g4 + v) come from the list copy or the band range
   auto compute = [=, &acc, &run_max, &lsum](int u, const Slot<D>& sl) {
@@ -1272,27 +1281,30 @@ __global__ __launch_bounds__(256, 2) void cur_attn_kernel(AttnArgs a) {
         }
       }
     }
-    const float pinf = a.pinf;
-    float tmax = fmax_nn(fmax_nn(fmax_nn(sa[0][0], sa[0][1], pinf), fmax_nn(sa[0][2], sa[0][3], pinf), pinf),
-                         fmax_nn(fmax_nn(sa[1][0], sa[1][1], pinf), fmax_nn(sa[1][2], sa[1][3], pinf), pinf), pinf);
-    {
-      auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(tmax), __float_as_uint(tmax), false, false);
-      tmax = fmax_nn(__uint_as_float(r[0]), __uint_as_float(r[1]), pinf);
-      r = __builtin_amdgcn_permlane32_swap(__float_as_uint(tmax), __float_as_uint(tmax), false, false);
-      tmax = fmax_nn(__uint_as_float(r[0]), __uint_as_float(r[1]), pinf);
-    }
-    // online softmax with a lazily raised reference (it moves only when a score exceeds it by more than 8
-    // in log2 units, so probabilities stay <= 256 and rescaling is rare)
-    const bool raise = tmax > run_max + 8.0f;            // false while both are -inf
-    if (__builtin_amdgcn_ballot_w64(raise) != 0) {        // uniform: rescale the rows that need it
-      const float nm = raise ? tmax : run_max;
-      const float alpha = raise ? __builtin_amdgcn_exp2f(run_max - nm) : 1.0f;   // exp2(-inf) = 0
-      lsum *= alpha;
+    float ref = lse2;
+    if constexpr (!SUB) {
+      const float pinf = a.pinf;
+      float tmax = fmax_nn(fmax_nn(fmax_nn(sa[0][0], sa[0][1], pinf), fmax_nn(sa[0][2], sa[0][3], pinf), pinf),
+                           fmax_nn(fmax_nn(sa[1][0], sa[1][1], pinf), fmax_nn(sa[1][2], sa[1][3], pinf), pinf), pinf);
+      {
+        auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(tmax), __float_as_uint(tmax), false, false);
+        tmax = fmax_nn(__uint_as_float(r[0]), __uint_as_float(r[1]), pinf);
+        r = __builtin_amdgcn_permlane32_swap(__float_as_uint(tmax), __float_as_uint(tmax), false, false);
+        tmax = fmax_nn(__uint_as_float(r[0]), __uint_as_float(r[1]), pinf);
+      }
+      // online softmax with a lazily raised reference (it moves only when a score exceeds it by more than
+      // 8 in log2 units, so probabilities stay <= 256 and rescaling is rare)
+      const bool raise = tmax > run_max + 8.0f;            // false while both are -inf
+      if (__builtin_amdgcn_ballot_w64(raise) != 0) {        // uniform: rescale the rows that need it
+        const float nm = raise ? tmax : run_max;
+        const float alpha = raise ? __builtin_amdgcn_exp2f(run_max - nm) : 1.0f;   // exp2(-inf) = 0
+        lsum *= alpha;
 #pragma unroll
-      for (int db = 0; db < DB; ++db) acc[db] *= alpha;
-      run_max = nm;
+        for (int db = 0; db < DB; ++db) acc[db] *= alpha;
+        run_max = nm;
+      }
+      ref = run_max == -INFINITY ? 0.0f : run_max;
     }
-    const float ref = run_max == -INFINITY ? 0.0f : run_max;
     float pr[8];
 #pragma unroll
     for (int c = 0; c < 2; ++c)
@@ -1350,6 +1362,15 @@ __global__ __launch_bounds__(256, 2) void cur_attn_kernel(AttnArgs a) {
   // ---- epilogue: lane (j16, g4) holds dims 16 db + 4 g4 .. +3 of row j16 ----------------------------
   lsum = row4_add(lsum);
   if (!row_ok) return;
+  if constexpr (SUB) {                    // the subtract term and the mass, at the row's position in rows
+    const int64_t srow = ((int64_t)b * a.k + p) * a.H + h;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+      *reinterpret_cast<float4*>(a.term_out + srow * D + db * 16 + 4 * g4) =
+          make_float4(acc[db][0], acc[db][1], acc[db][2], acc[db][3]);
+    if (g4 == 0) a.mass_out[srow] = lsum;
+    return;
+  }
   const int64_t orow = ((int64_t)b * a.N + row_i) * HD + (int64_t)h * D;
   const int64_t lrow = ((int64_t)b * a.N + row_i) * a.H + h;
   // the subtract term and mass are the previous loop's add term and mass of this row
@@ -1386,6 +1407,15 @@ __global__ __launch_bounds__(256, 2) void cur_attn_kernel(AttnArgs a) {
     a.lse_ref[lrow] = (run_max + log2f(lsum)) * 0.6931471805599453f - logf(msub);
     if (keep) a.mass_out[trow] = msub;
   }
+}
+
+template <int D>
+__global__ __launch_bounds__(256, 2) void cur_attn_kernel(AttnArgs a) {
+  cur_body<D, false>(a);
+}
+template <int D>
+__global__ __launch_bounds__(256, 2) void cur_sub_kernel(AttnArgs a) {
+  cur_body<D, true>(a);
 }
 
 // Tile records of the sparse update, each an int2 (column, aux):
@@ -1643,8 +1673,33 @@ extern "C" int fl_loop_sparse_attn_terms(const uint16_t* q_cur, const uint16_t* 
   FL_API_END
 }
 
+// Shapes the subtract pass covers: the segment kernels (a list of at most 2048 entries and, with a band,
+// their descriptor table), else the 64-row kernel with the list in LDS (a list of at most kListCap entries).
+static bool subtract_supported(int k, int c_list, int window, int N, int d) {
+  return seg_supported(k, c_list, window, N, d) ||
+         ((d == 64 || d == 128) && window >= 0 && c_list >= 0 && c_list <= kListCap);
+}
+
+extern "C" const char* fl_attn_kernel_name(int pass, int k, int c_list, int window, int B, int N, int H, int d) {
+  if (k < 1 || k > N || B < 1 || H < 1 || c_list < 0 || c_list > N || window < 0 || (d != 64 && d != 128))
+    return nullptr;
+  const int teams = seg_teams(k, c_list, window, N, d, B * H);
+  switch (pass) {
+    case FL_PASS_ADD:
+      return teams == 1 ? "seg1_cur_kernel" : teams == 2 ? "seg_cur_kernel"
+             : c_list <= kListCap ? "cur_attn_kernel" : "reuse_attn_kernel";
+    case FL_PASS_SUBTRACT:
+      return teams == 1 ? "seg1_sub_kernel" : teams == 2 ? "seg_sub_kernel"
+             : c_list <= kListCap ? "cur_sub_kernel" : nullptr;
+    case FL_PASS_BOTH:
+      return "loop_attn_kernel";
+    default:
+      return nullptr;
+  }
+}
+
 extern "C" int fl_loop_subtract_terms_supported(int k, int c_list, int window, int N, int d) {
-  return seg_supported(k, c_list, window, N, d) ? 1 : 0;
+  return subtract_supported(k, c_list, window, N, d) ? 1 : 0;
 }
 
 extern "C" int fl_loop_subtract_terms(const uint16_t* q_prev, const uint16_t* k_cache, const uint16_t* v_cache,
@@ -1664,16 +1719,40 @@ extern "C" int fl_loop_subtract_terms(const uint16_t* q_prev, const uint16_t* k_
   FL_REQUIRE(window >= 0, FL_E_SHAPE, "%s: window must be >= 0", fn);
   FL_REQUIRE(sm_scale > 0.0f && std::isfinite(sm_scale), FL_E_RANGE, "%s: sm_scale must be > 0", fn);
   if (k == 0) return FL_OK;
-  FL_REQUIRE(seg_supported(k, c_list, window, N, d), FL_E_UNSUPPORTED,
-             "%s: shape outside the segment kernel (needs window >= 1, c_list <= 2048; "
-             "fl_loop_sparse_attn runs both passes for every shape)", fn);
+  FL_REQUIRE(subtract_supported(k, c_list, window, N, d), FL_E_UNSUPPORTED,
+             "%s: column list of %d entries above %d (fl_loop_sparse_attn runs both passes for every shape)", fn,
+             c_list, kListCap);
   const hipStream_t st = static_cast<hipStream_t>(stream);
   FL_CHECK_LIST(fn, "rows", rows, B, k, 0, N, st);
   FL_CHECK_LIST(fn, "cols", cols, (int64_t)B * H, c_list, 0, N, st);
-  const int rc = check_f16_range(fn, "v_cache", v_cache, (int64_t)B * N * H * d, st);
-  if (rc != FL_OK) return rc;
-  return launch_seg_sub(q_prev, k_cache, v_cache, rows, k, cols, c_list, window, B, N, H, d, sm_scale, lse_ref,
-                        term_out, mass_out, st);
+  if (seg_supported(k, c_list, window, N, d)) {
+    // (the segment kernel's products with V run in fp16)
+    const int rc = check_f16_range(fn, "v_cache", v_cache, (int64_t)B * N * H * d, st);
+    if (rc != FL_OK) return rc;
+    return launch_seg_sub(q_prev, k_cache, v_cache, rows, k, cols, c_list, window, B, N, H, d, sm_scale, lse_ref,
+                          term_out, mass_out, st);
+  }
+  AttnArgs a{};
+  a.q_prev = q_prev;
+  a.k_cache = k_cache;
+  a.v_cache = v_cache;
+  a.rows = rows;
+  a.cols = cols;
+  a.lse_ref = const_cast<float*>(lse_ref);   // (read only in this pass)
+  a.term_out = term_out;
+  a.mass_out = mass_out;
+  a.k = k;
+  a.c_list = c_list;
+  a.window = window;
+  a.B = B;
+  a.N = N;
+  a.H = H;
+  a.scale_log2 = sm_scale * 1.4426950408889634f;
+  a.cache_current = 1;
+  a.pinf = INFINITY;
+  dim3 grid((unsigned)(((k + 63) / 64) * B * H));
+  if (d == 128) cur_sub_kernel<128><<<grid, 256, 0, st>>>(a);
+  else cur_sub_kernel<64><<<grid, 256, 0, st>>>(a);
+  return check_launch("cur_sub_kernel");
   FL_API_END
 }
-

@@ -101,6 +101,10 @@ __device__ __forceinline__ float fmax_nn(float x, float y, float pinf) { return 
 // Whether the segment kernels (fl_seg_attn.hip) cover a shape.
 bool seg_supported(int k, int c_list, int window, int N, int d);
 
+// Teams per workgroup of the segment kernel a shape takes (bh = B * H): 0 outside seg_supported, 1 for the
+// one-team kernels, 2 for the two-team ones.  The launchers below choose by it.
+int seg_teams(int k, int c_list, int window, int N, int d, int bh);
+
 // Segment kernel of the subtract pass over the previous loop's state; FL_E_UNSUPPORTED without a launch
 // outside seg_supported.
 int launch_seg_sub(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, const int32_t* rows, int k,

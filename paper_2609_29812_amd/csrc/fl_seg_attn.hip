@@ -1,5 +1,5 @@
-// Mass-corrected sparse attention update over row segments (Appendix D.2, Eq. 7; Sections 3.2, 4.2), in two
-// kernels that share one body.
+// Mass-corrected sparse attention update over row segments (Appendix D.2, Eq. 7; Sections 3.2, 4.2): two
+// passes, each in a two-team and a one-team layout, all from one body.
 //   seg_cur_kernel, the add pass, for a loop whose subtract term and mass are given (the previous loop's
 //   stored add term, or the subtract pass below) and whose caches already hold this loop's state:
 //     L_i = log sum_{j in S_i} exp(l_ij),  add_i = sum_j exp(l_ij - L_i) v_j,  l_ij = sigma q_i . k_j,
@@ -17,7 +17,9 @@
 // its last row -- form one sequence in which list and band tiles are interleaved evenly (the band tiles
 // stream from HBM while the list tiles, shared by every segment of the head and kept in L2, keep the
 // matrix cores busy).  Step s gives tile 2s to team 0 and tile 2s + 1 to team 1; each team keeps its own
-// softmax state, and the two are merged per row at the end.
+// softmax state, and the two are merged per row at the end.  Without a band and with enough rows, the
+// one-team kernels (seg1_*: four waves, step s takes tile s, no merge) run two workgroups per CU that step
+// independently instead of eight waves in lockstep.
 //
 // L2 sharing of the band.  Neighbouring segments of a head need the same band columns around their
 // boundary (about w columns).  Each segment walks the band tiles it shares with a neighbour before the
@@ -43,6 +45,8 @@ namespace fl {
 constexpr int kSegRows = 128;        // rows per segment at most (4 groups of 32)
 constexpr int kSegListCap = 2048;    // list entries kept in LDS
 constexpr int kSegTileCap = 2048;    // tile descriptors kept in LDS (list tiles + band tiles of a segment)
+constexpr int kSeg1TileCap = 128;    // the same for the one-team kernels (list tiles only: no band)
+static_assert((kSegListCap + kBN - 1) / kBN + 1 <= kSeg1TileCap, "the one-team table holds every list tile");
 constexpr int kSegSteps = 4;         // ring depth in steps
 
 struct SegArgs {
@@ -64,8 +68,11 @@ struct SegArgs {
   float pinf;                 // +inf (a kernel argument, so the median below is not folded into a max)
 };
 
-template <int D, bool SUB>
+template <int D, bool SUB, int TEAMS>
 __device__ __forceinline__ void seg_body(const SegArgs& a) {
+  static_assert(TEAMS == 1 || TEAMS == 2, "one or two teams of four waves");
+  constexpr int NT = 256 * TEAMS;         // threads
+  constexpr int kTileCap = TEAMS == 2 ? kSegTileCap : kSeg1TileCap;
   constexpr int KS = D / 16;              // k-steps of QK^T (16 dims each)
   constexpr int DB = D / 32;              // 32-dim output blocks
   constexpr int CH = D / 8;               // 16-byte chunks per row
@@ -76,16 +83,16 @@ __device__ __forceinline__ void seg_body(const SegArgs& a) {
   // The four ring slots and the list are separate LDS objects (a slot holds both teams' tiles): the compiler
   // then tells every LDS read apart from the LDS-DMA writes still in flight into the other slots (one
   // object would make it wait for all of them before each read).
-  __shared__ Slot<D> ring0[2], ring1[2], ring2[2], ring3[2];   // step slot s, team t: ring<s>[t]
+  __shared__ Slot<D> ring0[TEAMS], ring1[TEAMS], ring2[TEAMS], ring3[TEAMS];   // step slot s, team t: ring<s>[t]
   __shared__ __attribute__((aligned(16))) int lst[kSegListCap + kBN];   // the (b, h) list, kPad-padded
-  __shared__ int2 tdesc[kSegTileCap];     // per sequence position: first column or entry, kind, group bits
+  __shared__ int2 tdesc[kTileCap];        // per sequence position: first column or entry, kind, group bits
   __shared__ int s_grp[8];                // first and last row of each of the 4 groups
   __shared__ int s_meta[1];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int team = wave >> 2, w4 = wave & 3;
+  const int team = TEAMS == 2 ? wave >> 2 : 0, w4 = wave & 3;
   // the wave's row group: team 0 wave w takes group w, team 1 wave w group w + 2 (mod 4), so the two waves
   // of one group sit on different SIMDs when waves w and w + 4 share one (a band tile is often seen by one
   // or two neighbouring groups only)
@@ -135,9 +142,9 @@ __device__ __forceinline__ void seg_body(const SegArgs& a) {
     s_grp[2 * tid] = has ? rowp[gp0] : 0;
     s_grp[2 * tid + 1] = has ? rowp[min(gp0 + 32, P1) - 1] : -1;
   }
-  for (int i = tid; i < a.c_list; i += 512) lst[i] = cp[i];
+  for (int i = tid; i < a.c_list; i += NT) lst[i] = cp[i];
   __syncthreads();
-  for (int i = tid; i < a.c_list; i += 512)
+  for (int i = tid; i < a.c_list; i += NT)
     if (lst[i] <= lim && (i + 1 == a.c_list || lst[i + 1] > lim)) s_meta[0] = i + 1;
   __syncthreads();
   const int nA = __builtin_amdgcn_readfirstlane(s_meta[0]);
@@ -151,7 +158,7 @@ __device__ __forceinline__ void seg_body(const SegArgs& a) {
   // positions are handed out in pairs (position 2p to team 0, 2p + 1 to team 1), and both positions of a
   // pair hold the same kind of tile, so the two teams do similar work between two barriers
   const int nLP = (nL + 1) / 2, nBP = (nB + 1) / 2, nP = nLP + nBP;
-  const int n_tiles = min(2 * nP, kSegTileCap);   // (the host keeps 2 nP within the table)
+  const int n_tiles = min(2 * nP, kTileCap);   // (the host keeps 2 nP within the table)
   // band tiles shared with the previous segment ([bandLo, its last row]) and with the next one
   // ([its first row - w + 1, bandHi]); the rest in the middle
   int nBot = 0, nTop = 0;
@@ -175,7 +182,7 @@ __device__ __forceinline__ void seg_body(const SegArgs& a) {
   //   x: first list entry (list tile) or first column (band tile), bit 31 set for a band tile;
   //   y: bit g: group g (rows 32 g .. +31) sees some column of the tile; bit 8 + g: it sees every column;
   //      bits 16-20: the last existing column of the tile (band tiles end at the last row); bit 21: empty.
-  for (int u = tid; u < n_tiles; u += 512) {
+  for (int u = tid; u < n_tiles; u += NT) {
     const int pr = u >> 1, t = u & 1;
     const int before = (pr * nLP) / nP, after = ((pr + 1) * nLP) / nP;
     const bool is_list = after > before;
@@ -402,29 +409,29 @@ __device__ __forceinline__ void seg_body(const SegArgs& a) {
   // issues exactly NI VMEM operations per wave.
   __syncthreads();                        // the descriptors
   FL_WAIT_VM(0);                          // query fragments have arrived
-  const int n_steps = (n_tiles + 1) / 2;
+  const int n_steps = (n_tiles + TEAMS - 1) / TEAMS;
   const int n_loop = (n_steps + kSegSteps - 1) / kSegSteps * kSegSteps;
   issue(ring0[0], tile_offs(team));
   __builtin_amdgcn_sched_barrier(0);
-  issue(ring1[0], tile_offs(2 + team));
+  issue(ring1[0], tile_offs(TEAMS + team));
   __builtin_amdgcn_sched_barrier(0);
-  issue(ring2[0], tile_offs(4 + team));
+  issue(ring2[0], tile_offs(2 * TEAMS + team));
   int u = team;                           // this team's position at the current step
   int2 dsc = tdesc[u < n_tiles ? u : 0];  // its descriptor, read one step ahead
   FL_WAIT_VM(2 * NI);                     // step 0 has landed
   convert(ring0[0]);
   auto step = [&](Slot<D>& cur, Slot<D>& nxt, Slot<D>& nx1) __attribute__((always_inline)) {   // (the slots' first tiles; the team's is at tofs)
-    const Offs of = tile_offs(u + 6);
+    const Offs of = tile_offs(u + 3 * TEAMS);
     const int dx = __builtin_amdgcn_readfirstlane(dsc.x), dy = __builtin_amdgcn_readfirstlane(dsc.y);
     const bool have = u < n_tiles;
-    dsc = tdesc[u + 2 < n_tiles ? u + 2 : 0];
+    dsc = tdesc[u + TEAMS < n_tiles ? u + TEAMS : 0];
     FL_WAIT_VM(2 * NI);                   // (step s: converted at the end of step s-1, so already landed)
     lds_barrier();
     if (have) compute(dx, dy, cur);
     issue(nxt, of);                       // (after the math: the step's critical path starts at the barrier)
     FL_WAIT_VM(2 * NI);                   // step s+1 has landed (s+2 and s+3 may be in flight)
     convert(nx1);                         // its value rows to fp16, in the shadow of the other waves' math
-    u += 2;
+    u += TEAMS;
   };
   for (int s = 0; s < n_loop; s += kSegSteps) {
     step(ring0[0], ring3[0], ring1[0]);
@@ -440,7 +447,7 @@ __device__ __forceinline__ void seg_body(const SegArgs& a) {
   // 64 lanes) in slot grp of team 1's half, and the reference and sum of each lane's row (64 x 2) in slot
   // 3 of team 0's half.
   lsum = xor32_add(lsum);                 // the two half-waves hold disjoint columns of the same row
-  {
+  if constexpr (TEAMS == 2) {
     float* xs = reinterpret_cast<float*>(ring3[0].k) + grp * 128;
     float* xo = reinterpret_cast<float*>(grp == 0 ? ring0[1].k : grp == 1 ? ring1[1].k : grp == 2 ? ring2[1].k
                                                                                          : ring3[1].k);
@@ -533,27 +540,51 @@ __device__ __forceinline__ void seg_body(const SegArgs& a) {
 
 template <int D>
 __global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
-  seg_body<D, false>(a);
+  seg_body<D, false, 2>(a);
 }
 template <int D>
 __global__ __launch_bounds__(512, 2) void seg_sub_kernel(SegArgs a) {
-  seg_body<D, true>(a);
+  seg_body<D, true, 2>(a);
+}
+// One team of four waves (no band): two workgroups per CU instead of one lockstep workgroup of eight waves.
+template <int D>
+__global__ __launch_bounds__(256, 2) void seg1_cur_kernel(SegArgs a) {
+  seg_body<D, false, 1>(a);
+}
+template <int D>
+__global__ __launch_bounds__(256, 2) void seg1_sub_kernel(SegArgs a) {
+  seg_body<D, true, 1>(a);
 }
 
-// Whether the segment kernels cover a shape (a band, a list that fits in LDS, the descriptor table).
+// Whether the segment kernels cover a shape: a list that fits in LDS and, with a band, the descriptor table
+// (without one, the table holds at most ceil(c_list / 32) + 1 positions, within either kernel's).
 bool seg_supported(int k, int c_list, int window, int N, int d) {
-  if (window < 1 || c_list > kSegListCap || (d != 64 && d != 128) || k < 1) return false;
+  if (window < 0 || c_list > kSegListCap || (d != 64 && d != 128) || k < 1) return false;
+  if (window == 0) return true;
   // the descriptor table holds every position: at most ceil(c_list / 32) list tiles and ceil(N / 32) + 1 band
   // tiles, plus one empty position per kind when the counts are odd
   return (c_list + kBN - 1) / kBN + (N + kBN - 1) / kBN + 3 <= kSegTileCap;
 }
 
-// Segments per (batch, head): at least one per 128 rows; more (down to 64 rows) while the grid is below one
-// workgroup per CU.  Sets a.n_seg and a.seg_rows.
-static void seg_grid(SegArgs& a, int k, int bh) {
+// One team or two.  Without a band, the one-team kernel runs two independent workgroups per CU, each
+// stepping at its own pace, where the two-team workgroup steps eight waves in lockstep; it pays off once
+// there are about 1.5 full 128-row segments per CU (measured on the 16K batch-4 loops: 12-22 % faster
+// from 706 rows per (b, h) up, 12-14 % slower at 328).  With a band the two teams share the band tiles.
+static bool seg_one_team(int k, int window, int bh) {
+  return window == 0 && (int64_t)((k + kSegRows - 1) / kSegRows) * bh >= 384;
+}
+
+int seg_teams(int k, int c_list, int window, int N, int d, int bh) {
+  if (!seg_supported(k, c_list, window, N, d)) return 0;
+  return seg_one_team(k, window, bh) ? 1 : 2;
+}
+
+// Segments per (batch, head): at least one per 128 rows; more (down to 64 rows) while the grid is below
+// `per_cu` workgroups per CU.  Sets a.n_seg and a.seg_rows.
+static void seg_grid(SegArgs& a, int k, int bh, int per_cu) {
   constexpr int kCUs = 256;
   int n_seg = (k + kSegRows - 1) / kSegRows;
-  const int fill = (kCUs + bh - 1) / bh;
+  const int fill = (per_cu * kCUs + bh - 1) / bh;
   const int n_max = (k + 63) / 64;
   if (n_seg < fill) n_seg = std::min(fill, n_max);
   if (n_seg < 1) n_seg = 1;
@@ -568,16 +599,23 @@ static void seg_grid(SegArgs& a, int k, int bh) {
 int launch_seg_sub(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, const int32_t* rows, int k,
                    const int32_t* cols, int c_list, int window, int B, int N, int H, int d, float sm_scale,
                    const float* lse_ref, float* term_out, float* mass_out, hipStream_t st) {
-  if (!seg_supported(k, c_list, window, N, d)) return FL_E_UNSUPPORTED;
+  const int teams = seg_teams(k, c_list, window, N, d, B * H);
+  if (teams == 0) return FL_E_UNSUPPORTED;
   SegArgs a{};
   a.q = q; a.k_cache = k_cache; a.v_cache = v_cache; a.rows = rows; a.cols = cols;
   a.lse_ref = const_cast<float*>(lse_ref);   // (read only in this pass)
   a.term_out = term_out; a.mass_out = mass_out;
   a.k = k; a.c_list = c_list; a.window = window; a.B = B; a.N = N; a.H = H;
-  seg_grid(a, k, B * H);
+  const bool one = teams == 1;
+  seg_grid(a, k, B * H, one ? 2 : 1);
   a.scale_log2 = sm_scale * 1.4426950408889634f;
   a.pinf = INFINITY;
   dim3 grid((unsigned)(a.n_seg * B * H));
+  if (one) {
+    if (d == 128) seg1_sub_kernel<128><<<grid, 256, 0, st>>>(a);
+    else seg1_sub_kernel<64><<<grid, 256, 0, st>>>(a);
+    return check_launch("seg1_sub_kernel");
+  }
   if (d == 128) seg_sub_kernel<128><<<grid, 512, 0, st>>>(a);
   else seg_sub_kernel<64><<<grid, 512, 0, st>>>(a);
   return check_launch("seg_sub_kernel");
@@ -589,18 +627,23 @@ int launch_seg_cur(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v
                    const int32_t* cols, int c_list, int window, int B, int N, int H, int d, float sm_scale,
                    float* lse_ref, float* o, const float* term_prev, const float* mass_prev,
                    const int32_t* slot_prev, int k_prev, float* term_out, float* mass_out, hipStream_t st) {
-  // (without a band, the 64-row kernel over the list alone measured faster: the segment layout pays off
-  // when the band's HBM stream is there to overlap)
-  if (!seg_supported(k, c_list, window, N, d)) return FL_E_UNSUPPORTED;
+  const int teams = seg_teams(k, c_list, window, N, d, B * H);
+  if (teams == 0) return FL_E_UNSUPPORTED;
   SegArgs a{};
   a.q = q; a.k_cache = k_cache; a.v_cache = v_cache; a.rows = rows; a.cols = cols;
   a.lse_ref = lse_ref; a.o = o; a.term_prev = term_prev; a.mass_prev = mass_prev; a.slot_prev = slot_prev;
   a.term_out = term_out; a.mass_out = mass_out;
   a.k = k; a.k_prev = k_prev; a.c_list = c_list; a.window = window; a.B = B; a.N = N; a.H = H;
-  seg_grid(a, k, B * H);
+  const bool one = teams == 1;
+  seg_grid(a, k, B * H, one ? 2 : 1);
   a.scale_log2 = sm_scale * 1.4426950408889634f;
   a.pinf = INFINITY;
   dim3 grid((unsigned)(a.n_seg * B * H));
+  if (one) {
+    if (d == 128) seg1_cur_kernel<128><<<grid, 256, 0, st>>>(a);
+    else seg1_cur_kernel<64><<<grid, 256, 0, st>>>(a);
+    return check_launch("seg1_cur_kernel");
+  }
   if (d == 128) seg_cur_kernel<128><<<grid, 512, 0, st>>>(a);
   else seg_cur_kernel<64><<<grid, 512, 0, st>>>(a);
   return check_launch("seg_cur_kernel");

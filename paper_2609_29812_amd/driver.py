@@ -63,6 +63,13 @@ def setup(q1, k1, v1, base_bits, group, n_sink, t, window, tail=0):
     return st
 
 
+def subtract_pass_first(k, c_list, window, B, N, H, d):
+    """Whether a loop without stored terms runs as the subtract pass, the commit and the add pass (rather
+    than the two-pass kernel): with a band, where the segment kernels take both passes.  Without a band the
+    two-pass kernel, which reads each list tile once for both passes, measured faster on every workload."""
+    return window > 0 and fl.attn_kernel_name(fl.PASS_SUBTRACT, k, c_list, window, B, N, H, d) == "seg_sub_kernel"
+
+
 def sparse_step(st: LayerState, qr, qp, kr, kp, vr, vp, k_r, bits, keep=False):
     """Advance the layer by one sparse loop.  Returns the loop's outputs when keep=True."""
     idx, slot, key = fl.select_tokens(kr, kp, vr, vp, k_r, cand=st.cand)
@@ -74,7 +81,7 @@ def sparse_step(st: LayerState, qr, qp, kr, kp, vr, vp, k_r, bits, keep=False):
         mass = torch.empty(B, k, H, dtype=torch.float32, device=kr.device)
     k_new = v_new = None
     reuse = st.reuse and st.term is not None
-    split = not reuse and fl.subtract_terms_supported(k, st.cols.shape[2], st.window, N, d)
+    split = not reuse and subtract_pass_first(k, st.cols.shape[2], st.window, B, N, H, d)
     if reuse or split:
         term_prev, mass_prev, slot_prev = st.term, st.mass, st.slot_prev
         if split:

@@ -21,6 +21,7 @@ AXIS_CHANNEL = 1
 DQ_COMPACT = 0
 DQ_COMMIT = 1
 ATTN_DENSE = 1
+PASS_ADD, PASS_SUBTRACT, PASS_BOTH = 0, 1, 2
 
 _c_p = ctypes.c_void_p
 _c_i = ctypes.c_int
@@ -52,6 +53,7 @@ _SIGNATURES = {
                                          _c_i, _c_i, _c_i, _c_i, _c_f, _c_p, _c_p, _c_p, _c_p, _c_p, _c_i, _c_p,
                                          _c_p, _c_p, _c_sz, _c_p]),
     "fl_loop_subtract_terms_supported": (_c_i, [_c_i, _c_i, _c_i, _c_i, _c_i]),
+    "fl_attn_kernel_name": (ctypes.c_char_p, [_c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i]),
     "fl_loop_subtract_terms": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_i, _c_p, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_f,
                                       _c_p, _c_p, _c_p, _c_p]),
     "fl_column_scores_ws": (_c_sz, [_c_i, _c_i, _c_i]),
@@ -331,8 +333,15 @@ def loop_sparse_attn(q_cur, q_prev, k_cache, v_cache, k_new, v_new, slot, rows, 
     return o, lse_ref
 
 
+def attn_kernel_name(pass_, k, c_list, window, B, N, H, d):
+    """Name of the kernel an attention pass launches for the shape, or None (fl_attn_kernel_name; host only).
+    pass_: PASS_ADD (add pass over current caches), PASS_SUBTRACT or PASS_BOTH."""
+    name = load().fl_attn_kernel_name(pass_, k, c_list, window, B, N, H, d)
+    return None if name is None else name.decode()
+
+
 def subtract_terms_supported(k, c_list, window, N, d):
-    """Whether fl_loop_subtract_terms covers the shape (the segment kernel)."""
+    """Whether fl_loop_subtract_terms covers the shape (a column list of at most 3072 entries)."""
     return bool(load().fl_loop_subtract_terms_supported(k, c_list, window, N, d))
 
 

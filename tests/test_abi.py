@@ -180,3 +180,30 @@ def test_decode_noalloc_argument_checks(lib):
     assert dec(cn=None) == FL_E_NULL
     assert dec(B=64, T=65536, H=16, d=128) == FL_E_RANGE                     # beyond the scratch array
     assert b"scratch" in lib.fl_last_error()
+
+
+def test_attention_kernel_names(lib):
+    """The host-side query names the kernel each pass launches (no device call)."""
+    name = fl.attn_kernel_name
+    # 32K workload: band 512, list 2048, 1638 rows, 16 heads -> the two-team segment kernels
+    assert name(fl.PASS_ADD, 1638, 2048, 512, 1, 32768, 16, 128) == "seg_cur_kernel"
+    assert name(fl.PASS_SUBTRACT, 1638, 2048, 512, 1, 32768, 16, 128) == "seg_sub_kernel"
+    assert name(fl.PASS_BOTH, 1638, 2048, 512, 1, 32768, 16, 128) == "loop_attn_kernel"
+    # no band: one team from about 1.5 full 128-row segments per CU (ceil(k / 128) * B * H >= 384), else two
+    assert name(fl.PASS_ADD, 706, 1024, 0, 4, 16384, 16, 128) == "seg1_cur_kernel"      # 6 * 64 = 384
+    assert name(fl.PASS_SUBTRACT, 706, 1024, 0, 4, 16384, 16, 128) == "seg1_sub_kernel"
+    assert name(fl.PASS_ADD, 640, 1024, 0, 4, 16384, 16, 128) == "seg_cur_kernel"       # 5 * 64 = 320
+    assert name(fl.PASS_ADD, 410, 512, 0, 1, 4096, 16, 128) == "seg_cur_kernel"
+    # lists beyond the segment kernels' LDS copy: the 64-row kernels, then the record-driven one
+    assert name(fl.PASS_ADD, 500, 2049, 64, 1, 8192, 16, 128) == "cur_attn_kernel"
+    assert name(fl.PASS_SUBTRACT, 500, 3072, 0, 1, 8192, 16, 64) == "cur_sub_kernel"
+    assert name(fl.PASS_ADD, 500, 3073, 64, 1, 8192, 16, 128) == "reuse_attn_kernel"
+    assert name(fl.PASS_SUBTRACT, 500, 3073, 64, 1, 8192, 16, 128) is None
+    # arguments outside the domain
+    assert name(fl.PASS_ADD, 0, 512, 0, 1, 4096, 16, 128) is None
+    assert name(fl.PASS_ADD, 100, 512, 0, 1, 4096, 16, 96) is None
+    assert name(7, 100, 512, 0, 1, 4096, 16, 128) is None
+    # the subtract query agrees with the name
+    for args in [(1638, 2048, 512, 32768, 128), (100, 512, 0, 4096, 128), (100, 3073, 0, 4096, 128)]:
+        k, c, w, N, d = args
+        assert fl.subtract_terms_supported(k, c, w, N, d) == (name(fl.PASS_SUBTRACT, k, c, w, 1, N, 16, d) is not None)

@@ -365,7 +365,19 @@ def test_sparse_attn_stepwise_from_oracle_state(F, name, over):
                                        ("C4", dict(seq=1500, heads=2, batch=2, window=128, col_budget=4 + 128 + 200)),
                                        ("C4", dict(seq=1500, heads=2, window=128, n_sink=0, col_budget=128)),
                                        ("C4", dict(seq=1300, heads=2, head_dim=64, window=96, col_budget=4 + 96 + 120)),
-                                       ("C4", dict(seq=600, heads=2, window=64, col_budget=4 + 64 + 50))])
+                                       ("C4", dict(seq=600, heads=2, window=64, col_budget=4 + 64 + 50)),
+                                       # the 64-row kernel: no band (d = 128 with a ragged row tile, d = 64,
+                                       # two batch elements over seven sparse loops), and a band with a list
+                                       # longer than the segment kernel keeps
+                                       ("C2", dict(seq=900, heads=2, col_budget=100)),
+                                       ("C1", dict()),
+                                       ("C5", dict(seq=600, heads=2, batch=2)),
+                                       ("C4", dict(seq=2600, heads=1, window=64, col_budget=4 + 64 + 2100)),
+                                       # enough rows for the one-team kernels (ceil(k / 128) * B * H = 384)
+                                       ("C5", dict(seq=1600, heads=16, batch=2, loops=2, hot_frac=(0.9,),
+                                                   topk_frac=(0.9,), bits=(4,), col_budget=100)),
+                                       ("C5", dict(seq=1600, heads=16, head_dim=64, batch=2, loops=2,
+                                                   hot_frac=(0.9,), topk_frac=(0.9,), bits=(2,), col_budget=60))])
 def test_subtract_pass_then_add_pass_from_oracle_state(F, name, over):
     """fl_loop_subtract_terms on the oracle's loop r-1 state: every row's subtract term and mass against the
     oracle's subtract half of Eq. 7; then the new rows committed and the add pass run with those terms
@@ -381,6 +393,10 @@ def test_subtract_pass_then_add_pass_from_oracle_state(F, name, over):
     cols_np = np.stack([np.stack([rec.cols[b, h] for h in range(H)]) for b in range(B)])
     cols = up(cols_np)
     assert F.subtract_terms_supported(rec.loops[0].idx.shape[1], cols_np.shape[2], w.window, N, d)
+    for lr in rec.loops:
+        say(f" loop {lr.r}: k={lr.idx.shape[1]} subtract pass "
+            f"{F.attn_kernel_name(F.PASS_SUBTRACT, lr.idx.shape[1], cols_np.shape[2], w.window, B, N, H, d)}, add pass "
+            f"{F.attn_kernel_name(F.PASS_ADD, lr.idx.shape[1], cols_np.shape[2], w.window, B, N, H, d)}")
     for lr in rec.loops:
         r = lr.r
         k = lr.idx.shape[1]
@@ -423,21 +439,29 @@ def test_subtract_pass_then_add_pass_from_oracle_state(F, name, over):
 
 
 def test_subtract_pass_coverage_and_arguments(F):
-    """The query follows the segment kernel's domain (a band, a list of at most 2048 entries); outside it the
-    call returns FL_E_UNSUPPORTED without a launch; k = 0 is a no-op."""
+    """The query covers lists of at most 3072 entries (the segment kernel with a band and at most 2048, the
+    64-row kernel otherwise); beyond that the call returns FL_E_UNSUPPORTED without a launch; k = 0 is a
+    no-op."""
     from paper_2609_29812_amd.flashloop import FlashLoopError
     assert F.subtract_terms_supported(100, 512, 64, 4096, 128)
     assert F.subtract_terms_supported(100, 2048, 1, 4096, 64)
-    assert not F.subtract_terms_supported(100, 512, 0, 4096, 128)       # no band
-    assert not F.subtract_terms_supported(100, 2049, 64, 4096, 128)     # list beyond the LDS copy
+    assert F.subtract_terms_supported(100, 512, 0, 4096, 128)           # no band
+    assert F.subtract_terms_supported(100, 3072, 64, 4096, 128)         # beyond the segment kernel's list
+    assert not F.subtract_terms_supported(100, 3073, 64, 4096, 128)     # list beyond the LDS copy
+    assert not F.subtract_terms_supported(100, 3073, 0, 4096, 128)
     assert not F.subtract_terms_supported(100, 512, 64, 4096, 96)       # head dim
     B, N, H, d = 1, 256, 2, 64
     q = torch.zeros(B, N, H, d, dtype=torch.bfloat16, device="cuda")
     rows = torch.arange(0, N, 4, dtype=torch.int32, device="cuda").view(1, -1)
     cols = torch.arange(0, 32, dtype=torch.int32, device="cuda").view(1, 1, -1).repeat(1, H, 1).contiguous()
     lse = torch.zeros(B, N, H, dtype=torch.float32, device="cuda")
-    with pytest.raises(FlashLoopError, match="outside the segment kernel"):
-        F.subtract_terms(q, q, q, rows, cols, 0, lse)
+    N4 = 4096
+    q4 = torch.zeros(B, N4, H, d, dtype=torch.bfloat16, device="cuda")
+    rows4 = torch.arange(0, N4, 64, dtype=torch.int32, device="cuda").view(1, -1)
+    long_cols = torch.arange(0, 3100, dtype=torch.int32, device="cuda").view(1, 1, -1).repeat(1, H, 1).contiguous()
+    lse4 = torch.zeros(B, N4, H, dtype=torch.float32, device="cuda")
+    with pytest.raises(FlashLoopError, match="above 3072"):
+        F.subtract_terms(q4, q4, q4, rows4, long_cols, 0, lse4)
     empty = torch.zeros(1, 0, dtype=torch.int32, device="cuda")
     t, m = F.subtract_terms(q, q, q, empty, cols, 16, lse)
     assert t.shape == (1, 0, H, d) and m.shape == (1, 0, H)
