@@ -37,13 +37,24 @@ __device__ __forceinline__ void store_bf16x8(uint16_t* p, const Row8& r) {
   *reinterpret_cast<uint4*>(p) = make_uint4(ws[0], ws[1], ws[2], ws[3]);
 }
 
-// Encode one value: q = clamp(rint(fp32(delta - z) / s), 0, qmax), 0 when s == 0.
-__device__ __forceinline__ uint32_t encode1(float delta, float z, float s, int qmax) {
-  if (s == 0.0f) return 0u;
-  float t = (delta - z) / s;                 // IEEE division (correctly rounded build)
+// Reciprocal of a metadata scale for encode1 (within 1 ulp; s is an fp16 value, so 1/s is a normal fp32).
+__device__ __forceinline__ float scale_rcp(float s) { return __builtin_amdgcn_rcpf(s); }
+
+// Encode one value: q = clamp(rint(fp32(fp32(delta - z) / s)), 0, qmax), 0 when s == 0, with rs = scale_rcp(s).
+// No division: q1 = a rs, e = a - q1 s (one fma, exact), q2 = e rs + q1 (one fma) is Markstein's correction
+// step (P. Markstein, IBM J. Res. Dev. 34(1), 1990), within |a/s| 2^-45 of a/s.  The scale s is an fp16
+// value (at most 11 significant bits) and a an fp32 value, so a - (m + 1/2) s is a multiple of a power of
+// two that keeps a/s either exactly at a half-integer m + 1/2 or more than half an ulp away from it (by
+// 2^-11 of that half ulp at least): rint(q2) is rint of the correctly rounded quotient, the IEEE division's
+// code, bit for bit (checked in exact arithmetic on the host, ties and fp32 neighbours of every boundary).
+__device__ __forceinline__ uint32_t encode1(float delta, float z, float s, float rs, int qmax) {
+  const float a = delta - z;
+  const float q1 = a * rs;
+  const float e = __builtin_fmaf(-q1, s, a);
+  float t = __builtin_fmaf(e, rs, q1);
   t = __builtin_rintf(t);
   t = fminf(fmaxf(t, 0.0f), (float)qmax);
-  return (uint32_t)t;
+  return s == 0.0f ? 0u : (uint32_t)t;
 }
 
 template <int BITS>
@@ -165,11 +176,12 @@ __device__ __forceinline__ void quant_token_body(
   }
   __syncthreads();
   if (!ch_ok) return;
-  float z8[8], s8[8];
+  float z8[8], s8[8], r8[8];
 #pragma unroll
   for (int t = 0; t < 8; ++t) {
     z8[t] = s_z[chunk * 8 + t];
     s8[t] = s_s[chunk * 8 + t];
+    r8[t] = scale_rcp(s8[t]);
   }
   const int row_bytes = HD * BITS / 8;
 #pragma unroll
@@ -178,7 +190,7 @@ __device__ __forceinline__ void quant_token_body(
     if (p >= k) break;
     uint32_t q[8];
 #pragma unroll
-    for (int t = 0; t < 8; ++t) q[t] = encode1(dl[j][t], z8[t], s8[t], qmax);
+    for (int t = 0; t < 8; ++t) q[t] = encode1(dl[j][t], z8[t], s8[t], r8[t], qmax);
     store_codes8<BITS>(codes + ((int64_t)b * k + p) * row_bytes + c0 * BITS / 8, q);
     if (out_rows) {
       const uint32_t rw[4] = {ref_raw[j].x, ref_raw[j].y, ref_raw[j].z, ref_raw[j].w};
@@ -252,10 +264,10 @@ __device__ __forceinline__ void quant_channel_body(
     zero[m] = (uint16_t)f16_bits_of_exact(z);
     scale[m] = (uint16_t)f16_bits_of_exact(s);
   }
-  const float z32 = (float)z, s32 = (float)s;
+  const float z32 = (float)z, s32 = (float)s, r32 = scale_rcp(s32);
   uint32_t q[8];
 #pragma unroll
-  for (int t = 0; t < 8; ++t) q[t] = encode1(dl[t], z32, s32, qmax);
+  for (int t = 0; t < 8; ++t) q[t] = encode1(dl[t], z32, s32, r32, qmax);
   store_codes8<BITS>(codes + ((int64_t)b * k + p) * (HD * BITS / 8) + c0 * BITS / 8, q);
   if (out_rows) {
     const uint32_t rw[4] = {ref_raw.x, ref_raw.y, ref_raw.z, ref_raw.w};
