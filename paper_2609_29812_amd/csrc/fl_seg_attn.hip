@@ -238,10 +238,10 @@ __device__ __forceinline__ void seg_body(const SegArgs& a) {
     lsw[t] = (uint32_t)((lane % CH) ^ swz32_f<D>(lcol[t])) * 16 + head_off;
   }
   struct Offs { uint32_t o[NIK]; };
-  auto tile_offs = [&](int u) __attribute__((always_inline)) {
+  // (the descriptor of position u is passed in: the step reads the next DMA tile's a step ahead)
+  auto tile_offs_d = [&](int u, int2 dsc) __attribute__((always_inline)) {
     Offs r;
     const bool have = u < n_tiles;
-    const int2 dsc = tdesc[have ? u : 0];
     const int dx = __builtin_amdgcn_readfirstlane(dsc.x), dy = __builtin_amdgcn_readfirstlane(dsc.y);
     const bool in_list = dx >= 0;
     const int f = dx & 0x7FFFFFFF;
@@ -254,6 +254,9 @@ __device__ __forceinline__ void seg_body(const SegArgs& a) {
       r.o[t] = ((id != kPad) & (lcol[t] <= hi)) ? (uint32_t)id * rb + lsw[t] : kOOB;
     }
     return r;
+  };
+  auto tile_offs = [&](int u) __attribute__((always_inline)) {
+    return tile_offs_d(u, tdesc[u < n_tiles ? u : 0]);
   };
   auto issue = [&](Slot<D>& sl, const Offs& of) __attribute__((always_inline)) {
 #pragma unroll
@@ -425,10 +428,14 @@ __device__ __forceinline__ void seg_body(const SegArgs& a) {
   issue(ring2[0], tile_offs(2 * TEAMS + team));
   int u = team;                           // this team's position at the current step
   int2 dsc = tdesc[u < n_tiles ? u : 0];  // its descriptor, read one step ahead
+  // the descriptor of the tile the step DMAs, also read a step ahead, so the offsets at the top of a step
+  // wait on the list reads alone (1-2 % on both 32K passes)
+  int2 dsc_dma = tdesc[u + 3 * TEAMS < n_tiles ? u + 3 * TEAMS : 0];
   FL_WAIT_VM(2 * NI);                     // step 0 has landed
   convert(ring0[0]);
   auto step = [&](Slot<D>& cur, Slot<D>& nxt, Slot<D>& nx1) __attribute__((always_inline)) {   // (the slots' first tiles; the team's is at tofs)
-    const Offs of = tile_offs(u + 3 * TEAMS);
+    const Offs of = tile_offs_d(u + 3 * TEAMS, dsc_dma);
+    dsc_dma = tdesc[u + 4 * TEAMS < n_tiles ? u + 4 * TEAMS : 0];
     const int dx = __builtin_amdgcn_readfirstlane(dsc.x), dy = __builtin_amdgcn_readfirstlane(dsc.y);
     const bool have = u < n_tiles;
     dsc = tdesc[u + TEAMS < n_tiles ? u + TEAMS : 0];
