@@ -153,12 +153,12 @@ class Step:
                 # the subtract pass over the loop-1 state, then as loops 3, 4: quantize and commit in one
                 # pass, and the add pass over the caches with the just-computed subtract terms
                 sub, msub = timed(f"sub r{r}", lambda: fl.subtract_terms(qp, gs.k_hat, gs.v_hat, idx, gs.cols,
-                                                                         gs.window, gs.lse))
+                                                                         gs.window, gs.lse, v16=gs.v16))
                 timed(f"quant_kv r{r}", lambda: fl.kv_residual_quant_kv(
-                    kr, gs.k_hat, vr, gs.v_hat, idx, bits, gs.group, mode=fl.DQ_COMMIT))
+                    kr, gs.k_hat, vr, gs.v_hat, idx, bits, gs.group, mode=fl.DQ_COMMIT, v_f16=gs.v16))
                 timed(f"attn r{r}", lambda: fl.loop_sparse_attn(
                     qr, None, gs.k_hat, gs.v_hat, None, None, slot, idx, gs.cols, gs.window, gs.lse, gs.o,
-                    term_prev=sub, mass_prev=msub, slot_prev=slot, term_out=term, mass_out=mass))
+                    term_prev=sub, mass_prev=msub, slot_prev=slot, term_out=term, mass_out=mass, v16=gs.v16))
             elif r == 2:
                 # both passes: quantize (compact new rows), attend, then commit into the caches
                 (ck, sk, zk, k_new), (cv, sv, zv, v_new) = timed(f"quant_kv r{r}", lambda: fl.kv_residual_quant_kv(
@@ -168,13 +168,16 @@ class Step:
                     term_out=term, mass_out=mass))
                 timed(f"commit_kv r{r}", lambda: fl.kv_residual_dequant_kv(
                     (ck, sk, zk), (cv, sv, zv), idx, bits, gs.group, gs.k_hat, gs.v_hat, mode=fl.DQ_COMMIT))
+                if gs.v16 is not None:
+                    timed(f"v16 r{r}", lambda: fl.kv_f16_rows(gs.v_hat, idx, out=gs.v16))
             else:
                 # the add pass alone: quantize and commit in one pass, then attend over the caches
                 timed(f"quant_kv r{r}", lambda: fl.kv_residual_quant_kv(
-                    kr, gs.k_hat, vr, gs.v_hat, idx, bits, gs.group, mode=fl.DQ_COMMIT))
+                    kr, gs.k_hat, vr, gs.v_hat, idx, bits, gs.group, mode=fl.DQ_COMMIT, v_f16=gs.v16))
                 timed(f"attn r{r}", lambda: fl.loop_sparse_attn(
                     qr, None, gs.k_hat, gs.v_hat, None, None, slot, idx, gs.cols, gs.window, gs.lse, gs.o,
-                    term_prev=gs.term, mass_prev=gs.mass, slot_prev=gs.slot_prev, term_out=term, mass_out=mass))
+                    term_prev=gs.term, mass_prev=gs.mass, slot_prev=gs.slot_prev, term_out=term, mass_out=mass,
+                    v16=gs.v16))
             gs.term, gs.mass, gs.slot_prev = term, mass, slot
             trace.append((r, idx, slot))
             gs.cand = idx
@@ -488,10 +491,14 @@ def measure(w, dev, driver, fl, torch, steps, warmup, log_calls=False):
         kr, bits = w.k(r), w.bits_at(r)
         split = r == 2 and f"sub r{r}" in dur_us
         by, fl_ = attn_work(idx, cols, slot, N, H, d, w.window, B, reuse=r > 2 or split, current=r > 2 or split)
+        # the fp16 copy of the committed value rows (written by the quantizer, or after the separate commit)
+        v16_bytes = B * kr * H * d * 2 if gs.v16 is not None else 0
+        two_pass = r == 2 and not split
         work = {
             f"select r{r}": (select_bytes(n_cand, N, H * d, kr, B), 0.0),
             f"quant_kv r{r}": (codec_bytes(kr, H, d, bits, w.group, True, B)
-                               + codec_bytes(kr, H, d, bits, w.group, False, B) - B * kr * 4, 0.0),
+                               + codec_bytes(kr, H, d, bits, w.group, False, B) - B * kr * 4
+                               + (0 if two_pass else v16_bytes), 0.0),
             f"attn r{r}": (by, fl_),
         }
         if split:
@@ -499,6 +506,8 @@ def measure(w, dev, driver, fl, torch, steps, warmup, log_calls=False):
         elif r == 2:
             work[f"commit_kv r{r}"] = (commit_bytes(kr, H, d, bits, w.group, True, B)
                                        + commit_bytes(kr, H, d, bits, w.group, False, B) - B * kr * 4, 0.0)
+            if f"v16 r{r}" in dur_us:
+                work[f"v16 r{r}"] = (2 * v16_bytes + B * kr * 4, 0.0)   # bf16 rows read, fp16 rows written
         for name, (nb, nf) in work.items():
             us = dur_us[name]
             kernels[name] = {"us": round(us, 2), "GB/s": round(nb / us / 1e3, 1),

@@ -171,6 +171,27 @@ int fl_kv_residual_quant_kv(const uint16_t* k_cur, uint16_t* k_ref, const uint16
                             uint8_t* v_codes, uint16_t* v_scale, uint16_t* v_zero,
                             uint16_t* k_rows, uint16_t* v_rows, int mode, void* stream);
 
+/* (2c') The same with an fp16 copy of the value cache kept current -- for the attention calls of (3e).
+ * COMMIT mode of (2c) (no compact rows): rows idx of k_ref and v_ref are updated in place, and rows idx of
+ * v_f16 (fp16 [B, N, H, d], the value cache's copy) receive fp16(v_ref) of the updated rows, each value
+ * rounded to nearest even from its bf16 value (exact for 2^-14 <= |v| <= 65504; smaller magnitudes round
+ * to a multiple of 2^-24, larger ones overflow).  k_ref, v_ref and v_f16 are required and distinct.
+ * Other arguments and outputs as fl_kv_residual_quant_kv with mode FL_DQ_COMMIT. */
+int fl_kv_residual_quant_kv_v16(const uint16_t* k_cur, uint16_t* k_ref, const uint16_t* v_cur, uint16_t* v_ref,
+                                uint16_t* v_f16, const int32_t* idx, int k, int B, int N, int H, int d, int bits,
+                                int group, uint8_t* k_codes, uint16_t* k_scale, uint16_t* k_zero,
+                                uint8_t* v_codes, uint16_t* v_scale, uint16_t* v_zero, void* stream);
+
+/* (2c'') fp16 copy of rows of a bf16 tensor -- the value cache's copy for the attention calls of (3e).
+ *   x     : bf16 [B, N, H, d] (d a multiple of 8);  x_f16 : fp16 [B, N, H, d], distinct from x.
+ *   idx   : int32 [B, k] rows to copy (ascending, in [0, N)), or NULL with k = N for every row; k = 0
+ *           copies nothing (idx may then be NULL).
+ * x_f16[b, i] = fp16(x[b, i]) for the rows named, rounding as in (2c'); other rows are left unchanged.
+ * Used after the calls that write the value cache without the copy (the base codec of the set-up, the
+ * bf16 tail of (6), the COMMIT of (2d)). */
+int fl_kv_f16_rows(const uint16_t* x, const int32_t* idx, int k, int B, int N, int H, int d, uint16_t* x_f16,
+                   void* stream);
+
 /* (2d) Reconstruction of keys and values in one call -- Eq. 4 and Appendix D.3, Eq. 8 with the axes of
  * (2c).  Bitwise the results of fl_kv_residual_dequant for the keys (FL_AXIS_TOKEN) and the values
  * (FL_AXIS_CHANNEL) with the same bits, group and mode; one kernel launch.
@@ -251,7 +272,7 @@ int fl_loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev,
  *     only, with one 16-row group per wave;
  *   - with term_prev and k_new = v_new = NULL: k_cache and v_cache already hold X_hat^(r) of the updated
  *     rows (committed before this call, e.g. by fl_kv_residual_quant_commit), and every column is read
- *     from them.
+ *     from them; slot may then be NULL and no workspace is needed (no tile records are built).
  * term_prev and term_out may not alias.  Other arguments as fl_loop_sparse_attn (never DENSE).
  * ---------------------------------------------------------------------------------------------- */
 int fl_loop_sparse_attn_terms(const uint16_t* q_cur, const uint16_t* q_prev,
@@ -292,6 +313,27 @@ int fl_loop_subtract_terms(const uint16_t* q_prev, const uint16_t* k_cache, cons
                            const int32_t* rows, int k, const int32_t* cols, int c_list, int window,
                            int B, int N, int H, int d, float sm_scale, const float* lse_ref,
                            float* term_out, float* mass_out, void* stream);
+
+/* ------------------------------------------------------------------------------------------------
+ * (3e) The add pass over current caches and the subtract pass, reading the values from an fp16 copy.
+ * v_cache_f16 (fp16 [B, N, H, d]) must equal fp16(v_cache) row for row (kept by (2c') and (2c'')); the
+ * segment kernels then load value tiles as they are instead of converting them in LDS (the same
+ * rounding, so the results are bitwise those of the calls without the copy), and the other kernels
+ * ignore it.  fl_loop_sparse_attn_terms_v16: fl_loop_sparse_attn_terms with q_prev, k_new, v_new and
+ * slot NULL, term_prev required and no workspace (given terms over current caches build no tile
+ * records).  fl_loop_subtract_terms_v16: fl_loop_subtract_terms.  Arguments otherwise as there.
+ * ---------------------------------------------------------------------------------------------- */
+int fl_loop_sparse_attn_terms_v16(const uint16_t* q_cur, const uint16_t* k_cache, const uint16_t* v_cache,
+                                  const uint16_t* v_cache_f16, const int32_t* rows, int k, const int32_t* cols,
+                                  int c_list, int window, int B, int N, int H, int d, float sm_scale,
+                                  float* lse_ref, float* o, const float* term_prev, const float* mass_prev,
+                                  const int32_t* slot_prev, int k_prev, float* term_out, float* mass_out,
+                                  void* stream);
+
+int fl_loop_subtract_terms_v16(const uint16_t* q_prev, const uint16_t* k_cache, const uint16_t* v_cache,
+                               const uint16_t* v_cache_f16, const int32_t* rows, int k, const int32_t* cols,
+                               int c_list, int window, int B, int N, int H, int d, float sm_scale,
+                               const float* lse_ref, float* term_out, float* mass_out, void* stream);
 
 /* ------------------------------------------------------------------------------------------------
  * (3d) Which kernel an attention call launches -- for profilers that look the launch up in a trace.

@@ -1512,7 +1512,7 @@ extern "C" size_t fl_loop_sparse_attn_ws(int B, int N, int H, int d, int k, int 
 }
 
 static int loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev, const uint16_t* k_cache,
-                            const uint16_t* v_cache, const uint16_t* k_new, const uint16_t* v_new,
+                            const uint16_t* v_cache, const uint16_t* v16, const uint16_t* k_new, const uint16_t* v_new,
                             const int32_t* slot, const int32_t* rows, int k, const int32_t* cols, int c_list,
                             int window, int B, int N, int H, int d, float sm_scale, int flags, float* lse_ref,
                             float* o, const float* term_prev, const float* mass_prev, const int32_t* slot_prev,
@@ -1534,7 +1534,8 @@ static int loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev, const
     FL_REQUIRE(rows == nullptr && k == N, FL_E_SHAPE, "fl_loop_sparse_attn: DENSE needs rows == NULL and k == N");
     FL_REQUIRE(!reuse && term_out == nullptr, FL_E_UNSUPPORTED, "fl_loop_sparse_attn: DENSE keeps no terms");
   } else {
-    FL_REQUIRE(slot && rows && (reuse || q_prev), FL_E_NULL,
+    // (with given terms over current caches the tiles come straight from cols and the band: no slot map)
+    FL_REQUIRE(rows && (reuse || q_prev) && (slot || (reuse && k_new == nullptr)), FL_E_NULL,
                "fl_loop_sparse_attn: q_prev (unless reusing terms), slot and rows are required");
     FL_REQUIRE((k_new == nullptr) == (v_new == nullptr), FL_E_NULL,
                "fl_loop_sparse_attn: k_new and v_new go together");
@@ -1549,8 +1550,10 @@ static int loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev, const
       FL_REQUIRE(k_prev >= k && k_prev <= N, FL_E_RANGE, "fl_loop_sparse_attn: k_prev=%d outside [k, N]", k_prev);
     }
   }
-  const size_t need = attn_ws_bytes(B, N, H, k, c_list, dense);
-  FL_REQUIRE(dense || rec_layout(B, N, H, k, c_list).n_rec * sizeof(int2) <= ((size_t)1 << 31) - 8, FL_E_SHAPE,
+  // (given terms over current caches build no tile records: no workspace)
+  const bool current = !dense && reuse && k_new == nullptr;
+  const size_t need = current ? 0 : attn_ws_bytes(B, N, H, k, c_list, dense);
+  FL_REQUIRE(dense || current || rec_layout(B, N, H, k, c_list).n_rec * sizeof(int2) <= ((size_t)1 << 31) - 8, FL_E_SHAPE,
              "fl_loop_sparse_attn: tile records above 2^31 bytes (reduce B * H * c_list + B * (N + k))");
   FL_REQUIRE(need == 0 || (ws && ws_bytes >= need), FL_E_WORKSPACE,
              "fl_loop_sparse_attn: workspace of %zu bytes required", need);
@@ -1625,7 +1628,7 @@ static int loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev, const
   }
 #define FL_REUSE(DD, CC) reuse_attn_kernel<DD, CC><<<grid, 256, 0, st>>>(a)
   if (a.cache_current) {
-    const int rc = launch_seg_cur(q_cur, k_cache, v_cache, rows, k, cols, c_list, window, B, N, H, d, sm_scale, lse_ref,
+    const int rc = launch_seg_cur(q_cur, k_cache, v_cache, v16, rows, k, cols, c_list, window, B, N, H, d, sm_scale, lse_ref,
                                   o, term_prev, mass_prev, slot_prev, k_prev, term_out, mass_out, st);
     if (rc != FL_E_UNSUPPORTED) return rc;
   }
@@ -1651,9 +1654,9 @@ extern "C" int fl_loop_sparse_attn(const uint16_t* q_cur, const uint16_t* q_prev
                                    int d, float sm_scale, int flags, float* lse_ref, float* o,
                                    void* ws, size_t ws_bytes, void* stream) {
   FL_API_BEGIN
-  return loop_sparse_attn(q_cur, q_prev, k_cache, v_cache, k_new, v_new, slot, rows, k, cols, c_list, window, B,
-                          N, H, d, sm_scale, flags, lse_ref, o, nullptr, nullptr, nullptr, 0, nullptr, nullptr, ws,
-                          ws_bytes, stream);
+  return loop_sparse_attn(q_cur, q_prev, k_cache, v_cache, nullptr, k_new, v_new, slot, rows, k, cols, c_list,
+                          window, B, N, H, d, sm_scale, flags, lse_ref, o, nullptr, nullptr, nullptr, 0, nullptr,
+                          nullptr, ws, ws_bytes, stream);
   FL_API_END
 }
 
@@ -1667,9 +1670,26 @@ extern "C" int fl_loop_sparse_attn_terms(const uint16_t* q_cur, const uint16_t* 
                                          const int32_t* slot_prev, int k_prev, float* term_out,
                                          float* mass_out, void* ws, size_t ws_bytes, void* stream) {
   FL_API_BEGIN
-  return loop_sparse_attn(q_cur, q_prev, k_cache, v_cache, k_new, v_new, slot, rows, k, cols, c_list, window, B,
-                          N, H, d, sm_scale, 0, lse_ref, o, term_prev, mass_prev, slot_prev, k_prev, term_out,
-                          mass_out, ws, ws_bytes, stream);
+  return loop_sparse_attn(q_cur, q_prev, k_cache, v_cache, nullptr, k_new, v_new, slot, rows, k, cols, c_list,
+                          window, B, N, H, d, sm_scale, 0, lse_ref, o, term_prev, mass_prev, slot_prev, k_prev,
+                          term_out, mass_out, ws, ws_bytes, stream);
+  FL_API_END
+}
+
+extern "C" int fl_loop_sparse_attn_terms_v16(const uint16_t* q_cur, const uint16_t* k_cache, const uint16_t* v_cache,
+                                             const uint16_t* v_cache_f16, const int32_t* rows, int k,
+                                             const int32_t* cols, int c_list, int window, int B, int N, int H,
+                                             int d, float sm_scale, float* lse_ref, float* o,
+                                             const float* term_prev, const float* mass_prev,
+                                             const int32_t* slot_prev, int k_prev, float* term_out,
+                                             float* mass_out, void* stream) {
+  FL_API_BEGIN
+  FL_REQUIRE(v_cache_f16 != nullptr, FL_E_NULL, "fl_loop_sparse_attn_terms_v16: v_cache_f16 is required");
+  FL_REQUIRE(term_prev != nullptr, FL_E_NULL, "fl_loop_sparse_attn_terms_v16: term_prev is required");
+  // (current caches and given terms: no record workspace)
+  return loop_sparse_attn(q_cur, nullptr, k_cache, v_cache, v_cache_f16, nullptr, nullptr, nullptr, rows, k, cols,
+                          c_list, window, B, N, H, d, sm_scale, 0, lse_ref, o, term_prev, mass_prev, slot_prev,
+                          k_prev, term_out, mass_out, nullptr, 0, stream);
   FL_API_END
 }
 
@@ -1702,12 +1722,11 @@ extern "C" int fl_loop_subtract_terms_supported(int k, int c_list, int window, i
   return subtract_supported(k, c_list, window, N, d) ? 1 : 0;
 }
 
-extern "C" int fl_loop_subtract_terms(const uint16_t* q_prev, const uint16_t* k_cache, const uint16_t* v_cache,
-                                      const int32_t* rows, int k, const int32_t* cols, int c_list, int window,
-                                      int B, int N, int H, int d, float sm_scale, const float* lse_ref,
-                                      float* term_out, float* mass_out, void* stream) {
-  FL_API_BEGIN
-  const char* fn = "fl_loop_subtract_terms";
+// The subtract pass (fl_loop_subtract_terms, and with v16 an fp16 copy of v_cache for the segment kernels).
+static int subtract_terms(const char* fn, const uint16_t* q_prev, const uint16_t* k_cache, const uint16_t* v_cache,
+                          const uint16_t* v16, const int32_t* rows, int k, const int32_t* cols, int c_list,
+                          int window, int B, int N, int H, int d, float sm_scale, const float* lse_ref,
+                          float* term_out, float* mass_out, void* stream) {
   FL_REQUIRE(q_prev && k_cache && v_cache && lse_ref, FL_E_NULL, "%s: q_prev, k_cache, v_cache and lse_ref are required",
              fn);
   FL_REQUIRE(k == 0 || (rows && term_out && mass_out), FL_E_NULL, "%s: rows, term_out and mass_out are required", fn);
@@ -1729,7 +1748,7 @@ extern "C" int fl_loop_subtract_terms(const uint16_t* q_prev, const uint16_t* k_
     // (the segment kernel's products with V run in fp16)
     const int rc = check_f16_range(fn, "v_cache", v_cache, (int64_t)B * N * H * d, st);
     if (rc != FL_OK) return rc;
-    return launch_seg_sub(q_prev, k_cache, v_cache, rows, k, cols, c_list, window, B, N, H, d, sm_scale, lse_ref,
+    return launch_seg_sub(q_prev, k_cache, v_cache, v16, rows, k, cols, c_list, window, B, N, H, d, sm_scale, lse_ref,
                           term_out, mass_out, st);
   }
   AttnArgs a{};
@@ -1754,5 +1773,26 @@ extern "C" int fl_loop_subtract_terms(const uint16_t* q_prev, const uint16_t* k_
   if (d == 128) cur_sub_kernel<128><<<grid, 256, 0, st>>>(a);
   else cur_sub_kernel<64><<<grid, 256, 0, st>>>(a);
   return check_launch("cur_sub_kernel");
+}
+
+extern "C" int fl_loop_subtract_terms(const uint16_t* q_prev, const uint16_t* k_cache, const uint16_t* v_cache,
+                                      const int32_t* rows, int k, const int32_t* cols, int c_list, int window,
+                                      int B, int N, int H, int d, float sm_scale, const float* lse_ref,
+                                      float* term_out, float* mass_out, void* stream) {
+  FL_API_BEGIN
+  return subtract_terms("fl_loop_subtract_terms", q_prev, k_cache, v_cache, nullptr, rows, k, cols, c_list, window,
+                        B, N, H, d, sm_scale, lse_ref, term_out, mass_out, stream);
+  FL_API_END
+}
+
+extern "C" int fl_loop_subtract_terms_v16(const uint16_t* q_prev, const uint16_t* k_cache, const uint16_t* v_cache,
+                                          const uint16_t* v_cache_f16, const int32_t* rows, int k,
+                                          const int32_t* cols, int c_list, int window, int B, int N, int H, int d,
+                                          float sm_scale, const float* lse_ref, float* term_out, float* mass_out,
+                                          void* stream) {
+  FL_API_BEGIN
+  FL_REQUIRE(v_cache_f16 != nullptr, FL_E_NULL, "fl_loop_subtract_terms_v16: v_cache_f16 is required");
+  return subtract_terms("fl_loop_subtract_terms_v16", q_prev, k_cache, v_cache, v_cache_f16, rows, k, cols, c_list,
+                        window, B, N, H, d, sm_scale, lse_ref, term_out, mass_out, stream);
   FL_API_END
 }

@@ -107,13 +107,15 @@ int seg_teams(int k, int c_list, int window, int N, int d, int bh);
 
 // Segment kernel of the subtract pass over the previous loop's state; FL_E_UNSUPPORTED without a launch
 // outside seg_supported.
-int launch_seg_sub(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, const int32_t* rows, int k,
+int launch_seg_sub(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, const uint16_t* v16,
+                   const int32_t* rows, int k,
                    const int32_t* cols, int c_list, int window, int B, int N, int H, int d, float sm_scale,
                    const float* lse_ref, float* term_out, float* mass_out, hipStream_t st);
 
 // Segment kernel of the add pass over current caches (fl_seg_attn.hip); FL_E_UNSUPPORTED without a launch
 // when the shape is outside what it covers.
-int launch_seg_cur(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, const int32_t* rows, int k,
+int launch_seg_cur(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, const uint16_t* v16,
+                   const int32_t* rows, int k,
                    const int32_t* cols, int c_list, int window, int B, int N, int H, int d, float sm_scale,
                    float* lse_ref, float* o, const float* term_prev, const float* mass_prev,
                    const int32_t* slot_prev, int k_prev, float* term_out, float* mass_out, hipStream_t st);

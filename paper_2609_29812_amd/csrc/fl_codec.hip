@@ -37,6 +37,33 @@ __device__ __forceinline__ void store_bf16x8(uint16_t* p, const Row8& r) {
   *reinterpret_cast<uint4*>(p) = make_uint4(ws[0], ws[1], ws[2], ws[3]);
 }
 
+// Two fp32 values to packed fp16 (round to nearest even; v_cvt_pk_f16_f32, the conversion the attention
+// kernels apply to bf16 value rows in LDS).
+__device__ __forceinline__ uint32_t f16x2_bits(float a, float b) {
+  typedef float f2 __attribute__((ext_vector_type(2)));
+  typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f2){a, b}, h2));
+}
+
+// Eight bf16 values (as packed bits) to fp16.
+__device__ __forceinline__ uint4 bf16x8_to_f16(uint4 w) {
+  const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+  uint32_t o[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) o[t] = f16x2_bits(__uint_as_float(ws[t] << 16), __uint_as_float(ws[t] & 0xFFFF0000u));
+  return make_uint4(o[0], o[1], o[2], o[3]);
+}
+
+// The fp16 copy of a row chunk as store_bf16x8 writes it: each value rounded to bf16 first, then to fp16.
+__device__ __forceinline__ void store_f16x8_of_bf16(uint16_t* p, const Row8& r) {
+  uint32_t o[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+    o[t] = f16x2_bits(__uint_as_float(f32_to_bf16_rne(r.v[2 * t]) << 16),
+                      __uint_as_float(f32_to_bf16_rne(r.v[2 * t + 1]) << 16));
+  *reinterpret_cast<uint4*>(p) = make_uint4(o[0], o[1], o[2], o[3]);
+}
+
 // Reciprocal of a metadata scale for encode1 (within 1 ulp; s is an fp16 value, so 1/s is a normal fp32).
 __device__ __forceinline__ float scale_rcp(float s) { return __builtin_amdgcn_rcpf(s); }
 
@@ -223,7 +250,7 @@ __device__ __forceinline__ void quant_channel_body(
     const uint16_t* __restrict__ x_cur, const uint16_t* x_ref,
     const int32_t* __restrict__ idx, int k, int N, int HD, int G, uint8_t* __restrict__ codes,
     uint16_t* __restrict__ scale, uint16_t* __restrict__ zero, uint16_t* out_rows, bool commit,
-    int64_t local, int b) {
+    int64_t local, int b, uint16_t* out_f16 = nullptr) {
   constexpr int qmax = (1 << BITS) - 1;
   const int chunks = HD / 8;
   const bool ok = local < (int64_t)k * chunks;
@@ -278,6 +305,7 @@ __device__ __forceinline__ void quant_channel_body(
       o.v[t] = ref + (z32 + (float)q[t] * s32);
     }
     store_bf16x8(out_rows + (commit ? roff : ((int64_t)b * k + p) * HD + c0), o);
+    if (out_f16) store_f16x8_of_bf16(out_f16 + roff, o);   // (commit only: the cache row's fp16 copy)
   }
 }
 
@@ -307,6 +335,7 @@ struct QuantKV {
   uint16_t* v_zero;
   uint16_t* k_rows;
   uint16_t* v_rows;
+  uint16_t* v_f16;     // optional (commit): fp16 copy of the value cache, rows idx rewritten
   int k, N, HD, G;
   int kx, ky, vx;      // key workgroups per (row group, batch) and row groups; value workgroups per batch
   int commit;
@@ -323,7 +352,7 @@ __global__ __launch_bounds__(256) void quant_kv_kernel(QuantKV a) {
                                    a.k_zero, a.k_rows, a.commit != 0, r % a.kx, r / a.kx, b);
   } else {
     quant_channel_body<BITS>(a.v_cur, a.v_ref, a.idx, a.k, a.N, a.HD, a.G, a.v_codes, a.v_scale, a.v_zero,
-                             a.v_rows, a.commit != 0, (int64_t)(r - nkb) * 256 + threadIdx.x, b);
+                             a.v_rows, a.commit != 0, (int64_t)(r - nkb) * 256 + threadIdx.x, b, a.v_f16);
   }
 }
 
@@ -493,10 +522,32 @@ static int residual_quant(const char* fn, const uint16_t* x_cur, const uint16_t*
 
 // Keys (token axis) and values (channel axis) with one bit width and group size.  out rows: compact
 // k_rows / v_rows (each optional), or with commit the rows idx of k_ref / v_ref in place.
+// ---- fp16 copy of rows of a bf16 [B, N, HD] tensor (all rows, or rows idx) ------------------------------
+__global__ __launch_bounds__(256) void f16_rows_kernel(const uint16_t* __restrict__ x, const int32_t* __restrict__ idx,
+                                                       int k, int N, int HD, uint16_t* __restrict__ y) {
+  const int b = blockIdx.y;
+  const int chunks = HD / 8;
+  const int64_t local = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (local >= (int64_t)k * chunks) return;
+  const int p = (int)(local / chunks), c = (int)(local % chunks);
+  const int64_t i = idx ? (int64_t)idx[(int64_t)b * k + p] : (int64_t)p;
+  const int64_t off = ((int64_t)b * N + i) * HD + (int64_t)c * 8;
+  *reinterpret_cast<uint4*>(y + off) = bf16x8_to_f16(*reinterpret_cast<const uint4*>(x + off));
+}
+
+static int launch_f16_rows(const uint16_t* x, const int32_t* idx, int k, int B, int N, int HD, uint16_t* y,
+                           hipStream_t st) {
+  if (k == 0) return FL_OK;
+  dim3 grid((unsigned)(((int64_t)k * (HD / 8) + 255) / 256), B);
+  f16_rows_kernel<<<grid, 256, 0, st>>>(x, idx, k, N, HD, y);
+  return check_launch("f16_rows_kernel");
+}
+
 static int residual_quant_kv(const char* fn, const uint16_t* k_cur, uint16_t* k_ref, const uint16_t* v_cur,
                              uint16_t* v_ref, const int32_t* idx, int k, int B, int N, int H, int d, int bits,
                              int group, uint8_t* k_codes, uint16_t* k_scale, uint16_t* k_zero, uint8_t* v_codes,
                              uint16_t* v_scale, uint16_t* v_zero, uint16_t* k_rows, uint16_t* v_rows, bool commit,
+                             uint16_t* v_f16,
                              void* stream) {
   int rc = check_codec_args(fn, k_codes, k_cur, k, B, N, H, d, bits, group, FL_AXIS_TOKEN, true, k_scale,
                             k_zero, idx);
@@ -509,8 +560,10 @@ static int residual_quant_kv(const char* fn, const uint16_t* k_cur, uint16_t* k_
     rc = residual_quant(fn, k_cur, k_ref, idx, k, B, N, H, d, bits, group, FL_AXIS_TOKEN, k_codes, k_scale,
                         k_zero, commit ? k_ref : k_rows, commit, stream);
     if (rc != FL_OK) return rc;
-    return residual_quant(fn, v_cur, v_ref, idx, k, B, N, H, d, bits, group, FL_AXIS_CHANNEL, v_codes, v_scale,
-                          v_zero, commit ? v_ref : v_rows, commit, stream);
+    rc = residual_quant(fn, v_cur, v_ref, idx, k, B, N, H, d, bits, group, FL_AXIS_CHANNEL, v_codes, v_scale,
+                        v_zero, commit ? v_ref : v_rows, commit, stream);
+    if (rc != FL_OK || !v_f16) return rc;
+    return launch_f16_rows(v_ref, idx, k, B, N, H * d, v_f16, as_stream(stream));
   }
   const int HD = H * d;
   const int slices = group < 32 ? group : 32;
@@ -521,6 +574,7 @@ static int residual_quant_kv(const char* fn, const uint16_t* k_cur, uint16_t* k_
   a.v_codes = v_codes; a.v_scale = v_scale; a.v_zero = v_zero;
   a.k_rows = commit ? k_ref : k_rows;
   a.v_rows = commit ? v_ref : v_rows;
+  a.v_f16 = commit ? v_f16 : nullptr;
   a.k = k; a.N = N; a.HD = HD; a.G = group;
   a.kx = (HD + cw - 1) / cw;
   a.ky = (k + group - 1) / group;
@@ -609,7 +663,40 @@ extern "C" int fl_kv_residual_quant_kv(const uint16_t* k_cur, uint16_t* k_ref, c
   }
   FL_REQUIRE(k == 0 || k_codes != v_codes, FL_E_SHAPE, "%s: key and value codes must be distinct buffers", fn);
   return residual_quant_kv(fn, k_cur, k_ref, v_cur, v_ref, idx, k, B, N, H, d, bits, group, k_codes, k_scale,
-                           k_zero, v_codes, v_scale, v_zero, k_rows, v_rows, mode == FL_DQ_COMMIT, stream);
+                           k_zero, v_codes, v_scale, v_zero, k_rows, v_rows, mode == FL_DQ_COMMIT, nullptr, stream);
+  FL_API_END
+}
+
+extern "C" int fl_kv_residual_quant_kv_v16(const uint16_t* k_cur, uint16_t* k_ref, const uint16_t* v_cur,
+                                           uint16_t* v_ref, uint16_t* v_f16, const int32_t* idx, int k, int B, int N,
+                                           int H, int d, int bits, int group, uint8_t* k_codes, uint16_t* k_scale,
+                                           uint16_t* k_zero, uint8_t* v_codes, uint16_t* v_scale, uint16_t* v_zero,
+                                           void* stream) {
+  FL_API_BEGIN
+  const char* fn = "fl_kv_residual_quant_kv_v16";
+  FL_REQUIRE(k_ref && v_ref && v_f16, FL_E_NULL, "%s: k_ref, v_ref and v_f16 are required", fn);
+  FL_REQUIRE(k_ref != v_ref && (const void*)v_f16 != (const void*)v_ref && (const void*)v_f16 != (const void*)k_ref,
+             FL_E_SHAPE, "%s: the key cache, the value cache and its fp16 copy must be distinct", fn);
+  FL_REQUIRE(k == 0 || k_codes != v_codes, FL_E_SHAPE, "%s: key and value codes must be distinct buffers", fn);
+  return residual_quant_kv(fn, k_cur, k_ref, v_cur, v_ref, idx, k, B, N, H, d, bits, group, k_codes, k_scale,
+                           k_zero, v_codes, v_scale, v_zero, nullptr, nullptr, true, v_f16, stream);
+  FL_API_END
+}
+
+extern "C" int fl_kv_f16_rows(const uint16_t* x, const int32_t* idx, int k, int B, int N, int H, int d,
+                              uint16_t* x_f16, void* stream) {
+  FL_API_BEGIN
+  const char* fn = "fl_kv_f16_rows";
+  FL_REQUIRE(x && x_f16, FL_E_NULL, "%s: x and x_f16 are required", fn);
+  FL_REQUIRE((const void*)x != (const void*)x_f16, FL_E_SHAPE, "%s: x_f16 may not alias x", fn);
+  FL_REQUIRE(B >= 1 && N >= 1 && H >= 1 && d >= 8 && d % 8 == 0, FL_E_SHAPE,
+             "%s: need B, N, H >= 1 and d a multiple of 8", fn);
+  FL_REQUIRE(k >= 0 && k <= N, FL_E_RANGE, "%s: k=%d outside [0, N]", fn, k);
+  if (k == 0) return FL_OK;               // (an empty index list may come as NULL)
+  FL_REQUIRE(idx || k == N, FL_E_RANGE, "%s: k=%d with idx NULL (every row: k = N)", fn, k);
+  const hipStream_t st = as_stream(stream);
+  if (idx) FL_CHECK_LIST(fn, "idx", idx, B, k, 0, N, st);
+  return launch_f16_rows(x, idx, k, B, N, H * d, x_f16, st);
   FL_API_END
 }
 

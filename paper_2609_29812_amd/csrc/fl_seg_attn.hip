@@ -53,6 +53,7 @@ struct SegArgs {
   const uint16_t* q;          // [B, N, H, d] queries of this loop
   const uint16_t* k_cache;    // [B, N, H, d] this loop's K_hat, V_hat
   const uint16_t* v_cache;
+  const uint16_t* v16;        // optional fp16 copy of v_cache (same layout): the tiles' values need no conversion
   const int32_t* rows;        // [B, k] ascending updated rows
   const int32_t* cols;        // [B, H, c_list] ascending column list
   float* lse_ref;             // [B, N, H]
@@ -68,7 +69,7 @@ struct SegArgs {
   float pinf;                 // +inf (a kernel argument, so the median below is not folded into a max)
 };
 
-template <int D, bool SUB, int TEAMS>
+template <int D, bool SUB, int TEAMS, bool V16>
 __device__ __forceinline__ void seg_body(const SegArgs& a) {
   static_assert(TEAMS == 1 || TEAMS == 2, "one or two teams of four waves");
   constexpr int NT = 256 * TEAMS;         // threads
@@ -228,7 +229,7 @@ __device__ __forceinline__ void seg_body(const SegArgs& a) {
   const uint32_t rb = (uint32_t)(HD * 2);
   const uint32_t head_off = (uint32_t)(h * D * 2);
   const rsrc_t kcR = make_rsrc(a.k_cache + (int64_t)b * a.N * HD, (uint32_t)a.N * rb);
-  const rsrc_t vcR = make_rsrc(a.v_cache + (int64_t)b * a.N * HD, (uint32_t)a.N * rb);
+  const rsrc_t vcR = make_rsrc((V16 ? a.v16 : a.v_cache) + (int64_t)b * a.N * HD, (uint32_t)a.N * rb);
   int lcol[NIK];
   uint32_t lsw[NIK];
 #pragma unroll
@@ -431,8 +432,10 @@ __device__ __forceinline__ void seg_body(const SegArgs& a) {
   // the descriptor of the tile the step DMAs, also read a step ahead, so the offsets at the top of a step
   // wait on the list reads alone (1-2 % on both 32K passes)
   int2 dsc_dma = tdesc[u + 3 * TEAMS < n_tiles ? u + 3 * TEAMS : 0];
-  FL_WAIT_VM(2 * NI);                     // step 0 has landed
-  convert(ring0[0]);
+  if constexpr (!V16) {                   // (an fp16 copy of the values lands ready)
+    FL_WAIT_VM(2 * NI);                   // step 0 has landed
+    convert(ring0[0]);
+  }
   auto step = [&](Slot<D>& cur, Slot<D>& nxt, Slot<D>& nx1) __attribute__((always_inline)) {   // (the slots' first tiles; the team's is at tofs)
     const Offs of = tile_offs_d(u + 3 * TEAMS, dsc_dma);
     dsc_dma = tdesc[u + 4 * TEAMS < n_tiles ? u + 4 * TEAMS : 0];
@@ -443,8 +446,10 @@ __device__ __forceinline__ void seg_body(const SegArgs& a) {
     lds_barrier();
     if (have) compute(dx, dy, cur);
     issue(nxt, of);                       // (after the math: the step's critical path starts at the barrier)
-    FL_WAIT_VM(2 * NI);                   // step s+1 has landed (s+2 and s+3 may be in flight)
-    convert(nx1);                         // its value rows to fp16, in the shadow of the other waves' math
+    if constexpr (!V16) {
+      FL_WAIT_VM(2 * NI);                 // step s+1 has landed (s+2 and s+3 may be in flight)
+      convert(nx1);                       // its value rows to fp16, in the shadow of the other waves' math
+    }
     u += TEAMS;
   };
   for (int s = 0; s < n_loop; s += kSegSteps) {
@@ -552,23 +557,36 @@ __device__ __forceinline__ void seg_body(const SegArgs& a) {
   }
 }
 
-template <int D>
+// V16: the values come from the fp16 copy (a.v16) instead of being converted in LDS.
+template <int D, bool V16>
 __global__ __launch_bounds__(512, 2) void seg_cur_kernel(SegArgs a) {
-  seg_body<D, false, 2>(a);
+  seg_body<D, false, 2, V16>(a);
 }
-template <int D>
+template <int D, bool V16>
 __global__ __launch_bounds__(512, 2) void seg_sub_kernel(SegArgs a) {
-  seg_body<D, true, 2>(a);
+  seg_body<D, true, 2, V16>(a);
 }
 // One team of four waves (no band): two workgroups per CU instead of one lockstep workgroup of eight waves.
-template <int D>
+template <int D, bool V16>
 __global__ __launch_bounds__(256, 2) void seg1_cur_kernel(SegArgs a) {
-  seg_body<D, false, 1>(a);
+  seg_body<D, false, 1, V16>(a);
 }
-template <int D>
+template <int D, bool V16>
 __global__ __launch_bounds__(256, 2) void seg1_sub_kernel(SegArgs a) {
-  seg_body<D, true, 1>(a);
+  seg_body<D, true, 1, V16>(a);
 }
+
+// The launch of one of the four kernels for head dim d and an optional fp16 value copy.
+#define FL_SEG_LAUNCH(KERNEL, THREADS)                                                      \
+  do {                                                                                        \
+    if (d == 128) {                                                                           \
+      if (a.v16) KERNEL<128, true><<<grid, THREADS, 0, st>>>(a);                              \
+      else KERNEL<128, false><<<grid, THREADS, 0, st>>>(a);                                   \
+    } else {                                                                                  \
+      if (a.v16) KERNEL<64, true><<<grid, THREADS, 0, st>>>(a);                               \
+      else KERNEL<64, false><<<grid, THREADS, 0, st>>>(a);                                    \
+    }                                                                                         \
+  } while (0)
 
 // Whether the segment kernels cover a shape: a list that fits in LDS and, with a band, the descriptor table
 // (without one, the table holds at most ceil(c_list / 32) + 1 positions, within either kernel's).
@@ -610,13 +628,14 @@ static void seg_grid(SegArgs& a, int k, int bh, int per_cu) {
 // Subtract pass over the previous loop's state (queries q of loop r-1, caches X_hat^(r-1), lse_ref of loop
 // r-1): per updated row the term sum_j exp(sigma q . k_j - lse_ref) v_j and its mass, written at the row's
 // position in rows.  FL_E_UNSUPPORTED (nothing launched) outside seg_supported.
-int launch_seg_sub(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, const int32_t* rows, int k,
+int launch_seg_sub(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, const uint16_t* v16,
+                   const int32_t* rows, int k,
                    const int32_t* cols, int c_list, int window, int B, int N, int H, int d, float sm_scale,
                    const float* lse_ref, float* term_out, float* mass_out, hipStream_t st) {
   const int teams = seg_teams(k, c_list, window, N, d, B * H);
   if (teams == 0) return FL_E_UNSUPPORTED;
   SegArgs a{};
-  a.q = q; a.k_cache = k_cache; a.v_cache = v_cache; a.rows = rows; a.cols = cols;
+  a.q = q; a.k_cache = k_cache; a.v_cache = v_cache; a.v16 = v16; a.rows = rows; a.cols = cols;
   a.lse_ref = const_cast<float*>(lse_ref);   // (read only in this pass)
   a.term_out = term_out; a.mass_out = mass_out;
   a.k = k; a.c_list = c_list; a.window = window; a.B = B; a.N = N; a.H = H;
@@ -626,25 +645,24 @@ int launch_seg_sub(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v
   a.pinf = INFINITY;
   dim3 grid((unsigned)(a.n_seg * B * H));
   if (one) {
-    if (d == 128) seg1_sub_kernel<128><<<grid, 256, 0, st>>>(a);
-    else seg1_sub_kernel<64><<<grid, 256, 0, st>>>(a);
+    FL_SEG_LAUNCH(seg1_sub_kernel, 256);
     return check_launch("seg1_sub_kernel");
   }
-  if (d == 128) seg_sub_kernel<128><<<grid, 512, 0, st>>>(a);
-  else seg_sub_kernel<64><<<grid, 512, 0, st>>>(a);
+  FL_SEG_LAUNCH(seg_sub_kernel, 512);
   return check_launch("seg_sub_kernel");
 }
 
 // Launch of the segment kernel for a reuse loop over current caches; returns FL_E_UNSUPPORTED (nothing
 // launched) when the shape is outside what it covers, so the caller can take another kernel.
-int launch_seg_cur(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, const int32_t* rows, int k,
+int launch_seg_cur(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, const uint16_t* v16,
+                   const int32_t* rows, int k,
                    const int32_t* cols, int c_list, int window, int B, int N, int H, int d, float sm_scale,
                    float* lse_ref, float* o, const float* term_prev, const float* mass_prev,
                    const int32_t* slot_prev, int k_prev, float* term_out, float* mass_out, hipStream_t st) {
   const int teams = seg_teams(k, c_list, window, N, d, B * H);
   if (teams == 0) return FL_E_UNSUPPORTED;
   SegArgs a{};
-  a.q = q; a.k_cache = k_cache; a.v_cache = v_cache; a.rows = rows; a.cols = cols;
+  a.q = q; a.k_cache = k_cache; a.v_cache = v_cache; a.v16 = v16; a.rows = rows; a.cols = cols;
   a.lse_ref = lse_ref; a.o = o; a.term_prev = term_prev; a.mass_prev = mass_prev; a.slot_prev = slot_prev;
   a.term_out = term_out; a.mass_out = mass_out;
   a.k = k; a.k_prev = k_prev; a.c_list = c_list; a.window = window; a.B = B; a.N = N; a.H = H;
@@ -654,12 +672,10 @@ int launch_seg_cur(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v
   a.pinf = INFINITY;
   dim3 grid((unsigned)(a.n_seg * B * H));
   if (one) {
-    if (d == 128) seg1_cur_kernel<128><<<grid, 256, 0, st>>>(a);
-    else seg1_cur_kernel<64><<<grid, 256, 0, st>>>(a);
+    FL_SEG_LAUNCH(seg1_cur_kernel, 256);
     return check_launch("seg1_cur_kernel");
   }
-  if (d == 128) seg_cur_kernel<128><<<grid, 512, 0, st>>>(a);
-  else seg_cur_kernel<64><<<grid, 512, 0, st>>>(a);
+  FL_SEG_LAUNCH(seg_cur_kernel, 512);
   return check_launch("seg_cur_kernel");
 }
 

@@ -14,6 +14,9 @@ sparse_step() one sparse loop r >= 2: select the active rows among the previous 
               computes its subtract terms first, over the loop r-1 state, where the segment kernel covers
               the shape, and then runs as such a loop; otherwise it runs both passes in one kernel and
               commits after it.
+The layer also keeps an fp16 copy of the value cache (v16): the quantizers write it with the committed rows,
+and the attention's segment kernels load value tiles from it instead of converting bf16 tiles in LDS
+(bitwise the same results).
 prune_list()  a smaller column budget for the next loop (Section 4.2): keep the sinks and the entries the
               last loop's updated rows gave the most probability mass.  The next loop then runs both passes
               (its subtract pass recomputes the kept columns' share with the same lse_ref).
@@ -43,9 +46,10 @@ class LayerState:
     mass: torch.Tensor | None = None    # fp32 [B, k, H]
     slot_prev: torch.Tensor | None = None   # int32 [B, N] slot map of the last loop
     tail: int = 0                       # the most recent positions stored exactly in bf16 (Appendix E)
+    v16: torch.Tensor | None = None     # fp16 [B, N, H, d] copy of v_hat (kept current with it), or None
 
 
-def setup(q1, k1, v1, base_bits, group, n_sink, t, window, tail=0):
+def setup(q1, k1, v1, base_bits, group, n_sink, t, window, tail=0, v16=True):
     B, N, H, d = k1.shape
     k_hat = torch.empty_like(k1)
     v_hat = torch.empty_like(v1)
@@ -59,6 +63,7 @@ def setup(q1, k1, v1, base_bits, group, n_sink, t, window, tail=0):
     cols = fl.select_columns(col_key, n_sink, t)
     st = LayerState(k_hat, v_hat, o, lse, cols, None, window, group)
     st.tail = tail
+    st.v16 = fl.kv_f16_rows(v_hat) if v16 else None
     st.base = dict(codes_k=ck, scale_k=sk, zero_k=zk, codes_v=cv, scale_v=sv, zero_v=zv, col_key=col_key)
     return st
 
@@ -87,17 +92,20 @@ def sparse_step(st: LayerState, qr, qp, kr, kp, vr, vp, k_r, bits, keep=False):
         if split:
             # no stored terms: the subtract pass over the loop r-1 state first (its terms index this loop's
             # rows), so that the new rows can be committed before the add pass
-            term_prev, mass_prev = fl.subtract_terms(qp, st.k_hat, st.v_hat, idx, st.cols, st.window, st.lse)
+            term_prev, mass_prev = fl.subtract_terms(qp, st.k_hat, st.v_hat, idx, st.cols, st.window, st.lse,
+                                                     v16=st.v16)
             slot_prev = slot
-        # the add pass alone: commit the new rows first, then attend over the caches
+        # the add pass alone: commit the new rows first (and their fp16 values), then attend over the caches
         (ck, sk, zk, _), (cv, sv, zv, _) = fl.kv_residual_quant_kv(kr, st.k_hat, vr, st.v_hat, idx, bits,
-                                                                   st.group, mode=fl.DQ_COMMIT)
+                                                                   st.group, mode=fl.DQ_COMMIT, v_f16=st.v16)
         if st.tail:
             fl.kv_keep_recent(kr, idx, st.tail, cache=st.k_hat)
             fl.kv_keep_recent(vr, idx, st.tail, cache=st.v_hat)
+            if st.v16 is not None:
+                fl.kv_f16_rows(st.v_hat, idx, out=st.v16)
         fl.loop_sparse_attn(qr, None, st.k_hat, st.v_hat, None, None, slot, idx, st.cols, st.window, st.lse,
                             st.o, term_prev=term_prev, mass_prev=mass_prev, slot_prev=slot_prev, term_out=term,
-                            mass_out=mass)
+                            mass_out=mass, v16=st.v16)
     else:
         # both passes: the subtract pass needs the loop r-1 caches, so commit after the attention
         (ck, sk, zk, k_new), (cv, sv, zv, v_new) = fl.kv_residual_quant_kv(kr, st.k_hat, vr, st.v_hat, idx, bits,
@@ -112,6 +120,8 @@ def sparse_step(st: LayerState, qr, qp, kr, kp, vr, vp, k_r, bits, keep=False):
         if st.tail:
             fl.kv_keep_recent(kr, idx, st.tail, cache=st.k_hat)
             fl.kv_keep_recent(vr, idx, st.tail, cache=st.v_hat)
+        if st.v16 is not None:
+            fl.kv_f16_rows(st.v_hat, idx, out=st.v16)
     st.term, st.mass, st.slot_prev = term, mass, slot
     st.cand = idx
     if keep:   # (k_new / v_new are None when the loop committed straight into the caches)

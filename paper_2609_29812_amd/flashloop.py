@@ -46,6 +46,9 @@ _SIGNATURES = {
                                          _c_i, _c_i, _c_i, _c_p, _c_p, _c_p, _c_p, _c_p]),
     "fl_kv_residual_quant_kv": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_p, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i,
                                        _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_i, _c_p]),
+    "fl_kv_residual_quant_kv_v16": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i,
+                                           _c_i, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p]),
+    "fl_kv_f16_rows": (_c_i, [_c_p, _c_p, _c_i, _c_i, _c_i, _c_i, _c_i, _c_p, _c_p]),
     "fl_loop_sparse_attn_ws": (_c_sz, [_c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i]),
     "fl_loop_sparse_attn": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_i, _c_p, _c_i, _c_i,
                                    _c_i, _c_i, _c_i, _c_i, _c_f, _c_i, _c_p, _c_p, _c_p, _c_sz, _c_p]),
@@ -56,6 +59,11 @@ _SIGNATURES = {
     "fl_attn_kernel_name": (ctypes.c_char_p, [_c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i]),
     "fl_loop_subtract_terms": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_i, _c_p, _c_i, _c_i, _c_i, _c_i, _c_i, _c_i, _c_f,
                                       _c_p, _c_p, _c_p, _c_p]),
+    "fl_loop_sparse_attn_terms_v16": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_p, _c_i, _c_p, _c_i, _c_i, _c_i, _c_i,
+                                             _c_i, _c_i, _c_f, _c_p, _c_p, _c_p, _c_p, _c_p, _c_i, _c_p, _c_p,
+                                             _c_p]),
+    "fl_loop_subtract_terms_v16": (_c_i, [_c_p, _c_p, _c_p, _c_p, _c_p, _c_i, _c_p, _c_i, _c_i, _c_i, _c_i, _c_i,
+                                          _c_i, _c_f, _c_p, _c_p, _c_p, _c_p]),
     "fl_column_scores_ws": (_c_sz, [_c_i, _c_i, _c_i]),
     "fl_column_scores": (_c_i, [_c_p, _c_p, _c_i, _c_i, _c_i, _c_i, _c_p, _c_p, _c_sz, _c_p]),
     "fl_select_columns": (_c_i, [_c_p, _c_i, _c_i, _c_i, _c_i, _c_i, _c_p, _c_p]),
@@ -206,10 +214,12 @@ def kv_residual_quant_commit(x_cur, x_hat, idx, bits, group, axis, out=None):
     return codes, scale, zero
 
 
-def kv_residual_quant_kv(k_cur, k_ref, v_cur, v_ref, idx, bits, group, mode=DQ_COMPACT, rows=True):
+def kv_residual_quant_kv(k_cur, k_ref, v_cur, v_ref, idx, bits, group, mode=DQ_COMPACT, rows=True, v_f16=None):
     """Keys (token axis) and values (channel axis) in one call.  COMPACT: returns
     ((codes, scale, zero, rows) for keys, the same for values), rows None unless rows=True;
-    COMMIT: rows idx of k_ref / v_ref are updated in place and the rows entries are None."""
+    COMMIT: rows idx of k_ref / v_ref are updated in place and the rows entries are None; with v_f16 (fp16
+    [B, N, H, d], COMMIT only) its rows idx receive the fp16 copy of the updated values
+    (fl_kv_residual_quant_kv_v16)."""
     B, N, H, d = k_cur.shape
     _dev(k_cur, torch.bfloat16, "k_cur")
     _dev(v_cur, torch.bfloat16, "v_cur", k_cur.shape)
@@ -232,11 +242,34 @@ def kv_residual_quant_kv(k_cur, k_ref, v_cur, v_ref, idx, bits, group, mode=DQ_C
         return codes, scale, zero, out_rows
 
     ko, vo = outputs(AXIS_TOKEN), outputs(AXIS_CHANNEL)
+    if v_f16 is not None:
+        if mode != DQ_COMMIT:
+            raise FlashLoopError("kv_residual_quant_kv: v_f16 needs mode=DQ_COMMIT")
+        _dev(v_f16, torch.float16, "v_f16", k_cur.shape)
+        rc = load().fl_kv_residual_quant_kv_v16(_p(k_cur), _p(k_ref), _p(v_cur), _p(v_ref), _p(v_f16), _p(idx), k,
+                                                B, N, H, d, bits, group, _p(ko[0]), _p(ko[1]), _p(ko[2]),
+                                                _p(vo[0]), _p(vo[1]), _p(vo[2]), _stream())
+        _check(rc, "fl_kv_residual_quant_kv_v16")
+        return ko, vo
     rc = load().fl_kv_residual_quant_kv(_p(k_cur), _p(k_ref), _p(v_cur), _p(v_ref), _p(idx), k, B, N, H, d, bits,
                                         group, _p(ko[0]), _p(ko[1]), _p(ko[2]), _p(vo[0]), _p(vo[1]), _p(vo[2]),
                                         _p(ko[3]), _p(vo[3]), mode, _stream())
     _check(rc, "fl_kv_residual_quant_kv")
     return ko, vo
+
+
+def kv_f16_rows(x, idx=None, out=None):
+    """fp16 copy of rows of a bf16 [B, N, H, d] tensor (fl_kv_f16_rows): every row when idx is None, else
+    rows idx of `out` (fp16 [B, N, H, d], allocated when None); returns out."""
+    B, N, H, d = x.shape
+    _dev(x, torch.bfloat16, "x")
+    k = N if idx is None else idx.shape[1]
+    _dev(idx, torch.int32, "idx", None if idx is None else (B, k))
+    out = torch.empty(B, N, H, d, dtype=torch.float16, device=x.device) if out is None else out
+    _dev(out, torch.float16, "out", x.shape)
+    rc = load().fl_kv_f16_rows(_p(x), _p(idx), k, B, N, H, d, _p(out), _stream())
+    _check(rc, "fl_kv_f16_rows")
+    return out
 
 
 def kv_residual_dequant_kv(k_enc, v_enc, idx, bits, group, k_hat, v_hat, mode=DQ_COMPACT):
@@ -287,12 +320,13 @@ def kv_residual_dequant(codes, scale, zero, idx, bits, group, axis, x_hat, mode=
 # ---- (3) attention ----------------------------------------------------------------------------------
 def loop_sparse_attn(q_cur, q_prev, k_cache, v_cache, k_new, v_new, slot, rows, cols, window, lse_ref, o,
                      sm_scale=None, ws=None, term_prev=None, mass_prev=None, slot_prev=None, term_out=None,
-                     mass_out=None):
+                     mass_out=None, v16=None):
     """Mass-corrected update of rows `rows` (in place on lse_ref and o).
 
     term_out/mass_out (fp32 [B, k, H, d] / [B, k, H]) also keep this loop's add terms; term_prev/mass_prev with
     slot_prev (the previous loop's slot map) reuse the previous loop's add terms as the subtract terms, in
-    which case q_prev may be None, and k_new/v_new may be None when the caches already hold this loop's rows."""
+    which case q_prev may be None, and k_new/v_new may be None when the caches already hold this loop's rows.
+    v16: the fp16 copy of v_cache (given terms over current caches only; fl_loop_sparse_attn_terms_v16)."""
     B, N, H, d = q_cur.shape
     k = rows.shape[1]
     reuse = term_prev is not None
@@ -316,6 +350,16 @@ def loop_sparse_attn(q_cur, q_prev, k_cache, v_cache, k_new, v_new, slot, rows, 
     _dev(mass_out, torch.float32, "mass_out", (B, k, H))
     sm_scale = 1.0 / math.sqrt(d) if sm_scale is None else sm_scale
     lib = load()
+    if v16 is not None:
+        if not reuse or k_new is not None or v_new is not None:
+            raise FlashLoopError("loop_sparse_attn: v16 needs term_prev and current caches (k_new = v_new = None)")
+        _dev(v16, torch.float16, "v16", q_cur.shape)
+        rc = lib.fl_loop_sparse_attn_terms_v16(_p(q_cur), _p(k_cache), _p(v_cache), _p(v16), _p(rows), k, _p(cols),
+                                               c_list, window, B, N, H, d, sm_scale, _p(lse_ref), _p(o),
+                                               _p(term_prev), _p(mass_prev), _p(slot_prev), k_prev, _p(term_out),
+                                               _p(mass_out), _stream())
+        _check(rc, "fl_loop_sparse_attn_terms_v16")
+        return o, lse_ref
     need = lib.fl_loop_sparse_attn_ws(B, N, H, d, k, c_list, window, 0)
     if need and (ws is None or ws.numel() < need):
         ws = torch.empty(need, dtype=torch.uint8, device=q_cur.device)
@@ -346,9 +390,10 @@ def subtract_terms_supported(k, c_list, window, N, d):
 
 
 def subtract_terms(q_prev, k_cache, v_cache, rows, cols, window, lse_ref, term_out=None, mass_out=None,
-                   sm_scale=None):
+                   sm_scale=None, v16=None):
     """Subtract term and mass of Eq. 7 over the previous loop's state: (term fp32 [B, k, H, d], m fp32 [B, k, H])
-    in the row order of `rows` (fl_loop_subtract_terms)."""
+    in the row order of `rows` (fl_loop_subtract_terms; with v16, the fp16 copy of v_cache,
+    fl_loop_subtract_terms_v16)."""
     B, N, H, d = q_prev.shape
     k = rows.shape[1]
     for name, t in (("q_prev", q_prev), ("k_cache", k_cache), ("v_cache", v_cache)):
@@ -362,6 +407,13 @@ def subtract_terms(q_prev, k_cache, v_cache, rows, cols, window, lse_ref, term_o
     _dev(term_out, torch.float32, "term_out", (B, k, H, d))
     _dev(mass_out, torch.float32, "mass_out", (B, k, H))
     sm_scale = 1.0 / math.sqrt(d) if sm_scale is None else sm_scale
+    if v16 is not None:
+        _dev(v16, torch.float16, "v16", q_prev.shape)
+        rc = load().fl_loop_subtract_terms_v16(_p(q_prev), _p(k_cache), _p(v_cache), _p(v16), _p(rows), k, _p(cols),
+                                               c_list, window, B, N, H, d, sm_scale, _p(lse_ref), _p(term_out),
+                                               _p(mass_out), _stream())
+        _check(rc, "fl_loop_subtract_terms_v16")
+        return term_out, mass_out
     rc = load().fl_loop_subtract_terms(_p(q_prev), _p(k_cache), _p(v_cache), _p(rows), k, _p(cols), c_list, window,
                                        B, N, H, d, sm_scale, _p(lse_ref), _p(term_out), _p(mass_out), _stream())
     _check(rc, "fl_loop_subtract_terms")

@@ -80,3 +80,4 @@ def test_full_size_chain_matches_oracle(F, name, layer, heads):
                 assert_close(gl[b, rows, h], lr.lse[b, h][rows], f"loop {r} lse b={b} h={h}")
     assert np.array_equal(down_bits16(gs.k_hat), k_hat), "final K cache"
     assert np.array_equal(down_bits16(gs.v_hat), v_hat), "final V cache"
+    assert torch.equal(gs.v16.view(torch.int16), gs.v_hat.float().half().view(torch.int16)), "fp16 value copy"

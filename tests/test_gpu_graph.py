@@ -22,7 +22,7 @@ sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
 
 def _state(gs):
     return ([down(t) for t in (gs.o, gs.lse, gs.cand, gs.term, gs.mass, gs.slot_prev)]
-            + [down_bits16(t) for t in (gs.k_hat, gs.v_hat)])
+            + [down_bits16(t) for t in (gs.k_hat, gs.v_hat, gs.v16)])
 
 
 @pytest.mark.parametrize("name,over", [("C4", dict(seq=2000, heads=2, window=128, col_budget=4 + 128 + 300)),

@@ -327,6 +327,7 @@ def test_chain_matches_oracle(F, name, over):
             say(f" pruned after loop {r} to {want.shape[2]} entries")
     assert np.array_equal(down_bits16(gs.k_hat), rec.k_hat), "final K cache differs"
     assert np.array_equal(down_bits16(gs.v_hat), rec.v_hat), "final V cache differs"
+    assert torch.equal(gs.v16.view(torch.int16), gs.v_hat.float().half().view(torch.int16)), "fp16 value copy"
 
 
 @pytest.mark.parametrize("name,over", [("C4", dict(seq=1100, heads=2, window=100, col_budget=4 + 100 + 150)),
