@@ -420,6 +420,19 @@ def trace_summary(title, command, trace_dir, out_name):
     print("\n".join(lines[8:]), flush=True)
 
 
+def gpu_sleep_cycles(ms, torch):
+    """Cycles for torch.cuda._sleep (a spin kernel) to last about `ms` milliseconds, measured here."""
+    n = 1 << 20
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record()
+    torch.cuda._sleep(n)
+    b.record()
+    torch.cuda.synchronize()
+    per_ms = n / max(a.elapsed_time(b), 1e-3)
+    return int(min(max(ms * per_ms, 1e4), 1e10))
+
+
 def workload_config(w):
     return {"workload": w.name, "batch": w.batch, "seq": w.seq, "heads": w.heads, "head_dim": w.head_dim,
             "loops": w.loops, "sparse_loops": f"2-{w.loops}",
@@ -470,11 +483,16 @@ def measure(w, dev, driver, fl, torch, steps, warmup, log_calls=False):
     mode = "graph replay" if ms_graph is not None and ms_graph < ms_eager else "eager"
     ms_step = ms_graph if mode == "graph replay" else ms_eager
 
-    # per-call durations with events on the launch stream (a separate pass, same work)
+    # per-call durations with events on the launch stream (a separate pass, same work).  The GPU sleeps
+    # before each step of this pass, so that the host has queued the step's calls by the time it wakes and
+    # every event pair brackets kernels that run back to back (otherwise the GPU can idle inside an interval
+    # while Python issues the next call after a short kernel).
+    sleep_cycles = gpu_sleep_cycles(2.0, torch)
     events = {}
     reps = max(3, min(steps, 10))
     trace = None
     for _ in range(reps):
+        torch.cuda._sleep(sleep_cycles)
         trace = step.run(events)
     torch.cuda.synchronize()
     dur_us = {name: float(np.mean([a.elapsed_time(b) for a, b in pairs])) * 1e3 for name, pairs in events.items()}
