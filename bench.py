@@ -710,7 +710,8 @@ def kv_footprint(w):
     """Bytes of one layer's K and V state after the workload's last loop, stored three ways (Section 4.3, Eq. 4;
     Appendix E): a bf16 cache per loop (a looped model without the method); the packed streams the paper's
     engine keeps (int4 base codes and fp16 metadata, then each sparse loop's residual codes and metadata);
-    and the one in-place bf16 cache pair this implementation keeps."""
+    and the one in-place bf16 cache pair this implementation keeps, with the fp16 copy of the value cache
+    the attention reads."""
     B, N, H, d, G = w.batch, w.seq, w.heads, w.head_dim, w.group
     el = B * N * H * d
     per_loop_bf16 = w.loops * 2 * el * 2
@@ -722,7 +723,7 @@ def kv_footprint(w):
         res += 2 * B * k * H * d * w.bits_at(r) // 8
         res_meta += B * -(-k // G) * H * d * 4 + B * k * H * (d // G) * 4
     packed = base + base_meta + res + res_meta
-    working = 2 * el * 2
+    working = 2 * el * 2 + el * 2          # bf16 K and V caches, fp16 copy of the values
     mb = lambda x: round(x / 1e6, 1)
     return {"workload": w.name, "bf16_cache_per_loop_MB": mb(per_loop_bf16),
             "packed_MB": mb(packed), "packed_bytes": packed, "packed_parts_MB": {"base_codes": mb(base), "base_metadata": mb(base_meta),
