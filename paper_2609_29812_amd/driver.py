@@ -70,9 +70,13 @@ def setup(q1, k1, v1, base_bits, group, n_sink, t, window, tail=0, v16=True):
 
 def subtract_pass_first(k, c_list, window, B, N, H, d):
     """Whether a loop without stored terms runs as the subtract pass, the commit and the add pass (rather
-    than the two-pass kernel): with a band, where the segment kernels take both passes.  Without a band the
-    two-pass kernel, which reads each list tile once for both passes, measured faster on every workload."""
-    return window > 0 and fl.attn_kernel_name(fl.PASS_SUBTRACT, k, c_list, window, B, N, H, d) == "seg_sub_kernel"
+    than the two-pass kernel): where a segment kernel (one team or two) takes the subtract pass.  Each
+    segment pass streams the list tiles once more than the two-pass kernel does, but loads the value tiles
+    from the fp16 copy and keeps its rows on the chip; with the copy the three calls measured 15-25% faster
+    than quantize, two-pass kernel, commit and copy refresh, with a band and without one.  Shapes that only
+    the 64-row kernels cover keep the two-pass kernel."""
+    return fl.attn_kernel_name(fl.PASS_SUBTRACT, k, c_list, window, B, N, H, d) in ("seg_sub_kernel",
+                                                                                    "seg1_sub_kernel")
 
 
 def sparse_step(st: LayerState, qr, qp, kr, kp, vr, vp, k_r, bits, keep=False):
