@@ -131,6 +131,12 @@ __device__ __forceinline__ void seg_body(const SegArgs& a) {
       qf[ks] = __builtin_bit_cast(bf16x8, w);
     }
   }
+  // add pass: the row's slot in the previous loop's terms, looked up with the queries (the epilogue's other
+  // loads depend on it)
+  int pp = -1;
+  if constexpr (!SUB) {
+    if (row_ok && team == 0) pp = a.slot_prev[(int64_t)b * a.N + row_i];
+  }
 
   // ---- the list in LDS; nA = entries j with j + window <= max_row (the ones a row here can see) -------
   const int32_t* cp = a.cols + (int64_t)bh * a.c_list;
@@ -499,61 +505,92 @@ __device__ __forceinline__ void seg_body(const SegArgs& a) {
       }
     lsum = lsum * fs + l_o * fo;
     run_max = mm;
+    // (the combine stays here: sunk into the epilogue, team 1's partial would be live beside the
+    // epilogue's loads)
+#pragma unroll
+    for (int db = 0; db < DB; ++db) asm volatile("" : "+v"(acc[db]));
   }
-  // ---- epilogue: lane (r32, hw) holds dims 32 db + 8 j + 4 hw .. +3 of row r32 of the group -------------
-  if (!row_ok) return;
+  // ---- epilogue ----------------------------------------------------------------------------------------
+  // The wave's 32 x D results (lane (r32, hw) holds dims 32 db + 8 j + 4 hw .. +3 of row r32) go through LDS
+  // and back, so that every global access covers whole rows: 256 / D rows per instruction, each lane 16
+  // contiguous bytes (in the MFMA layout an instruction touches 32 rows, 32 bytes of each).  The wave's
+  // LDS block is its own: ring slot grp of the last team (two teams: the slot team 1's partial came
+  // through, already read; one team: the ring is idle after the last barrier).  Chunk c (16 bytes) of row
+  // rr sits at chunk position c ^ (rr & 7) of the row.
+  constexpr int CPR = D / 4;              // 16-byte chunks per row
+  constexpr int NR = 64 / CPR;            // rows per instruction
+  constexpr int NIE = 32 / NR;            // instructions per 32 rows
+  float* es = reinterpret_cast<float*>(grp == 0 ? ring0[TEAMS - 1].k : grp == 1 ? ring1[TEAMS - 1].k
+                                       : grp == 2 ? ring2[TEAMS - 1].k : ring3[TEAMS - 1].k);
+  auto es_at = [&](int rr, int c) __attribute__((always_inline)) { return es + (rr * CPR + (c ^ (rr & 7))) * 4; };
+  const int rsub = lane / CPR, cc = lane % CPR;   // this lane's row (within an instruction's rows) and chunk
+  const int g0 = P0 + 32 * grp;           // position in rows of the group's first row
+  const int nrow = min(32, P1 - g0);      // rows of the group (<= 0: none)
   if constexpr (SUB) {                    // the subtract term and the mass, at the row's position in rows
-    const int64_t srow = ((int64_t)b * a.k + pos) * a.H + h;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        *reinterpret_cast<float4*>(a.term_out + srow * D + db * 32 + 8 * j + 4 * hw) =
-            make_float4(acc[db][4 * j], acc[db][4 * j + 1], acc[db][4 * j + 2], acc[db][4 * j + 3]);
-    if (hw == 0) a.mass_out[srow] = lsum;
-    return;
-  }
-  const int p = pos;
-  const int ri = row_i;
-  const int64_t orow = ((int64_t)b * a.N + ri) * HD + (int64_t)h * D;
-  const int64_t lrow = ((int64_t)b * a.N + ri) * a.H + h;
-  const int pp = a.slot_prev[(int64_t)b * a.N + ri];
-  const int64_t tp = ((int64_t)b * a.k_prev + pp) * a.H + h;
-  const float msub = pp >= 0 ? a.mass_prev[tp] : 0.0f;
-  const float* subp = a.term_prev + tp * D;
-  const int64_t trow = ((int64_t)b * a.k + p) * a.H + h;
-  const bool keep_terms = a.term_out != nullptr;
-  if (!(msub > 0.0f) || !(lsum > 0.0f)) { // empty column set or vanished mass: unchanged
-    if (keep_terms) {
+        *reinterpret_cast<f32x4*>(es_at(r32, 8 * db + 2 * j + hw)) =
+            f32x4{acc[db][4 * j], acc[db][4 * j + 1], acc[db][4 * j + 2], acc[db][4 * j + 3]};
 #pragma unroll
-      for (int db = 0; db < DB; ++db)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          *reinterpret_cast<float4*>(a.term_out + trow * D + db * 32 + 8 * j + 4 * hw) = make_float4(0, 0, 0, 0);
-      if (hw == 0) a.mass_out[trow] = 0.0f;
+    for (int i = 0; i < NIE; ++i) {
+      const int rr = NR * i + rsub;
+      const f32x4 t = *reinterpret_cast<const f32x4*>(es_at(rr, cc));
+      if (rr < nrow)
+        *reinterpret_cast<f32x4*>(a.term_out + (((int64_t)b * a.k + g0 + rr) * a.H + h) * D + 4 * cc) = t;
     }
+    if (row_ok && hw == 0) a.mass_out[((int64_t)b * a.k + pos) * a.H + h] = lsum;
     return;
   }
-  const float fm = msub / lsum;
+  // add pass: rows whose previous term has mass and whose new columns have some are updated; the others
+  // keep their output and get a zero term and mass
+  const int64_t tp = ((int64_t)b * a.k_prev + (pp >= 0 ? pp : 0)) * a.H + h;
+  const float msub = pp >= 0 ? a.mass_prev[tp] : 0.0f;
 #pragma unroll
   for (int db = 0; db < DB; ++db)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int dim = db * 32 + 8 * j + 4 * hw;
-      const float4 sub = *reinterpret_cast<const float4*>(subp + dim);
-      const float4 add = make_float4(acc[db][4 * j] * fm, acc[db][4 * j + 1] * fm, acc[db][4 * j + 2] * fm,
-                                     acc[db][4 * j + 3] * fm);
-      float4 prev = *reinterpret_cast<const float4*>(a.o + orow + dim);
-      prev.x = prev.x - sub.x + add.x;
-      prev.y = prev.y - sub.y + add.y;
-      prev.z = prev.z - sub.z + add.z;
-      prev.w = prev.w - sub.w + add.w;
-      *reinterpret_cast<float4*>(a.o + orow + dim) = prev;
-      if (keep_terms) *reinterpret_cast<float4*>(a.term_out + trow * D + dim) = add;
+    for (int j = 0; j < 4; ++j)
+      *reinterpret_cast<f32x4*>(es_at(r32, 8 * db + 2 * j + hw)) =
+          f32x4{acc[db][4 * j], acc[db][4 * j + 1], acc[db][4 * j + 2], acc[db][4 * j + 3]};
+  __builtin_amdgcn_sched_barrier(0);      // (the accumulators' registers are free from here)
+  // the output rows and the previous terms in the row-contiguous layout (each row's slot was looked up
+  // with the queries); every load goes out before the first use
+  f32x4 po[NIE], ps[NIE];
+#pragma unroll
+  for (int i = 0; i < NIE; ++i) {
+    const int rr = NR * i + rsub;
+    const int ri = __shfl(row_i, rr, 64), pr = __shfl(pp, rr, 64);
+    const bool ld = rr < nrow && pr >= 0;
+    const int64_t orr = ((int64_t)b * a.N + (ld ? ri : 0)) * HD + (int64_t)h * D + 4 * cc;
+    const int64_t tpr = (((int64_t)b * a.k_prev + (ld ? pr : 0)) * a.H + h) * D + 4 * cc;
+    po[i] = ld ? *reinterpret_cast<const f32x4*>(a.o + orr) : f32x4{};
+    ps[i] = ld ? *reinterpret_cast<const f32x4*>(a.term_prev + tpr) : f32x4{};
+  }
+  const bool upd = row_ok && msub > 0.0f && lsum > 0.0f;
+  const float fsh = upd ? msub / lsum : -1.0f;    // the row's factor m / sum; negative: not updated
+  const bool keep_terms = a.term_out != nullptr;
+#pragma unroll
+  for (int i = 0; i < NIE; ++i) {
+    const int rr = NR * i + rsub;
+    // (both permutes before the branch: a permute reads 0 from a source lane that is switched off, and
+    // lane rr's own row in this instruction may be past the group's last)
+    const float f = __shfl(fsh, rr, 64);            // (negative for a row past the group's last)
+    const int ri = __shfl(row_i, rr, 64);
+    const f32x4 t = *reinterpret_cast<const f32x4*>(es_at(rr, cc));
+    const f32x4 add = f >= 0.0f ? f32x4{t[0] * f, t[1] * f, t[2] * f, t[3] * f} : f32x4{};
+    if (f >= 0.0f) {
+      *reinterpret_cast<f32x4*>(a.o + ((int64_t)b * a.N + ri) * HD + (int64_t)h * D + 4 * cc) =
+          (po[i] - ps[i]) + add;
     }
-  if (hw == 0) {
-    a.lse_ref[lrow] = (run_max + log2f(lsum)) * 0.6931471805599453f - logf(msub);
-    if (keep_terms) a.mass_out[trow] = msub;
+    if (keep_terms && rr < nrow)
+      *reinterpret_cast<f32x4*>(a.term_out + (((int64_t)b * a.k + g0 + rr) * a.H + h) * D + 4 * cc) = add;
+  }
+  if (row_ok && hw == 0) {
+    const int64_t trow = ((int64_t)b * a.k + pos) * a.H + h;
+    if (upd) a.lse_ref[((int64_t)b * a.N + row_i) * a.H + h] =
+        (run_max + log2f(lsum)) * 0.6931471805599453f - logf(msub);
+    if (keep_terms) a.mass_out[trow] = upd ? msub : 0.0f;
   }
 }
 

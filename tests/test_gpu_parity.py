@@ -378,7 +378,12 @@ def test_sparse_attn_stepwise_from_oracle_state(F, name, over):
                                        ("C5", dict(seq=1600, heads=16, batch=2, loops=2, hot_frac=(0.9,),
                                                    topk_frac=(0.9,), bits=(4,), col_budget=100)),
                                        ("C5", dict(seq=1600, heads=16, head_dim=64, batch=2, loops=2,
-                                                   hot_frac=(0.9,), topk_frac=(0.9,), bits=(2,), col_budget=60))])
+                                                   hot_frac=(0.9,), topk_frac=(0.9,), bits=(2,), col_budget=60)),
+                                       # d = 64 with 57-row segments: a group of 25 rows, so one of the
+                                       # epilogue's four-row instructions holds a single existing row
+                                       ("C5", dict(seq=1500, heads=2, head_dim=64, batch=1, loops=2,
+                                                   hot_frac=(0.3,), topk_frac=(0.3,), bits=(4,), col_budget=124,
+                                                   group=32))])
 def test_subtract_pass_then_add_pass_from_oracle_state(F, name, over):
     """fl_loop_subtract_terms on the oracle's loop r-1 state: every row's subtract term and mass against the
     oracle's subtract half of Eq. 7; then the new rows committed and the add pass run with those terms
