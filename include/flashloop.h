@@ -238,8 +238,9 @@ int fl_kv_residual_dequant_kv(const uint8_t* k_codes, const uint16_t* k_scale, c
  *                       Scratch: a prep kernel fills it with the column records of every tile on each
  *                       call (about 8 * (2 B H c_list + B (N + k)) bytes; FL_E_SHAPE above 2^31).
  * Precision.  q.k is a bf16 MFMA product with fp32 accumulation; softmax and the update are fp32.  p.v
- * depends on the path: the dense loop, the two-pass loop and the add pass over current caches with a band
- * (window > 0) convert the value rows to fp16 and multiply fp16 probabilities (exact conversion for
+ * depends on the path: the dense loop, the two-pass loop and the add pass over current caches in the
+ * segment kernels (c_list <= 2048, with or without a band) convert the value rows to fp16 (or read them from
+ * v_cache_f16) and multiply fp16 probabilities (exact conversion for
  * 2^-14 <= |v| <= 65504; smaller magnitudes round to a multiple of 2^-24; values beyond 65504 in magnitude
  * overflow to infinity and are outside the supported input range); the other add-pass paths keep values
  * in bf16 and split each probability into two bf16 parts (about 16 significant bits).
